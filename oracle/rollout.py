@@ -1,0 +1,113 @@
+"""The rollout loop: observe, act, step, auto-reset (test infrastructure).
+
+One rollout step for each env is the Dec-POMDP step of the paper's problem
+setting (Section 3): every agent i observes o_i, samples a_i from its policy
+pi_i(. | o_i), the joint action moves the state through P and yields the
+shared reward r; an env whose episode ended starts a fresh one drawn from rho
+(auto-reset, with the reset drawn at step t + 1).  Envs are independent, and
+step t of env e consumes only draws keyed by (e, t), so any subset of env ids
+can be rolled out on its own and matches the same envs in a full batch.
+
+Output layout (``n`` = number of env ids, A agents, D obs features):
+    obs      [T, n, A, D] float64  observation the step's action was taken on
+    logits   [T, n, A, nA] float64 the oracle's policy logits for that obs
+    actions  [T, n, A]    int64
+    reward   [T, n]       float32
+    done     [T, n]       uint8   bit 0 terminated, bit 1 truncated
+    obs_last [n, A, D]    float64 observation after the last step
+    states   list of the n env states after the last step
+"""
+
+import numpy as np
+
+from . import mlp, sampling
+
+
+def initial_states(env, cfg, seed, env_ids):
+    """States at t = 0 (the first episode of every env is drawn at step 0)."""
+    return [env.reset(cfg, seed, e, 0) for e in env_ids]
+
+
+def observe_all(env, cfg, states):
+    """[n, A, D] float64 observations and [n, A, nA] bool legal masks."""
+    A = cfg.n_agents
+    obs = np.stack([np.stack([env.observe(cfg, s, a) for a in range(A)]) for s in states])
+    mask = np.array([[env.legal_mask(cfg, s, a) for a in range(A)] for s in states], dtype=bool)
+    return obs, mask
+
+
+def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
+            states=None, logits_source=None, action_hook=None):
+    """Roll ``env_ids`` forward ``n_steps`` steps from absolute step ``t0``.
+
+    ``states`` are the env states at t0 (default: the initial states, t0 = 0).
+    ``logits_source(k, logits64)`` may return float32 logits [n, A, nA] to
+    sample from at step t0 + k instead of the oracle's own.
+    ``action_hook(k, i, agent, action, logits32, mask)`` may replace the
+    sampled action of env index i, agent ``agent``.
+    """
+    env_ids = list(env_ids)
+    if states is None:
+        if t0 != 0:
+            raise ValueError("states are required when t0 != 0")
+        states = initial_states(env, cfg, seed, env_ids)
+    states = [s.copy() for s in states]
+    n, A = len(env_ids), cfg.n_agents
+    nA = env.N_ACTIONS
+    out = {k: [] for k in ("obs", "logits", "actions", "reward", "done", "mask")}
+    for k in range(n_steps):
+        t = t0 + k
+        obs, mask = observe_all(env, cfg, states)
+        logits64 = mlp.forward(obs.reshape(n * A, -1), weights, biases, dtype).reshape(n, A, nA)
+        logits32 = logits64.astype(np.float32)
+        if logits_source is not None:
+            logits32 = np.asarray(logits_source(k, logits64), dtype=np.float32)
+        actions = np.zeros((n, A), dtype=np.int64)
+        for i, e in enumerate(env_ids):
+            for a in range(A):
+                act = sampling.sample_action(seed, e, t, a, list(logits32[i, a]), list(mask[i, a]))
+                if action_hook is not None:
+                    act = action_hook(k, i, a, act, logits32[i, a], mask[i, a])
+                actions[i, a] = act
+        rewards = np.zeros(n, dtype=np.float32)
+        dones = np.zeros(n, dtype=np.uint8)
+        for i, e in enumerate(env_ids):
+            states[i], rewards[i], dones[i] = env.step(cfg, seed, e, t, states[i], list(actions[i]))
+        out["obs"].append(obs)
+        out["mask"].append(mask)
+        out["logits"].append(logits64)
+        out["actions"].append(actions)
+        out["reward"].append(rewards)
+        out["done"].append(dones)
+    res = {k: np.stack(v) if v else None for k, v in out.items()}
+    res["obs_last"], res["mask_last"] = observe_all(env, cfg, states)
+    res["states"] = states
+    return res
+
+
+def env_only(env, cfg, seed, env_ids, t0, actions, states=None):
+    """Step ``env_ids`` with injected actions [T, n, A] from absolute step ``t0``.
+
+    Returns per-step post-transition observations obs_{t+1} [T, n, A, D]
+    (after any auto-reset), masks, rewards, dones and the final states.
+    """
+    env_ids = list(env_ids)
+    if states is None:
+        if t0 != 0:
+            raise ValueError("states are required when t0 != 0")
+        states = initial_states(env, cfg, seed, env_ids)
+    states = [s.copy() for s in states]
+    actions = np.asarray(actions)
+    T, n = actions.shape[0], len(env_ids)
+    obs_out, mask_out = [], []
+    rewards = np.zeros((T, n), dtype=np.float32)
+    dones = np.zeros((T, n), dtype=np.uint8)
+    for k in range(T):
+        for i, e in enumerate(env_ids):
+            states[i], rewards[k, i], dones[k, i] = env.step(
+                cfg, seed, e, t0 + k, states[i], list(actions[k, i]))
+        o, m = observe_all(env, cfg, states)
+        obs_out.append(o)
+        mask_out.append(m)
+    return {"obs": np.stack(obs_out), "mask": np.stack(mask_out), "reward": rewards,
+            "done": dones, "states": states}
