@@ -1,0 +1,211 @@
+/* rollout.h -- C ABI of the MI355X batched multi-agent rollout library.
+ *
+ * The library steps thousands of independent gridworld episodes and runs each
+ * agent's policy network forward to sample its next action, entirely on one
+ * GPU.  One rollout step of one env is the Dec-POMDP step of the paper's
+ * problem setting (Section 3): state s, joint action a = (a_1..a_N) drawn
+ * from the decentralised policies pi_i(a_i | o_i), transition P(s' | s, a),
+ * shared team reward r(s, a), per-agent observations o_i of s', and a fresh
+ * episode from the initial-state distribution rho when one ends.  The
+ * environments are those of Section 4 (environment table): Level-Based
+ * Foraging (LBF) is implemented; Overcooked and Hanabi kinds are reserved and
+ * report RL_EUNSUPPORTED until built.
+ *
+ * Conventions for every entry point
+ *   - Tensor pointers are DEVICE pointers (gfx950 global memory), owned by the
+ *     caller, laid out densely in row-major order with the shapes given below.
+ *     The library allocates no device memory and keeps no pointer after a call
+ *     returns.  Struct arguments are HOST pointers, read during the call only.
+ *   - `stream` is a hipStream_t passed as an opaque pointer (NULL = the null
+ *     stream).  Work is enqueued on it and the call returns without waiting;
+ *     results are ready when the stream is synchronised.
+ *   - Arguments are validated on the host before anything is enqueued.  On a
+ *     non-zero status nothing was launched; rollout_last_error() describes
+ *     the failure.  A device-side fault surfaces at the caller's next stream
+ *     synchronisation, not as a status.
+ *   - Step indices t are absolute: t = 0 is the step rollout_init prepares.
+ *     Every random decision of env e at step t is a pure function of
+ *     (seed, env_base + e, t): a run of 128 steps equals a run of 64 steps
+ *     followed by a run of 64 steps from t0 = 64, bit for bit, and env e of a
+ *     batch equals the same global env id in any other batch.
+ *   - Random draws: Philox4x64-10 (Salmon et al., SC'11), key (seed, 0),
+ *     counter (global env id, t, sub-stream, tag).  Actions are sampled by
+ *     the Gumbel-max rule; see policy/sampling below.
+ */
+#ifndef MI355X_ROLLOUT_H
+#define MI355X_ROLLOUT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t rl_status;
+enum {
+  RL_OK = 0,
+  RL_EINVAL = -1,       /* a required pointer is NULL, a size is <= 0 or out of range */
+  RL_EUNSUPPORTED = -2, /* env kind, dtype or size with no compiled kernel */
+  RL_ESHAPE = -3,       /* policy dims disagree with the env's obs size / action count */
+  RL_EDEVICE = -4       /* the HIP runtime reported an error when launching */
+};
+
+enum { RL_ENV_LBF = 0, RL_ENV_OVERCOOKED = 1, RL_ENV_HANABI = 2 };
+enum { RL_F32 = 0, RL_BF16 = 1 };
+
+/* Environment configuration (host struct).
+ *
+ * LBF (Level-Based Foraging): grid_h x grid_w cells (each 3..16, at most 256
+ * cells), n_agents in 1..4 agents with levels 1..max_agent_level, n_food in
+ * 1..8 foods with levels 1..max_food_level placed on interior cells, episodes
+ * truncated after max_steps steps (>= 1).  Observations have
+ * 3 * grid_h * grid_w features per agent; there are 6 actions
+ * (0 noop, 1 north, 2 south, 3 west, 4 east, 5 load).  The exact rules are in
+ * the LBF section below. */
+typedef struct {
+  int32_t kind;            /* RL_ENV_* */
+  int32_t n_envs;          /* E >= 1 envs in this batch */
+  int32_t n_agents;        /* A */
+  int32_t grid_h, grid_w;  /* LBF grid */
+  int32_t n_food;          /* LBF foods per episode */
+  int32_t max_agent_level; /* LBF agent levels are 1..max_agent_level (1..15) */
+  int32_t max_food_level;  /* LBF food levels are 1..max_food_level (1..15) */
+  int32_t max_steps;       /* episode step limit (truncation) */
+  int32_t oc_cook_time;    /* Overcooked: steps a full pot cooks (reserved, 0 for LBF) */
+  int32_t oc_soup_reward;  /* Overcooked: reward of a served soup (reserved, 0 for LBF) */
+  int32_t hn_colors, hn_ranks, hn_hand_size, hn_info_tokens, hn_life_tokens; /* Hanabi (reserved) */
+  int64_t env_base;        /* global id of env 0 of this batch (>= 0) */
+  uint64_t seed;           /* Philox key word 0 */
+} rl_env_config;
+
+/* Policy: x -> tanh(x W1^T + b1) -> tanh(. W2^T + b2) -> . W3^T + b3, one
+ * network shared by every agent (host struct holding device pointers).
+ * W_l is [dims[l+1], dims[l]] row-major (the nn.Linear layout) and b_l is
+ * [dims[l+1]], both of `dtype`.  Observations fed to the network have the
+ * same dtype; logits are always float32.  In RL_BF16 the hidden activations
+ * are rounded to bfloat16 (nearest even) before the next layer and every
+ * product is accumulated in float32.
+ * Limits: n_layers == 3; dims[0] (D) in 1..2048; dims[1], dims[2] multiples of
+ * 16 in 16..512; dims[3] (nA) in 1..32. */
+typedef struct {
+  int32_t dtype;    /* RL_F32 or RL_BF16 */
+  int32_t n_layers; /* must be 3 */
+  int32_t dims[4];  /* D, H1, H2, nA */
+  const void* W[3];
+  const void* b[3];
+} rl_policy;
+
+/* Trajectory outputs of rollout_run (host struct of device pointers).  Any
+ * pointer may be NULL ("do not write").  T = n_steps of the call. */
+typedef struct {
+  void* obs;         /* [T, E, A, D] policy dtype: o_t, the observation a_t was sampled from */
+  int32_t* actions;  /* [T, E, A] a_t */
+  float* logits;     /* [T, E, A, nA] policy logits at o_t (illegal actions are -inf) */
+  float* reward;     /* [T, E] shared team reward of the transition at t */
+  uint8_t* done;     /* [T, E] bit 0 terminated, bit 1 truncated; an env with done != 0
+                        starts a fresh episode at t + 1 */
+  void* obs_last;    /* [E, A, D] policy dtype: o_{t0+T}, the observation after the last step */
+} rl_traj;
+
+/* ---- host-only queries (no device work) ---- */
+
+/* Bytes of the env state buffer for `cfg` (0 if cfg is invalid). */
+size_t rl_state_bytes(const rl_env_config* cfg);
+/* Features per agent observation, D (<= 0 if cfg is invalid). */
+int32_t rl_obs_dim(const rl_env_config* cfg);
+/* Actions per agent, nA (<= 0 if cfg is invalid). */
+int32_t rl_num_actions(const rl_env_config* cfg);
+/* Description of the last failure on the calling thread; valid until the
+ * thread's next call into the library. */
+const char* rollout_last_error(void);
+
+/* ---- entry points ---- */
+
+/* rho: draw the first episode of every env at t = 0 (Section 3, initial-state
+ * distribution) and write its observation.
+ *   state     [rl_state_bytes(cfg)] bytes, written (layout below).
+ *   obs       [E, A, D] of obs_dtype, written; may be NULL.
+ *   legal     [E, A, nA] uint8 legal-action mask (1 = legal), written; may be NULL. */
+rl_status rollout_init(const rl_env_config* cfg, void* state, void* obs, int32_t obs_dtype,
+                       uint8_t* legal, void* stream);
+
+/* P, r, Omega with injected actions: advance every env n_steps steps from
+ * absolute step t0 (Section 3 transition and reward), auto-resetting ended
+ * episodes.  Step k (0 <= k < n_steps) applies actions[k] at t = t0 + k.
+ *   actions   [n_steps, E, A] int32, read.  An action outside 0..nA-1 (or,
+ *             for envs with a legality mask, an illegal one) acts as the
+ *             lowest-index legal action (LBF: noop).
+ *   obs_out   [n_steps, E, A, D] of obs_dtype: o_{t+1}, after any reset; may be NULL.
+ *   reward    [n_steps, E] float32; done [n_steps, E] uint8; either may be NULL.
+ *   legal_out [n_steps, E, A, nA] uint8 masks for o_{t+1}; may be NULL. */
+rl_status rollout_step(const rl_env_config* cfg, void* state, uint64_t t0, int32_t n_steps,
+                       const int32_t* actions, void* obs_out, int32_t obs_dtype, float* reward,
+                       uint8_t* done, uint8_t* legal_out, void* stream);
+
+/* pi(. | o): policy logits for `rows` observations.
+ *   obs    [rows, D] of policy->dtype, read.
+ *   legal  [rows, nA] uint8 or NULL (all legal); an illegal action's logit is -inf.
+ *   logits [rows, nA] float32, written. */
+rl_status policy_forward(const rl_policy* policy, const void* obs, const uint8_t* legal,
+                         int64_t rows, float* logits, void* stream);
+
+/* The full rollout loop: for t = t0 .. t0+n_steps-1, every env observes,
+ * every agent samples a_t from pi(. | o_t) by Gumbel-max, the env steps and
+ * auto-resets; results go to `out` (any field NULL = skipped).  Runs as one
+ * persistent kernel; `state` is left at step t0 + n_steps. */
+rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* state,
+                      uint64_t t0, int32_t n_steps, const rl_traj* out, void* stream);
+
+/* Gumbel-max sampling of the actions of step t from given logits (the
+ * sampling stage of rollout_run on its own).
+ *   logits  [E, A, nA] float32 read;  legal [E, A, nA] uint8 or NULL;
+ *   actions [E, A] int32 written. */
+rl_status rollout_sample(const rl_env_config* cfg, uint64_t t, const float* logits,
+                         const uint8_t* legal, int32_t* actions, void* stream);
+
+/* The sampler's noise function on its own: g[i] = float32(-ln(-ln((u[i] + 1/2) / 2^24)))
+ * evaluated in double precision, for 24-bit inputs u[i] (higher bits ignored).
+ *   u [n] uint32 read, g [n] float32 written. */
+rl_status rl_gumbel_noise(const uint32_t* u, int64_t n, float* g, void* stream);
+
+/* ---- sampling ----
+ * Action a of agent i of env e at step t uses Philox block
+ * (seed; env_base + e, t, i * 256 + a / 8, TAG_ACTION = 2), word (a % 8) / 2,
+ * its high 32-bit half for even a and low half for odd a; u = half >> 8 and
+ * g = noise(u).  The action is argmax_a float32(logit_a + g_a) with illegal
+ * actions and NaN scores counted as -inf, ties to the lowest index, and
+ * action 0 when every score is -inf.
+ *
+ * ---- LBF ----
+ * State buffer: int32 planes of E entries each, plane p of env e at
+ * state[p * E + e]:
+ *   p = i            (0 <= i < A)  agent i cell, row * grid_w + col
+ *   p = A + i                       agent i level
+ *   p = 2A + j       (0 <= j < F)  food j cell
+ *   p = 2A + F + j                  food j level
+ *   p = 2A + 2F                     eaten-food bitmask (bit j = food j eaten)
+ *   p = 2A + 2F + 1                 steps taken in the current episode
+ *   p = 2A + 2F + 2                 sum of the episode's food levels
+ * Reset at step t draws 32-bit words k = 0.. from blocks
+ * (seed; env, t, k / 8, TAG_RESET = 1), word (k % 8) / 2, high half first,
+ * and maps word k to 0..n-1 as (k_word * n) >> 32: A agent levels
+ * 1..max_agent_level, then F food levels 1..min(max_food_level, sum of agent
+ * levels), then F food cells (the drawn index among the interior cells free
+ * of food, row-major), then A agent cells (the drawn index among cells free of
+ * food and earlier agents, row-major).
+ * Step: a move (1..4) succeeds iff the target is on the grid, holds no uneaten
+ * food and no agent before the step, and no other agent moves to the same
+ * target; food j is eaten iff the agents choosing load that are 4-adjacent to
+ * it have levels summing to >= its level (a loader counts for every adjacent
+ * food); reward = float32(eaten levels) / float32(sum of food levels);
+ * done bit 0 when every food is eaten, bit 1 when the episode reaches
+ * max_steps; a done env is reset with the draws of step t + 1.
+ * Observation of agent i, 3 planes of grid_h x grid_w (plane-major): agent
+ * levels at agent cells, uneaten food levels at food cells, 1 at agent i's
+ * own cell.  Every action is always legal. */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MI355X_ROLLOUT_H */

@@ -1,0 +1,206 @@
+// C-ABI entry points: host-side validation, then one kernel launch on the
+// caller's stream.  No device memory is allocated and no call waits on the
+// device.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "rollout.h"
+#include "rl_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+rl_status fail(rl_status code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+rl_status ok() {
+  g_err[0] = '\0';
+  return RL_OK;
+}
+
+rl_status launched(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(RL_EDEVICE, "%s: launch failed: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+bool valid_dtype(int32_t dt) { return dt == RL_F32 || dt == RL_BF16; }
+
+// Checks cfg and fills the LBF kernel parameters.
+rl_status check_cfg(const rl_env_config* cfg, rl::LbfParams* p) {
+  if (!cfg) return fail(RL_EINVAL, "cfg is NULL");
+  if (cfg->kind == RL_ENV_OVERCOOKED || cfg->kind == RL_ENV_HANABI)
+    return fail(RL_EUNSUPPORTED, "env kind %d is not built in this library", cfg->kind);
+  if (cfg->kind != RL_ENV_LBF) return fail(RL_EINVAL, "unknown env kind %d", cfg->kind);
+  if (cfg->n_envs < 1 || cfg->n_envs > (1 << 26)) return fail(RL_EINVAL, "n_envs %d outside 1..2^26", cfg->n_envs);
+  if (cfg->env_base < 0) return fail(RL_EINVAL, "env_base must be >= 0");
+  if (cfg->n_agents < 1 || cfg->n_agents > rl::LBF_MAXA)
+    return fail(RL_EINVAL, "LBF n_agents %d outside 1..%d", cfg->n_agents, rl::LBF_MAXA);
+  if (cfg->n_food < 1 || cfg->n_food > rl::LBF_MAXF)
+    return fail(RL_EINVAL, "LBF n_food %d outside 1..%d", cfg->n_food, rl::LBF_MAXF);
+  if (cfg->grid_h < 3 || cfg->grid_h > 16 || cfg->grid_w < 3 || cfg->grid_w > 16)
+    return fail(RL_EINVAL, "LBF grid %dx%d outside 3..16", cfg->grid_h, cfg->grid_w);
+  const int hw = cfg->grid_h * cfg->grid_w;
+  if (cfg->n_food > (cfg->grid_h - 2) * (cfg->grid_w - 2))
+    return fail(RL_EINVAL, "LBF n_food %d exceeds the %d interior cells", cfg->n_food,
+                (cfg->grid_h - 2) * (cfg->grid_w - 2));
+  if (cfg->n_food + cfg->n_agents > hw) return fail(RL_EINVAL, "LBF grid too small for agents and food");
+  if (cfg->max_agent_level < 1 || cfg->max_agent_level > 15 || cfg->max_food_level < 1 || cfg->max_food_level > 15)
+    return fail(RL_EINVAL, "LBF levels must be in 1..15");
+  if (cfg->max_steps < 1) return fail(RL_EINVAL, "max_steps must be >= 1");
+  if (cfg->oc_cook_time || cfg->oc_soup_reward || cfg->hn_colors || cfg->hn_ranks || cfg->hn_hand_size ||
+      cfg->hn_info_tokens || cfg->hn_life_tokens)
+    return fail(RL_EINVAL, "Overcooked/Hanabi fields must be 0 for LBF");
+  if (p) {
+    p->E = cfg->n_envs;
+    p->A = cfg->n_agents;
+    p->F = cfg->n_food;
+    p->H = cfg->grid_h;
+    p->W = cfg->grid_w;
+    p->HW = hw;
+    p->D = 3 * hw;
+    p->Lmax = cfg->max_agent_level;
+    p->Fmax = cfg->max_food_level;
+    p->max_steps = cfg->max_steps;
+    p->wmagic = rl::div_magic((uint32_t)cfg->grid_w);
+    p->env_base = cfg->env_base;
+    p->seed = cfg->seed;
+  }
+  return RL_OK;
+}
+
+rl_status check_policy(const rl_policy* pol, rl::PolicyArgs* a) {
+  if (!pol) return fail(RL_EINVAL, "policy is NULL");
+  if (!valid_dtype(pol->dtype)) return fail(RL_EUNSUPPORTED, "policy dtype %d unsupported", pol->dtype);
+  if (pol->n_layers != 3) return fail(RL_EUNSUPPORTED, "policy must have 3 layers, got %d", pol->n_layers);
+  const int D = pol->dims[0], H1 = pol->dims[1], H2 = pol->dims[2], NA = pol->dims[3];
+  if (D < 1 || D > 2048) return fail(RL_EUNSUPPORTED, "policy input size %d outside 1..2048", D);
+  if (H1 < 16 || H1 > 512 || H1 % 16 || H2 < 16 || H2 > 512 || H2 % 16)
+    return fail(RL_EUNSUPPORTED, "hidden sizes %d, %d must be multiples of 16 in 16..512", H1, H2);
+  if (NA < 1 || NA > rl::MAX_NA) return fail(RL_EUNSUPPORTED, "action count %d outside 1..%d", NA, rl::MAX_NA);
+  for (int l = 0; l < 3; ++l)
+    if (!pol->W[l] || !pol->b[l]) return fail(RL_EINVAL, "policy weight or bias %d is NULL", l);
+  if (a) {
+    a->dt = pol->dtype == RL_F32 ? rl::DT_F32 : rl::DT_BF16;
+    a->D = D;
+    a->H1 = H1;
+    a->H2 = H2;
+    a->NA = NA;
+    for (int l = 0; l < 3; ++l) {
+      a->W[l] = pol->W[l];
+      a->b[l] = pol->b[l];
+    }
+  }
+  return RL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t rl_state_bytes(const rl_env_config* cfg) {
+  rl::LbfParams p;
+  if (check_cfg(cfg, &p) != RL_OK) return 0;
+  return (size_t)rl::lbf_planes(p.A, p.F) * (size_t)p.E * sizeof(int32_t);
+}
+
+int32_t rl_obs_dim(const rl_env_config* cfg) {
+  rl::LbfParams p;
+  const rl_status s = check_cfg(cfg, &p);
+  return s != RL_OK ? s : p.D;
+}
+
+int32_t rl_num_actions(const rl_env_config* cfg) {
+  const rl_status s = check_cfg(cfg, nullptr);
+  return s != RL_OK ? s : rl::LBF_NACT;
+}
+
+const char* rollout_last_error(void) { return g_err; }
+
+rl_status rollout_init(const rl_env_config* cfg, void* state, void* obs, int32_t obs_dtype, uint8_t* legal,
+                       void* stream) {
+  rl::LbfParams p;
+  rl_status s = check_cfg(cfg, &p);
+  if (s != RL_OK) return s;
+  if (!state) return fail(RL_EINVAL, "state is NULL");
+  if (obs && !valid_dtype(obs_dtype)) return fail(RL_EUNSUPPORTED, "obs dtype %d unsupported", obs_dtype);
+  const int dt = obs_dtype == RL_F32 ? rl::DT_F32 : rl::DT_BF16;
+  return launched(rl::launch_lbf_init(p, static_cast<int32_t*>(state), obs, dt, legal, (hipStream_t)stream),
+                  "rollout_init");
+}
+
+rl_status rollout_step(const rl_env_config* cfg, void* state, uint64_t t0, int32_t n_steps, const int32_t* actions,
+                       void* obs_out, int32_t obs_dtype, float* reward, uint8_t* done, uint8_t* legal_out,
+                       void* stream) {
+  rl::LbfParams p;
+  rl_status s = check_cfg(cfg, &p);
+  if (s != RL_OK) return s;
+  if (!state) return fail(RL_EINVAL, "state is NULL");
+  if (!actions) return fail(RL_EINVAL, "actions is NULL");
+  if (n_steps < 1) return fail(RL_EINVAL, "n_steps %d must be >= 1", n_steps);
+  if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
+  if (obs_out && !valid_dtype(obs_dtype)) return fail(RL_EUNSUPPORTED, "obs dtype %d unsupported", obs_dtype);
+  const int dt = obs_dtype == RL_F32 ? rl::DT_F32 : rl::DT_BF16;
+  return launched(rl::launch_lbf_step(p, static_cast<int32_t*>(state), t0, n_steps, actions, obs_out, dt, reward,
+                                      done, legal_out, (hipStream_t)stream),
+                  "rollout_step");
+}
+
+rl_status policy_forward(const rl_policy* policy, const void* obs, const uint8_t* legal, int64_t rows,
+                         float* logits, void* stream) {
+  rl::PolicyArgs a;
+  rl_status s = check_policy(policy, &a);
+  if (s != RL_OK) return s;
+  if (!obs || !logits) return fail(RL_EINVAL, "obs or logits is NULL");
+  if (rows < 1 || rows > ((int64_t)1 << 31)) return fail(RL_EINVAL, "rows %lld outside 1..2^31", (long long)rows);
+  if (rl::policy_lds_bytes(a) > rl::MAX_LDS_BYTES)
+    return fail(RL_EUNSUPPORTED, "policy tiles need more than 160 KiB of LDS");
+  return launched(rl::launch_policy_forward(a, obs, legal, rows, logits, (hipStream_t)stream), "policy_forward");
+}
+
+rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* state, uint64_t t0, int32_t n_steps,
+                      const rl_traj* out, void* stream) {
+  rl::LbfParams p;
+  rl_status s = check_cfg(cfg, &p);
+  if (s != RL_OK) return s;
+  rl::PolicyArgs a;
+  s = check_policy(policy, &a);
+  if (s != RL_OK) return s;
+  if (!state) return fail(RL_EINVAL, "state is NULL");
+  if (!out) return fail(RL_EINVAL, "out is NULL");
+  if (n_steps < 1) return fail(RL_EINVAL, "n_steps %d must be >= 1", n_steps);
+  if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
+  if (a.D != p.D) return fail(RL_ESHAPE, "policy input size %d != observation size %d", a.D, p.D);
+  if (a.NA != rl::LBF_NACT) return fail(RL_ESHAPE, "policy has %d actions, the env %d", a.NA, rl::LBF_NACT);
+  const rl::RunLayout L = rl::make_run_layout(p.A, p.D, a.H1, a.H2, a.dt);
+  if (L.total > rl::MAX_LDS_BYTES)
+    return fail(RL_EUNSUPPORTED, "rollout tile needs %zu bytes of LDS (max %zu)", L.total, rl::MAX_LDS_BYTES);
+  const rl::TrajArgs o{out->obs, out->actions, out->logits, out->reward, out->done, out->obs_last};
+  return launched(rl::launch_lbf_run(p, a, static_cast<int32_t*>(state), t0, n_steps, o, (hipStream_t)stream),
+                  "rollout_run");
+}
+
+rl_status rollout_sample(const rl_env_config* cfg, uint64_t t, const float* logits, const uint8_t* legal,
+                         int32_t* actions, void* stream) {
+  rl::LbfParams p;
+  rl_status s = check_cfg(cfg, &p);
+  if (s != RL_OK) return s;
+  if (!logits || !actions) return fail(RL_EINVAL, "logits or actions is NULL");
+  return launched(rl::launch_sample(p.seed, p.env_base, p.E, p.A, rl::LBF_NACT, t, logits, legal, actions,
+                                    (hipStream_t)stream),
+                  "rollout_sample");
+}
+
+rl_status rl_gumbel_noise(const uint32_t* u, int64_t n, float* g, void* stream) {
+  if (!u || !g) return fail(RL_EINVAL, "u or g is NULL");
+  if (n < 1 || n > ((int64_t)1 << 32)) return fail(RL_EINVAL, "n %lld outside 1..2^32", (long long)n);
+  return launched(rl::launch_gumbel(u, n, g, (hipStream_t)stream), "rl_gumbel_noise");
+}
+
+}  // extern "C"

@@ -1,0 +1,89 @@
+// Internal interface between the C-ABI layer and the kernel translation units.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rl_lbf.h"
+#include "rl_mlp.h"
+
+namespace rl {
+
+constexpr int TILE_E = 16;     // envs per workgroup in the env and rollout kernels
+constexpr int NTHREADS = 256;  // threads per workgroup (4 waves of 64)
+constexpr int MAX_NA = 32;     // largest action count of a policy head
+
+// Exact division by small divisors: x / d == umulhi(x, ceil(2^32 / d)) for
+// d >= 2 and x < 2^32 / d; d == 1 is flagged by magic == 0.
+__host__ __device__ inline uint32_t div_magic(uint32_t d) {
+  return d <= 1 ? 0u : (uint32_t)((((uint64_t)1 << 32) + d - 1) / d);
+}
+__device__ __forceinline__ int fdiv(int x, uint32_t magic) {
+  return magic ? (int)__umulhi((uint32_t)x, magic) : x;
+}
+
+struct PolicyArgs {
+  int dt;  // DT_F32 / DT_BF16
+  int D, H1, H2, NA;
+  const void* W[3];
+  const void* b[3];
+};
+
+struct TrajArgs {
+  void* obs;
+  int32_t* actions;
+  float* logits;
+  float* reward;
+  uint8_t* done;
+  void* obs_last;
+};
+
+// LDS layout of the fused rollout kernel for one env tile of TILE_E envs.
+struct RunLayout {
+  int R;               // policy rows per tile = TILE_E * A (a multiple of 16)
+  int ldx, ld1, ld2;   // leading dimensions of the obs, h1 and h2 tiles (elements)
+  size_t off_agrid, off_fgrid, off_acell, off_act, off_x, off_h1, off_h2, off_logit, off_score;
+  size_t total;        // bytes
+};
+
+__host__ __device__ inline RunLayout make_run_layout(int A, int D, int H1, int H2, int dt) {
+  RunLayout L;
+  const size_t es = dt == DT_F32 ? 4 : 2;
+  L.R = TILE_E * A;
+  L.ldx = dt == DT_F32 ? lds_ld<DT_F32>(D) : lds_ld<DT_BF16>(D);
+  L.ld1 = dt == DT_F32 ? lds_ld<DT_F32>(H1) : lds_ld<DT_BF16>(H1);
+  L.ld2 = dt == DT_F32 ? lds_ld<DT_F32>(H2) : lds_ld<DT_BF16>(H2);
+  size_t o = 0;
+  L.off_agrid = o; o += (size_t)TILE_E * LBF_MAXCELLS;
+  L.off_fgrid = o; o += (size_t)TILE_E * LBF_MAXCELLS;
+  L.off_acell = o; o += (size_t)TILE_E * LBF_MAXA * 4;
+  L.off_act = o;   o += (size_t)L.R * 4;
+  L.off_x = o;     o += (size_t)L.R * L.ldx * es;
+  o = (o + 15) & ~(size_t)15;
+  L.off_h1 = o;    o += (size_t)L.R * L.ld1 * es;
+  o = (o + 15) & ~(size_t)15;
+  L.off_h2 = o;    o += (size_t)L.R * L.ld2 * es;
+  o = (o + 15) & ~(size_t)15;
+  L.off_logit = o; o += (size_t)L.R * MAX_NA * 4;
+  L.off_score = o; o += (size_t)L.R * MAX_NA * 4;
+  L.total = o;
+  return L;
+}
+
+constexpr size_t MAX_LDS_BYTES = 160 * 1024;
+
+hipError_t launch_lbf_init(const LbfParams& p, int32_t* state, void* obs, int obs_dt, uint8_t* legal,
+                           hipStream_t s);
+hipError_t launch_lbf_step(const LbfParams& p, int32_t* state, uint64_t t0, int n_steps,
+                           const int32_t* actions, void* obs, int obs_dt, float* reward, uint8_t* done,
+                           uint8_t* legal, hipStream_t s);
+hipError_t launch_lbf_run(const LbfParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
+                          const TrajArgs& out, hipStream_t s);
+
+size_t policy_lds_bytes(const PolicyArgs& pol);
+hipError_t launch_policy_forward(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
+                                 float* logits, hipStream_t s);
+hipError_t launch_sample(uint64_t seed, int64_t env_base, int E, int A, int NA, uint64_t t, const float* logits,
+                         const uint8_t* legal, int32_t* actions, hipStream_t s);
+hipError_t launch_gumbel(const uint32_t* u, int64_t n, float* g, hipStream_t s);
+
+}  // namespace rl

@@ -1,0 +1,256 @@
+// Level-Based Foraging device logic: reset (rho) and transition (P, r) of one
+// env held in the registers of one lane.
+//
+// Rules (the environment of Section 4 / environment table, run as the
+// Dec-POMDP step of Section 3), with the readings the paper leaves open:
+//   reset   A agent levels, F food levels capped by the agents' level sum, F
+//           food cells on interior cells, A agent cells on free cells, each a
+//           uniform index among the free candidates in row-major order;
+//   moves   legal iff the target is on the grid and holds neither uneaten
+//           food nor an agent before the step; legal movers sharing a
+//           target all stay;
+//   loads   a food is eaten iff the 4-adjacent loaders' levels sum to at
+//           least its level (a loader counts for every adjacent food);
+//   reward  float32(eaten levels) / float32(total food levels of the episode);
+//   done    bit 0 all food eaten, bit 1 step limit reached.
+// Every loop runs over compile-time bounds (MAXA, MAXF) with runtime guards,
+// so all per-env arrays stay in registers.
+#pragma once
+#include "rl_philox.h"
+
+namespace rl {
+
+constexpr int LBF_MAXA = 4;
+constexpr int LBF_MAXF = 8;
+constexpr int LBF_MAXCELLS = 256;
+constexpr int LBF_NACT = 6;
+
+struct LbfParams {
+  int E, A, F, H, W, HW, D, Lmax, Fmax, max_steps;
+  uint32_t wmagic;  // ceil(2^32 / W): x / W == umulhi(x, wmagic) for 0 <= x < 2^16
+  int64_t env_base;
+  uint64_t seed;
+};
+
+__device__ __forceinline__ int lbf_row(const LbfParams& p, int cell) {
+  return (int)__umulhi((uint32_t)cell, p.wmagic);
+}
+
+struct LbfEnv {
+  int acell[LBF_MAXA];
+  int alevel[LBF_MAXA];
+  int fcell[LBF_MAXF];
+  int flevel[LBF_MAXF];
+  uint32_t eaten;  // bit j = food j eaten
+  int steps;       // steps taken in the episode
+  int den;         // sum of the episode's food levels
+};
+
+// Number of int32 state planes: A cells, A levels, F cells, F levels, eaten, steps, den.
+__host__ __device__ inline int lbf_planes(int A, int F) { return 2 * A + 2 * F + 3; }
+
+__device__ __forceinline__ void lbf_load(const int32_t* __restrict__ st, const LbfParams& p, int e,
+                                         LbfEnv& s) {
+  const int E = p.E, A = p.A, F = p.F;
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i)
+    if (i < A) {
+      s.acell[i] = st[(size_t)i * E + e];
+      s.alevel[i] = st[(size_t)(A + i) * E + e];
+    }
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j)
+    if (j < F) {
+      s.fcell[j] = st[(size_t)(2 * A + j) * E + e];
+      s.flevel[j] = st[(size_t)(2 * A + F + j) * E + e];
+    }
+  s.eaten = (uint32_t)st[(size_t)(2 * A + 2 * F) * E + e];
+  s.steps = st[(size_t)(2 * A + 2 * F + 1) * E + e];
+  s.den = st[(size_t)(2 * A + 2 * F + 2) * E + e];
+}
+
+__device__ __forceinline__ void lbf_store(int32_t* __restrict__ st, const LbfParams& p, int e,
+                                          const LbfEnv& s) {
+  const int E = p.E, A = p.A, F = p.F;
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i)
+    if (i < A) {
+      st[(size_t)i * E + e] = s.acell[i];
+      st[(size_t)(A + i) * E + e] = s.alevel[i];
+    }
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j)
+    if (j < F) {
+      st[(size_t)(2 * A + j) * E + e] = s.fcell[j];
+      st[(size_t)(2 * A + F + j) * E + e] = s.flevel[j];
+    }
+  st[(size_t)(2 * A + 2 * F) * E + e] = (int32_t)s.eaten;
+  st[(size_t)(2 * A + 2 * F + 1) * E + e] = s.steps;
+  st[(size_t)(2 * A + 2 * F + 2) * E + e] = s.den;
+}
+
+// The idx-th (0-based) free candidate among 0, 1, 2, ..., where count_le(x)
+// is the number of occupied candidates <= x: the least fixed point of
+// x = idx + count_le(x), reached by iterating from x = idx (at most n_occ + 1
+// iterations, count_le being monotone).
+template <typename CountLE>
+__device__ __forceinline__ int lbf_kth_free(int idx, int n_occ, CountLE count_le) {
+  int x = idx;
+  for (int it = 0; it <= n_occ; ++it) {
+    const int nx = idx + count_le(x);
+    if (nx == x) break;
+    x = nx;
+  }
+  return x;
+}
+
+// Draw a fresh episode for global env id `env` from the reset stream at step t.
+__device__ __forceinline__ void lbf_reset(const LbfParams& p, uint64_t env, uint64_t t, LbfEnv& s) {
+  const int A = p.A, F = p.F, W = p.W;
+  const int nd = 2 * A + 2 * F;
+  const Block4 b0 = draw_block(p.seed, env, t, 0, TAG_RESET);
+  Block4 b1 = b0, b2 = b0;
+  if (nd > 8) b1 = draw_block(p.seed, env, t, 1, TAG_RESET);
+  if (nd > 16) b2 = draw_block(p.seed, env, t, 2, TAG_RESET);
+  // The 24 draws as a flat register array; draw(k) selects with compares so
+  // that a runtime k never turns the array into scratch memory.
+  uint32_t dw[24];
+#pragma unroll
+  for (int q = 0; q < 24; ++q) dw[q] = block_u32(q < 8 ? b0 : (q < 16 ? b1 : b2), q & 7);
+  auto draw = [&](int k) -> uint32_t {
+    uint32_t v = 0;
+#pragma unroll
+    for (int q = 0; q < 24; ++q) v = (q == k) ? dw[q] : v;
+    return v;
+  };
+  int lsum = 0;
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i)
+    if (i < A) {
+      s.alevel[i] = 1 + (int)range_map(draw(i), (uint32_t)p.Lmax);
+      lsum += s.alevel[i];
+    }
+  const int fcap = p.Fmax < lsum ? p.Fmax : lsum;
+  int den = 0;
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j)
+    if (j < F) {
+      s.flevel[j] = 1 + (int)range_map(draw(A + j), (uint32_t)fcap);
+      den += s.flevel[j];
+    }
+  // Food on interior cells, indexed row-major over the (H-2) x (W-2) interior.
+  const int IW = W - 2;
+  const int NI = (p.H - 2) * IW;
+  int fint[LBF_MAXF];
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j)
+    if (j < F) {
+      const int idx = (int)range_map(draw(A + F + j), (uint32_t)(NI - j));
+      fint[j] = lbf_kth_free(idx, j, [&](int x) {
+        int c = 0;
+#pragma unroll
+        for (int q = 0; q < LBF_MAXF; ++q) c += (q < j && fint[q] <= x) ? 1 : 0;
+        return c;
+      });
+      const int fr = fint[j] / IW;
+      s.fcell[j] = (1 + fr) * W + 1 + (fint[j] - fr * IW);
+    }
+  // Agents on cells free of food and of earlier agents.
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i)
+    if (i < A) {
+      const int idx = (int)range_map(draw(A + 2 * F + i), (uint32_t)(p.HW - F - i));
+      s.acell[i] = lbf_kth_free(idx, F + i, [&](int x) {
+        int c = 0;
+#pragma unroll
+        for (int q = 0; q < LBF_MAXF; ++q) c += (q < F && s.fcell[q] <= x) ? 1 : 0;
+#pragma unroll
+        for (int r = 0; r < LBF_MAXA; ++r) c += (r < i && s.acell[r] <= x) ? 1 : 0;
+        return c;
+      });
+    }
+  s.eaten = 0;
+  s.steps = 0;
+  s.den = den;
+}
+
+// One transition with actions act[0..A-1] (out-of-range -> noop).
+// Writes reward and done; `s` becomes the post-transition state (no reset).
+__device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, const int (&act_in)[LBF_MAXA],
+                                               float& reward, uint32_t& done) {
+  const int A = p.A, F = p.F, W = p.W, H = p.H;
+  int act[LBF_MAXA];
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) act[i] = (act_in[i] >= 0 && act_in[i] < LBF_NACT) ? act_in[i] : 0;
+
+  int ar[LBF_MAXA], ac[LBF_MAXA], fr[LBF_MAXF], fc[LBF_MAXF];
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) {
+    ar[i] = lbf_row(p, s.acell[i]);
+    ac[i] = s.acell[i] - ar[i] * W;
+  }
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j) {
+    fr[j] = lbf_row(p, s.fcell[j]);
+    fc[j] = s.fcell[j] - fr[j] * W;
+  }
+
+  // 1. moves against the pre-step state
+  int tgt[LBF_MAXA];
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) {
+    tgt[i] = -1;
+    if (i < A && act[i] >= 1 && act[i] <= 4) {
+      const int r = ar[i], c = ac[i];
+      const int r2 = r + (act[i] == 1 ? -1 : act[i] == 2 ? 1 : 0);
+      const int c2 = c + (act[i] == 3 ? -1 : act[i] == 4 ? 1 : 0);
+      if (r2 >= 0 && r2 < H && c2 >= 0 && c2 < W) {
+        const int cell = r2 * W + c2;
+        bool blocked = false;
+#pragma unroll
+        for (int j = 0; j < LBF_MAXF; ++j)
+          if (j < F && !((s.eaten >> j) & 1u) && s.fcell[j] == cell) blocked = true;
+#pragma unroll
+        for (int k = 0; k < LBF_MAXA; ++k)
+          if (k < A && s.acell[k] == cell) blocked = true;
+        if (!blocked) tgt[i] = cell;
+      }
+    }
+  }
+  int newcell[LBF_MAXA];
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) {
+    bool contested = false;
+#pragma unroll
+    for (int k = 0; k < LBF_MAXA; ++k)
+      if (k != i && k < A && tgt[k] >= 0 && tgt[k] == tgt[i]) contested = true;
+    newcell[i] = (tgt[i] >= 0 && !contested) ? tgt[i] : s.acell[i];
+  }
+
+  // 2. loads, with the pre-step positions (loaders do not move)
+  int eaten_sum = 0;
+  uint32_t eaten = s.eaten;
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j) {
+    if (j < F && !((s.eaten >> j) & 1u)) {
+      int lsum = 0;
+#pragma unroll
+      for (int i = 0; i < LBF_MAXA; ++i)
+        if (i < A && act[i] == 5 && abs(ar[i] - fr[j]) + abs(ac[i] - fc[j]) == 1) lsum += s.alevel[i];
+      if (lsum > 0 && lsum >= s.flevel[j]) {
+        eaten |= 1u << j;
+        eaten_sum += s.flevel[j];
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i)
+    if (i < A) s.acell[i] = newcell[i];
+  s.eaten = eaten;
+  reward = (float)eaten_sum / (float)s.den;
+  s.steps += 1;
+  const uint32_t all = (F >= 32) ? 0xffffffffu : ((1u << F) - 1u);
+  done = ((eaten & all) == all ? 1u : 0u) | (s.steps >= p.max_steps ? 2u : 0u);
+}
+
+}  // namespace rl

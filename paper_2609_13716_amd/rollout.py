@@ -1,0 +1,289 @@
+"""Python binding of the C-ABI rollout library (argument marshalling only).
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of its own: it checks tensor shapes/dtypes/devices, builds the
+host structs, passes raw device pointers and the current HIP stream, and
+raises ``RolloutError`` on a non-zero status.  PyTorch supplies device memory
+and streams.  The library must have been built
+(``python -m paper_2609_13716_amd.build``); importing this module fails
+loudly otherwise -- there is no fallback path.
+"""
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librollout.so")
+
+RL_OK, RL_EINVAL, RL_EUNSUPPORTED, RL_ESHAPE, RL_EDEVICE = 0, -1, -2, -3, -4
+RL_ENV_LBF, RL_ENV_OVERCOOKED, RL_ENV_HANABI = 0, 1, 2
+RL_F32, RL_BF16 = 0, 1
+
+_TORCH_DT = {RL_F32: torch.float32, RL_BF16: torch.bfloat16}
+_DT_CODE = {"f32": RL_F32, "bf16": RL_BF16, torch.float32: RL_F32, torch.bfloat16: RL_BF16}
+
+
+class RolloutError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"status {status}: {message}")
+        self.status = status
+
+
+class _EnvConfig(ctypes.Structure):
+    _fields_ = [
+        ("kind", ctypes.c_int32), ("n_envs", ctypes.c_int32), ("n_agents", ctypes.c_int32),
+        ("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32), ("n_food", ctypes.c_int32),
+        ("max_agent_level", ctypes.c_int32), ("max_food_level", ctypes.c_int32),
+        ("max_steps", ctypes.c_int32), ("oc_cook_time", ctypes.c_int32),
+        ("oc_soup_reward", ctypes.c_int32), ("hn_colors", ctypes.c_int32),
+        ("hn_ranks", ctypes.c_int32), ("hn_hand_size", ctypes.c_int32),
+        ("hn_info_tokens", ctypes.c_int32), ("hn_life_tokens", ctypes.c_int32),
+        ("env_base", ctypes.c_int64), ("seed", ctypes.c_uint64),
+    ]
+
+
+class _Policy(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("dims", ctypes.c_int32 * 4),
+                ("W", ctypes.c_void_p * 3), ("b", ctypes.c_void_p * 3)]
+
+
+class _Traj(ctypes.Structure):
+    _fields_ = [("obs", ctypes.c_void_p), ("actions", ctypes.c_void_p), ("logits", ctypes.c_void_p),
+                ("reward", ctypes.c_void_p), ("done", ctypes.c_void_p), ("obs_last", ctypes.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_13716_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, cfgp, st = ctypes.c_void_p, ctypes.POINTER(_EnvConfig), ctypes.c_int32
+    lib.rl_state_bytes.argtypes, lib.rl_state_bytes.restype = [cfgp], ctypes.c_size_t
+    lib.rl_obs_dim.argtypes, lib.rl_obs_dim.restype = [cfgp], ctypes.c_int32
+    lib.rl_num_actions.argtypes, lib.rl_num_actions.restype = [cfgp], ctypes.c_int32
+    lib.rollout_last_error.argtypes, lib.rollout_last_error.restype = [], ctypes.c_char_p
+    lib.rollout_init.argtypes, lib.rollout_init.restype = [cfgp, P, P, ctypes.c_int32, P, P], st
+    lib.rollout_step.argtypes = [cfgp, P, ctypes.c_uint64, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P, P]
+    lib.rollout_step.restype = st
+    lib.policy_forward.argtypes = [ctypes.POINTER(_Policy), P, P, ctypes.c_int64, P, P]
+    lib.policy_forward.restype = st
+    lib.rollout_run.argtypes = [cfgp, ctypes.POINTER(_Policy), P, ctypes.c_uint64, ctypes.c_int32,
+                                ctypes.POINTER(_Traj), P]
+    lib.rollout_run.restype = st
+    lib.rollout_sample.argtypes = [cfgp, ctypes.c_uint64, P, P, P, P]
+    lib.rollout_sample.restype = st
+    lib.rl_gumbel_noise.argtypes, lib.rl_gumbel_noise.restype = [P, ctypes.c_int64, P, P], st
+    return lib
+
+
+lib = _load()
+
+# Every symbol the C header declares (checked by the test suite).
+EXPORTED = ("rl_state_bytes", "rl_obs_dim", "rl_num_actions", "rollout_last_error", "rollout_init",
+            "rollout_step", "policy_forward", "rollout_run", "rollout_sample", "rl_gumbel_noise")
+
+
+def _check(status):
+    if status != RL_OK:
+        raise RolloutError(status, lib.rollout_last_error().decode())
+
+
+@dataclass
+class EnvConfig:
+    """Mirror of ``rl_env_config`` (defaults: LBF 8x8, 2 agents, 3 foods)."""
+    n_envs: int
+    kind: int = RL_ENV_LBF
+    n_agents: int = 2
+    grid_h: int = 8
+    grid_w: int = 8
+    n_food: int = 3
+    max_agent_level: int = 2
+    max_food_level: int = 3
+    max_steps: int = 50
+    env_base: int = 0
+    seed: int = 0
+    extra: dict = field(default_factory=dict)  # Overcooked / Hanabi fields
+
+    def c(self):
+        s = _EnvConfig()
+        for k in ("kind", "n_envs", "n_agents", "grid_h", "grid_w", "n_food", "max_agent_level",
+                  "max_food_level", "max_steps", "env_base", "seed"):
+            setattr(s, k, getattr(self, k))
+        for k, v in self.extra.items():
+            setattr(s, k, v)
+        return s
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(t, name, dtype=None, shape=None):
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def rl_state_bytes(cfg):
+    return lib.rl_state_bytes(ctypes.byref(cfg.c()))
+
+
+def rl_obs_dim(cfg):
+    return lib.rl_obs_dim(ctypes.byref(cfg.c()))
+
+
+def rl_num_actions(cfg):
+    return lib.rl_num_actions(ctypes.byref(cfg.c()))
+
+
+class Policy:
+    """Device weights of the 3-layer MLP in the nn.Linear layout, and the C struct pointing at them."""
+
+    def __init__(self, weights, biases, dtype="f32", device="cuda"):
+        self.dtype = _DT_CODE[dtype]
+        tdt = _TORCH_DT[self.dtype]
+        self.W = [torch.as_tensor(w).to(device=device, dtype=tdt).contiguous() for w in weights]
+        self.b = [torch.as_tensor(b).to(device=device, dtype=tdt).contiguous() for b in biases]
+        self.dims = [self.W[0].shape[1]] + [w.shape[0] for w in self.W]
+
+    @property
+    def torch_dtype(self):
+        return _TORCH_DT[self.dtype]
+
+    def c(self):
+        p = _Policy()
+        p.dtype = self.dtype
+        p.n_layers = len(self.W)
+        for i, d in enumerate(self.dims):
+            p.dims[i] = d
+        for i in range(3):
+            p.W[i] = self.W[i].data_ptr()
+            p.b[i] = self.b[i].data_ptr()
+        return p
+
+
+def new_state(cfg, device="cuda"):
+    """A device buffer of rl_state_bytes(cfg) bytes (as int32)."""
+    n = rl_state_bytes(cfg)
+    if n == 0:
+        _check(lib.rl_obs_dim(ctypes.byref(cfg.c())))
+    return torch.empty(n // 4, dtype=torch.int32, device=device)
+
+
+def rollout_init(cfg, state, obs=None, legal=None, stream=None):
+    E, A = cfg.n_envs, cfg.n_agents
+    D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
+    _need(state, "state", torch.int32)
+    if obs is not None:
+        _need(obs, "obs", shape=(E, A, D))
+    _need(legal, "legal", torch.uint8, (E, A, nA))
+    code = _DT_CODE.get(obs.dtype, -1) if obs is not None else RL_F32
+    _check(lib.rollout_init(ctypes.byref(cfg.c()), _ptr(state), _ptr(obs), code, _ptr(legal), _stream(stream)))
+
+
+def rollout_step(cfg, state, t0, actions, obs_out=None, reward=None, done=None, legal_out=None, stream=None):
+    E, A = cfg.n_envs, cfg.n_agents
+    D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
+    _need(state, "state", torch.int32)
+    _need(actions, "actions", torch.int32)
+    if actions.dim() != 3 or tuple(actions.shape[1:]) != (E, A):
+        raise ValueError(f"actions must be [T, {E}, {A}], got {tuple(actions.shape)}")
+    T = actions.shape[0]
+    if obs_out is not None:
+        _need(obs_out, "obs_out", shape=(T, E, A, D))
+    _need(reward, "reward", torch.float32, (T, E))
+    _need(done, "done", torch.uint8, (T, E))
+    _need(legal_out, "legal_out", torch.uint8, (T, E, A, nA))
+    code = _DT_CODE.get(obs_out.dtype, -1) if obs_out is not None else RL_F32
+    _check(lib.rollout_step(ctypes.byref(cfg.c()), _ptr(state), t0, T, _ptr(actions), _ptr(obs_out), code,
+                            _ptr(reward), _ptr(done), _ptr(legal_out), _stream(stream)))
+
+
+def policy_forward(policy, obs, legal=None, logits=None, stream=None):
+    rows = obs.shape[0]
+    nA = policy.dims[3]
+    _need(obs, "obs", policy.torch_dtype, (rows, policy.dims[0]))
+    _need(legal, "legal", torch.uint8, (rows, nA))
+    if logits is None:
+        logits = torch.empty(rows, nA, dtype=torch.float32, device=obs.device)
+    _need(logits, "logits", torch.float32, (rows, nA))
+    pc = policy.c()
+    _check(lib.policy_forward(ctypes.byref(pc), _ptr(obs), _ptr(legal), rows, _ptr(logits), _stream(stream)))
+    return logits
+
+
+def rollout_run(cfg, policy, state, t0, n_steps, obs=None, actions=None, logits=None, reward=None, done=None,
+                obs_last=None, stream=None):
+    E, A = cfg.n_envs, cfg.n_agents
+    D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
+    T = n_steps
+    _need(state, "state", torch.int32)
+    _need(obs, "obs", policy.torch_dtype, (T, E, A, D))
+    _need(actions, "actions", torch.int32, (T, E, A))
+    _need(logits, "logits", torch.float32, (T, E, A, nA))
+    _need(reward, "reward", torch.float32, (T, E))
+    _need(done, "done", torch.uint8, (T, E))
+    _need(obs_last, "obs_last", policy.torch_dtype, (E, A, D))
+    tr = _Traj(obs=_ptr(obs), actions=_ptr(actions), logits=_ptr(logits), reward=_ptr(reward), done=_ptr(done),
+               obs_last=_ptr(obs_last))
+    pc = policy.c()
+    _check(lib.rollout_run(ctypes.byref(cfg.c()), ctypes.byref(pc), _ptr(state), t0, T, ctypes.byref(tr),
+                           _stream(stream)))
+
+
+def rollout_sample(cfg, t, logits, legal=None, actions=None, stream=None):
+    E, A, nA = cfg.n_envs, cfg.n_agents, rl_num_actions(cfg)
+    _need(logits, "logits", torch.float32, (E, A, nA))
+    _need(legal, "legal", torch.uint8, (E, A, nA))
+    if actions is None:
+        actions = torch.empty(E, A, dtype=torch.int32, device=logits.device)
+    _need(actions, "actions", torch.int32, (E, A))
+    _check(lib.rollout_sample(ctypes.byref(cfg.c()), t, _ptr(logits), _ptr(legal), _ptr(actions), _stream(stream)))
+    return actions
+
+
+def rl_gumbel_noise(u, g=None, stream=None):
+    _need(u, "u", torch.int32)
+    if g is None:
+        g = torch.empty(u.shape, dtype=torch.float32, device=u.device)
+    _need(g, "g", torch.float32, tuple(u.shape))
+    _check(lib.rl_gumbel_noise(_ptr(u), u.numel(), _ptr(g), _stream(stream)))
+    return g
+
+
+# ---- LBF state layout (see the LBF section of include/rollout.h) ----
+
+LBF_FIELDS = ("agent_cell", "agent_level", "food_cell", "food_level", "eaten", "steps", "den")
+
+
+def lbf_state_planes(cfg, state):
+    """Split a state buffer (host or device int32 tensor) into named [.., E] planes."""
+    E, A, F = cfg.n_envs, cfg.n_agents, cfg.n_food
+    p = state.reshape(2 * A + 2 * F + 3, E)
+    return {"agent_cell": p[:A], "agent_level": p[A:2 * A], "food_cell": p[2 * A:2 * A + F],
+            "food_level": p[2 * A + F:2 * A + 2 * F], "eaten": p[2 * A + 2 * F], "steps": p[2 * A + 2 * F + 1],
+            "den": p[2 * A + 2 * F + 2]}
+
+
+def lbf_pack_state(cfg, planes, device="cuda"):
+    """Inverse of lbf_state_planes: a state buffer from named planes ([A, E], [F, E] or [E])."""
+    E, A, F = cfg.n_envs, cfg.n_agents, cfg.n_food
+    buf = torch.empty(2 * A + 2 * F + 3, E, dtype=torch.int32)
+    v = lbf_state_planes(cfg, buf)
+    for k in LBF_FIELDS:
+        v[k].copy_(torch.as_tensor(planes[k], dtype=torch.int32).reshape(v[k].shape))
+    return buf.reshape(-1).to(device)

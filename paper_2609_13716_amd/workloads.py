@@ -1,0 +1,65 @@
+"""Seeded synthetic workloads and input generators.
+
+This module holds the sizes of the benchmark workloads and draws the inputs
+that both the GPU path and the CPU oracle consume: policy weights (normal,
+variance 1 / fan_in, float32) and injected actions (uniform integers).  It
+contains none of the rollout's arithmetic.
+
+Workloads (Level-Based Foraging; env dynamics and observation as documented
+in include/rollout.h):
+    lbf8_small   8x8, 2 agents, 3 foods, levels 1..2 / 1..3, 16 envs x 128 steps,
+                 MLP 192-64-64-6 float32 (a correctness-size workload)
+    lbf8_4096    8x8, 2 agents, 3 foods, levels 1..2 / 1..3, 4096 envs x 128 steps,
+                 MLP 192-128-128-6 in float32 and in bf16
+    lbf12_16k    12x12, 3 agents, 6 foods, levels 1..3 / 1..6, 16384 envs x 256 steps,
+                 MLP 432-256-256-6 bf16
+All LBF episodes are truncated after 50 steps.
+"""
+
+import numpy as np
+
+WORKLOADS = {
+    "lbf8_small": dict(env=dict(grid_h=8, grid_w=8, n_agents=2, n_food=3, max_agent_level=2, max_food_level=3,
+                                max_steps=50),
+                       n_envs=16, n_steps=128, hidden=(64, 64), dtypes=("f32",)),
+    "lbf8_4096": dict(env=dict(grid_h=8, grid_w=8, n_agents=2, n_food=3, max_agent_level=2, max_food_level=3,
+                               max_steps=50),
+                      n_envs=4096, n_steps=128, hidden=(128, 128), dtypes=("f32", "bf16")),
+    "lbf12_16k": dict(env=dict(grid_h=12, grid_w=12, n_agents=3, n_food=6, max_agent_level=3, max_food_level=6,
+                               max_steps=50),
+                      n_envs=16384, n_steps=256, hidden=(256, 256), dtypes=("bf16",)),
+}
+
+LBF_ACTIONS = 6
+
+
+def lbf_obs_dim(env):
+    return 3 * env["grid_h"] * env["grid_w"]
+
+
+def policy_dims(name):
+    w = WORKLOADS[name]
+    return (lbf_obs_dim(w["env"]), *w["hidden"], LBF_ACTIONS)
+
+
+def policy_weights(dims, seed, bias_scale=0.0):
+    """float32 weights W_l ~ N(0, 1/fan_in) in the [fan_out, fan_in] layout, and biases.
+
+    Biases are zero unless ``bias_scale`` > 0 (then N(0, bias_scale^2)).
+    """
+    rng = np.random.default_rng(seed)
+    ws, bs = [], []
+    for i in range(len(dims) - 1):
+        ws.append((rng.standard_normal((dims[i + 1], dims[i])) / np.sqrt(dims[i])).astype(np.float32))
+        bs.append((rng.standard_normal(dims[i + 1]) * bias_scale).astype(np.float32))
+    return ws, bs
+
+
+def injected_actions(n_steps, n_envs, n_agents, n_actions, seed, p_invalid=0.0):
+    """Uniform actions [T, E, A] int32; a fraction ``p_invalid`` is replaced by out-of-range values."""
+    rng = np.random.default_rng(seed)
+    a = rng.integers(0, n_actions, size=(n_steps, n_envs, n_agents), dtype=np.int64)
+    if p_invalid > 0:
+        bad = rng.random(a.shape) < p_invalid
+        a[bad] = rng.choice(np.array([-1, n_actions, n_actions + 7, 1 << 20]), size=int(bad.sum()))
+    return a.astype(np.int32)

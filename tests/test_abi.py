@@ -1,0 +1,131 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad arguments on the host.
+
+No call here reaches a kernel launch: each one fails host-side validation first.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_13716_amd import rollout as R
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "rollout.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_symbols_exported():
+    names = _declared()
+    assert "rollout_run" in names and "policy_forward" in names
+    assert sorted(R.EXPORTED) == names
+    for n in names:
+        assert hasattr(R.lib, n), n
+
+
+def _cfg(**kw):
+    base = dict(n_envs=16)
+    base.update(kw)
+    return R.EnvConfig(**base)
+
+
+def _status(cfg):
+    return R.lib.rl_obs_dim(ctypes.byref(cfg.c()))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_envs=0), R.RL_EINVAL),
+    (dict(n_agents=0), R.RL_EINVAL),
+    (dict(n_agents=5), R.RL_EINVAL),
+    (dict(n_food=9), R.RL_EINVAL),
+    (dict(grid_h=2), R.RL_EINVAL),
+    (dict(grid_w=17), R.RL_EINVAL),
+    (dict(grid_h=3, grid_w=3, n_food=2), R.RL_EINVAL),
+    (dict(max_agent_level=0), R.RL_EINVAL),
+    (dict(max_food_level=16), R.RL_EINVAL),
+    (dict(max_steps=0), R.RL_EINVAL),
+    (dict(env_base=-1), R.RL_EINVAL),
+    (dict(kind=7), R.RL_EINVAL),
+    (dict(kind=R.RL_ENV_OVERCOOKED), R.RL_EUNSUPPORTED),
+    (dict(kind=R.RL_ENV_HANABI), R.RL_EUNSUPPORTED),
+    (dict(extra={"hn_colors": 5}), R.RL_EINVAL),
+])
+def test_bad_config(kw, code):
+    cfg = _cfg(**kw)
+    assert _status(cfg) == code
+    assert R.rl_state_bytes(cfg) == 0
+    assert R.lib.rollout_last_error()
+
+
+def test_queries():
+    cfg = _cfg(n_envs=100, grid_h=12, grid_w=12, n_agents=3, n_food=6)
+    assert R.rl_obs_dim(cfg) == 432
+    assert R.rl_num_actions(cfg) == 6
+    assert R.rl_state_bytes(cfg) == (2 * 3 + 2 * 6 + 3) * 100 * 4
+
+
+def _policy_struct(dt=R.RL_F32, dims=(192, 64, 64, 6), layers=3, null_w=False):
+    p = R._Policy()
+    p.dtype, p.n_layers = dt, layers
+    for i, d in enumerate(dims):
+        p.dims[i] = d
+    for i in range(3):
+        p.W[i] = None if null_w else 0x1000
+        p.b[i] = 0x1000
+    return p
+
+
+def _run_status(cfg, pol, state=0x1000, n_steps=4, t0=0):
+    tr = R._Traj()
+    return R.lib.rollout_run(ctypes.byref(cfg.c()), ctypes.byref(pol), ctypes.c_void_p(state), t0, n_steps,
+                             ctypes.byref(tr), None)
+
+
+def test_error_paths_before_launch():
+    L = R.lib
+    cfg = _cfg()
+    c = cfg.c()
+    assert L.rollout_init(ctypes.byref(c), None, None, R.RL_F32, None, None) == R.RL_EINVAL
+    assert L.rollout_init(ctypes.byref(c), ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), 7, None,
+                          None) == R.RL_EUNSUPPORTED
+    assert L.rollout_step(ctypes.byref(c), ctypes.c_void_p(0x1000), 0, 1, None, None, 0, None, None, None,
+                          None) == R.RL_EINVAL
+    assert L.rollout_step(ctypes.byref(c), ctypes.c_void_p(0x1000), 0, 0, ctypes.c_void_p(0x1000), None, 0, None,
+                          None, None, None) == R.RL_EINVAL
+    assert L.rollout_step(ctypes.byref(c), ctypes.c_void_p(0x1000), (1 << 64) - 1, 2, ctypes.c_void_p(0x1000), None,
+                          0, None, None, None, None) == R.RL_EINVAL
+    # policy checks
+    assert _run_status(cfg, _policy_struct(dt=5)) == R.RL_EUNSUPPORTED
+    assert _run_status(cfg, _policy_struct(layers=2)) == R.RL_EUNSUPPORTED
+    assert _run_status(cfg, _policy_struct(dims=(192, 60, 64, 6))) == R.RL_EUNSUPPORTED
+    assert _run_status(cfg, _policy_struct(dims=(192, 64, 64, 33))) == R.RL_EUNSUPPORTED
+    assert _run_status(cfg, _policy_struct(null_w=True)) == R.RL_EINVAL
+    assert _run_status(cfg, _policy_struct(dims=(191, 64, 64, 6))) == R.RL_ESHAPE
+    assert _run_status(cfg, _policy_struct(dims=(192, 64, 64, 5))) == R.RL_ESHAPE
+    assert _run_status(cfg, _policy_struct(), state=0) == R.RL_EINVAL
+    assert _run_status(cfg, _policy_struct(), n_steps=0) == R.RL_EINVAL
+    # a tile that cannot fit in LDS: 16x16 grid, 4 agents, 512-wide float32 layers
+    big = _cfg(grid_h=16, grid_w=16, n_agents=4)
+    assert _run_status(big, _policy_struct(dims=(768, 512, 512, 6))) == R.RL_EUNSUPPORTED
+    assert "LDS" in L.rollout_last_error().decode()
+    # policy_forward and sampling
+    pol = _policy_struct()
+    assert L.policy_forward(ctypes.byref(pol), None, None, 10, ctypes.c_void_p(0x1000), None) == R.RL_EINVAL
+    assert L.policy_forward(ctypes.byref(pol), ctypes.c_void_p(0x1000), None, 0, ctypes.c_void_p(0x1000),
+                            None) == R.RL_EINVAL
+    assert L.rollout_sample(ctypes.byref(c), 0, None, None, ctypes.c_void_p(0x1000), None) == R.RL_EINVAL
+    assert L.rl_gumbel_noise(None, 10, ctypes.c_void_p(0x1000), None) == R.RL_EINVAL
+    assert L.rl_gumbel_noise(ctypes.c_void_p(0x1000), 0, ctypes.c_void_p(0x1000), None) == R.RL_EINVAL
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    cfg = _cfg()
+    with pytest.raises(ValueError):
+        R.rollout_init(cfg, torch.zeros(10, dtype=torch.int32))
