@@ -1,0 +1,253 @@
+"""Throughput of the batched multi-agent rollout on one MI355X.
+
+One step = one ``rollout_run`` over the whole batch: 4096 Level-Based
+Foraging envs (8x8 grid, 2 agents, 3 foods) x 128 steps, every agent's MLP
+(192-128-128-6) forward, Gumbel-max sampling, env step and auto-reset, with
+the trajectory (observations, actions, rewards, dones, final observation)
+written to HBM.  The headline is bf16; the same workload in float32, the
+env-only stepping kernel and the standalone policy forward are reported
+alongside.  Inputs (weights, initial states) are seeded synthetic data that
+is resident in HBM before the timed region starts.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+Prints one JSON line.
+"""
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "agent-env steps/sec incl. policy forward (1 MI355X) at 4096 envs; % HBM/MFMA peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+WORKLOAD = "lbf8_4096"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-envs", type=int, default=512, help="envs in the oracle's timed sample")
+    ap.add_argument("--only", choices=["run_bf16", "run_f32", "env_bf16", "policy_bf16"], default=None,
+                    help="time one kernel only (for profiler runs)")
+    return ap.parse_args()
+
+
+def csrc_hash():
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2609_13716_amd", "csrc", "*"))):
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def timed(fn, steps, warmup):
+    """Run fn warmup times, then `steps` times; returns (mean kernel ms from events, wall ms per step)."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for a, b in evs:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    kern = sum(a.elapsed_time(b) for a, b in evs) / steps
+    return kern, wall
+
+
+def roofline(bound, achieved, peak, unit, traffic=None):
+    return {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": traffic}
+
+
+def load_traffic(kernel_key):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it matches this source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except ValueError:
+        return None
+    if rec.get("csrc_hash") != csrc_hash():
+        return None
+    k = rec.get("kernels", {}).get(kernel_key)
+    return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(n_envs, T):
+    """The oracle, single-threaded, on the first n_envs envs of the workload for T steps."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import lbf, rollout as orollout
+    from paper_2609_13716_amd import workloads
+    w = workloads.WORKLOADS[WORKLOAD]
+    e = w["env"]
+    oc = lbf.Config(e["grid_h"], e["grid_w"], e["n_agents"], e["n_food"], e["max_agent_level"],
+                    e["max_food_level"], e["max_steps"])
+    ws, bs = workloads.policy_weights(workloads.policy_dims(WORKLOAD), seed=1000)
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        orollout.rollout(lbf, oc, 0, range(n_envs), 0, T, ws, bs, "bf16")
+        dt = time.perf_counter() - t0
+    agent_steps = n_envs * T * e["n_agents"]
+    return {"value": round(agent_steps / dt, 1), "unit": "agent-env steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n_envs} envs x {T} steps of {WORKLOAD} (bf16 policy), one thread, {dt:.1f} s",
+            "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the rollout shards over GPUs "
+              "by env id with no exchange, and this build times the single-GPU shard.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2609_13716_amd import rollout as R
+    from paper_2609_13716_amd import workloads
+
+    w = workloads.WORKLOADS[WORKLOAD]
+    E, T = w["n_envs"], w["n_steps"]
+    A = w["env"]["n_agents"]
+    cfg = R.EnvConfig(n_envs=E, seed=0, **w["env"])
+    D, nA = R.rl_obs_dim(cfg), R.rl_num_actions(cfg)
+    dims = workloads.policy_dims(WORKLOAD)
+    ws, bs = workloads.policy_weights(dims, seed=1000)
+    flop_per_row = 2 * sum(dims[i] * dims[i + 1] for i in range(3))
+    planes = 2 * A + 2 * w["env"]["n_food"] + 3
+    results = {}
+
+    def rollout_case(dt):
+        pol = R.Policy(ws, bs, dt)
+        es = 2 if dt == "bf16" else 4
+        state = R.new_state(cfg)
+        R.rollout_init(cfg, state)
+        obs = torch.empty(T, E, A, D, dtype=pol.torch_dtype, device="cuda")
+        acts = torch.empty(T, E, A, dtype=torch.int32, device="cuda")
+        rew = torch.empty(T, E, device="cuda")
+        done = torch.empty(T, E, dtype=torch.uint8, device="cuda")
+        last = torch.empty(E, A, D, dtype=pol.torch_dtype, device="cuda")
+        t_next = [0]
+
+        def step():
+            R.rollout_run(cfg, pol, state, t_next[0], T, obs=obs, actions=acts, reward=rew, done=done,
+                          obs_last=last)
+            t_next[0] += T
+
+        kern_ms, wall_ms = timed(step, args.steps, args.warmup)
+        # algorithmic bytes: trajectory outputs + final obs + state read and written once
+        nbytes = E * T * (A * D * es + A * 4 + 4 + 1) + E * A * D * es + 2 * E * planes * 4
+        flops = E * A * T * flop_per_row
+        agent_steps = E * A * T
+        return dict(kern_ms=kern_ms, wall_ms=wall_ms, bytes=nbytes, flops=flops,
+                    value=agent_steps / (wall_ms * 1e-3), env_steps_s=E * T / (wall_ms * 1e-3),
+                    gbs=nbytes / (kern_ms * 1e-3) / 1e9, tflops=flops / (kern_ms * 1e-3) / 1e12)
+
+    def env_case(dt):
+        tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+        es = 2 if dt == "bf16" else 4
+        state = R.new_state(cfg)
+        R.rollout_init(cfg, state)
+        g = torch.Generator(device="cuda")
+        g.manual_seed(7)
+        acts = torch.randint(0, nA, (T, E, A), dtype=torch.int32, device="cuda", generator=g)
+        obs = torch.empty(T, E, A, D, dtype=tdt, device="cuda")
+        rew = torch.empty(T, E, device="cuda")
+        done = torch.empty(T, E, dtype=torch.uint8, device="cuda")
+        t_next = [0]
+
+        def step():
+            R.rollout_step(cfg, state, t_next[0], acts, obs, rew, done)
+            t_next[0] += T
+
+        kern_ms, wall_ms = timed(step, args.steps, args.warmup)
+        nbytes = E * T * (A * 4 + A * D * es + 4 + 1) + 2 * E * planes * 4
+        return dict(kern_ms=kern_ms, wall_ms=wall_ms, bytes=nbytes, gbs=nbytes / (kern_ms * 1e-3) / 1e9,
+                    env_steps_s=E * T / (wall_ms * 1e-3))
+
+    def policy_case(dt):
+        pol = R.Policy(ws, bs, dt)
+        rows = E * A * T
+        g = torch.Generator(device="cuda")
+        g.manual_seed(3)
+        x = torch.randint(0, 3, (rows, D), device="cuda", generator=g).to(pol.torch_dtype)
+        logits = torch.empty(rows, nA, device="cuda")
+
+        def step():
+            R.policy_forward(pol, x, logits=logits)
+
+        kern_ms, wall_ms = timed(step, args.steps, args.warmup)
+        flops = rows * flop_per_row
+        return dict(kern_ms=kern_ms, rows=rows, flops=flops, tflops=flops / (kern_ms * 1e-3) / 1e12)
+
+    if args.only:
+        kind, dt = args.only.split("_")
+        {"run": rollout_case, "env": env_case, "policy": policy_case}[kind](dt)
+        torch.cuda.synchronize()
+        print(json.dumps({"only": args.only, "done": True}))
+        return
+
+    results["run_bf16"] = rollout_case("bf16")
+    results["run_f32"] = rollout_case("f32")
+    results["env_bf16"] = env_case("bf16")
+    results["env_f32"] = env_case("f32")
+    results["policy_bf16"] = policy_case("bf16")
+    results["policy_f32"] = policy_case("f32")
+
+    rb, rf = results["run_bf16"], results["run_f32"]
+    line = {
+        "metric": METRIC,
+        "value": round(rb["value"], 1),
+        "unit": "agent-env steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(rb["wall_ms"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded LBF episodes, random-init MLP weights N(0, 1/fan_in))",
+        "config": {"workload": "LBF 8x8, 2 agents, 3 food, 4096 envs x 128 steps, MLP 192-128-128-6 bf16",
+                   "n_envs": E, "n_agents": A, "steps_per_rollout": T, "parallelism": "single GPU"},
+        "env_steps_per_s": round(rb["env_steps_s"], 1),
+        "roofline": roofline("hbm", rb["gbs"], HBM_PEAK_GBS, "GB/s", load_traffic("lbf_run_kernel_bf16")),
+        "kernel_ms": round(rb["kern_ms"], 4),
+        "f32": {"value": round(rf["value"], 1), "ms_per_step": round(rf["wall_ms"], 4),
+                "kernel_ms": round(rf["kern_ms"], 4),
+                "roofline": roofline("mfma", rf["tflops"], MFMA_PEAK_TFLOPS["f32"], "TFLOP/s",
+                                     load_traffic("lbf_run_kernel_f32"))},
+        "env_only": {dt: {"env_steps_per_s": round(results[f"env_{dt}"]["env_steps_s"], 1),
+                          "kernel_ms": round(results[f"env_{dt}"]["kern_ms"], 4),
+                          "roofline": roofline("hbm", results[f"env_{dt}"]["gbs"], HBM_PEAK_GBS, "GB/s")}
+                     for dt in ("bf16", "f32")},
+        "policy_forward": {dt: {"rows": results[f"policy_{dt}"]["rows"],
+                                "kernel_ms": round(results[f"policy_{dt}"]["kern_ms"], 4),
+                                "roofline": roofline("mfma", results[f"policy_{dt}"]["tflops"],
+                                                     MFMA_PEAK_TFLOPS[dt], "TFLOP/s")}
+                           for dt in ("bf16", "f32")},
+        "csrc_hash": csrc_hash(),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(args.cpu_envs, T)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
