@@ -49,9 +49,11 @@ struct LbfEnv {
 // Number of int32 state planes: A cells, A levels, F cells, F levels, eaten, steps, den.
 __host__ __device__ inline int lbf_planes(int A, int F) { return 2 * A + 2 * F + 3; }
 
+// AC / FC: agent and food counts when known at compile time (0 = read from p).
+template <int AC = 0, int FC = 0>
 __device__ __forceinline__ void lbf_load(const int32_t* __restrict__ st, const LbfParams& p, int e,
                                          LbfEnv& s) {
-  const int E = p.E, A = p.A, F = p.F;
+  const int E = p.E, A = AC ? AC : p.A, F = FC ? FC : p.F;
 #pragma unroll
   for (int i = 0; i < LBF_MAXA; ++i)
     if (i < A) {
@@ -69,9 +71,10 @@ __device__ __forceinline__ void lbf_load(const int32_t* __restrict__ st, const L
   s.den = st[(size_t)(2 * A + 2 * F + 2) * E + e];
 }
 
+template <int AC = 0, int FC = 0>
 __device__ __forceinline__ void lbf_store(int32_t* __restrict__ st, const LbfParams& p, int e,
                                           const LbfEnv& s) {
-  const int E = p.E, A = p.A, F = p.F;
+  const int E = p.E, A = AC ? AC : p.A, F = FC ? FC : p.F;
 #pragma unroll
   for (int i = 0; i < LBF_MAXA; ++i)
     if (i < A) {
@@ -104,23 +107,22 @@ __device__ __forceinline__ int lbf_kth_free(int idx, int n_occ, CountLE count_le
   return x;
 }
 
-// Draw a fresh episode for global env id `env` from the reset stream at step t.
-__device__ __forceinline__ void lbf_reset(const LbfParams& p, uint64_t env, uint64_t t, LbfEnv& s) {
-  const int A = p.A, F = p.F, W = p.W;
-  const int nd = 2 * A + 2 * F;
-  const Block4 b0 = draw_block(p.seed, env, t, 0, TAG_RESET);
-  Block4 b1 = b0, b2 = b0;
-  if (nd > 8) b1 = draw_block(p.seed, env, t, 1, TAG_RESET);
-  if (nd > 16) b2 = draw_block(p.seed, env, t, 2, TAG_RESET);
-  // The 24 draws as a flat register array; draw(k) selects with compares so
-  // that a runtime k never turns the array into scratch memory.
-  uint32_t dw[24];
-#pragma unroll
-  for (int q = 0; q < 24; ++q) dw[q] = block_u32(q < 8 ? b0 : (q < 16 ? b1 : b2), q & 7);
+// Number of 32-bit reset draws (and Philox blocks) an episode of this config uses.
+__host__ __device__ inline int lbf_reset_draws(int A, int F) { return 2 * A + 2 * F; }
+constexpr int LBF_MAX_DRAWS = 2 * LBF_MAXA + 2 * LBF_MAXF;  // 24 = 3 blocks
+
+// Build a fresh episode from its reset draws dw[0..2A+2F-1] (draw k = 32-bit
+// word k of the reset stream of (env, t)).
+template <int AC = 0, int FC = 0>
+__device__ __forceinline__ void lbf_reset_from_draws(const LbfParams& p, const uint32_t (&dw)[LBF_MAX_DRAWS],
+                                                     LbfEnv& s) {
+  const int A = AC ? AC : p.A, F = FC ? FC : p.F, W = p.W;
+  // draw(k) selects with compares so that a runtime k never turns the
+  // array into scratch memory.
   auto draw = [&](int k) -> uint32_t {
     uint32_t v = 0;
 #pragma unroll
-    for (int q = 0; q < 24; ++q) v = (q == k) ? dw[q] : v;
+    for (int q = 0; q < LBF_MAX_DRAWS; ++q) v = (q == k) ? dw[q] : v;
     return v;
   };
   int lsum = 0;
@@ -174,11 +176,26 @@ __device__ __forceinline__ void lbf_reset(const LbfParams& p, uint64_t env, uint
   s.den = den;
 }
 
+// Draw a fresh episode for global env id `env` from the reset stream at step t.
+template <int AC = 0, int FC = 0>
+__device__ __forceinline__ void lbf_reset(const LbfParams& p, uint64_t env, uint64_t t, LbfEnv& s) {
+  const int nd = lbf_reset_draws(AC ? AC : p.A, FC ? FC : p.F);
+  const Block4 b0 = draw_block(p.seed, env, t, 0, TAG_RESET);
+  Block4 b1 = b0, b2 = b0;
+  if (nd > 8) b1 = draw_block(p.seed, env, t, 1, TAG_RESET);
+  if (nd > 16) b2 = draw_block(p.seed, env, t, 2, TAG_RESET);
+  uint32_t dw[LBF_MAX_DRAWS];
+#pragma unroll
+  for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = block_u32(q < 8 ? b0 : (q < 16 ? b1 : b2), q & 7);
+  lbf_reset_from_draws<AC, FC>(p, dw, s);
+}
+
 // One transition with actions act[0..A-1] (out-of-range -> noop).
 // Writes reward and done; `s` becomes the post-transition state (no reset).
+template <int AC = 0, int FC = 0>
 __device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, const int (&act_in)[LBF_MAXA],
                                                float& reward, uint32_t& done) {
-  const int A = p.A, F = p.F, W = p.W, H = p.H;
+  const int A = AC ? AC : p.A, F = FC ? FC : p.F, W = p.W, H = p.H;
   int act[LBF_MAXA];
 #pragma unroll
   for (int i = 0; i < LBF_MAXA; ++i) act[i] = (act_in[i] >= 0 && act_in[i] < LBF_NACT) ? act_in[i] : 0;

@@ -15,6 +15,7 @@
 //     (rl_mlp.h) with operand tiles in LDS;
 //   * sampling: one thread per (row, action) draws the Gumbel noise.
 #include "rl_internal.h"
+#include "rl_regmlp.h"
 #include "rl_sample.h"
 
 namespace rl {
@@ -37,17 +38,19 @@ struct LbfLds {
 // Write (on) or erase (!on) env `el`'s agents and uneaten foods in the LDS
 // grids.  Cell ids are masked to the grid buffer so that a malformed state
 // supplied by the caller cannot address LDS outside its own env's grid.
+template <int AC = 0, int FC = 0>
 __device__ __forceinline__ void lbf_paint(const LbfParams& p, const LbfEnv& s, int el, const LbfLds& L, bool on) {
   constexpr int CM = LBF_MAXCELLS - 1;
+  const int A = AC ? AC : p.A, F = FC ? FC : p.F;
 #pragma unroll
   for (int i = 0; i < LBF_MAXA; ++i)
-    if (i < p.A) {
+    if (i < A) {
       L.agrid[el * LBF_MAXCELLS + (s.acell[i] & CM)] = on ? (uint8_t)s.alevel[i] : 0;
       if (on) L.acell[el * LBF_MAXA + i] = s.acell[i];
     }
 #pragma unroll
   for (int j = 0; j < LBF_MAXF; ++j)
-    if (j < p.F && !((s.eaten >> j) & 1u))
+    if (j < F && !((s.eaten >> j) & 1u))
       L.fgrid[el * LBF_MAXCELLS + (s.fcell[j] & CM)] = on ? (uint8_t)s.flevel[j] : 0;
 }
 
@@ -66,13 +69,13 @@ __device__ __forceinline__ uint16_t small_int_to<uint16_t>(uint32_t v) {
 // gdst: the tile's first element in global [.., A, D] (or null); ldst: LDS
 // operand tile with leading dimension ldl (or null).  Rows of envs beyond
 // te_valid are zero in LDS and not written to global memory.
-template <typename OT>
+template <typename OT, int TE = TILE_E, int NT = NTHREADS>
 __device__ __forceinline__ void lbf_encode(const LbfParams& p, const LbfMagic& m, int te_valid, const LbfLds& L,
                                            OT* __restrict__ gdst, OT* __restrict__ ldst, int ldl, int tid) {
   const int A = p.A, D = p.D, HW = p.HW;
   if ((D & 7) == 0 && (HW & 7) == 0) {
-    const int nvec = TILE_E * A * (D >> 3);
-    for (int v = tid; v < nvec; v += NTHREADS) {
+    const int nvec = TE * A * (D >> 3);
+    for (int v = tid; v < nvec; v += NT) {
       const int idx = v << 3;
       const int r = fdiv(idx, m.d), k = idx - r * D;
       const int el = fdiv(r, m.a), a = r - el * A;
@@ -111,8 +114,8 @@ __device__ __forceinline__ void lbf_encode(const LbfParams& p, const LbfMagic& m
       }
     }
   } else {
-    const int total = TILE_E * A * D;
-    for (int idx = tid; idx < total; idx += NTHREADS) {
+    const int total = TE * A * D;
+    for (int idx = tid; idx < total; idx += NT) {
       const int r = fdiv(idx, m.d), k = idx - r * D;
       const int el = fdiv(r, m.a), a = r - el * A;
       const int plane = fdiv(k, m.hw), cell = k - plane * HW;
@@ -318,6 +321,233 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
   if (envlane) lbf_store(state, p, e, s);
 }
 
+// ------------------------------------ fused rollout, weights in registers ----
+//
+// Same step as lbf_run_kernel for compile-time policy sizes, restructured for
+// latency: the layer-1/2 weights live in registers and layer 3 in LDS for the
+// whole rollout; the Gumbel noise of NOISE_STEPS steps is drawn in one batch;
+// wave 0 computes layer 3, the Gumbel argmax (cross-lane, no LDS round trip)
+// and then steps its TE envs, drawing any reset blocks on idle lanes in
+// parallel.  TE envs per workgroup; two workgroups share a CU.
+
+constexpr int NOISE_STEPS = 8;
+
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <int DT, int D, int H1, int H2, int NA, int A, int F, int TE, int NW, int MINB>
+__global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p, LbfMagic m, PolicyArgs pol,
+                                                                 int32_t* __restrict__ state, uint64_t t0,
+                                                                 int n_steps, TrajArgs out) {
+  using T = typename DType<DT>::T;
+  using B = typename BOperand<DT>::type;
+  constexpr int NT = NW * 64;
+  constexpr int R = TE * A;
+  constexpr int MT = (R + 15) / 16;
+  constexpr int RP = MT * 16;
+  constexpr int LDX = lds_ld<DT>(D), LD1 = lds_ld<DT>(H1), LD2 = lds_ld<DT>(H2);
+  constexpr int K3 = round_up(H2, DType<DT>::KS) / DType<DT>::KS;
+  static_assert(NA <= 8, "one Philox block of action noise per row");
+  static_assert(TE <= 64, "env lanes live in wave 0");
+
+  __shared__ __align__(16) uint8_t agrid[TE * LBF_MAXCELLS];
+  __shared__ __align__(16) uint8_t fgrid[TE * LBF_MAXCELLS];
+  __shared__ int acell_s[TE * LBF_MAXA];
+  __shared__ int act_s[RP];
+  __shared__ __align__(16) T xs[RP * LDX];
+  __shared__ __align__(16) T h1s[RP * LD1];
+  __shared__ __align__(16) T h2s[RP * LD2];
+  __shared__ __align__(16) B w3s[K3 * 64];
+  __shared__ uint32_t nz[NOISE_STEPS * RP * 8];   // per (step, row): 8 draws, then float noise in place
+  __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];  // reset draws of envs being reset
+
+  const LbfLds L{agrid, fgrid, acell_s};
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int e0 = blockIdx.x * TE;
+  const int te_valid = min(TE, p.E - e0);
+  const int E = p.E;
+
+  RegLayer<DT, D, H1, NW> L1;
+  RegLayer<DT, H1, H2, NW> L2;
+  L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane);
+  L2.load(static_cast<const T*>(pol.W[1]), static_cast<const T*>(pol.b[1]), wave, lane);
+  const T* W3 = static_cast<const T*>(pol.W[2]);
+  if (tid < 64) {
+    const int n = lane & 15;
+    const T* row = W3 + (size_t)(n < NA ? n : 0) * H2;
+#pragma unroll
+    for (int ks = 0; ks < K3; ++ks) w3s[ks * 64 + lane] = load_operand_global<DT>(row, H2, ks, lane, n < NA);
+  }
+  const float b3 = (lane & 15) < NA ? DType<DT>::to_f32(static_cast<const T*>(pol.b[2])[lane & 15]) : 0.f;
+
+  // zero the grids and the K padding / unused rows of the operand tiles
+  zero_lds(agrid, sizeof(agrid), tid);
+  zero_lds(fgrid, sizeof(fgrid), tid);
+  for (int i = tid; i < RP * LDX; i += NT) xs[i] = (T)0;
+  for (int i = tid; i < RP * LD1; i += NT) h1s[i] = (T)0;
+  for (int i = tid; i < RP * LD2; i += NT) h2s[i] = (T)0;
+  __syncthreads();
+  const bool envlane = tid < te_valid;
+  const int e = e0 + tid;
+  LbfEnv s{};
+  if (envlane) {
+    lbf_load<A, F>(state, p, e, s);
+    lbf_paint<A, F>(p, s, tid, L, true);
+  }
+  constexpr int nd = 2 * A + 2 * F;
+  constexpr int nblk = (nd + 7) >> 3;
+
+  for (int k = 0; k < n_steps; ++k) {
+    const uint64_t t = t0 + (uint64_t)k;
+    const int sn = k % NOISE_STEPS;
+    if (sn == 0) {
+      // Gumbel noise of the next NOISE_STEPS steps: one Philox block per (step, row) ...
+      const int nb = min(NOISE_STEPS, n_steps - k);
+      for (int i = tid; i < nb * R; i += NT) {
+        const int st = i / R, row = i - st * R;
+        const int el = row / A, ag = row - el * A;
+        if (el < te_valid) {
+          const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + el), t + st, (uint64_t)ag * 256u,
+                                      TAG_ACTION);
+          uint32_t* d = nz + (st * RP + row) * 8;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) d[q] = block_u32(b, q);
+        }
+      }
+      __syncthreads();
+      // ... then the noise value of every action, in place
+      for (int i = tid; i < nb * R * NA; i += NT) {
+        const int sr = i / NA, a = i - sr * NA;
+        const int st = sr / R, row = sr - st * R;
+        uint32_t* d = nz + (st * RP + row) * 8 + a;
+        *d = __float_as_uint(gumbel24(*d >> 8));
+      }
+    }
+    __syncthreads();  // previous step's env updates (and the noise) are visible
+    lbf_encode<T, TE, NT>(p, m, te_valid, L, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr,
+                          xs, LDX, tid);
+    __syncthreads();
+    {
+      f32x4 acc[MT][RegLayer<DT, D, H1, NW>::OWN];
+      L1.template run<MT>(xs, LDX, acc, wave, lane);
+      L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane);
+    }
+    __syncthreads();
+    {
+      f32x4 acc[MT][RegLayer<DT, H1, H2, NW>::OWN];
+      L2.template run<MT>(h1s, LD1, acc, wave, lane);
+      L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      // layer 3 and Gumbel-max: lane holds action a = lane % 16 of rows 4 * (lane / 16) + r
+      const int a = lane & 15;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < K3; ++ks)
+          acc = mfma16<DT>(load_operand_lds<DT>(h2s, LD2, mt * 16 + (lane & 15), ks, lane), w3s[ks * 64 + lane], acc);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = mt * 16 + 4 * (lane >> 4) + r;
+          const float logit = acc[r] + b3;
+          const bool live = row < te_valid * A;
+          float sc = -INFINITY;
+          if (a < NA && row < R) sc = action_score(logit, __uint_as_float(nz[(sn * RP + row) * 8 + a]), true);
+          int best = a;
+#pragma unroll
+          for (int off = 8; off >= 1; off >>= 1) {
+            const float osc = __shfl_xor(sc, off, 16);
+            const int ob = __shfl_xor(best, off, 16);
+            if (osc > sc || (osc == sc && ob < best)) {
+              sc = osc;
+              best = ob;
+            }
+          }
+          if (live) {
+            if (a < NA && out.logits) out.logits[(((size_t)k * E + e0) * A + row) * NA + a] = logit;
+            if (a == 0) {
+              act_s[row] = best;
+              if (out.actions) out.actions[((size_t)k * E + e0) * A + row] = best;
+            }
+          }
+        }
+      }
+      wave_lds_sync();
+      uint32_t d = 0;
+      float r = 0.f;
+      if (envlane) {
+        int act[LBF_MAXA];
+#pragma unroll
+        for (int i = 0; i < LBF_MAXA; ++i) act[i] = i < A ? act_s[tid * A + i] : 0;
+        lbf_paint<A, F>(p, s, tid, L, false);
+        lbf_transition<A, F>(p, s, act, r, d);
+      }
+      // reset blocks of every env that ended, one Philox block per lane
+      const uint64_t done_mask = __ballot(envlane && d != 0);
+      if (done_mask) {
+        const int j = lane / nblk, blk = lane - j * nblk;
+        if (j < TE && ((done_mask >> j) & 1ull)) {
+          const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + j), t + 1, (uint64_t)blk, TAG_RESET);
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            if (blk * 8 + q < LBF_MAX_DRAWS) rdraw[j * LBF_MAX_DRAWS + blk * 8 + q] = block_u32(b, q);
+        }
+        wave_lds_sync();
+        if (envlane && d) {
+          uint32_t dw[LBF_MAX_DRAWS];
+#pragma unroll
+          for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[tid * LBF_MAX_DRAWS + q] : 0u;
+          lbf_reset_from_draws<A, F>(p, dw, s);
+        }
+      }
+      if (envlane) {
+        lbf_paint<A, F>(p, s, tid, L, true);
+        if (out.reward) out.reward[(size_t)k * E + e] = r;
+        if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
+      }
+    }
+  }
+  __syncthreads();
+  if (out.obs_last)
+    lbf_encode<T, TE, NT>(p, m, te_valid, L, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, nullptr, 0, tid);
+  if (envlane) lbf_store<A, F>(state, p, e, s);
+}
+
+// Compile-time shapes that run on lbf_rollout_kernel (everything else uses
+// lbf_run_kernel): LBF 8x8 with 2 agents and 3 foods (obs 192) under 64- and
+// 128-wide layers, and LBF 12x12 with 3 agents and 6 foods (obs 432) under
+// 256-wide layers.
+template <int DT, int D, int H1, int H2, int A, int F, int TE, int NW, int MINB>
+static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const PolicyArgs& pol, int32_t* state,
+                                     uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s) {
+  auto kern = lbf_rollout_kernel<DT, D, H1, H2, LBF_NACT, A, F, TE, NW, MINB>;
+  const dim3 grid((unsigned)((p.E + TE - 1) / TE));
+  kern<<<grid, NW * 64, 0, s>>>(p, m, pol, state, t0, n_steps, out);
+  return hipGetLastError();
+}
+
+static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const PolicyArgs& pol, int32_t* state,
+                                   uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s, hipError_t* err) {
+  if (pol.NA != LBF_NACT) return false;
+#define RL_REG_CASE(DTV, DV, H1V, H2V, AV, FV, TEV, NWV, MINBV)                                                   \
+  if (pol.dt == DTV && pol.D == DV && pol.H1 == H1V && pol.H2 == H2V && p.A == AV && p.F == FV) {                 \
+    *err = launch_rollout_reg<DTV, DV, H1V, H2V, AV, FV, TEV, NWV, MINBV>(p, m, pol, state, t0, n_steps, out, s); \
+    return true;                                                                                                  \
+  }
+  // (dtype, obs, hidden, hidden, agents, foods, envs per workgroup, waves, workgroups per CU)
+  RL_REG_CASE(DT_F32, 192, 64, 64, 2, 3, 8, 4, 2)
+  RL_REG_CASE(DT_BF16, 192, 64, 64, 2, 3, 8, 4, 2)
+  RL_REG_CASE(DT_F32, 192, 128, 128, 2, 3, 16, 4, 1)
+  RL_REG_CASE(DT_BF16, 192, 128, 128, 2, 3, 8, 4, 2)
+#undef RL_REG_CASE
+  return false;
+}
+
 // ------------------------------------------------------------ launchers ----
 
 static dim3 tiles(int E) { return dim3((unsigned)((E + TILE_E - 1) / TILE_E)); }
@@ -347,6 +577,8 @@ hipError_t launch_lbf_step(const LbfParams& p, int32_t* state, uint64_t t0, int 
 hipError_t launch_lbf_run(const LbfParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
                           const TrajArgs& out, hipStream_t s) {
   const LbfMagic m = make_magic(p, pol.NA);
+  hipError_t err;
+  if (try_launch_rollout_reg(p, m, pol, state, t0, n_steps, out, s, &err)) return err;
   const RunLayout RL = make_run_layout(p.A, p.D, pol.H1, pol.H2, pol.dt);
   if (pol.dt == DT_F32) {
     static bool attr_f32 = false;

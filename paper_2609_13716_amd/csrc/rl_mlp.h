@@ -10,8 +10,8 @@
 // both accumulating in float32.  Operand lanes: A row = lane % 16, B column =
 // lane % 16, each lane covering one K slice (lane / 16); the 16 x 16 result
 // holds row 4 * (lane / 16) + r, column lane % 16 in accumulator element r.
-// Hidden layers apply tanh and store in the layer dtype (bf16: round to
-// nearest even); the output layer stores float32 logits.
+// Hidden layers apply tanh (fast_tanh) and store in the layer dtype (bf16:
+// round to nearest even); the output layer stores float32 logits.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -52,6 +52,14 @@ struct DType<DT_BF16> {
 
 __host__ __device__ constexpr int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
+// tanh(x) = 1 - 2 / (exp(2x) + 1) with the hardware exp2 and reciprocal
+// (v_exp_f32, v_rcp_f32).  Absolute error is a few 1e-7; +-inf and large
+// |x| give +-1 exactly, NaN stays NaN.
+__device__ __forceinline__ float fast_tanh(float x) {
+  const float e = __builtin_amdgcn_exp2f(x * 2.8853900817779268f);  // 2 / ln(2)
+  return 1.f - 2.f * __builtin_amdgcn_rcpf(e + 1.f);
+}
+
 // Leading dimension (elements) of an LDS operand tile holding K columns:
 // K padded to the MFMA K step, plus 16 bytes so that consecutive rows start
 // on different LDS banks.
@@ -71,7 +79,6 @@ __device__ __forceinline__ f32x4 mma_tile(const typename DType<DT>::T* __restric
   if constexpr (DT == DT_F32) {
     const float* arow = in + (size_t)(m0 + (lane & 15)) * lda + (lane >> 4);
     const float* wrow = W + (size_t)(nok ? n : 0) * K + (lane >> 4);
-#pragma unroll 8
     for (int k0 = 0; k0 < Kpad; k0 += 4) {
       const float a = arow[k0];
       const float b = (nok && k0 + (lane >> 4) < K) ? wrow[k0] : 0.f;
@@ -81,7 +88,6 @@ __device__ __forceinline__ f32x4 mma_tile(const typename DType<DT>::T* __restric
     const uint16_t* arow = in + (size_t)(m0 + (lane & 15)) * lda + (lane >> 4) * 8;
     const uint16_t* wrow = W + (size_t)(nok ? n : 0) * K + (lane >> 4) * 8;
     const bool vec = (K & 7) == 0;
-#pragma unroll 2
     for (int k0 = 0; k0 < Kpad; k0 += 32) {
       const u32x4 a = *reinterpret_cast<const u32x4*>(arow + k0);
       u32x4 b = {0u, 0u, 0u, 0u};
@@ -126,7 +132,7 @@ __device__ __forceinline__ void mlp_hidden(const typename DType<DT>::T* in, int 
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = m0 + 4 * (lane >> 4) + r;
-      out[(size_t)row * ldo + col] = DTy::from_f32(tanhf(acc[r] + bias));
+      out[(size_t)row * ldo + col] = DTy::from_f32(fast_tanh(acc[r] + bias));
     }
   }
 }

@@ -1,0 +1,130 @@
+// Policy layers whose weights stay in registers for a whole rollout.
+//
+// A layer's N outputs are cut into 16-column tiles; tile j belongs to wave
+// j % NW.  At kernel start each wave loads the MFMA B operands of its tiles
+// for every K step into VGPRs (W in the nn.Linear layout [N x K]), so the
+// per-step matrix products read only the LDS activation tile and registers.
+// Same MFMA shapes and operand layouts as rl_mlp.h.
+#pragma once
+#include <type_traits>
+
+#include "rl_mlp.h"
+
+namespace rl {
+
+template <int DT>
+struct BOperand {
+  using type = float;  // f32: one K element per lane per K step of 4
+};
+template <>
+struct BOperand<DT_BF16> {
+  using type = u32x4;  // bf16: eight K elements per lane per K step of 32
+};
+
+template <int DT>
+__device__ __forceinline__ f32x4 mfma16(const typename BOperand<DT>::type& a, const typename BOperand<DT>::type& b,
+                                        f32x4 acc) {
+  if constexpr (DT == DT_F32) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+  } else {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc,
+                                                   0, 0, 0);
+  }
+}
+
+// The B operand (or an A operand read from a row) of one lane for K step ks:
+// f32 lanes hold element ks*4 + lane/16, bf16 lanes hold elements
+// ks*32 + (lane/16)*8 .. +7.  Elements at or beyond K read as zero.
+template <int DT>
+__device__ __forceinline__ typename BOperand<DT>::type load_operand_global(const typename DType<DT>::T* row, int K,
+                                                                           int ks, int lane, bool valid) {
+  if constexpr (DT == DT_F32) {
+    const int k = ks * 4 + (lane >> 4);
+    return (valid && k < K) ? row[k] : 0.f;
+  } else {
+    const int k0 = ks * 32 + (lane >> 4) * 8;
+    uint32_t h[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = (valid && k0 + 2 * q < K) ? row[k0 + 2 * q] : 0u;
+      const uint32_t hi = (valid && k0 + 2 * q + 1 < K) ? row[k0 + 2 * q + 1] : 0u;
+      h[q] = lo | (hi << 16);
+    }
+    return u32x4{h[0], h[1], h[2], h[3]};
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ typename BOperand<DT>::type load_operand_lds(const typename DType<DT>::T* tile, int ld,
+                                                                        int row, int ks, int lane) {
+  if constexpr (DT == DT_F32) {
+    return tile[row * ld + ks * 4 + (lane >> 4)];
+  } else {
+    return *reinterpret_cast<const u32x4*>(tile + row * ld + ks * 32 + (lane >> 4) * 8);
+  }
+}
+
+template <int DT, int K, int N, int NW>
+struct RegLayer {
+  using T = typename DType<DT>::T;
+  using B = typename BOperand<DT>::type;
+  static constexpr int KS = DType<DT>::KS;
+  static constexpr int KSTEPS = round_up(K, KS) / KS;
+  static constexpr int NT = N / 16;
+  static constexpr int OWN = (NT + NW - 1) / NW;
+  static_assert(N % 16 == 0, "layer width must be a multiple of 16");
+
+  B w[OWN][KSTEPS];
+  float bias[OWN];
+
+  __device__ __forceinline__ void load(const T* __restrict__ W, const T* __restrict__ b, int wave, int lane) {
+#pragma unroll
+    for (int o = 0; o < OWN; ++o) {
+      const int tile = wave + o * NW;
+      const bool valid = tile < NT;
+      const int n = tile * 16 + (lane & 15);
+      const T* row = W + (size_t)(valid ? n : 0) * K;
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks) w[o][ks] = load_operand_global<DT>(row, K, ks, lane, valid);
+      bias[o] = valid ? DType<DT>::to_f32(b[n]) : 0.f;
+    }
+  }
+
+  // acc[m][o] = in[m*16 .. m*16+15, :] . W[tile(o) cols]^T over all K steps.
+  template <int MT>
+  __device__ __forceinline__ void run(const T* in, int ld, f32x4 (&acc)[MT][OWN], int wave, int lane) const {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int o = 0; o < OWN; ++o) acc[m][o] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const B a = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks, lane);
+#pragma unroll
+        for (int o = 0; o < OWN; ++o)
+          if (wave + o * NW < NT) acc[m][o] = mfma16<DT>(a, w[o][ks], acc[m][o]);
+      }
+    }
+  }
+
+  // out = tanh(acc + bias) in the layer dtype, for the wave's tiles.
+  template <int MT>
+  __device__ __forceinline__ void store_tanh(const f32x4 (&acc)[MT][OWN], T* out, int ld, int wave, int lane) const {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int o = 0; o < OWN; ++o) {
+        if (wave + o * NW >= NT) continue;
+        const int col = (wave + o * NW) * 16 + (lane & 15);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = m * 16 + 4 * (lane >> 4) + r;
+          out[row * ld + col] = DType<DT>::from_f32(fast_tanh(acc[m][o][r] + bias[o]));
+        }
+      }
+  }
+};
+
+}  // namespace rl

@@ -352,3 +352,37 @@ def test_rollout_run_12x12_sampled_envs():
     assert np.array_equal(g_act, ref["actions"])
     assert_logits_close(logits[:, sample].cpu().numpy(), ref["logits"], RTOL["bf16"])
     assert [states_from_device(cfg, state)[e] for e in sample] == ref["states"]
+
+
+@pytest.mark.parametrize("name,dtype", [("lbf8_4096", "bf16"), ("lbf8_4096", "f32"), ("lbf8_small", "f32")])
+def test_rollout_logits_equal_policy_forward(name, dtype):
+    """The logits a rollout samples from are exactly policy_forward of the recorded observations."""
+    require_gpu()
+    w = workloads.WORKLOADS[name]
+    cfg = R.EnvConfig(n_envs=min(w["n_envs"], 1024), seed=9, **w["env"])
+    dims = workloads.policy_dims(name)
+    ws, bs = workloads.policy_weights(dims, seed=77, bias_scale=0.2)
+    pol = R.Policy(ws, bs, dtype)
+    _, g = _run_gpu(cfg, pol, 40)
+    obs = g["obs"].reshape(-1, dims[0]).cuda()
+    pf = R.policy_forward(pol, obs).cpu().reshape(g["logits"].shape)
+    assert torch.equal(pf, g["logits"])
+
+
+def test_rollout_run_generic_shapes():
+    """Shapes without a register-resident specialisation (5x7 grid, 4 agents, 2 foods, 32-wide layers)."""
+    require_gpu()
+    cfg = R.EnvConfig(n_envs=45, grid_h=5, grid_w=7, n_agents=4, n_food=2, max_agent_level=3, max_food_level=9,
+                      max_steps=20, seed=31, env_base=1000)
+    dims = (105, 32, 48, 6)
+    for dtype in ("f32", "bf16"):
+        ws, bs = workloads.policy_weights(dims, seed=5, bias_scale=0.1)
+        pol = R.Policy(ws, bs, dtype)
+        T = 70
+        state, g = _run_gpu(cfg, pol, T)
+        oc = oracle_cfg(cfg)
+        env_ids = list(range(1000, 1045))
+        hook = NearTieLockstep(g["actions"].numpy(), cfg.seed, env_ids, RTOL[dtype])
+        ref = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, dtype, action_hook=hook)
+        _check_traj(g, ref, slice(None), RTOL[dtype])
+        assert states_from_device(cfg, state) == ref["states"]
