@@ -403,6 +403,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     const int sn = k % NOISE_STEPS;
+    __syncthreads();  // wave 0 is done with the previous step (grids, noise, actions)
     if (sn == 0) {
       // Gumbel noise of the next NOISE_STEPS steps: one Philox block per (step, row) ...
       const int nb = min(NOISE_STEPS, n_steps - k);
@@ -425,8 +426,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         uint32_t* d = nz + (st * RP + row) * 8 + a;
         *d = __float_as_uint(gumbel24(*d >> 8));
       }
+      __syncthreads();
     }
-    __syncthreads();  // previous step's env updates (and the noise) are visible
     lbf_encode<T, TE, NT>(p, m, te_valid, L, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr,
                           xs, LDX, tid);
     __syncthreads();
