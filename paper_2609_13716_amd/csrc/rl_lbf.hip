@@ -135,6 +135,70 @@ __device__ __forceinline__ void lbf_encode(const LbfParams& p, const LbfMagic& m
   }
 }
 
+// lbf_encode with the tile shape known at compile time (D and the grid size
+// multiples of 8): every 16-byte vector of the tile is handled by one thread
+// in a fully unrolled loop, so the LDS grid reads of all iterations are in
+// flight together.
+template <typename OT, int TE, int A, int D, int NT>
+__device__ __forceinline__ void lbf_encode_ct(int te_valid, const LbfLds& L, OT* __restrict__ gdst,
+                                              OT* __restrict__ ldst, int ldl, int tid) {
+  constexpr int HW = D / 3;
+  static_assert(D % 8 == 0 && HW % 8 == 0, "vectorised encoder needs 8-aligned planes");
+  constexpr int NV = TE * A * D / 8;
+  constexpr int ITERS = (NV + NT - 1) / NT;
+  uint64_t bytes[ITERS];
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int v = tid + it * NT;
+    bytes[it] = 0;
+    if (v < NV) {
+      const int idx = v * 8;
+      const int r = idx / D, k = idx - r * D;
+      const int el = r / A, a = r - el * A;
+      const int plane = k / HW, cell0 = k - plane * HW;
+      if (el < te_valid) {
+        if (plane == 0) {
+          bytes[it] = *reinterpret_cast<const uint64_t*>(L.agrid + el * LBF_MAXCELLS + cell0);
+        } else if (plane == 1) {
+          bytes[it] = *reinterpret_cast<const uint64_t*>(L.fgrid + el * LBF_MAXCELLS + cell0);
+        } else {
+          const int c = L.acell[el * LBF_MAXA + a] - cell0;
+          if (c >= 0 && c < 8) bytes[it] = 1ull << (8 * c);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int v = tid + it * NT;
+    if (v >= NV) continue;
+    const int idx = v * 8;
+    const int r = idx / D, k = idx - r * D;
+    const int el = r / A;
+    OT vals[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) vals[q] = small_int_to<OT>((uint32_t)(bytes[it] >> (8 * q)) & 0xffu);
+    if constexpr (sizeof(OT) == 2) {
+      u32x4 w;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)vals[2 * q] | ((uint32_t)vals[2 * q + 1] << 16);
+      if (ldst) *reinterpret_cast<u32x4*>(ldst + (size_t)r * ldl + k) = w;
+      if (gdst && el < te_valid) *reinterpret_cast<u32x4*>(gdst + idx) = w;
+    } else {
+      const f32x4 w0 = {vals[0], vals[1], vals[2], vals[3]};
+      const f32x4 w1 = {vals[4], vals[5], vals[6], vals[7]};
+      if (ldst) {
+        *reinterpret_cast<f32x4*>(ldst + (size_t)r * ldl + k) = w0;
+        *reinterpret_cast<f32x4*>(ldst + (size_t)r * ldl + k + 4) = w1;
+      }
+      if (gdst && el < te_valid) {
+        *reinterpret_cast<f32x4*>(gdst + idx) = w0;
+        *reinterpret_cast<f32x4*>(gdst + idx + 4) = w1;
+      }
+    }
+  }
+}
+
 __device__ __forceinline__ void lbf_write_legal(const LbfParams& p, int te_valid, uint8_t* __restrict__ g, int tid) {
   const int n = te_valid * p.A * LBF_NACT;
   for (int i = tid; i < n; i += NTHREADS) g[i] = 1;
@@ -428,8 +492,9 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       }
       __syncthreads();
     }
-    lbf_encode<T, TE, NT>(p, m, te_valid, L, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr,
-                          xs, LDX, tid);
+    lbf_encode_ct<T, TE, A, D, NT>(te_valid, L,
+                                   out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, xs,
+                                   LDX, tid);
     __syncthreads();
     {
       f32x4 acc[MT][RegLayer<DT, D, H1, NW>::OWN];
@@ -446,29 +511,28 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     if (wave == 0) {
       // layer 3 and Gumbel-max: lane holds action a = lane % 16 of rows 4 * (lane / 16) + r
       const int a = lane & 15;
+      B w3r[K3];
+#pragma unroll
+      for (int ks = 0; ks < K3; ++ks) w3r[ks] = w3s[ks * 64 + lane];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
+        B a3[K3];
+#pragma unroll
+        for (int ks = 0; ks < K3; ++ks) a3[ks] = load_operand_lds<DT>(h2s, LD2, mt * 16 + (lane & 15), ks, lane);
+        float nzr[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) nzr[r] = __uint_as_float(nz[(sn * RP + mt * 16 + 4 * (lane >> 4) + r) * 8 + (a & 7)]);
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < K3; ++ks)
-          acc = mfma16<DT>(load_operand_lds<DT>(h2s, LD2, mt * 16 + (lane & 15), ks, lane), w3s[ks * 64 + lane], acc);
+        for (int ks = 0; ks < K3; ++ks) acc = mfma16<DT>(a3[ks], w3r[ks], acc);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = mt * 16 + 4 * (lane >> 4) + r;
           const float logit = acc[r] + b3;
           const bool live = row < te_valid * A;
-          float sc = -INFINITY;
-          if (a < NA && row < R) sc = action_score(logit, __uint_as_float(nz[(sn * RP + row) * 8 + a]), true);
+          float sc = action_score(logit, nzr[r], (a < NA) & (row < R));
           int best = a;
-#pragma unroll
-          for (int off = 8; off >= 1; off >>= 1) {
-            const float osc = __shfl_xor(sc, off, 16);
-            const int ob = __shfl_xor(best, off, 16);
-            if (osc > sc || (osc == sc && ob < best)) {
-              sc = osc;
-              best = ob;
-            }
-          }
+          row16_argmax(sc, best);
           if (live) {
             if (a < NA && out.logits) out.logits[(((size_t)k * E + e0) * A + row) * NA + a] = logit;
             if (a == 0) {
@@ -515,7 +579,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   }
   __syncthreads();
   if (out.obs_last)
-    lbf_encode<T, TE, NT>(p, m, te_valid, L, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, nullptr, 0, tid);
+    lbf_encode_ct<T, TE, A, D, NT>(te_valid, L, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, nullptr, 0, tid);
   if (envlane) lbf_store<A, F>(state, p, e, s);
 }
 

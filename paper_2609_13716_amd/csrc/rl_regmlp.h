@@ -97,14 +97,28 @@ struct RegLayer {
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int o = 0; o < OWN; ++o) acc[m][o] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (NT % NW == 0) {
+      // every wave owns OWN full tiles: a branch-free chain, so the compiler
+      // can issue the LDS operand loads ahead of the MFMAs
 #pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) {
+      for (int ks = 0; ks < KSTEPS; ++ks) {
 #pragma unroll
-      for (int m = 0; m < MT; ++m) {
-        const B a = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks, lane);
+        for (int m = 0; m < MT; ++m) {
+          const B a = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks, lane);
 #pragma unroll
-        for (int o = 0; o < OWN; ++o)
-          if (wave + o * NW < NT) acc[m][o] = mfma16<DT>(a, w[o][ks], acc[m][o]);
+          for (int o = 0; o < OWN; ++o) acc[m][o] = mfma16<DT>(a, w[o][ks], acc[m][o]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks) {
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          const B a = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks, lane);
+#pragma unroll
+          for (int o = 0; o < OWN; ++o)
+            if (wave + o * NW < NT) acc[m][o] = mfma16<DT>(a, w[o][ks], acc[m][o]);
+        }
       }
     }
   }
@@ -116,7 +130,7 @@ struct RegLayer {
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int o = 0; o < OWN; ++o) {
-        if (wave + o * NW >= NT) continue;
+        if (NT % NW != 0 && wave + o * NW >= NT) continue;
         const int col = (wave + o * NW) * 16 + (lane & 15);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -126,5 +140,26 @@ struct RegLayer {
       }
   }
 };
+
+// Cross-lane argmax within each 16-lane row of a wave: lexicographic max of
+// (score, -index), i.e. the first index of the largest score.  Uses DPP lane
+// permutations (no LDS traffic): swap neighbours, swap pairs, mirror each
+// half-row, mirror the row; after the four steps every lane of the row holds
+// the result.
+template <int CTRL>
+__device__ __forceinline__ void argmax_dpp_step(float& score, int& idx) {
+  const float os = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(score), CTRL, 0xf, 0xf, false));
+  const int oi = __builtin_amdgcn_update_dpp(0, idx, CTRL, 0xf, 0xf, false);
+  const bool take = (os > score) | ((os == score) & (oi < idx));
+  score = take ? os : score;
+  idx = take ? oi : idx;
+}
+
+__device__ __forceinline__ void row16_argmax(float& score, int& idx) {
+  argmax_dpp_step<0xB1>(score, idx);   // quad_perm [1,0,3,2]
+  argmax_dpp_step<0x4E>(score, idx);   // quad_perm [2,3,0,1]
+  argmax_dpp_step<0x141>(score, idx);  // row_half_mirror
+  argmax_dpp_step<0x140>(score, idx);  // row_mirror
+}
 
 }  // namespace rl

@@ -20,7 +20,7 @@ __device__ __forceinline__ float action_noise(uint64_t seed, uint64_t env, uint6
 __device__ __forceinline__ float action_score(float logit, float noise, bool legal) {
 #pragma clang fp contract(off)
   const float s = logit + noise;
-  return (!legal || __builtin_isnan(s)) ? -INFINITY : s;
+  return (legal & (s == s)) ? s : -INFINITY;
 }
 
 }  // namespace rl
