@@ -192,17 +192,16 @@ __device__ __forceinline__ void lbf_reset(const LbfParams& p, uint64_t env, uint
 
 // One transition with actions act[0..A-1] (out-of-range -> noop).
 // Writes reward and done; `s` becomes the post-transition state (no reset).
+// Written without data-dependent branches: every candidate move and load is
+// evaluated and the outcome selected, so the lanes of a wave never diverge.
 template <int AC = 0, int FC = 0>
 __device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, const int (&act_in)[LBF_MAXA],
                                                float& reward, uint32_t& done) {
   const int A = AC ? AC : p.A, F = FC ? FC : p.F, W = p.W, H = p.H;
-  int act[LBF_MAXA];
-#pragma unroll
-  for (int i = 0; i < LBF_MAXA; ++i) act[i] = (act_in[i] >= 0 && act_in[i] < LBF_NACT) ? act_in[i] : 0;
-
-  int ar[LBF_MAXA], ac[LBF_MAXA], fr[LBF_MAXF], fc[LBF_MAXF];
+  int act[LBF_MAXA], ar[LBF_MAXA], ac[LBF_MAXA], fr[LBF_MAXF], fc[LBF_MAXF];
 #pragma unroll
   for (int i = 0; i < LBF_MAXA; ++i) {
+    act[i] = ((unsigned)act_in[i] < (unsigned)LBF_NACT) ? act_in[i] : 0;
     ar[i] = lbf_row(p, s.acell[i]);
     ac[i] = s.acell[i] - ar[i] * W;
   }
@@ -212,27 +211,20 @@ __device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, co
     fc[j] = s.fcell[j] - fr[j] * W;
   }
 
-  // 1. moves against the pre-step state
+  // 1. moves against the pre-step state: tgt[i] = target cell of a legal move, else -1
   int tgt[LBF_MAXA];
 #pragma unroll
   for (int i = 0; i < LBF_MAXA; ++i) {
-    tgt[i] = -1;
-    if (i < A && act[i] >= 1 && act[i] <= 4) {
-      const int r = ar[i], c = ac[i];
-      const int r2 = r + (act[i] == 1 ? -1 : act[i] == 2 ? 1 : 0);
-      const int c2 = c + (act[i] == 3 ? -1 : act[i] == 4 ? 1 : 0);
-      if (r2 >= 0 && r2 < H && c2 >= 0 && c2 < W) {
-        const int cell = r2 * W + c2;
-        bool blocked = false;
+    const int r2 = ar[i] + (act[i] == 1 ? -1 : 0) + (act[i] == 2 ? 1 : 0);
+    const int c2 = ac[i] + (act[i] == 3 ? -1 : 0) + (act[i] == 4 ? 1 : 0);
+    const int cell = r2 * W + c2;
+    bool ok = (i < A) & (act[i] >= 1) & (act[i] <= 4) & (r2 >= 0) & (r2 < H) & (c2 >= 0) & (c2 < W);
 #pragma unroll
-        for (int j = 0; j < LBF_MAXF; ++j)
-          if (j < F && !((s.eaten >> j) & 1u) && s.fcell[j] == cell) blocked = true;
+    for (int j = 0; j < LBF_MAXF; ++j)
+      ok &= !((j < F) & !((s.eaten >> j) & 1u) & (s.fcell[j] == cell));
 #pragma unroll
-        for (int k = 0; k < LBF_MAXA; ++k)
-          if (k < A && s.acell[k] == cell) blocked = true;
-        if (!blocked) tgt[i] = cell;
-      }
-    }
+    for (int k = 0; k < LBF_MAXA; ++k) ok &= !((k < A) & (s.acell[k] == cell));
+    tgt[i] = ok ? cell : -1;
   }
   int newcell[LBF_MAXA];
 #pragma unroll
@@ -240,8 +232,8 @@ __device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, co
     bool contested = false;
 #pragma unroll
     for (int k = 0; k < LBF_MAXA; ++k)
-      if (k != i && k < A && tgt[k] >= 0 && tgt[k] == tgt[i]) contested = true;
-    newcell[i] = (tgt[i] >= 0 && !contested) ? tgt[i] : s.acell[i];
+      if (k != i) contested |= (k < A) & (tgt[k] == tgt[i]);
+    newcell[i] = ((tgt[i] >= 0) & !contested) ? tgt[i] : s.acell[i];
   }
 
   // 2. loads, with the pre-step positions (loaders do not move)
@@ -249,20 +241,18 @@ __device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, co
   uint32_t eaten = s.eaten;
 #pragma unroll
   for (int j = 0; j < LBF_MAXF; ++j) {
-    if (j < F && !((s.eaten >> j) & 1u)) {
-      int lsum = 0;
+    int lsum = 0;
 #pragma unroll
-      for (int i = 0; i < LBF_MAXA; ++i)
-        if (i < A && act[i] == 5 && abs(ar[i] - fr[j]) + abs(ac[i] - fc[j]) == 1) lsum += s.alevel[i];
-      if (lsum > 0 && lsum >= s.flevel[j]) {
-        eaten |= 1u << j;
-        eaten_sum += s.flevel[j];
-      }
+    for (int i = 0; i < LBF_MAXA; ++i) {
+      const bool adj = (abs(ar[i] - fr[j]) + abs(ac[i] - fc[j])) == 1;
+      lsum += ((i < A) & (act[i] == 5) & adj) ? s.alevel[i] : 0;
     }
+    const bool eat = (j < F) & !((s.eaten >> j) & 1u) & (lsum > 0) & (lsum >= s.flevel[j]);
+    eaten |= eat ? (1u << j) : 0u;
+    eaten_sum += eat ? s.flevel[j] : 0;
   }
 #pragma unroll
-  for (int i = 0; i < LBF_MAXA; ++i)
-    if (i < A) s.acell[i] = newcell[i];
+  for (int i = 0; i < LBF_MAXA; ++i) s.acell[i] = newcell[i];
   s.eaten = eaten;
   reward = (float)eaten_sum / (float)s.den;
   s.steps += 1;

@@ -390,9 +390,10 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
 // Same step as lbf_run_kernel for compile-time policy sizes, restructured for
 // latency: the layer-1/2 weights live in registers and layer 3 in LDS for the
 // whole rollout; the Gumbel noise of NOISE_STEPS steps is drawn in one batch;
-// wave 0 computes layer 3, the Gumbel argmax (cross-lane, no LDS round trip)
-// and then steps its TE envs, drawing any reset blocks on idle lanes in
-// parallel.  TE envs per workgroup; two workgroups share a CU.
+// wave 0 computes layer 3 transposed, the Gumbel argmax (in registers plus one
+// v_permlane16_swap, no LDS round trip) and then steps its TE envs, drawing
+// any reset blocks on idle lanes in parallel.  TE envs per workgroup; the
+// launch bounds let MINB workgroups share a CU.
 
 constexpr int NOISE_STEPS = 8;
 
@@ -445,7 +446,12 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
 #pragma unroll
     for (int ks = 0; ks < K3; ++ks) w3s[ks * 64 + lane] = load_operand_global<DT>(row, H2, ks, lane, n < NA);
   }
-  const float b3 = (lane & 15) < NA ? DType<DT>::to_f32(static_cast<const T*>(pol.b[2])[lane & 15]) : 0.f;
+  float b3r[4];  // bias of actions 4 * (lane / 16) + r, for the transposed layer 3
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int act = 4 * (lane >> 4) + r;
+    b3r[r] = act < NA ? DType<DT>::to_f32(static_cast<const T*>(pol.b[2])[act]) : 0.f;
+  }
 
   // zero the grids and the K padding / unused rows of the operand tiles
   zero_lds(agrid, sizeof(agrid), tid);
@@ -509,37 +515,55 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     }
     __syncthreads();
     if (wave == 0) {
-      // layer 3 and Gumbel-max: lane holds action a = lane % 16 of rows 4 * (lane / 16) + r
-      const int a = lane & 15;
+      // Layer 3 transposed, logits^T = W3 h2^T: lane holds row (lane % 16) of
+      // the M tile and actions 4 * (lane / 16) + r in accumulator element r.
+      // Each lane takes the Gumbel argmax of its four actions; one lane swap
+      // with the partner group (actions 0-3 <-> 4-7) finishes the row.
+      const int g = lane >> 4;
       B w3r[K3];
 #pragma unroll
       for (int ks = 0; ks < K3; ++ks) w3r[ks] = w3s[ks * 64 + lane];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
+        const int row = mt * 16 + (lane & 15);
         B a3[K3];
 #pragma unroll
-        for (int ks = 0; ks < K3; ++ks) a3[ks] = load_operand_lds<DT>(h2s, LD2, mt * 16 + (lane & 15), ks, lane);
-        float nzr[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) nzr[r] = __uint_as_float(nz[(sn * RP + mt * 16 + 4 * (lane >> 4) + r) * 8 + (a & 7)]);
+        for (int ks = 0; ks < K3; ++ks) a3[ks] = load_operand_lds<DT>(h2s, LD2, row, ks, lane);
+        const f32x4 nz4 = *reinterpret_cast<const f32x4*>(nz + (sn * RP + row) * 8 + 4 * (g & 1));
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < K3; ++ks) acc = mfma16<DT>(a3[ks], w3r[ks], acc);
+        for (int ks = 0; ks < K3; ++ks) acc = mfma16<DT>(w3r[ks], a3[ks], acc);
+        float best_s = -INFINITY;
+        int best_a = 0;
+        float logit[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int row = mt * 16 + 4 * (lane >> 4) + r;
-          const float logit = acc[r] + b3;
-          const bool live = row < te_valid * A;
-          float sc = action_score(logit, nzr[r], (a < NA) & (row < R));
-          int best = a;
-          row16_argmax(sc, best);
-          if (live) {
-            if (a < NA && out.logits) out.logits[(((size_t)k * E + e0) * A + row) * NA + a] = logit;
-            if (a == 0) {
-              act_s[row] = best;
-              if (out.actions) out.actions[((size_t)k * E + e0) * A + row] = best;
-            }
-          }
+          const int act = 4 * g + r;
+          logit[r] = acc[r] + b3r[r];
+          const float sc = action_score(logit[r], nz4[r], (act < NA) & (row < R));
+          const bool take = (r == 0) | (sc > best_s);
+          best_s = take ? sc : best_s;
+          best_a = take ? act : best_a;
+        }
+        {
+          const auto ps = __builtin_amdgcn_permlane16_swap(__float_as_uint(best_s), __float_as_uint(best_s), false,
+                                                           false);
+          const auto pa = __builtin_amdgcn_permlane16_swap((uint32_t)best_a, (uint32_t)best_a, false, false);
+          const float os = __uint_as_float((g & 1) ? ps[0] : ps[1]);
+          const int oa = (int)((g & 1) ? pa[0] : pa[1]);
+          const bool take = (os > best_s) | ((os == best_s) & (oa < best_a));
+          best_s = take ? os : best_s;
+          best_a = take ? oa : best_a;
+        }
+        const bool live = row < te_valid * A;
+        if (live && g == 0) {
+          act_s[row] = best_a;
+          if (out.actions) out.actions[((size_t)k * E + e0) * A + row] = best_a;
+        }
+        if (out.logits && live && g < 2) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (4 * g + r < NA) out.logits[(((size_t)k * E + e0) * A + row) * NA + 4 * g + r] = logit[r];
         }
       }
       wave_lds_sync();
