@@ -386,16 +386,8 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
 }
 
 // ------------------------------------ fused rollout, weights in registers ----
-//
-// Same step as lbf_run_kernel for compile-time policy sizes, restructured for
-// latency: the layer-1/2 weights live in registers and layer 3 in LDS for the
-// whole rollout; the Gumbel noise of NOISE_STEPS steps is drawn in one batch;
-// wave 0 computes layer 3 transposed, the Gumbel argmax (in registers plus one
-// v_permlane16_swap, no LDS round trip) and then steps its TE envs, drawing
-// any reset blocks on idle lanes in parallel.  TE envs per workgroup; the
-// launch bounds let MINB workgroups share a CU.
 
-constexpr int NOISE_STEPS = 8;
+constexpr int NOISE_STEPS = 16;
 
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -403,10 +395,63 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Write (on) or erase (!on) env el's non-zero observation features directly
+// in the MFMA operand tile: for each of its A rows, plane 0 holds every
+// agent's level at its cell, plane 1 every uneaten food's level, plane 2 a 1
+// at the row's own agent.  Cell ids are clamped into the grid so that a
+// malformed caller-supplied state cannot address outside the row.
+template <typename T, int A, int F>
+__device__ __forceinline__ void lbf_paint_tile(const LbfEnv& s, int el, T* xs, int ldx, int HW, bool on) {
+  const uint32_t cmax = (uint32_t)HW - 1u;
+  const T one = on ? small_int_to<T>(1u) : (T)0;
+#pragma unroll
+  for (int i = 0; i < A; ++i) {
+    T* xr = xs + (el * A + i) * ldx;
+#pragma unroll
+    for (int q = 0; q < A; ++q) xr[min((uint32_t)s.acell[q], cmax)] = on ? small_int_to<T>((uint32_t)s.alevel[q]) : (T)0;
+#pragma unroll
+    for (int j = 0; j < F; ++j)
+      if (!((s.eaten >> j) & 1u))
+        xr[HW + min((uint32_t)s.fcell[j], cmax)] = on ? small_int_to<T>((uint32_t)s.flevel[j]) : (T)0;
+    xr[2 * HW + min((uint32_t)s.acell[i], cmax)] = one;
+  }
+}
+
+// Copy the tile's live observation rows from LDS to global [.., A, D] rows
+// with 16-byte vectors.
+template <typename T, int R, int D, int LDX, int NT>
+__device__ __forceinline__ void copy_obs_rows(const T* xs, T* __restrict__ g, int rows_live, int tid) {
+  constexpr int VE = 16 / sizeof(T);
+  static_assert(D % VE == 0, "observation rows must be whole 16-byte vectors");
+  constexpr int VPR = D / VE;
+  constexpr int NV = R * VPR;
+#pragma unroll
+  for (int it = 0; it < (NV + NT - 1) / NT; ++it) {
+    const int v = tid + it * NT;
+    const int r = v / VPR, c = (v - r * VPR) * VE;
+    if (v < NV && r < rows_live)
+      *reinterpret_cast<u32x4*>(g + (size_t)r * D + c) = *reinterpret_cast<const u32x4*>(xs + r * LDX + c);
+  }
+}
+
+// Same step as lbf_run_kernel for compile-time policy sizes, restructured for
+// latency:
+//   * layer-1/2 weights live in registers and layer 3 in LDS for the whole
+//     rollout; layers are computed transposed so each lane ends with four
+//     consecutive outputs of one row;
+//   * observations are painted by the env lanes straight into the layer-1
+//     operand tile (only the non-zero features change), and copied to the
+//     trajectory while layer 1 runs;
+//   * the Gumbel noise of NOISE_STEPS steps is drawn in one batch by all
+//     lanes;
+//   * one "env wave" (wave 0) computes layer 3, the Gumbel argmax (in
+//     registers plus one v_permlane16_swap) and steps the TE envs, drawing the
+//     reset blocks of ended episodes on idle lanes in parallel.
+// TE envs per workgroup; the launch bounds let MINB workgroups share a CU.
 template <int DT, int D, int H1, int H2, int NA, int A, int F, int TE, int NW, int MINB>
-__global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p, LbfMagic m, PolicyArgs pol,
-                                                                 int32_t* __restrict__ state, uint64_t t0,
-                                                                 int n_steps, TrajArgs out) {
+__global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p, PolicyArgs pol,
+                                                                    int32_t* __restrict__ state, uint64_t t0,
+                                                                    int n_steps, TrajArgs out) {
   using T = typename DType<DT>::T;
   using B = typename BOperand<DT>::type;
   constexpr int NT = NW * 64;
@@ -417,32 +462,32 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   constexpr int K3 = round_up(H2, DType<DT>::KS) / DType<DT>::KS;
   static_assert(NA <= 8, "one Philox block of action noise per row");
   static_assert(TE <= 64, "env lanes live in wave 0");
+  static_assert(D % 3 == 0, "three observation planes");
+  static_assert(TE * ((2 * A + 2 * F + 7) / 8) <= 64, "one lane per reset block");
 
-  __shared__ __align__(16) uint8_t agrid[TE * LBF_MAXCELLS];
-  __shared__ __align__(16) uint8_t fgrid[TE * LBF_MAXCELLS];
-  __shared__ int acell_s[TE * LBF_MAXA];
-  __shared__ int act_s[RP];
   __shared__ __align__(16) T xs[RP * LDX];
   __shared__ __align__(16) T h1s[RP * LD1];
   __shared__ __align__(16) T h2s[RP * LD2];
   __shared__ __align__(16) B w3s[K3 * 64];
-  __shared__ uint32_t nz[NOISE_STEPS * RP * 8];   // per (step, row): 8 draws, then float noise in place
-  __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];  // reset draws of envs being reset
+  __shared__ int act_s[RP];
+  __shared__ __align__(16) uint32_t nz[NOISE_STEPS * RP * 8];  // per (step, row): 8 draws, then noise in place
+  __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];              // reset draws of envs being reset
 
-  const LbfLds L{agrid, fgrid, acell_s};
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE;
   const int te_valid = min(TE, p.E - e0);
-  const int E = p.E;
+  const int E = p.E, HW = p.HW;
+  constexpr int ew = 0;  // the env wave
+  constexpr int nd = 2 * A + 2 * F;
+  constexpr int nblk = (nd + 7) >> 3;
 
   RegLayer<DT, D, H1, NW> L1;
   RegLayer<DT, H1, H2, NW> L2;
   L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane);
   L2.load(static_cast<const T*>(pol.W[1]), static_cast<const T*>(pol.b[1]), wave, lane);
-  const T* W3 = static_cast<const T*>(pol.W[2]);
   if (tid < 64) {
     const int n = lane & 15;
-    const T* row = W3 + (size_t)(n < NA ? n : 0) * H2;
+    const T* row = static_cast<const T*>(pol.W[2]) + (size_t)(n < NA ? n : 0) * H2;
 #pragma unroll
     for (int ks = 0; ks < K3; ++ks) w3s[ks * 64 + lane] = load_operand_global<DT>(row, H2, ks, lane, n < NA);
   }
@@ -453,27 +498,23 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     b3r[r] = act < NA ? DType<DT>::to_f32(static_cast<const T*>(pol.b[2])[act]) : 0.f;
   }
 
-  // zero the grids and the K padding / unused rows of the operand tiles
-  zero_lds(agrid, sizeof(agrid), tid);
-  zero_lds(fgrid, sizeof(fgrid), tid);
+  // zero the operand tiles (their K padding and unused rows stay zero)
   for (int i = tid; i < RP * LDX; i += NT) xs[i] = (T)0;
   for (int i = tid; i < RP * LD1; i += NT) h1s[i] = (T)0;
   for (int i = tid; i < RP * LD2; i += NT) h2s[i] = (T)0;
   __syncthreads();
-  const bool envlane = tid < te_valid;
-  const int e = e0 + tid;
+  const bool envlane = wave == ew && lane < te_valid;
+  const int e = e0 + lane;
   LbfEnv s{};
   if (envlane) {
     lbf_load<A, F>(state, p, e, s);
-    lbf_paint<A, F>(p, s, tid, L, true);
+    lbf_paint_tile<T, A, F>(s, lane, xs, LDX, HW, true);
   }
-  constexpr int nd = 2 * A + 2 * F;
-  constexpr int nblk = (nd + 7) >> 3;
 
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     const int sn = k % NOISE_STEPS;
-    __syncthreads();  // wave 0 is done with the previous step (grids, noise, actions)
+    __syncthreads();  // the env wave is done with the previous step (tile, noise, actions)
     if (sn == 0) {
       // Gumbel noise of the next NOISE_STEPS steps: one Philox block per (step, row) ...
       const int nb = min(NOISE_STEPS, n_steps - k);
@@ -498,10 +539,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       }
       __syncthreads();
     }
-    lbf_encode_ct<T, TE, A, D, NT>(te_valid, L,
-                                   out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, xs,
-                                   LDX, tid);
-    __syncthreads();
+    if (out.obs) copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D,
+                                                 te_valid * A, tid);
     {
       f32x4 acc[MT][RegLayer<DT, D, H1, NW>::OWN];
       L1.template run<MT>(xs, LDX, acc, wave, lane);
@@ -514,7 +553,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane);
     }
     __syncthreads();
-    if (wave == 0) {
+    if (wave == ew) {
       // Layer 3 transposed, logits^T = W3 h2^T: lane holds row (lane % 16) of
       // the M tile and actions 4 * (lane / 16) + r in accumulator element r.
       // Each lane takes the Gumbel argmax of its four actions; one lane swap
@@ -572,8 +611,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       if (envlane) {
         int act[LBF_MAXA];
 #pragma unroll
-        for (int i = 0; i < LBF_MAXA; ++i) act[i] = i < A ? act_s[tid * A + i] : 0;
-        lbf_paint<A, F>(p, s, tid, L, false);
+        for (int i = 0; i < LBF_MAXA; ++i) act[i] = i < A ? act_s[lane * A + i] : 0;
+        lbf_paint_tile<T, A, F>(s, lane, xs, LDX, HW, false);
         lbf_transition<A, F>(p, s, act, r, d);
       }
       // reset blocks of every env that ended, one Philox block per lane
@@ -590,12 +629,12 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         if (envlane && d) {
           uint32_t dw[LBF_MAX_DRAWS];
 #pragma unroll
-          for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[tid * LBF_MAX_DRAWS + q] : 0u;
+          for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[lane * LBF_MAX_DRAWS + q] : 0u;
           lbf_reset_from_draws<A, F>(p, dw, s);
         }
       }
       if (envlane) {
-        lbf_paint<A, F>(p, s, tid, L, true);
+        lbf_paint_tile<T, A, F>(s, lane, xs, LDX, HW, true);
         if (out.reward) out.reward[(size_t)k * E + e] = r;
         if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
       }
@@ -603,7 +642,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   }
   __syncthreads();
   if (out.obs_last)
-    lbf_encode_ct<T, TE, A, D, NT>(te_valid, L, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, nullptr, 0, tid);
+    copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, te_valid * A, tid);
   if (envlane) lbf_store<A, F>(state, p, e, s);
 }
 
@@ -612,11 +651,11 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
 // 128-wide layers, and LBF 12x12 with 3 agents and 6 foods (obs 432) under
 // 256-wide layers.
 template <int DT, int D, int H1, int H2, int A, int F, int TE, int NW, int MINB>
-static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const PolicyArgs& pol, int32_t* state,
+static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic&, const PolicyArgs& pol, int32_t* state,
                                      uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s) {
   auto kern = lbf_rollout_kernel<DT, D, H1, H2, LBF_NACT, A, F, TE, NW, MINB>;
   const dim3 grid((unsigned)((p.E + TE - 1) / TE));
-  kern<<<grid, NW * 64, 0, s>>>(p, m, pol, state, t0, n_steps, out);
+  kern<<<grid, NW * 64, 0, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
 }
 

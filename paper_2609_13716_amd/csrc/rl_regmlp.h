@@ -74,8 +74,8 @@ struct RegLayer {
   static constexpr int OWN = (NT + NW - 1) / NW;
   static_assert(N % 16 == 0, "layer width must be a multiple of 16");
 
-  B w[OWN][KSTEPS];
-  float bias[OWN];
+  B w[OWN][KSTEPS];   // operand of output units tile*16 + lane%16
+  float bias[OWN][4]; // bias of output units tile*16 + 4*(lane/16) + r
 
   __device__ __forceinline__ void load(const T* __restrict__ W, const T* __restrict__ b, int wave, int lane) {
 #pragma unroll
@@ -86,11 +86,15 @@ struct RegLayer {
       const T* row = W + (size_t)(valid ? n : 0) * K;
 #pragma unroll
       for (int ks = 0; ks < KSTEPS; ++ks) w[o][ks] = load_operand_global<DT>(row, K, ks, lane, valid);
-      bias[o] = valid ? DType<DT>::to_f32(b[n]) : 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) bias[o][r] = valid ? DType<DT>::to_f32(b[tile * 16 + 4 * (lane >> 4) + r]) : 0.f;
     }
   }
 
-  // acc[m][o] = in[m*16 .. m*16+15, :] . W[tile(o) cols]^T over all K steps.
+  // Transposed products, out^T = W in^T: acc[m][o] element r holds output
+  // unit tile(o)*16 + 4*(lane/16) + r of row m*16 + lane%16.  (Each sum is
+  // the same MFMA chain as the untransposed product, so the values are
+  // bit-identical to it.)
   template <int MT>
   __device__ __forceinline__ void run(const T* in, int ld, f32x4 (&acc)[MT][OWN], int wave, int lane) const {
 #pragma unroll
@@ -106,7 +110,7 @@ struct RegLayer {
         for (int m = 0; m < MT; ++m) {
           const B a = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks, lane);
 #pragma unroll
-          for (int o = 0; o < OWN; ++o) acc[m][o] = mfma16<DT>(a, w[o][ks], acc[m][o]);
+          for (int o = 0; o < OWN; ++o) acc[m][o] = mfma16<DT>(w[o][ks], a, acc[m][o]);
         }
       }
     } else {
@@ -117,13 +121,14 @@ struct RegLayer {
           const B a = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks, lane);
 #pragma unroll
           for (int o = 0; o < OWN; ++o)
-            if (wave + o * NW < NT) acc[m][o] = mfma16<DT>(a, w[o][ks], acc[m][o]);
+            if (wave + o * NW < NT) acc[m][o] = mfma16<DT>(w[o][ks], a, acc[m][o]);
         }
       }
     }
   }
 
-  // out = tanh(acc + bias) in the layer dtype, for the wave's tiles.
+  // out = tanh(acc + bias) in the layer dtype: four consecutive units of one
+  // row per lane, stored with one 8-byte (bf16) or 16-byte (f32) LDS write.
   template <int MT>
   __device__ __forceinline__ void store_tanh(const f32x4 (&acc)[MT][OWN], T* out, int ld, int wave, int lane) const {
 #pragma unroll
@@ -131,11 +136,18 @@ struct RegLayer {
 #pragma unroll
       for (int o = 0; o < OWN; ++o) {
         if (NT % NW != 0 && wave + o * NW >= NT) continue;
-        const int col = (wave + o * NW) * 16 + (lane & 15);
+        const int row = m * 16 + (lane & 15);
+        const int col = (wave + o * NW) * 16 + 4 * (lane >> 4);
+        float v[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = m * 16 + 4 * (lane >> 4) + r;
-          out[row * ld + col] = DType<DT>::from_f32(fast_tanh(acc[m][o][r] + bias[o]));
+        for (int r = 0; r < 4; ++r) v[r] = fast_tanh(acc[m][o][r] + bias[o][r]);
+        if constexpr (DT == DT_F32) {
+          *reinterpret_cast<f32x4*>(out + row * ld + col) = f32x4{v[0], v[1], v[2], v[3]};
+        } else {
+          const uint32_t lo = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+          const uint32_t hi = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+          *reinterpret_cast<u32x2*>(out + row * ld + col) = u32x2{lo, hi};
         }
       }
   }
