@@ -36,6 +36,15 @@ __device__ __forceinline__ int lbf_row(const LbfParams& p, int cell) {
   return (int)__umulhi((uint32_t)cell, p.wmagic);
 }
 
+// Grid row of a cell when the width WC is known at compile time (0 = use p).
+template <int WC>
+__device__ __forceinline__ int lbf_row_ct(const LbfParams& p, int cell) {
+  if constexpr (WC > 0)
+    return (int)((uint32_t)cell / (uint32_t)WC);
+  else
+    return lbf_row(p, cell);
+}
+
 struct LbfEnv {
   int acell[LBF_MAXA];
   int alevel[LBF_MAXA];
@@ -194,20 +203,20 @@ __device__ __forceinline__ void lbf_reset(const LbfParams& p, uint64_t env, uint
 // Writes reward and done; `s` becomes the post-transition state (no reset).
 // Written without data-dependent branches: every candidate move and load is
 // evaluated and the outcome selected, so the lanes of a wave never diverge.
-template <int AC = 0, int FC = 0>
+template <int AC = 0, int FC = 0, int HC = 0, int WC = 0>
 __device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, const int (&act_in)[LBF_MAXA],
                                                float& reward, uint32_t& done) {
-  const int A = AC ? AC : p.A, F = FC ? FC : p.F, W = p.W, H = p.H;
+  const int A = AC ? AC : p.A, F = FC ? FC : p.F, W = WC ? WC : p.W, H = HC ? HC : p.H;
   int act[LBF_MAXA], ar[LBF_MAXA], ac[LBF_MAXA], fr[LBF_MAXF], fc[LBF_MAXF];
 #pragma unroll
   for (int i = 0; i < LBF_MAXA; ++i) {
     act[i] = ((unsigned)act_in[i] < (unsigned)LBF_NACT) ? act_in[i] : 0;
-    ar[i] = lbf_row(p, s.acell[i]);
+    ar[i] = lbf_row_ct<WC>(p, s.acell[i]);
     ac[i] = s.acell[i] - ar[i] * W;
   }
 #pragma unroll
   for (int j = 0; j < LBF_MAXF; ++j) {
-    fr[j] = lbf_row(p, s.fcell[j]);
+    fr[j] = lbf_row_ct<WC>(p, s.fcell[j]);
     fc[j] = s.fcell[j] - fr[j] * W;
   }
 

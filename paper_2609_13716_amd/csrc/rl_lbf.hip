@@ -441,28 +441,34 @@ __device__ __forceinline__ void copy_obs_rows(const T* xs, T* __restrict__ g, in
 //     consecutive outputs of one row;
 //   * observations are painted by the env lanes straight into the layer-1
 //     operand tile (only the non-zero features change), and copied to the
-//     trajectory while layer 1 runs;
-//   * the Gumbel noise of NOISE_STEPS steps is drawn in one batch by all
-//     lanes;
+//     trajectory while the layer-2 MFMAs run;
+//   * the Philox action draws of NOISE_STEPS steps are made in one batch by
+//     all lanes; the Gumbel noise of step k+1 is evaluated from them by the
+//     other waves while the env wave steps the envs at step k;
 //   * one "env wave" (wave 0) computes layer 3, the Gumbel argmax (in
 //     registers plus one v_permlane16_swap) and steps the TE envs, drawing the
 //     reset blocks of ended episodes on idle lanes in parallel.
 // TE envs per workgroup; the launch bounds let MINB workgroups share a CU.
-template <int DT, int D, int H1, int H2, int NA, int A, int F, int TE, int NW, int MINB>
+template <int DT, int GH, int GW, int H1, int H2, int NA, int A, int F, int TE, int NW, int MINB>
 __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p, PolicyArgs pol,
                                                                     int32_t* __restrict__ state, uint64_t t0,
                                                                     int n_steps, TrajArgs out) {
   using T = typename DType<DT>::T;
   using B = typename BOperand<DT>::type;
+  constexpr int HW = GH * GW, D = 3 * HW;
   constexpr int NT = NW * 64;
   constexpr int R = TE * A;
   constexpr int MT = (R + 15) / 16;
   constexpr int RP = MT * 16;
+  // With one M tile and A dividing 16, env e lives in lane e * A of wave 0,
+  // which after the argmax already holds its first agent's action; the
+  // others come from the next lanes by DPP row shifts (no LDS round trip).
+  constexpr bool DIRECT = MT == 1 && 16 % A == 0;
+  constexpr int ESTRIDE = DIRECT ? A : 1;  // lane of env e = e * ESTRIDE
   constexpr int LDX = lds_ld<DT>(D), LD1 = lds_ld<DT>(H1), LD2 = lds_ld<DT>(H2);
   constexpr int K3 = round_up(H2, DType<DT>::KS) / DType<DT>::KS;
   static_assert(NA <= 8, "one Philox block of action noise per row");
   static_assert(TE <= 64, "env lanes live in wave 0");
-  static_assert(D % 3 == 0, "three observation planes");
   static_assert(TE * ((2 * A + 2 * F + 7) / 8) <= 64, "one lane per reset block");
 
   __shared__ __align__(16) T xs[RP * LDX];
@@ -470,16 +476,25 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   __shared__ __align__(16) T h2s[RP * LD2];
   __shared__ __align__(16) B w3s[K3 * 64];
   __shared__ int act_s[RP];
-  __shared__ __align__(16) uint32_t nz[NOISE_STEPS * RP * 8];  // per (step, row): 8 draws, then noise in place
-  __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];              // reset draws of envs being reset
+  __shared__ uint32_t words[NOISE_STEPS * RP * 8];  // action Philox draws per (step, row)
+  __shared__ __align__(16) float nz[2][RP * 8];     // Gumbel noise per (row, action), by step parity
+  __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];    // reset draws of envs being reset
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE;
   const int te_valid = min(TE, p.E - e0);
-  const int E = p.E, HW = p.HW;
+  const int E = p.E;
   constexpr int ew = 0;  // the env wave
   constexpr int nd = 2 * A + 2 * F;
   constexpr int nblk = (nd + 7) >> 3;
+  // Gumbel noise of (row, action) items i0, i0 + stride, ... from the Philox
+  // draws of batch slot sn
+  auto draw_noise = [&](int sn, float* noise, int i0, int stride) {
+    for (int i = i0; i < R * NA; i += stride) {
+      const int row = i / NA, a = i - row * NA;
+      noise[row * 8 + a] = gumbel24(words[(sn * RP + row) * 8 + a] >> 8);
+    }
+  };
 
   RegLayer<DT, D, H1, NW> L1;
   RegLayer<DT, H1, H2, NW> L2;
@@ -503,12 +518,13 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   for (int i = tid; i < RP * LD1; i += NT) h1s[i] = (T)0;
   for (int i = tid; i < RP * LD2; i += NT) h2s[i] = (T)0;
   __syncthreads();
-  const bool envlane = wave == ew && lane < te_valid;
-  const int e = e0 + lane;
+  const int el = lane / ESTRIDE;  // env of this lane (when it is an env lane)
+  const bool envlane = wave == ew && lane % ESTRIDE == 0 && el < te_valid;
+  const int e = e0 + el;
   LbfEnv s{};
   if (envlane) {
     lbf_load<A, F>(state, p, e, s);
-    lbf_paint_tile<T, A, F>(s, lane, xs, LDX, HW, true);
+    lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
   }
 
   for (int k = 0; k < n_steps; ++k) {
@@ -516,7 +532,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     const int sn = k % NOISE_STEPS;
     __syncthreads();  // the env wave is done with the previous step (tile, noise, actions)
     if (sn == 0) {
-      // Gumbel noise of the next NOISE_STEPS steps: one Philox block per (step, row) ...
+      // Philox action draws of the next NOISE_STEPS steps, one block (8 draws)
+      // per (step, row), in one pass over all lanes
       const int nb = min(NOISE_STEPS, n_steps - k);
       for (int i = tid; i < nb * R; i += NT) {
         const int st = i / R, row = i - st * R;
@@ -524,23 +541,15 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         if (el < te_valid) {
           const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + el), t + st, (uint64_t)ag * 256u,
                                       TAG_ACTION);
-          uint32_t* d = nz + (st * RP + row) * 8;
+          uint32_t* d = words + (st * RP + row) * 8;
 #pragma unroll
           for (int q = 0; q < 8; ++q) d[q] = block_u32(b, q);
         }
       }
       __syncthreads();
-      // ... then the noise value of every action, in place
-      for (int i = tid; i < nb * R * NA; i += NT) {
-        const int sr = i / NA, a = i - sr * NA;
-        const int st = sr / R, row = sr - st * R;
-        uint32_t* d = nz + (st * RP + row) * 8 + a;
-        *d = __float_as_uint(gumbel24(*d >> 8));
-      }
+      draw_noise(0, nz[k & 1], tid, NT);  // noise of the batch's first step
       __syncthreads();
     }
-    if (out.obs) copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D,
-                                                 te_valid * A, tid);
     {
       f32x4 acc[MT][RegLayer<DT, D, H1, NW>::OWN];
       L1.template run<MT>(xs, LDX, acc, wave, lane);
@@ -550,6 +559,11 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     {
       f32x4 acc[MT][RegLayer<DT, H1, H2, NW>::OWN];
       L2.template run<MT>(h1s, LD1, acc, wave, lane);
+      // o_t to the trajectory while the layer-2 MFMAs run (the tile is only
+      // repainted after layer 3)
+      if (out.obs)
+        copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D, te_valid * A,
+                                        tid);
       L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane);
     }
     __syncthreads();
@@ -559,6 +573,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       // Each lane takes the Gumbel argmax of its four actions; one lane swap
       // with the partner group (actions 0-3 <-> 4-7) finishes the row.
       const int g = lane >> 4;
+      int act_d[LBF_MAXA] = {0, 0, 0, 0};  // DIRECT: this lane's env's actions
       B w3r[K3];
 #pragma unroll
       for (int ks = 0; ks < K3; ++ks) w3r[ks] = w3s[ks * 64 + lane];
@@ -568,7 +583,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         B a3[K3];
 #pragma unroll
         for (int ks = 0; ks < K3; ++ks) a3[ks] = load_operand_lds<DT>(h2s, LD2, row, ks, lane);
-        const f32x4 nz4 = *reinterpret_cast<const f32x4*>(nz + (sn * RP + row) * 8 + 4 * (g & 1));
+        const f32x4 nz4 = *reinterpret_cast<const f32x4*>(&nz[k & 1][row * 8 + 4 * (g & 1)]);
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < K3; ++ks) acc = mfma16<DT>(w3r[ks], a3[ks], acc);
@@ -596,8 +611,14 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         }
         const bool live = row < te_valid * A;
         if (live && g == 0) {
-          act_s[row] = best_a;
+          if constexpr (!DIRECT) act_s[row] = best_a;
           if (out.actions) out.actions[((size_t)k * E + e0) * A + row] = best_a;
+        }
+        if constexpr (DIRECT) {
+          act_d[0] = best_a;
+          if constexpr (A > 1) act_d[1] = __builtin_amdgcn_update_dpp(0, best_a, 0x101, 0xf, 0xf, false);  // row_shl:1
+          if constexpr (A > 2) act_d[2] = __builtin_amdgcn_update_dpp(0, best_a, 0x102, 0xf, 0xf, false);
+          if constexpr (A > 3) act_d[3] = __builtin_amdgcn_update_dpp(0, best_a, 0x103, 0xf, 0xf, false);
         }
         if (out.logits && live && g < 2) {
 #pragma unroll
@@ -605,21 +626,26 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
             if (4 * g + r < NA) out.logits[(((size_t)k * E + e0) * A + row) * NA + 4 * g + r] = logit[r];
         }
       }
-      wave_lds_sync();
+      if constexpr (!DIRECT) wave_lds_sync();
       uint32_t d = 0;
       float r = 0.f;
       if (envlane) {
         int act[LBF_MAXA];
 #pragma unroll
-        for (int i = 0; i < LBF_MAXA; ++i) act[i] = i < A ? act_s[lane * A + i] : 0;
-        lbf_paint_tile<T, A, F>(s, lane, xs, LDX, HW, false);
-        lbf_transition<A, F>(p, s, act, r, d);
+        for (int i = 0; i < LBF_MAXA; ++i) {
+          if constexpr (DIRECT)
+            act[i] = act_d[i];
+          else
+            act[i] = i < A ? act_s[lane * A + i] : 0;
+        }
+        lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, false);
+        lbf_transition<A, F, GH, GW>(p, s, act, r, d);
       }
       // reset blocks of every env that ended, one Philox block per lane
       const uint64_t done_mask = __ballot(envlane && d != 0);
       if (done_mask) {
         const int j = lane / nblk, blk = lane - j * nblk;
-        if (j < TE && ((done_mask >> j) & 1ull)) {
+        if (j < TE && ((done_mask >> (j * ESTRIDE)) & 1ull)) {
           const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + j), t + 1, (uint64_t)blk, TAG_RESET);
 #pragma unroll
           for (int q = 0; q < 8; ++q)
@@ -629,15 +655,19 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         if (envlane && d) {
           uint32_t dw[LBF_MAX_DRAWS];
 #pragma unroll
-          for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[lane * LBF_MAX_DRAWS + q] : 0u;
+          for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[el * LBF_MAX_DRAWS + q] : 0u;
           lbf_reset_from_draws<A, F>(p, dw, s);
         }
       }
       if (envlane) {
-        lbf_paint_tile<T, A, F>(s, lane, xs, LDX, HW, true);
+        lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
         if (out.reward) out.reward[(size_t)k * E + e] = r;
         if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
       }
+    } else if (k + 1 < n_steps && (k + 1) % NOISE_STEPS != 0) {
+      // the other waves: Gumbel noise of the next step, while the env wave steps
+      // (a new batch's first step is drawn with the batch)
+      draw_noise((k + 1) % NOISE_STEPS, nz[(k + 1) & 1], (wave - 1) * 64 + lane, (NW - 1) * 64);
     }
   }
   __syncthreads();
@@ -648,12 +678,11 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
 
 // Compile-time shapes that run on lbf_rollout_kernel (everything else uses
 // lbf_run_kernel): LBF 8x8 with 2 agents and 3 foods (obs 192) under 64- and
-// 128-wide layers, and LBF 12x12 with 3 agents and 6 foods (obs 432) under
-// 256-wide layers.
-template <int DT, int D, int H1, int H2, int A, int F, int TE, int NW, int MINB>
+// 128-wide layers.
+template <int DT, int GH, int GW, int H1, int H2, int A, int F, int TE, int NW, int MINB>
 static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic&, const PolicyArgs& pol, int32_t* state,
                                      uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s) {
-  auto kern = lbf_rollout_kernel<DT, D, H1, H2, LBF_NACT, A, F, TE, NW, MINB>;
+  auto kern = lbf_rollout_kernel<DT, GH, GW, H1, H2, LBF_NACT, A, F, TE, NW, MINB>;
   const dim3 grid((unsigned)((p.E + TE - 1) / TE));
   kern<<<grid, NW * 64, 0, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
@@ -662,16 +691,18 @@ static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic&, const 
 static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const PolicyArgs& pol, int32_t* state,
                                    uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s, hipError_t* err) {
   if (pol.NA != LBF_NACT) return false;
-#define RL_REG_CASE(DTV, DV, H1V, H2V, AV, FV, TEV, NWV, MINBV)                                                   \
-  if (pol.dt == DTV && pol.D == DV && pol.H1 == H1V && pol.H2 == H2V && p.A == AV && p.F == FV) {                 \
-    *err = launch_rollout_reg<DTV, DV, H1V, H2V, AV, FV, TEV, NWV, MINBV>(p, m, pol, state, t0, n_steps, out, s); \
-    return true;                                                                                                  \
+#define RL_REG_CASE(DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV)                                        \
+  if (pol.dt == DTV && p.H == GHV && p.W == GWV && pol.H1 == H1V && pol.H2 == H2V && p.A == AV &&            \
+      p.F == FV) {                                                                                           \
+    *err = launch_rollout_reg<DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV>(p, m, pol, state, t0, n_steps, \
+                                                                                out, s);                     \
+    return true;                                                                                             \
   }
-  // (dtype, obs, hidden, hidden, agents, foods, envs per workgroup, waves, workgroups per CU)
-  RL_REG_CASE(DT_F32, 192, 64, 64, 2, 3, 8, 4, 2)
-  RL_REG_CASE(DT_BF16, 192, 64, 64, 2, 3, 8, 4, 2)
-  RL_REG_CASE(DT_F32, 192, 128, 128, 2, 3, 16, 4, 1)
-  RL_REG_CASE(DT_BF16, 192, 128, 128, 2, 3, 8, 4, 2)
+  // (dtype, grid rows, grid cols, hidden, hidden, agents, foods, envs per workgroup, waves, workgroups per CU)
+  RL_REG_CASE(DT_F32, 8, 8, 64, 64, 2, 3, 8, 4, 2)
+  RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2)
+  RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1)
+  RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2)
 #undef RL_REG_CASE
   return false;
 }
