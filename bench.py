@@ -36,7 +36,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-envs", type=int, default=512, help="envs in the oracle's timed sample")
+    ap.add_argument("--cpu-envs", type=int, default=2048, help="envs in the oracle's timed sample")
     ap.add_argument("--only", choices=["run_bf16", "run_f32", "env_bf16", "policy_bf16"], default=None,
                     help="time one kernel only (for profiler runs)")
     return ap.parse_args()
