@@ -199,9 +199,10 @@ __device__ __forceinline__ void lbf_encode_ct(int te_valid, const LbfLds& L, OT*
   }
 }
 
+template <int NT = NTHREADS>
 __device__ __forceinline__ void lbf_write_legal(const LbfParams& p, int te_valid, uint8_t* __restrict__ g, int tid) {
   const int n = te_valid * p.A * LBF_NACT;
-  for (int i = tid; i < n; i += NTHREADS) g[i] = 1;
+  for (int i = tid; i < n; i += NT) g[i] = 1;
 }
 
 __device__ __forceinline__ void zero_lds(void* base, size_t bytes, int tid) {
@@ -504,7 +505,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     const int n = lane & 15;
     const T* row = static_cast<const T*>(pol.W[2]) + (size_t)(n < NA ? n : 0) * H2;
 #pragma unroll
-    for (int ks = 0; ks < K3; ++ks) w3s[ks * 64 + lane] = load_operand_global<DT>(row, H2, ks, lane, n < NA);
+    for (int ks = 0; ks < K3; ++ks) w3s[ks * 64 + lane] = load_operand_global<DT, H2>(row, H2, ks, lane, n < NA);
   }
   float b3r[4];  // bias of actions 4 * (lane / 16) + r, for the transposed layer 3
 #pragma unroll
@@ -526,6 +527,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     lbf_load<A, F>(state, p, e, s);
     lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
   }
+  // Let the prologue loads land here, once (see lbf_env_kernel).
+  __builtin_amdgcn_s_waitcnt(0);
 
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
@@ -707,6 +710,127 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
   return false;
 }
 
+// ------------------------------------------- env-only steps, one wave ----
+//
+// rollout_step for compile-time LBF shapes: one wave per workgroup owns TE
+// envs (lanes 0..TE-1 keep the env state in registers), paints the
+// observation rows into an LDS tile and copies the tile to the trajectory
+// with 16-byte stores that drain while the next transition runs.  The
+// actions of step k+2 are fetched as soon as step k has used its buffer.
+template <typename OT, int GH, int GW, int A, int F, int TE>
+__global__ __launch_bounds__(64) void lbf_env_kernel(LbfParams p, int32_t* __restrict__ state, uint64_t t0,
+                                                     int n_steps, const int32_t* __restrict__ actions,
+                                                     OT* __restrict__ obs, float* __restrict__ reward,
+                                                     uint8_t* __restrict__ done, uint8_t* __restrict__ legal) {
+  constexpr int HW = GH * GW, D = 3 * HW, R = TE * A;
+  constexpr int nd = 2 * A + 2 * F;
+  constexpr int nblk = (nd + 7) >> 3;
+  static_assert(TE <= 64 && TE * nblk <= 64, "one wave");
+  __shared__ __align__(16) OT xs[R * D];
+  __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];
+
+  const int lane = threadIdx.x;
+  const int e0 = blockIdx.x * TE;
+  const int te_valid = min(TE, p.E - e0);
+  const int E = p.E;
+  const bool envlane = lane < te_valid;
+  const int e = e0 + lane;
+
+  for (int i = lane; i < R * D; i += 64) xs[i] = (OT)0;
+  wave_lds_sync();
+  LbfEnv s{};
+  // Two loop-carried action buffers: the actions of step k+2 are loaded right
+  // after step k used its buffer, so each load has a whole step to land.
+  // (Scalar loads for these were measured slower.)
+  int act0[LBF_MAXA] = {0, 0, 0, 0}, act1[LBF_MAXA] = {0, 0, 0, 0};
+  // The tile's actions of step k are fetched with scalar (uniform-address)
+  // loads, which are counted apart from the vector stores of the trajectory,
+  // so waiting for them never waits for earlier steps' stores to drain; each
+  // env lane then picks its own.
+  auto load_actions = [&](int k, int (&dst)[LBF_MAXA]) {
+    if (envlane && k < n_steps) {
+#pragma unroll
+      for (int i = 0; i < A; ++i) dst[i] = actions[((size_t)k * E + e) * A + i];
+    }
+  };
+
+  if (envlane) {
+    lbf_load<A, F>(state, p, e, s);
+    lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, true);
+  }
+  load_actions(0, act0);
+  load_actions(1, act1);
+  // Let the prologue loads land here, once: otherwise the first in-loop use
+  // of a loaded value gets a full vector-memory wait that executes on every
+  // iteration and so waits for the previous steps' trajectory stores.
+  __builtin_amdgcn_s_waitcnt(0);
+  auto step = [&](int k, const int (&act)[LBF_MAXA]) {
+    const uint64_t t = t0 + (uint64_t)k;
+    uint32_t d = 0;
+    float r = 0.f;
+    if (envlane) {
+      lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, false);
+      lbf_transition<A, F, GH, GW>(p, s, act, r, d);
+    }
+    const uint64_t done_mask = __ballot(envlane && d != 0);
+    if (done_mask) {
+      const int j = lane / nblk, blk = lane - j * nblk;
+      if (j < TE && ((done_mask >> j) & 1ull)) {
+        const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + j), t + 1, (uint64_t)blk, TAG_RESET);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (blk * 8 + q < LBF_MAX_DRAWS) rdraw[j * LBF_MAX_DRAWS + blk * 8 + q] = block_u32(b, q);
+      }
+      wave_lds_sync();
+      if (envlane && d) {
+        uint32_t dw[LBF_MAX_DRAWS];
+#pragma unroll
+        for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[lane * LBF_MAX_DRAWS + q] : 0u;
+        lbf_reset_from_draws<A, F>(p, dw, s);
+      }
+    }
+    if (envlane) {
+      lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, true);
+      if (reward) reward[(size_t)k * E + e] = r;
+      if (done) done[(size_t)k * E + e] = (uint8_t)d;
+    }
+    wave_lds_sync();
+    if (obs) copy_obs_rows<OT, R, D, D, 64>(xs, obs + ((size_t)k * E + e0) * A * D, te_valid * A, lane);
+    if (legal) lbf_write_legal<64>(p, te_valid, legal + ((size_t)k * E + e0) * A * LBF_NACT, lane);
+  };
+  for (int k = 0; k < n_steps; k += 2) {
+    step(k, act0);
+    load_actions(k + 2, act0);
+    if (k + 1 < n_steps) {
+      step(k + 1, act1);
+      load_actions(k + 3, act1);
+    }
+  }
+  if (envlane) lbf_store<A, F>(state, p, e, s);
+}
+
+template <typename OT, int GH, int GW, int A, int F, int TE>
+static hipError_t launch_env_ct(const LbfParams& p, int32_t* state, uint64_t t0, int n_steps,
+                                const int32_t* actions, void* obs, float* reward, uint8_t* done, uint8_t* legal,
+                                hipStream_t s) {
+  lbf_env_kernel<OT, GH, GW, A, F, TE><<<dim3((unsigned)((p.E + TE - 1) / TE)), 64, 0, s>>>(
+      p, state, t0, n_steps, actions, static_cast<OT*>(obs), reward, done, legal);
+  return hipGetLastError();
+}
+
+static bool try_launch_env_ct(const LbfParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,
+                              void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s,
+                              hipError_t* err) {
+  if (p.H == 8 && p.W == 8 && p.A == 2 && p.F == 3) {
+    *err = obs_dt == DT_F32 ? launch_env_ct<float, 8, 8, 2, 3, 8>(p, state, t0, n_steps, actions, obs, reward, done,
+                                                                   legal, s)
+                            : launch_env_ct<uint16_t, 8, 8, 2, 3, 8>(p, state, t0, n_steps, actions, obs, reward,
+                                                                      done, legal, s);
+    return true;
+  }
+  return false;
+}
+
 // ------------------------------------------------------------ launchers ----
 
 static dim3 tiles(int E) { return dim3((unsigned)((E + TILE_E - 1) / TILE_E)); }
@@ -723,6 +847,8 @@ hipError_t launch_lbf_init(const LbfParams& p, int32_t* state, void* obs, int ob
 
 hipError_t launch_lbf_step(const LbfParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,
                            void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s) {
+  hipError_t err;
+  if (try_launch_env_ct(p, state, t0, n_steps, actions, obs, obs_dt, reward, done, legal, s, &err)) return err;
   const LbfMagic m = make_magic(p, LBF_NACT);
   if (obs_dt == DT_F32)
     lbf_step_kernel<float><<<tiles(p.E), NTHREADS, 0, s>>>(p, m, state, t0, n_steps, actions,

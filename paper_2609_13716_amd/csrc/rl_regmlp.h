@@ -35,10 +35,18 @@ __device__ __forceinline__ f32x4 mfma16(const typename BOperand<DT>::type& a, co
 // The B operand (or an A operand read from a row) of one lane for K step ks:
 // f32 lanes hold element ks*4 + lane/16, bf16 lanes hold elements
 // ks*32 + (lane/16)*8 .. +7.  Elements at or beyond K read as zero.
-template <int DT>
+template <int DT, int KC = 0>
 __device__ __forceinline__ typename BOperand<DT>::type load_operand_global(const typename DType<DT>::T* row, int K,
                                                                            int ks, int lane, bool valid) {
-  if constexpr (DT == DT_F32) {
+  if constexpr (KC > 0 && KC % DType<DT>::KS == 0) {
+    // K a multiple of the K step (known at compile time): every element is
+    // in range, one vector load per lane
+    if constexpr (DT == DT_F32) {
+      return valid ? row[ks * 4 + (lane >> 4)] : 0.f;
+    } else {
+      return valid ? *reinterpret_cast<const u32x4*>(row + ks * 32 + (lane >> 4) * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
+  } else if constexpr (DT == DT_F32) {
     const int k = ks * 4 + (lane >> 4);
     return (valid && k < K) ? row[k] : 0.f;
   } else {
@@ -85,7 +93,7 @@ struct RegLayer {
       const int n = tile * 16 + (lane & 15);
       const T* row = W + (size_t)(valid ? n : 0) * K;
 #pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) w[o][ks] = load_operand_global<DT>(row, K, ks, lane, valid);
+      for (int ks = 0; ks < KSTEPS; ++ks) w[o][ks] = load_operand_global<DT, K>(row, K, ks, lane, valid);
 #pragma unroll
       for (int r = 0; r < 4; ++r) bias[o][r] = valid ? DType<DT>::to_f32(b[tile * 16 + 4 * (lane >> 4) + r]) : 0.f;
     }
