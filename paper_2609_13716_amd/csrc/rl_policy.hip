@@ -1,6 +1,7 @@
 // Standalone policy forward (obs -> logits on the MFMA MLP), standalone
 // Gumbel-max sampling from given logits, and the sampler's noise function.
 #include "rl_internal.h"
+#include "rl_regmlp.h"
 #include "rl_sample.h"
 
 namespace rl {
@@ -80,8 +81,157 @@ __global__ __launch_bounds__(NTHREADS) void policy_forward_kernel(PolicyArgs pol
   }
 }
 
+// Persistent policy forward for compile-time sizes: each workgroup keeps the
+// layer-1/2 weights in registers and layer 3 in LDS, and loops over tiles of
+// MT * 16 rows (stage the observation tile with 16-byte loads, three MFMA
+// layers computed transposed, masked logits out).  MINB workgroups share a
+// CU so that one's loads overlap another's matrix work.
+template <int DT, int D, int H1, int H2, int NA, int NW, int MT, int MINB>
+__global__ __launch_bounds__(NW * 64, MINB) void policy_fwd_reg_kernel(PolicyArgs pol, const void* __restrict__ obs_v,
+                                                                       const uint8_t* __restrict__ legal,
+                                                                       int64_t rows, float* __restrict__ logits) {
+  using T = typename DType<DT>::T;
+  using B = typename BOperand<DT>::type;
+  constexpr int NT = NW * 64, BM = MT * 16;
+  constexpr int LDX = lds_ld<DT>(D), LD1 = lds_ld<DT>(H1), LD2 = lds_ld<DT>(H2);
+  constexpr int K3 = round_up(H2, DType<DT>::KS) / DType<DT>::KS;
+  constexpr int VE = 16 / sizeof(T);
+  static_assert(D % VE == 0, "observation rows are whole 16-byte vectors");
+  static_assert(NA <= 16, "one transposed M tile of actions");
+  static_assert(MT <= NW, "one layer-3 M tile per wave");
+  __shared__ __align__(16) T xs[BM * LDX];
+  __shared__ __align__(16) T h1s[BM * LD1];
+  __shared__ __align__(16) T h2s[BM * LD2];
+  __shared__ __align__(16) B w3s[K3 * 64];
+  const T* obs = static_cast<const T*>(obs_v);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  RegLayer<DT, D, H1, NW> L1;
+  RegLayer<DT, H1, H2, NW> L2;
+  L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane);
+  L2.load(static_cast<const T*>(pol.W[1]), static_cast<const T*>(pol.b[1]), wave, lane);
+  if (tid < 64) {
+    const int n = lane & 15;
+    const T* row = static_cast<const T*>(pol.W[2]) + (size_t)(n < NA ? n : 0) * H2;
+#pragma unroll
+    for (int ks = 0; ks < K3; ++ks) w3s[ks * 64 + lane] = load_operand_global<DT, H2>(row, H2, ks, lane, n < NA);
+  }
+  float b3r[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int a = 4 * (lane >> 4) + r;
+    b3r[r] = a < NA ? DType<DT>::to_f32(static_cast<const T*>(pol.b[2])[a]) : 0.f;
+  }
+  for (int i = tid; i < BM * LDX; i += NT) xs[i] = (T)0;
+  for (int i = tid; i < BM * LD1; i += NT) h1s[i] = (T)0;
+  for (int i = tid; i < BM * LD2; i += NT) h2s[i] = (T)0;
+  __syncthreads();
+
+  // Software pipeline over this workgroup's tiles: the observation tile of
+  // the next iteration is loaded into registers while the current one is
+  // computed, and a tile's logits are stored at the start of the next
+  // iteration, after that prefetch is issued, so that waiting for the
+  // prefetch never waits for just-issued stores.
+  const int64_t ntiles = (rows + BM - 1) / BM;
+  constexpr int VPR = D / VE, NV = BM * VPR, IT = (NV + NT - 1) / NT;
+  u32x4 v[IT];
+  auto prefetch = [&](int64_t tile) {
+    const int64_t row0 = tile * BM;
+    const int nrow = tile < ntiles ? (int)min((int64_t)BM, rows - row0) : 0;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int i = tid + it * NT;
+      const int r = i / VPR, c = (i - r * VPR) * VE;
+      v[it] = (i < NV && r < nrow) ? *reinterpret_cast<const u32x4*>(obs + (size_t)(row0 + r) * D + c)
+                                    : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  float lg[4] = {0.f, 0.f, 0.f, 0.f};
+  int64_t lg_row = -1;  // global row of the pending logits (-1: none)
+  auto store_logits = [&]() {
+    if (lg_row >= 0) {
+      const size_t gr = (size_t)lg_row * NA;
+      const int g = lane >> 4;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = 4 * g + r;
+        if (a < NA) {
+          const bool ok = legal == nullptr || legal[gr + a] != 0;
+          logits[gr + a] = ok ? lg[r] : -INFINITY;
+        }
+      }
+    }
+  };
+  prefetch(blockIdx.x);
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t row0 = tile * BM;
+    const int nrow = (int)min((int64_t)BM, rows - row0);
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int i = tid + it * NT;
+      const int r = i / VPR, c = (i - r * VPR) * VE;
+      if (i < NV) *reinterpret_cast<u32x4*>(xs + r * LDX + c) = v[it];
+    }
+    __syncthreads();
+    if (tile + gridDim.x < ntiles) prefetch(tile + gridDim.x);
+    store_logits();
+    lg_row = -1;
+    {
+      f32x4 acc[MT][RegLayer<DT, D, H1, NW>::OWN];
+      L1.template run<MT>(xs, LDX, acc, wave, lane);
+      L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane);
+    }
+    __syncthreads();
+    {
+      f32x4 acc[MT][RegLayer<DT, H1, H2, NW>::OWN];
+      L2.template run<MT>(h1s, LD1, acc, wave, lane);
+      L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane);
+    }
+    __syncthreads();
+    if (wave < MT) {
+      const int row = wave * 16 + (lane & 15);
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < K3; ++ks)
+        acc = mfma16<DT>(w3s[ks * 64 + lane], load_operand_lds<DT>(h2s, LD2, row, ks, lane), acc);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) lg[r] = acc[r] + b3r[r];
+      lg_row = row < nrow ? row0 + row : -1;
+    }
+  }
+  store_logits();
+}
+
+template <int DT, int D, int H1, int H2, int NA, int NW, int MT, int MINB>
+static hipError_t launch_policy_reg(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
+                                    float* logits, hipStream_t s) {
+  constexpr int BM = MT * 16;
+  const int64_t ntiles = (rows + BM - 1) / BM;
+  const unsigned grid = (unsigned)(ntiles < (int64_t)256 * MINB ? ntiles : (int64_t)256 * MINB);
+  policy_fwd_reg_kernel<DT, D, H1, H2, NA, NW, MT, MINB><<<dim3(grid), NW * 64, 0, s>>>(pol, obs, legal, rows, logits);
+  return hipGetLastError();
+}
+
+static bool try_launch_policy_reg(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
+                                  float* logits, hipStream_t s, hipError_t* err) {
+#define RL_PF_CASE(DTV, DV, H1V, H2V, NAV, NWV, MTV, MINBV)                                              \
+  if (pol.dt == DTV && pol.D == DV && pol.H1 == H1V && pol.H2 == H2V && pol.NA == NAV) {                   \
+    *err = launch_policy_reg<DTV, DV, H1V, H2V, NAV, NWV, MTV, MINBV>(pol, obs, legal, rows, logits, s); \
+    return true;                                                                                         \
+  }
+  // (dtype, D, H1, H2, nA, waves, 16-row M tiles per workgroup tile, workgroups per CU)
+  RL_PF_CASE(DT_BF16, 192, 128, 128, 6, 4, 4, 2)
+  RL_PF_CASE(DT_F32, 192, 128, 128, 6, 4, 4, 1)
+  RL_PF_CASE(DT_BF16, 192, 64, 64, 6, 4, 4, 2)
+  RL_PF_CASE(DT_F32, 192, 64, 64, 6, 4, 4, 2)
+#undef RL_PF_CASE
+  return false;
+}
+
 hipError_t launch_policy_forward(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
                                  float* logits, hipStream_t s) {
+  hipError_t err;
+  if (try_launch_policy_reg(pol, obs, legal, rows, logits, s, &err)) return err;
   const PolicyLayout PL = pick_policy_layout(pol);
   const dim3 grid((unsigned)((rows + PL.BM - 1) / PL.BM));
   if (pol.dt == DT_F32) {
