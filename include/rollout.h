@@ -8,8 +8,8 @@
  * shared team reward r(s, a), per-agent observations o_i of s', and a fresh
  * episode from the initial-state distribution rho when one ends.  The
  * environments are those of Section 4 (environment table): Level-Based
- * Foraging (LBF) is implemented; Overcooked and Hanabi kinds are reserved and
- * report RL_EUNSUPPORTED until built.
+ * Foraging (LBF) and an Overcooked-style two-agent kitchen are implemented;
+ * the Hanabi kind is reserved and reports RL_EUNSUPPORTED until built.
  *
  * Conventions for every entry point
  *   - Tensor pointers are DEVICE pointers (gfx950 global memory), owned by the
@@ -62,7 +62,14 @@ enum { RL_F32 = 0, RL_BF16 = 1 };
  * truncated after max_steps steps (>= 1).  Observations have
  * 3 * grid_h * grid_w features per agent; there are 6 actions
  * (0 noop, 1 north, 2 south, 3 west, 4 east, 5 load).  The exact rules are in
- * the LBF section below. */
+ * the LBF section below.
+ *
+ * Overcooked: n_agents == 2, oc_cook_time in 1..255, oc_soup_reward in
+ * 0..2^20, max_steps >= 1; grid_h, grid_w, n_food and the level fields must
+ * be 0.  Observations have 26 * 45 = 1170 features per agent and there are
+ * 6 actions (0 noop, 1 north, 2 south, 3 west, 4 east, 5 interact).  Rules in
+ * the Overcooked section below.
+ * Fields of another kind must be 0 (RL_EINVAL otherwise). */
 typedef struct {
   int32_t kind;            /* RL_ENV_* */
   int32_t n_envs;          /* E >= 1 envs in this batch */
@@ -72,8 +79,8 @@ typedef struct {
   int32_t max_agent_level; /* LBF agent levels are 1..max_agent_level (1..15) */
   int32_t max_food_level;  /* LBF food levels are 1..max_food_level (1..15) */
   int32_t max_steps;       /* episode step limit (truncation) */
-  int32_t oc_cook_time;    /* Overcooked: steps a full pot cooks (reserved, 0 for LBF) */
-  int32_t oc_soup_reward;  /* Overcooked: reward of a served soup (reserved, 0 for LBF) */
+  int32_t oc_cook_time;    /* Overcooked: steps a full pot cooks (0 for LBF) */
+  int32_t oc_soup_reward;  /* Overcooked: reward of a served soup (0 for LBF) */
   int32_t hn_colors, hn_ranks, hn_hand_size, hn_info_tokens, hn_life_tokens; /* Hanabi (reserved) */
   int64_t env_base;        /* global id of env 0 of this batch (>= 0) */
   uint64_t seed;           /* Philox key word 0 */
@@ -203,7 +210,51 @@ rl_status rl_gumbel_noise(const uint32_t* u, int64_t n, float* g, void* stream);
  * max_steps; a done env is reset with the draws of step t + 1.
  * Observation of agent i, 3 planes of grid_h x grid_w (plane-major): agent
  * levels at agent cells, uneaten food levels at food cells, 1 at agent i's
- * own cell.  Every action is always legal. */
+ * own cell.  Every action is always legal.
+ *
+ * ---- Overcooked ----
+ * A kitchen of W x H cells (W in 5..9, H in 4..5) at the top-left of a fixed
+ * 5 x 9 canvas, cell id = row * 9 + col; canvas cells outside the kitchen are
+ * counters.  Cell kinds: floor, counter, onion dispenser, plate dispenser,
+ * pot (one or two), serving cell.  Each env keeps one kitchen for the whole
+ * launch sequence; it is drawn from the stream (seed; env, attempt, k / 8,
+ * TAG_LAYOUT = 3) with 32-bit draws k = 0.. taken as for LBF resets and
+ * u(n) = (draw * n) >> 32: W = 5 + u(5), H = 4 + u(2); u(((H-2)(W-2)) / 4 + 1)
+ * interior counters, each on the u(n)-th remaining interior floor cell
+ * (row-major); n_onion = 1 + u(2), n_pot = 1 + u(2); then n_onion onion
+ * dispensers, n_pot pots, one plate dispenser and one serving cell, each on
+ * the u(n)-th candidate, a border counter that is not a kitchen corner and has
+ * a floor 4-neighbour (row-major).  An attempt is kept iff the floor is
+ * 4-connected with >= 2 cells and no station ran out of candidates; attempts
+ * 0..63 are tried in order, then attempt 64 with no interior counters.
+ * Reset at step t (stream TAG_RESET): agent 0 on the u(n_floor)-th floor
+ * cell, agent 1 on the u(n_floor - 1)-th of the others, both facing north,
+ * empty hands, pots and counters, step count 0.
+ * Step: a move (1..4) turns the agent that way even when blocked, and
+ * succeeds iff the faced cell is floor and held no agent before the step and
+ * the other agent does not move there too.  Then interact (5), agent 0 first,
+ * on the faced cell: take an onion / a plate from a dispenser with an empty
+ * hand; put an onion in a pot with < 3 onions (the third sets the timer to
+ * cook_time); take soup from a pot with 3 onions and timer 0 with a plate
+ * (the pot empties); deliver soup on the serving cell (reward += soup_reward);
+ * place a held item on an empty counter or pick one up with an empty hand.
+ * Pots that were cooking (3 onions, timer > 0) before the step count down by
+ * one.  done = 2 (truncated) when the episode reaches max_steps; a done env
+ * is reset (kitchen kept) with the draws of step t + 1.  Out-of-range actions
+ * act as noop; every action is always legal.
+ * State buffer: 32 int32 planes of E entries (plane p of env e at
+ * state[p * E + e]): 0-17 nine 45-bit cell masks as (low, high) word pairs --
+ * floor, counter, onion dispenser, plate dispenser, pot, serving cell, onion /
+ * plate / soup lying on a counter; 18 W | H << 8; 19-20 agent cells; 21-22
+ * facings (0 N, 1 S, 2 W, 3 E); 23-24 held items (0 none, 1 onion, 2 plate,
+ * 3 soup); 25-26 the pot cells in row-major order (-1: no second pot); 27-28
+ * onions in those pots; 29-30 their timers; 31 steps taken in the episode.
+ * Observation of agent i, 26 planes of 45 canvas cells (plane-major): 0 own
+ * cell, 1 other agent's cell, 2-5 own facing and 6-9 the other's (at the
+ * agent's cell), 10-14 counter / onion / plate / pot / serving cells, 15-17
+ * onion / plate / soup on a counter, 18-20 own held onion / plate / soup and
+ * 21-23 the other's (at the holder's cell), 24 onions in each pot and 25 its
+ * remaining cook timer (at the pot cell). */
 
 #ifdef __cplusplus
 }

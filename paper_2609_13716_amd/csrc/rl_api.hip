@@ -32,14 +32,16 @@ rl_status launched(hipError_t e, const char* what) {
 
 bool valid_dtype(int32_t dt) { return dt == RL_F32 || dt == RL_BF16; }
 
-// Checks cfg and fills the LBF kernel parameters.
-rl_status check_cfg(const rl_env_config* cfg, rl::LbfParams* p) {
-  if (!cfg) return fail(RL_EINVAL, "cfg is NULL");
-  if (cfg->kind == RL_ENV_OVERCOOKED || cfg->kind == RL_ENV_HANABI)
-    return fail(RL_EUNSUPPORTED, "env kind %d is not built in this library", cfg->kind);
-  if (cfg->kind != RL_ENV_LBF) return fail(RL_EINVAL, "unknown env kind %d", cfg->kind);
-  if (cfg->n_envs < 1 || cfg->n_envs > (1 << 26)) return fail(RL_EINVAL, "n_envs %d outside 1..2^26", cfg->n_envs);
-  if (cfg->env_base < 0) return fail(RL_EINVAL, "env_base must be >= 0");
+// A validated env configuration: its kind and the kernel parameters of that kind.
+struct EnvSpec {
+  int kind;
+  rl::LbfParams lbf;
+  rl::OcParams oc;
+  int E, A, D, NA;
+  size_t state_bytes;
+};
+
+rl_status check_lbf(const rl_env_config* cfg, EnvSpec* es) {
   if (cfg->n_agents < 1 || cfg->n_agents > rl::LBF_MAXA)
     return fail(RL_EINVAL, "LBF n_agents %d outside 1..%d", cfg->n_agents, rl::LBF_MAXA);
   if (cfg->n_food < 1 || cfg->n_food > rl::LBF_MAXF)
@@ -53,26 +55,67 @@ rl_status check_cfg(const rl_env_config* cfg, rl::LbfParams* p) {
   if (cfg->n_food + cfg->n_agents > hw) return fail(RL_EINVAL, "LBF grid too small for agents and food");
   if (cfg->max_agent_level < 1 || cfg->max_agent_level > 15 || cfg->max_food_level < 1 || cfg->max_food_level > 15)
     return fail(RL_EINVAL, "LBF levels must be in 1..15");
-  if (cfg->max_steps < 1) return fail(RL_EINVAL, "max_steps must be >= 1");
   if (cfg->oc_cook_time || cfg->oc_soup_reward || cfg->hn_colors || cfg->hn_ranks || cfg->hn_hand_size ||
       cfg->hn_info_tokens || cfg->hn_life_tokens)
     return fail(RL_EINVAL, "Overcooked/Hanabi fields must be 0 for LBF");
-  if (p) {
-    p->E = cfg->n_envs;
-    p->A = cfg->n_agents;
-    p->F = cfg->n_food;
-    p->H = cfg->grid_h;
-    p->W = cfg->grid_w;
-    p->HW = hw;
-    p->D = 3 * hw;
-    p->Lmax = cfg->max_agent_level;
-    p->Fmax = cfg->max_food_level;
-    p->max_steps = cfg->max_steps;
-    p->wmagic = rl::div_magic((uint32_t)cfg->grid_w);
-    p->env_base = cfg->env_base;
-    p->seed = cfg->seed;
-  }
+  rl::LbfParams& p = es->lbf;
+  p.E = cfg->n_envs;
+  p.A = cfg->n_agents;
+  p.F = cfg->n_food;
+  p.H = cfg->grid_h;
+  p.W = cfg->grid_w;
+  p.HW = hw;
+  p.D = 3 * hw;
+  p.Lmax = cfg->max_agent_level;
+  p.Fmax = cfg->max_food_level;
+  p.max_steps = cfg->max_steps;
+  p.wmagic = rl::div_magic((uint32_t)cfg->grid_w);
+  p.env_base = cfg->env_base;
+  p.seed = cfg->seed;
+  es->A = p.A;
+  es->D = p.D;
+  es->NA = rl::LBF_NACT;
+  es->state_bytes = (size_t)rl::lbf_planes(p.A, p.F) * (size_t)p.E * sizeof(int32_t);
   return RL_OK;
+}
+
+rl_status check_overcooked(const rl_env_config* cfg, EnvSpec* es) {
+  if (cfg->n_agents != 2) return fail(RL_EINVAL, "Overcooked has 2 agents, got %d", cfg->n_agents);
+  if (cfg->oc_cook_time < 1 || cfg->oc_cook_time > 255)
+    return fail(RL_EINVAL, "Overcooked cook_time %d outside 1..255", cfg->oc_cook_time);
+  if (cfg->oc_soup_reward < 0 || cfg->oc_soup_reward > (1 << 20))
+    return fail(RL_EINVAL, "Overcooked soup_reward %d outside 0..2^20", cfg->oc_soup_reward);
+  if (cfg->grid_h || cfg->grid_w || cfg->n_food || cfg->max_agent_level || cfg->max_food_level ||
+      cfg->hn_colors || cfg->hn_ranks || cfg->hn_hand_size || cfg->hn_info_tokens || cfg->hn_life_tokens)
+    return fail(RL_EINVAL, "LBF/Hanabi fields must be 0 for Overcooked");
+  rl::OcParams& p = es->oc;
+  p.E = cfg->n_envs;
+  p.cook_time = cfg->oc_cook_time;
+  p.soup_reward = cfg->oc_soup_reward;
+  p.max_steps = cfg->max_steps;
+  p.env_base = cfg->env_base;
+  p.seed = cfg->seed;
+  es->A = 2;
+  es->D = rl::OC_D;
+  es->NA = rl::OC_NACT;
+  es->state_bytes = (size_t)rl::OC_PLANES_STATE * (size_t)p.E * sizeof(int32_t);
+  return RL_OK;
+}
+
+// Checks cfg and fills the kernel parameters of its kind.
+rl_status check_cfg(const rl_env_config* cfg, EnvSpec* es) {
+  EnvSpec local;
+  if (!es) es = &local;
+  if (!cfg) return fail(RL_EINVAL, "cfg is NULL");
+  if (cfg->kind == RL_ENV_HANABI) return fail(RL_EUNSUPPORTED, "env kind %d is not built in this library", cfg->kind);
+  if (cfg->kind != RL_ENV_LBF && cfg->kind != RL_ENV_OVERCOOKED)
+    return fail(RL_EINVAL, "unknown env kind %d", cfg->kind);
+  if (cfg->n_envs < 1 || cfg->n_envs > (1 << 26)) return fail(RL_EINVAL, "n_envs %d outside 1..2^26", cfg->n_envs);
+  if (cfg->env_base < 0) return fail(RL_EINVAL, "env_base must be >= 0");
+  if (cfg->max_steps < 1) return fail(RL_EINVAL, "max_steps must be >= 1");
+  es->kind = cfg->kind;
+  es->E = cfg->n_envs;
+  return cfg->kind == RL_ENV_LBF ? check_lbf(cfg, es) : check_overcooked(cfg, es);
 }
 
 rl_status check_policy(const rl_policy* pol, rl::PolicyArgs* a) {
@@ -105,41 +148,45 @@ rl_status check_policy(const rl_policy* pol, rl::PolicyArgs* a) {
 extern "C" {
 
 size_t rl_state_bytes(const rl_env_config* cfg) {
-  rl::LbfParams p;
-  if (check_cfg(cfg, &p) != RL_OK) return 0;
-  return (size_t)rl::lbf_planes(p.A, p.F) * (size_t)p.E * sizeof(int32_t);
+  EnvSpec es;
+  if (check_cfg(cfg, &es) != RL_OK) return 0;
+  return es.state_bytes;
 }
 
 int32_t rl_obs_dim(const rl_env_config* cfg) {
-  rl::LbfParams p;
-  const rl_status s = check_cfg(cfg, &p);
-  return s != RL_OK ? s : p.D;
+  EnvSpec es;
+  const rl_status s = check_cfg(cfg, &es);
+  return s != RL_OK ? s : es.D;
 }
 
 int32_t rl_num_actions(const rl_env_config* cfg) {
-  const rl_status s = check_cfg(cfg, nullptr);
-  return s != RL_OK ? s : rl::LBF_NACT;
+  EnvSpec es;
+  const rl_status s = check_cfg(cfg, &es);
+  return s != RL_OK ? s : es.NA;
 }
 
 const char* rollout_last_error(void) { return g_err; }
 
 rl_status rollout_init(const rl_env_config* cfg, void* state, void* obs, int32_t obs_dtype, uint8_t* legal,
                        void* stream) {
-  rl::LbfParams p;
-  rl_status s = check_cfg(cfg, &p);
+  EnvSpec es;
+  rl_status s = check_cfg(cfg, &es);
   if (s != RL_OK) return s;
   if (!state) return fail(RL_EINVAL, "state is NULL");
   if (obs && !valid_dtype(obs_dtype)) return fail(RL_EUNSUPPORTED, "obs dtype %d unsupported", obs_dtype);
   const int dt = obs_dtype == RL_F32 ? rl::DT_F32 : rl::DT_BF16;
-  return launched(rl::launch_lbf_init(p, static_cast<int32_t*>(state), obs, dt, legal, (hipStream_t)stream),
+  int32_t* st = static_cast<int32_t*>(state);
+  const hipStream_t hs = (hipStream_t)stream;
+  return launched(es.kind == RL_ENV_LBF ? rl::launch_lbf_init(es.lbf, st, obs, dt, legal, hs)
+                                        : rl::launch_oc_init(es.oc, st, obs, dt, legal, hs),
                   "rollout_init");
 }
 
 rl_status rollout_step(const rl_env_config* cfg, void* state, uint64_t t0, int32_t n_steps, const int32_t* actions,
                        void* obs_out, int32_t obs_dtype, float* reward, uint8_t* done, uint8_t* legal_out,
                        void* stream) {
-  rl::LbfParams p;
-  rl_status s = check_cfg(cfg, &p);
+  EnvSpec es;
+  rl_status s = check_cfg(cfg, &es);
   if (s != RL_OK) return s;
   if (!state) return fail(RL_EINVAL, "state is NULL");
   if (!actions) return fail(RL_EINVAL, "actions is NULL");
@@ -147,8 +194,11 @@ rl_status rollout_step(const rl_env_config* cfg, void* state, uint64_t t0, int32
   if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
   if (obs_out && !valid_dtype(obs_dtype)) return fail(RL_EUNSUPPORTED, "obs dtype %d unsupported", obs_dtype);
   const int dt = obs_dtype == RL_F32 ? rl::DT_F32 : rl::DT_BF16;
-  return launched(rl::launch_lbf_step(p, static_cast<int32_t*>(state), t0, n_steps, actions, obs_out, dt, reward,
-                                      done, legal_out, (hipStream_t)stream),
+  int32_t* st = static_cast<int32_t*>(state);
+  const hipStream_t hs = (hipStream_t)stream;
+  return launched(es.kind == RL_ENV_LBF
+                      ? rl::launch_lbf_step(es.lbf, st, t0, n_steps, actions, obs_out, dt, reward, done, legal_out, hs)
+                      : rl::launch_oc_step(es.oc, st, t0, n_steps, actions, obs_out, dt, reward, done, legal_out, hs),
                   "rollout_step");
 }
 
@@ -166,8 +216,8 @@ rl_status policy_forward(const rl_policy* policy, const void* obs, const uint8_t
 
 rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* state, uint64_t t0, int32_t n_steps,
                       const rl_traj* out, void* stream) {
-  rl::LbfParams p;
-  rl_status s = check_cfg(cfg, &p);
+  EnvSpec es;
+  rl_status s = check_cfg(cfg, &es);
   if (s != RL_OK) return s;
   rl::PolicyArgs a;
   s = check_policy(policy, &a);
@@ -176,23 +226,27 @@ rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* s
   if (!out) return fail(RL_EINVAL, "out is NULL");
   if (n_steps < 1) return fail(RL_EINVAL, "n_steps %d must be >= 1", n_steps);
   if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
-  if (a.D != p.D) return fail(RL_ESHAPE, "policy input size %d != observation size %d", a.D, p.D);
-  if (a.NA != rl::LBF_NACT) return fail(RL_ESHAPE, "policy has %d actions, the env %d", a.NA, rl::LBF_NACT);
-  const rl::RunLayout L = rl::make_run_layout(p.A, p.D, a.H1, a.H2, a.dt);
-  if (L.total > rl::MAX_LDS_BYTES)
-    return fail(RL_EUNSUPPORTED, "rollout tile needs %zu bytes of LDS (max %zu)", L.total, rl::MAX_LDS_BYTES);
+  if (a.D != es.D) return fail(RL_ESHAPE, "policy input size %d != observation size %d", a.D, es.D);
+  if (a.NA != es.NA) return fail(RL_ESHAPE, "policy has %d actions, the env %d", a.NA, es.NA);
+  const size_t lds = es.kind == RL_ENV_LBF ? rl::make_run_layout(es.A, es.D, a.H1, a.H2, a.dt).total
+                                           : rl::oc_run_lds_bytes(a);
+  if (lds > rl::MAX_LDS_BYTES)
+    return fail(RL_EUNSUPPORTED, "rollout tile needs %zu bytes of LDS (max %zu)", lds, rl::MAX_LDS_BYTES);
   const rl::TrajArgs o{out->obs, out->actions, out->logits, out->reward, out->done, out->obs_last};
-  return launched(rl::launch_lbf_run(p, a, static_cast<int32_t*>(state), t0, n_steps, o, (hipStream_t)stream),
+  int32_t* st = static_cast<int32_t*>(state);
+  const hipStream_t hs = (hipStream_t)stream;
+  return launched(es.kind == RL_ENV_LBF ? rl::launch_lbf_run(es.lbf, a, st, t0, n_steps, o, hs)
+                                        : rl::launch_oc_run(es.oc, a, st, t0, n_steps, o, hs),
                   "rollout_run");
 }
 
 rl_status rollout_sample(const rl_env_config* cfg, uint64_t t, const float* logits, const uint8_t* legal,
                          int32_t* actions, void* stream) {
-  rl::LbfParams p;
-  rl_status s = check_cfg(cfg, &p);
+  EnvSpec es;
+  rl_status s = check_cfg(cfg, &es);
   if (s != RL_OK) return s;
   if (!logits || !actions) return fail(RL_EINVAL, "logits or actions is NULL");
-  return launched(rl::launch_sample(p.seed, p.env_base, p.E, p.A, rl::LBF_NACT, t, logits, legal, actions,
+  return launched(rl::launch_sample(cfg->seed, cfg->env_base, es.E, es.A, es.NA, t, logits, legal, actions,
                                     (hipStream_t)stream),
                   "rollout_sample");
 }

@@ -5,6 +5,7 @@
 
 #include "rl_lbf.h"
 #include "rl_mlp.h"
+#include "rl_overcooked.h"
 
 namespace rl {
 
@@ -19,6 +20,19 @@ __host__ __device__ inline uint32_t div_magic(uint32_t d) {
 }
 __device__ __forceinline__ int fdiv(int x, uint32_t magic) {
   return magic ? (int)__umulhi((uint32_t)x, magic) : x;
+}
+
+// Make this wave's earlier LDS writes visible to its later LDS reads.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <int NT = NTHREADS>
+__device__ __forceinline__ void zero_lds(void* base, size_t bytes, int tid) {
+  uint32_t* w = reinterpret_cast<uint32_t*>(base);
+  for (size_t i = tid; i < bytes / 4; i += NT) w[i] = 0u;
 }
 
 struct PolicyArgs {
@@ -78,6 +92,13 @@ hipError_t launch_lbf_step(const LbfParams& p, int32_t* state, uint64_t t0, int 
                            uint8_t* legal, hipStream_t s);
 hipError_t launch_lbf_run(const LbfParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
                           const TrajArgs& out, hipStream_t s);
+
+hipError_t launch_oc_init(const OcParams& p, int32_t* state, void* obs, int obs_dt, uint8_t* legal, hipStream_t s);
+hipError_t launch_oc_step(const OcParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,
+                          void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s);
+size_t oc_run_lds_bytes(const PolicyArgs& pol);
+hipError_t launch_oc_run(const OcParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
+                         const TrajArgs& out, hipStream_t s);
 
 size_t policy_lds_bytes(const PolicyArgs& pol);
 hipError_t launch_policy_forward(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,

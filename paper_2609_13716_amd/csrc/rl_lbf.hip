@@ -54,17 +54,6 @@ __device__ __forceinline__ void lbf_paint(const LbfParams& p, const LbfEnv& s, i
       L.fgrid[el * LBF_MAXCELLS + (s.fcell[j] & CM)] = on ? (uint8_t)s.flevel[j] : 0;
 }
 
-template <typename OT>
-__device__ __forceinline__ OT small_int_to(uint32_t v);
-template <>
-__device__ __forceinline__ float small_int_to<float>(uint32_t v) {
-  return (float)v;
-}
-template <>
-__device__ __forceinline__ uint16_t small_int_to<uint16_t>(uint32_t v) {
-  return (uint16_t)(__float_as_uint((float)v) >> 16);  // exact: small integers are bf16 values
-}
-
 // Observation rows of the tile: element (r, k) with r = el * A + a.
 // gdst: the tile's first element in global [.., A, D] (or null); ldst: LDS
 // operand tile with leading dimension ldl (or null).  Rows of envs beyond
@@ -203,11 +192,6 @@ template <int NT = NTHREADS>
 __device__ __forceinline__ void lbf_write_legal(const LbfParams& p, int te_valid, uint8_t* __restrict__ g, int tid) {
   const int n = te_valid * p.A * LBF_NACT;
   for (int i = tid; i < n; i += NT) g[i] = 1;
-}
-
-__device__ __forceinline__ void zero_lds(void* base, size_t bytes, int tid) {
-  uint32_t* w = reinterpret_cast<uint32_t*>(base);
-  for (size_t i = tid; i < bytes / 4; i += NTHREADS) w[i] = 0u;
 }
 
 // ---------------------------------------------------------------- init ----
@@ -389,12 +373,6 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
 // ------------------------------------ fused rollout, weights in registers ----
 
 constexpr int NOISE_STEPS = 16;
-
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
 
 // Write (on) or erase (!on) env el's non-zero observation features directly
 // in the MFMA operand tile: for each of its A rows, plane 0 holds every

@@ -48,6 +48,19 @@ struct DType<DT_BF16> {
 
 __host__ __device__ constexpr int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
+// A small non-negative integer (an observation feature) in a layer dtype;
+// exact in bf16 up to 256.
+template <typename OT>
+__device__ __forceinline__ OT small_int_to(uint32_t v);
+template <>
+__device__ __forceinline__ float small_int_to<float>(uint32_t v) {
+  return (float)v;
+}
+template <>
+__device__ __forceinline__ uint16_t small_int_to<uint16_t>(uint32_t v) {
+  return (uint16_t)(__float_as_uint((float)v) >> 16);
+}
+
 // tanh(x) = 1 - 2 / (exp(2x) + 1) with the hardware exp2 and reciprocal
 // (v_exp_f32, v_rcp_f32).  Absolute error is a few 1e-7; +-inf and large
 // |x| give +-1 exactly, NaN stays NaN.

@@ -1,0 +1,329 @@
+// Overcooked-style kitchen kernels: init (layout + first episode), env-only
+// steps with injected actions, and the fused rollout.
+//
+// Each workgroup owns OC_TE envs; env lane e keeps its kitchen in registers
+// (cell sets as 45-bit masks).  Observations live in an LDS tile of
+// 2 * OC_TE rows x 1170 features: the layout planes are painted once (the
+// kitchen never changes), and each step the env lanes erase and repaint only
+// the features that can change (agents, facings, held items, pots, and the
+// counters whose item changed); the tile is then copied to the trajectory.
+// The fused rollout runs the policy with the streaming MFMA MLP of rl_mlp.h
+// (weights read from L2 every step) and samples one action per (row, action)
+// lane.
+#include "rl_internal.h"
+#include "rl_overcooked.h"
+#include "rl_sample.h"
+
+namespace rl {
+
+constexpr int OC_TE = 8;  // envs per workgroup
+
+template <typename T>
+__device__ __forceinline__ void oc_put(T* xr, int plane, int cell, uint32_t v) {
+  xr[plane * OC_NCELL + cell] = small_int_to<T>(v);
+}
+
+// Layout planes 10-14 of both rows of env el (never change during a launch).
+template <typename T>
+__device__ __forceinline__ void oc_paint_static(const OcEnv& s, T* tile, int ld, int el) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    T* xr = tile + (size_t)(el * 2 + i) * ld;
+    const uint64_t kinds[5] = {s.counter, s.onion, s.plate, s.pot, s.serve};
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      uint64_t m = kinds[k];
+      while (m) {
+        oc_put(xr, 10 + k, __builtin_ctzll(m), 1u);
+        m &= m - 1;
+      }
+    }
+  }
+}
+
+// Agent, facing, held and pot features of both rows (on: write, else erase).
+template <typename T>
+__device__ __forceinline__ void oc_paint_agents(const OcEnv& s, T* tile, int ld, int el, bool on) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    T* xr = tile + (size_t)(el * 2 + i) * ld;
+    const int me = i, ot = 1 - i;
+    const uint32_t one = on ? 1u : 0u;
+    oc_put(xr, 0, s.acell[me], one);
+    oc_put(xr, 1, s.acell[ot], one);
+    oc_put(xr, 2 + (s.face[me] & 3), s.acell[me], one);
+    oc_put(xr, 6 + (s.face[ot] & 3), s.acell[ot], one);
+    if (s.held[me]) oc_put(xr, 17 + (s.held[me] & 3), s.acell[me], one);
+    if (s.held[ot]) oc_put(xr, 20 + (s.held[ot] & 3), s.acell[ot], one);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      if (s.pcell[j] >= 0) {
+        oc_put(xr, 24, s.pcell[j], on ? (uint32_t)s.pon[j] : 0u);
+        oc_put(xr, 25, s.pcell[j], on ? (uint32_t)s.ptm[j] : 0u);
+      }
+  }
+}
+
+// Item features (planes 15-17) at the counters in `cells`: erase all three,
+// then write the item currently there.
+template <typename T>
+__device__ __forceinline__ void oc_paint_items(const OcEnv& s, T* tile, int ld, int el, uint64_t cells) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    T* xr = tile + (size_t)(el * 2 + i) * ld;
+    uint64_t m = cells;
+    while (m) {
+      const int c = __builtin_ctzll(m);
+      m &= m - 1;
+      oc_put(xr, 15, c, 0u);
+      oc_put(xr, 16, c, 0u);
+      oc_put(xr, 17, c, 0u);
+      const int it = oc_item_at(s, c);
+      if (it) oc_put(xr, 14 + it, c, 1u);
+    }
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void oc_paint_all(const OcEnv& s, T* tile, int ld, int el) {
+  oc_paint_static(s, tile, ld, el);
+  oc_paint_agents(s, tile, ld, el, true);
+  oc_paint_items(s, tile, ld, el, s.it_onion | s.it_plate | s.it_soup);
+}
+
+// One env step of env lane el (tile rows el*2, el*2+1 kept in sync).
+template <typename T>
+__device__ __forceinline__ void oc_step_lane(const OcParams& p, OcEnv& s, int el, uint64_t genv, uint64_t t,
+                                             const int (&act)[2], T* tile, int ld, float& r, uint32_t& d) {
+  oc_paint_agents(s, tile, ld, el, false);
+  uint64_t changed;
+  oc_transition(p, s, act, r, d, changed);
+  if (d) {
+    const uint64_t had = s.it_onion | s.it_plate | s.it_soup;
+    oc_reset(p, genv, t + 1, s);
+    oc_paint_items(s, tile, ld, el, had | changed);
+  } else {
+    oc_paint_items(s, tile, ld, el, changed);
+  }
+  oc_paint_agents(s, tile, ld, el, true);
+}
+
+// Copy n elements from LDS (16-byte aligned) to global (4-byte aligned):
+// 16-byte stores when the destination allows, 4-byte words otherwise.
+template <typename T>
+__device__ __forceinline__ void copy_tile(const T* src, T* __restrict__ dst, int n, int tid, int nt) {
+  const int nbytes = n * (int)sizeof(T);
+  int done_words = 0;
+  if ((reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+    const u32x4* s4 = reinterpret_cast<const u32x4*>(src);
+    u32x4* g4 = reinterpret_cast<u32x4*>(dst);
+    const int nq = nbytes >> 4;
+    for (int i = tid; i < nq; i += nt) g4[i] = s4[i];
+    done_words = nq * 4;
+  }
+  const uint32_t* s = reinterpret_cast<const uint32_t*>(src);
+  uint32_t* g = reinterpret_cast<uint32_t*>(dst);
+  for (int i = done_words + tid; i < (nbytes >> 2); i += nt) g[i] = s[i];
+}
+
+// -------------------------------------------------------------- init ----
+
+template <typename OT>
+__global__ __launch_bounds__(64) void oc_init_kernel(OcParams p, int32_t* __restrict__ state, OT* __restrict__ obs,
+                                                     uint8_t* __restrict__ legal) {
+  __shared__ __align__(16) OT tile[OC_TE * 2 * OC_D];
+  const int lane = threadIdx.x, e0 = blockIdx.x * OC_TE, te_valid = min(OC_TE, p.E - e0);
+  zero_lds<64>(tile, sizeof(tile), lane);
+  wave_lds_sync();
+  if (lane < te_valid) {
+    OcEnv s;
+    const uint64_t genv = (uint64_t)(p.env_base + e0 + lane);
+    oc_layout(p, genv, s);
+    oc_reset(p, genv, 0, s);
+    oc_store(state, p.E, e0 + lane, s);
+    oc_paint_all(s, tile, OC_D, lane);
+  }
+  wave_lds_sync();
+  if (obs) copy_tile(tile, obs + (size_t)e0 * 2 * OC_D, te_valid * 2 * OC_D, lane, 64);
+  if (legal)
+    for (int i = lane; i < te_valid * 2 * OC_NACT; i += 64) legal[(size_t)e0 * 2 * OC_NACT + i] = 1;
+}
+
+// ---------------------------------------------------------- env-only ----
+
+template <typename OT>
+__global__ __launch_bounds__(64) void oc_env_kernel(OcParams p, int32_t* __restrict__ state, uint64_t t0, int n_steps,
+                                                    const int32_t* __restrict__ actions, OT* __restrict__ obs,
+                                                    float* __restrict__ reward, uint8_t* __restrict__ done,
+                                                    uint8_t* __restrict__ legal) {
+  __shared__ __align__(16) OT tile[OC_TE * 2 * OC_D];
+  const int lane = threadIdx.x, e0 = blockIdx.x * OC_TE, te_valid = min(OC_TE, p.E - e0);
+  const int E = p.E;
+  const bool envlane = lane < te_valid;
+  const int e = e0 + lane;
+  zero_lds<64>(tile, sizeof(tile), lane);
+  wave_lds_sync();
+  OcEnv s;
+  if (envlane) {
+    oc_load(state, E, e, s);
+    oc_paint_all(s, tile, OC_D, lane);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  for (int k = 0; k < n_steps; ++k) {
+    const uint64_t t = t0 + (uint64_t)k;
+    if (envlane) {
+      const int act[2] = {actions[((size_t)k * E + e) * 2], actions[((size_t)k * E + e) * 2 + 1]};
+      float r;
+      uint32_t d;
+      oc_step_lane(p, s, lane, (uint64_t)(p.env_base + e), t, act, tile, OC_D, r, d);
+      if (reward) reward[(size_t)k * E + e] = r;
+      if (done) done[(size_t)k * E + e] = (uint8_t)d;
+    }
+    wave_lds_sync();
+    if (obs) copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * OC_D, te_valid * 2 * OC_D, lane, 64);
+    if (legal)
+      for (int i = lane; i < te_valid * 2 * OC_NACT; i += 64) legal[((size_t)k * E + e0) * 2 * OC_NACT + i] = 1;
+    wave_lds_sync();
+  }
+  if (envlane) oc_store(state, E, e, s);
+}
+
+// ----------------------------------------------------- fused rollout ----
+
+template <int DT>
+__global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs pol, int32_t* __restrict__ state,
+                                                          uint64_t t0, int n_steps, TrajArgs out) {
+  using T = typename DType<DT>::T;
+  constexpr int R = OC_TE * 2, NA = OC_NACT;
+  constexpr int LDX = lds_ld<DT>(OC_D);
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int ld1 = lds_ld<DT>(pol.H1), ld2 = lds_ld<DT>(pol.H2);
+  T* xs = reinterpret_cast<T*>(smem);
+  T* h1 = xs + R * LDX;
+  T* h2 = h1 + R * ld1;
+  float* lg = reinterpret_cast<float*>(h2 + R * ld2);
+  float* sc = lg + R * MAX_NA;
+  int* act_s = reinterpret_cast<int*>(sc + R * MAX_NA);
+  const size_t total = (size_t)((uint8_t*)(act_s + R) - smem);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int e0 = blockIdx.x * OC_TE, te_valid = min(OC_TE, p.E - e0), E = p.E;
+  const T* W1 = static_cast<const T*>(pol.W[0]);
+  const T* W2 = static_cast<const T*>(pol.W[1]);
+  const T* W3 = static_cast<const T*>(pol.W[2]);
+  const T* b1 = static_cast<const T*>(pol.b[0]);
+  const T* b2 = static_cast<const T*>(pol.b[1]);
+  const T* b3 = static_cast<const T*>(pol.b[2]);
+  zero_lds(smem, total, tid);
+  __syncthreads();
+  const bool envlane = tid < te_valid;
+  const int e = e0 + tid;
+  OcEnv s;
+  if (envlane) {
+    oc_load(state, E, e, s);
+    oc_paint_all(s, xs, LDX, tid);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  for (int k = 0; k < n_steps; ++k) {
+    const uint64_t t = t0 + (uint64_t)k;
+    __syncthreads();  // the env lanes' repaint of the previous step is visible
+    if (out.obs) {
+      T* g = static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D;
+      for (int r = 0; r < te_valid * 2; ++r) copy_tile(xs + r * LDX, g + (size_t)r * OC_D, OC_D, tid, NTHREADS);
+    }
+    mlp_hidden<DT>(xs, LDX, R, OC_D, W1, b1, pol.H1, h1, ld1, wave, NTHREADS / 64, lane);
+    __syncthreads();
+    mlp_hidden<DT>(h1, ld1, R, pol.H1, W2, b2, pol.H2, h2, ld2, wave, NTHREADS / 64, lane);
+    __syncthreads();
+    mlp_logits<DT>(h2, ld2, R, pol.H2, W3, b3, NA, lg, MAX_NA, wave, NTHREADS / 64, lane);
+    __syncthreads();
+    for (int idx = tid; idx < R * NA; idx += NTHREADS) {
+      const int r = idx / NA, a = idx - r * NA, el = r >> 1, ag = r & 1;
+      if (el < te_valid) {
+        const float g = action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t, ag, a);
+        sc[r * MAX_NA + a] = action_score(lg[r * MAX_NA + a], g, true);
+        if (out.logits) out.logits[((size_t)k * E + e0) * 2 * NA + idx] = lg[r * MAX_NA + a];
+      }
+    }
+    __syncthreads();
+    if (tid < R && (tid >> 1) < te_valid) {
+      int best = 0;
+      float bs = -INFINITY;
+      for (int a = 0; a < NA; ++a) {
+        const float v = sc[tid * MAX_NA + a];
+        if (v > bs) {
+          bs = v;
+          best = a;
+        }
+      }
+      act_s[tid] = best;
+      if (out.actions) out.actions[((size_t)k * E + e0) * 2 + tid] = best;
+    }
+    __syncthreads();
+    if (envlane) {
+      const int act[2] = {act_s[tid * 2], act_s[tid * 2 + 1]};
+      float r;
+      uint32_t d;
+      oc_step_lane(p, s, tid, (uint64_t)(p.env_base + e), t, act, xs, LDX, r, d);
+      if (out.reward) out.reward[(size_t)k * E + e] = r;
+      if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
+    }
+  }
+  __syncthreads();
+  if (out.obs_last) {
+    T* g = static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * OC_D;
+    for (int r = 0; r < te_valid * 2; ++r) copy_tile(xs + r * LDX, g + (size_t)r * OC_D, OC_D, tid, NTHREADS);
+  }
+  if (envlane) oc_store(state, E, e, s);
+}
+
+// ---------------------------------------------------------- launchers ----
+
+static dim3 oc_tiles(int E) { return dim3((unsigned)((E + OC_TE - 1) / OC_TE)); }
+
+size_t oc_run_lds_bytes(const PolicyArgs& pol) {
+  constexpr int R = OC_TE * 2;
+  const size_t es = pol.dt == DT_F32 ? 4 : 2;
+  const int ldx = pol.dt == DT_F32 ? lds_ld<DT_F32>(OC_D) : lds_ld<DT_BF16>(OC_D);
+  const int ld1 = pol.dt == DT_F32 ? lds_ld<DT_F32>(pol.H1) : lds_ld<DT_BF16>(pol.H1);
+  const int ld2 = pol.dt == DT_F32 ? lds_ld<DT_F32>(pol.H2) : lds_ld<DT_BF16>(pol.H2);
+  return (size_t)R * (ldx + ld1 + ld2) * es + (size_t)R * MAX_NA * 4 * 2 + (size_t)R * 4;
+}
+
+hipError_t launch_oc_init(const OcParams& p, int32_t* state, void* obs, int obs_dt, uint8_t* legal, hipStream_t s) {
+  if (obs_dt == DT_F32)
+    oc_init_kernel<float><<<oc_tiles(p.E), 64, 0, s>>>(p, state, static_cast<float*>(obs), legal);
+  else
+    oc_init_kernel<uint16_t><<<oc_tiles(p.E), 64, 0, s>>>(p, state, static_cast<uint16_t*>(obs), legal);
+  return hipGetLastError();
+}
+
+hipError_t launch_oc_step(const OcParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,
+                          void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s) {
+  if (obs_dt == DT_F32)
+    oc_env_kernel<float><<<oc_tiles(p.E), 64, 0, s>>>(p, state, t0, n_steps, actions, static_cast<float*>(obs), reward,
+                                                      done, legal);
+  else
+    oc_env_kernel<uint16_t><<<oc_tiles(p.E), 64, 0, s>>>(p, state, t0, n_steps, actions, static_cast<uint16_t*>(obs),
+                                                         reward, done, legal);
+  return hipGetLastError();
+}
+
+hipError_t launch_oc_run(const OcParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
+                         const TrajArgs& out, hipStream_t s) {
+  const size_t lds = oc_run_lds_bytes(pol);
+  if (pol.dt == DT_F32) {
+    hipError_t e = hipFuncSetAttribute((const void*)oc_run_kernel<DT_F32>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)MAX_LDS_BYTES);
+    if (e != hipSuccess) return e;
+    oc_run_kernel<DT_F32><<<oc_tiles(p.E), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
+  } else {
+    hipError_t e = hipFuncSetAttribute((const void*)oc_run_kernel<DT_BF16>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)MAX_LDS_BYTES);
+    if (e != hipSuccess) return e;
+    oc_run_kernel<DT_BF16><<<oc_tiles(p.E), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace rl

@@ -92,7 +92,11 @@ def _check(status):
 
 @dataclass
 class EnvConfig:
-    """Mirror of ``rl_env_config`` (defaults: LBF 8x8, 2 agents, 3 foods)."""
+    """Mirror of ``rl_env_config`` (defaults: LBF 8x8, 2 agents, 3 foods).
+
+    Only the fields of ``kind`` are passed to the library (the LBF grid
+    fields are sent as 0 for other kinds); ``extra`` holds the Overcooked /
+    Hanabi fields by their C names."""
     n_envs: int
     kind: int = RL_ENV_LBF
     n_agents: int = 2
@@ -108,12 +112,20 @@ class EnvConfig:
 
     def c(self):
         s = _EnvConfig()
-        for k in ("kind", "n_envs", "n_agents", "grid_h", "grid_w", "n_food", "max_agent_level",
-                  "max_food_level", "max_steps", "env_base", "seed"):
+        names = ("kind", "n_envs", "n_agents", "max_steps", "env_base", "seed")
+        if self.kind == RL_ENV_LBF:
+            names += ("grid_h", "grid_w", "n_food", "max_agent_level", "max_food_level")
+        for k in names:
             setattr(s, k, getattr(self, k))
         for k, v in self.extra.items():
             setattr(s, k, v)
         return s
+
+
+def overcooked_config(n_envs, cook_time=20, soup_reward=20, max_steps=400, env_base=0, seed=0):
+    """An ``EnvConfig`` for the two-agent Overcooked-style kitchen."""
+    return EnvConfig(n_envs, kind=RL_ENV_OVERCOOKED, n_agents=2, max_steps=max_steps, env_base=env_base, seed=seed,
+                     extra={"oc_cook_time": cook_time, "oc_soup_reward": soup_reward})
 
 
 def _ptr(t):
@@ -286,4 +298,44 @@ def lbf_pack_state(cfg, planes, device="cuda"):
     v = lbf_state_planes(cfg, buf)
     for k in LBF_FIELDS:
         v[k].copy_(torch.as_tensor(planes[k], dtype=torch.int32).reshape(v[k].shape))
+    return buf.reshape(-1).to(device)
+
+
+# ---- Overcooked state layout (see the Overcooked section of include/rollout.h) ----
+
+OC_MASKS = ("floor", "counter", "onion", "plate", "pot", "serve", "item_onion", "item_plate", "item_soup")
+OC_N_PLANES = 32
+
+
+def oc_state_planes(cfg, state):
+    """Split an Overcooked state buffer into named planes: 45-bit cell masks as
+    int64 [E] (from their lo/hi words), and int32 [E] / [2, E] fields."""
+    E = cfg.n_envs
+    p = state.reshape(OC_N_PLANES, E)
+    out = {}
+    for i, k in enumerate(OC_MASKS):
+        lo = p[2 * i].to(torch.int64) & 0xFFFFFFFF
+        hi = p[2 * i + 1].to(torch.int64) & 0xFFFFFFFF
+        out[k] = lo | (hi << 32)
+    out["W"] = p[18] & 0xFF
+    out["H"] = (p[18] >> 8) & 0xFF
+    out["agent_cell"], out["facing"], out["held"] = p[19:21], p[21:23], p[23:25]
+    out["pot_cell"], out["pot_onions"], out["pot_timer"] = p[25:27], p[27:29], p[29:31]
+    out["steps"] = p[31]
+    return out
+
+
+def oc_pack_state(cfg, planes, device="cuda"):
+    """Inverse of oc_state_planes: a state buffer from named planes."""
+    E = cfg.n_envs
+    buf = torch.empty(OC_N_PLANES, E, dtype=torch.int32)
+    for i, k in enumerate(OC_MASKS):
+        m = torch.as_tensor(planes[k], dtype=torch.int64).reshape(E)
+        buf[2 * i] = (((m & 0xFFFFFFFF) ^ 0x80000000) - 0x80000000).to(torch.int32)  # low word as signed int32
+        buf[2 * i + 1] = (m >> 32).to(torch.int32)
+    buf[18] = (torch.as_tensor(planes["W"]) | (torch.as_tensor(planes["H"]) << 8)).to(torch.int32).reshape(E)
+    for lo, k in ((19, "agent_cell"), (21, "facing"), (23, "held"), (25, "pot_cell"), (27, "pot_onions"),
+                  (29, "pot_timer")):
+        buf[lo:lo + 2] = torch.as_tensor(planes[k], dtype=torch.int32).reshape(2, E)
+    buf[31] = torch.as_tensor(planes["steps"], dtype=torch.int32).reshape(E)
     return buf.reshape(-1).to(device)

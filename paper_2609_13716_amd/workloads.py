@@ -14,6 +14,11 @@ in include/rollout.h):
     lbf12_16k    12x12, 3 agents, 6 foods, levels 1..3 / 1..6, 16384 envs x 256 steps,
                  MLP 432-256-256-6 bf16
 All LBF episodes are truncated after 50 steps.
+
+Overcooked-style kitchen (two agents; seeded random kitchens of 5x4 to 9x5,
+rules and observation as documented in include/rollout.h):
+    oc_4096      4096 envs x 400 steps, cook time 20, soup reward 20, episodes of
+                 400 steps, MLP 1170-256-256-6 bf16
 """
 
 import numpy as np
@@ -28,17 +33,27 @@ WORKLOADS = {
     "lbf12_16k": dict(env=dict(grid_h=12, grid_w=12, n_agents=3, n_food=6, max_agent_level=3, max_food_level=6,
                                max_steps=50),
                       n_envs=16384, n_steps=256, hidden=(256, 256), dtypes=("bf16",)),
+    "oc_4096": dict(kind="overcooked", env=dict(cook_time=20, soup_reward=20, max_steps=400),
+                    n_envs=4096, n_steps=400, hidden=(256, 256), dtypes=("bf16",)),
 }
 
 LBF_ACTIONS = 6
+OC_ACTIONS = 6
+OC_OBS_DIM = 26 * 45
 
 
 def lbf_obs_dim(env):
     return 3 * env["grid_h"] * env["grid_w"]
 
 
+def kind(name):
+    return WORKLOADS[name].get("kind", "lbf")
+
+
 def policy_dims(name):
     w = WORKLOADS[name]
+    if kind(name) == "overcooked":
+        return (OC_OBS_DIM, *w["hidden"], OC_ACTIONS)
     return (lbf_obs_dim(w["env"]), *w["hidden"], LBF_ACTIONS)
 
 

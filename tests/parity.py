@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import lbf, sampling
+from oracle import lbf, overcooked, sampling
 
 
 def require_gpu():
@@ -44,6 +44,86 @@ def states_to_device(cfg, states):
         "den": np.array([s.den for s in states]),
     }
     return R.lbf_pack_state(cfg, planes)
+
+
+def oc_oracle_cfg(cfg):
+    return overcooked.Config(cfg.extra["oc_cook_time"], cfg.extra["oc_soup_reward"], cfg.max_steps, 2)
+
+
+_OC_KIND_OF_MASK = (("counter", overcooked.COUNTER), ("onion", overcooked.ONION), ("plate", overcooked.PLATE),
+                    ("pot", overcooked.POT), ("serve", overcooked.SERVE))
+_OC_ITEM_OF_MASK = (("item_onion", overcooked.HELD_ONION), ("item_plate", overcooked.HELD_PLATE),
+                    ("item_soup", overcooked.HELD_SOUP))
+
+
+def oc_states_from_device(cfg, state):
+    """Oracle Overcooked State objects from a device (or host) state buffer.
+
+    Checks on the way that the cell masks partition the canvas and that the
+    pot slots list the POT cells in row-major order."""
+    from paper_2609_13716_amd import rollout as R
+    v = {k: t.cpu().numpy() for k, t in R.oc_state_planes(cfg, state.cpu()).items()}
+    out = []
+    full = (1 << overcooked.NCELL) - 1
+    for e in range(cfg.n_envs):
+        masks = {k: int(v[k][e]) for k in R.OC_MASKS}
+        union = masks["floor"]
+        for k, _ in _OC_KIND_OF_MASK:
+            assert union & masks[k] == 0, f"env {e}: cell masks overlap"
+            union |= masks[k]
+        assert union == full, f"env {e}: cell masks do not cover the canvas"
+        cells = [overcooked.FLOOR] * overcooked.NCELL
+        items = [0] * overcooked.NCELL
+        for c in range(overcooked.NCELL):
+            for k, kind in _OC_KIND_OF_MASK:
+                if (masks[k] >> c) & 1:
+                    cells[c] = kind
+            for k, it in _OC_ITEM_OF_MASK:
+                if (masks[k] >> c) & 1:
+                    assert items[c] == 0 and cells[c] == overcooked.COUNTER, f"env {e}: bad item at {c}"
+                    items[c] = it
+        pots = [c for c in range(overcooked.NCELL) if cells[c] == overcooked.POT]
+        slots = [int(x) for x in v["pot_cell"][:, e]]
+        assert slots == (pots + [-1, -1])[:2], f"env {e}: pot slots {slots} vs pots {pots}"
+        out.append(overcooked.State(
+            int(v["W"][e]), int(v["H"][e]), cells, items, [int(x) for x in v["agent_cell"][:, e]],
+            [int(x) for x in v["facing"][:, e]], [int(x) for x in v["held"][:, e]],
+            {c: int(v["pot_onions"][j, e]) for j, c in enumerate(pots)},
+            {c: int(v["pot_timer"][j, e]) for j, c in enumerate(pots)}, int(v["steps"][e])))
+    return out
+
+
+def oc_states_to_device(cfg, states, device="cuda"):
+    from paper_2609_13716_amd import rollout as R
+    planes = {k: [] for k in R.OC_MASKS}
+    for k in ("W", "H", "steps"):
+        planes[k] = []
+    for k in ("agent_cell", "facing", "held", "pot_cell", "pot_onions", "pot_timer"):
+        planes[k] = [[], []]
+    for s in states:
+        planes["floor"].append(sum(1 << c for c in range(overcooked.NCELL) if s.cells[c] == overcooked.FLOOR))
+        for k, kind in _OC_KIND_OF_MASK:
+            planes[k].append(sum(1 << c for c in range(overcooked.NCELL) if s.cells[c] == kind))
+        for k, it in _OC_ITEM_OF_MASK:
+            planes[k].append(sum(1 << c for c in range(overcooked.NCELL) if s.items[c] == it))
+        planes["W"].append(s.W)
+        planes["H"].append(s.H)
+        planes["steps"].append(s.step_count)
+        pots = (s.pots() + [-1, -1])[:2]
+        for i in range(2):
+            planes["agent_cell"][i].append(s.agent_cell[i])
+            planes["facing"][i].append(s.facing[i])
+            planes["held"][i].append(s.held[i])
+            planes["pot_cell"][i].append(pots[i])
+            planes["pot_onions"][i].append(s.pot_onions.get(pots[i], 0))
+            planes["pot_timer"][i].append(s.pot_timer.get(pots[i], 0))
+    return R.oc_pack_state(cfg, {k: np.array(v, dtype=np.int64) for k, v in planes.items()}, device)
+
+
+def oc_state_tuple(s):
+    """Comparable form of an oracle Overcooked State."""
+    return (s.W, s.H, tuple(s.cells), tuple(s.items), tuple(s.agent_cell), tuple(s.facing), tuple(s.held),
+            tuple(sorted(s.pot_onions.items())), tuple(sorted(s.pot_timer.items())), s.step_count)
 
 
 def logit_tol(ref, rtol):

@@ -52,7 +52,7 @@ def _status(cfg):
     (dict(max_steps=0), R.RL_EINVAL),
     (dict(env_base=-1), R.RL_EINVAL),
     (dict(kind=7), R.RL_EINVAL),
-    (dict(kind=R.RL_ENV_OVERCOOKED), R.RL_EUNSUPPORTED),
+    (dict(kind=R.RL_ENV_OVERCOOKED), R.RL_EINVAL),  # cook_time 0
     (dict(kind=R.RL_ENV_HANABI), R.RL_EUNSUPPORTED),
     (dict(extra={"hn_colors": 5}), R.RL_EINVAL),
 ])
@@ -61,6 +61,35 @@ def test_bad_config(kw, code):
     assert _status(cfg) == code
     assert R.rl_state_bytes(cfg) == 0
     assert R.lib.rollout_last_error()
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(cook_time=0), R.RL_EINVAL),
+    (dict(cook_time=256), R.RL_EINVAL),
+    (dict(soup_reward=-1), R.RL_EINVAL),
+    (dict(max_steps=0), R.RL_EINVAL),
+])
+def test_bad_overcooked_config(kw, code):
+    cfg = R.overcooked_config(16, **kw)
+    assert _status(cfg) == code
+    assert R.rl_state_bytes(cfg) == 0
+
+
+def test_overcooked_rejects_other_kinds_fields():
+    for name, v in (("n_agents", 3), ("grid_h", 5), ("n_food", 1), ("max_food_level", 2), ("hn_colors", 5)):
+        c = R.overcooked_config(16).c()
+        setattr(c, name, v)
+        assert R.lib.rl_obs_dim(ctypes.byref(c)) == R.RL_EINVAL, name
+
+
+def test_overcooked_queries():
+    cfg = R.overcooked_config(100)
+    assert R.rl_obs_dim(cfg) == 26 * 45
+    assert R.rl_num_actions(cfg) == 6
+    assert R.rl_state_bytes(cfg) == 32 * 100 * 4
+    # the fused rollout checks the policy against the kitchen's sizes
+    assert _run_status(cfg, _policy_struct(dims=(192, 64, 64, 6))) == R.RL_ESHAPE
+    assert _run_status(cfg, _policy_struct(dims=(1170, 64, 64, 5))) == R.RL_ESHAPE
 
 
 def test_queries():
