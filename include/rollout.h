@@ -8,8 +8,8 @@
  * shared team reward r(s, a), per-agent observations o_i of s', and a fresh
  * episode from the initial-state distribution rho when one ends.  The
  * environments are those of Section 4 (environment table): Level-Based
- * Foraging (LBF) and an Overcooked-style two-agent kitchen are implemented;
- * the Hanabi kind is reserved and reports RL_EUNSUPPORTED until built.
+ * Foraging (LBF), an Overcooked-style two-agent kitchen and two-player
+ * Hanabi are implemented.
  *
  * Conventions for every entry point
  *   - Tensor pointers are DEVICE pointers (gfx950 global memory), owned by the
@@ -69,6 +69,12 @@ enum { RL_F32 = 0, RL_BF16 = 1 };
  * be 0.  Observations have 26 * 45 = 1170 features per agent and there are
  * 6 actions (0 noop, 1 north, 2 south, 3 west, 4 east, 5 interact).  Rules in
  * the Overcooked section below.
+ *
+ * Hanabi: n_agents == 2 and the standard game (hn_colors 5, hn_ranks 5,
+ * hn_hand_size 5, hn_info_tokens 8, hn_life_tokens 3; other positive values
+ * give RL_EUNSUPPORTED), max_steps >= 1 (truncation; a game cannot last 100
+ * moves, so 1000 never truncates).  Observations have 658 features (0/1) per
+ * agent and there are 20 actions; rules in the Hanabi section below.
  * Fields of another kind must be 0 (RL_EINVAL otherwise). */
 typedef struct {
   int32_t kind;            /* RL_ENV_* */
@@ -81,7 +87,7 @@ typedef struct {
   int32_t max_steps;       /* episode step limit (truncation) */
   int32_t oc_cook_time;    /* Overcooked: steps a full pot cooks (0 for LBF) */
   int32_t oc_soup_reward;  /* Overcooked: reward of a served soup (0 for LBF) */
-  int32_t hn_colors, hn_ranks, hn_hand_size, hn_info_tokens, hn_life_tokens; /* Hanabi (reserved) */
+  int32_t hn_colors, hn_ranks, hn_hand_size, hn_info_tokens, hn_life_tokens; /* Hanabi (0 otherwise) */
   int64_t env_base;        /* global id of env 0 of this batch (>= 0) */
   uint64_t seed;           /* Philox key word 0 */
 } rl_env_config;
@@ -254,7 +260,53 @@ rl_status rl_gumbel_noise(const uint32_t* u, int64_t n, float* g, void* stream);
  * agent's cell), 10-14 counter / onion / plate / pot / serving cells, 15-17
  * onion / plate / soup on a counter, 18-20 own held onion / plate / soup and
  * 21-23 the other's (at the holder's cell), 24 onions in each pot and 25 its
- * remaining cook timer (at the pot cell). */
+ * remaining cook timer (at the pot cell).
+ *
+ * ---- Hanabi ----
+ * Cards: id = colour * 5 + rank - 1; per colour, rank 1 has 3 copies, ranks
+ * 2-4 two, rank 5 one (50 cards).  Reset at step t: the ordered deck (colours
+ * in order, ranks ascending with their copies) is shuffled by Fisher-Yates,
+ * for i = 49 down to 1 swapping cards i and j = u(i + 1), with draw k = 0..48
+ * of the TAG_RESET stream taken as for LBF; player 0 holds deck[0..4] in slots
+ * 0..4, player 1 deck[5..9], deck[10] is drawn next; player 0 moves first
+ * with 8 info tokens and 3 lives.
+ * Actions of the player to move: 0-4 discard slot, 5-9 play slot, 10-14
+ * hint colour c to the partner, 15-19 hint rank r.  Legal: play a held slot;
+ * discard a held slot when tokens < 8; hint when tokens > 0 and the partner
+ * holds a matching card.  The other player has no legal action: its mask row
+ * is all zero, its logits all -inf, and its sampled / injected action (0)
+ * is ignored.  An illegal injected action of the mover acts as its lowest
+ * legal action.
+ * Step: a play that is one above its colour's firework extends it (reward
+ * +1; a completed firework returns a token if below 8), otherwise the card
+ * is discarded and a life lost; a discard returns a token.  The hand then
+ * closes up and the next deck card, if any, enters the last slot with blank
+ * knowledge.  A hint costs a token: matching partner cards learn that value
+ * exactly, the others lose it from their possible set.  The game ends (done
+ * bit 0) when the last life is lost (that step's reward is minus the
+ * fireworks total, so the game scores 0), when every firework is complete,
+ * or on the second move after the move that drew the last card.
+ * State buffer: 35 int32 planes of E entries (plane p of env e at
+ * state[p * E + e]): 0-12 the deck, card k in byte k % 4 of plane k / 4;
+ * 13-14 the hands (5-bit card ids, slot s at bit 5s); 15-16 cards held;
+ * 17-18 possible colours and 19-20 possible ranks (5-bit masks, slot s at bit
+ * 5s); 21-22 hinted colour + 1 and 23-24 hinted rank (3 bits per slot, 0 =
+ * none); 25 firework heights (3 bits per colour); 26-27 discarded copies
+ * (2 bits per card id, ids 0-15 then 16-24); 28 info tokens; 29 lives; 30
+ * player to move; 31 moves left after the deck ran out (-1 before); 32 index
+ * of the next deck card; 33 steps taken; 34 the last move (bit 0 present, 1
+ * actor, 2-3 kind: play, discard, hint colour, hint rank; 4 hint target; 5-7
+ * hinted colour + 1; 8-10 hinted rank; 11-15 revealed slots; 16-18 acted slot
+ * + 1; 19-23 acted card + 1; 24 play succeeded; 25 token gained).
+ * Observation of agent i, 658 features (0/1): the partner's hand (5 slots x
+ * 25 card one-hot), 2 bits for a short hand (own, partner), a 40-bit
+ * thermometer of the cards left in the deck, per colour a one-hot of its
+ * firework height (25), token (8) and life (3) thermometers, per card id a
+ * thermometer of its discarded copies (50), the last move (55: actor relative
+ * to i, kind, hint target relative to i, hinted colour, hinted rank, revealed
+ * slots, acted slot, acted card, play succeeded, token gained), and the
+ * knowledge of agent i's then the partner's hand (5 slots x (25 plausible
+ * cards, hinted colour, hinted rank)). */
 
 #ifdef __cplusplus
 }

@@ -37,6 +37,7 @@ struct EnvSpec {
   int kind;
   rl::LbfParams lbf;
   rl::OcParams oc;
+  rl::HnParams hn;
   int E, A, D, NA;
   size_t state_bytes;
 };
@@ -102,20 +103,44 @@ rl_status check_overcooked(const rl_env_config* cfg, EnvSpec* es) {
   return RL_OK;
 }
 
+rl_status check_hanabi(const rl_env_config* cfg, EnvSpec* es) {
+  if (cfg->n_agents != 2) return fail(RL_EINVAL, "Hanabi is built for 2 players, got %d", cfg->n_agents);
+  if (cfg->hn_colors < 1 || cfg->hn_ranks < 1 || cfg->hn_hand_size < 1 || cfg->hn_info_tokens < 1 ||
+      cfg->hn_life_tokens < 1)
+    return fail(RL_EINVAL, "Hanabi colours, ranks, hand size, info and life tokens must be >= 1");
+  if (cfg->hn_colors != rl::HN_COLOURS || cfg->hn_ranks != rl::HN_RANKS || cfg->hn_hand_size != rl::HN_HAND ||
+      cfg->hn_info_tokens != rl::HN_INFO || cfg->hn_life_tokens != rl::HN_LIVES)
+    return fail(RL_EUNSUPPORTED, "Hanabi is built for 5 colours, 5 ranks, hands of 5, 8 info tokens, 3 lives");
+  if (cfg->grid_h || cfg->grid_w || cfg->n_food || cfg->max_agent_level || cfg->max_food_level ||
+      cfg->oc_cook_time || cfg->oc_soup_reward)
+    return fail(RL_EINVAL, "LBF/Overcooked fields must be 0 for Hanabi");
+  rl::HnParams& p = es->hn;
+  p.E = cfg->n_envs;
+  p.max_steps = cfg->max_steps;
+  p.env_base = cfg->env_base;
+  p.seed = cfg->seed;
+  es->A = 2;
+  es->D = rl::HN_OBS;
+  es->NA = rl::HN_NACT;
+  es->state_bytes = (size_t)rl::HN_PLANES_STATE * (size_t)p.E * sizeof(int32_t);
+  return RL_OK;
+}
+
 // Checks cfg and fills the kernel parameters of its kind.
 rl_status check_cfg(const rl_env_config* cfg, EnvSpec* es) {
   EnvSpec local;
   if (!es) es = &local;
   if (!cfg) return fail(RL_EINVAL, "cfg is NULL");
-  if (cfg->kind == RL_ENV_HANABI) return fail(RL_EUNSUPPORTED, "env kind %d is not built in this library", cfg->kind);
-  if (cfg->kind != RL_ENV_LBF && cfg->kind != RL_ENV_OVERCOOKED)
+  if (cfg->kind != RL_ENV_LBF && cfg->kind != RL_ENV_OVERCOOKED && cfg->kind != RL_ENV_HANABI)
     return fail(RL_EINVAL, "unknown env kind %d", cfg->kind);
   if (cfg->n_envs < 1 || cfg->n_envs > (1 << 26)) return fail(RL_EINVAL, "n_envs %d outside 1..2^26", cfg->n_envs);
   if (cfg->env_base < 0) return fail(RL_EINVAL, "env_base must be >= 0");
   if (cfg->max_steps < 1) return fail(RL_EINVAL, "max_steps must be >= 1");
   es->kind = cfg->kind;
   es->E = cfg->n_envs;
-  return cfg->kind == RL_ENV_LBF ? check_lbf(cfg, es) : check_overcooked(cfg, es);
+  return cfg->kind == RL_ENV_LBF ? check_lbf(cfg, es)
+         : cfg->kind == RL_ENV_OVERCOOKED ? check_overcooked(cfg, es)
+                                          : check_hanabi(cfg, es);
 }
 
 rl_status check_policy(const rl_policy* pol, rl::PolicyArgs* a) {
@@ -177,8 +202,9 @@ rl_status rollout_init(const rl_env_config* cfg, void* state, void* obs, int32_t
   const int dt = obs_dtype == RL_F32 ? rl::DT_F32 : rl::DT_BF16;
   int32_t* st = static_cast<int32_t*>(state);
   const hipStream_t hs = (hipStream_t)stream;
-  return launched(es.kind == RL_ENV_LBF ? rl::launch_lbf_init(es.lbf, st, obs, dt, legal, hs)
-                                        : rl::launch_oc_init(es.oc, st, obs, dt, legal, hs),
+  return launched(es.kind == RL_ENV_LBF          ? rl::launch_lbf_init(es.lbf, st, obs, dt, legal, hs)
+                  : es.kind == RL_ENV_OVERCOOKED ? rl::launch_oc_init(es.oc, st, obs, dt, legal, hs)
+                                                 : rl::launch_hn_init(es.hn, st, obs, dt, legal, hs),
                   "rollout_init");
 }
 
@@ -196,10 +222,14 @@ rl_status rollout_step(const rl_env_config* cfg, void* state, uint64_t t0, int32
   const int dt = obs_dtype == RL_F32 ? rl::DT_F32 : rl::DT_BF16;
   int32_t* st = static_cast<int32_t*>(state);
   const hipStream_t hs = (hipStream_t)stream;
-  return launched(es.kind == RL_ENV_LBF
-                      ? rl::launch_lbf_step(es.lbf, st, t0, n_steps, actions, obs_out, dt, reward, done, legal_out, hs)
-                      : rl::launch_oc_step(es.oc, st, t0, n_steps, actions, obs_out, dt, reward, done, legal_out, hs),
-                  "rollout_step");
+  hipError_t e;
+  if (es.kind == RL_ENV_LBF)
+    e = rl::launch_lbf_step(es.lbf, st, t0, n_steps, actions, obs_out, dt, reward, done, legal_out, hs);
+  else if (es.kind == RL_ENV_OVERCOOKED)
+    e = rl::launch_oc_step(es.oc, st, t0, n_steps, actions, obs_out, dt, reward, done, legal_out, hs);
+  else
+    e = rl::launch_hn_step(es.hn, st, t0, n_steps, actions, obs_out, dt, reward, done, legal_out, hs);
+  return launched(e, "rollout_step");
 }
 
 rl_status policy_forward(const rl_policy* policy, const void* obs, const uint8_t* legal, int64_t rows,
@@ -228,15 +258,17 @@ rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* s
   if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
   if (a.D != es.D) return fail(RL_ESHAPE, "policy input size %d != observation size %d", a.D, es.D);
   if (a.NA != es.NA) return fail(RL_ESHAPE, "policy has %d actions, the env %d", a.NA, es.NA);
-  const size_t lds = es.kind == RL_ENV_LBF ? rl::make_run_layout(es.A, es.D, a.H1, a.H2, a.dt).total
-                                           : rl::oc_run_lds_bytes(a);
+  const size_t lds = es.kind == RL_ENV_LBF          ? rl::make_run_layout(es.A, es.D, a.H1, a.H2, a.dt).total
+                     : es.kind == RL_ENV_OVERCOOKED ? rl::oc_run_lds_bytes(a)
+                                                    : rl::hn_run_lds_bytes(a);
   if (lds > rl::MAX_LDS_BYTES)
     return fail(RL_EUNSUPPORTED, "rollout tile needs %zu bytes of LDS (max %zu)", lds, rl::MAX_LDS_BYTES);
   const rl::TrajArgs o{out->obs, out->actions, out->logits, out->reward, out->done, out->obs_last};
   int32_t* st = static_cast<int32_t*>(state);
   const hipStream_t hs = (hipStream_t)stream;
-  return launched(es.kind == RL_ENV_LBF ? rl::launch_lbf_run(es.lbf, a, st, t0, n_steps, o, hs)
-                                        : rl::launch_oc_run(es.oc, a, st, t0, n_steps, o, hs),
+  return launched(es.kind == RL_ENV_LBF          ? rl::launch_lbf_run(es.lbf, a, st, t0, n_steps, o, hs)
+                  : es.kind == RL_ENV_OVERCOOKED ? rl::launch_oc_run(es.oc, a, st, t0, n_steps, o, hs)
+                                                 : rl::launch_hn_run(es.hn, a, st, t0, n_steps, o, hs),
                   "rollout_run");
 }
 

@@ -1,0 +1,402 @@
+// Two-player Hanabi device logic: one game held in the registers of one lane
+// as packed bit fields, plus the observation feature function.
+//
+// Hanabi is an environment of Section 4 (environment table), run as the
+// Dec-POMDP step of Section 3 with the standard game: 5 colours x 5 ranks,
+// 50 cards, hands of 5, 8 info tokens, 3 lives, 20 actions.  Rules, the
+// state-buffer layout and the observation are documented in
+// include/rollout.h.  Hands and per-card knowledge are arrays of small
+// fields in one 32-bit word each, so closing up a hand after a play is two
+// masks and a shift; the deck is 13 words of 4 card bytes, read with a
+// select chain (no dynamically indexed registers).
+#pragma once
+#include "rl_philox.h"
+
+namespace rl {
+
+constexpr int HN_COLOURS = 5, HN_RANKS = 5, HN_HAND = 5, HN_INFO = 8, HN_LIVES = 3;
+constexpr int HN_CARDS = 50, HN_KINDS = 25, HN_NACT = 20, HN_OBS = 658;
+constexpr int HN_DECK_WORDS = 13;
+constexpr int HN_PLANES_STATE = 35;  // int32 state planes per env
+enum : int { HN_PLAY = 0, HN_DISCARD = 1, HN_HINT_COLOUR = 2, HN_HINT_RANK = 3 };
+
+struct HnParams {
+  int E, max_steps;
+  int64_t env_base;
+  uint64_t seed;
+};
+
+struct HnEnv {
+  uint32_t deck[HN_DECK_WORDS];  // card k in byte k % 4 of word k / 4
+  uint32_t hand[2];              // 5-bit card id per slot (slot s at bit 5s); unused slots 0
+  uint32_t kc[2], kr[2];         // possible colours / ranks, 5 bits per slot
+  uint32_t hc[2], hr[2];         // hinted colour + 1 / hinted rank, 3 bits per slot (0: none)
+  int n[2];                      // cards held
+  uint32_t fw;                   // firework heights, 3 bits per colour
+  uint32_t disc0, disc1;         // discarded copies, 2 bits per card id (ids 0-15, 16-24)
+  int info, lives, cur, turns_left, next, steps;
+  uint32_t last;                 // packed last action, 0 before the first move
+};
+
+// Packed last action: bit 0 present, 1 actor, 2-3 kind, 4 hint target,
+// 5-7 hinted colour + 1, 8-10 hinted rank, 11-15 revealed slots,
+// 16-18 acted slot + 1, 19-23 acted card + 1, 24 play succeeded, 25 token gained.
+
+__device__ __forceinline__ uint32_t hn_field(uint32_t w, int width, int i) {
+  return (w >> (width * i)) & ((1u << width) - 1u);
+}
+
+// Remove field i of a packed array of `width`-bit fields; later fields move down one.
+__device__ __forceinline__ uint32_t hn_remove(uint32_t w, int width, int i) {
+  const uint32_t low = (1u << (width * i)) - 1u;
+  return (w & low) | ((w >> width) & ~low);
+}
+
+__device__ __forceinline__ int hn_deck_card(const HnEnv& s, int k) {
+  uint32_t w = 0;
+#pragma unroll
+  for (int i = 0; i < HN_DECK_WORDS; ++i) w = (i == (k >> 2)) ? s.deck[i] : w;
+  return (int)((w >> (8 * (k & 3))) & 0xffu);
+}
+
+__device__ __forceinline__ int hn_disc(const HnEnv& s, int card) {
+  return card < 16 ? (int)((s.disc0 >> (2 * card)) & 3u) : (int)((s.disc1 >> (2 * (card - 16))) & 3u);
+}
+
+__device__ __forceinline__ void hn_add_disc(HnEnv& s, int card) {
+  if (card < 16)
+    s.disc0 += 1u << (2 * card);
+  else
+    s.disc1 += 1u << (2 * (card - 16));
+}
+
+// A fresh game at step t: Fisher-Yates over the ordered deck through this
+// lane's 52-byte LDS slot, with the reset stream's draws (j = u(i + 1) for
+// i = 49 down to 1).
+__device__ __forceinline__ void hn_reset(const HnParams& p, uint64_t env, uint64_t t, HnEnv& s,
+                                         uint8_t* __restrict__ slot) {
+  // ordered deck: per colour, rank 1 x3, ranks 2-4 x2, rank 5 x1
+  for (int k = 0; k < HN_CARDS; ++k) {
+    const int c = k / 10, o = k - c * 10;
+    const int r = o < 3 ? 0 : o < 5 ? 1 : o < 7 ? 2 : o < 9 ? 3 : 4;
+    slot[k] = (uint8_t)(c * HN_RANKS + r);
+  }
+  Block4 b{0, 0, 0, 0};
+  for (int i = HN_CARDS - 1, k = 0; i >= 1; --i, ++k) {
+    if ((k & 7) == 0) b = draw_block(p.seed, env, t, (uint64_t)(k >> 3), TAG_RESET);
+    const int j = (int)range_map(block_u32(b, k & 7), (uint32_t)(i + 1));
+    const uint8_t a = slot[i], c = slot[j];
+    slot[i] = c;
+    slot[j] = a;
+  }
+#pragma unroll
+  for (int w = 0; w < HN_DECK_WORDS; ++w) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (4 * w + q < HN_CARDS) v |= (uint32_t)slot[4 * w + q] << (8 * q);
+    s.deck[w] = v;
+  }
+#pragma unroll
+  for (int pl = 0; pl < 2; ++pl) {
+    uint32_t h = 0;
+#pragma unroll
+    for (int q = 0; q < HN_HAND; ++q) h |= (uint32_t)hn_deck_card(s, pl * HN_HAND + q) << (5 * q);
+    s.hand[pl] = h;
+    s.n[pl] = HN_HAND;
+    s.kc[pl] = s.kr[pl] = 0x1ffffffu;  // every colour and rank possible in all 5 slots
+    s.hc[pl] = s.hr[pl] = 0;
+  }
+  s.fw = 0;
+  s.disc0 = s.disc1 = 0;
+  s.info = HN_INFO;
+  s.lives = HN_LIVES;
+  s.cur = 0;
+  s.turns_left = -1;
+  s.next = 2 * HN_HAND;
+  s.steps = 0;
+  s.last = 0;
+}
+
+// Legal actions of the player to move as a 20-bit mask.  (Player-indexed
+// fields are picked with selects, not indexed by the mover: a register array
+// indexed at run time would live in scratch memory.)
+__device__ __forceinline__ uint32_t hn_legal(const HnEnv& s) {
+  const bool one = s.cur == 1;
+  const int np = one ? s.n[1] : s.n[0], nq = one ? s.n[0] : s.n[1];
+  const uint32_t hq = one ? s.hand[0] : s.hand[1];
+  const uint32_t held = (1u << np) - 1u;
+  uint32_t m = held << HN_HAND;                   // play
+  if (s.info < HN_INFO) m |= held;                // discard
+  if (s.info > 0) {
+    uint32_t cols = 0, ranks = 0;
+#pragma unroll
+    for (int i = 0; i < HN_HAND; ++i)
+      if (i < nq) {
+        const int card = (int)hn_field(hq, 5, i);
+        cols |= 1u << (card / HN_RANKS);
+        ranks |= 1u << (card % HN_RANKS);
+      }
+    m |= cols << (2 * HN_HAND);
+    m |= ranks << (2 * HN_HAND + HN_COLOURS);
+  }
+  return m;
+}
+
+// Exchange the two players' hands and knowledge when `sw` (so that the mover
+// can be addressed as player 0 with constant indices).
+__device__ __forceinline__ void hn_orient(HnEnv& s, bool sw) {
+  auto x = [sw](uint32_t& a, uint32_t& b) {
+    const uint32_t t0 = sw ? b : a, t1 = sw ? a : b;
+    a = t0;
+    b = t1;
+  };
+  x(s.hand[0], s.hand[1]);
+  x(s.kc[0], s.kc[1]);
+  x(s.kr[0], s.kr[1]);
+  x(s.hc[0], s.hc[1]);
+  x(s.hr[0], s.hr[1]);
+  const int n0 = sw ? s.n[1] : s.n[0], n1 = sw ? s.n[0] : s.n[1];
+  s.n[0] = n0;
+  s.n[1] = n1;
+}
+
+// One move of the player to move (an illegal or out-of-range action acts as
+// its lowest legal one); `s` becomes the post-transition state (no reset).
+__device__ __forceinline__ void hn_transition(const HnParams& p, HnEnv& s, int a_in, float& reward, uint32_t& done) {
+  const uint32_t legal = hn_legal(s);
+  const int a = ((unsigned)a_in < (unsigned)HN_NACT && ((legal >> a_in) & 1u)) ? a_in : __builtin_ctz(legal);
+  const int mover = s.cur;
+  hn_orient(s, mover == 1);
+  constexpr int pl = 0, q = 1;  // the mover and its partner after hn_orient
+  int rew = 0;
+  bool drew_last = false;
+  const int fw_total_before = (int)(hn_field(s.fw, 3, 0) + hn_field(s.fw, 3, 1) + hn_field(s.fw, 3, 2) +
+                                    hn_field(s.fw, 3, 3) + hn_field(s.fw, 3, 4));
+  if (a < 2 * HN_HAND) {
+    const int slot = a % HN_HAND;
+    const bool play = a >= HN_HAND;
+    const int card = (int)hn_field(s.hand[pl], 5, slot);
+    uint32_t last = 1u | ((uint32_t)mover << 1) | ((uint32_t)(play ? HN_PLAY : HN_DISCARD) << 2) |
+                    ((uint32_t)(slot + 1) << 16) | ((uint32_t)(card + 1) << 19);
+    if (!play) {
+      hn_add_disc(s, card);
+      s.info += 1;
+      last |= 1u << 25;
+    } else {
+      const int c = card / HN_RANKS, r = card % HN_RANKS + 1;
+      if ((int)hn_field(s.fw, 3, c) + 1 == r) {
+        s.fw += 1u << (3 * c);
+        rew = 1;
+        last |= 1u << 24;
+        if (r == HN_RANKS && s.info < HN_INFO) {
+          s.info += 1;
+          last |= 1u << 25;
+        }
+      } else {
+        hn_add_disc(s, card);
+        s.lives -= 1;
+      }
+    }
+    s.hand[pl] = hn_remove(s.hand[pl], 5, slot);
+    s.kc[pl] = hn_remove(s.kc[pl], 5, slot);
+    s.kr[pl] = hn_remove(s.kr[pl], 5, slot);
+    s.hc[pl] = hn_remove(s.hc[pl], 3, slot);
+    s.hr[pl] = hn_remove(s.hr[pl], 3, slot);
+    s.n[pl] -= 1;
+    if (s.next < HN_CARDS) {
+      const int sh = 5 * s.n[pl];
+      s.hand[pl] |= (uint32_t)hn_deck_card(s, s.next) << sh;
+      s.kc[pl] |= 31u << sh;
+      s.kr[pl] |= 31u << sh;
+      s.n[pl] += 1;
+      s.next += 1;
+      drew_last = s.next == HN_CARDS;
+    }
+    s.last = last;
+  } else {
+    const int h = a - 2 * HN_HAND;
+    const bool colour = h < HN_COLOURS;
+    const int v = colour ? h : h - HN_COLOURS;  // colour, or rank - 1
+    uint32_t revealed = 0;
+    uint32_t mask = colour ? s.kc[q] : s.kr[q];  // the knowledge words the hint updates
+    uint32_t hint = colour ? s.hc[q] : s.hr[q];
+#pragma unroll
+    for (int i = 0; i < HN_HAND; ++i)
+      if (i < s.n[q]) {
+        const int card = (int)hn_field(s.hand[q], 5, i);
+        const bool match = colour ? card / HN_RANKS == v : card % HN_RANKS == v;
+        if (match) {
+          mask = (mask & ~(31u << (5 * i))) | ((1u << v) << (5 * i));
+          hint = (hint & ~(7u << (3 * i))) | ((uint32_t)(v + 1) << (3 * i));
+          revealed |= 1u << i;
+        } else {
+          mask &= ~((1u << v) << (5 * i));
+        }
+      }
+    s.kc[q] = colour ? mask : s.kc[q];
+    s.hc[q] = colour ? hint : s.hc[q];
+    s.kr[q] = colour ? s.kr[q] : mask;
+    s.hr[q] = colour ? s.hr[q] : hint;
+    s.info -= 1;
+    s.last = 1u | ((uint32_t)mover << 1) | ((uint32_t)(colour ? HN_HINT_COLOUR : HN_HINT_RANK) << 2) |
+             ((uint32_t)(1 - mover) << 4) | (colour ? (uint32_t)(v + 1) << 5 : (uint32_t)(v + 1) << 8) |
+             (revealed << 11);
+  }
+  hn_orient(s, mover == 1);
+  if (s.turns_left > 0) s.turns_left -= 1;
+  if (drew_last) s.turns_left = 2;
+  bool terminated = false;
+  if (s.lives == 0) {
+    terminated = true;
+    rew = -fw_total_before;
+  } else if (s.fw == 0x5b6du /* every height 5 */ || s.turns_left == 0) {
+    terminated = true;
+  }
+  s.cur = 1 - mover;
+  s.steps += 1;
+  reward = (float)rew;
+  done = (terminated ? 1u : 0u) | (s.steps >= p.max_steps ? 2u : 0u);
+}
+
+// State planes (int32, E entries each); see include/rollout.h.
+__device__ __forceinline__ void hn_load(const int32_t* __restrict__ st, int E, int e, HnEnv& s) {
+  auto w = [&](int pl) { return (uint32_t)st[(size_t)pl * E + e]; };
+#pragma unroll
+  for (int i = 0; i < HN_DECK_WORDS; ++i) s.deck[i] = w(i);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    s.hand[i] = w(13 + i);
+    s.n[i] = (int)w(15 + i);
+    s.kc[i] = w(17 + i);
+    s.kr[i] = w(19 + i);
+    s.hc[i] = w(21 + i);
+    s.hr[i] = w(23 + i);
+  }
+  s.fw = w(25);
+  s.disc0 = w(26);
+  s.disc1 = w(27);
+  s.info = (int)w(28);
+  s.lives = (int)w(29);
+  s.cur = (int)w(30);
+  s.turns_left = (int)w(31);
+  s.next = (int)w(32);
+  s.steps = (int)w(33);
+  s.last = w(34);
+}
+
+__device__ __forceinline__ void hn_store(int32_t* __restrict__ st, int E, int e, const HnEnv& s) {
+  auto w = [&](int pl, uint32_t v) { st[(size_t)pl * E + e] = (int32_t)v; };
+#pragma unroll
+  for (int i = 0; i < HN_DECK_WORDS; ++i) w(i, s.deck[i]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    w(13 + i, s.hand[i]);
+    w(15 + i, (uint32_t)s.n[i]);
+    w(17 + i, s.kc[i]);
+    w(19 + i, s.kr[i]);
+    w(21 + i, s.hc[i]);
+    w(23 + i, s.hr[i]);
+  }
+  w(25, s.fw);
+  w(26, s.disc0);
+  w(27, s.disc1);
+  w(28, (uint32_t)s.info);
+  w(29, (uint32_t)s.lives);
+  w(30, (uint32_t)s.cur);
+  w(31, (uint32_t)s.turns_left);
+  w(32, (uint32_t)s.next);
+  w(33, (uint32_t)s.steps);
+  w(34, s.last);
+}
+
+// What the observation encoder reads of one game (kept in LDS, one per env).
+struct HnView {
+  uint32_t hand[2], kc[2], kr[2], hc[2], hr[2];
+  int n[2];
+  uint32_t fw, disc0, disc1;
+  int info, lives, next, cur;
+  uint32_t last;
+};
+
+__device__ __forceinline__ void hn_view(const HnEnv& s, HnView& v) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    v.hand[i] = s.hand[i];
+    v.kc[i] = s.kc[i];
+    v.kr[i] = s.kr[i];
+    v.hc[i] = s.hc[i];
+    v.hr[i] = s.hr[i];
+    v.n[i] = s.n[i];
+  }
+  v.fw = s.fw;
+  v.disc0 = s.disc0;
+  v.disc1 = s.disc1;
+  v.info = s.info;
+  v.lives = s.lives;
+  v.next = s.next;
+  v.cur = s.cur;
+  v.last = s.last;
+}
+
+// Feature f (0..657) of the observation of player `me`, as 0 or 1.
+__device__ __forceinline__ uint32_t hn_feature(const HnView& v, int me, int f) {
+  const int ot = 1 - me;
+  if (f < 125) {  // partner hand
+    const int slot = f / 25, c = f - slot * 25;
+    return (slot < v.n[ot] && (int)hn_field(v.hand[ot], 5, slot) == c) ? 1u : 0u;
+  }
+  f -= 125;
+  if (f < 2) return (f == 0 ? v.n[me] : v.n[ot]) < HN_HAND ? 1u : 0u;
+  f -= 2;
+  if (f < 40) return HN_CARDS - v.next > f ? 1u : 0u;
+  f -= 40;
+  if (f < 25) {
+    const int c = f / 5, r = f - c * 5;
+    return (int)hn_field(v.fw, 3, c) == r + 1 ? 1u : 0u;
+  }
+  f -= 25;
+  if (f < 8) return v.info > f ? 1u : 0u;
+  f -= 8;
+  if (f < 3) return v.lives > f ? 1u : 0u;
+  f -= 3;
+  if (f < 50) {
+    const int c = f / 10, o = f - c * 10;
+    const int r = o < 3 ? 0 : o < 5 ? 1 : o < 7 ? 2 : o < 9 ? 3 : 4;
+    const int start = r == 0 ? 0 : 2 * r + 1;
+    const int card = c * HN_RANKS + r;
+    const int cnt = card < 16 ? (int)((v.disc0 >> (2 * card)) & 3u) : (int)((v.disc1 >> (2 * (card - 16))) & 3u);
+    return cnt > o - start ? 1u : 0u;
+  }
+  f -= 50;
+  if (f < 55) {
+    const uint32_t L = v.last;
+    if (!(L & 1u)) return 0u;
+    const int actor = (int)((L >> 1) & 1u), kind = (int)((L >> 2) & 3u), target = (int)((L >> 4) & 1u);
+    const bool hint = kind >= HN_HINT_COLOUR;
+    if (f < 2) return f == ((actor - me) & 1) ? 1u : 0u;
+    if (f < 6) return f - 2 == kind ? 1u : 0u;
+    if (f < 8) return (hint && f - 6 == ((target - me) & 1)) ? 1u : 0u;
+    if (f < 13) return (int)((L >> 5) & 7u) == f - 8 + 1 ? 1u : 0u;   // hinted colour (0 when none)
+    if (f < 18) return (int)((L >> 8) & 7u) == f - 13 + 1 ? 1u : 0u;  // hinted rank
+    if (f < 23) return (L >> (11 + f - 18)) & 1u;                     // revealed slots
+    if (f < 28) return (int)((L >> 16) & 7u) == f - 23 + 1 ? 1u : 0u; // acted slot
+    if (f < 53) return (int)((L >> 19) & 31u) == f - 28 + 1 ? 1u : 0u;
+    return (L >> (24 + f - 53)) & 1u;                                 // success, token
+  }
+  f -= 55;
+  {
+    const int j = f / 175, rem = f - j * 175;
+    const int who = j == 0 ? me : ot;
+    const int slot = rem / 35, g = rem - slot * 35;
+    if (slot >= v.n[who]) return 0u;
+    if (g < 25) {
+      const int c = g / 5, r = g - c * 5;
+      return ((hn_field(v.kc[who], 5, slot) >> c) & (hn_field(v.kr[who], 5, slot) >> r) & 1u);
+    }
+    if (g < 30) return (int)hn_field(v.hc[who], 3, slot) == g - 25 + 1 ? 1u : 0u;
+    return (int)hn_field(v.hr[who], 3, slot) == g - 30 + 1 ? 1u : 0u;
+  }
+}
+
+}  // namespace rl

@@ -5,6 +5,7 @@
 
 #include "rl_lbf.h"
 #include "rl_mlp.h"
+#include "rl_hanabi.h"
 #include "rl_overcooked.h"
 
 namespace rl {
@@ -98,6 +99,13 @@ hipError_t launch_oc_step(const OcParams& p, int32_t* state, uint64_t t0, int n_
                           void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s);
 size_t oc_run_lds_bytes(const PolicyArgs& pol);
 hipError_t launch_oc_run(const OcParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
+                         const TrajArgs& out, hipStream_t s);
+
+hipError_t launch_hn_init(const HnParams& p, int32_t* state, void* obs, int obs_dt, uint8_t* legal, hipStream_t s);
+hipError_t launch_hn_step(const HnParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,
+                          void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s);
+size_t hn_run_lds_bytes(const PolicyArgs& pol);
+hipError_t launch_hn_run(const HnParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
                          const TrajArgs& out, hipStream_t s);
 
 size_t policy_lds_bytes(const PolicyArgs& pol);

@@ -77,16 +77,17 @@ __host__ __device__ constexpr int lds_ld(int K) {
   return DT == DT_F32 ? round_up(K, 4) + 4 : round_up(K, 32) + 8;
 }
 
-// One 16 x 16 output tile: acc += A[m0:m0+16, 0:Kpad] * W[n0:n0+16, 0:Kpad]^T.
+// One 16 x 16 output tile: acc += A[16 rows, 0:Kpad] * W[n0:n0+16, 0:Kpad]^T,
+// where `a` points at element 0 of A row (lane % 16) of the tile.
 template <int DT>
-__device__ __forceinline__ f32x4 mma_tile(const typename DType<DT>::T* __restrict__ in, int lda, int m0,
-                                          int Kpad, int K, const typename DType<DT>::T* __restrict__ W,
-                                          int n0, int N, int lane) {
+__device__ __forceinline__ f32x4 mma_tile_row(const typename DType<DT>::T* __restrict__ a_row, int Kpad, int K,
+                                              const typename DType<DT>::T* __restrict__ W, int n0, int N,
+                                              int lane) {
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   const int n = n0 + (lane & 15);
   const bool nok = n < N;
   if constexpr (DT == DT_F32) {
-    const float* arow = in + (size_t)(m0 + (lane & 15)) * lda + (lane >> 4);
+    const float* arow = a_row + (lane >> 4);
     const float* wrow = W + (size_t)(nok ? n : 0) * K + (lane >> 4);
     for (int k0 = 0; k0 < Kpad; k0 += 4) {
       const float a = arow[k0];
@@ -94,7 +95,7 @@ __device__ __forceinline__ f32x4 mma_tile(const typename DType<DT>::T* __restric
       acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
     }
   } else {
-    const uint16_t* arow = in + (size_t)(m0 + (lane & 15)) * lda + (lane >> 4) * 8;
+    const uint16_t* arow = a_row + (lane >> 4) * 8;
     const uint16_t* wrow = W + (size_t)(nok ? n : 0) * K + (lane >> 4) * 8;
     const bool vec = (K & 7) == 0;
     for (int k0 = 0; k0 < Kpad; k0 += 32) {
@@ -122,6 +123,14 @@ __device__ __forceinline__ f32x4 mma_tile(const typename DType<DT>::T* __restric
   return acc;
 }
 
+// The same tile for rows m0..m0+15 of a row-major A with leading dimension lda.
+template <int DT>
+__device__ __forceinline__ f32x4 mma_tile(const typename DType<DT>::T* __restrict__ in, int lda, int m0,
+                                          int Kpad, int K, const typename DType<DT>::T* __restrict__ W,
+                                          int n0, int N, int lane) {
+  return mma_tile_row<DT>(in + (size_t)(m0 + (lane & 15)) * lda, Kpad, K, W, n0, N, lane);
+}
+
 // A hidden layer: out = tanh(in W^T + b), stored in the layer dtype.
 // R rows (multiple of 16), N outputs (multiple of 16).
 template <int DT>
@@ -136,6 +145,29 @@ __device__ __forceinline__ void mlp_hidden(const typename DType<DT>::T* in, int 
   for (int tile = wave; tile < mt * nt; tile += nwaves) {
     const int m0 = (tile / nt) << 4, n0 = (tile % nt) << 4;
     const f32x4 acc = mma_tile<DT>(in, lda, m0, Kpad, K, W, n0, N, lane);
+    const int col = n0 + (lane & 15);
+    const float bias = DTy::to_f32(b[col]);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = m0 + 4 * (lane >> 4) + r;
+      out[(size_t)row * ldo + col] = DTy::from_f32(fast_tanh(acc[r] + bias));
+    }
+  }
+}
+
+// mlp_hidden over the A rows rows[0..R-1] of `in` (row indices in LDS).
+template <int DT>
+__device__ __forceinline__ void mlp_hidden_rows(const typename DType<DT>::T* in, int lda, const int* rows, int R,
+                                                int K, const typename DType<DT>::T* __restrict__ W,
+                                                const typename DType<DT>::T* __restrict__ b, int N,
+                                                typename DType<DT>::T* out, int ldo, int wave, int nwaves,
+                                                int lane) {
+  using DTy = DType<DT>;
+  const int Kpad = round_up(K, DTy::KS);
+  const int mt = R >> 4, nt = N >> 4;
+  for (int tile = wave; tile < mt * nt; tile += nwaves) {
+    const int m0 = (tile / nt) << 4, n0 = (tile % nt) << 4;
+    const f32x4 acc = mma_tile_row<DT>(in + (size_t)rows[m0 + (lane & 15)] * lda, Kpad, K, W, n0, N, lane);
     const int col = n0 + (lane & 15);
     const float bias = DTy::to_f32(b[col]);
 #pragma unroll

@@ -128,6 +128,13 @@ def overcooked_config(n_envs, cook_time=20, soup_reward=20, max_steps=400, env_b
                      extra={"oc_cook_time": cook_time, "oc_soup_reward": soup_reward})
 
 
+def hanabi_config(n_envs, max_steps=1000, env_base=0, seed=0):
+    """An ``EnvConfig`` for two-player Hanabi (5 colours x 5 ranks, hands of 5, 8 info tokens, 3 lives)."""
+    return EnvConfig(n_envs, kind=RL_ENV_HANABI, n_agents=2, max_steps=max_steps, env_base=env_base, seed=seed,
+                     extra={"hn_colors": 5, "hn_ranks": 5, "hn_hand_size": 5, "hn_info_tokens": 8,
+                            "hn_life_tokens": 3})
+
+
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
@@ -338,4 +345,32 @@ def oc_pack_state(cfg, planes, device="cuda"):
                   (29, "pot_timer")):
         buf[lo:lo + 2] = torch.as_tensor(planes[k], dtype=torch.int32).reshape(2, E)
     buf[31] = torch.as_tensor(planes["steps"], dtype=torch.int32).reshape(E)
+    return buf.reshape(-1).to(device)
+
+
+# ---- Hanabi state layout (see the Hanabi section of include/rollout.h) ----
+
+HN_N_PLANES = 35
+HN_FIELDS = {"hand": (13, 2), "n": (15, 2), "kc": (17, 2), "kr": (19, 2), "hc": (21, 2), "hr": (23, 2),
+             "fw": (25, 1), "disc0": (26, 1), "disc1": (27, 1), "info": (28, 1), "lives": (29, 1), "cur": (30, 1),
+             "turns_left": (31, 1), "next": (32, 1), "steps": (33, 1), "last": (34, 1)}
+
+
+def hn_state_planes(cfg, state):
+    """Split a Hanabi state buffer into named int32 planes: "deck" [13, E] and the packed fields."""
+    p = state.reshape(HN_N_PLANES, cfg.n_envs)
+    out = {"deck": p[0:13]}
+    for k, (lo, n) in HN_FIELDS.items():
+        out[k] = p[lo:lo + n] if n > 1 else p[lo]
+    return out
+
+
+def hn_pack_state(cfg, planes, device="cuda"):
+    """Inverse of hn_state_planes."""
+    E = cfg.n_envs
+    buf = torch.empty(HN_N_PLANES, E, dtype=torch.int32)
+    buf[0:13] = torch.as_tensor(planes["deck"], dtype=torch.int64).reshape(13, E).to(torch.int32)
+    for k, (lo, n) in HN_FIELDS.items():
+        v = torch.as_tensor(planes[k], dtype=torch.int64).reshape(n, E)
+        buf[lo:lo + n] = (((v & 0xFFFFFFFF) ^ 0x80000000) - 0x80000000).to(torch.int32)
     return buf.reshape(-1).to(device)

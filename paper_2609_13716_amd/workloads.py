@@ -19,6 +19,10 @@ Overcooked-style kitchen (two agents; seeded random kitchens of 5x4 to 9x5,
 rules and observation as documented in include/rollout.h):
     oc_4096      4096 envs x 400 steps, cook time 20, soup reward 20, episodes of
                  400 steps, MLP 1170-256-256-6 bf16
+
+Two-player Hanabi (5 colours x 5 ranks, hands of 5, 8 info tokens, 3 lives):
+    hn_4096      4096 envs x 80 steps, MLP 658-512-512-20 bf16 on the mover's
+                 observation, illegal actions masked
 """
 
 import numpy as np
@@ -35,11 +39,15 @@ WORKLOADS = {
                       n_envs=16384, n_steps=256, hidden=(256, 256), dtypes=("bf16",)),
     "oc_4096": dict(kind="overcooked", env=dict(cook_time=20, soup_reward=20, max_steps=400),
                     n_envs=4096, n_steps=400, hidden=(256, 256), dtypes=("bf16",)),
+    "hn_4096": dict(kind="hanabi", env=dict(max_steps=1000), n_envs=4096, n_steps=80, hidden=(512, 512),
+                    dtypes=("bf16",)),
 }
 
 LBF_ACTIONS = 6
 OC_ACTIONS = 6
 OC_OBS_DIM = 26 * 45
+HN_ACTIONS = 20
+HN_OBS_DIM = 658
 
 
 def lbf_obs_dim(env):
@@ -54,6 +62,8 @@ def policy_dims(name):
     w = WORKLOADS[name]
     if kind(name) == "overcooked":
         return (OC_OBS_DIM, *w["hidden"], OC_ACTIONS)
+    if kind(name) == "hanabi":
+        return (HN_OBS_DIM, *w["hidden"], HN_ACTIONS)
     return (lbf_obs_dim(w["env"]), *w["hidden"], LBF_ACTIONS)
 
 

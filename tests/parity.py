@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import lbf, overcooked, sampling
+from oracle import hanabi, lbf, overcooked, sampling
 
 
 def require_gpu():
@@ -124,6 +124,87 @@ def oc_state_tuple(s):
     """Comparable form of an oracle Overcooked State."""
     return (s.W, s.H, tuple(s.cells), tuple(s.items), tuple(s.agent_cell), tuple(s.facing), tuple(s.held),
             tuple(sorted(s.pot_onions.items())), tuple(sorted(s.pot_timer.items())), s.step_count)
+
+
+def hn_oracle_cfg(cfg):
+    return hanabi.Config(max_steps=cfg.max_steps)
+
+
+def _hn_last_from_word(L):
+    if not L & 1:
+        return None
+    kind = (L >> 2) & 3
+    hint = kind in (hanabi.LAST_HINT_COLOUR, hanabi.LAST_HINT_RANK)
+    return hanabi.LastAction(actor=(L >> 1) & 1, kind=kind, target=(L >> 4) & 1 if hint else -1,
+                             colour=((L >> 5) & 7) - 1 if kind == hanabi.LAST_HINT_COLOUR else -1,
+                             rank=(L >> 8) & 7 if kind == hanabi.LAST_HINT_RANK else -1,
+                             revealed=(L >> 11) & 31, slot=((L >> 16) & 7) - 1, card=((L >> 19) & 31) - 1,
+                             success=bool((L >> 24) & 1), token=bool((L >> 25) & 1))
+
+
+def _hn_last_to_word(a):
+    if a is None:
+        return 0
+    w = 1 | (a.actor << 1) | (a.kind << 2) | (a.revealed << 11) | ((a.slot + 1) << 16) | ((a.card + 1) << 19)
+    w |= (int(a.success) << 24) | (int(a.token) << 25)
+    if a.kind in (hanabi.LAST_HINT_COLOUR, hanabi.LAST_HINT_RANK):
+        w |= a.target << 4
+    if a.kind == hanabi.LAST_HINT_COLOUR:
+        w |= (a.colour + 1) << 5
+    if a.kind == hanabi.LAST_HINT_RANK:
+        w |= a.rank << 8
+    return w
+
+
+def hn_states_from_device(cfg, state):
+    """Oracle Hanabi State objects from a device (or host) state buffer."""
+    from paper_2609_13716_amd import rollout as R
+    v = {k: t.cpu().numpy().astype(np.int64) & 0xFFFFFFFF for k, t in R.hn_state_planes(cfg, state.cpu()).items()}
+    out = []
+    for e in range(cfg.n_envs):
+        deck = [(int(v["deck"][k // 4, e]) >> (8 * (k % 4))) & 0xFF for k in range(50)]
+        hands, know = [], []
+        for p in range(2):
+            n = int(v["n"][p, e])
+            hands.append([(int(v["hand"][p, e]) >> (5 * i)) & 31 for i in range(n)])
+            know.append([hanabi.Knowledge((int(v["kc"][p, e]) >> (5 * i)) & 31, (int(v["kr"][p, e]) >> (5 * i)) & 31,
+                                          ((int(v["hc"][p, e]) >> (3 * i)) & 7) - 1,
+                                          ((int(v["hr"][p, e]) >> (3 * i)) & 7) or -1) for i in range(n)])
+        disc = [(int(v["disc0"][e]) >> (2 * c)) & 3 if c < 16 else (int(v["disc1"][e]) >> (2 * (c - 16))) & 3
+                for c in range(25)]
+        tl = int(v["turns_left"][e])
+        out.append(hanabi.State(deck, int(v["next"][e]), hands, know, [(int(v["fw"][e]) >> (3 * c)) & 7
+                                                                        for c in range(5)],
+                                disc, int(v["info"][e]), int(v["lives"][e]), int(v["cur"][e]),
+                                tl - (1 << 32) if tl >= 1 << 31 else tl, _hn_last_from_word(int(v["last"][e])),
+                                int(v["steps"][e])))
+    return out
+
+
+def hn_states_to_device(cfg, states, device="cuda"):
+    from paper_2609_13716_amd import rollout as R
+    E = len(states)
+    pl = {"deck": np.zeros((13, E), np.int64)}
+    for k, (_, n) in R.HN_FIELDS.items():
+        pl[k] = np.zeros((n, E), np.int64) if n > 1 else np.zeros(E, np.int64)
+    for e, s in enumerate(states):
+        for k in range(50):
+            pl["deck"][k // 4, e] |= s.deck[k] << (8 * (k % 4))
+        for p in range(2):
+            pl["n"][p, e] = len(s.hands[p])
+            for i, (x, kn) in enumerate(zip(s.hands[p], s.know[p])):
+                pl["hand"][p, e] |= x << (5 * i)
+                pl["kc"][p, e] |= kn.colours << (5 * i)
+                pl["kr"][p, e] |= kn.ranks << (5 * i)
+                pl["hc"][p, e] |= (kn.hint_colour + 1) << (3 * i)
+                pl["hr"][p, e] |= max(kn.hint_rank, 0) << (3 * i)
+        pl["fw"][e] = sum(f << (3 * c) for c, f in enumerate(s.fireworks))
+        pl["disc0"][e] = sum(s.discards[c] << (2 * c) for c in range(16))
+        pl["disc1"][e] = sum(s.discards[c] << (2 * (c - 16)) for c in range(16, 25))
+        pl["info"][e], pl["lives"][e], pl["cur"][e] = s.info, s.lives, s.cur
+        pl["turns_left"][e], pl["next"][e], pl["steps"][e] = s.turns_left, s.next_card, s.step_count
+        pl["last"][e] = _hn_last_to_word(s.last)
+    return R.hn_pack_state(cfg, pl, device)
 
 
 def logit_tol(ref, rtol):

@@ -53,7 +53,7 @@ def _status(cfg):
     (dict(env_base=-1), R.RL_EINVAL),
     (dict(kind=7), R.RL_EINVAL),
     (dict(kind=R.RL_ENV_OVERCOOKED), R.RL_EINVAL),  # cook_time 0
-    (dict(kind=R.RL_ENV_HANABI), R.RL_EUNSUPPORTED),
+    (dict(kind=R.RL_ENV_HANABI), R.RL_EINVAL),  # game sizes 0
     (dict(extra={"hn_colors": 5}), R.RL_EINVAL),
 ])
 def test_bad_config(kw, code):
@@ -80,6 +80,20 @@ def test_overcooked_rejects_other_kinds_fields():
         c = R.overcooked_config(16).c()
         setattr(c, name, v)
         assert R.lib.rl_obs_dim(ctypes.byref(c)) == R.RL_EINVAL, name
+
+
+def test_hanabi_config_checks():
+    cfg = R.hanabi_config(100)
+    assert R.rl_obs_dim(cfg) == 658 and R.rl_num_actions(cfg) == 20
+    assert R.rl_state_bytes(cfg) == 35 * 100 * 4
+    for name, v, code in (("hn_colors", 4, R.RL_EUNSUPPORTED), ("hn_hand_size", 4, R.RL_EUNSUPPORTED),
+                          ("hn_life_tokens", 0, R.RL_EINVAL), ("n_agents", 3, R.RL_EINVAL),
+                          ("grid_w", 3, R.RL_EINVAL), ("oc_cook_time", 20, R.RL_EINVAL)):
+        c = R.hanabi_config(16).c()
+        setattr(c, name, v)
+        assert R.lib.rl_obs_dim(ctypes.byref(c)) == code, name
+    assert _run_status(cfg, _policy_struct(dims=(658, 64, 64, 6))) == R.RL_ESHAPE
+    assert _run_status(cfg, _policy_struct(dims=(600, 64, 64, 20))) == R.RL_ESHAPE
 
 
 def test_overcooked_queries():
