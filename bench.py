@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--cpu-envs", type=int, default=2048, help="envs in the oracle's timed sample")
     ap.add_argument("--only", choices=["run_bf16", "run_f32", "env_bf16", "policy_bf16"], default=None,
                     help="time one kernel only (for profiler runs)")
+    ap.add_argument("--workload-only", default=None,
+                    help="time one secondary workload only (lbf12_16k, oc_4096, hn_4096; for profiler runs)")
+    ap.add_argument("--no-workloads", action="store_true", help="skip the secondary workloads")
     return ap.parse_args()
 
 
@@ -86,6 +89,72 @@ def load_traffic(kernel_key):
         return None
     k = rec.get("kernels", {}).get(kernel_key)
     return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+def env_config(R, workloads, name, n_envs=None, seed=0):
+    w = workloads.WORKLOADS[name]
+    E = w["n_envs"] if n_envs is None else n_envs
+    kind = workloads.kind(name)
+    if kind == "overcooked":
+        return R.overcooked_config(E, seed=seed, **w["env"])
+    if kind == "hanabi":
+        return R.hanabi_config(E, seed=seed, **w["env"])
+    return R.EnvConfig(n_envs=E, seed=seed, **w["env"])
+
+
+def measure_workload(R, workloads, name, dt, steps, warmup):
+    """rollout_run and rollout_step of one workload at full size: times, throughput and rooflines."""
+    import torch
+    w = workloads.WORKLOADS[name]
+    cfg = env_config(R, workloads, name)
+    E, T, A = cfg.n_envs, w["n_steps"], cfg.n_agents
+    D, nA = R.rl_obs_dim(cfg), R.rl_num_actions(cfg)
+    dims = workloads.policy_dims(name)
+    ws, bs = workloads.policy_weights(dims, seed=1000)
+    pol = R.Policy(ws, bs, dt)
+    es = 2 if dt == "bf16" else 4
+    acting = 1 if workloads.kind(name) == "hanabi" else A  # Hanabi: only the mover's row affects an action
+    flop_per_row = 2 * sum(dims[i] * dims[i + 1] for i in range(3))
+    state_bytes = R.rl_state_bytes(cfg)
+    state = R.new_state(cfg)
+    R.rollout_init(cfg, state)
+    obs = torch.empty(T, E, A, D, dtype=pol.torch_dtype, device="cuda")
+    acts = torch.empty(T, E, A, dtype=torch.int32, device="cuda")
+    rew = torch.empty(T, E, device="cuda")
+    done = torch.empty(T, E, dtype=torch.uint8, device="cuda")
+    t_next = [0]
+
+    def run():
+        R.rollout_run(cfg, pol, state, t_next[0], T, obs=obs, actions=acts, reward=rew, done=done)
+        t_next[0] += T
+
+    kern_ms, wall_ms = timed(run, steps, warmup)
+    nbytes = E * T * (A * D * es + A * 4 + 4 + 1) + 2 * state_bytes
+    flops = E * T * acting * flop_per_row
+    out = {"workload": name, "dtype": dt, "n_envs": E, "steps_per_rollout": T, "policy": "-".join(map(str, dims)),
+           "value": round(E * T * acting / (wall_ms * 1e-3), 1), "unit": "agent-env steps/s",
+           "env_steps_per_s": round(E * T / (wall_ms * 1e-3), 1), "ms_per_step": round(wall_ms, 4),
+           "kernel_ms": round(kern_ms, 4),
+           "roofline_hbm": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"),
+           "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s")}
+    # env-only stepping with injected uniform actions (illegal ones fall back to the lowest legal action)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+    inj = torch.randint(0, nA, (T, E, A), dtype=torch.int32, device="cuda", generator=g)
+    R.rollout_init(cfg, state)
+    t_next[0] = 0
+
+    def env():
+        R.rollout_step(cfg, state, t_next[0], inj, obs, rew, done)
+        t_next[0] += T
+
+    kern_ms, wall_ms = timed(env, steps, warmup)
+    nbytes = E * T * (A * 4 + A * D * es + 4 + 1) + 2 * state_bytes
+    out["env_only"] = {"env_steps_per_s": round(E * T / (wall_ms * 1e-3), 1), "kernel_ms": round(kern_ms, 4),
+                       "roofline": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s")}
+    del obs
+    torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(n_envs, T):
@@ -196,6 +265,11 @@ def main():
         flops = rows * flop_per_row
         return dict(kern_ms=kern_ms, rows=rows, flops=flops, tflops=flops / (kern_ms * 1e-3) / 1e12)
 
+    if args.workload_only:
+        print(json.dumps(measure_workload(R, workloads, args.workload_only, "bf16", args.steps, args.warmup)),
+              flush=True)
+        return
+
     if args.only:
         kind, dt = args.only.split("_")
         {"run": rollout_case, "env": env_case, "policy": policy_case}[kind](dt)
@@ -244,6 +318,10 @@ def main():
                            for dt in ("bf16", "f32")},
         "csrc_hash": csrc_hash(),
     }
+    if not args.no_workloads:
+        # the other workloads at full size, bf16, a few timed launches each
+        line["workloads"] = {n: measure_workload(R, workloads, n, "bf16", min(args.steps, 5), 1)
+                             for n in ("lbf12_16k", "oc_4096", "hn_4096")}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.cpu_envs, T)
     print(json.dumps(line), flush=True)

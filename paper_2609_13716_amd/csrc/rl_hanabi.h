@@ -8,7 +8,8 @@
 // include/rollout.h.  Hands and per-card knowledge are arrays of small
 // fields in one 32-bit word each, so closing up a hand after a play is two
 // masks and a shift; the deck is 13 words of 4 card bytes, read with a
-// select chain (no dynamically indexed registers).
+// select chain (no dynamically indexed registers).  A reset's Fisher-Yates
+// shuffle runs across a whole wave, one deck position per lane.
 #pragma once
 #include "rl_philox.h"
 
@@ -70,38 +71,48 @@ __device__ __forceinline__ void hn_add_disc(HnEnv& s, int card) {
     s.disc1 += 1u << (2 * (card - 16));
 }
 
-// A fresh game at step t: Fisher-Yates over the ordered deck through this
-// lane's 52-byte LDS slot, with the reset stream's draws (j = u(i + 1) for
-// i = 49 down to 1).
-__device__ __forceinline__ void hn_reset(const HnParams& p, uint64_t env, uint64_t t, HnEnv& s,
-                                         uint8_t* __restrict__ slot) {
-  // ordered deck: per colour, rank 1 x3, ranks 2-4 x2, rank 5 x1
-  for (int k = 0; k < HN_CARDS; ++k) {
-    const int c = k / 10, o = k - c * 10;
-    const int r = o < 3 ? 0 : o < 5 ? 1 : o < 7 ? 2 : o < 9 ? 3 : 4;
-    slot[k] = (uint8_t)(c * HN_RANKS + r);
-  }
+// The deck of a fresh game at step t, shuffled by one whole wave (all lanes
+// call this with the same env and t): lane l < 50 holds the card at position
+// l, starting from the ordered deck (per colour: rank 1 x3, ranks 2-4 x2,
+// rank 5 x1); Fisher-Yates for i = 49 down to 1 swaps positions i and
+// j = u(i + 1), with draw k = 49 - i of the reset stream.  Lanes 0..6 first
+// evaluate the 7 Philox blocks of the 49 draws; every swap is then two
+// readlanes.  The 13 packed deck words (card k in byte k % 4 of word k / 4)
+// are written to `words` (LDS).
+__device__ __forceinline__ void hn_wave_shuffle(uint64_t seed, uint64_t env, uint64_t t, int lane,
+                                                uint32_t* __restrict__ words) {
   Block4 b{0, 0, 0, 0};
-  for (int i = HN_CARDS - 1, k = 0; i >= 1; --i, ++k) {
-    if ((k & 7) == 0) b = draw_block(p.seed, env, t, (uint64_t)(k >> 3), TAG_RESET);
-    const int j = (int)range_map(block_u32(b, k & 7), (uint32_t)(i + 1));
-    const uint8_t a = slot[i], c = slot[j];
-    slot[i] = c;
-    slot[j] = a;
-  }
+  if (lane < 7) b = draw_block(seed, env, t, (uint64_t)lane, TAG_RESET);
+  const int c = lane / 10, o = lane - c * 10;
+  int a = c * HN_RANKS + (o < 3 ? 0 : o < 5 ? 1 : o < 7 ? 2 : o < 9 ? 3 : 4);
 #pragma unroll
-  for (int w = 0; w < HN_DECK_WORDS; ++w) {
-    uint32_t v = 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (4 * w + q < HN_CARDS) v |= (uint32_t)slot[4 * w + q] << (8 * q);
-    s.deck[w] = v;
+  for (int k = 0; k < HN_CARDS - 1; ++k) {
+    const int i = HN_CARDS - 1 - k;
+    const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)block_u32(b, k & 7), k >> 3);
+    const int j = (int)range_map(d, (uint32_t)(i + 1));
+    const int ai = __builtin_amdgcn_readlane(a, i), aj = __builtin_amdgcn_readlane(a, j);
+    a = lane == i ? aj : lane == j ? ai : a;
   }
+  uint32_t v = lane < HN_CARDS ? (uint32_t)a << (8 * (lane & 3)) : 0u;
+  v |= (uint32_t)__shfl_xor((int)v, 1);
+  v |= (uint32_t)__shfl_xor((int)v, 2);
+  if ((lane & 3) == 0 && lane < 4 * HN_DECK_WORDS) words[lane >> 2] = v;
+}
+
+// A fresh game on the shuffled deck `words`: player 0 holds cards 0..4 in
+// slots 0..4, player 1 cards 5..9, card 10 is drawn next; player 0 moves
+// first with all tokens and lives, blank knowledge, no fireworks or discards.
+__device__ __forceinline__ void hn_deal(HnEnv& s, const uint32_t* __restrict__ words) {
+#pragma unroll
+  for (int w = 0; w < HN_DECK_WORDS; ++w) s.deck[w] = words[w];
 #pragma unroll
   for (int pl = 0; pl < 2; ++pl) {
     uint32_t h = 0;
 #pragma unroll
-    for (int q = 0; q < HN_HAND; ++q) h |= (uint32_t)hn_deck_card(s, pl * HN_HAND + q) << (5 * q);
+    for (int q = 0; q < HN_HAND; ++q) {
+      const int k = pl * HN_HAND + q;  // compile-time position: a fixed byte of a fixed word
+      h |= ((s.deck[k >> 2] >> (8 * (k & 3))) & 0xffu) << (5 * q);
+    }
     s.hand[pl] = h;
     s.n[pl] = HN_HAND;
     s.kc[pl] = s.kr[pl] = 0x1ffffffu;  // every colour and rank possible in all 5 slots
@@ -339,15 +350,47 @@ __device__ __forceinline__ void hn_view(const HnEnv& s, HnView& v) {
   v.last = s.last;
 }
 
-// Feature f (0..657) of the observation of player `me`, as 0 or 1.
+// The view of a wave-uniform env as seen by player `me`, in scalar registers:
+// player-indexed fields are reordered so that index 0 is the observer and 1
+// its partner (by selects: a register array indexed at run time would live
+// in scratch memory).
+__device__ __forceinline__ HnView hn_view_oriented(const HnView& v, int me) {
+  auto u = [](uint32_t x) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)x); };
+  auto i = [](int x) { return __builtin_amdgcn_readfirstlane(x); };
+  const bool sw = me == 1;
+  HnView r;
+  r.hand[0] = u(sw ? v.hand[1] : v.hand[0]);
+  r.hand[1] = u(sw ? v.hand[0] : v.hand[1]);
+  r.kc[0] = u(sw ? v.kc[1] : v.kc[0]);
+  r.kc[1] = u(sw ? v.kc[0] : v.kc[1]);
+  r.kr[0] = u(sw ? v.kr[1] : v.kr[0]);
+  r.kr[1] = u(sw ? v.kr[0] : v.kr[1]);
+  r.hc[0] = u(sw ? v.hc[1] : v.hc[0]);
+  r.hc[1] = u(sw ? v.hc[0] : v.hc[1]);
+  r.hr[0] = u(sw ? v.hr[1] : v.hr[0]);
+  r.hr[1] = u(sw ? v.hr[0] : v.hr[1]);
+  r.n[0] = i(sw ? v.n[1] : v.n[0]);
+  r.n[1] = i(sw ? v.n[0] : v.n[1]);
+  r.fw = u(v.fw);
+  r.disc0 = u(v.disc0);
+  r.disc1 = u(v.disc1);
+  r.info = i(v.info);
+  r.lives = i(v.lives);
+  r.next = i(v.next);
+  r.cur = i(v.cur);
+  r.last = u(v.last);
+  return r;
+}
+
+// Feature f (0..657) of the observation of player `me`, as 0 or 1, from the
+// view oriented for `me` (hn_view_oriented).
 __device__ __forceinline__ uint32_t hn_feature(const HnView& v, int me, int f) {
-  const int ot = 1 - me;
   if (f < 125) {  // partner hand
     const int slot = f / 25, c = f - slot * 25;
-    return (slot < v.n[ot] && (int)hn_field(v.hand[ot], 5, slot) == c) ? 1u : 0u;
+    return (slot < v.n[1] && (int)hn_field(v.hand[1], 5, slot) == c) ? 1u : 0u;
   }
   f -= 125;
-  if (f < 2) return (f == 0 ? v.n[me] : v.n[ot]) < HN_HAND ? 1u : 0u;
+  if (f < 2) return (f == 0 ? v.n[0] : v.n[1]) < HN_HAND ? 1u : 0u;
   f -= 2;
   if (f < 40) return HN_CARDS - v.next > f ? 1u : 0u;
   f -= 40;
@@ -386,16 +429,16 @@ __device__ __forceinline__ uint32_t hn_feature(const HnView& v, int me, int f) {
   }
   f -= 55;
   {
-    const int j = f / 175, rem = f - j * 175;
-    const int who = j == 0 ? me : ot;
+    const int j = f / 175, rem = f - j * 175;  // j = 0: the observer's hand, 1: the partner's
     const int slot = rem / 35, g = rem - slot * 35;
-    if (slot >= v.n[who]) return 0u;
+    if (slot >= (j ? v.n[1] : v.n[0])) return 0u;
     if (g < 25) {
       const int c = g / 5, r = g - c * 5;
-      return ((hn_field(v.kc[who], 5, slot) >> c) & (hn_field(v.kr[who], 5, slot) >> r) & 1u);
+      const uint32_t kc = j ? v.kc[1] : v.kc[0], kr = j ? v.kr[1] : v.kr[0];
+      return ((hn_field(kc, 5, slot) >> c) & (hn_field(kr, 5, slot) >> r) & 1u);
     }
-    if (g < 30) return (int)hn_field(v.hc[who], 3, slot) == g - 25 + 1 ? 1u : 0u;
-    return (int)hn_field(v.hr[who], 3, slot) == g - 30 + 1 ? 1u : 0u;
+    if (g < 30) return (int)hn_field(j ? v.hc[1] : v.hc[0], 3, slot) == g - 25 + 1 ? 1u : 0u;
+    return (int)hn_field(j ? v.hr[1] : v.hr[0], 3, slot) == g - 30 + 1 ? 1u : 0u;
   }
 }
 

@@ -9,41 +9,42 @@
 // that is copied to the trajectory.  In the fused rollout only the mover's
 // row goes through the policy (the other player has no legal action): its
 // rows are gathered from the tile by index, and the MLP is the streaming
-// MFMA MLP of rl_mlp.h.
+// MFMA MLP of rl_mlp.h.  When games end, the waves shuffle the new decks
+// (one wave per deck) before the env lanes deal them.
 #include "rl_hanabi.h"
 #include "rl_internal.h"
 #include "rl_sample.h"
 
 namespace rl {
 
-constexpr int HN_DECK_SLOT = 52;  // LDS bytes of one lane's Fisher-Yates deck
-
 struct HnTile {
   HnView view;
   uint32_t legal;  // mover's 20-bit legal mask
 };
 
-// Paint rows 2*el + me (el < te_valid) of the observation tile.
-template <typename T, int TE, int NT>
-__device__ __forceinline__ void hn_paint(const HnTile* __restrict__ envs, int te_valid, T* tile, int ld, int tid) {
-  const int n = 2 * te_valid * HN_OBS;
-  for (int idx = tid; idx < n; idx += NT) {
-    const int r = idx / HN_OBS, f = idx - r * HN_OBS;
-    tile[(size_t)r * ld + f] = small_int_to<T>(hn_feature(envs[r >> 1].view, r & 1, f));
+// Paint rows 2*el + me (el < te_valid) of the observation tile, one row per
+// wave at a time: the row's game view is read once into scalar registers and
+// the wave's lanes take 64 consecutive features per pass.
+template <typename T, int NW>
+__device__ __forceinline__ void hn_paint(const HnTile* __restrict__ envs, int te_valid, T* tile, int ld, int wave,
+                                         int lane) {
+  for (int r = wave; r < 2 * te_valid; r += NW) {
+    const HnView v = hn_view_oriented(envs[r >> 1].view, r & 1);
+    T* row = tile + (size_t)r * ld;
+    for (int f = lane; f < HN_OBS; f += 64) row[f] = small_int_to<T>(hn_feature(v, r & 1, f));
   }
 }
 
-// Copy `rows` rows of `len` elements from an LDS tile (leading dimension ld)
-// to consecutive global rows; rows of 4-byte multiples, 4-byte words.
-template <typename T, int NT>
-__device__ __forceinline__ void hn_copy_rows(const T* src, int ld, T* __restrict__ dst, int len, int rows, int tid) {
-  constexpr int PER = 4 / (int)sizeof(T);
-  const int wpr = len / PER, ldw = ld / PER;
+// Copy `rows` rows of HN_OBS elements from an LDS tile with leading dimension
+// LD to consecutive global rows, in 4-byte words.
+template <typename T, int LD, int NT>
+__device__ __forceinline__ void hn_copy_rows(const T* src, T* __restrict__ dst, int rows, int tid) {
+  constexpr int PER = 4 / (int)sizeof(T), WPR = HN_OBS / PER, LDW = LD / PER;
   const uint32_t* s = reinterpret_cast<const uint32_t*>(src);
   uint32_t* g = reinterpret_cast<uint32_t*>(dst);
-  for (int i = tid; i < rows * wpr; i += NT) {
-    const int r = i / wpr, w = i - r * wpr;
-    g[i] = s[r * ldw + w];
+  for (int i = tid; i < rows * WPR; i += NT) {
+    const int r = i / WPR, w = i - r * WPR;
+    g[i] = s[r * LDW + w];
   }
 }
 
@@ -62,26 +63,49 @@ __device__ __forceinline__ void hn_publish(const HnEnv& s, HnTile& t) {
   t.legal = hn_legal(s);
 }
 
+// Shuffles for the envs of the tile flagged in need[] (drawn at step t):
+// wave w takes envs w, w + NW, ...
+template <int NW>
+__device__ __forceinline__ void hn_shuffle_flagged(const HnParams& p, int e0, int te_valid, uint64_t t,
+                                                   const uint32_t* need, uint32_t (*words)[HN_DECK_WORDS], int wave,
+                                                   int lane) {
+  for (int el = wave; el < te_valid; el += NW)
+    if (need[el]) hn_wave_shuffle(p.seed, (uint64_t)(p.env_base + e0 + el), t, lane, words[el]);
+}
+
+// need[TE] = whether any env lane (all in wave 0) has d != 0; read after a barrier.
+__device__ __forceinline__ void hn_flag_any(uint32_t* need, int TE, uint32_t d, int wave, int lane) {
+  if (wave == 0) {
+    const bool any = __builtin_amdgcn_ballot_w64(d != 0) != 0;
+    if (lane == 0) need[TE] = any ? 1u : 0u;
+  }
+}
+
 // -------------------------------------------------------------- init ----
 
 template <typename OT, int TE>
 __global__ __launch_bounds__(NTHREADS) void hn_init_kernel(HnParams p, int32_t* __restrict__ state,
                                                            OT* __restrict__ obs, uint8_t* __restrict__ legal) {
+  constexpr int NW = NTHREADS / 64;
   __shared__ HnTile envs[TE];
-  __shared__ __align__(16) uint8_t decks[TE][HN_DECK_SLOT];
+  __shared__ uint32_t words[TE][HN_DECK_WORDS];
   __shared__ __align__(16) OT tile[2 * TE * HN_OBS];
-  const int tid = threadIdx.x, e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0);
+  for (int el = wave; el < te_valid; el += NW)
+    hn_wave_shuffle(p.seed, (uint64_t)(p.env_base + e0 + el), 0, lane, words[el]);
+  __syncthreads();
   if (tid < te_valid) {
     HnEnv s;
-    hn_reset(p, (uint64_t)(p.env_base + e0 + tid), 0, s, decks[tid]);
+    hn_deal(s, words[tid]);
     hn_store(state, p.E, e0 + tid, s);
     hn_publish(s, envs[tid]);
   }
   __syncthreads();
   if (obs) {
-    hn_paint<OT, TE, NTHREADS>(envs, te_valid, tile, HN_OBS, tid);
+    hn_paint<OT, NW>(envs, te_valid, tile, HN_OBS, wave, lane);
     __syncthreads();
-    hn_copy_rows<OT, NTHREADS>(tile, HN_OBS, obs + (size_t)e0 * 2 * HN_OBS, HN_OBS, 2 * te_valid, tid);
+    copy_tile(tile, obs + (size_t)e0 * 2 * HN_OBS, 2 * te_valid * HN_OBS, tid, NTHREADS);
   }
   if (legal) hn_write_legal<NTHREADS>(envs, te_valid, legal + (size_t)e0 * 2 * HN_NACT, tid);
 }
@@ -93,33 +117,46 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
                                                           int n_steps, const int32_t* __restrict__ actions,
                                                           OT* __restrict__ obs, float* __restrict__ reward,
                                                           uint8_t* __restrict__ done, uint8_t* __restrict__ legal) {
+  constexpr int NW = NTHREADS / 64;
   __shared__ HnTile envs[TE];
-  __shared__ __align__(16) uint8_t decks[TE][HN_DECK_SLOT];
+  __shared__ uint32_t need[TE + 1];  // per env, then "any" at [TE]
+  __shared__ uint32_t words[TE][HN_DECK_WORDS];
   __shared__ __align__(16) OT tile[2 * TE * HN_OBS];
-  const int tid = threadIdx.x, e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
   const bool envlane = tid < te_valid;
   const int e = e0 + tid;
   HnEnv s;
   if (envlane) hn_load(state, E, e, s);
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
+    uint32_t d = 0;
     if (envlane) {
       float r;
-      uint32_t d;
       hn_transition(p, s, actions[((size_t)k * E + e) * 2 + s.cur], r, d);
-      if (d) hn_reset(p, (uint64_t)(p.env_base + e), t + 1, s, decks[tid]);
-      hn_publish(s, envs[tid]);
+      need[tid] = d;
+      if (!d) hn_publish(s, envs[tid]);
       if (reward) reward[(size_t)k * E + e] = r;
       if (done) done[(size_t)k * E + e] = (uint8_t)d;
     }
+    hn_flag_any(need, TE, d, wave, lane);
     __syncthreads();
-    if (obs) {
-      hn_paint<OT, TE, NTHREADS>(envs, te_valid, tile, HN_OBS, tid);
+    if (need[TE]) {  // some game of the tile ended: deal new ones drawn at t + 1
+      hn_shuffle_flagged<NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
       __syncthreads();
-      hn_copy_rows<OT, NTHREADS>(tile, HN_OBS, obs + ((size_t)k * E + e0) * 2 * HN_OBS, HN_OBS, 2 * te_valid, tid);
+      if (d) {
+        hn_deal(s, words[tid]);
+        hn_publish(s, envs[tid]);
+      }
+      __syncthreads();
+    }
+    if (obs) {
+      hn_paint<OT, NW>(envs, te_valid, tile, HN_OBS, wave, lane);
+      __syncthreads();
+      copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * HN_OBS, 2 * te_valid * HN_OBS, tid, NTHREADS);
     }
     if (legal) hn_write_legal<NTHREADS>(envs, te_valid, legal + ((size_t)k * E + e0) * 2 * HN_NACT, tid);
-    __syncthreads();  // the tile and masks are read before the next move rewrites them
+    __syncthreads();  // the tile, views and masks are read before the next move rewrites them
   }
   if (envlane) hn_store(state, E, e, s);
 }
@@ -130,7 +167,7 @@ constexpr int HN_RUN_TE = 16;  // envs (and mover rows) per workgroup
 
 struct HnRunLayout {
   int ldx, ld1, ld2;
-  size_t off_x, off_h1, off_h2, off_lg, off_sc, off_env, off_deck, off_rows, total;
+  size_t off_x, off_h1, off_h2, off_lg, off_sc, off_env, off_words, off_need, off_rows, total;
 };
 
 __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt) {
@@ -140,15 +177,15 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt) {
   L.ld1 = dt == DT_F32 ? lds_ld<DT_F32>(H1) : lds_ld<DT_BF16>(H1);
   L.ld2 = dt == DT_F32 ? lds_ld<DT_F32>(H2) : lds_ld<DT_BF16>(H2);
   size_t o = 0;
-  L.off_x = o;    o += (size_t)2 * HN_RUN_TE * L.ldx * es;
-  L.off_h1 = o;   o += (size_t)HN_RUN_TE * L.ld1 * es;
-  L.off_h2 = o;   o += (size_t)HN_RUN_TE * L.ld2 * es;
-  L.off_lg = o;   o += (size_t)HN_RUN_TE * MAX_NA * 4;
-  L.off_sc = o;   o += (size_t)HN_RUN_TE * MAX_NA * 4;
-  L.off_env = o;  o += (size_t)HN_RUN_TE * sizeof(HnTile);
-  o = (o + 15) & ~(size_t)15;
-  L.off_deck = o; o += (size_t)HN_RUN_TE * HN_DECK_SLOT;
-  L.off_rows = o; o += (size_t)HN_RUN_TE * 4;
+  L.off_x = o;     o += (size_t)2 * HN_RUN_TE * L.ldx * es;
+  L.off_h1 = o;    o += (size_t)HN_RUN_TE * L.ld1 * es;
+  L.off_h2 = o;    o += (size_t)HN_RUN_TE * L.ld2 * es;
+  L.off_lg = o;    o += (size_t)HN_RUN_TE * MAX_NA * 4;
+  L.off_sc = o;    o += (size_t)HN_RUN_TE * MAX_NA * 4;
+  L.off_env = o;   o += (size_t)HN_RUN_TE * sizeof(HnTile);
+  L.off_words = o; o += (size_t)HN_RUN_TE * HN_DECK_WORDS * 4;
+  L.off_need = o;  o += (size_t)(HN_RUN_TE + 1) * 4;
+  L.off_rows = o;  o += (size_t)HN_RUN_TE * 4;
   L.total = o;
   return L;
 }
@@ -159,7 +196,8 @@ template <int DT>
 __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs pol, int32_t* __restrict__ state,
                                                           uint64_t t0, int n_steps, TrajArgs out) {
   using T = typename DType<DT>::T;
-  constexpr int TE = HN_RUN_TE, NA = HN_NACT;
+  constexpr int TE = HN_RUN_TE, NA = HN_NACT, NW = NTHREADS / 64;
+  constexpr int LDX = lds_ld<DT>(HN_OBS);
   extern __shared__ __align__(16) uint8_t smem[];
   const HnRunLayout L = hn_run_layout(pol.H1, pol.H2, DT);
   T* xs = reinterpret_cast<T*>(smem + L.off_x);
@@ -168,7 +206,8 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
   float* lg = reinterpret_cast<float*>(smem + L.off_lg);
   float* sc = reinterpret_cast<float*>(smem + L.off_sc);
   HnTile* envs = reinterpret_cast<HnTile*>(smem + L.off_env);
-  uint8_t* decks = smem + L.off_deck;
+  uint32_t(*words)[HN_DECK_WORDS] = reinterpret_cast<uint32_t(*)[HN_DECK_WORDS]>(smem + L.off_words);
+  uint32_t* need = reinterpret_cast<uint32_t*>(smem + L.off_need);
   int* rows = reinterpret_cast<int*>(smem + L.off_rows);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -192,16 +231,16 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     __syncthreads();  // the previous move's views are published
-    hn_paint<T, TE, NTHREADS>(envs, te_valid, xs, L.ldx, tid);
+    hn_paint<T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
     if (out.obs)
-      hn_copy_rows<T, NTHREADS>(xs, L.ldx, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * HN_OBS, HN_OBS,
-                                2 * te_valid, tid);
-    mlp_hidden_rows<DT>(xs, L.ldx, rows, TE, HN_OBS, W1, b1, pol.H1, h1, L.ld1, wave, NTHREADS / 64, lane);
+      hn_copy_rows<T, LDX, NTHREADS>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * HN_OBS,
+                                     2 * te_valid, tid);
+    mlp_hidden_rows<DT>(xs, LDX, rows, TE, HN_OBS, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane);
     __syncthreads();
-    mlp_hidden<DT>(h1, L.ld1, TE, pol.H1, W2, b2, pol.H2, h2, L.ld2, wave, NTHREADS / 64, lane);
+    mlp_hidden<DT>(h1, L.ld1, TE, pol.H1, W2, b2, pol.H2, h2, L.ld2, wave, NW, lane);
     __syncthreads();
-    mlp_logits<DT>(h2, L.ld2, TE, pol.H2, W3, b3, NA, lg, MAX_NA, wave, NTHREADS / 64, lane);
+    mlp_logits<DT>(h2, L.ld2, TE, pol.H2, W3, b3, NA, lg, MAX_NA, wave, NW, lane);
     __syncthreads();
     for (int idx = tid; idx < te_valid * NA; idx += NTHREADS) {
       const int el = idx / NA, a = idx - el * NA;
@@ -216,6 +255,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
       }
     }
     __syncthreads();
+    uint32_t d = 0;
     if (envlane) {
       int best = 0;
       float bs = -INFINITY;
@@ -231,21 +271,32 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
         out.actions[((size_t)k * E + e) * 2 + 1 - s.cur] = 0;
       }
       float r;
-      uint32_t d;
       hn_transition(p, s, best, r, d);
-      if (d) hn_reset(p, (uint64_t)(p.env_base + e), t + 1, s, decks + tid * HN_DECK_SLOT);
-      hn_publish(s, envs[tid]);
-      rows[tid] = 2 * tid + s.cur;
+      need[tid] = d;
+      if (!d) {
+        hn_publish(s, envs[tid]);
+        rows[tid] = 2 * tid + s.cur;
+      }
       if (out.reward) out.reward[(size_t)k * E + e] = r;
       if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
+    }
+    hn_flag_any(need, TE, d, wave, lane);
+    __syncthreads();
+    if (need[TE]) {
+      hn_shuffle_flagged<NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
+      __syncthreads();
+      if (d) {
+        hn_deal(s, words[tid]);
+        hn_publish(s, envs[tid]);
+        rows[tid] = 2 * tid + s.cur;
+      }
     }
   }
   __syncthreads();
   if (out.obs_last) {
-    hn_paint<T, TE, NTHREADS>(envs, te_valid, xs, L.ldx, tid);
+    hn_paint<T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
-    hn_copy_rows<T, NTHREADS>(xs, L.ldx, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * HN_OBS, HN_OBS,
-                              2 * te_valid, tid);
+    hn_copy_rows<T, LDX, NTHREADS>(xs, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * HN_OBS, 2 * te_valid, tid);
   }
   if (envlane) hn_store(state, E, e, s);
 }
@@ -281,7 +332,7 @@ hipError_t launch_hn_run(const HnParams& p, const PolicyArgs& pol, int32_t* stat
                          const TrajArgs& out, hipStream_t s) {
   const size_t lds = hn_run_lds_bytes(pol);
   const void* fn = pol.dt == DT_F32 ? (const void*)hn_run_kernel<DT_F32> : (const void*)hn_run_kernel<DT_BF16>;
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)MAX_LDS_BYTES);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   if (pol.dt == DT_F32)
     hn_run_kernel<DT_F32><<<hn_tiles(p.E, HN_RUN_TE), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);

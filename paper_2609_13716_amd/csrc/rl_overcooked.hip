@@ -108,24 +108,6 @@ __device__ __forceinline__ void oc_step_lane(const OcParams& p, OcEnv& s, int el
   oc_paint_agents(s, tile, ld, el, true);
 }
 
-// Copy n elements from LDS (16-byte aligned) to global (4-byte aligned):
-// 16-byte stores when the destination allows, 4-byte words otherwise.
-template <typename T>
-__device__ __forceinline__ void copy_tile(const T* src, T* __restrict__ dst, int n, int tid, int nt) {
-  const int nbytes = n * (int)sizeof(T);
-  int done_words = 0;
-  if ((reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
-    const u32x4* s4 = reinterpret_cast<const u32x4*>(src);
-    u32x4* g4 = reinterpret_cast<u32x4*>(dst);
-    const int nq = nbytes >> 4;
-    for (int i = tid; i < nq; i += nt) g4[i] = s4[i];
-    done_words = nq * 4;
-  }
-  const uint32_t* s = reinterpret_cast<const uint32_t*>(src);
-  uint32_t* g = reinterpret_cast<uint32_t*>(dst);
-  for (int i = done_words + tid; i < (nbytes >> 2); i += nt) g[i] = s[i];
-}
-
 // -------------------------------------------------------------- init ----
 
 template <typename OT>
