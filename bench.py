@@ -37,8 +37,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-envs", type=int, default=2048, help="envs in the oracle's timed sample")
-    ap.add_argument("--only", choices=["run_bf16", "run_f32", "env_bf16", "policy_bf16"], default=None,
-                    help="time one kernel only (for profiler runs)")
+    ap.add_argument("--only", choices=["run_bf16", "run_f32", "env_bf16", "policy_bf16", "copy"], default=None,
+                    help="time one kernel only (for profiler runs); 'copy' runs a plain 512 MiB device copy, "
+                         "the reference for scaling HBM byte counters")
     ap.add_argument("--workload-only", default=None,
                     help="time one secondary workload only (lbf12_16k, oc_4096, hn_4096; for profiler runs)")
     ap.add_argument("--no-workloads", action="store_true", help="skip the secondary workloads")
@@ -268,6 +269,16 @@ def main():
     if args.workload_only:
         print(json.dumps(measure_workload(R, workloads, args.workload_only, "bf16", args.steps, args.warmup)),
               flush=True)
+        return
+
+    if args.only == "copy":
+        n = 512 << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"only": "copy", "bytes_read": n, "bytes_written": n}))
         return
 
     if args.only:

@@ -19,7 +19,8 @@ philox    Philox4x64-10 block function and the derived integer draws.
 sampling  Gumbel-max categorical sampling over masked fp32 logits.
 mlp       Per-agent tanh MLP in fp64, with bf16 rounding emulation.
 lbf       Level-Based Foraging: reset, step, observation.
-overcooked, hanabi  the other two environments (where present).
+overcooked  Overcooked-style two-agent kitchen: layout, reset, step, observation.
+hanabi    Two-player Hanabi: deal, legality, step, observation.
 rollout   The rollout loop: observe, act, step, auto-reset.
 
 Environment rules that the paper leaves open (it names the environments and
