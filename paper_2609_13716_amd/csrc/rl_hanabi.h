@@ -321,125 +321,115 @@ __device__ __forceinline__ void hn_store(int32_t* __restrict__ st, int E, int e,
   w(34, s.last);
 }
 
-// What the observation encoder reads of one game (kept in LDS, one per env).
-struct HnView {
-  uint32_t hand[2], kc[2], kr[2], hc[2], hr[2];
-  int n[2];
-  uint32_t fw, disc0, disc1;
-  int info, lives, next, cur;
-  uint32_t last;
-};
+// The observation as a 658-bit vector in eleven 64-bit words (bit f = feature
+// f), built by the game's own lane with whole-field bit operations; every
+// field sits at a compile-time offset.
+constexpr int HN_OBS_WORDS = (HN_OBS + 63) / 64;
 
-__device__ __forceinline__ void hn_view(const HnEnv& s, HnView& v) {
+template <int OFF, int WIDTH>
+__device__ __forceinline__ void hn_deposit(uint64_t (&w)[HN_OBS_WORDS], uint64_t v) {
+  static_assert(WIDTH <= 64 && OFF + WIDTH <= HN_OBS_WORDS * 64, "field");
+  constexpr int i = OFF >> 6, sh = OFF & 63;
+  w[i] |= v << sh;
+  if constexpr (sh + WIDTH > 64) w[i + 1] |= v >> (64 - sh);
+}
+
+__device__ __forceinline__ uint64_t hn_therm(int n, int width) {  // n ones (clamped to width) from bit 0
+  const int k = n < 0 ? 0 : n > width ? width : n;
+  return k >= 64 ? ~0ull : ((1ull << k) - 1ull);
+}
+
+// The 35-bit knowledge field of one card: 25 plausible cards, hinted colour, hinted rank.
+__device__ __forceinline__ uint64_t hn_know_bits(uint32_t kc, uint32_t kr, uint32_t hc, uint32_t hr) {
+  // spread the 5 colour bits to the bottom of 5-bit groups; times the rank mask fills each group
+  uint64_t spread = 0;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    v.hand[i] = s.hand[i];
-    v.kc[i] = s.kc[i];
-    v.kr[i] = s.kr[i];
-    v.hc[i] = s.hc[i];
-    v.hr[i] = s.hr[i];
-    v.n[i] = s.n[i];
-  }
+  for (int c = 0; c < HN_COLOURS; ++c) spread |= (uint64_t)((kc >> c) & 1u) << (5 * c);
+  const uint64_t plaus = spread * (uint64_t)kr;
+  const uint64_t hcol = hc ? (1ull << (hc - 1)) : 0ull;
+  const uint64_t hrank = hr ? (1ull << (hr - 1)) : 0ull;
+  return plaus | (hcol << 25) | (hrank << 30);
+}
+
+__device__ __forceinline__ void hn_obs_bits(const HnEnv& s, int me, uint64_t (&w)[HN_OBS_WORDS]) {
+#pragma unroll
+  for (int i = 0; i < HN_OBS_WORDS; ++i) w[i] = 0;
+  // player-indexed fields as seen by `me`: index 0 the observer, 1 its partner
+  // (selects: a register array indexed at run time would live in scratch)
+  struct {
+    uint32_t hand[2], kc[2], kr[2], hc[2], hr[2];
+    int n[2];
+    uint32_t fw, disc0, disc1, last;
+    int info, lives, next;
+  } v;
+  const bool sw = me == 1;
+  v.hand[0] = sw ? s.hand[1] : s.hand[0];
+  v.hand[1] = sw ? s.hand[0] : s.hand[1];
+  v.kc[0] = sw ? s.kc[1] : s.kc[0];
+  v.kc[1] = sw ? s.kc[0] : s.kc[1];
+  v.kr[0] = sw ? s.kr[1] : s.kr[0];
+  v.kr[1] = sw ? s.kr[0] : s.kr[1];
+  v.hc[0] = sw ? s.hc[1] : s.hc[0];
+  v.hc[1] = sw ? s.hc[0] : s.hc[1];
+  v.hr[0] = sw ? s.hr[1] : s.hr[0];
+  v.hr[1] = sw ? s.hr[0] : s.hr[1];
+  v.n[0] = sw ? s.n[1] : s.n[0];
+  v.n[1] = sw ? s.n[0] : s.n[1];
   v.fw = s.fw;
   v.disc0 = s.disc0;
   v.disc1 = s.disc1;
+  v.last = s.last;
   v.info = s.info;
   v.lives = s.lives;
   v.next = s.next;
-  v.cur = s.cur;
-  v.last = s.last;
-}
-
-// The view of a wave-uniform env as seen by player `me`, in scalar registers:
-// player-indexed fields are reordered so that index 0 is the observer and 1
-// its partner (by selects: a register array indexed at run time would live
-// in scratch memory).
-__device__ __forceinline__ HnView hn_view_oriented(const HnView& v, int me) {
-  auto u = [](uint32_t x) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)x); };
-  auto i = [](int x) { return __builtin_amdgcn_readfirstlane(x); };
-  const bool sw = me == 1;
-  HnView r;
-  r.hand[0] = u(sw ? v.hand[1] : v.hand[0]);
-  r.hand[1] = u(sw ? v.hand[0] : v.hand[1]);
-  r.kc[0] = u(sw ? v.kc[1] : v.kc[0]);
-  r.kc[1] = u(sw ? v.kc[0] : v.kc[1]);
-  r.kr[0] = u(sw ? v.kr[1] : v.kr[0]);
-  r.kr[1] = u(sw ? v.kr[0] : v.kr[1]);
-  r.hc[0] = u(sw ? v.hc[1] : v.hc[0]);
-  r.hc[1] = u(sw ? v.hc[0] : v.hc[1]);
-  r.hr[0] = u(sw ? v.hr[1] : v.hr[0]);
-  r.hr[1] = u(sw ? v.hr[0] : v.hr[1]);
-  r.n[0] = i(sw ? v.n[1] : v.n[0]);
-  r.n[1] = i(sw ? v.n[0] : v.n[1]);
-  r.fw = u(v.fw);
-  r.disc0 = u(v.disc0);
-  r.disc1 = u(v.disc1);
-  r.info = i(v.info);
-  r.lives = i(v.lives);
-  r.next = i(v.next);
-  r.cur = i(v.cur);
-  r.last = u(v.last);
-  return r;
-}
-
-// Feature f (0..657) of the observation of player `me`, as 0 or 1, from the
-// view oriented for `me` (hn_view_oriented).
-__device__ __forceinline__ uint32_t hn_feature(const HnView& v, int me, int f) {
-  if (f < 125) {  // partner hand
-    const int slot = f / 25, c = f - slot * 25;
-    return (slot < v.n[1] && (int)hn_field(v.hand[1], 5, slot) == c) ? 1u : 0u;
+  // partner hand: 5 slots x 25-bit one-hot of the card
+#define HN_PARTNER_SLOT(S)                                                                                  \
+  hn_deposit<25 * (S), 25>(w, (S) < v.n[1] ? (1ull << hn_field(v.hand[1], 5, (S))) : 0ull);
+  HN_PARTNER_SLOT(0) HN_PARTNER_SLOT(1) HN_PARTNER_SLOT(2) HN_PARTNER_SLOT(3) HN_PARTNER_SLOT(4)
+#undef HN_PARTNER_SLOT
+  hn_deposit<125, 2>(w, (v.n[0] < HN_HAND ? 1ull : 0ull) | (v.n[1] < HN_HAND ? 2ull : 0ull));
+  hn_deposit<127, 40>(w, hn_therm(HN_CARDS - v.next, 40));
+  uint64_t fw = 0;
+#pragma unroll
+  for (int c = 0; c < HN_COLOURS; ++c) {
+    const uint32_t h = hn_field(v.fw, 3, c);
+    fw |= h ? (1ull << (5 * c + h - 1)) : 0ull;
   }
-  f -= 125;
-  if (f < 2) return (f == 0 ? v.n[0] : v.n[1]) < HN_HAND ? 1u : 0u;
-  f -= 2;
-  if (f < 40) return HN_CARDS - v.next > f ? 1u : 0u;
-  f -= 40;
-  if (f < 25) {
-    const int c = f / 5, r = f - c * 5;
-    return (int)hn_field(v.fw, 3, c) == r + 1 ? 1u : 0u;
+  hn_deposit<167, 25>(w, fw);
+  hn_deposit<192, 8>(w, hn_therm(v.info, 8));
+  hn_deposit<200, 3>(w, hn_therm(v.lives, 3));
+  uint64_t disc = 0;  // per card id, a thermometer as long as its copies (3,2,2,2,1 per colour)
+#pragma unroll
+  for (int card = 0; card < HN_KINDS; ++card) {
+    const int r = card % HN_RANKS, c = card / HN_RANKS;
+    const int off = c * 10 + (r == 0 ? 0 : 2 * r + 1), copies = r == 0 ? 3 : r == 4 ? 1 : 2;
+    const uint32_t cnt = card < 16 ? (v.disc0 >> (2 * card)) & 3u : (v.disc1 >> (2 * (card - 16))) & 3u;
+    disc |= hn_therm((int)cnt, copies) << off;
   }
-  f -= 25;
-  if (f < 8) return v.info > f ? 1u : 0u;
-  f -= 8;
-  if (f < 3) return v.lives > f ? 1u : 0u;
-  f -= 3;
-  if (f < 50) {
-    const int c = f / 10, o = f - c * 10;
-    const int r = o < 3 ? 0 : o < 5 ? 1 : o < 7 ? 2 : o < 9 ? 3 : 4;
-    const int start = r == 0 ? 0 : 2 * r + 1;
-    const int card = c * HN_RANKS + r;
-    const int cnt = card < 16 ? (int)((v.disc0 >> (2 * card)) & 3u) : (int)((v.disc1 >> (2 * (card - 16))) & 3u);
-    return cnt > o - start ? 1u : 0u;
-  }
-  f -= 50;
-  if (f < 55) {
-    const uint32_t L = v.last;
-    if (!(L & 1u)) return 0u;
+  hn_deposit<203, 50>(w, disc);
+  const uint32_t L = v.last;
+  if (L & 1u) {  // last move: 2 + 4 + 2 + 5 + 5 + 5 + 5 bits, then the card (25), success, token
     const int actor = (int)((L >> 1) & 1u), kind = (int)((L >> 2) & 3u), target = (int)((L >> 4) & 1u);
-    const bool hint = kind >= HN_HINT_COLOUR;
-    if (f < 2) return f == ((actor - me) & 1) ? 1u : 0u;
-    if (f < 6) return f - 2 == kind ? 1u : 0u;
-    if (f < 8) return (hint && f - 6 == ((target - me) & 1)) ? 1u : 0u;
-    if (f < 13) return (int)((L >> 5) & 7u) == f - 8 + 1 ? 1u : 0u;   // hinted colour (0 when none)
-    if (f < 18) return (int)((L >> 8) & 7u) == f - 13 + 1 ? 1u : 0u;  // hinted rank
-    if (f < 23) return (L >> (11 + f - 18)) & 1u;                     // revealed slots
-    if (f < 28) return (int)((L >> 16) & 7u) == f - 23 + 1 ? 1u : 0u; // acted slot
-    if (f < 53) return (int)((L >> 19) & 31u) == f - 28 + 1 ? 1u : 0u;
-    return (L >> (24 + f - 53)) & 1u;                                 // success, token
+    const uint32_t hcol = (L >> 5) & 7u, hrank = (L >> 8) & 7u, slot = (L >> 16) & 7u, card = (L >> 19) & 31u;
+    uint64_t a = (1ull << ((actor - me) & 1)) | (1ull << (2 + kind));
+    if (kind >= HN_HINT_COLOUR) a |= 1ull << (6 + ((target - me) & 1));
+    if (hcol) a |= 1ull << (8 + hcol - 1);
+    if (hrank) a |= 1ull << (13 + hrank - 1);
+    a |= (uint64_t)((L >> 11) & 31u) << 18;
+    if (slot) a |= 1ull << (23 + slot - 1);
+    if (card) a |= 1ull << (28 + card - 1);
+    a |= (uint64_t)((L >> 24) & 3u) << 53;
+    hn_deposit<253, 55>(w, a);
   }
-  f -= 55;
-  {
-    const int j = f / 175, rem = f - j * 175;  // j = 0: the observer's hand, 1: the partner's
-    const int slot = rem / 35, g = rem - slot * 35;
-    if (slot >= (j ? v.n[1] : v.n[0])) return 0u;
-    if (g < 25) {
-      const int c = g / 5, r = g - c * 5;
-      const uint32_t kc = j ? v.kc[1] : v.kc[0], kr = j ? v.kr[1] : v.kr[0];
-      return ((hn_field(kc, 5, slot) >> c) & (hn_field(kr, 5, slot) >> r) & 1u);
-    }
-    if (g < 30) return (int)hn_field(j ? v.hc[1] : v.hc[0], 3, slot) == g - 25 + 1 ? 1u : 0u;
-    return (int)hn_field(j ? v.hr[1] : v.hr[0], 3, slot) == g - 30 + 1 ? 1u : 0u;
-  }
+  // knowledge: the observer's hand, then the partner's, 5 slots x 35 bits each
+#define HN_KNOW_SLOT(J, S)                                                                                  \
+  hn_deposit<308 + 175 * (J) + 35 * (S), 35>(                                                               \
+      w, (S) < v.n[J] ? hn_know_bits(hn_field(v.kc[J], 5, (S)), hn_field(v.kr[J], 5, (S)),                  \
+                                     hn_field(v.hc[J], 3, (S)), hn_field(v.hr[J], 3, (S)))                  \
+                      : 0ull);
+  HN_KNOW_SLOT(0, 0) HN_KNOW_SLOT(0, 1) HN_KNOW_SLOT(0, 2) HN_KNOW_SLOT(0, 3) HN_KNOW_SLOT(0, 4)
+  HN_KNOW_SLOT(1, 0) HN_KNOW_SLOT(1, 1) HN_KNOW_SLOT(1, 2) HN_KNOW_SLOT(1, 3) HN_KNOW_SLOT(1, 4)
+#undef HN_KNOW_SLOT
 }
 
 }  // namespace rl

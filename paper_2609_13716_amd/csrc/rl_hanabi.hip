@@ -2,11 +2,10 @@
 // actions, and the fused rollout.
 //
 // Env lane e of wave 0 holds its game in registers (rl_hanabi.h).  After
-// every move it publishes what the observation reads (HnView) and the
-// mover's legal-action mask to LDS; then all threads of the workgroup paint
-// the two 658-feature observations of every env of the tile, feature-parallel
-// (consecutive lanes take consecutive features of one row), into an LDS tile
-// that is copied to the trajectory.  In the fused rollout only the mover's
+// every move it builds both players' 658-feature observations as bit vectors
+// and publishes them with the mover's legal-action mask to LDS; then all
+// waves expand the bits into an LDS tile (consecutive lanes take consecutive
+// features of one row) that is copied to the trajectory.  In the fused rollout only the mover's
 // row goes through the policy (the other player has no legal action): its
 // rows are gathered from the tile by index, and the MLP is the streaming
 // MFMA MLP of rl_mlp.h.  When games end, the waves shuffle the new decks
@@ -18,20 +17,25 @@
 namespace rl {
 
 struct HnTile {
-  HnView view;
-  uint32_t legal;  // mover's 20-bit legal mask
+  uint64_t bits[2][HN_OBS_WORDS];  // both players' observations as bit vectors
+  int cur;                         // the player to move
+  uint32_t legal;                  // mover's 20-bit legal mask
 };
 
-// Paint rows 2*el + me (el < te_valid) of the observation tile, one row per
-// wave at a time: the row's game view is read once into scalar registers and
-// the wave's lanes take 64 consecutive features per pass.
+// Paint rows 2*el + me (el < te_valid) of the observation tile from the
+// published bit vectors: one row per wave at a time, lane l writes features
+// l, l + 64, ...
 template <typename T, int NW>
 __device__ __forceinline__ void hn_paint(const HnTile* __restrict__ envs, int te_valid, T* tile, int ld, int wave,
                                          int lane) {
   for (int r = wave; r < 2 * te_valid; r += NW) {
-    const HnView v = hn_view_oriented(envs[r >> 1].view, r & 1);
+    const uint64_t* w = envs[r >> 1].bits[r & 1];
     T* row = tile + (size_t)r * ld;
-    for (int f = lane; f < HN_OBS; f += 64) row[f] = small_int_to<T>(hn_feature(v, r & 1, f));
+#pragma unroll
+    for (int i = 0; i < HN_OBS_WORDS; ++i) {
+      const int f = 64 * i + lane;
+      if (f < HN_OBS) row[f] = small_int_to<T>((uint32_t)(w[i] >> lane) & 1u);
+    }
   }
 }
 
@@ -54,12 +58,21 @@ __device__ __forceinline__ void hn_write_legal(const HnTile* __restrict__ envs, 
                                                int tid) {
   for (int i = tid; i < te_valid * 2 * HN_NACT; i += NT) {
     const int el = i / (2 * HN_NACT), rem = i - el * 2 * HN_NACT, ag = rem / HN_NACT, a = rem - ag * HN_NACT;
-    g[i] = (ag == envs[el].view.cur) ? (uint8_t)((envs[el].legal >> a) & 1u) : (uint8_t)0;
+    g[i] = (ag == envs[el].cur) ? (uint8_t)((envs[el].legal >> a) & 1u) : (uint8_t)0;
   }
 }
 
+// What the workgroup reads of a game after each move: both observations as
+// bit vectors, the mover and its legal actions.
 __device__ __forceinline__ void hn_publish(const HnEnv& s, HnTile& t) {
-  hn_view(s, t.view);
+#pragma unroll
+  for (int me = 0; me < 2; ++me) {
+    uint64_t w[HN_OBS_WORDS];
+    hn_obs_bits(s, me, w);
+#pragma unroll
+    for (int i = 0; i < HN_OBS_WORDS; ++i) t.bits[me][i] = w[i];
+  }
+  t.cur = s.cur;
   t.legal = hn_legal(s);
 }
 
@@ -156,7 +169,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
       copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * HN_OBS, 2 * te_valid * HN_OBS, tid, NTHREADS);
     }
     if (legal) hn_write_legal<NTHREADS>(envs, te_valid, legal + ((size_t)k * E + e0) * 2 * HN_NACT, tid);
-    __syncthreads();  // the tile, views and masks are read before the next move rewrites them
+    __syncthreads();  // the tile and masks are read before the next move rewrites them
   }
   if (envlane) hn_store(state, E, e, s);
 }
@@ -182,6 +195,7 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt) {
   L.off_h2 = o;    o += (size_t)HN_RUN_TE * L.ld2 * es;
   L.off_lg = o;    o += (size_t)HN_RUN_TE * MAX_NA * 4;
   L.off_sc = o;    o += (size_t)HN_RUN_TE * MAX_NA * 4;
+  o = (o + 15) & ~(size_t)15;
   L.off_env = o;   o += (size_t)HN_RUN_TE * sizeof(HnTile);
   L.off_words = o; o += (size_t)HN_RUN_TE * HN_DECK_WORDS * 4;
   L.off_need = o;  o += (size_t)(HN_RUN_TE + 1) * 4;
@@ -230,13 +244,13 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
   if (tid < TE) rows[tid] = 2 * tid + (envlane ? s.cur : 0);  // the mover's row (a zero row for padding)
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
-    __syncthreads();  // the previous move's views are published
+    __syncthreads();  // the previous move's observations are published
     hn_paint<T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
     if (out.obs)
       hn_copy_rows<T, LDX, NTHREADS>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * HN_OBS,
                                      2 * te_valid, tid);
-    mlp_hidden_rows<DT>(xs, LDX, rows, TE, HN_OBS, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane);
+    mlp_input_layer_const<DT, HN_OBS>(xs, LDX, rows, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane);
     __syncthreads();
     mlp_hidden<DT>(h1, L.ld1, TE, pol.H1, W2, b2, pol.H2, h2, L.ld2, wave, NW, lane);
     __syncthreads();
@@ -244,7 +258,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
     __syncthreads();
     for (int idx = tid; idx < te_valid * NA; idx += NTHREADS) {
       const int el = idx / NA, a = idx - el * NA;
-      const int cur = envs[el].view.cur;
+      const int cur = envs[el].cur;
       const bool ok = (envs[el].legal >> a) & 1u;
       const float g = action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t, cur, a);
       sc[el * MAX_NA + a] = action_score(lg[el * MAX_NA + a], g, ok);

@@ -316,7 +316,7 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
     // o_t -> LDS operand tile (+ trajectory)
     lbf_encode<T>(p, m, te_valid, L, gobs ? gobs + ((size_t)k * p.E + e0) * A * D : nullptr, xs, RL.ldx, tid);
     __syncthreads();
-    mlp_hidden<DT>(xs, RL.ldx, R, D, W1, b1, pol.H1, h1, RL.ld1, wave, NTHREADS / 64, lane);
+    mlp_input_layer<DT>(xs, RL.ldx, nullptr, R, D, W1, b1, pol.H1, h1, RL.ld1, wave, NTHREADS / 64, lane);
     __syncthreads();
     mlp_hidden<DT>(h1, RL.ld1, R, pol.H1, W2, b2, pol.H2, h2, RL.ld2, wave, NTHREADS / 64, lane);
     __syncthreads();

@@ -126,193 +126,234 @@ __device__ __forceinline__ f32x4 mfma_step(u32x4 a, u32x4 b, f32x4 acc) {
                                                  0, 0, 0);
 }
 
-// G adjacent 16 x 16 output tiles of the same 16 rows:
-// acc[g] = A[16 rows, 0:Kpad] * W[n0+16g : n0+16g+16, 0:Kpad]^T, where `a_row`
-// points at element 0 of A row (lane % 16).  The k-steps inside K run
-// branch-free (unconditional weight loads, output rows past N read row 0 and
-// are zeroed after the load) so that the loads of several steps and tiles
-// are in flight together; the one partial step at the end is guarded.  Each
-// tile's sum runs over k in the same order for every G, so results do not
-// depend on G.
-template <int DT, int G, int AL>
-__device__ __forceinline__ void mma_tiles_row(const typename DType<DT>::T* __restrict__ a_row, int Kpad, int K,
-                                              const typename DType<DT>::T* __restrict__ W, int n0, int N, int lane,
-                                              f32x4 (&acc)[G]) {
+// MT x G output tiles of 16 x 16: rows of MT row tiles against G adjacent
+// output-column tiles, acc[m][g] = A_m[16 rows, 0:Kpad] * W[n0+16g .. +16, 0:Kpad]^T,
+// where a_row[m] points at element 0 of this lane's A row (lane % 16) in row
+// tile m.  Every weight fragment loaded from L2 feeds MT MFMAs (one per row
+// tile) and every activation fragment G.  The k-steps inside K run
+// branch-free (unconditional weight loads; output rows past N read row 0 and
+// are zeroed after the load) and software-pipelined: a ring of PF k-steps'
+// weight fragments is in flight, each slot consumed and then refilled in
+// place, so loads overlap the MFMAs of earlier steps without register copies.
+// The loop is kept rolled (these kernels run many different phases per step
+// and must stay within the instruction cache).  The one partial step at the
+// end is guarded.  Each tile's sum runs over k in the same order whatever G
+// and MT are, so results do not depend on them.
+template <int DT, int G, int MT, int AL>
+__device__ __forceinline__ void mma_tiles(const typename DType<DT>::T* const (&a_row)[MT], int Kpad, int K,
+                                          const typename DType<DT>::T* __restrict__ W, int n0, int N, int lane,
+                                          f32x4 (&acc)[MT][G]) {
   using T = typename DType<DT>::T;
   using BT = typename std::conditional<DT == DT_F32, float, u32x4>::type;
   constexpr int KS = DType<DT>::KS;
   constexpr int KL = DT == DT_F32 ? 1 : 8;  // k values per lane per step
+  constexpr int PF = G >= 4 ? 2 : 4;        // k-steps of weights in flight
   const T* wrow[G];
   bool nok[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int n = n0 + 16 * g + (lane & 15);
     nok[g] = n < N;
     wrow[g] = W + (size_t)(nok[g] ? n : 0) * K + (lane >> 4) * KL;
   }
-  const T* arow = a_row + (lane >> 4) * KL;
-  const int kfull = K / KS * KS;
-  auto a_at = [&](int k0) -> BT {
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[m][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int koff = (lane >> 4) * KL;
+  auto a_at = [&](int m, int k0) -> BT {
     if constexpr (DT == DT_F32)
-      return arow[k0];
+      return a_row[m][koff + k0];
     else
-      return *reinterpret_cast<const u32x4*>(arow + k0);
+      return *reinterpret_cast<const u32x4*>(a_row[m] + koff + k0);
   };
-#pragma unroll(G >= 4 ? 2 : 4)
-  for (int k0 = 0; k0 < kfull; k0 += KS) {
-    const BT a = a_at(k0);
+  auto b_at = [&](int g, int k0) -> BT {
+    if constexpr (DT == DT_F32)
+      return wrow[g][k0];
+    else
+      return load_w8<AL>(wrow[g] + k0);
+  };
+  auto mfma_all = [&](int k0, const BT (&b)[G]) {
+    BT a[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) a[m] = a_at(m, k0);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      BT bg;
+      if constexpr (DT == DT_F32)
+        bg = nok[g] ? b[g] : 0.f;
+      else
+        bg = nok[g] ? b[g] : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[m][g] = mfma_step(a[m], bg, acc[m][g]);
+    }
+  };
+  const int nsteps = K / KS, nmain = nsteps / PF * PF;
+  if (nmain > 0) {
+    BT ring[PF][G];
+#pragma unroll
+    for (int u = 0; u < PF; ++u)
+#pragma unroll
+      for (int g = 0; g < G; ++g) ring[u][g] = b_at(g, u * KS);
+#pragma nounroll
+    for (int s0 = 0; s0 < nmain; s0 += PF) {
+#pragma unroll
+      for (int u = 0; u < PF; ++u) {
+        mfma_all((s0 + u) * KS, ring[u]);
+        const int nxt = min(s0 + PF + u, nmain - 1) * KS;  // past the end: reload the last step (unused)
+#pragma unroll
+        for (int g = 0; g < G; ++g) ring[u][g] = b_at(g, nxt);
+      }
+    }
+  }
+  for (int st = nmain; st < nsteps; ++st) {  // full steps left over from the pipelined groups
     BT b[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      if constexpr (DT == DT_F32)
-        b[g] = wrow[g][k0];
-      else
-        b[g] = load_w8<AL>(wrow[g] + k0);
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      if constexpr (DT == DT_F32)
-        b[g] = nok[g] ? b[g] : 0.f;
-      else
-        b[g] = nok[g] ? b[g] : u32x4{0u, 0u, 0u, 0u};
-      acc[g] = mfma_step(a, b[g], acc[g]);
-    }
+    for (int g = 0; g < G; ++g) b[g] = b_at(g, st * KS);
+    mfma_all(st * KS, b);
   }
-  if (kfull < Kpad) {  // the partial last step
-    const int k0 = kfull, kk = k0 + (lane >> 4) * KL;
-    const BT a = a_at(k0);
+  if (nsteps * KS < Kpad) {  // the partial last step
+    const int k0 = nsteps * KS, kk = k0 + koff;
+    BT b[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      BT b = load_b_tail<DT>(wrow[g], k0, kk, K);
-      if constexpr (DT == DT_F32)
-        b = nok[g] ? b : 0.f;
-      else
-        b = nok[g] ? b : u32x4{0u, 0u, 0u, 0u};
-      acc[g] = mfma_step(a, b, acc[g]);
-    }
+    for (int g = 0; g < G; ++g) b[g] = load_b_tail<DT>(wrow[g], k0, kk, K);
+    mfma_all(k0, b);
   }
 }
 
-// One tile (G = 1).
-template <int DT>
-__device__ __forceinline__ f32x4 mma_tile_row(const typename DType<DT>::T* __restrict__ a_row, int Kpad, int K,
-                                              const typename DType<DT>::T* __restrict__ W, int n0, int N,
-                                              int lane) {
-  f32x4 acc[1];
-  if (DT == DT_F32 || weight_align(K) == WALIGN_16)
-    mma_tiles_row<DT, 1, WALIGN_16>(a_row, Kpad, K, W, n0, N, lane, acc);
-  else if (weight_align(K) == WALIGN_4)
-    mma_tiles_row<DT, 1, WALIGN_4>(a_row, Kpad, K, W, n0, N, lane, acc);
-  else
-    mma_tiles_row<DT, 1, WALIGN_2>(a_row, Kpad, K, W, n0, N, lane, acc);
-  return acc[0];
-}
-
-// The same tile for rows m0..m0+15 of a row-major A with leading dimension lda.
-template <int DT>
-__device__ __forceinline__ f32x4 mma_tile(const typename DType<DT>::T* __restrict__ in, int lda, int m0,
-                                          int Kpad, int K, const typename DType<DT>::T* __restrict__ W,
-                                          int n0, int N, int lane) {
-  return mma_tile_row<DT>(in + (size_t)(m0 + (lane & 15)) * lda, Kpad, K, W, n0, N, lane);
-}
-
-// A dense layer over R rows (a multiple of 16) in groups of G output tiles
-// per wave.  Row r of the input is in[rows ? rows[r] : r].  Hidden layers
-// (LOGITS false) store tanh(x W^T + b) in the layer dtype to `out`; the
-// output layer stores x W^T + b as float32 to `logits` (columns < N only).
-template <int DT, int G, int AL, bool LOGITS>
-__device__ __forceinline__ void mlp_layer_g(const typename DType<DT>::T* in, int lda, const int* rows, int R, int K,
+// A dense layer over R = 16 * MT rows in groups of G output tiles per wave;
+// each wave's work item covers all MT row tiles.  Row r of the input is
+// in[rows ? rows[r] : r].  Hidden layers (LOGITS false) store
+// tanh(x W^T + b) in the layer dtype to `out`; the output layer stores
+// x W^T + b as float32 to `logits` (columns < N only).
+template <int DT, int G, int MT, int AL, bool LOGITS>
+__device__ __forceinline__ void mlp_layer_g(const typename DType<DT>::T* in, int lda, const int* rows, int K,
                                             const typename DType<DT>::T* __restrict__ W,
                                             const typename DType<DT>::T* __restrict__ b, int N,
                                             typename DType<DT>::T* out, float* logits, int ldo, int wave, int nwaves,
                                             int lane) {
+  using T = typename DType<DT>::T;
   using DTy = DType<DT>;
   const int Kpad = round_up(K, DTy::KS);
-  const int mt = R >> 4, nt = (N + 15) >> 4, ng = (nt + G - 1) / G;
-  for (int item = wave; item < mt * ng; item += nwaves) {
-    const int m0 = (item / ng) << 4, n0 = (item % ng) * 16 * G;
-    const int r = m0 + (lane & 15);
-    f32x4 acc[G];
-    mma_tiles_row<DT, G, AL>(in + (size_t)(rows ? rows[r] : r) * lda, Kpad, K, W, n0, N, lane, acc);
+  const int nt = (N + 15) >> 4, ng = (nt + G - 1) / G;
+  const T* a_row[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const int r = 16 * m + (lane & 15);
+    a_row[m] = in + (size_t)(rows ? rows[r] : r) * lda;
+  }
+  for (int item = wave; item < ng; item += nwaves) {
+    const int n0 = item * 16 * G;
+    float bias[G];  // loaded before the k loop so that its latency hides behind the MFMAs
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int col = n0 + 16 * g + (lane & 15);
+      bias[g] = DTy::to_f32(b[col < N ? col : 0]);
+    }
+    f32x4 acc[MT][G];
+    mma_tiles<DT, G, MT, AL>(a_row, Kpad, K, W, n0, N, lane, acc);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const int col = n0 + 16 * g + (lane & 15);
       if (col < N) {
-        const float bias = DTy::to_f32(b[col]);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = m0 + 4 * (lane >> 4) + q;
-          if constexpr (LOGITS)
-            logits[(size_t)row * ldo + col] = acc[g][q] + bias;
-          else
-            out[(size_t)row * ldo + col] = DTy::from_f32(fast_tanh(acc[g][q] + bias));
-        }
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = 16 * m + 4 * (lane >> 4) + q;
+            if constexpr (LOGITS)
+              logits[(size_t)row * ldo + col] = acc[m][g][q] + bias[g];
+            else
+              out[(size_t)row * ldo + col] = DTy::from_f32(fast_tanh(acc[m][g][q] + bias[g]));
+          }
       }
     }
   }
 }
 
+template <int DT, int MT, int AL, bool LOGITS>
+__device__ __forceinline__ void mlp_layer_mt(const typename DType<DT>::T* in, int lda, const int* rows, int K,
+                                             const typename DType<DT>::T* __restrict__ W,
+                                             const typename DType<DT>::T* __restrict__ b, int N,
+                                             typename DType<DT>::T* out, float* logits, int ldo, int wave,
+                                             int nwaves, int lane) {
+  const int nt = (N + 15) >> 4;
+  if (nt >= 4 * nwaves && nt % 4 == 0)
+    mlp_layer_g<DT, 4, MT, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+  else if (nt >= 2 * nwaves && nt % 2 == 0)
+    mlp_layer_g<DT, 2, MT, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+  else
+    mlp_layer_g<DT, 1, MT, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+}
+
+// Picks the row-tile count (R = 16, 32, 48 or 64) and the widest tile group
+// that still gives every wave work.
 template <int DT, int AL, bool LOGITS>
 __device__ __forceinline__ void mlp_layer_al(const typename DType<DT>::T* in, int lda, const int* rows, int R, int K,
                                              const typename DType<DT>::T* __restrict__ W,
                                              const typename DType<DT>::T* __restrict__ b, int N,
                                              typename DType<DT>::T* out, float* logits, int ldo, int wave,
                                              int nwaves, int lane) {
-  const int tiles = (R >> 4) * ((N + 15) >> 4);
-  if (tiles >= 4 * nwaves && ((N + 15) >> 4) % 4 == 0)
-    mlp_layer_g<DT, 4, AL, LOGITS>(in, lda, rows, R, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
-  else if (tiles >= 2 * nwaves && ((N + 15) >> 4) % 2 == 0)
-    mlp_layer_g<DT, 2, AL, LOGITS>(in, lda, rows, R, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
-  else
-    mlp_layer_g<DT, 1, AL, LOGITS>(in, lda, rows, R, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+  switch (R >> 4) {
+    case 1:
+      mlp_layer_mt<DT, 1, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+      break;
+    case 2:
+      mlp_layer_mt<DT, 2, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+      break;
+    case 3:
+      mlp_layer_mt<DT, 3, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+      break;
+    default:
+      mlp_layer_mt<DT, 4, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+  }
 }
 
-// Picks the weight-load width for K and the widest tile group that still
-// gives every wave work.
-template <int DT, bool LOGITS>
-__device__ __forceinline__ void mlp_layer(const typename DType<DT>::T* in, int lda, const int* rows, int R, int K,
-                                          const typename DType<DT>::T* __restrict__ W,
-                                          const typename DType<DT>::T* __restrict__ b, int N,
-                                          typename DType<DT>::T* out, float* logits, int ldo, int wave, int nwaves,
-                                          int lane) {
+// The first layer for any input width K (picks the weight-load width at run time).
+template <int DT>
+__device__ __forceinline__ void mlp_input_layer(const typename DType<DT>::T* in, int lda, const int* rows, int R,
+                                                int K, const typename DType<DT>::T* __restrict__ W,
+                                                const typename DType<DT>::T* __restrict__ b, int N,
+                                                typename DType<DT>::T* out, int ldo, int wave, int nwaves,
+                                                int lane) {
   const int al = DT == DT_F32 ? WALIGN_16 : weight_align(K);
   if (al == WALIGN_16)
-    mlp_layer_al<DT, WALIGN_16, LOGITS>(in, lda, rows, R, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+    mlp_layer_al<DT, WALIGN_16, false>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
   else if (al == WALIGN_4)
-    mlp_layer_al<DT, WALIGN_4, LOGITS>(in, lda, rows, R, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+    mlp_layer_al<DT, WALIGN_4, false>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
   else
-    mlp_layer_al<DT, WALIGN_2, LOGITS>(in, lda, rows, R, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+    mlp_layer_al<DT, WALIGN_2, false>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
 }
 
-// A hidden layer: out = tanh(in W^T + b), stored in the layer dtype.
-// R rows (multiple of 16), N outputs (multiple of 16).
+// The first layer for an input width KC known at compile time.
+template <int DT, int KC>
+__device__ __forceinline__ void mlp_input_layer_const(const typename DType<DT>::T* in, int lda, const int* rows,
+                                                      int R, const typename DType<DT>::T* __restrict__ W,
+                                                      const typename DType<DT>::T* __restrict__ b, int N,
+                                                      typename DType<DT>::T* out, int ldo, int wave, int nwaves,
+                                                      int lane) {
+  constexpr int AL = DT == DT_F32 ? WALIGN_16 : weight_align(KC);
+  mlp_layer_al<DT, AL, false>(in, lda, rows, R, KC, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
+}
+
+// A hidden layer after the first: K (a hidden width) is a multiple of 16.
+// R rows: 16, 32, 48 or 64.
 template <int DT>
 __device__ __forceinline__ void mlp_hidden(const typename DType<DT>::T* in, int lda, int R, int K,
                                            const typename DType<DT>::T* __restrict__ W,
                                            const typename DType<DT>::T* __restrict__ b, int N,
                                            typename DType<DT>::T* out, int ldo, int wave, int nwaves,
                                            int lane) {
-  mlp_layer<DT, false>(in, lda, nullptr, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
+  mlp_layer_al<DT, WALIGN_16, false>(in, lda, nullptr, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
 }
 
-// mlp_hidden over the A rows rows[0..R-1] of `in` (row indices in LDS).
-template <int DT>
-__device__ __forceinline__ void mlp_hidden_rows(const typename DType<DT>::T* in, int lda, const int* rows, int R,
-                                                int K, const typename DType<DT>::T* __restrict__ W,
-                                                const typename DType<DT>::T* __restrict__ b, int N,
-                                                typename DType<DT>::T* out, int ldo, int wave, int nwaves,
-                                                int lane) {
-  mlp_layer<DT, false>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
-}
-
-// The output layer: logits = in W^T + b as float32, N <= 32 actions.
+// The output layer: logits = in W^T + b as float32, N <= 32 actions, K a multiple of 16.
 template <int DT>
 __device__ __forceinline__ void mlp_logits(const typename DType<DT>::T* in, int lda, int R, int K,
                                            const typename DType<DT>::T* __restrict__ W,
                                            const typename DType<DT>::T* __restrict__ b, int N, float* out,
                                            int ldo, int wave, int nwaves, int lane) {
-  mlp_layer<DT, true>(in, lda, nullptr, R, K, W, b, N, nullptr, out, ldo, wave, nwaves, lane);
+  mlp_layer_al<DT, WALIGN_16, true>(in, lda, nullptr, R, K, W, b, N, nullptr, out, ldo, wave, nwaves, lane);
 }
 
 }  // namespace rl

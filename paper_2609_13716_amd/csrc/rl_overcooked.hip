@@ -1,9 +1,9 @@
 // Overcooked-style kitchen kernels: init (layout + first episode), env-only
 // steps with injected actions, and the fused rollout.
 //
-// Each workgroup owns OC_TE envs; env lane e keeps its kitchen in registers
+// Each workgroup owns a tile of envs; env lane e keeps its kitchen in registers
 // (cell sets as 45-bit masks).  Observations live in an LDS tile of
-// 2 * OC_TE rows x 1170 features: the layout planes are painted once (the
+// 2 rows per env x 1170 features: the layout planes are painted once (the
 // kitchen never changes), and each step the env lanes erase and repaint only
 // the features that can change (agents, facings, held items, pots, and the
 // counters whose item changed); the tile is then copied to the trajectory.
@@ -16,7 +16,7 @@
 
 namespace rl {
 
-constexpr int OC_TE = 8;  // envs per workgroup
+constexpr int OC_TE = 8;  // envs per workgroup of the init and env-only kernels (one wave)
 
 template <typename T>
 __device__ __forceinline__ void oc_put(T* xr, int plane, int cell, uint32_t v) {
@@ -172,11 +172,11 @@ __global__ __launch_bounds__(64) void oc_env_kernel(OcParams p, int32_t* __restr
 
 // ----------------------------------------------------- fused rollout ----
 
-template <int DT>
+template <int DT, int TE>
 __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs pol, int32_t* __restrict__ state,
                                                           uint64_t t0, int n_steps, TrajArgs out) {
   using T = typename DType<DT>::T;
-  constexpr int R = OC_TE * 2, NA = OC_NACT;
+  constexpr int R = TE * 2, NA = OC_NACT;
   constexpr int LDX = lds_ld<DT>(OC_D);
   extern __shared__ __align__(16) uint8_t smem[];
   const int ld1 = lds_ld<DT>(pol.H1), ld2 = lds_ld<DT>(pol.H2);
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
   const size_t total = (size_t)((uint8_t*)(act_s + R) - smem);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int e0 = blockIdx.x * OC_TE, te_valid = min(OC_TE, p.E - e0), E = p.E;
+  const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
   const T* W1 = static_cast<const T*>(pol.W[0]);
   const T* W2 = static_cast<const T*>(pol.W[1]);
   const T* W3 = static_cast<const T*>(pol.W[2]);
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
       T* g = static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D;
       for (int r = 0; r < te_valid * 2; ++r) copy_tile(xs + r * LDX, g + (size_t)r * OC_D, OC_D, tid, NTHREADS);
     }
-    mlp_hidden<DT>(xs, LDX, R, OC_D, W1, b1, pol.H1, h1, ld1, wave, NTHREADS / 64, lane);
+    mlp_input_layer_const<DT, OC_D>(xs, LDX, nullptr, R, W1, b1, pol.H1, h1, ld1, wave, NTHREADS / 64, lane);
     __syncthreads();
     mlp_hidden<DT>(h1, ld1, R, pol.H1, W2, b2, pol.H2, h2, ld2, wave, NTHREADS / 64, lane);
     __syncthreads();
@@ -261,10 +261,11 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
 
 // ---------------------------------------------------------- launchers ----
 
-static dim3 oc_tiles(int E) { return dim3((unsigned)((E + OC_TE - 1) / OC_TE)); }
+static dim3 oc_tiles(int E, int te) { return dim3((unsigned)((E + te - 1) / te)); }
 
-size_t oc_run_lds_bytes(const PolicyArgs& pol) {
-  constexpr int R = OC_TE * 2;
+// LDS of the fused kitchen rollout with te envs (2 * te policy rows) per workgroup.
+static size_t oc_run_lds_bytes_te(const PolicyArgs& pol, int te) {
+  const int R = te * 2;
   const size_t es = pol.dt == DT_F32 ? 4 : 2;
   const int ldx = pol.dt == DT_F32 ? lds_ld<DT_F32>(OC_D) : lds_ld<DT_BF16>(OC_D);
   const int ld1 = pol.dt == DT_F32 ? lds_ld<DT_F32>(pol.H1) : lds_ld<DT_BF16>(pol.H1);
@@ -272,40 +273,49 @@ size_t oc_run_lds_bytes(const PolicyArgs& pol) {
   return (size_t)R * (ldx + ld1 + ld2) * es + (size_t)R * MAX_NA * 4 * 2 + (size_t)R * 4;
 }
 
+// 16 envs per workgroup (two row tiles share every weight fragment) when their tiles fit in LDS, else 8.
+static int oc_run_te(const PolicyArgs& pol) { return oc_run_lds_bytes_te(pol, 16) <= MAX_LDS_BYTES ? 16 : 8; }
+
+size_t oc_run_lds_bytes(const PolicyArgs& pol) { return oc_run_lds_bytes_te(pol, oc_run_te(pol)); }
+
 hipError_t launch_oc_init(const OcParams& p, int32_t* state, void* obs, int obs_dt, uint8_t* legal, hipStream_t s) {
   if (obs_dt == DT_F32)
-    oc_init_kernel<float><<<oc_tiles(p.E), 64, 0, s>>>(p, state, static_cast<float*>(obs), legal);
+    oc_init_kernel<float><<<oc_tiles(p.E, OC_TE), 64, 0, s>>>(p, state, static_cast<float*>(obs), legal);
   else
-    oc_init_kernel<uint16_t><<<oc_tiles(p.E), 64, 0, s>>>(p, state, static_cast<uint16_t*>(obs), legal);
+    oc_init_kernel<uint16_t><<<oc_tiles(p.E, OC_TE), 64, 0, s>>>(p, state, static_cast<uint16_t*>(obs), legal);
   return hipGetLastError();
 }
 
 hipError_t launch_oc_step(const OcParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,
                           void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s) {
   if (obs_dt == DT_F32)
-    oc_env_kernel<float><<<oc_tiles(p.E), 64, 0, s>>>(p, state, t0, n_steps, actions, static_cast<float*>(obs), reward,
+    oc_env_kernel<float><<<oc_tiles(p.E, OC_TE), 64, 0, s>>>(p, state, t0, n_steps, actions, static_cast<float*>(obs), reward,
                                                       done, legal);
   else
-    oc_env_kernel<uint16_t><<<oc_tiles(p.E), 64, 0, s>>>(p, state, t0, n_steps, actions, static_cast<uint16_t*>(obs),
+    oc_env_kernel<uint16_t><<<oc_tiles(p.E, OC_TE), 64, 0, s>>>(p, state, t0, n_steps, actions, static_cast<uint16_t*>(obs),
                                                          reward, done, legal);
+  return hipGetLastError();
+}
+
+template <int DT, int TE>
+static hipError_t launch_oc_run_te(const OcParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0,
+                                   int n_steps, const TrajArgs& out, size_t lds, hipStream_t s) {
+  hipError_t e = hipFuncSetAttribute((const void*)oc_run_kernel<DT, TE>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)lds);
+  if (e != hipSuccess) return e;
+  oc_run_kernel<DT, TE><<<oc_tiles(p.E, TE), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
 }
 
 hipError_t launch_oc_run(const OcParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
                          const TrajArgs& out, hipStream_t s) {
-  const size_t lds = oc_run_lds_bytes(pol);
-  if (pol.dt == DT_F32) {
-    hipError_t e = hipFuncSetAttribute((const void*)oc_run_kernel<DT_F32>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)MAX_LDS_BYTES);
-    if (e != hipSuccess) return e;
-    oc_run_kernel<DT_F32><<<oc_tiles(p.E), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
-  } else {
-    hipError_t e = hipFuncSetAttribute((const void*)oc_run_kernel<DT_BF16>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)MAX_LDS_BYTES);
-    if (e != hipSuccess) return e;
-    oc_run_kernel<DT_BF16><<<oc_tiles(p.E), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
-  }
-  return hipGetLastError();
+  const int te = oc_run_te(pol);
+  const size_t lds = oc_run_lds_bytes_te(pol, te);
+  if (pol.dt == DT_F32)
+    return te == 16 ? launch_oc_run_te<DT_F32, 16>(p, pol, state, t0, n_steps, out, lds, s)
+                    : launch_oc_run_te<DT_F32, 8>(p, pol, state, t0, n_steps, out, lds, s);
+  return te == 16 ? launch_oc_run_te<DT_BF16, 16>(p, pol, state, t0, n_steps, out, lds, s)
+                  : launch_oc_run_te<DT_BF16, 8>(p, pol, state, t0, n_steps, out, lds, s);
 }
 
 }  // namespace rl

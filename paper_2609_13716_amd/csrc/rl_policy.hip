@@ -64,7 +64,7 @@ __global__ __launch_bounds__(NTHREADS) void policy_forward_kernel(PolicyArgs pol
   for (int idx = tid; idx < BM * PL.ld1; idx += NTHREADS) h1[idx] = (T)0;
   for (int idx = tid; idx < BM * PL.ld2; idx += NTHREADS) h2[idx] = (T)0;
   __syncthreads();
-  mlp_hidden<DT>(xs, PL.ldx, BM, D, static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), pol.H1, h1,
+  mlp_input_layer<DT>(xs, PL.ldx, nullptr, BM, D, static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), pol.H1, h1,
                  PL.ld1, wave, NTHREADS / 64, lane);
   __syncthreads();
   mlp_hidden<DT>(h1, PL.ld1, BM, pol.H1, static_cast<const T*>(pol.W[1]), static_cast<const T*>(pol.b[1]), pol.H2,
