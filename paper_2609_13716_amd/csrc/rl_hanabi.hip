@@ -135,41 +135,49 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
   __shared__ uint32_t need[TE + 1];  // per env, then "any" at [TE]
   __shared__ uint32_t words[TE][HN_DECK_WORDS];
   __shared__ __align__(16) OT tile[2 * TE * HN_OBS];
+  __shared__ int32_t act_lds[ACT_CHUNK * TE * 2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
   const bool envlane = tid < te_valid;
   const int e = e0 + tid;
   HnEnv s;
   if (envlane) hn_load(state, E, e, s);
-  for (int k = 0; k < n_steps; ++k) {
-    const uint64_t t = t0 + (uint64_t)k;
-    uint32_t d = 0;
-    if (envlane) {
-      float r;
-      hn_transition(p, s, actions[((size_t)k * E + e) * 2 + s.cur], r, d);
-      need[tid] = d;
-      if (!d) hn_publish(s, envs[tid]);
-      if (reward) reward[(size_t)k * E + e] = r;
-      if (done) done[(size_t)k * E + e] = (uint8_t)d;
-    }
-    hn_flag_any(need, TE, d, wave, lane);
+  for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
+    const int nk = min(ACT_CHUNK, n_steps - k0);
+    // no global loads inside the step loop: a load there would wait for every earlier trajectory store
+    stage_actions<TE * 2, NTHREADS>(actions, E, e0, te_valid * 2, 2, k0, nk, act_lds, tid);
     __syncthreads();
-    if (need[TE]) {  // some game of the tile ended: deal new ones drawn at t + 1
-      hn_shuffle_flagged<NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
-      __syncthreads();
-      if (d) {
-        hn_deal(s, words[tid]);
-        hn_publish(s, envs[tid]);
+    for (int kk = 0; kk < nk; ++kk) {
+      const int k = k0 + kk;
+      const uint64_t t = t0 + (uint64_t)k;
+      uint32_t d = 0;
+      if (envlane) {
+        float r;
+        hn_transition(p, s, act_lds[kk * TE * 2 + tid * 2 + s.cur], r, d);
+        need[tid] = d;
+        if (!d) hn_publish(s, envs[tid]);
+        if (reward) reward[(size_t)k * E + e] = r;
+        if (done) done[(size_t)k * E + e] = (uint8_t)d;
       }
+      hn_flag_any(need, TE, d, wave, lane);
       __syncthreads();
+      if (need[TE]) {  // some game of the tile ended: deal new ones drawn at t + 1
+        hn_shuffle_flagged<NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
+        __syncthreads();
+        if (d) {
+          hn_deal(s, words[tid]);
+          hn_publish(s, envs[tid]);
+        }
+        __syncthreads();
+      }
+      if (obs) {
+        hn_paint<OT, NW>(envs, te_valid, tile, HN_OBS, wave, lane);
+        __syncthreads();
+        copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * HN_OBS, 2 * te_valid * HN_OBS, tid, NTHREADS);
+      }
+      if (legal) hn_write_legal<NTHREADS>(envs, te_valid, legal + ((size_t)k * E + e0) * 2 * HN_NACT, tid);
+      __syncthreads();  // the tile and masks are read before the next move rewrites them
     }
-    if (obs) {
-      hn_paint<OT, NW>(envs, te_valid, tile, HN_OBS, wave, lane);
-      __syncthreads();
-      copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * HN_OBS, 2 * te_valid * HN_OBS, tid, NTHREADS);
-    }
-    if (legal) hn_write_legal<NTHREADS>(envs, te_valid, legal + ((size_t)k * E + e0) * 2 * HN_NACT, tid);
-    __syncthreads();  // the tile and masks are read before the next move rewrites them
   }
   if (envlane) hn_store(state, E, e, s);
 }
@@ -247,9 +255,6 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
     __syncthreads();  // the previous move's observations are published
     hn_paint<T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
-    if (out.obs)
-      hn_copy_rows<T, LDX, NTHREADS>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * HN_OBS,
-                                     2 * te_valid, tid);
     mlp_input_layer_const<DT, HN_OBS>(xs, LDX, rows, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane);
     __syncthreads();
     mlp_hidden<DT>(h1, L.ld1, TE, pol.H1, W2, b2, pol.H2, h2, L.ld2, wave, NW, lane);
@@ -268,6 +273,11 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
         lo[(1 - cur) * NA + a] = -INFINITY;
       }
     }
+    // The trajectory copy of o_t is issued after the step's weight loads: a
+    // wave's loads wait for its earlier stores (one in-order counter).
+    if (out.obs)
+      hn_copy_rows<T, LDX, NTHREADS>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * HN_OBS,
+                                     2 * te_valid, tid);
     __syncthreads();
     uint32_t d = 0;
     if (envlane) {

@@ -54,6 +54,21 @@ __device__ __forceinline__ void copy_tile(const T* src, T* __restrict__ dst, int
   for (int i = done_words + tid; i < (nbytes >> 2); i += nt) g[i] = s[i];
 }
 
+// Injected actions are staged through LDS in chunks of this many steps.
+constexpr int ACT_CHUNK = 64;
+
+// Stage the actions of steps k0 .. k0+nk-1 of one env tile into LDS: the
+// tile's `live` contiguous int32 per step (its envs x A agents) go to
+// lds[kk * PER + j]; PER is the full tile's count.
+template <int PER, int NT>
+__device__ __forceinline__ void stage_actions(const int32_t* __restrict__ actions, int E, int e0, int live, int A,
+                                              int k0, int nk, int32_t* lds, int tid) {
+  for (int i = tid; i < nk * PER; i += NT) {
+    const int kk = i / PER, j = i - kk * PER;
+    lds[i] = j < live ? actions[((size_t)(k0 + kk) * E + e0) * A + j] : 0;
+  }
+}
+
 struct PolicyArgs {
   int dt;  // DT_F32 / DT_BF16
   int D, H1, H2, NA;

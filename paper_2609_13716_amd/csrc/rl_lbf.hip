@@ -231,6 +231,7 @@ __global__ __launch_bounds__(NTHREADS) void lbf_step_kernel(LbfParams p, LbfMagi
   __shared__ __align__(16) uint8_t agrid[TILE_E * LBF_MAXCELLS];
   __shared__ __align__(16) uint8_t fgrid[TILE_E * LBF_MAXCELLS];
   __shared__ int acell[TILE_E * LBF_MAXA];
+  __shared__ int32_t act_lds[ACT_CHUNK * TILE_E * LBF_MAXA];
   const LbfLds L{agrid, fgrid, acell};
   const int tid = threadIdx.x;
   const int e0 = blockIdx.x * TILE_E;
@@ -246,26 +247,32 @@ __global__ __launch_bounds__(NTHREADS) void lbf_step_kernel(LbfParams p, LbfMagi
     lbf_load(state, p, e, s);
     lbf_paint(p, s, tid, L, true);
   }
-  for (int k = 0; k < n_steps; ++k) {
-    const uint64_t t = t0 + (uint64_t)k;
-    __syncthreads();  // the encoders of the previous step are done with the grids
-    if (envlane) {
-      int act[LBF_MAXA];
+  for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
+    const int nk = min(ACT_CHUNK, n_steps - k0);
+    __syncthreads();  // the previous chunk's actions are consumed
+    // no global loads inside the step loop: a load there would wait for every earlier trajectory store
+    stage_actions<TILE_E * LBF_MAXA, NTHREADS>(actions, p.E, e0, te_valid * A, A, k0, nk, act_lds, tid);
+    for (int kk = 0; kk < nk; ++kk) {
+      const int k = k0 + kk;
+      const uint64_t t = t0 + (uint64_t)k;
+      __syncthreads();  // the encoders of the previous step are done with the grids (and the actions are staged)
+      if (envlane) {
+        int act[LBF_MAXA];
 #pragma unroll
-      for (int i = 0; i < LBF_MAXA; ++i)
-        act[i] = i < A ? actions[((size_t)k * p.E + e) * A + i] : 0;
-      lbf_paint(p, s, tid, L, false);
-      float r;
-      uint32_t d;
-      lbf_transition(p, s, act, r, d);
-      if (d) lbf_reset(p, (uint64_t)(p.env_base + e), t + 1, s);
-      lbf_paint(p, s, tid, L, true);
-      if (reward) reward[(size_t)k * p.E + e] = r;
-      if (done) done[(size_t)k * p.E + e] = (uint8_t)d;
+        for (int i = 0; i < LBF_MAXA; ++i) act[i] = i < A ? act_lds[kk * TILE_E * LBF_MAXA + tid * A + i] : 0;
+        lbf_paint(p, s, tid, L, false);
+        float r;
+        uint32_t d;
+        lbf_transition(p, s, act, r, d);
+        if (d) lbf_reset(p, (uint64_t)(p.env_base + e), t + 1, s);
+        lbf_paint(p, s, tid, L, true);
+        if (reward) reward[(size_t)k * p.E + e] = r;
+        if (done) done[(size_t)k * p.E + e] = (uint8_t)d;
+      }
+      __syncthreads();
+      if (obs) lbf_encode<OT>(p, m, te_valid, L, obs + ((size_t)k * p.E + e0) * A * p.D, nullptr, 0, tid);
+      if (legal) lbf_write_legal(p, te_valid, legal + ((size_t)k * p.E + e0) * A * LBF_NACT, tid);
     }
-    __syncthreads();
-    if (obs) lbf_encode<OT>(p, m, te_valid, L, obs + ((size_t)k * p.E + e0) * A * p.D, nullptr, 0, tid);
-    if (legal) lbf_write_legal(p, te_valid, legal + ((size_t)k * p.E + e0) * A * LBF_NACT, tid);
   }
   if (envlane) lbf_store(state, p, e, s);
 }
@@ -706,6 +713,7 @@ __global__ __launch_bounds__(64) void lbf_env_kernel(LbfParams p, int32_t* __res
   static_assert(TE <= 64 && TE * nblk <= 64, "one wave");
   __shared__ __align__(16) OT xs[R * D];
   __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];
+  __shared__ int32_t act_lds[ACT_CHUNK * TE * A];
 
   const int lane = threadIdx.x;
   const int e0 = blockIdx.x * TE;
@@ -717,72 +725,56 @@ __global__ __launch_bounds__(64) void lbf_env_kernel(LbfParams p, int32_t* __res
   for (int i = lane; i < R * D; i += 64) xs[i] = (OT)0;
   wave_lds_sync();
   LbfEnv s{};
-  // Two loop-carried action buffers: the actions of step k+2 are loaded right
-  // after step k used its buffer, so each load has a whole step to land.
-  // (Scalar loads for these were measured slower.)
-  int act0[LBF_MAXA] = {0, 0, 0, 0}, act1[LBF_MAXA] = {0, 0, 0, 0};
-  // The tile's actions of step k are fetched with scalar (uniform-address)
-  // loads, which are counted apart from the vector stores of the trajectory,
-  // so waiting for them never waits for earlier steps' stores to drain; each
-  // env lane then picks its own.
-  auto load_actions = [&](int k, int (&dst)[LBF_MAXA]) {
-    if (envlane && k < n_steps) {
-#pragma unroll
-      for (int i = 0; i < A; ++i) dst[i] = actions[((size_t)k * E + e) * A + i];
-    }
-  };
-
   if (envlane) {
     lbf_load<A, F>(state, p, e, s);
     lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, true);
   }
-  load_actions(0, act0);
-  load_actions(1, act1);
-  // Let the prologue loads land here, once: otherwise the first in-loop use
-  // of a loaded value gets a full vector-memory wait that executes on every
-  // iteration and so waits for the previous steps' trajectory stores.
-  __builtin_amdgcn_s_waitcnt(0);
-  auto step = [&](int k, const int (&act)[LBF_MAXA]) {
-    const uint64_t t = t0 + (uint64_t)k;
-    uint32_t d = 0;
-    float r = 0.f;
-    if (envlane) {
-      lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, false);
-      lbf_transition<A, F, GH, GW>(p, s, act, r, d);
-    }
-    const uint64_t done_mask = __ballot(envlane && d != 0);
-    if (done_mask) {
-      const int j = lane / nblk, blk = lane - j * nblk;
-      if (j < TE && ((done_mask >> j) & 1ull)) {
-        const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + j), t + 1, (uint64_t)blk, TAG_RESET);
+  for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
+    const int nk = min(ACT_CHUNK, n_steps - k0);
+    // The loop has no global loads: the chunk's actions are staged in LDS
+    // first.  (gfx9 counts loads and trajectory stores in one in-order
+    // counter, so a load inside the loop would wait for every earlier store.)
+    stage_actions<TE * A, 64>(actions, E, e0, te_valid * A, A, k0, nk, act_lds, lane);
+    wave_lds_sync();
+    for (int kk = 0; kk < nk; ++kk) {
+      const int k = k0 + kk;
+      const uint64_t t = t0 + (uint64_t)k;
+      uint32_t d = 0;
+      float r = 0.f;
+      if (envlane) {
+        int act[LBF_MAXA] = {0, 0, 0, 0};
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
-          if (blk * 8 + q < LBF_MAX_DRAWS) rdraw[j * LBF_MAX_DRAWS + blk * 8 + q] = block_u32(b, q);
+        for (int i = 0; i < A; ++i) act[i] = act_lds[kk * TE * A + lane * A + i];
+        lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, false);
+        lbf_transition<A, F, GH, GW>(p, s, act, r, d);
+      }
+      const uint64_t done_mask = __ballot(envlane && d != 0);
+      if (done_mask) {
+        const int j = lane / nblk, blk = lane - j * nblk;
+        if (j < TE && ((done_mask >> j) & 1ull)) {
+          const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + j), t + 1, (uint64_t)blk, TAG_RESET);
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            if (blk * 8 + q < LBF_MAX_DRAWS) rdraw[j * LBF_MAX_DRAWS + blk * 8 + q] = block_u32(b, q);
+        }
+        wave_lds_sync();
+        if (envlane && d) {
+          uint32_t dw[LBF_MAX_DRAWS];
+#pragma unroll
+          for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[lane * LBF_MAX_DRAWS + q] : 0u;
+          lbf_reset_from_draws<A, F>(p, dw, s);
+        }
+      }
+      if (envlane) {
+        lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, true);
+        if (reward) reward[(size_t)k * E + e] = r;
+        if (done) done[(size_t)k * E + e] = (uint8_t)d;
       }
       wave_lds_sync();
-      if (envlane && d) {
-        uint32_t dw[LBF_MAX_DRAWS];
-#pragma unroll
-        for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[lane * LBF_MAX_DRAWS + q] : 0u;
-        lbf_reset_from_draws<A, F>(p, dw, s);
-      }
+      if (obs) copy_obs_rows<OT, R, D, D, 64>(xs, obs + ((size_t)k * E + e0) * A * D, te_valid * A, lane);
+      if (legal) lbf_write_legal<64>(p, te_valid, legal + ((size_t)k * E + e0) * A * LBF_NACT, lane);
     }
-    if (envlane) {
-      lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, true);
-      if (reward) reward[(size_t)k * E + e] = r;
-      if (done) done[(size_t)k * E + e] = (uint8_t)d;
-    }
-    wave_lds_sync();
-    if (obs) copy_obs_rows<OT, R, D, D, 64>(xs, obs + ((size_t)k * E + e0) * A * D, te_valid * A, lane);
-    if (legal) lbf_write_legal<64>(p, te_valid, legal + ((size_t)k * E + e0) * A * LBF_NACT, lane);
-  };
-  for (int k = 0; k < n_steps; k += 2) {
-    step(k, act0);
-    load_actions(k + 2, act0);
-    if (k + 1 < n_steps) {
-      step(k + 1, act1);
-      load_actions(k + 3, act1);
-    }
+    wave_lds_sync();  // the chunk's actions are read before the next chunk overwrites them
   }
   if (envlane) lbf_store<A, F>(state, p, e, s);
 }

@@ -139,6 +139,7 @@ __global__ __launch_bounds__(64) void oc_env_kernel(OcParams p, int32_t* __restr
                                                     float* __restrict__ reward, uint8_t* __restrict__ done,
                                                     uint8_t* __restrict__ legal) {
   __shared__ __align__(16) OT tile[OC_TE * 2 * OC_D];
+  __shared__ int32_t act_lds[ACT_CHUNK * OC_TE * 2];
   const int lane = threadIdx.x, e0 = blockIdx.x * OC_TE, te_valid = min(OC_TE, p.E - e0);
   const int E = p.E;
   const bool envlane = lane < te_valid;
@@ -150,22 +151,28 @@ __global__ __launch_bounds__(64) void oc_env_kernel(OcParams p, int32_t* __restr
     oc_load(state, E, e, s);
     oc_paint_all(s, tile, OC_D, lane);
   }
-  __builtin_amdgcn_s_waitcnt(0);
-  for (int k = 0; k < n_steps; ++k) {
-    const uint64_t t = t0 + (uint64_t)k;
-    if (envlane) {
-      const int act[2] = {actions[((size_t)k * E + e) * 2], actions[((size_t)k * E + e) * 2 + 1]};
-      float r;
-      uint32_t d;
-      oc_step_lane(p, s, lane, (uint64_t)(p.env_base + e), t, act, tile, OC_D, r, d);
-      if (reward) reward[(size_t)k * E + e] = r;
-      if (done) done[(size_t)k * E + e] = (uint8_t)d;
+  for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
+    const int nk = min(ACT_CHUNK, n_steps - k0);
+    // no global loads inside the step loop: a load there would wait for every earlier trajectory store
+    stage_actions<OC_TE * 2, 64>(actions, E, e0, te_valid * 2, 2, k0, nk, act_lds, lane);
+    wave_lds_sync();
+    for (int kk = 0; kk < nk; ++kk) {
+      const int k = k0 + kk;
+      const uint64_t t = t0 + (uint64_t)k;
+      if (envlane) {
+        const int act[2] = {act_lds[kk * OC_TE * 2 + lane * 2], act_lds[kk * OC_TE * 2 + lane * 2 + 1]};
+        float r;
+        uint32_t d;
+        oc_step_lane(p, s, lane, (uint64_t)(p.env_base + e), t, act, tile, OC_D, r, d);
+        if (reward) reward[(size_t)k * E + e] = r;
+        if (done) done[(size_t)k * E + e] = (uint8_t)d;
+      }
+      wave_lds_sync();
+      if (obs) copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * OC_D, te_valid * 2 * OC_D, lane, 64);
+      if (legal)
+        for (int i = lane; i < te_valid * 2 * OC_NACT; i += 64) legal[((size_t)k * E + e0) * 2 * OC_NACT + i] = 1;
+      wave_lds_sync();
     }
-    wave_lds_sync();
-    if (obs) copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * OC_D, te_valid * 2 * OC_D, lane, 64);
-    if (legal)
-      for (int i = lane; i < te_valid * 2 * OC_NACT; i += 64) legal[((size_t)k * E + e0) * 2 * OC_NACT + i] = 1;
-    wave_lds_sync();
   }
   if (envlane) oc_store(state, E, e, s);
 }
@@ -209,10 +216,6 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     __syncthreads();  // the env lanes' repaint of the previous step is visible
-    if (out.obs) {
-      T* g = static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D;
-      for (int r = 0; r < te_valid * 2; ++r) copy_tile(xs + r * LDX, g + (size_t)r * OC_D, OC_D, tid, NTHREADS);
-    }
     mlp_input_layer_const<DT, OC_D>(xs, LDX, nullptr, R, W1, b1, pol.H1, h1, ld1, wave, NTHREADS / 64, lane);
     __syncthreads();
     mlp_hidden<DT>(h1, ld1, R, pol.H1, W2, b2, pol.H2, h2, ld2, wave, NTHREADS / 64, lane);
@@ -226,6 +229,12 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
         sc[r * MAX_NA + a] = action_score(lg[r * MAX_NA + a], g, true);
         if (out.logits) out.logits[((size_t)k * E + e0) * 2 * NA + idx] = lg[r * MAX_NA + a];
       }
+    }
+    // The trajectory copy of o_t is issued after the step's weight loads: a
+    // wave's loads wait for its earlier stores (one in-order counter).
+    if (out.obs) {
+      T* g = static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D;
+      for (int r = 0; r < te_valid * 2; ++r) copy_tile(xs + r * LDX, g + (size_t)r * OC_D, OC_D, tid, NTHREADS);
     }
     __syncthreads();
     if (tid < R && (tid >> 1) < te_valid) {
