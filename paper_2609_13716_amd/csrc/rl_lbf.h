@@ -263,7 +263,8 @@ __device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, co
 #pragma unroll
   for (int i = 0; i < LBF_MAXA; ++i) s.acell[i] = newcell[i];
   s.eaten = eaten;
-  reward = (float)eaten_sum / (float)s.den;
+  // one IEEE division, skipped when no env of the wave ate (the quotient is then +0)
+  reward = __builtin_amdgcn_ballot_w64(eaten_sum != 0) ? (float)eaten_sum / (float)s.den : 0.f;
   s.steps += 1;
   const uint32_t all = (F >= 32) ? 0xffffffffu : ((1u << F) - 1u);
   done = ((eaten & all) == all ? 1u : 0u) | (s.steps >= p.max_steps ? 2u : 0u);

@@ -396,9 +396,9 @@ __device__ __forceinline__ void lbf_paint_tile(const LbfEnv& s, int el, T* xs, i
 #pragma unroll
     for (int q = 0; q < A; ++q) xr[min((uint32_t)s.acell[q], cmax)] = on ? small_int_to<T>((uint32_t)s.alevel[q]) : (T)0;
 #pragma unroll
-    for (int j = 0; j < F; ++j)
-      if (!((s.eaten >> j) & 1u))
-        xr[HW + min((uint32_t)s.fcell[j], cmax)] = on ? small_int_to<T>((uint32_t)s.flevel[j]) : (T)0;
+    for (int j = 0; j < F; ++j)  // an eaten food writes 0 at its own (distinct) cell: no branch
+      xr[HW + min((uint32_t)s.fcell[j], cmax)] =
+          (on && !((s.eaten >> j) & 1u)) ? small_int_to<T>((uint32_t)s.flevel[j]) : (T)0;
     xr[2 * HW + min((uint32_t)s.acell[i], cmax)] = one;
   }
 }
