@@ -9,7 +9,8 @@
 // fields in one 32-bit word each, so closing up a hand after a play is two
 // masks and a shift; the deck is 13 words of 4 card bytes, read with a
 // select chain (no dynamically indexed registers).  A reset's Fisher-Yates
-// shuffle runs across a whole wave, one deck position per lane.
+// shuffle runs across a whole wave, one deck position per lane, and the
+// observation is assembled from fields computed by many threads.
 #pragma once
 #include "rl_philox.h"
 
@@ -321,60 +322,30 @@ __device__ __forceinline__ void hn_store(int32_t* __restrict__ st, int E, int e,
   w(34, s.last);
 }
 
-// The observation as a 658-bit vector in eleven 64-bit words (bit f = feature
-// f), built by the game's own lane with whole-field bit operations; every
-// field sits at a compile-time offset.
+// The observation as a 658-bit vector in eleven 64-bit words (bit f =
+// feature f), assembled from 26 fields per row that different threads
+// compute in parallel (hn_field_bits) and OR into the row's words.
 constexpr int HN_OBS_WORDS = (HN_OBS + 63) / 64;
+constexpr int HN_NFIELDS = 26;
 
-template <int OFF, int WIDTH>
-__device__ __forceinline__ void hn_deposit(uint64_t (&w)[HN_OBS_WORDS], uint64_t v) {
-  static_assert(WIDTH <= 64 && OFF + WIDTH <= HN_OBS_WORDS * 64, "field");
-  constexpr int i = OFF >> 6, sh = OFF & 63;
-  w[i] |= v << sh;
-  if constexpr (sh + WIDTH > 64) w[i + 1] |= v >> (64 - sh);
-}
+// What the field computations read of one game (published to LDS after each move).
+struct HnPub {
+  uint32_t hand[2], kc[2], kr[2], hc[2], hr[2];
+  int n[2];
+  uint32_t fw, disc0, disc1, last;
+  int info, lives, next, cur;
+};
 
-__device__ __forceinline__ uint64_t hn_therm(int n, int width) {  // n ones (clamped to width) from bit 0
-  const int k = n < 0 ? 0 : n > width ? width : n;
-  return k >= 64 ? ~0ull : ((1ull << k) - 1ull);
-}
-
-// The 35-bit knowledge field of one card: 25 plausible cards, hinted colour, hinted rank.
-__device__ __forceinline__ uint64_t hn_know_bits(uint32_t kc, uint32_t kr, uint32_t hc, uint32_t hr) {
-  // spread the 5 colour bits to the bottom of 5-bit groups; times the rank mask fills each group
-  uint64_t spread = 0;
+__device__ __forceinline__ void hn_pub(const HnEnv& s, HnPub& v) {
 #pragma unroll
-  for (int c = 0; c < HN_COLOURS; ++c) spread |= (uint64_t)((kc >> c) & 1u) << (5 * c);
-  const uint64_t plaus = spread * (uint64_t)kr;
-  const uint64_t hcol = hc ? (1ull << (hc - 1)) : 0ull;
-  const uint64_t hrank = hr ? (1ull << (hr - 1)) : 0ull;
-  return plaus | (hcol << 25) | (hrank << 30);
-}
-
-__device__ __forceinline__ void hn_obs_bits(const HnEnv& s, int me, uint64_t (&w)[HN_OBS_WORDS]) {
-#pragma unroll
-  for (int i = 0; i < HN_OBS_WORDS; ++i) w[i] = 0;
-  // player-indexed fields as seen by `me`: index 0 the observer, 1 its partner
-  // (selects: a register array indexed at run time would live in scratch)
-  struct {
-    uint32_t hand[2], kc[2], kr[2], hc[2], hr[2];
-    int n[2];
-    uint32_t fw, disc0, disc1, last;
-    int info, lives, next;
-  } v;
-  const bool sw = me == 1;
-  v.hand[0] = sw ? s.hand[1] : s.hand[0];
-  v.hand[1] = sw ? s.hand[0] : s.hand[1];
-  v.kc[0] = sw ? s.kc[1] : s.kc[0];
-  v.kc[1] = sw ? s.kc[0] : s.kc[1];
-  v.kr[0] = sw ? s.kr[1] : s.kr[0];
-  v.kr[1] = sw ? s.kr[0] : s.kr[1];
-  v.hc[0] = sw ? s.hc[1] : s.hc[0];
-  v.hc[1] = sw ? s.hc[0] : s.hc[1];
-  v.hr[0] = sw ? s.hr[1] : s.hr[0];
-  v.hr[1] = sw ? s.hr[0] : s.hr[1];
-  v.n[0] = sw ? s.n[1] : s.n[0];
-  v.n[1] = sw ? s.n[0] : s.n[1];
+  for (int i = 0; i < 2; ++i) {
+    v.hand[i] = s.hand[i];
+    v.kc[i] = s.kc[i];
+    v.kr[i] = s.kr[i];
+    v.hc[i] = s.hc[i];
+    v.hr[i] = s.hr[i];
+    v.n[i] = s.n[i];
+  }
   v.fw = s.fw;
   v.disc0 = s.disc0;
   v.disc1 = s.disc1;
@@ -382,33 +353,68 @@ __device__ __forceinline__ void hn_obs_bits(const HnEnv& s, int me, uint64_t (&w
   v.info = s.info;
   v.lives = s.lives;
   v.next = s.next;
-  // partner hand: 5 slots x 25-bit one-hot of the card
-#define HN_PARTNER_SLOT(S)                                                                                  \
-  hn_deposit<25 * (S), 25>(w, (S) < v.n[1] ? (1ull << hn_field(v.hand[1], 5, (S))) : 0ull);
-  HN_PARTNER_SLOT(0) HN_PARTNER_SLOT(1) HN_PARTNER_SLOT(2) HN_PARTNER_SLOT(3) HN_PARTNER_SLOT(4)
-#undef HN_PARTNER_SLOT
-  hn_deposit<125, 2>(w, (v.n[0] < HN_HAND ? 1ull : 0ull) | (v.n[1] < HN_HAND ? 2ull : 0ull));
-  hn_deposit<127, 40>(w, hn_therm(HN_CARDS - v.next, 40));
-  uint64_t fw = 0;
-#pragma unroll
-  for (int c = 0; c < HN_COLOURS; ++c) {
-    const uint32_t h = hn_field(v.fw, 3, c);
-    fw |= h ? (1ull << (5 * c + h - 1)) : 0ull;
+  v.cur = s.cur;
+}
+
+__device__ __forceinline__ uint64_t hn_therm(int n, int width) {  // n ones (clamped to width) from bit 0
+  const int k = n < 0 ? 0 : n > width ? width : n;
+  return k >= 64 ? ~0ull : ((1ull << k) - 1ull);
+}
+
+// Field f (0..25) of player me's observation: its bits, and in `off` the
+// feature index of its bit 0.  Fields: 0-4 partner slots (25-bit one-hot),
+// 5 short hands, 6 deck thermometer, 7 fireworks, 8 tokens, 9 lives, 10-14
+// the discard thermometers of one colour, 15 the last move, 16-25 the
+// knowledge of one slot (observer's hand, then the partner's).  `v` is
+// normally in LDS; player indices are plain memory indices there.
+__device__ __forceinline__ uint64_t hn_field_bits(const HnPub& v, int me, int f, int& off) {
+  const int pt = 1 - me;
+  if (f < 5) {
+    off = 25 * f;
+    return f < v.n[pt] ? (1ull << hn_field(v.hand[pt], 5, f)) : 0ull;
   }
-  hn_deposit<167, 25>(w, fw);
-  hn_deposit<192, 8>(w, hn_therm(v.info, 8));
-  hn_deposit<200, 3>(w, hn_therm(v.lives, 3));
-  uint64_t disc = 0;  // per card id, a thermometer as long as its copies (3,2,2,2,1 per colour)
-#pragma unroll
-  for (int card = 0; card < HN_KINDS; ++card) {
-    const int r = card % HN_RANKS, c = card / HN_RANKS;
-    const int off = c * 10 + (r == 0 ? 0 : 2 * r + 1), copies = r == 0 ? 3 : r == 4 ? 1 : 2;
-    const uint32_t cnt = card < 16 ? (v.disc0 >> (2 * card)) & 3u : (v.disc1 >> (2 * (card - 16))) & 3u;
-    disc |= hn_therm((int)cnt, copies) << off;
+  if (f == 5) {
+    off = 125;
+    return (v.n[me] < HN_HAND ? 1ull : 0ull) | (v.n[pt] < HN_HAND ? 2ull : 0ull);
   }
-  hn_deposit<203, 50>(w, disc);
-  const uint32_t L = v.last;
-  if (L & 1u) {  // last move: 2 + 4 + 2 + 5 + 5 + 5 + 5 bits, then the card (25), success, token
+  if (f == 6) {
+    off = 127;
+    return hn_therm(HN_CARDS - v.next, 40);
+  }
+  if (f == 7) {
+    off = 167;
+    uint64_t fw = 0;
+#pragma unroll
+    for (int c = 0; c < HN_COLOURS; ++c) {
+      const uint32_t h = hn_field(v.fw, 3, c);
+      fw |= h ? (1ull << (5 * c + h - 1)) : 0ull;
+    }
+    return fw;
+  }
+  if (f == 8) {
+    off = 192;
+    return hn_therm(v.info, 8);
+  }
+  if (f == 9) {
+    off = 200;
+    return hn_therm(v.lives, 3);
+  }
+  if (f < 15) {  // one colour's discards: thermometers of 3, 2, 2, 2, 1 copies
+    const int c = f - 10;
+    off = 203 + 10 * c;
+    uint64_t d = 0;
+#pragma unroll
+    for (int r = 0; r < HN_RANKS; ++r) {
+      const int card = c * HN_RANKS + r;
+      const uint32_t cnt = card < 16 ? (v.disc0 >> (2 * card)) & 3u : (v.disc1 >> (2 * (card - 16))) & 3u;
+      d |= hn_therm((int)cnt, r == 0 ? 3 : r == 4 ? 1 : 2) << (r == 0 ? 0 : 2 * r + 1);
+    }
+    return d;
+  }
+  if (f == 15) {  // last move: 2 + 4 + 2 + 5 + 5 + 5 + 5 bits, then the card (25), success, token
+    off = 253;
+    const uint32_t L = v.last;
+    if (!(L & 1u)) return 0ull;
     const int actor = (int)((L >> 1) & 1u), kind = (int)((L >> 2) & 3u), target = (int)((L >> 4) & 1u);
     const uint32_t hcol = (L >> 5) & 7u, hrank = (L >> 8) & 7u, slot = (L >> 16) & 7u, card = (L >> 19) & 31u;
     uint64_t a = (1ull << ((actor - me) & 1)) | (1ull << (2 + kind));
@@ -419,17 +425,19 @@ __device__ __forceinline__ void hn_obs_bits(const HnEnv& s, int me, uint64_t (&w
     if (slot) a |= 1ull << (23 + slot - 1);
     if (card) a |= 1ull << (28 + card - 1);
     a |= (uint64_t)((L >> 24) & 3u) << 53;
-    hn_deposit<253, 55>(w, a);
+    return a;
   }
-  // knowledge: the observer's hand, then the partner's, 5 slots x 35 bits each
-#define HN_KNOW_SLOT(J, S)                                                                                  \
-  hn_deposit<308 + 175 * (J) + 35 * (S), 35>(                                                               \
-      w, (S) < v.n[J] ? hn_know_bits(hn_field(v.kc[J], 5, (S)), hn_field(v.kr[J], 5, (S)),                  \
-                                     hn_field(v.hc[J], 3, (S)), hn_field(v.hr[J], 3, (S)))                  \
-                      : 0ull);
-  HN_KNOW_SLOT(0, 0) HN_KNOW_SLOT(0, 1) HN_KNOW_SLOT(0, 2) HN_KNOW_SLOT(0, 3) HN_KNOW_SLOT(0, 4)
-  HN_KNOW_SLOT(1, 0) HN_KNOW_SLOT(1, 1) HN_KNOW_SLOT(1, 2) HN_KNOW_SLOT(1, 3) HN_KNOW_SLOT(1, 4)
-#undef HN_KNOW_SLOT
+  // knowledge of one card: 25 plausible cards, hinted colour, hinted rank
+  const int j = (f - 16) / 5, sl = (f - 16) - 5 * j, who = j ? pt : me;
+  off = 308 + 175 * j + 35 * sl;
+  if (sl >= v.n[who]) return 0ull;
+  const uint32_t kc = hn_field(v.kc[who], 5, sl), kr = hn_field(v.kr[who], 5, sl);
+  const uint32_t hc = hn_field(v.hc[who], 3, sl), hr = hn_field(v.hr[who], 3, sl);
+  uint64_t spread = 0;  // colour bits at the bottom of 5-bit groups; times the rank mask fills each group
+#pragma unroll
+  for (int c = 0; c < HN_COLOURS; ++c) spread |= (uint64_t)((kc >> c) & 1u) << (5 * c);
+  const uint64_t plaus = spread * (uint64_t)kr;
+  return plaus | ((hc ? 1ull << (hc - 1) : 0ull) << 25) | ((hr ? 1ull << (hr - 1) : 0ull) << 30);
 }
 
 }  // namespace rl

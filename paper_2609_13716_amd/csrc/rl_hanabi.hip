@@ -17,19 +17,45 @@
 namespace rl {
 
 struct HnTile {
-  uint64_t bits[2][HN_OBS_WORDS];  // both players' observations as bit vectors
-  int cur;                         // the player to move
+  uint64_t bits[2][HN_OBS_WORDS];  // both players' observations as bit vectors (zero between steps)
+  HnPub pub;                       // the game as of the last move
   uint32_t legal;                  // mover's 20-bit legal mask
 };
 
+// Assemble the observation bit vectors of every row of the tile: thread t
+// computes field t / (2 TE) of row t % (2 TE) (consecutive lanes take the
+// same field of different rows, so a wave runs few of the field branches) and
+// ORs it into the row's words (LDS atomics; the words are zero beforehand).
+// Needs the published games.
+template <int TE, int NT>
+__device__ __forceinline__ void hn_build_bits(HnTile* envs, int te_valid, int tid) {
+  for (int t = tid; t < 2 * TE * HN_NFIELDS; t += NT) {
+    const int f = t / (2 * TE), row = t - f * (2 * TE), el = row >> 1, me = row & 1;
+    if (el >= te_valid) continue;
+    int off;
+    const uint64_t v = hn_field_bits(envs[el].pub, me, f, off);
+    if (v) {
+      unsigned long long* w = reinterpret_cast<unsigned long long*>(envs[el].bits[me]);
+      const int i = off >> 6, sh = off & 63;
+      atomicOr(w + i, (unsigned long long)(v << sh));
+      if (sh && (v >> (64 - sh))) atomicOr(w + i + 1, (unsigned long long)(v >> (64 - sh)));
+    }
+  }
+}
+
 // Paint rows 2*el + me (el < te_valid) of the observation tile from the
-// published bit vectors: one row per wave at a time, lane l writes features
-// l, l + 64, ...
+// assembled bit vectors, one row per wave at a time (lane l writes features
+// l, l + 64, ...), and clear the vectors for the next step.
 template <typename T, int NW>
-__device__ __forceinline__ void hn_paint(const HnTile* __restrict__ envs, int te_valid, T* tile, int ld, int wave,
-                                         int lane) {
+__device__ __forceinline__ void hn_paint(HnTile* envs, int te_valid, T* tile, int ld, int wave, int lane) {
   for (int r = wave; r < 2 * te_valid; r += NW) {
-    const uint64_t* w = envs[r >> 1].bits[r & 1];
+    uint64_t* wp = envs[r >> 1].bits[r & 1];
+    uint64_t w[HN_OBS_WORDS];
+#pragma unroll
+    for (int i = 0; i < HN_OBS_WORDS; ++i) w[i] = wp[i];
+    if (lane == 0)  // after every lane's read (one wave's LDS operations complete in order)
+#pragma unroll
+      for (int i = 0; i < HN_OBS_WORDS; ++i) wp[i] = 0;
     T* row = tile + (size_t)r * ld;
 #pragma unroll
     for (int i = 0; i < HN_OBS_WORDS; ++i) {
@@ -58,21 +84,14 @@ __device__ __forceinline__ void hn_write_legal(const HnTile* __restrict__ envs, 
                                                int tid) {
   for (int i = tid; i < te_valid * 2 * HN_NACT; i += NT) {
     const int el = i / (2 * HN_NACT), rem = i - el * 2 * HN_NACT, ag = rem / HN_NACT, a = rem - ag * HN_NACT;
-    g[i] = (ag == envs[el].cur) ? (uint8_t)((envs[el].legal >> a) & 1u) : (uint8_t)0;
+    g[i] = (ag == envs[el].pub.cur) ? (uint8_t)((envs[el].legal >> a) & 1u) : (uint8_t)0;
   }
 }
 
-// What the workgroup reads of a game after each move: both observations as
-// bit vectors, the mover and its legal actions.
+// What the workgroup reads of a game after each move: the packed game and
+// the mover's legal actions.
 __device__ __forceinline__ void hn_publish(const HnEnv& s, HnTile& t) {
-#pragma unroll
-  for (int me = 0; me < 2; ++me) {
-    uint64_t w[HN_OBS_WORDS];
-    hn_obs_bits(s, me, w);
-#pragma unroll
-    for (int i = 0; i < HN_OBS_WORDS; ++i) t.bits[me][i] = w[i];
-  }
-  t.cur = s.cur;
+  hn_pub(s, t.pub);
   t.legal = hn_legal(s);
 }
 
@@ -105,6 +124,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_init_kernel(HnParams p, int32_t* 
   __shared__ __align__(16) OT tile[2 * TE * HN_OBS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0);
+  zero_lds<NTHREADS>(envs, sizeof(envs), tid);  // the bit vectors start clear
   for (int el = wave; el < te_valid; el += NW)
     hn_wave_shuffle(p.seed, (uint64_t)(p.env_base + e0 + el), 0, lane, words[el]);
   __syncthreads();
@@ -116,6 +136,8 @@ __global__ __launch_bounds__(NTHREADS) void hn_init_kernel(HnParams p, int32_t* 
   }
   __syncthreads();
   if (obs) {
+    hn_build_bits<TE, NTHREADS>(envs, te_valid, tid);
+    __syncthreads();
     hn_paint<OT, NW>(envs, te_valid, tile, HN_OBS, wave, lane);
     __syncthreads();
     copy_tile(tile, obs + (size_t)e0 * 2 * HN_OBS, 2 * te_valid * HN_OBS, tid, NTHREADS);
@@ -140,6 +162,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
   const bool envlane = tid < te_valid;
   const int e = e0 + tid;
+  zero_lds<NTHREADS>(envs, sizeof(envs), tid);  // the bit vectors start clear
   HnEnv s;
   if (envlane) hn_load(state, E, e, s);
   for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
@@ -171,6 +194,8 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
         __syncthreads();
       }
       if (obs) {
+        hn_build_bits<TE, NTHREADS>(envs, te_valid, tid);
+        __syncthreads();
         hn_paint<OT, NW>(envs, te_valid, tile, HN_OBS, wave, lane);
         __syncthreads();
         copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * HN_OBS, 2 * te_valid * HN_OBS, tid, NTHREADS);
@@ -252,7 +277,9 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
   if (tid < TE) rows[tid] = 2 * tid + (envlane ? s.cur : 0);  // the mover's row (a zero row for padding)
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
-    __syncthreads();  // the previous move's observations are published
+    __syncthreads();  // the previous move's games are published
+    hn_build_bits<TE, NTHREADS>(envs, te_valid, tid);
+    __syncthreads();
     hn_paint<T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
     mlp_input_layer_const<DT, HN_OBS>(xs, LDX, rows, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane);
@@ -263,7 +290,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
     __syncthreads();
     for (int idx = tid; idx < te_valid * NA; idx += NTHREADS) {
       const int el = idx / NA, a = idx - el * NA;
-      const int cur = envs[el].cur;
+      const int cur = envs[el].pub.cur;
       const bool ok = (envs[el].legal >> a) & 1u;
       const float g = action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t, cur, a);
       sc[el * MAX_NA + a] = action_score(lg[el * MAX_NA + a], g, ok);
@@ -318,6 +345,8 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
   }
   __syncthreads();
   if (out.obs_last) {
+    hn_build_bits<TE, NTHREADS>(envs, te_valid, tid);
+    __syncthreads();
     hn_paint<T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
     hn_copy_rows<T, LDX, NTHREADS>(xs, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * HN_OBS, 2 * te_valid, tid);
