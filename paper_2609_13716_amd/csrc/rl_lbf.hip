@@ -695,86 +695,88 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
   return false;
 }
 
-// ------------------------------------------- env-only steps, one wave ----
+// --------------------------------------- env-only steps, two waves ----
 //
-// rollout_step for compile-time LBF shapes: one wave per workgroup owns TE
-// envs (lanes 0..TE-1 keep the env state in registers), paints the
-// observation rows into an LDS tile and copies the tile to the trajectory
-// with 16-byte stores that drain while the next transition runs.  The
-// actions of step k+2 are fetched as soon as step k has used its buffer.
+// rollout_step for compile-time LBF shapes.  Wave 0 owns TE envs (lanes
+// 0..TE-1 keep the env state in registers) and paints each step's
+// observation rows into one of two LDS tiles; wave 1 copies the tile of the
+// previous step to the trajectory with 16-byte stores, so the copy overlaps
+// the next transition.  The paint is incremental: a tile is updated from the
+// state it held two steps earlier (kept in registers).  The chunk's actions
+// are staged in LDS first, so the step loop has no global loads.
 template <typename OT, int GH, int GW, int A, int F, int TE>
-__global__ __launch_bounds__(64) void lbf_env_kernel(LbfParams p, int32_t* __restrict__ state, uint64_t t0,
-                                                     int n_steps, const int32_t* __restrict__ actions,
-                                                     OT* __restrict__ obs, float* __restrict__ reward,
-                                                     uint8_t* __restrict__ done, uint8_t* __restrict__ legal) {
+__global__ __launch_bounds__(128) void lbf_env_kernel(LbfParams p, int32_t* __restrict__ state, uint64_t t0,
+                                                      int n_steps, const int32_t* __restrict__ actions,
+                                                      OT* __restrict__ obs, float* __restrict__ reward,
+                                                      uint8_t* __restrict__ done, uint8_t* __restrict__ legal) {
   constexpr int HW = GH * GW, D = 3 * HW, R = TE * A;
   constexpr int nd = 2 * A + 2 * F;
   constexpr int nblk = (nd + 7) >> 3;
-  static_assert(TE <= 64 && TE * nblk <= 64, "one wave");
-  __shared__ __align__(16) OT xs[R * D];
+  static_assert(TE <= 64 && TE * nblk <= 64, "one env wave");
+  __shared__ __align__(16) OT xs[2][R * D];
   __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];
   __shared__ int32_t act_lds[ACT_CHUNK * TE * A];
 
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE;
   const int te_valid = min(TE, p.E - e0);
   const int E = p.E;
-  const bool envlane = lane < te_valid;
+  const bool envlane = wave == 0 && lane < te_valid;
   const int e = e0 + lane;
 
-  for (int i = lane; i < R * D; i += 64) xs[i] = (OT)0;
-  wave_lds_sync();
-  LbfEnv s{};
-  if (envlane) {
-    lbf_load<A, F>(state, p, e, s);
-    lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, true);
-  }
+  zero_lds<128>(xs, sizeof(xs), tid);
+  __syncthreads();
+  LbfEnv s{}, sprev{};  // the state, and the state before the last transition (what the other tile shows)
+  if (envlane) lbf_load<A, F>(state, p, e, s);
   for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
     const int nk = min(ACT_CHUNK, n_steps - k0);
-    // The loop has no global loads: the chunk's actions are staged in LDS
-    // first.  (gfx9 counts loads and trajectory stores in one in-order
-    // counter, so a load inside the loop would wait for every earlier store.)
-    stage_actions<TE * A, 64>(actions, E, e0, te_valid * A, A, k0, nk, act_lds, lane);
-    wave_lds_sync();
+    stage_actions<TE * A, 128>(actions, E, e0, te_valid * A, A, k0, nk, act_lds, tid);
+    __syncthreads();
     for (int kk = 0; kk < nk; ++kk) {
       const int k = k0 + kk;
-      const uint64_t t = t0 + (uint64_t)k;
-      uint32_t d = 0;
-      float r = 0.f;
-      if (envlane) {
-        int act[LBF_MAXA] = {0, 0, 0, 0};
+      OT* tile = xs[k & 1];
+      if (wave == 0) {
+        const uint64_t t = t0 + (uint64_t)k;
+        uint32_t d = 0;
+        float r = 0.f;
+        if (envlane) {
+          int act[LBF_MAXA] = {0, 0, 0, 0};
 #pragma unroll
-        for (int i = 0; i < A; ++i) act[i] = act_lds[kk * TE * A + lane * A + i];
-        lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, false);
-        lbf_transition<A, F, GH, GW>(p, s, act, r, d);
-      }
-      const uint64_t done_mask = __ballot(envlane && d != 0);
-      if (done_mask) {
-        const int j = lane / nblk, blk = lane - j * nblk;
-        if (j < TE && ((done_mask >> j) & 1ull)) {
-          const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + j), t + 1, (uint64_t)blk, TAG_RESET);
-#pragma unroll
-          for (int q = 0; q < 8; ++q)
-            if (blk * 8 + q < LBF_MAX_DRAWS) rdraw[j * LBF_MAX_DRAWS + blk * 8 + q] = block_u32(b, q);
+          for (int i = 0; i < A; ++i) act[i] = act_lds[kk * TE * A + lane * A + i];
+          if (k >= 2) lbf_paint_tile<OT, A, F>(sprev, lane, tile, D, HW, false);  // the tile shows step k-2
+          sprev = s;
+          lbf_transition<A, F, GH, GW>(p, s, act, r, d);
         }
-        wave_lds_sync();
-        if (envlane && d) {
-          uint32_t dw[LBF_MAX_DRAWS];
+        const uint64_t done_mask = __ballot(envlane && d != 0);
+        if (done_mask) {
+          const int j = lane / nblk, blk = lane - j * nblk;
+          if (j < TE && ((done_mask >> j) & 1ull)) {
+            const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + j), t + 1, (uint64_t)blk, TAG_RESET);
 #pragma unroll
-          for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[lane * LBF_MAX_DRAWS + q] : 0u;
-          lbf_reset_from_draws<A, F>(p, dw, s);
+            for (int q = 0; q < 8; ++q)
+              if (blk * 8 + q < LBF_MAX_DRAWS) rdraw[j * LBF_MAX_DRAWS + blk * 8 + q] = block_u32(b, q);
+          }
+          wave_lds_sync();
+          if (envlane && d) {
+            uint32_t dw[LBF_MAX_DRAWS];
+#pragma unroll
+            for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[lane * LBF_MAX_DRAWS + q] : 0u;
+            lbf_reset_from_draws<A, F>(p, dw, s);
+          }
+        }
+        if (envlane) {
+          lbf_paint_tile<OT, A, F>(s, lane, tile, D, HW, true);
+          if (reward) reward[(size_t)k * E + e] = r;
+          if (done) done[(size_t)k * E + e] = (uint8_t)d;
         }
       }
-      if (envlane) {
-        lbf_paint_tile<OT, A, F>(s, lane, xs, D, HW, true);
-        if (reward) reward[(size_t)k * E + e] = r;
-        if (done) done[(size_t)k * E + e] = (uint8_t)d;
+      __syncthreads();  // tile k is painted; tile k-1 is copied
+      if (wave == 1) {
+        if (obs) copy_obs_rows<OT, R, D, D, 64>(tile, obs + ((size_t)k * E + e0) * A * D, te_valid * A, lane);
+        if (legal) lbf_write_legal<64>(p, te_valid, legal + ((size_t)k * E + e0) * A * LBF_NACT, lane);
       }
-      wave_lds_sync();
-      if (obs) copy_obs_rows<OT, R, D, D, 64>(xs, obs + ((size_t)k * E + e0) * A * D, te_valid * A, lane);
-      if (legal) lbf_write_legal<64>(p, te_valid, legal + ((size_t)k * E + e0) * A * LBF_NACT, lane);
     }
-    wave_lds_sync();  // the chunk's actions are read before the next chunk overwrites them
+    __syncthreads();  // the chunk's actions are read (and its last tile copied) before the next chunk
   }
   if (envlane) lbf_store<A, F>(state, p, e, s);
 }
@@ -783,7 +785,7 @@ template <typename OT, int GH, int GW, int A, int F, int TE>
 static hipError_t launch_env_ct(const LbfParams& p, int32_t* state, uint64_t t0, int n_steps,
                                 const int32_t* actions, void* obs, float* reward, uint8_t* done, uint8_t* legal,
                                 hipStream_t s) {
-  lbf_env_kernel<OT, GH, GW, A, F, TE><<<dim3((unsigned)((p.E + TE - 1) / TE)), 64, 0, s>>>(
+  lbf_env_kernel<OT, GH, GW, A, F, TE><<<dim3((unsigned)((p.E + TE - 1) / TE)), 128, 0, s>>>(
       p, state, t0, n_steps, actions, static_cast<OT*>(obs), reward, done, legal);
   return hipGetLastError();
 }
