@@ -65,19 +65,6 @@ __device__ __forceinline__ void hn_paint(HnTile* envs, int te_valid, T* tile, in
   }
 }
 
-// Copy `rows` rows of HN_OBS elements from an LDS tile with leading dimension
-// LD to consecutive global rows, in 4-byte words.
-template <typename T, int LD, int NT>
-__device__ __forceinline__ void hn_copy_rows(const T* src, T* __restrict__ dst, int rows, int tid) {
-  constexpr int PER = 4 / (int)sizeof(T), WPR = HN_OBS / PER, LDW = LD / PER;
-  const uint32_t* s = reinterpret_cast<const uint32_t*>(src);
-  uint32_t* g = reinterpret_cast<uint32_t*>(dst);
-  for (int i = tid; i < rows * WPR; i += NT) {
-    const int r = i / WPR, w = i - r * WPR;
-    g[i] = s[r * LDW + w];
-  }
-}
-
 // Legal masks of both players of envs 0..te_valid-1 ([env][agent][20] bytes).
 template <int NT>
 __device__ __forceinline__ void hn_write_legal(const HnTile* __restrict__ envs, int te_valid, uint8_t* __restrict__ g,
@@ -303,8 +290,8 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
     // The trajectory copy of o_t is issued after the step's weight loads: a
     // wave's loads wait for its earlier stores (one in-order counter).
     if (out.obs)
-      hn_copy_rows<T, LDX, NTHREADS>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * HN_OBS,
-                                     2 * te_valid, tid);
+      copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * HN_OBS, HN_OBS,
+                         2 * te_valid, tid, NTHREADS);
     __syncthreads();
     uint32_t d = 0;
     if (envlane) {
@@ -349,7 +336,8 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
     __syncthreads();
     hn_paint<T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
-    hn_copy_rows<T, LDX, NTHREADS>(xs, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * HN_OBS, 2 * te_valid, tid);
+    copy_rows_global16(xs, LDX, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * HN_OBS, HN_OBS, 2 * te_valid,
+                       tid, NTHREADS);
   }
   if (envlane) hn_store(state, E, e, s);
 }

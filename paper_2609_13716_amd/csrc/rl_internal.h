@@ -54,6 +54,42 @@ __device__ __forceinline__ void copy_tile(const T* src, T* __restrict__ dst, int
   for (int i = done_words + tid; i < (nbytes >> 2); i += nt) g[i] = s[i];
 }
 
+// Copy `rows` rows of `len` elements (len * sizeof(T) a multiple of 4) from
+// an LDS tile whose rows start 16-byte aligned (leading dimension ld) to
+// consecutive global rows that are 4-byte aligned: per row, the words before
+// the first 16-byte boundary and after the last one go as 4-byte stores, the
+// rest as 16-byte stores (their LDS source is read as four words).
+template <typename T>
+__device__ __forceinline__ void copy_rows_global16(const T* src, int ld, T* __restrict__ dst, int len, int rows,
+                                                   int tid, int nt) {
+  const int lb = len * (int)sizeof(T), ldb = ld * (int)sizeof(T);
+  const int maxch = lb / 16;
+  const uint8_t* s8 = reinterpret_cast<const uint8_t*>(src);
+  uint8_t* d8 = reinterpret_cast<uint8_t*>(dst);
+  // 16-byte body
+  for (int i = tid; i < rows * maxch; i += nt) {
+    const int r = i / maxch, c = i - r * maxch;
+    uint8_t* drow = d8 + (size_t)r * lb;
+    const int head = (int)((16 - (reinterpret_cast<uintptr_t>(drow) & 15)) & 15);
+    if (c < (lb - head) / 16) {
+      const uint32_t* sp = reinterpret_cast<const uint32_t*>(s8 + (size_t)r * ldb + head + 16 * c);
+      const u32x4 v = {sp[0], sp[1], sp[2], sp[3]};
+      *reinterpret_cast<u32x4*>(drow + head + 16 * c) = v;
+    }
+  }
+  // head and tail words (at most 3 + 3 per row)
+  for (int i = tid; i < rows * 8; i += nt) {
+    const int r = i >> 3, q = i & 7;
+    uint8_t* drow = d8 + (size_t)r * lb;
+    const int head = (int)((16 - (reinterpret_cast<uintptr_t>(drow) & 15)) & 15);
+    const int h = head < lb ? head : lb;
+    const int tail0 = h + (lb - h) / 16 * 16;
+    const int off = q < 4 ? 4 * q : tail0 + 4 * (q - 4);
+    if ((q < 4 && off < h) || (q >= 4 && off < lb))
+      *reinterpret_cast<uint32_t*>(drow + off) = *reinterpret_cast<const uint32_t*>(s8 + (size_t)r * ldb + off);
+  }
+}
+
 // Injected actions are staged through LDS in chunks of this many steps.
 constexpr int ACT_CHUNK = 64;
 

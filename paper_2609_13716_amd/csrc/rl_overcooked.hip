@@ -232,10 +232,9 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
     }
     // The trajectory copy of o_t is issued after the step's weight loads: a
     // wave's loads wait for its earlier stores (one in-order counter).
-    if (out.obs) {
-      T* g = static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D;
-      for (int r = 0; r < te_valid * 2; ++r) copy_tile(xs + r * LDX, g + (size_t)r * OC_D, OC_D, tid, NTHREADS);
-    }
+    if (out.obs)
+      copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D, OC_D, te_valid * 2,
+                         tid, NTHREADS);
     __syncthreads();
     if (tid < R && (tid >> 1) < te_valid) {
       int best = 0;
@@ -261,10 +260,9 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
     }
   }
   __syncthreads();
-  if (out.obs_last) {
-    T* g = static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * OC_D;
-    for (int r = 0; r < te_valid * 2; ++r) copy_tile(xs + r * LDX, g + (size_t)r * OC_D, OC_D, tid, NTHREADS);
-  }
+  if (out.obs_last)
+    copy_rows_global16(xs, LDX, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * OC_D, OC_D, te_valid * 2, tid,
+                       NTHREADS);
   if (envlane) oc_store(state, E, e, s);
 }
 
