@@ -453,6 +453,11 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   constexpr int ESTRIDE = DIRECT ? A : 1;  // lane of env e = e * ESTRIDE
   constexpr int LDX = lds_ld<DT>(D), LD1 = lds_ld<DT>(H1), LD2 = lds_ld<DT>(H2);
   constexpr int K3 = round_up(H2, DType<DT>::KS) / DType<DT>::KS;
+  // LEAN: the resident weights leave too few registers for the env step, so
+  // the biases and the env state wait in LDS between uses.
+  constexpr int REG_BUDGET = 512 / ((NW * MINB + 3) / 4);
+  constexpr bool LEAN =
+      RegLayer<DT, D, H1, NW>::WREGS + RegLayer<DT, H1, H2, NW>::WREGS + 160 > REG_BUDGET;
   static_assert(NA <= 8, "one Philox block of action noise per row");
   static_assert(TE <= 64, "env lanes live in wave 0");
   static_assert(TE * ((2 * A + 2 * F + 7) / 8) <= 64, "one lane per reset block");
@@ -465,6 +470,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   __shared__ uint32_t words[NOISE_STEPS * RP * 8];  // action Philox draws per (step, row)
   __shared__ __align__(16) float nz[2][RP * 8];     // Gumbel noise per (row, action), by step parity
   __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];    // reset draws of envs being reset
+  __shared__ __align__(16) float bias_s[LEAN ? H1 + H2 : 4];
+  __shared__ LbfEnv env_s[LEAN ? TE : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE;
@@ -482,8 +489,12 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     }
   };
 
-  RegLayer<DT, D, H1, NW> L1;
-  RegLayer<DT, H1, H2, NW> L2;
+  RegLayer<DT, D, H1, NW, LEAN> L1;
+  RegLayer<DT, H1, H2, NW, LEAN> L2;
+  if constexpr (LEAN) {
+    for (int i = tid; i < H1 + H2; i += NT)
+      bias_s[i] = DType<DT>::to_f32(i < H1 ? static_cast<const T*>(pol.b[0])[i] : static_cast<const T*>(pol.b[1])[i - H1]);
+  }
   L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane);
   L2.load(static_cast<const T*>(pol.W[1]), static_cast<const T*>(pol.b[1]), wave, lane);
   if (tid < 64) {
@@ -507,10 +518,13 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   const int el = lane / ESTRIDE;  // env of this lane (when it is an env lane)
   const bool envlane = wave == ew && lane % ESTRIDE == 0 && el < te_valid;
   const int e = e0 + el;
+  // The env state; when LEAN it is kept in LDS between steps and reloaded by
+  // the whole env wave, so it is dead (not holding registers) during the MLP.
   LbfEnv s{};
   if (envlane) {
     lbf_load<A, F>(state, p, e, s);
     lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
+    if constexpr (LEAN) env_s[el] = s;
   }
   // Let the prologue loads land here, once (see lbf_env_kernel).
   __builtin_amdgcn_s_waitcnt(0);
@@ -539,42 +553,52 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       __syncthreads();
     }
     {
-      f32x4 acc[MT][RegLayer<DT, D, H1, NW>::OWN];
+      f32x4 acc[MT][RegLayer<DT, D, H1, NW, LEAN>::OWN];
       L1.template run<MT>(xs, LDX, acc, wave, lane);
-      L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane);
+      L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane, bias_s);
     }
     __syncthreads();
     {
-      f32x4 acc[MT][RegLayer<DT, H1, H2, NW>::OWN];
+      f32x4 acc[MT][RegLayer<DT, H1, H2, NW, LEAN>::OWN];
       L2.template run<MT>(h1s, LD1, acc, wave, lane);
       // o_t to the trajectory while the layer-2 MFMAs run (the tile is only
       // repainted after layer 3)
       if (out.obs)
         copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D, te_valid * A,
                                         tid);
-      L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane);
+      L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane, bias_s + H1);
     }
     __syncthreads();
     if (wave == ew) {
+      if constexpr (LEAN) s = env_s[min(el, TE - 1)];
       // Layer 3 transposed, logits^T = W3 h2^T: lane holds row (lane % 16) of
       // the M tile and actions 4 * (lane / 16) + r in accumulator element r.
       // Each lane takes the Gumbel argmax of its four actions; one lane swap
       // with the partner group (actions 0-3 <-> 4-7) finishes the row.
       const int g = lane >> 4;
       int act_d[LBF_MAXA] = {0, 0, 0, 0};  // DIRECT: this lane's env's actions
-      B w3r[K3];
+      // With one M tile the W3 operands are loaded once into registers; with
+      // several the M tiles run one at a time (not unrolled) and read W3 from
+      // LDS per K step, which keeps the env wave within the register budget
+      // of the layers whose weights stay resident.
+      B w3r[DIRECT ? K3 : 1];
+      if constexpr (DIRECT) {
 #pragma unroll
-      for (int ks = 0; ks < K3; ++ks) w3r[ks] = w3s[ks * 64 + lane];
-#pragma unroll
+        for (int ks = 0; ks < K3; ++ks) w3r[ks] = w3s[ks * 64 + lane];
+      }
+#pragma nounroll
       for (int mt = 0; mt < MT; ++mt) {
         const int row = mt * 16 + (lane & 15);
-        B a3[K3];
-#pragma unroll
-        for (int ks = 0; ks < K3; ++ks) a3[ks] = load_operand_lds<DT>(h2s, LD2, row, ks, lane);
         const f32x4 nz4 = *reinterpret_cast<const f32x4*>(&nz[k & 1][row * 8 + 4 * (g & 1)]);
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < K3; ++ks) acc = mfma16<DT>(w3r[ks], a3[ks], acc);
+        for (int ks = 0; ks < K3; ++ks) {
+          // (keeps the W3 loads in the loop: hoisted out of it they would hold
+          // registers through the whole step)
+          if constexpr (!DIRECT) asm volatile("" ::: "memory");
+          acc = mfma16<DT>(DIRECT ? w3r[DIRECT ? ks : 0] : w3s[ks * 64 + lane],
+                           load_operand_lds<DT>(h2s, LD2, row, ks, lane), acc);
+        }
         float best_s = -INFINITY;
         int best_a = 0;
         float logit[4];
@@ -651,6 +675,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
         if (out.reward) out.reward[(size_t)k * E + e] = r;
         if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
+        if constexpr (LEAN) env_s[el] = s;
       }
     } else if (k + 1 < n_steps && (k + 1) % NOISE_STEPS != 0) {
       // the other waves: Gumbel noise of the next step, while the env wave steps
@@ -661,6 +686,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   __syncthreads();
   if (out.obs_last)
     copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, te_valid * A, tid);
+  if constexpr (LEAN) s = env_s[min(el, TE - 1)];
   if (envlane) lbf_store<A, F>(state, p, e, s);
 }
 
@@ -691,6 +717,7 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
   RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2)
   RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1)
   RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2)
+  RL_REG_CASE(DT_BF16, 12, 12, 256, 256, 3, 6, 16, 8, 1)
 #undef RL_REG_CASE
   return false;
 }

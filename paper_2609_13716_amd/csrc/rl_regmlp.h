@@ -72,7 +72,10 @@ __device__ __forceinline__ typename BOperand<DT>::type load_operand_lds(const ty
   }
 }
 
-template <int DT, int K, int N, int NW>
+// BL: the bias lives in an fp32 LDS array of N entries (filled by the caller
+// before the first store_tanh) instead of registers, for layers whose
+// resident weights leave no room for it.
+template <int DT, int K, int N, int NW, bool BL = false>
 struct RegLayer {
   using T = typename DType<DT>::T;
   using B = typename BOperand<DT>::type;
@@ -80,10 +83,12 @@ struct RegLayer {
   static constexpr int KSTEPS = round_up(K, KS) / KS;
   static constexpr int NT = N / 16;
   static constexpr int OWN = (NT + NW - 1) / NW;
+  // VGPRs per lane that the resident operands take
+  static constexpr int WREGS = OWN * KSTEPS * (int)(sizeof(B) / 4) + (BL ? 0 : 4 * OWN);
   static_assert(N % 16 == 0, "layer width must be a multiple of 16");
 
-  B w[OWN][KSTEPS];   // operand of output units tile*16 + lane%16
-  float bias[OWN][4]; // bias of output units tile*16 + 4*(lane/16) + r
+  B w[OWN][KSTEPS];                 // operand of output units tile*16 + lane%16
+  float bias[BL ? 1 : OWN][4];      // bias of output units tile*16 + 4*(lane/16) + r
 
   __device__ __forceinline__ void load(const T* __restrict__ W, const T* __restrict__ b, int wave, int lane) {
 #pragma unroll
@@ -94,8 +99,11 @@ struct RegLayer {
       const T* row = W + (size_t)(valid ? n : 0) * K;
 #pragma unroll
       for (int ks = 0; ks < KSTEPS; ++ks) w[o][ks] = load_operand_global<DT, K>(row, K, ks, lane, valid);
+      if constexpr (!BL) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) bias[o][r] = valid ? DType<DT>::to_f32(b[tile * 16 + 4 * (lane >> 4) + r]) : 0.f;
+        for (int r = 0; r < 4; ++r)
+          bias[o][r] = valid ? DType<DT>::to_f32(b[tile * 16 + 4 * (lane >> 4) + r]) : 0.f;
+      }
     }
   }
 
@@ -138,7 +146,8 @@ struct RegLayer {
   // out = tanh(acc + bias) in the layer dtype: four consecutive units of one
   // row per lane, stored with one 8-byte (bf16) or 16-byte (f32) LDS write.
   template <int MT>
-  __device__ __forceinline__ void store_tanh(const f32x4 (&acc)[MT][OWN], T* out, int ld, int wave, int lane) const {
+  __device__ __forceinline__ void store_tanh(const f32x4 (&acc)[MT][OWN], T* out, int ld, int wave, int lane,
+                                             const float* bias_lds = nullptr) const {
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -146,9 +155,18 @@ struct RegLayer {
         if (NT % NW != 0 && wave + o * NW >= NT) continue;
         const int row = m * 16 + (lane & 15);
         const int col = (wave + o * NW) * 16 + 4 * (lane >> 4);
+        float bo[4];
+        if constexpr (BL) {
+          const f32x4 b4 = *reinterpret_cast<const f32x4*>(bias_lds + col);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) bo[r] = b4[r];
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) bo[r] = bias[o][r];
+        }
         float v[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = fast_tanh(acc[m][o][r] + bias[o][r]);
+        for (int r = 0; r < 4; ++r) v[r] = fast_tanh(acc[m][o][r] + bo[r]);
         if constexpr (DT == DT_F32) {
           *reinterpret_cast<f32x4*>(out + row * ld + col) = f32x4{v[0], v[1], v[2], v[3]};
         } else {

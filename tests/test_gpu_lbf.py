@@ -354,7 +354,35 @@ def test_rollout_run_12x12_sampled_envs():
     assert [states_from_device(cfg, state)[e] for e in sample] == ref["states"]
 
 
-@pytest.mark.parametrize("name,dtype", [("lbf8_4096", "bf16"), ("lbf8_4096", "f32"), ("lbf8_small", "f32")])
+def test_rollout_run_12x12_small_full_parity():
+    """Every env of a 12x12 batch that spans three workgroups and a ragged tail, against the oracle."""
+    require_gpu()
+    name = "lbf12_16k"
+    w = workloads.WORKLOADS[name]
+    cfg = R.EnvConfig(n_envs=37, seed=6, env_base=40, **w["env"])
+    dims = workloads.policy_dims(name)
+    ws, bs = workloads.policy_weights(dims, seed=1003, bias_scale=0.1)
+    pol = R.Policy(ws, bs, "bf16")
+    T = 70
+    _note(f"rollout_run {name} n_envs=37 T={T} bf16")
+    state, g = _run_gpu(cfg, pol, T)
+    oc = oracle_cfg(cfg)
+    env_ids = list(range(40, 77))
+    hook = NearTieLockstep(g["actions"].numpy(), cfg.seed, env_ids, RTOL["bf16"])
+    ref = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, "bf16", action_hook=hook)
+    _check_traj(g, ref, slice(None), RTOL["bf16"])
+    assert states_from_device(cfg, state) == ref["states"]
+    assert ref["done"].any(), "the run should cross episode ends (max_steps 50)"
+    strict = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, "bf16",
+                             logits_source=lambda k, _: g["logits"][k].numpy())
+    assert np.array_equal(strict["actions"], g["actions"].numpy())
+    obs = g["obs"].reshape(-1, dims[0]).cuda()
+    pf = R.policy_forward(pol, obs).cpu().reshape(g["logits"].shape)
+    assert torch.equal(pf, g["logits"])
+
+
+@pytest.mark.parametrize("name,dtype", [("lbf8_4096", "bf16"), ("lbf8_4096", "f32"), ("lbf8_small", "f32"),
+                                        ("lbf12_16k", "bf16")])
 def test_rollout_logits_equal_policy_forward(name, dtype):
     """The logits a rollout samples from are exactly policy_forward of the recorded observations."""
     require_gpu()
