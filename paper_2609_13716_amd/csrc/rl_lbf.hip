@@ -404,19 +404,36 @@ __device__ __forceinline__ void lbf_paint_tile(const LbfEnv& s, int el, T* xs, i
 }
 
 // Copy the tile's live observation rows from LDS to global [.., A, D] rows
-// with 16-byte vectors.
-template <typename T, int R, int D, int LDX, int NT>
-__device__ __forceinline__ void copy_obs_rows(const T* xs, T* __restrict__ g, int rows_live, int tid) {
+// with 16-byte vectors (g == nullptr: no copy).  CLEAR: each vector is
+// zeroed in LDS after it is read, which leaves the tile blank for the next
+// paint.  The vectors of a thread go in groups of G: all reads of a group
+// are issued before its first store, so a group waits for LDS once.
+template <typename T, int R, int D, int LDX, int NT, bool CLEAR = false, int G = 4>
+__device__ __forceinline__ void copy_obs_rows(T* xs, T* __restrict__ g, int rows_live, int tid) {
   constexpr int VE = 16 / sizeof(T);
   static_assert(D % VE == 0, "observation rows must be whole 16-byte vectors");
   constexpr int VPR = D / VE;
   constexpr int NV = R * VPR;
+  constexpr int IT = (NV + NT - 1) / NT;
 #pragma unroll
-  for (int it = 0; it < (NV + NT - 1) / NT; ++it) {
-    const int v = tid + it * NT;
-    const int r = v / VPR, c = (v - r * VPR) * VE;
-    if (v < NV && r < rows_live)
-      *reinterpret_cast<u32x4*>(g + (size_t)r * D + c) = *reinterpret_cast<const u32x4*>(xs + r * LDX + c);
+  for (int i0 = 0; i0 < IT; i0 += G) {
+    u32x4 val[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      const int v = tid + (i0 + j) * NT;
+      const int r = v / VPR, c = (v - r * VPR) * VE;
+      // rows past rows_live are inside the tile: reading them is harmless
+      if (i0 + j < IT && (NV % NT == 0 || v < NV)) val[j] = *reinterpret_cast<const u32x4*>(xs + r * LDX + c);
+    }
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      const int v = tid + (i0 + j) * NT;
+      const int r = v / VPR, c = (v - r * VPR) * VE;
+      if (i0 + j < IT && (NV % NT == 0 || v < NV) && r < rows_live) {
+        if (g) *reinterpret_cast<u32x4*>(g + (size_t)r * D + c) = val[j];
+        if constexpr (CLEAR) *reinterpret_cast<u32x4*>(xs + r * LDX + c) = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
   }
 }
 
@@ -426,8 +443,9 @@ __device__ __forceinline__ void copy_obs_rows(const T* xs, T* __restrict__ g, in
 //     rollout; layers are computed transposed so each lane ends with four
 //     consecutive outputs of one row;
 //   * observations are painted by the env lanes straight into the layer-1
-//     operand tile (only the non-zero features change), and copied to the
-//     trajectory while the layer-2 MFMAs run;
+//     operand tile (only the non-zero features are written), and copied to
+//     the trajectory while the layer-2 MFMAs run by all waves, which clear
+//     the tile behind the copy;
 //   * the Philox action draws of NOISE_STEPS steps are made in one batch by
 //     all lanes; the Gumbel noise of step k+1 is evaluated from them by the
 //     other waves while the env wave steps the envs at step k;
@@ -561,11 +579,10 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     {
       f32x4 acc[MT][RegLayer<DT, H1, H2, NW, LEAN>::OWN];
       L2.template run<MT>(h1s, LD1, acc, wave, lane);
-      // o_t to the trajectory while the layer-2 MFMAs run (the tile is only
-      // repainted after layer 3)
-      if (out.obs)
-        copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D, te_valid * A,
-                                        tid);
+      // o_t to the trajectory while the layer-2 MFMAs run, clearing the tile
+      // behind the copy (the env wave paints o_{t+1} onto it after layer 3)
+      copy_obs_rows<T, R, D, LDX, NT, true>(
+          xs, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, te_valid * A, tid);
       L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane, bias_s + H1);
     }
     __syncthreads();
@@ -650,7 +667,6 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
           else
             act[i] = i < A ? act_s[lane * A + i] : 0;
         }
-        lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, false);
         lbf_transition<A, F, GH, GW>(p, s, act, r, d);
       }
       // reset blocks of every env that ended, one Philox block per lane
@@ -727,10 +743,11 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
 // rollout_step for compile-time LBF shapes.  Wave 0 owns TE envs (lanes
 // 0..TE-1 keep the env state in registers) and paints each step's
 // observation rows into one of two LDS tiles; wave 1 copies the tile of the
-// previous step to the trajectory with 16-byte stores, so the copy overlaps
-// the next transition.  The paint is incremental: a tile is updated from the
-// state it held two steps earlier (kept in registers).  The chunk's actions
-// are staged in LDS first, so the step loop has no global loads.
+// previous step to the trajectory with 16-byte stores and clears it behind
+// the copy, so that the copy overlaps the next transition and the env lanes
+// paint onto a blank tile (no erase on their path).  The chunk's actions are
+// staged in LDS first and read one step ahead, so the step loop has no
+// global loads.
 template <typename OT, int GH, int GW, int A, int F, int TE>
 __global__ __launch_bounds__(128) void lbf_env_kernel(LbfParams p, int32_t* __restrict__ state, uint64_t t0,
                                                       int n_steps, const int32_t* __restrict__ actions,
@@ -753,27 +770,26 @@ __global__ __launch_bounds__(128) void lbf_env_kernel(LbfParams p, int32_t* __re
 
   zero_lds<128>(xs, sizeof(xs), tid);
   __syncthreads();
-  LbfEnv s{}, sprev{};  // the state, and the state before the last transition (what the other tile shows)
+  LbfEnv s{};
   if (envlane) lbf_load<A, F>(state, p, e, s);
   for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
     const int nk = min(ACT_CHUNK, n_steps - k0);
     stage_actions<TE * A, 128>(actions, E, e0, te_valid * A, A, k0, nk, act_lds, tid);
     __syncthreads();
+    // the env lane's actions of the next step, read one step ahead
+    int act[LBF_MAXA] = {0, 0, 0, 0};
+    if (envlane) {
+#pragma unroll
+      for (int i = 0; i < A; ++i) act[i] = act_lds[lane * A + i];
+    }
     for (int kk = 0; kk < nk; ++kk) {
       const int k = k0 + kk;
-      OT* tile = xs[k & 1];
+      OT* tile = xs[k & 1];  // blank: wave 1 cleared it when it copied step k-2
       if (wave == 0) {
         const uint64_t t = t0 + (uint64_t)k;
         uint32_t d = 0;
         float r = 0.f;
-        if (envlane) {
-          int act[LBF_MAXA] = {0, 0, 0, 0};
-#pragma unroll
-          for (int i = 0; i < A; ++i) act[i] = act_lds[kk * TE * A + lane * A + i];
-          if (k >= 2) lbf_paint_tile<OT, A, F>(sprev, lane, tile, D, HW, false);  // the tile shows step k-2
-          sprev = s;
-          lbf_transition<A, F, GH, GW>(p, s, act, r, d);
-        }
+        if (envlane) lbf_transition<A, F, GH, GW>(p, s, act, r, d);
         const uint64_t done_mask = __ballot(envlane && d != 0);
         if (done_mask) {
           const int j = lane / nblk, blk = lane - j * nblk;
@@ -792,14 +808,20 @@ __global__ __launch_bounds__(128) void lbf_env_kernel(LbfParams p, int32_t* __re
           }
         }
         if (envlane) {
-          lbf_paint_tile<OT, A, F>(s, lane, tile, D, HW, true);
+          if (obs) lbf_paint_tile<OT, A, F>(s, lane, tile, D, HW, true);
           if (reward) reward[(size_t)k * E + e] = r;
           if (done) done[(size_t)k * E + e] = (uint8_t)d;
+          if (kk + 1 < nk) {
+#pragma unroll
+            for (int i = 0; i < A; ++i) act[i] = act_lds[(kk + 1) * TE * A + lane * A + i];
+          }
         }
       }
-      __syncthreads();  // tile k is painted; tile k-1 is copied
+      __syncthreads();  // tile k is painted; tile k-1 is copied and cleared
       if (wave == 1) {
-        if (obs) copy_obs_rows<OT, R, D, D, 64>(tile, obs + ((size_t)k * E + e0) * A * D, te_valid * A, lane);
+        if (obs)
+          copy_obs_rows<OT, R, D, D, 64, true, ((R * D * sizeof(OT) / 16 + 63) / 64 < 8 ? (R * D * sizeof(OT) / 16 + 63) / 64 : 8)>(
+              tile, obs + ((size_t)k * E + e0) * A * D, te_valid * A, lane);
         if (legal) lbf_write_legal<64>(p, te_valid, legal + ((size_t)k * E + e0) * A * LBF_NACT, lane);
       }
     }
@@ -825,6 +847,13 @@ static bool try_launch_env_ct(const LbfParams& p, int32_t* state, uint64_t t0, i
                                                                    legal, s)
                             : launch_env_ct<uint16_t, 8, 8, 2, 3, 8>(p, state, t0, n_steps, actions, obs, reward,
                                                                       done, legal, s);
+    return true;
+  }
+  if (p.H == 12 && p.W == 12 && p.A == 3 && p.F == 6) {
+    *err = obs_dt == DT_F32 ? launch_env_ct<float, 12, 12, 3, 6, 8>(p, state, t0, n_steps, actions, obs, reward,
+                                                                     done, legal, s)
+                            : launch_env_ct<uint16_t, 12, 12, 3, 6, 8>(p, state, t0, n_steps, actions, obs, reward,
+                                                                        done, legal, s);
     return true;
   }
   return false;

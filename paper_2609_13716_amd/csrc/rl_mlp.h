@@ -30,6 +30,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float x) { return __builtin_bit_
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
+// Two floats -> two bfloat16 in one dword (lo in bits 0-15), round to nearest
+// even: one v_cvt_pk_bf16_f32, the same rounding as f32_to_bf16.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
+}
+
 template <int DT>
 struct DType;
 template <>

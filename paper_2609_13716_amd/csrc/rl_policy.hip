@@ -1,5 +1,7 @@
 // Standalone policy forward (obs -> logits on the MFMA MLP), standalone
 // Gumbel-max sampling from given logits, and the sampler's noise function.
+#include <type_traits>
+
 #include "rl_internal.h"
 #include "rl_regmlp.h"
 #include "rl_sample.h"
@@ -228,10 +230,321 @@ static bool try_launch_policy_reg(const PolicyArgs& pol, const void* obs, const 
   return false;
 }
 
+// ------------------------------------------------ tiled policy forward ----
+//
+// bf16 policy forward for wide layers (the 12x12 LBF, kitchen and Hanabi
+// policies), structured as three chained GEMMs per tile of BM rows:
+//   * 4 waves in a 2 x 2 grid over (output units, rows); each wave holds the
+//     fp32 accumulators of HMAX/2 units x BM/2 rows for a whole layer;
+//   * layer-1 weights and observations, and layer-2 weights, are staged
+//     through a ring of NB LDS buffers, one K slice of 32 at a time; every
+//     weight byte staged serves all BM rows of the tile.  With NB = 3 the
+//     global loads of slice s+3 are issued a full step before they are
+//     stored to LDS, and the MFMA operands of slice s+1 are read from LDS
+//     while the MFMAs of slice s run;
+//   * h1 stays in LDS; h2 overwrites it once layer 2 has read it;
+//   * layer 3 is computed transposed (actions x rows) from h2.
+// As in the register-resident kernels, every output is one MFMA chain over K
+// in increasing order, bias added after, so the logits are bit-identical to
+// the other policy paths.
+constexpr int PT_KC = 32;  // K slice per step: one bf16 MFMA K step
+constexpr int PT_NT = 256;
+
+template <int HMAX, int BM, int NB>
+struct PtLayout {
+  static constexpr int LDH = HMAX + 8;  // pitch of the resident activation tile
+  static constexpr size_t H_BYTES = (size_t)BM * LDH * 2;
+  static constexpr size_t W_BYTES = (size_t)HMAX * PT_KC * 2;  // one staged weight slice
+  static constexpr size_t X_BYTES = (size_t)BM * PT_KC * 2;    // one staged observation slice
+  static constexpr size_t OFF_W = H_BYTES;
+  static constexpr size_t OFF_X = OFF_W + NB * W_BYTES;
+  static constexpr size_t OFF_B = OFF_X + NB * X_BYTES;  // fp32 biases of layers 1 and 2
+  static constexpr size_t TOTAL = OFF_B + 2 * HMAX * 4;
+};
+
+// Element offset of 16-byte vector q (k = 8q..8q+7) of row n in a staged
+// slice: rows of 64 bytes, vectors XOR-swizzled by (n / 2) % 4 so that any 8
+// consecutive rows of an MFMA operand read fill the 32 LDS banks without
+// conflict.  The swizzle does not change when n moves by 16 (an operand tile).
+__device__ __forceinline__ int pt_slot(int n, int q) { return n * PT_KC + 8 * (q ^ ((n >> 1) & 3)); }
+
+// Buffer resource over `bytes` bytes at p (raw: loads past the end read 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t pt_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+// Zero the elements of an 8-element bf16 vector at or beyond `left` (the
+// number of the vector's elements that lie inside the row).
+__device__ __forceinline__ u32x4 pt_mask8(u32x4 v, int left) {
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t m = 2 * d + 1 < left ? 0xffffffffu : 2 * d < left ? 0x0000ffffu : 0u;
+    v[d] &= m;
+  }
+  return v;
+}
+
+template <int HMAX, int BM, int NB, int MINB>
+__global__ __launch_bounds__(PT_NT, MINB) void policy_fwd_tiled_kernel(PolicyArgs pol, const uint16_t* __restrict__ obs,
+                                                                 const uint8_t* __restrict__ legal, int64_t rows,
+                                                                 float* __restrict__ logits) {
+  using L = PtLayout<HMAX, BM, NB>;
+  constexpr int UT = HMAX / 32;  // unit tiles of a wave (half the units)
+  constexpr int RT = BM / 32;    // row tiles of a wave (half the rows)
+  constexpr int HH = HMAX / 2;   // units of a wave
+  constexpr int WV = HMAX * 4 / PT_NT, XV = (BM * 4 + PT_NT - 1) / PT_NT;  // staged vectors per thread
+  static_assert(NB == 2 || NB == 3, "two or three slice buffers");
+  static_assert(HMAX * 4 % PT_NT == 0, "whole weight vectors per thread");
+  extern __shared__ __align__(16) uint8_t smem[];
+  uint16_t* hs = reinterpret_cast<uint16_t*>(smem);
+  uint16_t* wst = reinterpret_cast<uint16_t*>(smem + L::OFF_W);
+  uint16_t* xst = reinterpret_cast<uint16_t*>(smem + L::OFF_X);
+  float* bias_s = reinterpret_cast<float*>(smem + L::OFF_B);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wu = wave & 1, wr = wave >> 1;
+  const int D = pol.D, NA = pol.NA;
+  const int64_t row0 = (int64_t)blockIdx.x * BM;
+  const int nrow = (int)min((int64_t)BM, rows - row0);
+  const uint16_t* W3 = static_cast<const uint16_t*>(pol.W[2]);
+
+  for (int i = tid; i < 2 * HMAX; i += PT_NT)
+    bias_s[i] = bf16_to_f32(i < HMAX ? static_cast<const uint16_t*>(pol.b[0])[i]
+                                     : static_cast<const uint16_t*>(pol.b[1])[i - HMAX]);
+
+  // One dense tanh layer of HMAX units: out = tanh(in W^T + b) into hs.
+  // Layer 1 (tag true) stages observation rows with the weights; layer 2
+  // reads its input from hs.
+  auto layer = [&](auto l1_tag, const uint16_t* __restrict__ W, int K, const float* bias) {
+    constexpr bool L1 = decltype(l1_tag)::value;
+    const int nsteps = (K + PT_KC - 1) / PT_KC;
+    // Weight slices are fetched one step before they are stored to LDS (they
+    // come from L2); observation slices, which come from HBM, PX steps
+    // before, through a ring of PX register slots (slot = slice % PX).
+    constexpr int PX = NB == 3 ? 4 : 1;
+    u32x4 wv[WV], xv[PX][XV];
+    // per-thread byte offsets of the staged vectors (global) and their LDS
+    // slots, fixed for the layer; the slice offset goes in a scalar register
+    const __amdgpu_buffer_rsrc_t wres = pt_rsrc(W, (uint32_t)HMAX * K * 2);
+    const __amdgpu_buffer_rsrc_t xres = pt_rsrc(obs + (size_t)row0 * D, (uint32_t)nrow * D * 2);
+    int wgo[WV], wlo[WV], xgo[XV], xlo[XV];
+#pragma unroll
+    for (int j = 0; j < WV; ++j) {
+      const int v = tid + j * PT_NT, n = v >> 2, q = v & 3;
+      wgo[j] = (n * K + 8 * q) * 2;
+      wlo[j] = pt_slot(n, q);
+    }
+#pragma unroll
+    for (int j = 0; j < XV; ++j) {
+      const int v = tid + j * PT_NT, r = v >> 2, q = v & 3;
+      xgo[j] = (r * D + 8 * q) * 2;  // rows past nrow lie past the resource: read as 0
+      xlo[j] = pt_slot(r, q);
+    }
+    constexpr bool XALL = BM * 4 % PT_NT == 0;  // every thread stages XV observation vectors
+    auto fetch_w = [&](int st) {
+#pragma unroll
+      for (int j = 0; j < WV; ++j) wv[j] = __builtin_amdgcn_raw_buffer_load_b128(wres, wgo[j], st * PT_KC * 2, 0);
+    };
+    auto fetch_x = [&](int st, u32x4 (&x)[XV]) {
+      if constexpr (L1) {
+#pragma unroll
+        for (int j = 0; j < XV; ++j)
+          if (XALL || tid + j * PT_NT < BM * 4)
+            x[j] = __builtin_amdgcn_raw_buffer_load_b128(xres, xgo[j], st * PT_KC * 2, 0);
+      }
+    };
+    // store slice st to LDS buffer st % NB, zeroing what lies past K in the
+    // partial last slice (uniform branch; q = tid % 4 for every vector)
+    auto stage = [&](int st, u32x4 (&x)[XV]) {
+      const int k0 = st * PT_KC;
+      const bool part = k0 + PT_KC > K;
+      const int left = K - k0 - 8 * (tid & 3);
+      uint16_t* wb = wst + (st % NB) * (HMAX * PT_KC);
+#pragma unroll
+      for (int j = 0; j < WV; ++j) *reinterpret_cast<u32x4*>(wb + wlo[j]) = part ? pt_mask8(wv[j], left) : wv[j];
+      if constexpr (L1) {
+        uint16_t* xb = xst + (st % NB) * (BM * PT_KC);
+#pragma unroll
+        for (int j = 0; j < XV; ++j)
+          if (XALL || tid + j * PT_NT < BM * 4)
+            *reinterpret_cast<u32x4*>(xb + xlo[j]) = part ? pt_mask8(x[j], left) : x[j];
+      }
+    };
+    // MFMA operands of slice st (staged in buffer st % NB): unit tiles of W
+    // and row tiles of the input, at fixed offsets from one lane base each
+    const int a_lo = pt_slot(wu * HH + (lane & 15), lane >> 4);
+    const int b_lo = L1 ? pt_slot(wr * (BM / 2) + (lane & 15), lane >> 4)
+                        : (wr * (BM / 2) + (lane & 15)) * L::LDH + 8 * (lane >> 4);
+    auto frags = [&](int st, u32x4 (&a)[UT], u32x4 (&b)[RT]) {
+      const uint16_t* wb = wst + (st % NB) * (HMAX * PT_KC) + a_lo;
+#pragma unroll
+      for (int ut = 0; ut < UT; ++ut) a[ut] = *reinterpret_cast<const u32x4*>(wb + ut * 16 * PT_KC);
+      if constexpr (L1) {
+        const uint16_t* xb = xst + (st % NB) * (BM * PT_KC) + b_lo;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) b[rt] = *reinterpret_cast<const u32x4*>(xb + rt * 16 * PT_KC);
+      } else {
+        const uint16_t* hb = hs + b_lo + st * PT_KC;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) b[rt] = *reinterpret_cast<const u32x4*>(hb + rt * 16 * L::LDH);
+      }
+    };
+    f32x4 acc[UT][RT];
+#pragma unroll
+    for (int ut = 0; ut < UT; ++ut)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) acc[ut][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto mma = [&](const u32x4 (&a)[UT], const u32x4 (&b)[RT]) {
+#pragma unroll
+      for (int ut = 0; ut < UT; ++ut)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) acc[ut][rt] = mfma16<DT_BF16>(a[ut], b[rt], acc[ut][rt]);
+    };
+    if constexpr (NB == 3) {
+      // prologue: slices 0 and 1 in LDS, weights of slice 2 and observations
+      // of slices 2 .. PX+1 in flight
+      fetch_w(0);
+      fetch_x(0, xv[0]);
+      stage(0, xv[0]);
+      if (1 < nsteps) {
+        fetch_w(1);
+        fetch_x(1, xv[1]);
+        stage(1, xv[1]);
+      }
+      if (2 < nsteps) fetch_w(2);
+#pragma unroll
+      for (int u = 2; u < PX + 2; ++u)
+        if (u < nsteps) fetch_x(u, xv[u % PX]);
+      __syncthreads();
+      u32x4 a0[UT], b0[RT], a1[UT], b1[RT];
+      frags(0, a0, b0);
+      // one step (U = st % PX): store slice st+2 (its buffer was last read at
+      // step st-1), fetch the weights of slice st+3 and the observations of
+      // slice st+2+PX into the slot just stored, read slice st+1's operands,
+      // then run slice st's MFMAs, behind which these memory operations land
+      auto step = [&](auto u_tag, int st, const u32x4 (&a)[UT], const u32x4 (&b)[RT], u32x4 (&an)[UT],
+                      u32x4 (&bn)[RT]) {
+        constexpr int U = decltype(u_tag)::value;
+        if (st + 2 < nsteps) stage(st + 2, xv[(U + 2) % PX]);
+        if (st + 3 < nsteps) fetch_w(st + 3);
+        if (st + 2 + PX < nsteps) fetch_x(st + 2 + PX, xv[(U + 2) % PX]);
+        if (st + 1 < nsteps) frags(st + 1, an, bn);
+        mma(a, b);
+        __syncthreads();
+      };
+      static_assert(PX % 2 == 0, "operand registers alternate within the unrolled steps");
+      for (int st = 0; st < nsteps; st += 4) {
+        step(std::integral_constant<int, 0>{}, st, a0, b0, a1, b1);
+        if (st + 1 < nsteps) step(std::integral_constant<int, 1>{}, st + 1, a1, b1, a0, b0);
+        if (st + 2 < nsteps) step(std::integral_constant<int, 2>{}, st + 2, a0, b0, a1, b1);
+        if (st + 3 < nsteps) step(std::integral_constant<int, 3>{}, st + 3, a1, b1, a0, b0);
+      }
+    } else {
+      fetch_w(0);
+      fetch_x(0, xv[0]);
+      stage(0, xv[0]);
+      __syncthreads();
+      for (int st = 0; st < nsteps; ++st) {
+        if (st + 1 < nsteps) {
+          fetch_w(st + 1);
+          fetch_x(st + 1, xv[0]);
+        }
+        u32x4 a[UT], b[RT];
+        frags(st, a, b);
+        mma(a, b);
+        if (st + 1 < nsteps) stage(st + 1, xv[0]);
+        __syncthreads();
+      }
+    }
+    // every wave is past its last read of hs (layer 2 input): overwrite it
+#pragma unroll
+    for (int ut = 0; ut < UT; ++ut) {
+      const int u0 = wu * HH + ut * 16 + 4 * (lane >> 4);
+      const f32x4 b4 = *reinterpret_cast<const f32x4*>(bias + u0);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const int r = wr * (BM / 2) + rt * 16 + (lane & 15);
+        float v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = fast_tanh(acc[ut][rt][q] + b4[q]);
+        const uint32_t lo = pack_bf16x2(v[0], v[1]);
+        const uint32_t hi = pack_bf16x2(v[2], v[3]);
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        *reinterpret_cast<u32x2*>(hs + r * L::LDH + u0) = u32x2{lo, hi};
+      }
+    }
+    __syncthreads();
+  };
+  layer(std::true_type{}, static_cast<const uint16_t*>(pol.W[0]), D, bias_s);
+  layer(std::false_type{}, static_cast<const uint16_t*>(pol.W[1]), HMAX, bias_s + HMAX);
+
+  // layer 3, transposed: logits^T = W3 h2^T, items (action tile, row tile)
+  constexpr int K3 = HMAX / PT_KC;
+  const int nat = (NA + 15) >> 4;
+  for (int item = wave; item < nat * (BM / 16); item += PT_NT / 64) {
+    const int mt = item % nat, rt = item / nat;
+    const int a_row = mt * 16 + (lane & 15);
+    const uint16_t* w3r = W3 + (size_t)(a_row < NA ? a_row : 0) * HMAX + 8 * (lane >> 4);
+    const int r = rt * 16 + (lane & 15);
+    u32x4 a3[K3];
+#pragma unroll
+    for (int ks = 0; ks < K3; ++ks)
+      a3[ks] = a_row < NA ? *reinterpret_cast<const u32x4*>(w3r + ks * PT_KC) : u32x4{0u, 0u, 0u, 0u};
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < K3; ++ks)
+      acc = mfma16<DT_BF16>(a3[ks], *reinterpret_cast<const u32x4*>(hs + r * L::LDH + ks * PT_KC + 8 * (lane >> 4)),
+                            acc);
+    if (r < nrow) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int act = mt * 16 + 4 * (lane >> 4) + q;
+        if (act < NA) {
+          const size_t gi = (size_t)(row0 + r) * NA + act;
+          const float lg = acc[q] + bf16_to_f32(static_cast<const uint16_t*>(pol.b[2])[act]);
+          logits[gi] = (legal == nullptr || legal[gi] != 0) ? lg : -INFINITY;
+        }
+      }
+    }
+  }
+}
+
+template <int HMAX, int BM, int NB, int MINB>
+static hipError_t launch_policy_tiled(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
+                                      float* logits, hipStream_t s) {
+  using L = PtLayout<HMAX, BM, NB>;
+  static_assert(L::TOTAL <= MAX_LDS_BYTES, "tile fits in LDS");
+  static bool attr = false;
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute((const void*)policy_fwd_tiled_kernel<HMAX, BM, NB, MINB>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::TOTAL);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const unsigned grid = (unsigned)((rows + BM - 1) / BM);
+  policy_fwd_tiled_kernel<HMAX, BM, NB, MINB><<<dim3(grid), PT_NT, L::TOTAL, s>>>(
+      pol, static_cast<const uint16_t*>(obs), legal, rows, logits);
+  return hipGetLastError();
+}
+
+// Shapes the tiled kernel serves: bf16, two hidden layers of 256 or of 512
+// units, an even input width.
+static bool try_launch_policy_tiled(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
+                                    float* logits, hipStream_t s, hipError_t* err) {
+  if (pol.dt != DT_BF16 || pol.D % 2 != 0 || pol.H1 != pol.H2 || pol.NA > MAX_NA) return false;
+  if (pol.H1 == 256)
+    *err = launch_policy_tiled<256, 128, 3, 1>(pol, obs, legal, rows, logits, s);
+  else if (pol.H1 == 512)
+    *err = launch_policy_tiled<512, 64, 2, 1>(pol, obs, legal, rows, logits, s);
+  else
+    return false;
+  return true;
+}
+
 hipError_t launch_policy_forward(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
                                  float* logits, hipStream_t s) {
   hipError_t err;
   if (try_launch_policy_reg(pol, obs, legal, rows, logits, s, &err)) return err;
+  if (try_launch_policy_tiled(pol, obs, legal, rows, logits, s, &err)) return err;
   const PolicyLayout PL = pick_policy_layout(pol);
   const dim3 grid((unsigned)((rows + PL.BM - 1) / PL.BM));
   if (pol.dt == DT_F32) {

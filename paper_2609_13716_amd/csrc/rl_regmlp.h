@@ -170,8 +170,8 @@ struct RegLayer {
         if constexpr (DT == DT_F32) {
           *reinterpret_cast<f32x4*>(out + row * ld + col) = f32x4{v[0], v[1], v[2], v[3]};
         } else {
-          const uint32_t lo = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
-          const uint32_t hi = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+          const uint32_t lo = pack_bf16x2(v[0], v[1]);
+          const uint32_t hi = pack_bf16x2(v[2], v[3]);
           typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
           *reinterpret_cast<u32x2*>(out + row * ld + col) = u32x2{lo, hi};
         }

@@ -92,6 +92,8 @@ def test_init_matches_oracle(dtype):
     (dict(n_envs=37), 120, torch.bfloat16),
     (dict(n_envs=21, grid_h=12, grid_w=12, n_agents=3, n_food=6, max_agent_level=3, max_food_level=6), 110,
      torch.bfloat16),
+    (dict(n_envs=13, grid_h=12, grid_w=12, n_agents=3, n_food=6, max_agent_level=3, max_food_level=6), 70,
+     torch.float32),
     (dict(n_envs=19, grid_h=5, grid_w=7, n_agents=4, n_food=2, max_agent_level=3, max_food_level=9,
           max_steps=13), 60, torch.float32),
     (dict(n_envs=5, grid_h=3, grid_w=3, n_agents=2, n_food=1, max_steps=7), 40, torch.float32),
@@ -200,7 +202,7 @@ def test_brute_force_3x3_gpu():
 # ------------------------------------------------------------------ policy
 
 @pytest.mark.parametrize("dims", [(192, 64, 64, 6), (192, 128, 128, 6), (432, 256, 256, 6), (27, 16, 32, 6),
-                                  (658, 512, 512, 20)])
+                                  (658, 512, 512, 20), (1170, 256, 256, 6), (1170, 64, 96, 6), (300, 512, 32, 20)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_policy_forward_parity(dims, dtype):
     require_gpu()
