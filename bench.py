@@ -154,6 +154,16 @@ def measure_workload(R, workloads, name, dt, steps, warmup):
     out["env_only"] = {"env_steps_per_s": round(E * T / (wall_ms * 1e-3), 1), "kernel_ms": round(kern_ms, 4),
                        "roofline": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s")}
     del obs
+    # standalone policy forward over a batch of this workload's observations
+    rows = min(E * A * T, 1 << 18)
+    g.manual_seed(8)
+    x = torch.randint(0, 3, (rows, D), device="cuda", generator=g).to(pol.torch_dtype)
+    lg = torch.empty(rows, nA, device="cuda")
+    kern_ms, _ = timed(lambda: R.policy_forward(pol, x, logits=lg), steps, warmup)
+    out["policy_forward"] = {"rows": rows, "kernel_ms": round(kern_ms, 4),
+                             "roofline": roofline("mfma", rows * flop_per_row / (kern_ms * 1e-3) / 1e12,
+                                                  MFMA_PEAK_TFLOPS[dt], "TFLOP/s")}
+    del x, lg
     torch.cuda.empty_cache()
     return out
 
