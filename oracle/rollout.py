@@ -36,8 +36,34 @@ def observe_all(env, cfg, states):
     return obs, mask
 
 
+def policy_logits(obs, weights, biases, dtype, policy_index=None):
+    """Logits [n, A, nA] float64 of observations [n, A, D].
+
+    Without ``policy_index`` every agent uses the one network (weights,
+    biases).  With it, ``weights[p]`` and ``biases[p]`` are the layers of
+    policy p of a population and agent a of env index i acts with policy
+    ``policy_index[i][a]``: the ego agent and its teammates of the ad hoc
+    teamwork objective (Section 3, the J_AHT equation) each run their own
+    network.  An index outside the population selects policy 0 (reading).
+    """
+    n, A, D = obs.shape
+    flat = obs.reshape(n * A, D)
+    if policy_index is None:
+        return mlp.forward(flat, weights, biases, dtype).reshape(n, A, -1)
+    ids = np.asarray(policy_index, dtype=np.int64).reshape(n * A)
+    ids = np.where((ids >= 0) & (ids < len(weights)), ids, 0)
+    out = None
+    for p in np.unique(ids):
+        sel = ids == p
+        lg = mlp.forward(flat[sel], weights[p], biases[p], dtype)
+        if out is None:
+            out = np.zeros((n * A, lg.shape[1]), dtype=np.float64)
+        out[sel] = lg
+    return out.reshape(n, A, -1)
+
+
 def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
-            states=None, logits_source=None, action_hook=None):
+            states=None, logits_source=None, action_hook=None, policy_index=None):
     """Roll ``env_ids`` forward ``n_steps`` steps from absolute step ``t0``.
 
     ``states`` are the env states at t0 (default: the initial states, t0 = 0).
@@ -45,6 +71,8 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     sample from at step t0 + k instead of the oracle's own.
     ``action_hook(k, i, agent, action, logits32, mask)`` may replace the
     sampled action of env index i, agent ``agent``.
+    ``policy_index`` [n, A]: per-agent policies of a population (see
+    ``policy_logits``); ``weights`` and ``biases`` are then per policy.
     """
     env_ids = list(env_ids)
     if states is None:
@@ -58,7 +86,7 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     for k in range(n_steps):
         t = t0 + k
         obs, mask = observe_all(env, cfg, states)
-        logits64 = mlp.forward(obs.reshape(n * A, -1), weights, biases, dtype).reshape(n, A, nA)
+        logits64 = policy_logits(obs, weights, biases, dtype, policy_index)
         logits32 = logits64.astype(np.float32)
         if logits_source is not None:
             logits32 = np.asarray(logits_source(k, logits64), dtype=np.float32)
