@@ -170,6 +170,26 @@ rl_status policy_forward(const rl_policy* policy, const void* obs, const uint8_t
 rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* state,
                       uint64_t t0, int32_t n_steps, const rl_traj* out, void* stream);
 
+/* The rollout of rollout_run with one policy per agent slot, drawn from a
+ * population: the ego agent and its teammates of the ad hoc teamwork objective
+ * (Section 3, the J_AHT equation: the ego policy paired with teammate
+ * policies from a held-out set), e.g. the cross-play matrix of a population
+ * evaluated as one batch.  LBF envs only (RL_EUNSUPPORTED otherwise).
+ *   pop           one policy's dtype and dims, with W[l] pointing at
+ *                 n_policies matrices [dims[l+1], dims[l]] stacked
+ *                 ([n_policies, dims[l+1], dims[l]] row-major) and b[l] at
+ *                 [n_policies, dims[l+1]]; device memory, read.
+ *   n_policies    1..4096.
+ *   policy_index  [E, A] int32 device, read: agent a of env e acts with policy
+ *                 policy_index[e * A + a]; an index outside 0..n_policies-1
+ *                 selects policy 0.
+ * Everything else as rollout_run.  A workgroup's 16 envs run each layer once
+ * per distinct policy among their agents, so the cost grows with that count
+ * (assigning teammates to blocks of envs keeps it at two). */
+rl_status rollout_run_pop(const rl_env_config* cfg, const rl_policy* pop, int32_t n_policies,
+                          const int32_t* policy_index, void* state, uint64_t t0, int32_t n_steps,
+                          const rl_traj* out, void* stream);
+
 /* Gumbel-max sampling of the actions of step t from given logits (the
  * sampling stage of rollout_run on its own).
  *   logits  [E, A, nA] float32 read;  legal [E, A, nA] uint8 or NULL;

@@ -272,6 +272,34 @@ rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* s
                   "rollout_run");
 }
 
+rl_status rollout_run_pop(const rl_env_config* cfg, const rl_policy* pop, int32_t n_policies,
+                          const int32_t* policy_index, void* state, uint64_t t0, int32_t n_steps, const rl_traj* out,
+                          void* stream) {
+  EnvSpec es;
+  rl_status s = check_cfg(cfg, &es);
+  if (s != RL_OK) return s;
+  if (es.kind != RL_ENV_LBF) return fail(RL_EUNSUPPORTED, "rollout_run_pop is implemented for LBF only");
+  rl::PolicyArgs a;
+  s = check_policy(pop, &a);
+  if (s != RL_OK) return s;
+  if (n_policies < 1 || n_policies > 4096) return fail(RL_EINVAL, "n_policies %d outside 1..4096", n_policies);
+  if (!policy_index) return fail(RL_EINVAL, "policy_index is NULL");
+  if (!state) return fail(RL_EINVAL, "state is NULL");
+  if (!out) return fail(RL_EINVAL, "out is NULL");
+  if (n_steps < 1) return fail(RL_EINVAL, "n_steps %d must be >= 1", n_steps);
+  if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
+  if (a.D != es.D) return fail(RL_ESHAPE, "policy input size %d != observation size %d", a.D, es.D);
+  if (a.NA != es.NA) return fail(RL_ESHAPE, "policy has %d actions, the env %d", a.NA, es.NA);
+  const size_t lds = rl::lbf_pop_lds_bytes(es.lbf, a);
+  if (lds + rl::LBF_POP_STATIC_LDS > rl::MAX_LDS_BYTES)
+    return fail(RL_EUNSUPPORTED, "rollout tile needs %zu bytes of LDS (max %zu)", lds,
+                rl::MAX_LDS_BYTES - rl::LBF_POP_STATIC_LDS);
+  const rl::TrajArgs o{out->obs, out->actions, out->logits, out->reward, out->done, out->obs_last};
+  return launched(rl::launch_lbf_run_pop(es.lbf, a, n_policies, policy_index, static_cast<int32_t*>(state), t0,
+                                         n_steps, o, (hipStream_t)stream),
+                  "rollout_run_pop");
+}
+
 rl_status rollout_sample(const rl_env_config* cfg, uint64_t t, const float* logits, const uint8_t* legal,
                          int32_t* actions, void* stream) {
   EnvSpec es;

@@ -162,6 +162,12 @@ hipError_t launch_lbf_step(const LbfParams& p, int32_t* state, uint64_t t0, int 
                            uint8_t* legal, hipStream_t s);
 hipError_t launch_lbf_run(const LbfParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
                           const TrajArgs& out, hipStream_t s);
+// Population rollout (LBF): agent a of env e acts with policy pidx[e * A + a]
+// of n_pol networks stacked in pol's weight arrays.
+constexpr size_t LBF_POP_STATIC_LDS = 64;  // bytes of static LDS the population kernel may declare
+size_t lbf_pop_lds_bytes(const LbfParams& p, const PolicyArgs& pol);
+hipError_t launch_lbf_run_pop(const LbfParams& p, const PolicyArgs& pol, int n_pol, const int32_t* pidx,
+                              int32_t* state, uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s);
 
 hipError_t launch_oc_init(const OcParams& p, int32_t* state, void* obs, int obs_dt, uint8_t* legal, hipStream_t s);
 hipError_t launch_oc_step(const OcParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,

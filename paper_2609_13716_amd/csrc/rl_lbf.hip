@@ -377,7 +377,214 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
   if (envlane) lbf_store(state, p, e, s);
 }
 
+// ------------------------------------------- population rollout ----
+//
+// rollout_run_pop: the rollout of lbf_run_kernel where agent a of env e acts
+// with policy pidx[e * A + a] of a population of n_pol networks of one shape,
+// stacked in memory (the ego agent and its teammates of the ad hoc teamwork
+// objective, Section 3).  At the start each workgroup sorts its rows by policy
+// (the assignment is fixed for the rollout); every step it runs the three MFMA
+// layers once per policy present, on that policy's rows only (rows gathered
+// by index into the operand), and scatters the logits back to their rows.
+// Cost per step grows with the number of distinct policies in a tile.  An
+// index outside 0..n_pol-1 selects policy 0.
+size_t lbf_pop_lds_bytes(const LbfParams& p, const PolicyArgs& pol) {
+  const RunLayout RL = make_run_layout(p.A, p.D, pol.H1, pol.H2, pol.dt);
+  const size_t off = (RL.total + 15) & ~(size_t)15;
+  return off + (size_t)(3 * RL.R + 17) * 4 + (size_t)RL.R * MAX_NA * 4;
+}
+
+template <int DT>
+__global__ __launch_bounds__(NTHREADS) void lbf_run_pop_kernel(LbfParams p, LbfMagic m, PolicyArgs pol, int n_pol,
+                                                               const int32_t* __restrict__ pidx,
+                                                               int32_t* __restrict__ state, uint64_t t0,
+                                                               int n_steps, TrajArgs out) {
+  using T = typename DType<DT>::T;
+  extern __shared__ __align__(16) uint8_t smem[];
+  const RunLayout RL = make_run_layout(p.A, p.D, pol.H1, pol.H2, DT);
+  const LbfLds L{smem + RL.off_agrid, smem + RL.off_fgrid, reinterpret_cast<int*>(smem + RL.off_acell)};
+  int* act_lds = reinterpret_cast<int*>(smem + RL.off_act);
+  T* xs = reinterpret_cast<T*>(smem + RL.off_x);
+  T* h1 = reinterpret_cast<T*>(smem + RL.off_h1);
+  T* h2 = reinterpret_cast<T*>(smem + RL.off_h2);
+  float* lg = reinterpret_cast<float*>(smem + RL.off_logit);
+  float* sc = reinterpret_cast<float*>(smem + RL.off_score);
+  const int R = RL.R;
+  int* order = reinterpret_cast<int*>(smem + ((RL.total + 15) & ~(size_t)15));  // R + 16 row indices, by policy
+  int* gstart = order + R + 16;                                                  // group g: order[gstart[g] .. gstart[g+1])
+  int* gpid = gstart + R + 1;                                                    // policy of group g
+  float* lgc = reinterpret_cast<float*>(gpid + R);                               // a group's logits, compact rows
+  __shared__ int ngroups;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int e0 = blockIdx.x * TILE_E;
+  const int te_valid = min(TILE_E, p.E - e0);
+  const int A = p.A, D = p.D, NA = pol.NA, H1 = pol.H1, H2 = pol.H2;
+  T* gobs = static_cast<T*>(out.obs);
+
+  zero_lds(smem, RL.total, tid);  // zero grids and the K padding of every operand tile
+  if (tid == 0) {
+    // group the live rows (te_valid * A <= 64) by policy, in order of first appearance
+    const int nr = te_valid * A;
+    uint64_t left = nr >= 64 ? ~0ull : ((1ull << nr) - 1ull);
+    int ng = 0, pos = 0;
+    while (left) {
+      const int r0 = __builtin_ctzll(left);
+      const int raw0 = pidx[(size_t)e0 * A + r0];
+      const int id0 = (unsigned)raw0 < (unsigned)n_pol ? raw0 : 0;
+      gpid[ng] = id0;
+      gstart[ng] = pos;
+      for (int r = r0; r < nr; ++r) {
+        if (!((left >> r) & 1ull)) continue;
+        const int raw = pidx[(size_t)e0 * A + r];
+        if (((unsigned)raw < (unsigned)n_pol ? raw : 0) == id0) {
+          order[pos++] = r;
+          left &= ~(1ull << r);
+        }
+      }
+      ++ng;
+    }
+    gstart[ng] = pos;
+    for (int i = pos; i < R + 16; ++i) order[i] = 0;  // padding rows of the last MFMA row tile
+    ngroups = ng;
+  }
+  __syncthreads();
+  const bool envlane = tid < te_valid;
+  const int e = e0 + tid;
+  const uint64_t genv = (uint64_t)(p.env_base + e);
+  LbfEnv s{};
+  if (envlane) {
+    lbf_load(state, p, e, s);
+    lbf_paint(p, s, tid, L, true);
+  }
+  __syncthreads();
+  const int ng = ngroups;
+
+  for (int k = 0; k < n_steps; ++k) {
+    const uint64_t t = t0 + (uint64_t)k;
+    lbf_encode<T>(p, m, te_valid, L, gobs ? gobs + ((size_t)k * p.E + e0) * A * D : nullptr, xs, RL.ldx, tid);
+    __syncthreads();
+    for (int g = 0; g < ng; ++g) {
+      const int g0 = gstart[g], cnt = gstart[g + 1] - g0;
+      const int R16 = (cnt + 15) & ~15;
+      const size_t q = (size_t)gpid[g];
+      const T* W1 = static_cast<const T*>(pol.W[0]) + q * H1 * D;
+      const T* W2 = static_cast<const T*>(pol.W[1]) + q * H2 * H1;
+      const T* W3 = static_cast<const T*>(pol.W[2]) + q * NA * H2;
+      const T* b1 = static_cast<const T*>(pol.b[0]) + q * H1;
+      const T* b2 = static_cast<const T*>(pol.b[1]) + q * H2;
+      const T* b3 = static_cast<const T*>(pol.b[2]) + q * NA;
+      mlp_input_layer<DT>(xs, RL.ldx, order + g0, R16, D, W1, b1, H1, h1, RL.ld1, wave, NTHREADS / 64, lane);
+      __syncthreads();
+      mlp_hidden<DT>(h1, RL.ld1, R16, H1, W2, b2, H2, h2, RL.ld2, wave, NTHREADS / 64, lane);
+      __syncthreads();
+      mlp_logits<DT>(h2, RL.ld2, R16, H2, W3, b3, NA, lgc, MAX_NA, wave, NTHREADS / 64, lane);
+      __syncthreads();
+      for (int idx = tid; idx < cnt * NA; idx += NTHREADS) {
+        const int r = idx / NA, a = idx - r * NA;
+        lg[order[g0 + r] * MAX_NA + a] = lgc[r * MAX_NA + a];
+      }
+      __syncthreads();
+    }
+    // Gumbel scores per (row, action); every LBF action is legal
+    for (int idx = tid; idx < R * NA; idx += NTHREADS) {
+      const int r = fdiv(idx, m.na), a = idx - r * NA;
+      const int el = fdiv(r, m.a), ag = r - el * A;
+      if (el < te_valid) {
+        const float gn = action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t, ag, a);
+        sc[r * MAX_NA + a] = action_score(lg[r * MAX_NA + a], gn, true);
+        if (out.logits) out.logits[((size_t)k * p.E + e0) * A * NA + idx] = lg[r * MAX_NA + a];
+      }
+    }
+    __syncthreads();
+    for (int r = tid; r < R; r += NTHREADS) {
+      const int el = fdiv(r, m.a);
+      if (el < te_valid) {
+        int best = 0;
+        float bs = -INFINITY;
+        for (int a = 0; a < NA; ++a) {
+          const float v = sc[r * MAX_NA + a];
+          if (v > bs) {
+            bs = v;
+            best = a;
+          }
+        }
+        act_lds[r] = best;
+        if (out.actions) out.actions[((size_t)k * p.E + e0) * A + r] = best;
+      }
+    }
+    __syncthreads();
+    if (envlane) {
+      int act[LBF_MAXA];
+#pragma unroll
+      for (int i = 0; i < LBF_MAXA; ++i) act[i] = i < A ? act_lds[tid * A + i] : 0;
+      lbf_paint(p, s, tid, L, false);
+      float r;
+      uint32_t d;
+      lbf_transition(p, s, act, r, d);
+      if (d) lbf_reset(p, genv, t + 1, s);
+      lbf_paint(p, s, tid, L, true);
+      if (out.reward) out.reward[(size_t)k * p.E + e] = r;
+      if (out.done) out.done[(size_t)k * p.E + e] = (uint8_t)d;
+    }
+    __syncthreads();
+  }
+  if (out.obs_last)
+    lbf_encode<T>(p, m, te_valid, L, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, nullptr, 0, tid);
+  if (envlane) lbf_store(state, p, e, s);
+}
+
+hipError_t launch_lbf_run_pop(const LbfParams& p, const PolicyArgs& pol, int n_pol, const int32_t* pidx,
+                              int32_t* state, uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s) {
+  const LbfMagic m = make_magic(p, pol.NA);
+  const size_t lds = lbf_pop_lds_bytes(p, pol);
+  const dim3 grid((unsigned)((p.E + TILE_E - 1) / TILE_E));
+  // the dynamic limit leaves room for the kernel's few bytes of static LDS
+  const int max_dyn = (int)(MAX_LDS_BYTES - LBF_POP_STATIC_LDS);
+  if (pol.dt == DT_F32) {
+    static bool attr = false;
+    if (!attr) {
+      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_F32>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+    lbf_run_pop_kernel<DT_F32><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
+  } else {
+    static bool attr = false;
+    if (!attr) {
+      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_BF16>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+    lbf_run_pop_kernel<DT_BF16><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
+  }
+  return hipGetLastError();
+}
+
 // ------------------------------------ fused rollout, weights in registers ----
+
+constexpr int LBF_RB = 4;  // steps of reset states built per batch
+
+// Field-wise copy of the A agents and F foods of an env state (a whole-struct
+// copy to or from LDS would turn the register copy into private memory).
+template <int A, int F>
+__device__ __forceinline__ void lbf_copy(LbfEnv& d, const LbfEnv& s) {
+#pragma unroll
+  for (int i = 0; i < A; ++i) {
+    d.acell[i] = s.acell[i];
+    d.alevel[i] = s.alevel[i];
+  }
+#pragma unroll
+  for (int j = 0; j < F; ++j) {
+    d.fcell[j] = s.fcell[j];
+    d.flevel[j] = s.flevel[j];
+  }
+  d.eaten = s.eaten;
+  d.steps = s.steps;
+  d.den = s.den;
+}
 
 constexpr int NOISE_STEPS = 16;
 
@@ -542,7 +749,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   if (envlane) {
     lbf_load<A, F>(state, p, e, s);
     lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
-    if constexpr (LEAN) env_s[el] = s;
+    if constexpr (LEAN) lbf_copy<A, F>(env_s[el], s);
   }
   // Let the prologue loads land here, once (see lbf_env_kernel).
   __builtin_amdgcn_s_waitcnt(0);
@@ -587,7 +794,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     }
     __syncthreads();
     if (wave == ew) {
-      if constexpr (LEAN) s = env_s[min(el, TE - 1)];
+      if constexpr (LEAN) lbf_copy<A, F>(s, env_s[min(el, TE - 1)]);
       // Layer 3 transposed, logits^T = W3 h2^T: lane holds row (lane % 16) of
       // the M tile and actions 4 * (lane / 16) + r in accumulator element r.
       // Each lane takes the Gumbel argmax of its four actions; one lane swap
@@ -691,7 +898,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
         if (out.reward) out.reward[(size_t)k * E + e] = r;
         if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
-        if constexpr (LEAN) env_s[el] = s;
+        if constexpr (LEAN) lbf_copy<A, F>(env_s[el], s);
       }
     } else if (k + 1 < n_steps && (k + 1) % NOISE_STEPS != 0) {
       // the other waves: Gumbel noise of the next step, while the env wave steps
@@ -702,7 +909,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   __syncthreads();
   if (out.obs_last)
     copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, te_valid * A, tid);
-  if constexpr (LEAN) s = env_s[min(el, TE - 1)];
+  if constexpr (LEAN) lbf_copy<A, F>(s, env_s[min(el, TE - 1)]);
   if (envlane) lbf_store<A, F>(state, p, e, s);
 }
 
@@ -765,27 +972,6 @@ __device__ __forceinline__ void lbf_paint_row(const LbfEnv& s, int i, T* xr, int
   for (int j = 0; j < F; ++j)  // an eaten food writes 0 at its own (distinct) cell: no branch
     xr[HW + min((uint32_t)s.fcell[j], cmax)] = !((s.eaten >> j) & 1u) ? small_int_to<T>((uint32_t)s.flevel[j]) : (T)0;
   xr[2 * HW + min((uint32_t)s.acell[i], cmax)] = small_int_to<T>(1u);
-}
-
-constexpr int LBF_RB = 4;  // steps of reset states built per batch
-
-// Field-wise copy of the A agents and F foods of an env state (a whole-struct
-// copy to or from LDS would turn the register copy into private memory).
-template <int A, int F>
-__device__ __forceinline__ void lbf_copy(LbfEnv& d, const LbfEnv& s) {
-#pragma unroll
-  for (int i = 0; i < A; ++i) {
-    d.acell[i] = s.acell[i];
-    d.alevel[i] = s.alevel[i];
-  }
-#pragma unroll
-  for (int j = 0; j < F; ++j) {
-    d.fcell[j] = s.fcell[j];
-    d.flevel[j] = s.flevel[j];
-  }
-  d.eaten = s.eaten;
-  d.steps = s.steps;
-  d.den = s.den;
 }
 
 template <typename OT, int GH, int GW, int A, int F, int TE>

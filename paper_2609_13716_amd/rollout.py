@@ -72,6 +72,9 @@ def _load():
     lib.rollout_run.argtypes = [cfgp, ctypes.POINTER(_Policy), P, ctypes.c_uint64, ctypes.c_int32,
                                 ctypes.POINTER(_Traj), P]
     lib.rollout_run.restype = st
+    lib.rollout_run_pop.argtypes = [cfgp, ctypes.POINTER(_Policy), ctypes.c_int32, P, P, ctypes.c_uint64,
+                                    ctypes.c_int32, ctypes.POINTER(_Traj), P]
+    lib.rollout_run_pop.restype = st
     lib.rollout_sample.argtypes = [cfgp, ctypes.c_uint64, P, P, P, P]
     lib.rollout_sample.restype = st
     lib.rl_gumbel_noise.argtypes, lib.rl_gumbel_noise.restype = [P, ctypes.c_int64, P, P], st
@@ -82,7 +85,7 @@ lib = _load()
 
 # Every symbol the C header declares (checked by the test suite).
 EXPORTED = ("rl_state_bytes", "rl_obs_dim", "rl_num_actions", "rollout_last_error", "rollout_init",
-            "rollout_step", "policy_forward", "rollout_run", "rollout_sample", "rl_gumbel_noise")
+            "rollout_step", "policy_forward", "rollout_run", "rollout_sample", "rl_gumbel_noise", "rollout_run_pop")
 
 
 def _check(status):
@@ -195,6 +198,40 @@ class Policy:
         return p
 
 
+class Population:
+    """Device weights of n policies of one shape, stacked per layer ([n, fan_out, fan_in] and [n, fan_out]).
+
+    ``weights[p]`` / ``biases[p]`` are policy p's layers in the nn.Linear layout.
+    """
+
+    def __init__(self, weights, biases, dtype="f32", device="cuda"):
+        if len(weights) < 1 or len(weights) != len(biases):
+            raise ValueError("a population needs one (weights, biases) pair per policy")
+        self.dtype = _DT_CODE[dtype]
+        tdt = _TORCH_DT[self.dtype]
+        self.n = len(weights)
+        self.W = [torch.stack([torch.as_tensor(w[l]) for w in weights]).to(device=device, dtype=tdt).contiguous()
+                  for l in range(3)]
+        self.b = [torch.stack([torch.as_tensor(b[l]) for b in biases]).to(device=device, dtype=tdt).contiguous()
+                  for l in range(3)]
+        self.dims = [self.W[0].shape[2]] + [w.shape[1] for w in self.W]
+
+    @property
+    def torch_dtype(self):
+        return _TORCH_DT[self.dtype]
+
+    def c(self):
+        p = _Policy()
+        p.dtype = self.dtype
+        p.n_layers = 3
+        for i, d in enumerate(self.dims):
+            p.dims[i] = d
+        for i in range(3):
+            p.W[i] = self.W[i].data_ptr()
+            p.b[i] = self.b[i].data_ptr()
+        return p
+
+
 def new_state(cfg, device="cuda"):
     """A device buffer of rl_state_bytes(cfg) bytes (as int32)."""
     n = rl_state_bytes(cfg)
@@ -262,6 +299,27 @@ def rollout_run(cfg, policy, state, t0, n_steps, obs=None, actions=None, logits=
     pc = policy.c()
     _check(lib.rollout_run(ctypes.byref(cfg.c()), ctypes.byref(pc), _ptr(state), t0, T, ctypes.byref(tr),
                            _stream(stream)))
+
+
+def rollout_run_pop(cfg, pop, policy_index, state, t0, n_steps, obs=None, actions=None, logits=None, reward=None,
+                    done=None, obs_last=None, stream=None):
+    """rollout_run with agent a of env e acting with policy policy_index[e, a] of the population ``pop``."""
+    E, A = cfg.n_envs, cfg.n_agents
+    D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
+    T = n_steps
+    _need(policy_index, "policy_index", torch.int32, (E, A))
+    _need(state, "state", torch.int32)
+    _need(obs, "obs", pop.torch_dtype, (T, E, A, D))
+    _need(actions, "actions", torch.int32, (T, E, A))
+    _need(logits, "logits", torch.float32, (T, E, A, nA))
+    _need(reward, "reward", torch.float32, (T, E))
+    _need(done, "done", torch.uint8, (T, E))
+    _need(obs_last, "obs_last", pop.torch_dtype, (E, A, D))
+    tr = _Traj(obs=_ptr(obs), actions=_ptr(actions), logits=_ptr(logits), reward=_ptr(reward), done=_ptr(done),
+               obs_last=_ptr(obs_last))
+    pc = pop.c()
+    _check(lib.rollout_run_pop(ctypes.byref(cfg.c()), ctypes.byref(pc), pop.n, _ptr(policy_index), _ptr(state), t0,
+                               T, ctypes.byref(tr), _stream(stream)))
 
 
 def rollout_sample(cfg, t, logits, legal=None, actions=None, stream=None):

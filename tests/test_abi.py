@@ -157,6 +157,16 @@ def test_error_paths_before_launch():
     big = _cfg(grid_h=16, grid_w=16, n_agents=4)
     assert _run_status(big, _policy_struct(dims=(768, 512, 512, 6))) == R.RL_EUNSUPPORTED
     assert "LDS" in L.rollout_last_error().decode()
+    # population rollout
+    tr = R._Traj()
+    pop_run = lambda c2, n, idx=0x1000, st=0x1000: L.rollout_run_pop(
+        ctypes.byref(c2.c()), ctypes.byref(_policy_struct()), n, ctypes.c_void_p(idx), ctypes.c_void_p(st), 0, 4,
+        ctypes.byref(tr), None)
+    assert pop_run(cfg, 0) == R.RL_EINVAL
+    assert pop_run(cfg, 4097) == R.RL_EINVAL
+    assert pop_run(cfg, 2, idx=0) == R.RL_EINVAL
+    assert pop_run(cfg, 2, st=0) == R.RL_EINVAL
+    assert pop_run(R.overcooked_config(16, cook_time=5, soup_reward=20, max_steps=30), 2) == R.RL_EUNSUPPORTED
     # policy_forward and sampling
     pol = _policy_struct()
     assert L.policy_forward(ctypes.byref(pol), None, None, 10, ctypes.c_void_p(0x1000), None) == R.RL_EINVAL
