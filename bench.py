@@ -168,6 +168,44 @@ def measure_workload(R, workloads, name, dt, steps, warmup):
     return out
 
 
+def measure_population(R, workloads, name, dt, steps, warmup):
+    """rollout_run_pop of a population workload at full size: time, throughput and rooflines."""
+    import torch
+    w = workloads.WORKLOADS[name]
+    cfg = env_config(R, workloads, name)
+    E, T, A = cfg.n_envs, w["n_steps"], cfg.n_agents
+    D = R.rl_obs_dim(cfg)
+    dims = workloads.policy_dims(name)
+    ws, bs = workloads.population_weights(name, seed=1000)
+    pop = R.Population(ws, bs, dt)
+    idx = torch.as_tensor(workloads.population_index(name)).cuda()
+    es = 2 if dt == "bf16" else 4
+    flop_per_row = 2 * sum(dims[i] * dims[i + 1] for i in range(3))
+    state = R.new_state(cfg)
+    R.rollout_init(cfg, state)
+    obs = torch.empty(T, E, A, D, dtype=pop.torch_dtype, device="cuda")
+    acts = torch.empty(T, E, A, dtype=torch.int32, device="cuda")
+    rew = torch.empty(T, E, device="cuda")
+    done = torch.empty(T, E, dtype=torch.uint8, device="cuda")
+    t_next = [0]
+
+    def run():
+        R.rollout_run_pop(cfg, pop, idx, state, t_next[0], T, obs=obs, actions=acts, reward=rew, done=done)
+        t_next[0] += T
+
+    kern_ms, wall_ms = timed(run, steps, warmup)
+    nbytes = E * T * (A * D * es + A * 4 + 4 + 1) + 2 * R.rl_state_bytes(cfg)
+    flops = E * T * A * flop_per_row
+    n_teammates = w["population"] - 1
+    return {"workload": name, "dtype": dt, "n_envs": E, "steps_per_rollout": T, "policy": "-".join(map(str, dims)),
+            "population": w["population"], "assignment": f"agent 0: ego; agent 1: one of {n_teammates} teammates "
+                                                          f"per block of {E // n_teammates} envs",
+            "value": round(E * T * A / (wall_ms * 1e-3), 1), "unit": "agent-env steps/s",
+            "ms_per_step": round(wall_ms, 4), "kernel_ms": round(kern_ms, 4),
+            "roofline_hbm": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"),
+            "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s")}
+
+
 def cpu_baseline(n_envs, T):
     """The oracle, single-threaded, on the first n_envs envs of the workload for T steps."""
     import numpy as np
@@ -277,7 +315,8 @@ def main():
         return dict(kern_ms=kern_ms, rows=rows, flops=flops, tflops=flops / (kern_ms * 1e-3) / 1e12)
 
     if args.workload_only:
-        print(json.dumps(measure_workload(R, workloads, args.workload_only, "bf16", args.steps, args.warmup)),
+        measure = measure_population if "population" in workloads.WORKLOADS[args.workload_only] else measure_workload
+        print(json.dumps(measure(R, workloads, args.workload_only, "bf16", args.steps, args.warmup)),
               flush=True)
         return
 
@@ -343,6 +382,8 @@ def main():
         # the other workloads at full size, bf16, a few timed launches each
         line["workloads"] = {n: measure_workload(R, workloads, n, "bf16", min(args.steps, 5), 1)
                              for n in ("lbf12_16k", "oc_4096", "hn_4096")}
+        line["workloads"]["lbf8_4096_pop"] = measure_population(R, workloads, "lbf8_4096_pop", "bf16",
+                                                                min(args.steps, 5), 1)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.cpu_envs, T)
     print(json.dumps(line), flush=True)

@@ -22,6 +22,7 @@ lbf       Level-Based Foraging: reset, step, observation.
 overcooked  Overcooked-style two-agent kitchen: layout, reset, step, observation.
 hanabi    Two-player Hanabi: deal, legality, step, observation.
 rollout   The rollout loop: observe, act, step, auto-reset.
+actor_critic  log pi(a) of sampled actions and generalised advantage estimates.
 
 Environment rules that the paper leaves open (it names the environments and
 their sources, Section 4 "Environments" and the environment table, but does

@@ -20,7 +20,7 @@ Output layout (``n`` = number of env ids, A agents, D obs features):
 
 import numpy as np
 
-from . import mlp, sampling
+from . import actor_critic, mlp, sampling
 
 
 def initial_states(env, cfg, seed, env_ids):
@@ -63,7 +63,7 @@ def policy_logits(obs, weights, biases, dtype, policy_index=None):
 
 
 def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
-            states=None, logits_source=None, action_hook=None, policy_index=None):
+            states=None, logits_source=None, action_hook=None, policy_index=None, value_head=False):
     """Roll ``env_ids`` forward ``n_steps`` steps from absolute step ``t0``.
 
     ``states`` are the env states at t0 (default: the initial states, t0 = 0).
@@ -73,6 +73,11 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     sampled action of env index i, agent ``agent``.
     ``policy_index`` [n, A]: per-agent policies of a population (see
     ``policy_logits``); ``weights`` and ``biases`` are then per policy.
+    ``value_head``: the network has nA + 1 outputs, the last being the
+    critic's value V(o); the result then also holds ``value`` [T, n, A],
+    ``value_last`` [n, A] (V of obs_last) and ``logp`` [T, n, A], the float64
+    log-probability of each sampled action under the float32 logits it was
+    sampled from (``logits`` keeps the nA action logits).
     """
     env_ids = list(env_ids)
     if states is None:
@@ -82,11 +87,14 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     states = [s.copy() for s in states]
     n, A = len(env_ids), cfg.n_agents
     nA = env.N_ACTIONS
-    out = {k: [] for k in ("obs", "logits", "actions", "reward", "done", "mask")}
+    out = {k: [] for k in ("obs", "logits", "actions", "reward", "done", "mask", "value", "logp")}
     for k in range(n_steps):
         t = t0 + k
         obs, mask = observe_all(env, cfg, states)
         logits64 = policy_logits(obs, weights, biases, dtype, policy_index)
+        if value_head:
+            out["value"].append(logits64[..., nA])
+            logits64 = logits64[..., :nA]
         logits32 = logits64.astype(np.float32)
         if logits_source is not None:
             logits32 = np.asarray(logits_source(k, logits64), dtype=np.float32)
@@ -97,6 +105,9 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
                 if action_hook is not None:
                     act = action_hook(k, i, a, act, logits32[i, a], mask[i, a])
                 actions[i, a] = act
+        if value_head:
+            out["logp"].append(np.array([[actor_critic.log_prob(logits32[i, a], actions[i, a], mask[i, a])
+                                          for a in range(A)] for i in range(n)]))
         rewards = np.zeros(n, dtype=np.float32)
         dones = np.zeros(n, dtype=np.uint8)
         for i, e in enumerate(env_ids):
@@ -109,6 +120,8 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
         out["done"].append(dones)
     res = {k: np.stack(v) if v else None for k, v in out.items()}
     res["obs_last"], res["mask_last"] = observe_all(env, cfg, states)
+    if value_head:
+        res["value_last"] = policy_logits(res["obs_last"], weights, biases, dtype, policy_index)[..., nA]
     res["states"] = states
     return res
 

@@ -23,6 +23,12 @@ rules and observation as documented in include/rollout.h):
 Two-player Hanabi (5 colours x 5 ranks, hands of 5, 8 info tokens, 3 lives):
     hn_4096      4096 envs x 80 steps, MLP 658-512-512-20 bf16 on the mover's
                  observation, illegal actions masked
+
+Population rollout (ad hoc teamwork evaluation: one ego policy paired with a
+set of teammate policies, all of one shape):
+    lbf8_4096_pop  lbf8_4096's envs, a population of 9 MLPs 192-128-128-6 bf16:
+                 agent 0 of every env is the ego (policy 0), agent 1 of env e
+                 is teammate 1 + e // 512 (8 blocks of 512 envs, one teammate each)
 """
 
 import numpy as np
@@ -41,6 +47,9 @@ WORKLOADS = {
                     n_envs=4096, n_steps=400, hidden=(256, 256), dtypes=("bf16",)),
     "hn_4096": dict(kind="hanabi", env=dict(max_steps=1000), n_envs=4096, n_steps=80, hidden=(512, 512),
                     dtypes=("bf16",)),
+    "lbf8_4096_pop": dict(env=dict(grid_h=8, grid_w=8, n_agents=2, n_food=3, max_agent_level=2, max_food_level=3,
+                                   max_steps=50),
+                          n_envs=4096, n_steps=128, hidden=(128, 128), dtypes=("bf16",), population=9),
 }
 
 LBF_ACTIONS = 6
@@ -88,3 +97,27 @@ def injected_actions(n_steps, n_envs, n_agents, n_actions, seed, p_invalid=0.0):
         bad = rng.random(a.shape) < p_invalid
         a[bad] = rng.choice(np.array([-1, n_actions, n_actions + 7, 1 << 20]), size=int(bad.sum()))
     return a.astype(np.int32)
+
+
+def population_index(name):
+    """[E, A] int32 policy of every agent of a population workload: agent 0 the ego (policy 0), the other
+    agents of env e the teammate 1 + e // (E / (P - 1))."""
+    w = WORKLOADS[name]
+    E, A, P = w["n_envs"], w["env"]["n_agents"], w["population"]
+    block = max(1, E // (P - 1))
+    idx = np.zeros((E, A), dtype=np.int32)
+    for a in range(1, A):
+        idx[:, a] = 1 + np.minimum(np.arange(E) // block, P - 2)
+    return idx
+
+
+def population_weights(name, seed):
+    """Per-policy (weights, biases) of a population workload, policy p drawn with seed + p."""
+    dims = policy_dims(name)
+    ws, bs = [], []
+    for p in range(WORKLOADS[name]["population"]):
+        w, b = policy_weights(dims, seed + p)
+        ws.append(w)
+        bs.append(b)
+    return ws, bs
+
