@@ -121,6 +121,14 @@ typedef struct {
   void* obs_last;    /* [E, A, D] policy dtype: o_{t0+T}, the observation after the last step */
 } rl_traj;
 
+/* Actor-critic outputs of rollout_run_ac (host struct of device pointers).
+ * Any pointer may be NULL ("do not write"). */
+typedef struct {
+  float* value;       /* [T, E, A] V(o_t): the critic's value of the observation a_t was sampled from */
+  float* logp;        /* [T, E, A] log pi(a_t | o_t) under the float32 logits a_t was sampled from */
+  float* value_last;  /* [E, A] V(o_{t0+T}), for bootstrapping the next advantage estimate */
+} rl_ac_traj;
+
 /* ---- host-only queries (no device work) ---- */
 
 /* Bytes of the env state buffer for `cfg` (0 if cfg is invalid). */
@@ -169,6 +177,31 @@ rl_status policy_forward(const rl_policy* policy, const void* obs, const uint8_t
  * persistent kernel; `state` is left at step t0 + n_steps. */
 rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* state,
                       uint64_t t0, int32_t n_steps, const rl_traj* out, void* stream);
+
+/* rollout_run for an actor-critic network: the policy's last layer has
+ * nA + 1 outputs, the first nA being the action logits (sampled as in
+ * rollout_run) and the last the critic's value V(o) of the same observation
+ * (a value head on the shared trunk).  Besides `out` it writes `ac`: V(o_t),
+ * log pi(a_t | o_t) = l_a - (m + log sum_i exp(l_i - m)) over the nA float32
+ * logits l (m their maximum), and V of the observation after the last step.
+ * These are what a PPO-style learner consumes after a rollout (the learners
+ * the paper benchmarks build on PPO, appendix "Algorithms Overview").  LBF
+ * envs only (RL_EUNSUPPORTED otherwise); dims[3] must be nA + 1 (RL_ESHAPE). */
+rl_status rollout_run_ac(const rl_env_config* cfg, const rl_policy* policy, void* state, uint64_t t0,
+                         int32_t n_steps, const rl_traj* out, const rl_ac_traj* ac, void* stream);
+
+/* Generalised advantage estimation over a stored trajectory (float32), a
+ * backward scan per (env, agent):
+ *   delta_t = r_t + gamma (1 - d_t) V_{t+1} - V_t,  A_t = delta_t + gamma lambda (1 - d_t) A_{t+1},
+ *   A_T = 0, V_T = value_last, R_t = A_t + V_t,
+ * with d_t = 1 where done[t] != 0: an episode end (terminated or truncated)
+ * cuts the recurrence, as the next observation starts a fresh episode.
+ *   reward [T, E] float32, done [T, E] uint8, value [T, E, A] float32 and
+ *   value_last [E, A] float32 read; adv [T, E, A] written; ret [T, E, A]
+ *   written, may be NULL.  gamma and lambda in [0, 1]. */
+rl_status rl_gae(const float* reward, const uint8_t* done, const float* value, const float* value_last,
+                 int32_t n_steps, int32_t n_envs, int32_t n_agents, float gamma, float lambda, float* adv,
+                 float* ret, void* stream);
 
 /* The rollout of rollout_run with one policy per agent slot, drawn from a
  * population: the ego agent and its teammates of the ad hoc teamwork objective

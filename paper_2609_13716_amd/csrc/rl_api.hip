@@ -272,6 +272,48 @@ rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* s
                   "rollout_run");
 }
 
+rl_status rollout_run_ac(const rl_env_config* cfg, const rl_policy* policy, void* state, uint64_t t0,
+                         int32_t n_steps, const rl_traj* out, const rl_ac_traj* ac, void* stream) {
+  EnvSpec es;
+  rl_status s = check_cfg(cfg, &es);
+  if (s != RL_OK) return s;
+  if (es.kind != RL_ENV_LBF) return fail(RL_EUNSUPPORTED, "rollout_run_ac is implemented for LBF only");
+  rl::PolicyArgs a;
+  s = check_policy(policy, &a);
+  if (s != RL_OK) return s;
+  if (!state) return fail(RL_EINVAL, "state is NULL");
+  if (!out || !ac) return fail(RL_EINVAL, "out or ac is NULL");
+  if (n_steps < 1) return fail(RL_EINVAL, "n_steps %d must be >= 1", n_steps);
+  if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
+  if (a.D != es.D) return fail(RL_ESHAPE, "policy input size %d != observation size %d", a.D, es.D);
+  if (a.NA != es.NA + 1)
+    return fail(RL_ESHAPE, "policy has %d outputs, the env's %d actions plus the value need %d", a.NA, es.NA,
+                es.NA + 1);
+  a.VH = 1;
+  const size_t lds = rl::make_run_layout(es.A, es.D, a.H1, a.H2, a.dt).total;
+  if (lds > rl::MAX_LDS_BYTES)
+    return fail(RL_EUNSUPPORTED, "rollout tile needs %zu bytes of LDS (max %zu)", lds, rl::MAX_LDS_BYTES);
+  rl::TrajArgs o{out->obs, out->actions, out->logits, out->reward, out->done, out->obs_last};
+  o.value = ac->value;
+  o.logp = ac->logp;
+  o.value_last = ac->value_last;
+  return launched(rl::launch_lbf_run(es.lbf, a, static_cast<int32_t*>(state), t0, n_steps, o, (hipStream_t)stream),
+                  "rollout_run_ac");
+}
+
+rl_status rl_gae(const float* reward, const uint8_t* done, const float* value, const float* value_last,
+                 int32_t n_steps, int32_t n_envs, int32_t n_agents, float gamma, float lambda, float* adv,
+                 float* ret, void* stream) {
+  if (!reward || !done || !value || !value_last || !adv) return fail(RL_EINVAL, "a required pointer is NULL");
+  if (n_steps < 1 || n_envs < 1 || n_agents < 1) return fail(RL_EINVAL, "sizes must be >= 1");
+  if ((int64_t)n_envs * n_agents > ((int64_t)1 << 31)) return fail(RL_EINVAL, "n_envs * n_agents exceeds 2^31");
+  if (!(gamma >= 0.f && gamma <= 1.f) || !(lambda >= 0.f && lambda <= 1.f))
+    return fail(RL_EINVAL, "gamma and lambda must lie in [0, 1]");
+  return launched(rl::launch_gae(reward, done, value, value_last, n_steps, n_envs, n_agents, gamma, lambda, adv,
+                                 ret, (hipStream_t)stream),
+                  "rl_gae");
+}
+
 rl_status rollout_run_pop(const rl_env_config* cfg, const rl_policy* pop, int32_t n_policies,
                           const int32_t* policy_index, void* state, uint64_t t0, int32_t n_steps, const rl_traj* out,
                           void* stream) {

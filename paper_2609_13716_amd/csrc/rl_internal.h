@@ -107,9 +107,10 @@ __device__ __forceinline__ void stage_actions(const int32_t* __restrict__ action
 
 struct PolicyArgs {
   int dt;  // DT_F32 / DT_BF16
-  int D, H1, H2, NA;
+  int D, H1, H2, NA;  // NA: outputs of layer 3 (actions, plus the value when VH)
   const void* W[3];
   const void* b[3];
+  int VH = 0;  // 1: the last of the NA outputs is the critic's value V(o), the others are action logits
 };
 
 struct TrajArgs {
@@ -119,6 +120,9 @@ struct TrajArgs {
   float* reward;
   uint8_t* done;
   void* obs_last;
+  float* value = nullptr;       // [T, E, A] V(o_t) (value head only)
+  float* logp = nullptr;        // [T, E, A] log pi(a_t | o_t) of the sampled action
+  float* value_last = nullptr;  // [E, A] V(o_{t0+T})
 };
 
 // LDS layout of the fused rollout kernel for one env tile of TILE_E envs.
@@ -162,6 +166,10 @@ hipError_t launch_lbf_step(const LbfParams& p, int32_t* state, uint64_t t0, int 
                            uint8_t* legal, hipStream_t s);
 hipError_t launch_lbf_run(const LbfParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
                           const TrajArgs& out, hipStream_t s);
+// Generalised advantage estimation over [T, E, A] values (rl_ac.hip).
+hipError_t launch_gae(const float* reward, const uint8_t* done, const float* value, const float* value_last, int T,
+                      int E, int A, float gamma, float lambda, float* adv, float* ret, hipStream_t s);
+
 // Population rollout (LBF): agent a of env e acts with policy pidx[e * A + a]
 // of n_pol networks stacked in pol's weight arrays.
 constexpr size_t LBF_POP_STATIC_LDS = 64;  // bytes of static LDS the population kernel may declare

@@ -297,7 +297,7 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TILE_E;
   const int te_valid = min(TILE_E, p.E - e0);
-  const int A = p.A, D = p.D, NA = pol.NA, R = RL.R;
+  const int A = p.A, D = p.D, NOUT = pol.NA, NA = NOUT - pol.VH, R = RL.R;
   const T* W1 = static_cast<const T*>(pol.W[0]);
   const T* W2 = static_cast<const T*>(pol.W[1]);
   const T* W3 = static_cast<const T*>(pol.W[2]);
@@ -327,7 +327,7 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
     __syncthreads();
     mlp_hidden<DT>(h1, RL.ld1, R, pol.H1, W2, b2, pol.H2, h2, RL.ld2, wave, NTHREADS / 64, lane);
     __syncthreads();
-    mlp_logits<DT>(h2, RL.ld2, R, pol.H2, W3, b3, NA, lg, MAX_NA, wave, NTHREADS / 64, lane);
+    mlp_logits<DT>(h2, RL.ld2, R, pol.H2, W3, b3, NOUT, lg, MAX_NA, wave, NTHREADS / 64, lane);
     __syncthreads();
     // Gumbel scores per (row, action); every LBF action is legal
     for (int idx = tid; idx < R * NA; idx += NTHREADS) {
@@ -353,7 +353,10 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
           }
         }
         act_lds[r] = best;
-        if (out.actions) out.actions[((size_t)k * p.E + e0) * A + r] = best;
+        const size_t gr = ((size_t)k * p.E + e0) * A + r;
+        if (out.actions) out.actions[gr] = best;
+        if (out.logp) out.logp[gr] = log_softmax_at(lg + r * MAX_NA, NA, best);
+        if (out.value) out.value[gr] = lg[r * MAX_NA + NA];
       }
     }
     __syncthreads();
@@ -372,8 +375,19 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
     }
     __syncthreads();
   }
-  if (out.obs_last)
-    lbf_encode<T>(p, m, te_valid, L, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, nullptr, 0, tid);
+  if (out.obs_last || out.value_last)
+    lbf_encode<T>(p, m, te_valid, L, out.obs_last ? static_cast<T*>(out.obs_last) + (size_t)e0 * A * D : nullptr,
+                  out.value_last ? xs : nullptr, RL.ldx, tid);
+  if (out.value_last) {  // V(o_{t0+T}): one more pass of the network over the final observation
+    __syncthreads();
+    mlp_input_layer<DT>(xs, RL.ldx, nullptr, R, D, W1, b1, pol.H1, h1, RL.ld1, wave, NTHREADS / 64, lane);
+    __syncthreads();
+    mlp_hidden<DT>(h1, RL.ld1, R, pol.H1, W2, b2, pol.H2, h2, RL.ld2, wave, NTHREADS / 64, lane);
+    __syncthreads();
+    mlp_logits<DT>(h2, RL.ld2, R, pol.H2, W3, b3, NOUT, lg, MAX_NA, wave, NTHREADS / 64, lane);
+    __syncthreads();
+    for (int r = tid; r < te_valid * A; r += NTHREADS) out.value_last[(size_t)e0 * A + r] = lg[r * MAX_NA + NA];
+  }
   if (envlane) lbf_store(state, p, e, s);
 }
 
@@ -1114,7 +1128,7 @@ hipError_t launch_lbf_step(const LbfParams& p, int32_t* state, uint64_t t0, int 
 
 hipError_t launch_lbf_run(const LbfParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
                           const TrajArgs& out, hipStream_t s) {
-  const LbfMagic m = make_magic(p, pol.NA);
+  const LbfMagic m = make_magic(p, pol.NA - pol.VH);
   hipError_t err;
   if (try_launch_rollout_reg(p, m, pol, state, t0, n_steps, out, s, &err)) return err;
   const RunLayout RL = make_run_layout(p.A, p.D, pol.H1, pol.H2, pol.dt);

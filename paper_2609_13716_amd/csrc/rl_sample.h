@@ -23,4 +23,14 @@ __device__ __forceinline__ float action_score(float logit, float noise, bool leg
   return (legal & (s == s)) ? s : -INFINITY;
 }
 
+// log pi(a) of a softmax over the n logits l[0..n-1] (all legal), in float32:
+// l[a] - (m + log(sum exp(l - m))) with m the largest logit.
+__device__ __forceinline__ float log_softmax_at(const float* l, int n, int a) {
+  float m = l[0];
+  for (int i = 1; i < n; ++i) m = fmaxf(m, l[i]);
+  float s = 0.f;
+  for (int i = 0; i < n; ++i) s += expf(l[i] - m);
+  return l[a] - (m + logf(s));
+}
+
 }  // namespace rl

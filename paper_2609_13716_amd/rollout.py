@@ -55,6 +55,10 @@ class _Traj(ctypes.Structure):
                 ("reward", ctypes.c_void_p), ("done", ctypes.c_void_p), ("obs_last", ctypes.c_void_p)]
 
 
+class _AcTraj(ctypes.Structure):
+    _fields_ = [("value", ctypes.c_void_p), ("logp", ctypes.c_void_p), ("value_last", ctypes.c_void_p)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_13716_amd.build`")
@@ -72,6 +76,12 @@ def _load():
     lib.rollout_run.argtypes = [cfgp, ctypes.POINTER(_Policy), P, ctypes.c_uint64, ctypes.c_int32,
                                 ctypes.POINTER(_Traj), P]
     lib.rollout_run.restype = st
+    lib.rollout_run_ac.argtypes = [cfgp, ctypes.POINTER(_Policy), P, ctypes.c_uint64, ctypes.c_int32,
+                                   ctypes.POINTER(_Traj), ctypes.POINTER(_AcTraj), P]
+    lib.rollout_run_ac.restype = st
+    lib.rl_gae.argtypes = [P, P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_float,
+                           P, P, P]
+    lib.rl_gae.restype = st
     lib.rollout_run_pop.argtypes = [cfgp, ctypes.POINTER(_Policy), ctypes.c_int32, P, P, ctypes.c_uint64,
                                     ctypes.c_int32, ctypes.POINTER(_Traj), P]
     lib.rollout_run_pop.restype = st
@@ -85,7 +95,8 @@ lib = _load()
 
 # Every symbol the C header declares (checked by the test suite).
 EXPORTED = ("rl_state_bytes", "rl_obs_dim", "rl_num_actions", "rollout_last_error", "rollout_init",
-            "rollout_step", "policy_forward", "rollout_run", "rollout_sample", "rl_gumbel_noise", "rollout_run_pop")
+            "rollout_step", "policy_forward", "rollout_run", "rollout_sample", "rl_gumbel_noise", "rollout_run_pop",
+            "rollout_run_ac", "rl_gae")
 
 
 def _check(status):
@@ -299,6 +310,47 @@ def rollout_run(cfg, policy, state, t0, n_steps, obs=None, actions=None, logits=
     pc = policy.c()
     _check(lib.rollout_run(ctypes.byref(cfg.c()), ctypes.byref(pc), _ptr(state), t0, T, ctypes.byref(tr),
                            _stream(stream)))
+
+
+def rollout_run_ac(cfg, policy, state, t0, n_steps, value=None, logp=None, value_last=None, obs=None, actions=None,
+                   logits=None, reward=None, done=None, obs_last=None, stream=None):
+    """rollout_run for an actor-critic network (last layer: nA logits, then the value); also writes
+    value [T, E, A], logp [T, E, A] and value_last [E, A]."""
+    E, A = cfg.n_envs, cfg.n_agents
+    D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
+    T = n_steps
+    _need(state, "state", torch.int32)
+    _need(obs, "obs", policy.torch_dtype, (T, E, A, D))
+    _need(actions, "actions", torch.int32, (T, E, A))
+    _need(logits, "logits", torch.float32, (T, E, A, nA))
+    _need(reward, "reward", torch.float32, (T, E))
+    _need(done, "done", torch.uint8, (T, E))
+    _need(obs_last, "obs_last", policy.torch_dtype, (E, A, D))
+    _need(value, "value", torch.float32, (T, E, A))
+    _need(logp, "logp", torch.float32, (T, E, A))
+    _need(value_last, "value_last", torch.float32, (E, A))
+    tr = _Traj(obs=_ptr(obs), actions=_ptr(actions), logits=_ptr(logits), reward=_ptr(reward), done=_ptr(done),
+               obs_last=_ptr(obs_last))
+    ac = _AcTraj(value=_ptr(value), logp=_ptr(logp), value_last=_ptr(value_last))
+    pc = policy.c()
+    _check(lib.rollout_run_ac(ctypes.byref(cfg.c()), ctypes.byref(pc), _ptr(state), t0, T, ctypes.byref(tr),
+                              ctypes.byref(ac), _stream(stream)))
+
+
+def gae(reward, done, value, value_last, gamma, lam, adv=None, ret=None, stream=None):
+    """Advantages (and returns) [T, E, A] of a stored trajectory; see rl_gae in include/rollout.h."""
+    T, E, A = value.shape
+    _need(reward, "reward", torch.float32, (T, E))
+    _need(done, "done", torch.uint8, (T, E))
+    _need(value, "value", torch.float32, (T, E, A))
+    _need(value_last, "value_last", torch.float32, (E, A))
+    if adv is None:
+        adv = torch.empty(T, E, A, device=value.device)
+    _need(adv, "adv", torch.float32, (T, E, A))
+    _need(ret, "ret", torch.float32, (T, E, A))
+    _check(lib.rl_gae(_ptr(reward), _ptr(done), _ptr(value), _ptr(value_last), T, E, A, gamma, lam, _ptr(adv),
+                      _ptr(ret), _stream(stream)))
+    return adv, ret
 
 
 def rollout_run_pop(cfg, pop, policy_index, state, t0, n_steps, obs=None, actions=None, logits=None, reward=None,

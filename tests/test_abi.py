@@ -167,6 +167,20 @@ def test_error_paths_before_launch():
     assert pop_run(cfg, 2, idx=0) == R.RL_EINVAL
     assert pop_run(cfg, 2, st=0) == R.RL_EINVAL
     assert pop_run(R.overcooked_config(16, cook_time=5, soup_reward=20, max_steps=30), 2) == R.RL_EUNSUPPORTED
+    # actor-critic rollout and GAE
+    ac = R._AcTraj()
+    ac_run = lambda c2, pol2, acp=ctypes.byref(ac): L.rollout_run_ac(
+        ctypes.byref(c2.c()), ctypes.byref(pol2), ctypes.c_void_p(0x1000), 0, 4, ctypes.byref(tr), acp, None)
+    assert ac_run(cfg, _policy_struct(dims=(192, 64, 64, 6))) == R.RL_ESHAPE  # needs nA + 1 outputs
+    assert ac_run(cfg, _policy_struct(dims=(192, 64, 64, 7)), acp=None) == R.RL_EINVAL
+    assert ac_run(R.overcooked_config(16, cook_time=5, soup_reward=20, max_steps=30),
+                  _policy_struct(dims=(1170, 64, 64, 7))) == R.RL_EUNSUPPORTED
+    g = lambda *a: L.rl_gae(*a)
+    vp = ctypes.c_void_p(0x1000)
+    assert g(None, vp, vp, vp, 4, 4, 2, 0.99, 0.95, vp, None, None) == R.RL_EINVAL
+    assert g(vp, vp, vp, vp, 0, 4, 2, 0.99, 0.95, vp, None, None) == R.RL_EINVAL
+    assert g(vp, vp, vp, vp, 4, 4, 2, 1.5, 0.95, vp, None, None) == R.RL_EINVAL
+    assert g(vp, vp, vp, vp, 4, 4, 2, 0.99, -0.1, vp, None, None) == R.RL_EINVAL
     # policy_forward and sampling
     pol = _policy_struct()
     assert L.policy_forward(ctypes.byref(pol), None, None, 10, ctypes.c_void_p(0x1000), None) == R.RL_EINVAL
