@@ -206,6 +206,47 @@ def measure_population(R, workloads, name, dt, steps, warmup):
             "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s")}
 
 
+def measure_actor_critic(R, workloads, name, dt, steps, warmup):
+    """rollout_run_ac then rl_gae of an actor-critic workload at full size: times, throughput and rooflines."""
+    import torch
+    w = workloads.WORKLOADS[name]
+    cfg = env_config(R, workloads, name)
+    E, T, A = cfg.n_envs, w["n_steps"], cfg.n_agents
+    D, nA = R.rl_obs_dim(cfg), R.rl_num_actions(cfg)
+    dims = workloads.policy_dims(name)
+    ws, bs = workloads.policy_weights(dims, seed=1000)
+    pol = R.Policy(ws, bs, dt)
+    es = 2 if dt == "bf16" else 4
+    flop_per_row = 2 * sum(dims[i] * dims[i + 1] for i in range(3))
+    state = R.new_state(cfg)
+    R.rollout_init(cfg, state)
+    f = dict(device="cuda")
+    obs = torch.empty(T, E, A, D, dtype=pol.torch_dtype, **f)
+    acts = torch.empty(T, E, A, dtype=torch.int32, **f)
+    rew, done = torch.empty(T, E, **f), torch.empty(T, E, dtype=torch.uint8, **f)
+    value, logp, vlast = torch.empty(T, E, A, **f), torch.empty(T, E, A, **f), torch.empty(E, A, **f)
+    adv, ret = torch.empty(T, E, A, **f), torch.empty(T, E, A, **f)
+    t_next = [0]
+
+    def run():
+        R.rollout_run_ac(cfg, pol, state, t_next[0], T, value=value, logp=logp, value_last=vlast, obs=obs,
+                         actions=acts, reward=rew, done=done)
+        t_next[0] += T
+
+    kern_ms, wall_ms = timed(run, steps, warmup)
+    nbytes = E * T * (A * D * es + A * 4 + 4 + 1 + A * 8) + E * A * 4 + 2 * R.rl_state_bytes(cfg)
+    flops = E * T * A * flop_per_row
+    gae_ms, _ = timed(lambda: R.gae(rew, done, value, vlast, w["gamma"], w["lam"], adv=adv, ret=ret), steps, warmup)
+    gae_bytes = T * E * (4 + 1) + T * E * A * (4 + 8) + E * A * 4
+    return {"workload": name, "dtype": dt, "n_envs": E, "steps_per_rollout": T, "policy": "-".join(map(str, dims)),
+            "value": round(E * T * A / (wall_ms * 1e-3), 1), "unit": "agent-env steps/s",
+            "ms_per_step": round(wall_ms, 4), "kernel_ms": round(kern_ms, 4),
+            "roofline_hbm": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"),
+            "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s"),
+            "gae": {"kernel_ms": round(gae_ms, 4),
+                    "roofline": roofline("hbm", gae_bytes / (gae_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s")}}
+
+
 def cpu_baseline(n_envs, T):
     """The oracle, single-threaded, on the first n_envs envs of the workload for T steps."""
     import numpy as np
@@ -315,7 +356,9 @@ def main():
         return dict(kern_ms=kern_ms, rows=rows, flops=flops, tflops=flops / (kern_ms * 1e-3) / 1e12)
 
     if args.workload_only:
-        measure = measure_population if "population" in workloads.WORKLOADS[args.workload_only] else measure_workload
+        wl = workloads.WORKLOADS[args.workload_only]
+        measure = (measure_population if "population" in wl else
+                   measure_actor_critic if wl.get("value_head") else measure_workload)
         print(json.dumps(measure(R, workloads, args.workload_only, "bf16", args.steps, args.warmup)),
               flush=True)
         return
@@ -382,6 +425,8 @@ def main():
         # the other workloads at full size, bf16, a few timed launches each
         line["workloads"] = {n: measure_workload(R, workloads, n, "bf16", min(args.steps, 5), 1)
                              for n in ("lbf12_16k", "oc_4096", "hn_4096")}
+        line["workloads"]["lbf8_4096_ac"] = measure_actor_critic(R, workloads, "lbf8_4096_ac", "bf16",
+                                                                 min(args.steps, 5), 1)
         line["workloads"]["lbf8_4096_pop"] = measure_population(R, workloads, "lbf8_4096_pop", "bf16",
                                                                 min(args.steps, 5), 1)
     if not args.no_cpu_baseline:

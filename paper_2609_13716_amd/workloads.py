@@ -24,6 +24,12 @@ Two-player Hanabi (5 colours x 5 ranks, hands of 5, 8 info tokens, 3 lives):
     hn_4096      4096 envs x 80 steps, MLP 658-512-512-20 bf16 on the mover's
                  observation, illegal actions masked
 
+Actor-critic rollout (what a PPO-style learner consumes after a rollout):
+    lbf8_4096_ac lbf8_4096's envs, an MLP 192-128-128-7 bf16 whose last output
+                 is the value head; the rollout writes values and log pi(a), then
+                 generalised advantage estimation (gamma 0.99, lambda 0.95) runs
+                 over the stored trajectory
+
 Population rollout (ad hoc teamwork evaluation: one ego policy paired with a
 set of teammate policies, all of one shape):
     lbf8_4096_pop  lbf8_4096's envs, a population of 9 MLPs 192-128-128-6 bf16:
@@ -47,6 +53,10 @@ WORKLOADS = {
                     n_envs=4096, n_steps=400, hidden=(256, 256), dtypes=("bf16",)),
     "hn_4096": dict(kind="hanabi", env=dict(max_steps=1000), n_envs=4096, n_steps=80, hidden=(512, 512),
                     dtypes=("bf16",)),
+    "lbf8_4096_ac": dict(env=dict(grid_h=8, grid_w=8, n_agents=2, n_food=3, max_agent_level=2, max_food_level=3,
+                                  max_steps=50),
+                         n_envs=4096, n_steps=128, hidden=(128, 128), dtypes=("bf16",), value_head=True,
+                         gamma=0.99, lam=0.95),
     "lbf8_4096_pop": dict(env=dict(grid_h=8, grid_w=8, n_agents=2, n_food=3, max_agent_level=2, max_food_level=3,
                                    max_steps=50),
                           n_envs=4096, n_steps=128, hidden=(128, 128), dtypes=("bf16",), population=9),
@@ -68,7 +78,10 @@ def kind(name):
 
 
 def policy_dims(name):
+    """(D, H1, H2, outputs): the outputs include the value when the workload has a value head."""
     w = WORKLOADS[name]
+    if w.get("value_head"):
+        return (lbf_obs_dim(w["env"]), *w["hidden"], LBF_ACTIONS + 1)
     if kind(name) == "overcooked":
         return (OC_OBS_DIM, *w["hidden"], OC_ACTIONS)
     if kind(name) == "hanabi":
