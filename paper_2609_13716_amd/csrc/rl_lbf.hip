@@ -658,6 +658,34 @@ __device__ __forceinline__ void copy_obs_rows(T* xs, T* __restrict__ g, int rows
   }
 }
 
+// The value of lane l in the partner group of 16 lanes (groups 0 <-> 1, 2 <-> 3).
+__device__ __forceinline__ float partner16(float x) {
+  const auto pr = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(((threadIdx.x >> 4) & 1) ? pr[0] : pr[1]);
+}
+
+// log pi(a) of a row of the transposed layer 3, whose NA <= 8 action logits
+// sit in two partner lane groups (actions 4 g + r in logit[r] of group g):
+// a float32 log-softmax with the max and the exp-sum combined over the pair.
+// Both lanes of a pair return the same value (a sum of two floats commutes).
+template <int NA>
+__device__ __forceinline__ float row_log_pi(const float (&logit)[4], int g, int a) {
+  float m = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    if (4 * g + r < NA) m = fmaxf(m, logit[r]);
+  m = fmaxf(m, partner16(m));
+  float sum = 0.f, c = 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if (4 * g + r < NA) sum += expf(logit[r] - m);
+    if (4 * g + r == a) c = logit[r];
+  }
+  sum += partner16(sum);
+  const float oc = partner16(c);
+  return ((a >> 2) == g ? c : oc) - (m + logf(sum));
+}
+
 // Same step as lbf_run_kernel for compile-time policy sizes, restructured for
 // latency:
 //   * layer-1/2 weights live in registers and layer 3 in LDS for the whole
@@ -674,7 +702,10 @@ __device__ __forceinline__ void copy_obs_rows(T* xs, T* __restrict__ g, int rows
 //     registers plus one v_permlane16_swap) and steps the TE envs, drawing the
 //     reset blocks of ended episodes on idle lanes in parallel.
 // TE envs per workgroup; the launch bounds let MINB workgroups share a CU.
-template <int DT, int GH, int GW, int H1, int H2, int NA, int A, int F, int TE, int NW, int MINB>
+// VH: layer 3 has one more output, the value head V(o) of an actor-critic
+// network, written with log pi of each sampled action and, after the last
+// step, V of the final observation.
+template <int DT, int GH, int GW, int H1, int H2, int NA, int A, int F, int TE, int NW, int MINB, bool VH = false>
 __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p, PolicyArgs pol,
                                                                     int32_t* __restrict__ state, uint64_t t0,
                                                                     int n_steps, TrajArgs out) {
@@ -697,7 +728,9 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   constexpr int REG_BUDGET = 512 / ((NW * MINB + 3) / 4);
   constexpr bool LEAN =
       RegLayer<DT, D, H1, NW>::WREGS + RegLayer<DT, H1, H2, NW>::WREGS + 160 > REG_BUDGET;
-  static_assert(NA <= 8, "one Philox block of action noise per row");
+  constexpr int NOUT = NA + (VH ? 1 : 0);  // layer-3 outputs: the actions, then the value
+  static_assert(NA <= 8 && NOUT <= 8, "one Philox block of action noise per row; outputs in two lane groups");
+  static_assert(!(VH && LEAN), "the value head runs on shapes whose env state stays in registers");
   static_assert(TE <= 64, "env lanes live in wave 0");
   static_assert(TE * ((2 * A + 2 * F + 7) / 8) <= 64, "one lane per reset block");
 
@@ -738,15 +771,15 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   L2.load(static_cast<const T*>(pol.W[1]), static_cast<const T*>(pol.b[1]), wave, lane);
   if (tid < 64) {
     const int n = lane & 15;
-    const T* row = static_cast<const T*>(pol.W[2]) + (size_t)(n < NA ? n : 0) * H2;
+    const T* row = static_cast<const T*>(pol.W[2]) + (size_t)(n < NOUT ? n : 0) * H2;
 #pragma unroll
-    for (int ks = 0; ks < K3; ++ks) w3s[ks * 64 + lane] = load_operand_global<DT, H2>(row, H2, ks, lane, n < NA);
+    for (int ks = 0; ks < K3; ++ks) w3s[ks * 64 + lane] = load_operand_global<DT, H2>(row, H2, ks, lane, n < NOUT);
   }
-  float b3r[4];  // bias of actions 4 * (lane / 16) + r, for the transposed layer 3
+  float b3r[4];  // bias of outputs 4 * (lane / 16) + r, for the transposed layer 3
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int act = 4 * (lane >> 4) + r;
-    b3r[r] = act < NA ? DType<DT>::to_f32(static_cast<const T*>(pol.b[2])[act]) : 0.f;
+    b3r[r] = act < NOUT ? DType<DT>::to_f32(static_cast<const T*>(pol.b[2])[act]) : 0.f;
   }
 
   // zero the operand tiles (their K padding and unused rows stay zero)
@@ -864,6 +897,14 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
           if constexpr (!DIRECT) act_s[row] = best_a;
           if (out.actions) out.actions[((size_t)k * E + e0) * A + row] = best_a;
         }
+        if constexpr (VH) {
+          const size_t gr = ((size_t)k * E + e0) * A + row;
+          if (live && g == NA / 4 && out.value) out.value[gr] = logit[NA % 4];
+          if (out.logp) {
+            const float lp = row_log_pi<NA>(logit, g, best_a);
+            if (live && g == 0) out.logp[gr] = lp;
+          }
+        }
         if constexpr (DIRECT) {
           act_d[0] = best_a;
           if constexpr (A > 1) act_d[1] = __builtin_amdgcn_update_dpp(0, best_a, 0x101, 0xf, 0xf, false);  // row_shl:1
@@ -923,6 +964,33 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   __syncthreads();
   if (out.obs_last)
     copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, te_valid * A, tid);
+  if constexpr (VH) {
+    if (out.value_last) {  // V(o_{t0+T}): one more pass of the network over the final tile
+      {
+        f32x4 acc[MT][RegLayer<DT, D, H1, NW, LEAN>::OWN];
+        L1.template run<MT>(xs, LDX, acc, wave, lane);
+        L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane, bias_s);
+      }
+      __syncthreads();
+      {
+        f32x4 acc[MT][RegLayer<DT, H1, H2, NW, LEAN>::OWN];
+        L2.template run<MT>(h1s, LD1, acc, wave, lane);
+        L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane, bias_s + H1);
+      }
+      __syncthreads();
+      if (wave == ew) {  // (the whole wave takes part in the MFMAs)
+        for (int mt = 0; mt < MT; ++mt) {
+          const int row = mt * 16 + (lane & 15);
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < K3; ++ks)
+            acc = mfma16<DT>(w3s[ks * 64 + lane], load_operand_lds<DT>(h2s, LD2, row, ks, lane), acc);
+          if ((lane >> 4) == NA / 4 && row < te_valid * A)
+            out.value_last[(size_t)e0 * A + row] = acc[NA % 4] + b3r[NA % 4];
+        }
+      }
+    }
+  }
   if constexpr (LEAN) lbf_copy<A, F>(s, env_s[min(el, TE - 1)]);
   if (envlane) lbf_store<A, F>(state, p, e, s);
 }
@@ -930,10 +998,10 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
 // Compile-time shapes that run on lbf_rollout_kernel (everything else uses
 // lbf_run_kernel): LBF 8x8 with 2 agents and 3 foods (obs 192) under 64- and
 // 128-wide layers.
-template <int DT, int GH, int GW, int H1, int H2, int A, int F, int TE, int NW, int MINB>
+template <int DT, int GH, int GW, int H1, int H2, int A, int F, int TE, int NW, int MINB, bool VH>
 static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic&, const PolicyArgs& pol, int32_t* state,
                                      uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s) {
-  auto kern = lbf_rollout_kernel<DT, GH, GW, H1, H2, LBF_NACT, A, F, TE, NW, MINB>;
+  auto kern = lbf_rollout_kernel<DT, GH, GW, H1, H2, LBF_NACT, A, F, TE, NW, MINB, VH>;
   const dim3 grid((unsigned)((p.E + TE - 1) / TE));
   kern<<<grid, NW * 64, 0, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
@@ -941,20 +1009,25 @@ static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic&, const 
 
 static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const PolicyArgs& pol, int32_t* state,
                                    uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s, hipError_t* err) {
-  if (pol.NA != LBF_NACT) return false;
-#define RL_REG_CASE(DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV)                                        \
+  if (pol.NA != LBF_NACT + pol.VH) return false;
+#define RL_REG_CASE(DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV, VHV)                                    \
   if (pol.dt == DTV && p.H == GHV && p.W == GWV && pol.H1 == H1V && pol.H2 == H2V && p.A == AV &&            \
-      p.F == FV) {                                                                                           \
-    *err = launch_rollout_reg<DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV>(p, m, pol, state, t0, n_steps, \
-                                                                                out, s);                     \
+      p.F == FV && pol.VH == VHV) {                                                                          \
+    *err = launch_rollout_reg<DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV, VHV>(p, m, pol, state, t0,    \
+                                                                                     n_steps, out, s);       \
     return true;                                                                                             \
   }
-  // (dtype, grid rows, grid cols, hidden, hidden, agents, foods, envs per workgroup, waves, workgroups per CU)
-  RL_REG_CASE(DT_F32, 8, 8, 64, 64, 2, 3, 8, 4, 2)
-  RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2)
-  RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1)
-  RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2)
-  RL_REG_CASE(DT_BF16, 12, 12, 256, 256, 3, 6, 16, 8, 1)
+  // (dtype, grid rows, grid cols, hidden, hidden, agents, foods, envs per workgroup, waves, workgroups per CU,
+  //  value head)
+  RL_REG_CASE(DT_F32, 8, 8, 64, 64, 2, 3, 8, 4, 2, 0)
+  RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2, 0)
+  RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1, 0)
+  RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2, 0)
+  RL_REG_CASE(DT_BF16, 12, 12, 256, 256, 3, 6, 16, 8, 1, 0)
+  RL_REG_CASE(DT_F32, 8, 8, 64, 64, 2, 3, 8, 4, 2, 1)
+  RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2, 1)
+  RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1, 1)
+  RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2, 1)
 #undef RL_REG_CASE
   return false;
 }

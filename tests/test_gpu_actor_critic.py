@@ -7,7 +7,8 @@ the GPU's own float32 logits (strict run), so the check isolates the
 log-softmax arithmetic: 1e-5 relative plus 1e-6.  GAE (float32 on the GPU,
 float64 in the oracle) agrees within 1e-5 relative plus 1e-5 over 128 steps.
 A value head that is all zeros but its bias leaves every other output exactly
-as rollout_run's (same MFMA chains for the action columns).
+as rollout_run's (same MFMA chains for the action columns), on the generic
+and on the register-resident kernel.
 """
 
 import sys
@@ -93,12 +94,16 @@ def test_actor_critic_rollout_parity(dims, dtype):
     assert (g["logp"].numpy() <= 0).all()
 
 
-def test_value_head_leaves_the_rollout_unchanged():
+@pytest.mark.parametrize("dims", [(192, 48, 32, 6), (192, 64, 64, 6), (192, 128, 128, 6)])
+def test_value_head_leaves_the_rollout_unchanged(dims):
+    """With and without the value head each shape runs on one kernel family
+    (generic for 48-32, register-resident for 64-64 and 128-128), whose action
+    columns take the same MFMA chains either way."""
     require_gpu()
     cfg = R.EnvConfig(n_envs=45, seed=4)
-    dims = (192, 48, 32, 6)  # a shape both entry points run on the same (generic) kernel
     T = 40
     for dtype in ("f32", "bf16"):
+        _note(f"value head off/on {dims} {dtype}")
         ws, bs = workloads.policy_weights(dims, seed=8, bias_scale=0.2)
         wv = [w.copy() for w in ws]
         bv = [b.copy() for b in bs]
