@@ -88,6 +88,11 @@ typedef struct {
   int32_t oc_cook_time;    /* Overcooked: steps a full pot cooks (0 for LBF) */
   int32_t oc_soup_reward;  /* Overcooked: reward of a served soup (0 for LBF) */
   int32_t hn_colors, hn_ranks, hn_hand_size, hn_info_tokens, hn_life_tokens; /* Hanabi (0 otherwise) */
+  int32_t lbf_const_levels; /* LBF, 0 or 1: 1 is the constant-levels variant (the paper's LBF task table):
+                               every agent at max_agent_level and every food at max_food_level, which
+                               must not exceed n_agents * max_agent_level; the level draws of a reset are
+                               still made and ignored, so cells are those of the drawn-levels game.
+                               0 (and for other kinds) = levels drawn at each reset */
   int64_t env_base;        /* global id of env 0 of this batch (>= 0) */
   uint64_t seed;           /* Philox key word 0 */
 } rl_env_config;

@@ -64,6 +64,11 @@ class Config:
     max_agent_level: int
     max_food_level: int
     max_steps: int = 50
+    # the constant-levels variant of the paper's LBF task table: every agent at
+    # max_agent_level, every food at max_food_level.  Reading: the reset still
+    # takes its level draws (and ignores them), so cells match the game with
+    # drawn levels under the same seed.
+    const_levels: bool = False
 
     @property
     def obs_dim(self):
@@ -92,6 +97,9 @@ def reset(cfg, seed, env_id, t):
     agent_level = [1 + philox.uniform_int(next(draws), cfg.max_agent_level) for _ in range(A)]
     fmax = min(cfg.max_food_level, sum(agent_level))
     food_level = [1 + philox.uniform_int(next(draws), fmax) for _ in range(F)]
+    if cfg.const_levels:
+        agent_level = [cfg.max_agent_level] * A
+        food_level = [cfg.max_food_level] * F
     food_cell = []
     for _ in range(F):
         free = [r * W + c for r in range(1, H - 1) for c in range(1, W - 1)

@@ -56,6 +56,11 @@ rl_status check_lbf(const rl_env_config* cfg, EnvSpec* es) {
   if (cfg->n_food + cfg->n_agents > hw) return fail(RL_EINVAL, "LBF grid too small for agents and food");
   if (cfg->max_agent_level < 1 || cfg->max_agent_level > 15 || cfg->max_food_level < 1 || cfg->max_food_level > 15)
     return fail(RL_EINVAL, "LBF levels must be in 1..15");
+  if (cfg->lbf_const_levels != 0 && cfg->lbf_const_levels != 1)
+    return fail(RL_EINVAL, "lbf_const_levels must be 0 or 1");
+  if (cfg->lbf_const_levels && cfg->max_food_level > cfg->n_agents * cfg->max_agent_level)
+    return fail(RL_EINVAL, "constant food level %d exceeds the agents' total level %d", cfg->max_food_level,
+                cfg->n_agents * cfg->max_agent_level);
   if (cfg->oc_cook_time || cfg->oc_soup_reward || cfg->hn_colors || cfg->hn_ranks || cfg->hn_hand_size ||
       cfg->hn_info_tokens || cfg->hn_life_tokens)
     return fail(RL_EINVAL, "Overcooked/Hanabi fields must be 0 for LBF");
@@ -70,6 +75,7 @@ rl_status check_lbf(const rl_env_config* cfg, EnvSpec* es) {
   p.Lmax = cfg->max_agent_level;
   p.Fmax = cfg->max_food_level;
   p.max_steps = cfg->max_steps;
+  p.const_levels = cfg->lbf_const_levels;
   p.wmagic = rl::div_magic((uint32_t)cfg->grid_w);
   p.env_base = cfg->env_base;
   p.seed = cfg->seed;
@@ -87,7 +93,7 @@ rl_status check_overcooked(const rl_env_config* cfg, EnvSpec* es) {
   if (cfg->oc_soup_reward < 0 || cfg->oc_soup_reward > (1 << 20))
     return fail(RL_EINVAL, "Overcooked soup_reward %d outside 0..2^20", cfg->oc_soup_reward);
   if (cfg->grid_h || cfg->grid_w || cfg->n_food || cfg->max_agent_level || cfg->max_food_level ||
-      cfg->hn_colors || cfg->hn_ranks || cfg->hn_hand_size || cfg->hn_info_tokens || cfg->hn_life_tokens)
+      cfg->lbf_const_levels || cfg->hn_colors || cfg->hn_ranks || cfg->hn_hand_size || cfg->hn_info_tokens || cfg->hn_life_tokens)
     return fail(RL_EINVAL, "LBF/Hanabi fields must be 0 for Overcooked");
   rl::OcParams& p = es->oc;
   p.E = cfg->n_envs;
@@ -112,7 +118,7 @@ rl_status check_hanabi(const rl_env_config* cfg, EnvSpec* es) {
       cfg->hn_info_tokens != rl::HN_INFO || cfg->hn_life_tokens != rl::HN_LIVES)
     return fail(RL_EUNSUPPORTED, "Hanabi is built for 5 colours, 5 ranks, hands of 5, 8 info tokens, 3 lives");
   if (cfg->grid_h || cfg->grid_w || cfg->n_food || cfg->max_agent_level || cfg->max_food_level ||
-      cfg->oc_cook_time || cfg->oc_soup_reward)
+      cfg->lbf_const_levels || cfg->oc_cook_time || cfg->oc_soup_reward)
     return fail(RL_EINVAL, "LBF/Overcooked fields must be 0 for Hanabi");
   rl::HnParams& p = es->hn;
   p.E = cfg->n_envs;

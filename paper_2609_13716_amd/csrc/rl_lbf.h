@@ -27,6 +27,7 @@ constexpr int LBF_NACT = 6;
 
 struct LbfParams {
   int E, A, F, H, W, HW, D, Lmax, Fmax, max_steps;
+  int const_levels;  // 1: agents at Lmax and foods at Fmax (level draws made and ignored)
   uint32_t wmagic;  // ceil(2^32 / W): x / W == umulhi(x, wmagic) for 0 <= x < 2^16
   int64_t env_base;
   uint64_t seed;
@@ -138,7 +139,7 @@ __device__ __forceinline__ void lbf_reset_from_draws(const LbfParams& p, const u
 #pragma unroll
   for (int i = 0; i < LBF_MAXA; ++i)
     if (i < A) {
-      s.alevel[i] = 1 + (int)range_map(draw(i), (uint32_t)p.Lmax);
+      s.alevel[i] = p.const_levels ? p.Lmax : 1 + (int)range_map(draw(i), (uint32_t)p.Lmax);
       lsum += s.alevel[i];
     }
   const int fcap = p.Fmax < lsum ? p.Fmax : lsum;
@@ -146,7 +147,7 @@ __device__ __forceinline__ void lbf_reset_from_draws(const LbfParams& p, const u
 #pragma unroll
   for (int j = 0; j < LBF_MAXF; ++j)
     if (j < F) {
-      s.flevel[j] = 1 + (int)range_map(draw(A + j), (uint32_t)fcap);
+      s.flevel[j] = p.const_levels ? p.Fmax : 1 + (int)range_map(draw(A + j), (uint32_t)fcap);
       den += s.flevel[j];
     }
   // Food on interior cells, indexed row-major over the (H-2) x (W-2) interior.

@@ -41,7 +41,7 @@ class _EnvConfig(ctypes.Structure):
         ("oc_soup_reward", ctypes.c_int32), ("hn_colors", ctypes.c_int32),
         ("hn_ranks", ctypes.c_int32), ("hn_hand_size", ctypes.c_int32),
         ("hn_info_tokens", ctypes.c_int32), ("hn_life_tokens", ctypes.c_int32),
-        ("env_base", ctypes.c_int64), ("seed", ctypes.c_uint64),
+        ("lbf_const_levels", ctypes.c_int32), ("env_base", ctypes.c_int64), ("seed", ctypes.c_uint64),
     ]
 
 
@@ -120,6 +120,7 @@ class EnvConfig:
     max_agent_level: int = 2
     max_food_level: int = 3
     max_steps: int = 50
+    const_levels: bool = False  # LBF constant-levels variant: agents at max_agent_level, foods at max_food_level
     env_base: int = 0
     seed: int = 0
     extra: dict = field(default_factory=dict)  # Overcooked / Hanabi fields
@@ -129,6 +130,7 @@ class EnvConfig:
         names = ("kind", "n_envs", "n_agents", "max_steps", "env_base", "seed")
         if self.kind == RL_ENV_LBF:
             names += ("grid_h", "grid_w", "n_food", "max_agent_level", "max_food_level")
+            s.lbf_const_levels = int(self.const_levels)
         for k in names:
             setattr(s, k, getattr(self, k))
         for k, v in self.extra.items():

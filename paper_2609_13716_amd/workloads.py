@@ -49,6 +49,11 @@ WORKLOADS = {
     "lbf12_16k": dict(env=dict(grid_h=12, grid_w=12, n_agents=3, n_food=6, max_agent_level=3, max_food_level=6,
                                max_steps=50),
                       n_envs=16384, n_steps=256, hidden=(256, 256), dtypes=("bf16",)),
+    # the constant-levels variant on a 7x7 grid: agents at level 1, foods at
+    # level 2, so every food takes both agents loading together
+    "lbf7_const_4096": dict(env=dict(grid_h=7, grid_w=7, n_agents=2, n_food=3, max_agent_level=1, max_food_level=2,
+                                     max_steps=50, const_levels=True),
+                            n_envs=4096, n_steps=128, hidden=(128, 128), dtypes=("bf16",)),
     "oc_4096": dict(kind="overcooked", env=dict(cook_time=20, soup_reward=20, max_steps=400),
                     n_envs=4096, n_steps=400, hidden=(256, 256), dtypes=("bf16",)),
     "hn_4096": dict(kind="hanabi", env=dict(max_steps=1000), n_envs=4096, n_steps=80, hidden=(512, 512),

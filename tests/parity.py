@@ -16,7 +16,7 @@ def require_gpu():
 
 def oracle_cfg(cfg):
     return lbf.Config(cfg.grid_h, cfg.grid_w, cfg.n_agents, cfg.n_food, cfg.max_agent_level, cfg.max_food_level,
-                      cfg.max_steps)
+                      cfg.max_steps, cfg.const_levels)
 
 
 def states_from_device(cfg, state):

@@ -55,6 +55,8 @@ def _status(cfg):
     (dict(kind=R.RL_ENV_OVERCOOKED), R.RL_EINVAL),  # cook_time 0
     (dict(kind=R.RL_ENV_HANABI), R.RL_EINVAL),  # game sizes 0
     (dict(extra={"hn_colors": 5}), R.RL_EINVAL),
+    (dict(extra={"lbf_const_levels": 2}), R.RL_EINVAL),
+    (dict(const_levels=True, max_agent_level=1, max_food_level=3), R.RL_EINVAL),  # food level 3 > 2 agents * 1
 ])
 def test_bad_config(kw, code):
     cfg = _cfg(**kw)
@@ -76,7 +78,8 @@ def test_bad_overcooked_config(kw, code):
 
 
 def test_overcooked_rejects_other_kinds_fields():
-    for name, v in (("n_agents", 3), ("grid_h", 5), ("n_food", 1), ("max_food_level", 2), ("hn_colors", 5)):
+    for name, v in (("n_agents", 3), ("grid_h", 5), ("n_food", 1), ("max_food_level", 2), ("hn_colors", 5),
+                    ("lbf_const_levels", 1)):
         c = R.overcooked_config(16).c()
         setattr(c, name, v)
         assert R.lib.rl_obs_dim(ctypes.byref(c)) == R.RL_EINVAL, name
@@ -88,7 +91,8 @@ def test_hanabi_config_checks():
     assert R.rl_state_bytes(cfg) == 35 * 100 * 4
     for name, v, code in (("hn_colors", 4, R.RL_EUNSUPPORTED), ("hn_hand_size", 4, R.RL_EUNSUPPORTED),
                           ("hn_life_tokens", 0, R.RL_EINVAL), ("n_agents", 3, R.RL_EINVAL),
-                          ("grid_w", 3, R.RL_EINVAL), ("oc_cook_time", 20, R.RL_EINVAL)):
+                          ("grid_w", 3, R.RL_EINVAL), ("oc_cook_time", 20, R.RL_EINVAL),
+                          ("lbf_const_levels", 1, R.RL_EINVAL)):
         c = R.hanabi_config(16).c()
         setattr(c, name, v)
         assert R.lib.rl_obs_dim(ctypes.byref(c)) == code, name
@@ -196,3 +200,9 @@ def test_binding_rejects_host_tensors():
     cfg = _cfg()
     with pytest.raises(ValueError):
         R.rollout_init(cfg, torch.zeros(10, dtype=torch.int32))
+
+
+def test_constant_levels_config_is_accepted():
+    cfg = _cfg(grid_h=7, grid_w=7, const_levels=True, max_agent_level=1, max_food_level=2)
+    assert _status(cfg) == 147
+    assert cfg.c().lbf_const_levels == 1 and _cfg().c().lbf_const_levels == 0

@@ -97,6 +97,8 @@ def test_init_matches_oracle(dtype):
     (dict(n_envs=19, grid_h=5, grid_w=7, n_agents=4, n_food=2, max_agent_level=3, max_food_level=9,
           max_steps=13), 60, torch.float32),
     (dict(n_envs=5, grid_h=3, grid_w=3, n_agents=2, n_food=1, max_steps=7), 40, torch.float32),
+    (dict(n_envs=23, grid_h=7, grid_w=7, n_agents=2, n_food=3, max_agent_level=1, max_food_level=2,
+          const_levels=True), 90, torch.bfloat16),
 ])
 def test_env_only_parity(cfgkw, T, dtype):
     require_gpu()
@@ -416,3 +418,29 @@ def test_rollout_run_generic_shapes():
         ref = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, dtype, action_hook=hook)
         _check_traj(g, ref, slice(None), RTOL[dtype])
         assert states_from_device(cfg, state) == ref["states"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rollout_run_7x7_constant_levels(dtype):
+    """The 7x7 constant-levels variant (agents at level 1, foods at level 2), every env of two workgroups and a
+    ragged tail against the oracle; levels in the final states are the constants."""
+    require_gpu()
+    name = "lbf7_const_4096"
+    w = workloads.WORKLOADS[name]
+    cfg = R.EnvConfig(n_envs=41, seed=12, env_base=7, **w["env"])
+    dims = workloads.policy_dims(name)
+    assert dims[0] == 147
+    ws, bs = workloads.policy_weights(dims, seed=71, bias_scale=0.1)
+    pol = R.Policy(ws, bs, dtype)
+    T = 80
+    _note(f"rollout_run {name} n_envs=41 T={T} {dtype}")
+    state, g = _run_gpu(cfg, pol, T)
+    oc = oracle_cfg(cfg)
+    env_ids = list(range(7, 48))
+    hook = NearTieLockstep(g["actions"].numpy(), cfg.seed, env_ids, RTOL[dtype])
+    ref = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, dtype, action_hook=hook)
+    _check_traj(g, ref, slice(None), RTOL[dtype])
+    states = states_from_device(cfg, state)
+    assert states == ref["states"]
+    assert all(s.agent_level == [1, 1] and s.food_level == [2, 2, 2] for s in states)
+    assert ref["done"].any()
