@@ -20,7 +20,7 @@ Output layout (``n`` = number of env ids, A agents, D obs features):
 
 import numpy as np
 
-from . import actor_critic, mlp, sampling
+from . import actor_critic, mlp, s5, sampling
 
 
 def initial_states(env, cfg, seed, env_ids):
@@ -63,7 +63,8 @@ def policy_logits(obs, weights, biases, dtype, policy_index=None):
 
 
 def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
-            states=None, logits_source=None, action_hook=None, policy_index=None, value_head=False):
+            states=None, logits_source=None, action_hook=None, policy_index=None, value_head=False,
+            recurrent=None, carry=None):
     """Roll ``env_ids`` forward ``n_steps`` steps from absolute step ``t0``.
 
     ``states`` are the env states at t0 (default: the initial states, t0 = 0).
@@ -78,6 +79,12 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     ``value_last`` [n, A] (V of obs_last) and ``logp`` [T, n, A], the float64
     log-probability of each sampled action under the float32 logits it was
     sampled from (``logits`` keeps the nA action logits).
+    ``recurrent``: an ``s5.Params`` actor-critic that replaces (weights,
+    biases) and implies ``value_head``; ``carry`` [n * A, P] complex is its
+    state at t0 (rows env-major, default zeros).  An agent's state is zeroed
+    at every step whose observation starts an episode (step counter 0); the
+    result also holds ``carry``, the state after the last step (value_last is
+    computed without advancing it).
     """
     env_ids = list(env_ids)
     if states is None:
@@ -88,10 +95,24 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     n, A = len(env_ids), cfg.n_agents
     nA = env.N_ACTIONS
     out = {k: [] for k in ("obs", "logits", "actions", "reward", "done", "mask", "value", "logp")}
+    if recurrent is not None:
+        value_head = True
+        carry = s5.initial_state(n * A, recurrent) if carry is None else np.array(carry, dtype=np.complex128)
+
+    def net(obs, states, commit):
+        nonlocal carry
+        if recurrent is None:
+            return policy_logits(obs, weights, biases, dtype, policy_index)
+        start = np.repeat([s.step_count == 0 for s in states], A)
+        lg, v, x = s5.step(recurrent, obs.reshape(n * A, -1), carry, start, dtype)
+        if commit:
+            carry = x
+        return np.concatenate([lg, v[:, None]], axis=1).reshape(n, A, -1)
+
     for k in range(n_steps):
         t = t0 + k
         obs, mask = observe_all(env, cfg, states)
-        logits64 = policy_logits(obs, weights, biases, dtype, policy_index)
+        logits64 = net(obs, states, True)
         if value_head:
             out["value"].append(logits64[..., nA])
             logits64 = logits64[..., :nA]
@@ -121,8 +142,10 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     res = {k: np.stack(v) if v else None for k, v in out.items()}
     res["obs_last"], res["mask_last"] = observe_all(env, cfg, states)
     if value_head:
-        res["value_last"] = policy_logits(res["obs_last"], weights, biases, dtype, policy_index)[..., nA]
+        res["value_last"] = net(res["obs_last"], states, False)[..., nA]
     res["states"] = states
+    if recurrent is not None:
+        res["carry"] = carry
     return res
 
 

@@ -107,6 +107,31 @@ def policy_weights(dims, seed, bias_scale=0.0):
     return ws, bs
 
 
+def s5_params(D, H, P, F, n_actions, seed):
+    """Synthetic continuous-time parameters of an S5 actor-critic (float32 arrays).
+
+    Encoder [H, D]; S5 with Re(lambda) = -0.5 and Im(lambda_p) = pi * p (the
+    shape of the diagonalised HiPPO-N start of S5), log step uniform in
+    [log 1e-3, log 1e-1], B and C complex normal (variance 1/H and 1/P split
+    over real and imaginary parts), D standard normal; actor and critic heads
+    H -> F -> F -> F -> (n_actions | 1) with N(0, 1/fan_in) weights."""
+    rng = np.random.default_rng(seed)
+    we, be = policy_weights((D, H), seed + 1, bias_scale=0.1)
+    aw, ab = policy_weights((H, F, F, F, n_actions), seed + 2, bias_scale=0.1)
+    cw, cb = policy_weights((H, F, F, F, 1), seed + 3, bias_scale=0.1)
+    f32 = np.float32
+    return dict(
+        w_enc=we[0], b_enc=be[0],
+        lam_re=np.full(P, -0.5, f32), lam_im=(np.pi * np.arange(P)).astype(f32),
+        log_dt=rng.uniform(np.log(1e-3), np.log(1e-1), P).astype(f32),
+        b_re=(rng.standard_normal((P, H)) / np.sqrt(2 * H)).astype(f32),
+        b_im=(rng.standard_normal((P, H)) / np.sqrt(2 * H)).astype(f32),
+        c_re=(rng.standard_normal((H, P)) / np.sqrt(2 * P)).astype(f32),
+        c_im=(rng.standard_normal((H, P)) / np.sqrt(2 * P)).astype(f32),
+        d=rng.standard_normal(H).astype(f32),
+        actor_w=aw, actor_b=ab, critic_w=cw, critic_b=cb)
+
+
 def injected_actions(n_steps, n_envs, n_agents, n_actions, seed, p_invalid=0.0):
     """Uniform actions [T, E, A] int32; a fraction ``p_invalid`` is replaced by out-of-range values."""
     rng = np.random.default_rng(seed)
