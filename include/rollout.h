@@ -228,6 +228,74 @@ rl_status rollout_run_pop(const rl_env_config* cfg, const rl_policy* pop, int32_
                           const int32_t* policy_index, void* state, uint64_t t0, int32_t n_steps,
                           const rl_traj* out, void* stream);
 
+/* ---- recurrent S5 actor-critic (the paper's ego agent, Appendix on agent
+ * architectures: dense encoder, S5 of model width 128 and state 128, actor
+ * and critic heads of three 1024-unit layers) ----
+ *
+ * Network, per agent row and step:  u = tanh(W_enc o + b_enc)       [H]
+ *   x_t = Lambda_bar x_{t-1} + B_bar u    (complex [P]; x_{t-1} := 0 when o
+ *                                          is the first of its episode)
+ *   y = Re(C x_t) + d * u                 [H]
+ *   actor:  three tanh layers of width F, then nA logits;
+ *   critic: three tanh layers of width F, then one value.
+ * S5 is Smith et al., ICLR 2023; the reset at episode starts follows Lu et
+ * al., NeurIPS 2023.  Dense layers are bfloat16 (nn.Linear layout [out, in]),
+ * every product accumulates in float32 and u, y and the head activations are
+ * rounded to bfloat16; the S5 parameters and state are float32.  Every
+ * pointer is device memory, 16-byte aligned.
+ * Limits: dtype RL_BF16; H a multiple of 64 in 64..256; P a multiple of 16 in
+ * 16..256; F a multiple of 128 in 128..4096; nA in 1..16; D (the env's
+ * observation size) at most 1024. */
+typedef struct {
+  int32_t dtype;       /* RL_BF16 */
+  int32_t obs_dim;     /* D, must equal rl_obs_dim(cfg) */
+  int32_t d_model;     /* H */
+  int32_t d_state;     /* P */
+  int32_t head_width;  /* F */
+  int32_t n_actions;   /* nA, must equal rl_num_actions(cfg) */
+  const void* w_enc;   /* [H, D] */
+  const void* b_enc;   /* [H] */
+  const float* lambda_bar; /* [2, P]: real parts, then imaginary parts (from rl_s5_discretize) */
+  const float* b_bar;      /* [2, P, H] */
+  const float* c;          /* [2, H, P] */
+  const float* d;          /* [H] */
+  const void* actor_w[4];  /* [F, H], [F, F], [F, F], [nA, F] */
+  const void* actor_b[4];
+  const void* critic_w[4]; /* [F, H], [F, F], [F, F], [1, F] */
+  const void* critic_b[4];
+} rl_s5_policy;
+
+/* Zero-order hold of the continuous S5 parameters (Smith et al., Section 2):
+ * lambda_bar = exp(lambda dt), b_bar = (lambda_bar - 1) / lambda * b with
+ * dt = exp(log_dt), evaluated in double precision and rounded to float32.
+ *   lambda [2, P] (real parts < 0), log_dt [P], b [2, P, H] read;
+ *   lambda_bar [2, P], b_bar [2, P, H] written.  P, H >= 1. */
+rl_status rl_s5_discretize(int32_t d_state, int32_t d_model, const float* lambda, const float* log_dt,
+                           const float* b, float* lambda_bar, float* b_bar, void* stream);
+
+/* Bytes of the device workspace rollout_run_s5 needs for cfg and policy
+ * (hidden activations of both heads, y, two observation tiles, actions);
+ * 0 if either is invalid. */
+size_t rl_s5_workspace_bytes(const rl_env_config* cfg, const rl_s5_policy* policy);
+
+/* The rollout loop of rollout_run_ac with the recurrent S5 actor-critic
+ * (LBF only).  Each step runs the policy on o_t (the carried state zeroed
+ * for rows whose episode starts at o_t, i.e. whose env step counter is 0),
+ * samples a_t by Gumbel-max from the logits, and steps the envs.
+ *   carry      [E * A, 2, P] float32 (rows env-major; real then imaginary
+ *              parts): the S5 state of every agent, read and left at step
+ *              t0 + n_steps; its content is irrelevant for rows that start an
+ *              episode at t0 (zeros are a valid start).
+ *   out, ac    as rollout_run_ac; value_last is V(o_{t0+T}) computed without
+ *              advancing carry.
+ *   workspace  rl_s5_workspace_bytes(cfg, policy) bytes of device memory,
+ *              owned by the caller, not read across calls.
+ * The call is a sequence of kernels on `stream` (per step: encoder and S5,
+ * three head layers, output layers and sampling, env step). */
+rl_status rollout_run_s5(const rl_env_config* cfg, const rl_s5_policy* policy, void* state, float* carry,
+                         uint64_t t0, int32_t n_steps, const rl_traj* out, const rl_ac_traj* ac, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
 /* Gumbel-max sampling of the actions of step t from given logits (the
  * sampling stage of rollout_run on its own).
  *   logits  [E, A, nA] float32 read;  legal [E, A, nA] uint8 or NULL;

@@ -307,6 +307,95 @@ rl_status rollout_run_ac(const rl_env_config* cfg, const rl_policy* policy, void
                   "rollout_run_ac");
 }
 
+rl_status rl_s5_discretize(int32_t d_state, int32_t d_model, const float* lambda, const float* log_dt,
+                           const float* b, float* lambda_bar, float* b_bar, void* stream) {
+  if (!lambda || !log_dt || !b || !lambda_bar || !b_bar) return fail(RL_EINVAL, "a required pointer is NULL");
+  if (d_state < 1 || d_model < 1 || (int64_t)d_state * d_model > ((int64_t)1 << 30))
+    return fail(RL_EINVAL, "d_state %d, d_model %d out of range", d_state, d_model);
+  return launched(rl::launch_s5_discretize(d_state, d_model, lambda, log_dt, b, lambda_bar, b_bar,
+                                           (hipStream_t)stream),
+                  "rl_s5_discretize");
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+static rl_status check_s5(const rl_env_config* cfg, const rl_s5_policy* pol, EnvSpec* es, rl::S5Net* net) {
+  rl_status s = check_cfg(cfg, es);
+  if (s != RL_OK) return s;
+  if (es->kind != RL_ENV_LBF) return fail(RL_EUNSUPPORTED, "rollout_run_s5 is implemented for LBF only");
+  if (!pol) return fail(RL_EINVAL, "policy is NULL");
+  if (pol->dtype != RL_BF16) return fail(RL_EUNSUPPORTED, "the S5 policy runs in bfloat16 only");
+  const int H = pol->d_model, P = pol->d_state, F = pol->head_width, NA = pol->n_actions;
+  if (H < 64 || H > 256 || H % 64) return fail(RL_EUNSUPPORTED, "d_model %d must be a multiple of 64 in 64..256", H);
+  if (P < 16 || P > 256 || P % 16) return fail(RL_EUNSUPPORTED, "d_state %d must be a multiple of 16 in 16..256", P);
+  if (F < 128 || F > 4096 || F % 128)
+    return fail(RL_EUNSUPPORTED, "head_width %d must be a multiple of 128 in 128..4096", F);
+  if (pol->obs_dim != es->D) return fail(RL_ESHAPE, "policy obs_dim %d != observation size %d", pol->obs_dim, es->D);
+  if (es->D > 1024) return fail(RL_EUNSUPPORTED, "observation size %d above 1024", es->D);
+  if (NA != es->NA) return fail(RL_ESHAPE, "policy has %d actions, the env %d", NA, es->NA);
+  const void* ptrs[] = {pol->w_enc, pol->b_enc, pol->lambda_bar, pol->b_bar, pol->c, pol->d};
+  for (const void* q : ptrs)
+    if (!q || !aligned16(q)) return fail(RL_EINVAL, "an S5 parameter pointer is NULL or not 16-byte aligned");
+  for (int l = 0; l < 4; ++l)
+    if (!pol->actor_w[l] || !pol->actor_b[l] || !pol->critic_w[l] || !pol->critic_b[l] ||
+        !aligned16(pol->actor_w[l]) || !aligned16(pol->actor_b[l]) || !aligned16(pol->critic_w[l]) ||
+        !aligned16(pol->critic_b[l]))
+      return fail(RL_EINVAL, "head layer %d pointer is NULL or not 16-byte aligned", l);
+  if (rl::s5_front_lds_bytes(es->D, H, P) > rl::MAX_LDS_BYTES)
+    return fail(RL_EUNSUPPORTED, "S5 tile needs more than %zu bytes of LDS", rl::MAX_LDS_BYTES);
+  net->D = es->D;
+  net->H = H;
+  net->P = P;
+  net->F = F;
+  net->NA = NA;
+  net->w_enc = pol->w_enc;
+  net->b_enc = pol->b_enc;
+  net->lbar = pol->lambda_bar;
+  net->bbar = pol->b_bar;
+  net->c = pol->c;
+  net->d = pol->d;
+  for (int l = 0; l < 4; ++l) {
+    net->actor_w[l] = pol->actor_w[l];
+    net->actor_b[l] = pol->actor_b[l];
+    net->critic_w[l] = pol->critic_w[l];
+    net->critic_b[l] = pol->critic_b[l];
+  }
+  return RL_OK;
+}
+
+size_t rl_s5_workspace_bytes(const rl_env_config* cfg, const rl_s5_policy* policy) {
+  EnvSpec es;
+  rl::S5Net net;
+  if (check_s5(cfg, policy, &es, &net) != RL_OK) return 0;
+  return rl::s5_workspace(es.lbf, net).bytes;
+}
+
+rl_status rollout_run_s5(const rl_env_config* cfg, const rl_s5_policy* policy, void* state, float* carry,
+                         uint64_t t0, int32_t n_steps, const rl_traj* out, const rl_ac_traj* ac, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  EnvSpec es;
+  rl::S5Net net;
+  rl_status s = check_s5(cfg, policy, &es, &net);
+  if (s != RL_OK) return s;
+  if (!state || !carry) return fail(RL_EINVAL, "state or carry is NULL");
+  if (!out || !ac) return fail(RL_EINVAL, "out or ac is NULL");
+  if (n_steps < 1) return fail(RL_EINVAL, "n_steps %d must be >= 1", n_steps);
+  if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
+  if ((int64_t)es.E * es.A > ((int64_t)1 << 24)) return fail(RL_EINVAL, "n_envs * n_agents above 2^24");
+  const size_t need = rl::s5_workspace(es.lbf, net).bytes;
+  if (!workspace || !aligned16(workspace) || workspace_bytes < need)
+    return fail(RL_EINVAL, "workspace needs %zu bytes, 16-byte aligned (got %zu)", need, workspace_bytes);
+  if ((out->obs && !aligned16(out->obs)) || (out->obs_last && !aligned16(out->obs_last)))
+    return fail(RL_EINVAL, "obs and obs_last must be 16-byte aligned");
+  rl::TrajArgs o{out->obs, out->actions, out->logits, out->reward, out->done, out->obs_last};
+  o.value = ac->value;
+  o.logp = ac->logp;
+  o.value_last = ac->value_last;
+  return launched(rl::launch_s5_rollout(es.lbf, net, static_cast<int32_t*>(state), carry, t0, n_steps, o, workspace,
+                                        (hipStream_t)stream),
+                  "rollout_run_s5");
+}
+
 rl_status rl_gae(const float* reward, const uint8_t* done, const float* value, const float* value_last,
                  int32_t n_steps, int32_t n_envs, int32_t n_agents, float gamma, float lambda, float* adv,
                  float* ret, void* stream) {

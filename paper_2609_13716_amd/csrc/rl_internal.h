@@ -166,6 +166,33 @@ hipError_t launch_lbf_step(const LbfParams& p, int32_t* state, uint64_t t0, int 
                            uint8_t* legal, hipStream_t s);
 hipError_t launch_lbf_run(const LbfParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
                           const TrajArgs& out, hipStream_t s);
+// Observe the stored LBF states into obs [E, A, D] bf16 (no reset).
+hipError_t launch_lbf_observe(const LbfParams& p, const int32_t* state, uint16_t* obs, hipStream_t s);
+
+// Recurrent S5 actor-critic (rl_s5.hip): bf16 dense layers, float32 S5.
+struct S5Net {
+  int D, H, P, F, NA;
+  const void* w_enc;  // [H, D]
+  const void* b_enc;
+  const float* lbar;  // [2, P] discretised diagonal (real, imaginary)
+  const float* bbar;  // [2, P, H]
+  const float* c;     // [2, H, P]
+  const float* d;     // [H]
+  const void* actor_w[4];
+  const void* actor_b[4];
+  const void* critic_w[4];
+  const void* critic_b[4];
+};
+struct S5Workspace {
+  size_t off_obs, off_y, off_h, off_act, bytes;
+};
+S5Workspace s5_workspace(const LbfParams& p, const S5Net& net);
+size_t s5_front_lds_bytes(int D, int H, int P);
+hipError_t launch_s5_discretize(int P, int H, const float* lam, const float* log_dt, const float* b, float* lbar,
+                                float* bbar, hipStream_t s);
+hipError_t launch_s5_rollout(const LbfParams& p, const S5Net& net, int32_t* state, float* carry, uint64_t t0,
+                             int n_steps, const TrajArgs& out, void* workspace, hipStream_t s);
+
 // Generalised advantage estimation over [T, E, A] values (rl_ac.hip).
 hipError_t launch_gae(const float* reward, const uint8_t* done, const float* value, const float* value_last, int T,
                       int E, int A, float gamma, float lambda, float* adv, float* ret, hipStream_t s);

@@ -196,7 +196,9 @@ __device__ __forceinline__ void lbf_write_legal(const LbfParams& p, int te_valid
 
 // ---------------------------------------------------------------- init ----
 
-template <typename OT>
+// RESET: draw every env's first episode (step 0) and store it; otherwise
+// only observe the stored states.
+template <typename OT, bool RESET = true>
 __global__ __launch_bounds__(NTHREADS) void lbf_init_kernel(LbfParams p, LbfMagic m, int32_t* __restrict__ state,
                                                             OT* __restrict__ obs, uint8_t* __restrict__ legal) {
   __shared__ __align__(16) uint8_t agrid[TILE_E * LBF_MAXCELLS];
@@ -211,8 +213,12 @@ __global__ __launch_bounds__(NTHREADS) void lbf_init_kernel(LbfParams p, LbfMagi
   __syncthreads();
   if (tid < te_valid) {
     LbfEnv s{};
-    lbf_reset(p, (uint64_t)(p.env_base + e0 + tid), 0, s);
-    lbf_store(state, p, e0 + tid, s);
+    if constexpr (RESET) {
+      lbf_reset(p, (uint64_t)(p.env_base + e0 + tid), 0, s);
+      lbf_store(state, p, e0 + tid, s);
+    } else {
+      lbf_load(state, p, e0 + tid, s);
+    }
     lbf_paint(p, s, tid, L, true);
   }
   __syncthreads();
@@ -1182,6 +1188,12 @@ hipError_t launch_lbf_init(const LbfParams& p, int32_t* state, void* obs, int ob
     lbf_init_kernel<float><<<tiles(p.E), NTHREADS, 0, s>>>(p, m, state, static_cast<float*>(obs), legal);
   else
     lbf_init_kernel<uint16_t><<<tiles(p.E), NTHREADS, 0, s>>>(p, m, state, static_cast<uint16_t*>(obs), legal);
+  return hipGetLastError();
+}
+
+hipError_t launch_lbf_observe(const LbfParams& p, const int32_t* state, uint16_t* obs, hipStream_t s) {
+  const LbfMagic m = make_magic(p, LBF_NACT);
+  lbf_init_kernel<uint16_t, false><<<tiles(p.E), NTHREADS, 0, s>>>(p, m, const_cast<int32_t*>(state), obs, nullptr);
   return hipGetLastError();
 }
 

@@ -1,0 +1,518 @@
+// Recurrent S5 actor-critic in the rollout loop (LBF), bfloat16 dense layers.
+//
+// The ego agent of the paper's experiments: observations through a dense
+// encoder into an S5 layer (model width H, complex diagonal state of size P),
+// then separate actor and critic heads of three F-wide tanh layers.  S5
+// (Smith et al., ICLR 2023): zero-order hold of x' = Lambda x + B u gives
+// Lambda_bar = exp(Lambda Delta), B_bar = Lambda^-1 (Lambda_bar - 1) B; a step
+// is x_t = Lambda_bar x_{t-1} + B_bar u_t, y_t = Re(C x_t) + D u_t, with the
+// state zeroed at an episode's first step (as Lu et al., NeurIPS 2023, do
+// for reinforcement learning).
+//
+// One rollout step is six launches on one stream:
+//   front  per 32 rows: observation tile -> encoder (bf16 MFMA, tanh) -> the
+//          S5 step in float32 MFMA (B_bar u as two real products, the
+//          complex diagonal update with the reset, Re(C x) as two real
+//          products) -> y in bf16, the carried state updated in place;
+//   heads  three grouped GEMMs (actor and critic in one launch, 128 x 128
+//          tiles, LDS double buffering, bias + tanh epilogue in bf16);
+//   out    output layers (logits, value), Gumbel-max sampling with the
+//          rollout's Philox draws, log pi of the sampled action;
+//   env    one LBF step with the sampled actions (the env-only kernels).
+// The heads dominate (2 x (H F + 2 F F) MACs per row): they are the GEMMs
+// that the MFMA roofline is taken on.
+#include "rl_internal.h"
+#include "rl_mlp.h"
+#include "rl_sample.h"
+
+namespace rl {
+
+// ------------------------------------------------------- discretisation ----
+
+// Zero-order hold in float64 (rounded once to float32 at the end):
+// lambda_bar = exp(lambda dt), b_bar[p, h] = (lambda_bar - 1) / lambda * b[p, h].
+__global__ void s5_discretize_kernel(int P, int H, const float* __restrict__ lam, const float* __restrict__ log_dt,
+                                     const float* __restrict__ b, float* __restrict__ lbar,
+                                     float* __restrict__ bbar) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;  // p * H + h
+  if (i >= P * H) return;
+  const int p = i / H;
+  const double lr = lam[p], li = lam[P + p], dt = exp((double)log_dt[p]);
+  const double mag = exp(lr * dt);
+  const double er = mag * cos(li * dt), ei = mag * sin(li * dt);  // lambda_bar
+  // (lambda_bar - 1) / lambda
+  const double nr = er - 1.0, ni = ei, den = lr * lr + li * li;
+  const double qr = (nr * lr + ni * li) / den, qi = (ni * lr - nr * li) / den;
+  const double br = b[i], bi = b[(size_t)P * H + i];
+  bbar[i] = (float)(qr * br - qi * bi);
+  bbar[(size_t)P * H + i] = (float)(qr * bi + qi * br);
+  if (i % H == 0) {
+    lbar[p] = (float)er;
+    lbar[P + p] = (float)ei;
+  }
+}
+
+hipError_t launch_s5_discretize(int P, int H, const float* lam, const float* log_dt, const float* b, float* lbar,
+                                float* bbar, hipStream_t s) {
+  const int n = P * H;
+  s5_discretize_kernel<<<dim3((unsigned)((n + 255) / 256)), 256, 0, s>>>(P, H, lam, log_dt, b, lbar, bbar);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- front ----
+
+constexpr int S5_RT = 32;   // rows per front workgroup
+constexpr int S5_NT = 256;  // threads of the front, head and output kernels
+constexpr int S5_NW = S5_NT / 64;
+
+struct S5Lds {
+  int ldx, ldu, ldf, ldxf;
+  size_t off_u, off_xf, total;  // region 0 (obs tile, then u as float) at 0
+};
+
+__host__ __device__ inline S5Lds s5_lds(int D, int H, int P) {
+  S5Lds L;
+  L.ldx = lds_ld<DT_BF16>(D);
+  L.ldu = lds_ld<DT_BF16>(H);
+  L.ldf = H + 1;       // odd strides: the float32 operand rows of a 16-row tile start on different banks
+  L.ldxf = 2 * P + 1;  // state tile: real parts, then imaginary parts
+  const size_t r0 = (size_t)S5_RT * (L.ldx * 2 > L.ldf * 4 ? L.ldx * 2 : L.ldf * 4);
+  L.off_u = (r0 + 15) / 16 * 16;
+  L.off_xf = (L.off_u + (size_t)S5_RT * L.ldu * 2 + 15) / 16 * 16;
+  L.total = L.off_xf + (size_t)S5_RT * L.ldxf * 4;
+  return L;
+}
+
+size_t s5_front_lds_bytes(int D, int H, int P) { return s5_lds(D, H, P).total; }
+
+struct S5FrontArgs {
+  const uint16_t* obs;   // [R, D] bf16
+  const int32_t* state;  // env state planes; an episode starts where plane step_plane is 0
+  int step_plane, E, A, R, D, H, P;
+  float* carry;  // [R, 2P]: real parts, then imaginary parts
+  int commit;    // write the new state back (0: value of the final observation only)
+  const uint16_t* w_enc;
+  const uint16_t* b_enc;
+  const float* lbar;  // [2, P]
+  const float* bbar;  // [2, P, H]
+  const float* c;     // [2, H, P]
+  const float* d;     // [H]
+  uint16_t* y;        // [R, H] bf16
+};
+
+__global__ __launch_bounds__(S5_NT) void s5_front_kernel(S5FrontArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  constexpr int MT = S5_RT / 16;
+  const S5Lds L = s5_lds(a.D, a.H, a.P);
+  uint16_t* xs = reinterpret_cast<uint16_t*>(smem);
+  float* uf = reinterpret_cast<float*>(smem);  // replaces xs once the encoder is done
+  uint16_t* us = reinterpret_cast<uint16_t*>(smem + L.off_u);
+  float* xf = reinterpret_cast<float*>(smem + L.off_xf);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r0 = blockIdx.x * S5_RT;
+  const int D = a.D, H = a.H, P = a.P;
+
+  // observation tile (zero past D and past the last row)
+  for (int i = tid; i < S5_RT * L.ldx; i += S5_NT) {
+    const int r = i / L.ldx, c = i - r * L.ldx;
+    xs[i] = (r0 + r < a.R && c < D) ? a.obs[(size_t)(r0 + r) * D + c] : (uint16_t)0;
+  }
+  __syncthreads();
+  // u = tanh(W_enc o + b_enc), rounded to bf16
+  mlp_input_layer<DT_BF16>(xs, L.ldx, nullptr, S5_RT, D, a.w_enc, a.b_enc, H, us, L.ldu, wave, S5_NW, lane);
+  __syncthreads();
+  for (int i = tid; i < S5_RT * H; i += S5_NT) {
+    const int r = i / H, h = i - r * H;
+    uf[r * L.ldf + h] = bf16_to_f32(us[r * L.ldu + h]);
+  }
+  __syncthreads();
+
+  // x_new = Lambda_bar x (zeroed at an episode start) + B_bar u, per 16 states
+  const float* a_u[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) a_u[m] = uf + (16 * m + (lane & 15)) * L.ldf;
+  for (int item = wave; item < P / 16; item += S5_NW) {
+    const int n0 = item * 16;
+    f32x4 bre[MT][1], bim[MT][1];
+    mma_tiles<DT_F32, 1, MT, WALIGN_16>(a_u, H, H, a.bbar, n0, P, lane, bre);
+    mma_tiles<DT_F32, 1, MT, WALIGN_16>(a_u, H, H, a.bbar + (size_t)P * H, n0, P, lane, bim);
+    const int p = n0 + (lane & 15);
+    const float lr = a.lbar[p], li = a.lbar[P + p];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int rl = 16 * m + 4 * (lane >> 4) + q, row = r0 + rl;
+        float xr = 0.f, xi = 0.f;
+        if (row < a.R) {
+          const int e = row / a.A;
+          if (a.state[(size_t)a.step_plane * a.E + e] != 0) {
+            xr = a.carry[(size_t)row * 2 * P + p];
+            xi = a.carry[(size_t)row * 2 * P + P + p];
+          }
+        }
+        const float nr = lr * xr - li * xi + bre[m][0][q];
+        const float ni = lr * xi + li * xr + bim[m][0][q];
+        xf[rl * L.ldxf + p] = nr;
+        xf[rl * L.ldxf + P + p] = ni;
+        if (a.commit && row < a.R) {
+          a.carry[(size_t)row * 2 * P + p] = nr;
+          a.carry[(size_t)row * 2 * P + P + p] = ni;
+        }
+      }
+  }
+  __syncthreads();
+
+  // y = Re(C x) + D u = C_re x_re - C_im x_im + D u, rounded to bf16
+  const float* a_re[MT];
+  const float* a_im[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    a_re[m] = xf + (16 * m + (lane & 15)) * L.ldxf;
+    a_im[m] = a_re[m] + P;
+  }
+  for (int item = wave; item < H / 16; item += S5_NW) {
+    const int n0 = item * 16;
+    f32x4 cre[MT][1], cim[MT][1];
+    mma_tiles<DT_F32, 1, MT, WALIGN_16>(a_re, P, P, a.c, n0, H, lane, cre);
+    mma_tiles<DT_F32, 1, MT, WALIGN_16>(a_im, P, P, a.c + (size_t)H * P, n0, H, lane, cim);
+    const int h = n0 + (lane & 15);
+    const float dh = a.d[h];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int rl = 16 * m + 4 * (lane >> 4) + q, row = r0 + rl;
+        const float yv = cre[m][0][q] - cim[m][0][q] + dh * uf[rl * L.ldf + h];
+        if (row < a.R) a.y[(size_t)row * H + h] = f32_to_bf16(yv);
+      }
+  }
+}
+
+// ---------------------------------------------------------------- heads ----
+//
+// out[z] = tanh(in[z] W[z]^T + b[z]) in bf16 for the two heads z (grouped in
+// one launch).  128 x 128 output tiles, 4 waves of 64 x 64, K in stages of 64
+// through double-buffered LDS (16-byte chunks XOR-swizzled by row so that
+// each 8-lane group of a fragment read covers all 32 banks).  The product is
+// taken transposed (W rows as the MFMA A operand), so each lane ends with
+// four consecutive outputs of one row: 8-byte stores.  Tiles are dealt so that
+// each XCD gets a contiguous range of one head's row blocks: that XCD's L2
+// then holds one head's weights and each input row block once.
+
+constexpr int HG_BM = 128, HG_BN = 128, HG_BK = 64;
+
+struct HeadGemmArgs {
+  const uint16_t* in[2];
+  int lda;
+  const uint16_t* w[2];  // [N, K]
+  const uint16_t* b[2];  // [N]
+  uint16_t* out[2];
+  int ldo, M, N, K;
+};
+
+__device__ __forceinline__ int hg_off(int row, int chunk) { return row * HG_BK + ((chunk ^ (row & 7)) << 3); }
+
+__global__ __launch_bounds__(S5_NT, 2) void s5_head_gemm_kernel(HeadGemmArgs g) {
+  __shared__ __align__(16) uint16_t sa[2][HG_BM * HG_BK];
+  __shared__ __align__(16) uint16_t sb[2][HG_BN * HG_BK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int mt = (g.M + HG_BM - 1) / HG_BM, nt = g.N / HG_BN;
+  const int total = 2 * mt * nt;
+  const int L = blockIdx.x;
+  const int T = (total % 8 == 0) ? (L % 8) * (total / 8) + L / 8 : L;  // XCD-contiguous tile ranges
+  const int z = T / (mt * nt), rem = T - z * mt * nt;
+  const int m0 = (rem / nt) * HG_BM, n0 = (rem % nt) * HG_BN;
+  const uint16_t* __restrict__ A = g.in[z];
+  const uint16_t* __restrict__ W = g.w[z];
+  const int wm = wave >> 1, wn = wave & 1;
+
+  u32x4 ra[4], rb[4];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int q = tid + S5_NT * i, row = q >> 3, c = q & 7;
+      const int ar = min(m0 + row, g.M - 1);
+      ra[i] = *reinterpret_cast<const u32x4*>(A + (size_t)ar * g.lda + k0 + c * 8);
+      rb[i] = *reinterpret_cast<const u32x4*>(W + (size_t)(n0 + row) * g.K + k0 + c * 8);
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int q = tid + S5_NT * i, row = q >> 3, c = q & 7;
+      *reinterpret_cast<u32x4*>(&sa[buf][hg_off(row, c)]) = ra[i];
+      *reinterpret_cast<u32x4*>(&sb[buf][hg_off(row, c)]) = rb[i];
+    }
+  };
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int nk = g.K / HG_BK;
+  for (int s = 0; s < nk; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < nk) gload((s + 1) * HG_BK);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int c = kk * 4 + (lane >> 4);
+      u32x4 fw[4], fx[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int nr = wn * 64 + j * 16 + (lane & 15);
+        fw[j] = *reinterpret_cast<const u32x4*>(&sb[buf][hg_off(nr, c)]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int mr = wm * 64 + i * 16 + (lane & 15);
+        fx[i] = *reinterpret_cast<const u32x4*>(&sa[buf][hg_off(mr, c)]);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[j][i] = mfma_step(fw[j], fx[i], acc[j][i]);
+    }
+    if (s + 1 < nk) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  const uint16_t* __restrict__ bias = g.b[z];
+  uint16_t* __restrict__ out = g.out[z];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int nb = n0 + wn * 64 + j * 16 + 4 * (lane >> 4);
+    const uint2 bw = *reinterpret_cast<const uint2*>(bias + nb);
+    const float b0 = bf16_to_f32((uint16_t)(bw.x & 0xffffu)), b1 = bf16_to_f32((uint16_t)(bw.x >> 16));
+    const float b2 = bf16_to_f32((uint16_t)(bw.y & 0xffffu)), b3 = bf16_to_f32((uint16_t)(bw.y >> 16));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + wm * 64 + i * 16 + (lane & 15);
+      if (m < g.M) {
+        uint2 v;
+        v.x = pack_bf16x2(fast_tanh(acc[j][i][0] + b0), fast_tanh(acc[j][i][1] + b1));
+        v.y = pack_bf16x2(fast_tanh(acc[j][i][2] + b2), fast_tanh(acc[j][i][3] + b3));
+        *reinterpret_cast<uint2*>(out + (size_t)m * g.ldo + nb) = v;
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------- output ----
+
+struct S5OutArgs {
+  const uint16_t* ha;  // [R, F] last actor hidden layer
+  const uint16_t* hc;  // [R, F] last critic hidden layer
+  const uint16_t* wa;  // [nA, F]
+  const uint16_t* ba;
+  const uint16_t* wc;  // [1, F]
+  const uint16_t* bc;
+  int R, F, NA, A;
+  uint64_t seed, t;
+  int64_t env_base;
+  int sample;  // 0: value only (into value)
+  int32_t* actions;
+  float* logits;  // [R, nA] or null
+  float* value;   // [R] or null
+  float* logp;    // [R] or null
+};
+
+// One wave per 16 rows: the two output layers as MFMA chains over F, then
+// lanes 0-15 sample their row.
+__global__ __launch_bounds__(S5_NT) void s5_out_kernel(S5OutArgs o) {
+  __shared__ float lg[S5_NW][16][17];
+  __shared__ float vs[S5_NW][16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r0 = (blockIdx.x * S5_NW + wave) * 16;
+  if (r0 >= o.R) return;  // (no block-wide barrier below)
+  const int rr = min(r0 + (lane & 15), o.R - 1);
+  const int al = weight_align(o.F);
+  {
+    const uint16_t* a_row[1] = {o.hc + (size_t)rr * o.F};
+    f32x4 acc[1][1];
+    if (al == WALIGN_16)
+      mma_tiles<DT_BF16, 1, 1, WALIGN_16>(a_row, o.F, o.F, o.wc, 0, 1, lane, acc);
+    else
+      mma_tiles<DT_BF16, 1, 1, WALIGN_4>(a_row, o.F, o.F, o.wc, 0, 1, lane, acc);
+    if ((lane & 15) == 0) {
+      const float b = bf16_to_f32(o.bc[0]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) vs[wave][4 * (lane >> 4) + q] = acc[0][0][q] + b;
+    }
+  }
+  if (o.sample) {
+    const uint16_t* a_row[1] = {o.ha + (size_t)rr * o.F};
+    f32x4 acc[1][1];
+    if (al == WALIGN_16)
+      mma_tiles<DT_BF16, 1, 1, WALIGN_16>(a_row, o.F, o.F, o.wa, 0, o.NA, lane, acc);
+    else
+      mma_tiles<DT_BF16, 1, 1, WALIGN_4>(a_row, o.F, o.F, o.wa, 0, o.NA, lane, acc);
+    const int a = lane & 15;
+    const float b = a < o.NA ? bf16_to_f32(o.ba[a]) : 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) lg[wave][4 * (lane >> 4) + q][a] = acc[0][0][q] + b;
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  const int row = r0 + lane;
+  if (lane < 16 && row < o.R) {
+    if (o.value) o.value[row] = vs[wave][lane];
+    if (o.sample) {
+      const float* l = lg[wave][lane];
+      const int e = row / o.A, ag = row - e * o.A;
+      int best = 0;
+      float bs = -INFINITY;
+      for (int k = 0; k < o.NA; ++k) {
+        const float sc = action_score(l[k], action_noise(o.seed, (uint64_t)(o.env_base + e), o.t, ag, k), true);
+        if (sc > bs) {
+          bs = sc;
+          best = k;
+        }
+      }
+      o.actions[row] = best;
+      if (o.logits)
+        for (int k = 0; k < o.NA; ++k) o.logits[(size_t)row * o.NA + k] = l[k];
+      if (o.logp) o.logp[row] = log_softmax_at(l, o.NA, best);
+    }
+  }
+}
+
+// ------------------------------------------------------------- the loop ----
+
+static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+S5Workspace s5_workspace(const LbfParams& p, const S5Net& net) {
+  S5Workspace w;
+  const size_t R = (size_t)p.E * p.A;
+  size_t off = 0;
+  w.off_obs = off;
+  off += align256(2 * R * p.D * 2);
+  w.off_y = off;
+  off += align256(R * net.H * 2);
+  w.off_h = off;
+  off += align256(4 * R * net.F * 2);
+  w.off_act = off;
+  off += align256(R * 4);
+  w.bytes = off;
+  return w;
+}
+
+hipError_t launch_s5_rollout(const LbfParams& p, const S5Net& net, int32_t* state, float* carry, uint64_t t0,
+                             int n_steps, const TrajArgs& out, void* workspace, hipStream_t s) {
+  const S5Workspace W = s5_workspace(p, net);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  const int E = p.E, A = p.A, D = p.D, R = E * A, H = net.H, F = net.F, NA = net.NA;
+  const size_t obs_stride = (size_t)R * D;
+  uint16_t* obs_ws = reinterpret_cast<uint16_t*>(ws + W.off_obs);
+  uint16_t* ybuf = reinterpret_cast<uint16_t*>(ws + W.off_y);
+  uint16_t* hbuf = reinterpret_cast<uint16_t*>(ws + W.off_h);
+  uint16_t* ha[2] = {hbuf, hbuf + (size_t)R * F};
+  uint16_t* hc[2] = {hbuf + 2 * (size_t)R * F, hbuf + 3 * (size_t)R * F};
+  int32_t* act_ws = reinterpret_cast<int32_t*>(ws + W.off_act);
+  auto obs_slot = [&](int k) -> uint16_t* {
+    if (k < n_steps && out.obs) return static_cast<uint16_t*>(out.obs) + (size_t)k * obs_stride;
+    if (k == n_steps && out.obs_last) return static_cast<uint16_t*>(out.obs_last);
+    return obs_ws + (size_t)(k & 1) * obs_stride;
+  };
+  const size_t front_lds = s5_front_lds_bytes(D, H, net.P);
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)s5_front_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)MAX_LDS_BYTES);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  S5FrontArgs fa{};
+  fa.state = state;
+  fa.step_plane = 2 * A + 2 * p.F + 1;
+  fa.E = E;
+  fa.A = A;
+  fa.R = R;
+  fa.D = D;
+  fa.H = H;
+  fa.P = net.P;
+  fa.carry = carry;
+  fa.w_enc = static_cast<const uint16_t*>(net.w_enc);
+  fa.b_enc = static_cast<const uint16_t*>(net.b_enc);
+  fa.lbar = net.lbar;
+  fa.bbar = net.bbar;
+  fa.c = net.c;
+  fa.d = net.d;
+  fa.y = ybuf;
+  const dim3 front_grid((unsigned)((R + S5_RT - 1) / S5_RT));
+  const int mtiles = (R + HG_BM - 1) / HG_BM;
+  const dim3 head_grid((unsigned)(2 * mtiles * (F / HG_BN)));
+  const dim3 out_grid((unsigned)((R + 16 * S5_NW - 1) / (16 * S5_NW)));
+
+  // the policy on the observations in obs_slot(k): y, the three head layers, then the output kernel
+  auto policy = [&](int k, int commit, const S5OutArgs& oa) -> hipError_t {
+    fa.obs = obs_slot(k);
+    fa.commit = commit;
+    s5_front_kernel<<<front_grid, S5_NT, front_lds, s>>>(fa);
+    HeadGemmArgs g{};
+    g.M = R;
+    g.N = F;
+    g.ldo = F;
+    for (int l = 0; l < 3; ++l) {
+      const int src = (l + 1) & 1, dst = l & 1;  // layer 0 -> buffer 0, 1 -> 1, 2 -> 0
+      g.K = l == 0 ? H : F;
+      g.lda = g.K;
+      g.in[0] = l == 0 ? ybuf : ha[src];
+      g.in[1] = l == 0 ? ybuf : hc[src];
+      g.w[0] = static_cast<const uint16_t*>(net.actor_w[l]);
+      g.w[1] = static_cast<const uint16_t*>(net.critic_w[l]);
+      g.b[0] = static_cast<const uint16_t*>(net.actor_b[l]);
+      g.b[1] = static_cast<const uint16_t*>(net.critic_b[l]);
+      g.out[0] = ha[dst];
+      g.out[1] = hc[dst];
+      s5_head_gemm_kernel<<<head_grid, S5_NT, 0, s>>>(g);
+    }
+    s5_out_kernel<<<out_grid, S5_NT, 0, s>>>(oa);
+    return hipGetLastError();
+  };
+  S5OutArgs oa{};
+  oa.ha = ha[0];
+  oa.hc = hc[0];
+  oa.wa = static_cast<const uint16_t*>(net.actor_w[3]);
+  oa.ba = static_cast<const uint16_t*>(net.actor_b[3]);
+  oa.wc = static_cast<const uint16_t*>(net.critic_w[3]);
+  oa.bc = static_cast<const uint16_t*>(net.critic_b[3]);
+  oa.R = R;
+  oa.F = F;
+  oa.NA = NA;
+  oa.A = A;
+  oa.seed = p.seed;
+  oa.env_base = p.env_base;
+
+  hipError_t err = launch_lbf_observe(p, state, obs_slot(0), s);
+  if (err != hipSuccess) return err;
+  for (int k = 0; k < n_steps; ++k) {
+    const size_t ko = (size_t)k * R;
+    oa.t = t0 + (uint64_t)k;
+    oa.sample = 1;
+    oa.actions = out.actions ? out.actions + ko : act_ws;
+    oa.logits = out.logits ? out.logits + ko * NA : nullptr;
+    oa.value = out.value ? out.value + ko : nullptr;
+    oa.logp = out.logp ? out.logp + ko : nullptr;
+    if ((err = policy(k, 1, oa)) != hipSuccess) return err;
+    err = launch_lbf_step(p, state, t0 + (uint64_t)k, 1, oa.actions, obs_slot(k + 1), DT_BF16,
+                          out.reward ? out.reward + (size_t)k * E : nullptr,
+                          out.done ? out.done + (size_t)k * E : nullptr, nullptr, s);
+    if (err != hipSuccess) return err;
+  }
+  if (out.value_last) {  // V(o_{t0+T}) from the state the next call would start from (not committed)
+    oa.sample = 0;
+    oa.actions = nullptr;
+    oa.logits = nullptr;
+    oa.logp = nullptr;
+    oa.value = out.value_last;
+    if ((err = policy(n_steps, 0, oa)) != hipSuccess) return err;
+  }
+  return hipSuccess;
+}
+
+}  // namespace rl

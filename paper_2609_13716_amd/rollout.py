@@ -13,6 +13,7 @@ import ctypes
 import os
 from dataclasses import dataclass, field
 
+import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -59,6 +60,15 @@ class _AcTraj(ctypes.Structure):
     _fields_ = [("value", ctypes.c_void_p), ("logp", ctypes.c_void_p), ("value_last", ctypes.c_void_p)]
 
 
+class _S5Policy(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("obs_dim", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("d_state", ctypes.c_int32), ("head_width", ctypes.c_int32), ("n_actions", ctypes.c_int32),
+                ("w_enc", ctypes.c_void_p), ("b_enc", ctypes.c_void_p), ("lambda_bar", ctypes.c_void_p),
+                ("b_bar", ctypes.c_void_p), ("c", ctypes.c_void_p), ("d", ctypes.c_void_p),
+                ("actor_w", ctypes.c_void_p * 4), ("actor_b", ctypes.c_void_p * 4),
+                ("critic_w", ctypes.c_void_p * 4), ("critic_b", ctypes.c_void_p * 4)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_13716_amd.build`")
@@ -88,6 +98,13 @@ def _load():
     lib.rollout_sample.argtypes = [cfgp, ctypes.c_uint64, P, P, P, P]
     lib.rollout_sample.restype = st
     lib.rl_gumbel_noise.argtypes, lib.rl_gumbel_noise.restype = [P, ctypes.c_int64, P, P], st
+    s5p = ctypes.POINTER(_S5Policy)
+    lib.rl_s5_discretize.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P, P, P]
+    lib.rl_s5_discretize.restype = st
+    lib.rl_s5_workspace_bytes.argtypes, lib.rl_s5_workspace_bytes.restype = [cfgp, s5p], ctypes.c_size_t
+    lib.rollout_run_s5.argtypes = [cfgp, s5p, P, P, ctypes.c_uint64, ctypes.c_int32, ctypes.POINTER(_Traj),
+                                   ctypes.POINTER(_AcTraj), P, ctypes.c_size_t, P]
+    lib.rollout_run_s5.restype = st
     return lib
 
 
@@ -96,7 +113,7 @@ lib = _load()
 # Every symbol the C header declares (checked by the test suite).
 EXPORTED = ("rl_state_bytes", "rl_obs_dim", "rl_num_actions", "rollout_last_error", "rollout_init",
             "rollout_step", "policy_forward", "rollout_run", "rollout_sample", "rl_gumbel_noise", "rollout_run_pop",
-            "rollout_run_ac", "rl_gae")
+            "rollout_run_ac", "rl_gae", "rl_s5_discretize", "rl_s5_workspace_bytes", "rollout_run_s5")
 
 
 def _check(status):
@@ -337,6 +354,92 @@ def rollout_run_ac(cfg, policy, state, t0, n_steps, value=None, logp=None, value
     pc = policy.c()
     _check(lib.rollout_run_ac(ctypes.byref(cfg.c()), ctypes.byref(pc), _ptr(state), t0, T, ctypes.byref(tr),
                               ctypes.byref(ac), _stream(stream)))
+
+
+class S5Policy:
+    """Device parameters of the recurrent S5 actor-critic (bfloat16 dense layers, float32 S5).
+
+    ``params``: continuous-time parameters as numpy arrays (keys w_enc, b_enc,
+    lam_re, lam_im, log_dt, b_re, b_im, c_re, c_im, d, actor_w, actor_b,
+    critic_w, critic_b); lambda_bar and b_bar are made on the device by
+    rl_s5_discretize."""
+
+    def __init__(self, params, device="cuda", stream=None):
+        bf = lambda a: torch.as_tensor(np.asarray(a, np.float32)).to(device=device, dtype=torch.bfloat16).contiguous()
+        f32 = lambda a: torch.as_tensor(np.ascontiguousarray(a, np.float32)).to(device).contiguous()
+        self.w_enc, self.b_enc = bf(params["w_enc"]), bf(params["b_enc"])
+        self.D, self.H = self.w_enc.shape[1], self.w_enc.shape[0]
+        self.P = len(params["lam_re"])
+        self.actor_w = [bf(w) for w in params["actor_w"]]
+        self.actor_b = [bf(b) for b in params["actor_b"]]
+        self.critic_w = [bf(w) for w in params["critic_w"]]
+        self.critic_b = [bf(b) for b in params["critic_b"]]
+        self.F, self.nA = self.actor_w[0].shape[0], self.actor_w[3].shape[0]
+        self.lam = f32(np.stack([params["lam_re"], params["lam_im"]]))
+        self.log_dt = f32(params["log_dt"])
+        self.b = f32(np.stack([params["b_re"], params["b_im"]]))
+        self.c_mat = f32(np.stack([params["c_re"], params["c_im"]]))
+        self.d = f32(params["d"])
+        self.lambda_bar = torch.empty(2, self.P, device=device)
+        self.b_bar = torch.empty(2, self.P, self.H, device=device)
+        s5_discretize(self.lam, self.log_dt, self.b, self.lambda_bar, self.b_bar, stream)
+
+    def c(self):
+        p = _S5Policy(dtype=RL_BF16, obs_dim=self.D, d_model=self.H, d_state=self.P, head_width=self.F,
+                      n_actions=self.nA, w_enc=self.w_enc.data_ptr(), b_enc=self.b_enc.data_ptr(),
+                      lambda_bar=self.lambda_bar.data_ptr(), b_bar=self.b_bar.data_ptr(), c=self.c_mat.data_ptr(),
+                      d=self.d.data_ptr())
+        for l in range(4):
+            p.actor_w[l], p.actor_b[l] = self.actor_w[l].data_ptr(), self.actor_b[l].data_ptr()
+            p.critic_w[l], p.critic_b[l] = self.critic_w[l].data_ptr(), self.critic_b[l].data_ptr()
+        return p
+
+
+def s5_discretize(lam, log_dt, b, lambda_bar, b_bar, stream=None):
+    """Zero-order hold on the device: lam [2, P], log_dt [P], b [2, P, H] -> lambda_bar [2, P], b_bar [2, P, H]."""
+    P, H = b.shape[1], b.shape[2]
+    _need(lam, "lam", torch.float32, (2, P))
+    _need(log_dt, "log_dt", torch.float32, (P,))
+    _need(b, "b", torch.float32, (2, P, H))
+    _need(lambda_bar, "lambda_bar", torch.float32, (2, P))
+    _need(b_bar, "b_bar", torch.float32, (2, P, H))
+    _check(lib.rl_s5_discretize(P, H, _ptr(lam), _ptr(log_dt), _ptr(b), _ptr(lambda_bar), _ptr(b_bar),
+                                _stream(stream)))
+
+
+def s5_workspace_bytes(cfg, policy):
+    return lib.rl_s5_workspace_bytes(ctypes.byref(cfg.c()), ctypes.byref(policy.c()))
+
+
+def rollout_run_s5(cfg, policy, state, carry, t0, n_steps, value=None, logp=None, value_last=None, obs=None,
+                   actions=None, logits=None, reward=None, done=None, obs_last=None, workspace=None, stream=None):
+    """rollout_run_ac with the recurrent S5 actor-critic; ``carry`` [E * A, 2, P] float32 is the S5 state.
+    ``workspace``: a uint8 device tensor of at least s5_workspace_bytes(cfg, policy) bytes (allocated when None)."""
+    E, A = cfg.n_envs, cfg.n_agents
+    D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
+    T = n_steps
+    _need(state, "state", torch.int32)
+    _need(carry, "carry", torch.float32, (E * A, 2, policy.P))
+    _need(obs, "obs", torch.bfloat16, (T, E, A, D))
+    _need(actions, "actions", torch.int32, (T, E, A))
+    _need(logits, "logits", torch.float32, (T, E, A, nA))
+    _need(reward, "reward", torch.float32, (T, E))
+    _need(done, "done", torch.uint8, (T, E))
+    _need(obs_last, "obs_last", torch.bfloat16, (E, A, D))
+    _need(value, "value", torch.float32, (T, E, A))
+    _need(logp, "logp", torch.float32, (T, E, A))
+    _need(value_last, "value_last", torch.float32, (E, A))
+    pc = policy.c()
+    nbytes = lib.rl_s5_workspace_bytes(ctypes.byref(cfg.c()), ctypes.byref(pc))
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=carry.device)
+    tr = _Traj(obs=_ptr(obs), actions=_ptr(actions), logits=_ptr(logits), reward=_ptr(reward), done=_ptr(done),
+               obs_last=_ptr(obs_last))
+    ac = _AcTraj(value=_ptr(value), logp=_ptr(logp), value_last=_ptr(value_last))
+    _check(lib.rollout_run_s5(ctypes.byref(cfg.c()), ctypes.byref(pc), _ptr(state), _ptr(carry), t0, T,
+                              ctypes.byref(tr), ctypes.byref(ac), _ptr(workspace), workspace.numel(),
+                              _stream(stream)))
+    return workspace
 
 
 def gae(reward, done, value, value_last, gamma, lam, adv=None, ret=None, stream=None):
