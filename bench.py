@@ -247,6 +247,44 @@ def measure_actor_critic(R, workloads, name, dt, steps, warmup):
                     "roofline": roofline("hbm", gae_bytes / (gae_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s")}}
 
 
+def measure_s5(R, workloads, name, dt, steps, warmup):
+    """rollout_run_s5 (recurrent S5 actor-critic) at full size: time, throughput, dense-layer MFMA rate."""
+    import torch
+    w = workloads.WORKLOADS[name]
+    cfg = env_config(R, workloads, name)
+    E, T, A = cfg.n_envs, w["n_steps"], cfg.n_agents
+    D, nA = R.rl_obs_dim(cfg), R.rl_num_actions(cfg)
+    H, P, F = w["s5"]["d_model"], w["s5"]["d_state"], w["s5"]["head_width"]
+    pol = R.S5Policy(workloads.s5_params(D, H, P, F, nA, seed=1000))
+    state = R.new_state(cfg)
+    R.rollout_init(cfg, state)
+    f = dict(device="cuda")
+    carry = torch.zeros(E * A, 2, P, **f)
+    obs = torch.empty(T, E, A, D, dtype=torch.bfloat16, **f)
+    acts = torch.empty(T, E, A, dtype=torch.int32, **f)
+    rew, done = torch.empty(T, E, **f), torch.empty(T, E, dtype=torch.uint8, **f)
+    value, logp, vlast = torch.empty(T, E, A, **f), torch.empty(T, E, A, **f), torch.empty(E, A, **f)
+    wsp = torch.empty(R.s5_workspace_bytes(cfg, pol), dtype=torch.uint8, **f)
+    t_next = [0]
+
+    def run():
+        R.rollout_run_s5(cfg, pol, state, carry, t_next[0], T, value=value, logp=logp, value_last=vlast, obs=obs,
+                         actions=acts, reward=rew, done=done, workspace=wsp)
+        t_next[0] += T
+
+    kern_ms, wall_ms = timed(run, steps, warmup)
+    head_macs = 2 * (H * F + 2 * F * F) + F * (nA + 1)
+    macs_per_row = D * H + 4 * P * H + head_macs  # encoder, B_bar u and Re(C x) as real products, heads
+    rows = E * A * (T + 1)  # T steps plus the value of the final observation
+    return {"workload": name, "dtype": dt, "n_envs": E, "steps_per_rollout": T,
+            "policy": f"S5 D{D}-H{H}-P{P}, heads 3x{F}", "value": round(E * T * A / (wall_ms * 1e-3), 1),
+            "unit": "agent-env steps/s", "ms_per_step": round(wall_ms, 4), "kernel_ms": round(kern_ms, 4),
+            "roofline_mfma": roofline("mfma", 2 * macs_per_row * rows / (kern_ms * 1e-3) / 1e12,
+                                      MFMA_PEAK_TFLOPS[dt], "TFLOP/s"),
+            "note": "MFMA rate over the whole rollout (every kernel of every step); per-kernel times in the "
+                    "rocprofv3 summary of this workload"}
+
+
 def cpu_baseline(n_envs, T):
     """The oracle, single-threaded, on the first n_envs envs of the workload for T steps."""
     import numpy as np
@@ -357,7 +395,7 @@ def main():
 
     if args.workload_only:
         wl = workloads.WORKLOADS[args.workload_only]
-        measure = (measure_population if "population" in wl else
+        measure = (measure_population if "population" in wl else measure_s5 if "s5" in wl else
                    measure_actor_critic if wl.get("value_head") else measure_workload)
         print(json.dumps(measure(R, workloads, args.workload_only, "bf16", args.steps, args.warmup)),
               flush=True)
@@ -429,6 +467,7 @@ def main():
                                                                  min(args.steps, 5), 1)
         line["workloads"]["lbf8_4096_pop"] = measure_population(R, workloads, "lbf8_4096_pop", "bf16",
                                                                 min(args.steps, 5), 1)
+        line["workloads"]["lbf8_4096_s5"] = measure_s5(R, workloads, "lbf8_4096_s5", "bf16", min(args.steps, 3), 1)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.cpu_envs, T)
     print(json.dumps(line), flush=True)

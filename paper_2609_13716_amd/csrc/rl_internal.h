@@ -184,7 +184,7 @@ struct S5Net {
   const void* critic_b[4];
 };
 struct S5Workspace {
-  size_t off_obs, off_y, off_h, off_act, bytes;
+  size_t off_obs, off_y, off_h, off_act, off_wcat, bytes;
 };
 S5Workspace s5_workspace(const LbfParams& p, const S5Net& net);
 size_t s5_front_lds_bytes(int D, int H, int P);

@@ -146,21 +146,23 @@ __device__ __forceinline__ f32x4 mfma_step(u32x4 a, u32x4 b, f32x4 acc) {
 // The loop is kept rolled (these kernels run many different phases per step
 // and must stay within the instruction cache).  The one partial step at the
 // end is guarded.  Each tile's sum runs over k in the same order whatever G
-// and MT are, so results do not depend on them.
-template <int DT, int G, int MT, int AL>
+// and MT are, so results do not depend on them.  PFX > 0 sets the ring depth
+// (deeper rings hide more of the weight-load latency in short, long-K chains);
+// tile g covers output columns n0 + gstride * g (gstride 16: adjacent tiles).
+template <int DT, int G, int MT, int AL, int PFX = 0>
 __device__ __forceinline__ void mma_tiles(const typename DType<DT>::T* const (&a_row)[MT], int Kpad, int K,
                                           const typename DType<DT>::T* __restrict__ W, int n0, int N, int lane,
-                                          f32x4 (&acc)[MT][G]) {
+                                          f32x4 (&acc)[MT][G], int gstride = 16) {
   using T = typename DType<DT>::T;
   using BT = typename std::conditional<DT == DT_F32, float, u32x4>::type;
   constexpr int KS = DType<DT>::KS;
   constexpr int KL = DT == DT_F32 ? 1 : 8;  // k values per lane per step
-  constexpr int PF = G >= 4 ? 2 : 4;        // k-steps of weights in flight
+  constexpr int PF = PFX > 0 ? PFX : G >= 4 ? 2 : 4;  // k-steps of weights in flight
   const T* wrow[G];
   bool nok[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    const int n = n0 + 16 * g + (lane & 15);
+    const int n = n0 + gstride * g + (lane & 15);
     nok[g] = n < N;
     wrow[g] = W + (size_t)(nok[g] ? n : 0) * K + (lane >> 4) * KL;
   }

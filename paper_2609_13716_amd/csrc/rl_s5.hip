@@ -61,13 +61,15 @@ hipError_t launch_s5_discretize(int P, int H, const float* lam, const float* log
 
 // ---------------------------------------------------------------- front ----
 
-constexpr int S5_RT = 32;   // rows per front workgroup
-constexpr int S5_NT = 256;  // threads of the front, head and output kernels
+constexpr int S5_RT = 32;    // rows per front workgroup
+constexpr int S5F_NT = 512;  // front: 8 waves, one 16-column item each per phase (latency hiding)
+constexpr int S5F_NW = S5F_NT / 64;
+constexpr int S5_NT = 256;  // threads of the head and output kernels
 constexpr int S5_NW = S5_NT / 64;
 
 struct S5Lds {
   int ldx, ldu, ldf, ldxf;
-  size_t off_u, off_xf, total;  // region 0 (obs tile, then u as float) at 0
+  size_t off_u, off_xf, off_keep, total;  // region 0 (obs tile, then u as float) at 0
 };
 
 __host__ __device__ inline S5Lds s5_lds(int D, int H, int P) {
@@ -79,7 +81,8 @@ __host__ __device__ inline S5Lds s5_lds(int D, int H, int P) {
   const size_t r0 = (size_t)S5_RT * (L.ldx * 2 > L.ldf * 4 ? L.ldx * 2 : L.ldf * 4);
   L.off_u = (r0 + 15) / 16 * 16;
   L.off_xf = (L.off_u + (size_t)S5_RT * L.ldu * 2 + 15) / 16 * 16;
-  L.total = L.off_xf + (size_t)S5_RT * L.ldxf * 4;
+  L.off_keep = L.off_xf + (size_t)S5_RT * L.ldxf * 4;
+  L.total = L.off_keep + S5_RT * 4;
   return L;
 }
 
@@ -95,12 +98,20 @@ struct S5FrontArgs {
   const uint16_t* b_enc;
   const float* lbar;  // [2, P]
   const float* bbar;  // [2, P, H]
-  const float* c;     // [2, H, P]
+  const float* wcat;  // [H, 2P]: C_re | -C_im, so that Re(C x) is one product with [x_re | x_im]
   const float* d;     // [H]
   uint16_t* y;        // [R, H] bf16
 };
 
-__global__ __launch_bounds__(S5_NT) void s5_front_kernel(S5FrontArgs a) {
+// [C_re | -C_im] as one [H, 2P] matrix.
+__global__ void s5_cat_kernel(int H, int P, const float* __restrict__ c, float* __restrict__ wcat) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;  // h * 2P + k
+  if (i >= H * 2 * P) return;
+  const int h = i / (2 * P), k = i - h * 2 * P;
+  wcat[i] = k < P ? c[(size_t)h * P + k] : -c[(size_t)H * P + (size_t)h * P + (k - P)];
+}
+
+__global__ __launch_bounds__(S5F_NT) void s5_front_kernel(S5FrontArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   constexpr int MT = S5_RT / 16;
   const S5Lds L = s5_lds(a.D, a.H, a.P);
@@ -108,20 +119,46 @@ __global__ __launch_bounds__(S5_NT) void s5_front_kernel(S5FrontArgs a) {
   float* uf = reinterpret_cast<float*>(smem);  // replaces xs once the encoder is done
   uint16_t* us = reinterpret_cast<uint16_t*>(smem + L.off_u);
   float* xf = reinterpret_cast<float*>(smem + L.off_xf);
+  int* keep_s = reinterpret_cast<int*>(smem + L.off_keep);  // 1: the row's episode continues (carry used)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r0 = blockIdx.x * S5_RT;
   const int D = a.D, H = a.H, P = a.P;
 
-  // observation tile (zero past D and past the last row)
-  for (int i = tid; i < S5_RT * L.ldx; i += S5_NT) {
-    const int r = i / L.ldx, c = i - r * L.ldx;
-    xs[i] = (r0 + r < a.R && c < D) ? a.obs[(size_t)(r0 + r) * D + c] : (uint16_t)0;
+  if (tid < S5_RT) {
+    const int row = r0 + tid;
+    keep_s[tid] = row < a.R && a.state[(size_t)a.step_plane * a.E + row / a.A] != 0;
+  }
+  // observation tile (zero past D and past the last row): 16-byte chunks
+  // when rows are whole chunks (all loads issued before the stores)
+  if (D % 8 == 0) {
+    const int cpr = L.ldx / 8;  // chunks per LDS row (the K padding included)
+    constexpr int CI = 4;
+    for (int i0 = tid; i0 < S5_RT * cpr; i0 += CI * S5F_NT) {
+      u32x4 v[CI];
+#pragma unroll
+      for (int j = 0; j < CI; ++j) {
+        const int i = i0 + j * S5F_NT, r = i / cpr, c = (i - r * cpr) * 8;
+        v[j] = (i < S5_RT * cpr && r0 + r < a.R && c < D)
+                   ? *reinterpret_cast<const u32x4*>(a.obs + (size_t)(r0 + r) * D + c)
+                   : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int j = 0; j < CI; ++j) {
+        const int i = i0 + j * S5F_NT, r = i / cpr, c = (i - r * cpr) * 8;
+        if (i < S5_RT * cpr) *reinterpret_cast<u32x4*>(xs + r * L.ldx + c) = v[j];
+      }
+    }
+  } else {
+    for (int i = tid; i < S5_RT * L.ldx; i += S5F_NT) {
+      const int r = i / L.ldx, c = i - r * L.ldx;
+      xs[i] = (r0 + r < a.R && c < D) ? a.obs[(size_t)(r0 + r) * D + c] : (uint16_t)0;
+    }
   }
   __syncthreads();
   // u = tanh(W_enc o + b_enc), rounded to bf16
-  mlp_input_layer<DT_BF16>(xs, L.ldx, nullptr, S5_RT, D, a.w_enc, a.b_enc, H, us, L.ldu, wave, S5_NW, lane);
+  mlp_input_layer<DT_BF16>(xs, L.ldx, nullptr, S5_RT, D, a.w_enc, a.b_enc, H, us, L.ldu, wave, S5F_NW, lane);
   __syncthreads();
-  for (int i = tid; i < S5_RT * H; i += S5_NT) {
+  for (int i = tid; i < S5_RT * H; i += S5F_NT) {
     const int r = i / H, h = i - r * H;
     uf[r * L.ldf + h] = bf16_to_f32(us[r * L.ldu + h]);
   }
@@ -131,28 +168,33 @@ __global__ __launch_bounds__(S5_NT) void s5_front_kernel(S5FrontArgs a) {
   const float* a_u[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) a_u[m] = uf + (16 * m + (lane & 15)) * L.ldf;
-  for (int item = wave; item < P / 16; item += S5_NW) {
+  for (int item = wave; item < P / 16; item += S5F_NW) {
     const int n0 = item * 16;
-    f32x4 bre[MT][1], bim[MT][1];
-    mma_tiles<DT_F32, 1, MT, WALIGN_16>(a_u, H, H, a.bbar, n0, P, lane, bre);
-    mma_tiles<DT_F32, 1, MT, WALIGN_16>(a_u, H, H, a.bbar + (size_t)P * H, n0, P, lane, bim);
+    // the real and imaginary rows of these 16 states as two tiles of one chain
+    // ([2P, H] rows n0.. and P + n0..), 16 k-steps of weights in flight
+    f32x4 bu[MT][2];
+    mma_tiles<DT_F32, 2, MT, WALIGN_16, 16>(a_u, H, H, a.bbar, n0, 2 * P, lane, bu, P);
     const int p = n0 + (lane & 15);
     const float lr = a.lbar[p], li = a.lbar[P + p];
+    // previous states of this lane's rows, loaded together (rows past the end read the last row)
+    float xo[MT][4][2];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const size_t row = (size_t)min(r0 + 16 * m + 4 * (lane >> 4) + q, a.R - 1);
+        xo[m][q][0] = a.carry[row * 2 * P + p];
+        xo[m][q][1] = a.carry[row * 2 * P + P + p];
+      }
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int rl = 16 * m + 4 * (lane >> 4) + q, row = r0 + rl;
-        float xr = 0.f, xi = 0.f;
-        if (row < a.R) {
-          const int e = row / a.A;
-          if (a.state[(size_t)a.step_plane * a.E + e] != 0) {
-            xr = a.carry[(size_t)row * 2 * P + p];
-            xi = a.carry[(size_t)row * 2 * P + P + p];
-          }
-        }
-        const float nr = lr * xr - li * xi + bre[m][0][q];
-        const float ni = lr * xi + li * xr + bim[m][0][q];
+        const bool keep = keep_s[rl] != 0;
+        const float xr = keep ? xo[m][q][0] : 0.f, xi = keep ? xo[m][q][1] : 0.f;
+        const float nr = lr * xr - li * xi + bu[m][0][q];
+        const float ni = lr * xi + li * xr + bu[m][1][q];
         xf[rl * L.ldxf + p] = nr;
         xf[rl * L.ldxf + P + p] = ni;
         if (a.commit && row < a.R) {
@@ -163,19 +205,14 @@ __global__ __launch_bounds__(S5_NT) void s5_front_kernel(S5FrontArgs a) {
   }
   __syncthreads();
 
-  // y = Re(C x) + D u = C_re x_re - C_im x_im + D u, rounded to bf16
-  const float* a_re[MT];
-  const float* a_im[MT];
+  // y = Re(C x) + D u = [C_re | -C_im] [x_re | x_im] + D u, rounded to bf16
+  const float* a_x[MT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) {
-    a_re[m] = xf + (16 * m + (lane & 15)) * L.ldxf;
-    a_im[m] = a_re[m] + P;
-  }
-  for (int item = wave; item < H / 16; item += S5_NW) {
+  for (int m = 0; m < MT; ++m) a_x[m] = xf + (16 * m + (lane & 15)) * L.ldxf;
+  for (int item = wave; item < H / 16; item += S5F_NW) {
     const int n0 = item * 16;
-    f32x4 cre[MT][1], cim[MT][1];
-    mma_tiles<DT_F32, 1, MT, WALIGN_16>(a_re, P, P, a.c, n0, H, lane, cre);
-    mma_tiles<DT_F32, 1, MT, WALIGN_16>(a_im, P, P, a.c + (size_t)H * P, n0, H, lane, cim);
+    f32x4 cy[MT][1];
+    mma_tiles<DT_F32, 1, MT, WALIGN_16, 16>(a_x, 2 * P, 2 * P, a.wcat, n0, H, lane, cy);
     const int h = n0 + (lane & 15);
     const float dh = a.d[h];
 #pragma unroll
@@ -183,7 +220,7 @@ __global__ __launch_bounds__(S5_NT) void s5_front_kernel(S5FrontArgs a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int rl = 16 * m + 4 * (lane >> 4) + q, row = r0 + rl;
-        const float yv = cre[m][0][q] - cim[m][0][q] + dh * uf[rl * L.ldf + h];
+        const float yv = cy[m][0][q] + dh * uf[rl * L.ldf + h];
         if (row < a.R) a.y[(size_t)row * H + h] = f32_to_bf16(yv);
       }
   }
@@ -321,62 +358,90 @@ struct S5OutArgs {
   float* logp;    // [R] or null
 };
 
-// One wave per 16 rows: the two output layers as MFMA chains over F, then
-// lanes 0-15 sample their row.
+// 16 rows per workgroup: wave w takes the K slice [w F / 4, (w + 1) F / 4)
+// of both output layers (MFMA chains over 16-byte fragments), the four
+// partial sums meet in LDS and lanes 0-15 of wave 0 finish and sample a row.
 __global__ __launch_bounds__(S5_NT) void s5_out_kernel(S5OutArgs o) {
-  __shared__ float lg[S5_NW][16][17];
-  __shared__ float vs[S5_NW][16];
+  __shared__ float lp[S5_NW][16][17];
+  __shared__ float vp[S5_NW][16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int r0 = (blockIdx.x * S5_NW + wave) * 16;
-  if (r0 >= o.R) return;  // (no block-wide barrier below)
+  const int r0 = blockIdx.x * 16;
   const int rr = min(r0 + (lane & 15), o.R - 1);
-  const int al = weight_align(o.F);
-  {
-    const uint16_t* a_row[1] = {o.hc + (size_t)rr * o.F};
-    f32x4 acc[1][1];
-    if (al == WALIGN_16)
-      mma_tiles<DT_BF16, 1, 1, WALIGN_16>(a_row, o.F, o.F, o.wc, 0, 1, lane, acc);
-    else
-      mma_tiles<DT_BF16, 1, 1, WALIGN_4>(a_row, o.F, o.F, o.wc, 0, 1, lane, acc);
-    if ((lane & 15) == 0) {
-      const float b = bf16_to_f32(o.bc[0]);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) vs[wave][4 * (lane >> 4) + q] = acc[0][0][q] + b;
+  const int n = lane & 15;
+  const int kq = o.F / S5_NW, kb = wave * kq;
+  const uint16_t* xa = o.ha + (size_t)rr * o.F + kb + 8 * (lane >> 4);
+  const uint16_t* xc = o.hc + (size_t)rr * o.F + kb + 8 * (lane >> 4);
+  const uint16_t* wa = o.wa + (size_t)(n < o.NA ? n : 0) * o.F + kb + 8 * (lane >> 4);
+  const uint16_t* wc = o.wc + kb + 8 * (lane >> 4);
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  f32x4 acc_a = {0.f, 0.f, 0.f, 0.f}, acc_c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+  for (int k = 0; k < kq; k += 32) {
+    const u32x4 fc = *reinterpret_cast<const u32x4*>(xc + k);
+    const u32x4 gc = *reinterpret_cast<const u32x4*>(wc + k);
+    acc_c = mfma_step(fc, n == 0 ? gc : zero, acc_c);
+    if (o.sample) {
+      const u32x4 fa = *reinterpret_cast<const u32x4*>(xa + k);
+      const u32x4 ga = *reinterpret_cast<const u32x4*>(wa + k);
+      acc_a = mfma_step(fa, n < o.NA ? ga : zero, acc_a);
     }
   }
-  if (o.sample) {
-    const uint16_t* a_row[1] = {o.ha + (size_t)rr * o.F};
-    f32x4 acc[1][1];
-    if (al == WALIGN_16)
-      mma_tiles<DT_BF16, 1, 1, WALIGN_16>(a_row, o.F, o.F, o.wa, 0, o.NA, lane, acc);
-    else
-      mma_tiles<DT_BF16, 1, 1, WALIGN_4>(a_row, o.F, o.F, o.wa, 0, o.NA, lane, acc);
-    const int a = lane & 15;
-    const float b = a < o.NA ? bf16_to_f32(o.ba[a]) : 0.f;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) lg[wave][4 * (lane >> 4) + q][a] = acc[0][0][q] + b;
+  for (int q = 0; q < 4; ++q) {
+    lp[wave][4 * (lane >> 4) + q][n] = acc_a[q];
+    if (n == 0) vp[wave][4 * (lane >> 4) + q] = acc_c[q];
   }
-  __builtin_amdgcn_s_waitcnt(0);
-  __builtin_amdgcn_wave_barrier();
-  const int row = r0 + lane;
-  if (lane < 16 && row < o.R) {
-    if (o.value) o.value[row] = vs[wave][lane];
+  __syncthreads();
+  const int row = r0 + tid;
+  if (tid < 16 && row < o.R) {
+    float v = bf16_to_f32(o.bc[0]);
+#pragma unroll
+    for (int w = 0; w < S5_NW; ++w) v += vp[w][tid];
+    if (o.value) o.value[row] = v;
     if (o.sample) {
-      const float* l = lg[wave][lane];
+      float l[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        float x = k < o.NA ? bf16_to_f32(o.ba[k]) : 0.f;
+#pragma unroll
+        for (int w = 0; w < S5_NW; ++w) x += lp[w][tid][k];
+        l[k] = x;
+      }
       const int e = row / o.A, ag = row - e * o.A;
+      // noise of action k: draw k % 8 of Philox block (env, t, agent * 256 + k / 8, action tag), top 24 bits
+      const Block4 b0 = draw_block(o.seed, (uint64_t)(o.env_base + e), o.t, (uint64_t)ag * 256u, TAG_ACTION);
+      Block4 b1 = b0;
+      if (o.NA > 8) b1 = draw_block(o.seed, (uint64_t)(o.env_base + e), o.t, (uint64_t)ag * 256u + 1u, TAG_ACTION);
       int best = 0;
-      float bs = -INFINITY;
-      for (int k = 0; k < o.NA; ++k) {
-        const float sc = action_score(l[k], action_noise(o.seed, (uint64_t)(o.env_base + e), o.t, ag, k), true);
-        if (sc > bs) {
-          bs = sc;
-          best = k;
+      float bs = -INFINITY, best_l = l[0];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        if (k < o.NA) {
+          const float nz = gumbel24(block_u32(k < 8 ? b0 : b1, k & 7) >> 8);
+          const float sc = action_score(l[k], nz, true);
+          if (sc > bs) {
+            bs = sc;
+            best = k;
+            best_l = l[k];
+          }
         }
       }
       o.actions[row] = best;
       if (o.logits)
-        for (int k = 0; k < o.NA; ++k) o.logits[(size_t)row * o.NA + k] = l[k];
-      if (o.logp) o.logp[row] = log_softmax_at(l, o.NA, best);
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+          if (k < o.NA) o.logits[(size_t)row * o.NA + k] = l[k];
+      if (o.logp) {  // float32 log-softmax, as log_softmax_at
+        float m = l[0];
+#pragma unroll
+        for (int k = 1; k < 16; ++k)
+          if (k < o.NA) m = fmaxf(m, l[k]);
+        float sum = 0.f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+          if (k < o.NA) sum += expf(l[k] - m);
+        o.logp[row] = best_l - (m + logf(sum));
+      }
     }
   }
 }
@@ -397,6 +462,8 @@ S5Workspace s5_workspace(const LbfParams& p, const S5Net& net) {
   off += align256(4 * R * net.F * 2);
   w.off_act = off;
   off += align256(R * 4);
+  w.off_wcat = off;
+  off += align256((size_t)net.H * 2 * net.P * 4);
   w.bytes = off;
   return w;
 }
@@ -440,19 +507,19 @@ hipError_t launch_s5_rollout(const LbfParams& p, const S5Net& net, int32_t* stat
   fa.b_enc = static_cast<const uint16_t*>(net.b_enc);
   fa.lbar = net.lbar;
   fa.bbar = net.bbar;
-  fa.c = net.c;
+  fa.wcat = reinterpret_cast<const float*>(ws + W.off_wcat);
   fa.d = net.d;
   fa.y = ybuf;
   const dim3 front_grid((unsigned)((R + S5_RT - 1) / S5_RT));
   const int mtiles = (R + HG_BM - 1) / HG_BM;
   const dim3 head_grid((unsigned)(2 * mtiles * (F / HG_BN)));
-  const dim3 out_grid((unsigned)((R + 16 * S5_NW - 1) / (16 * S5_NW)));
+  const dim3 out_grid((unsigned)((R + 15) / 16));
 
   // the policy on the observations in obs_slot(k): y, the three head layers, then the output kernel
   auto policy = [&](int k, int commit, const S5OutArgs& oa) -> hipError_t {
     fa.obs = obs_slot(k);
     fa.commit = commit;
-    s5_front_kernel<<<front_grid, S5_NT, front_lds, s>>>(fa);
+    s5_front_kernel<<<front_grid, S5F_NT, front_lds, s>>>(fa);
     HeadGemmArgs g{};
     g.M = R;
     g.N = F;
@@ -488,6 +555,8 @@ hipError_t launch_s5_rollout(const LbfParams& p, const S5Net& net, int32_t* stat
   oa.seed = p.seed;
   oa.env_base = p.env_base;
 
+  s5_cat_kernel<<<dim3((unsigned)((H * 2 * net.P + 255) / 256)), 256, 0, s>>>(
+      H, net.P, net.c, reinterpret_cast<float*>(ws + W.off_wcat));
   hipError_t err = launch_lbf_observe(p, state, obs_slot(0), s);
   if (err != hipSuccess) return err;
   for (int k = 0; k < n_steps; ++k) {

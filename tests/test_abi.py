@@ -206,3 +206,45 @@ def test_constant_levels_config_is_accepted():
     cfg = _cfg(grid_h=7, grid_w=7, const_levels=True, max_agent_level=1, max_food_level=2)
     assert _status(cfg) == 147
     assert cfg.c().lbf_const_levels == 1 and _cfg().c().lbf_const_levels == 0
+
+
+def _s5_struct(**kw):
+    v = dict(dtype=R.RL_BF16, obs_dim=192, d_model=128, d_state=128, head_width=1024, n_actions=6)
+    v.update(kw)
+    p = R._S5Policy(**{k: v[k] for k in ("dtype", "obs_dim", "d_model", "d_state", "head_width", "n_actions")})
+    for name in ("w_enc", "b_enc", "lambda_bar", "b_bar", "c", "d"):
+        setattr(p, name, v.get(name, 0x1000))
+    for l in range(4):
+        p.actor_w[l] = p.actor_b[l] = p.critic_w[l] = p.critic_b[l] = v.get("heads", 0x2000)
+    return p
+
+
+def _s5_status(cfg, pol, carry=0x3000, ws_bytes=1 << 30, workspace=0x4000, n_steps=4):
+    tr, ac = R._Traj(), R._AcTraj()
+    return R.lib.rollout_run_s5(ctypes.byref(cfg.c()), ctypes.byref(pol), ctypes.c_void_p(0x1000),
+                                ctypes.c_void_p(carry) if carry else None, 0, n_steps, ctypes.byref(tr),
+                                ctypes.byref(ac), ctypes.c_void_p(workspace) if workspace else None, ws_bytes, None)
+
+
+def test_s5_checks_before_launch():
+    cfg = _cfg()
+    good = _s5_struct()
+    need = R.lib.rl_s5_workspace_bytes(ctypes.byref(cfg.c()), ctypes.byref(good))
+    E, A = 16, 2
+    assert need >= 4 * E * A * 1024 * 2 + E * A * 128 * 2
+    for kw, code in ((dict(dtype=R.RL_F32), R.RL_EUNSUPPORTED), (dict(d_model=96), R.RL_EUNSUPPORTED),
+                     (dict(d_state=24), R.RL_EUNSUPPORTED), (dict(head_width=1000), R.RL_EUNSUPPORTED),
+                     (dict(obs_dim=191), R.RL_ESHAPE), (dict(n_actions=5), R.RL_ESHAPE),
+                     (dict(w_enc=0), R.RL_EINVAL), (dict(c=0x1004), R.RL_EINVAL), (dict(heads=0x2008), R.RL_EINVAL)):
+        p = _s5_struct(**kw)
+        assert _s5_status(cfg, p) == code, kw
+        assert R.lib.rl_s5_workspace_bytes(ctypes.byref(cfg.c()), ctypes.byref(p)) == 0, kw
+    assert _s5_status(cfg, good, carry=0) == R.RL_EINVAL
+    assert _s5_status(cfg, good, ws_bytes=need - 1) == R.RL_EINVAL
+    assert _s5_status(cfg, good, workspace=0x4008) == R.RL_EINVAL
+    assert _s5_status(cfg, good, n_steps=0) == R.RL_EINVAL
+    assert _s5_status(R.overcooked_config(16), good) == R.RL_EUNSUPPORTED
+    L = R.lib
+    assert L.rl_s5_discretize(0, 4, None, None, None, None, None, None) == R.RL_EINVAL
+    assert L.rl_s5_discretize(4, 4, ctypes.c_void_p(0x1000), None, ctypes.c_void_p(0x1000),
+                              ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), None) == R.RL_EINVAL
