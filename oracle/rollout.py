@@ -20,7 +20,7 @@ Output layout (``n`` = number of env ids, A agents, D obs features):
 
 import numpy as np
 
-from . import actor_critic, mlp, s5, sampling
+from . import actor_critic, lbf_heuristics, mlp, s5, sampling
 
 
 def initial_states(env, cfg, seed, env_ids):
@@ -64,7 +64,7 @@ def policy_logits(obs, weights, biases, dtype, policy_index=None):
 
 def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
             states=None, logits_source=None, action_hook=None, policy_index=None, value_head=False,
-            recurrent=None, carry=None):
+            recurrent=None, carry=None, teammates=None):
     """Roll ``env_ids`` forward ``n_steps`` steps from absolute step ``t0``.
 
     ``states`` are the env states at t0 (default: the initial states, t0 = 0).
@@ -85,6 +85,8 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     at every step whose observation starts an episode (step counter 0); the
     result also holds ``carry``, the state after the last step (value_last is
     computed without advancing it).
+    ``teammates`` [n, A] (LBF): -1 = the agent acts with the network, k >= 0 =
+    heuristic k of ``lbf_heuristics`` (its logits replace the network's).
     """
     env_ids = list(env_ids)
     if states is None:
@@ -113,6 +115,11 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
         t = t0 + k
         obs, mask = observe_all(env, cfg, states)
         logits64 = net(obs, states, True)
+        if teammates is not None:
+            for i in range(n):
+                for a in range(A):
+                    if teammates[i][a] >= 0:
+                        logits64[i, a, :nA] = lbf_heuristics.logits(cfg, states[i], a, int(teammates[i][a]))
         if value_head:
             out["value"].append(logits64[..., nA])
             logits64 = logits64[..., :nA]
