@@ -125,8 +125,17 @@ def measure_workload(R, workloads, name, dt, steps, warmup):
     done = torch.empty(T, E, dtype=torch.uint8, device="cuda")
     t_next = [0]
 
+    tm = None
+    if w.get("teammates"):  # agent 0 the policy, agent 1 heuristic kind e mod 9 (a cross-play block per kind)
+        tm = torch.full((E, A), -1, dtype=torch.int32)
+        tm[:, 1] = torch.arange(E, dtype=torch.int32) % 9
+        tm = tm.cuda()
+
     def run():
-        R.rollout_run(cfg, pol, state, t_next[0], T, obs=obs, actions=acts, reward=rew, done=done)
+        if tm is None:
+            R.rollout_run(cfg, pol, state, t_next[0], T, obs=obs, actions=acts, reward=rew, done=done)
+        else:
+            R.rollout_run_teams(cfg, pol, tm, state, t_next[0], T, obs=obs, actions=acts, reward=rew, done=done)
         t_next[0] += T
 
     kern_ms, wall_ms = timed(run, steps, warmup)
@@ -462,7 +471,7 @@ def main():
     if not args.no_workloads:
         # the other workloads at full size, bf16, a few timed launches each
         line["workloads"] = {n: measure_workload(R, workloads, n, "bf16", min(args.steps, 5), 1)
-                             for n in ("lbf12_16k", "oc_4096", "hn_4096")}
+                             for n in ("lbf12_16k", "oc_4096", "hn_4096", "lbf7_const_4096", "lbf7_teams_4096")}
         line["workloads"]["lbf8_4096_ac"] = measure_actor_critic(R, workloads, "lbf8_4096_ac", "bf16",
                                                                  min(args.steps, 5), 1)
         line["workloads"]["lbf8_4096_pop"] = measure_population(R, workloads, "lbf8_4096_pop", "bf16",

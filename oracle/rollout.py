@@ -85,8 +85,8 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     at every step whose observation starts an episode (step counter 0); the
     result also holds ``carry``, the state after the last step (value_last is
     computed without advancing it).
-    ``teammates`` [n, A] (LBF): -1 = the agent acts with the network, k >= 0 =
-    heuristic k of ``lbf_heuristics`` (its logits replace the network's).
+    ``teammates`` [n, A] (LBF): k in 0..8 = heuristic k of ``lbf_heuristics``
+    (its logits replace the network's); any other value = the network.
     """
     env_ids = list(env_ids)
     if states is None:
@@ -118,7 +118,7 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
         if teammates is not None:
             for i in range(n):
                 for a in range(A):
-                    if teammates[i][a] >= 0:
+                    if 0 <= teammates[i][a] < len(lbf_heuristics.KINDS):
                         logits64[i, a, :nA] = lbf_heuristics.logits(cfg, states[i], a, int(teammates[i][a]))
         if value_head:
             out["value"].append(logits64[..., nA])

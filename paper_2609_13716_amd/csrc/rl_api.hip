@@ -278,6 +278,31 @@ rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* s
                   "rollout_run");
 }
 
+rl_status rollout_run_teams(const rl_env_config* cfg, const rl_policy* policy, const int32_t* teammates, void* state,
+                            uint64_t t0, int32_t n_steps, const rl_traj* out, void* stream) {
+  EnvSpec es;
+  rl_status s = check_cfg(cfg, &es);
+  if (s != RL_OK) return s;
+  if (es.kind != RL_ENV_LBF) return fail(RL_EUNSUPPORTED, "rollout_run_teams is implemented for LBF only");
+  rl::PolicyArgs a;
+  s = check_policy(policy, &a);
+  if (s != RL_OK) return s;
+  if (!teammates) return fail(RL_EINVAL, "teammates is NULL");
+  if (!state) return fail(RL_EINVAL, "state is NULL");
+  if (!out) return fail(RL_EINVAL, "out is NULL");
+  if (n_steps < 1) return fail(RL_EINVAL, "n_steps %d must be >= 1", n_steps);
+  if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
+  if (a.D != es.D) return fail(RL_ESHAPE, "policy input size %d != observation size %d", a.D, es.D);
+  if (a.NA != es.NA) return fail(RL_ESHAPE, "policy has %d actions, the env %d", a.NA, es.NA);
+  const size_t lds = rl::make_run_layout(es.A, es.D, a.H1, a.H2, a.dt).total;
+  if (lds > rl::MAX_LDS_BYTES)
+    return fail(RL_EUNSUPPORTED, "rollout tile needs %zu bytes of LDS (max %zu)", lds, rl::MAX_LDS_BYTES);
+  rl::TrajArgs o{out->obs, out->actions, out->logits, out->reward, out->done, out->obs_last};
+  o.teammates = teammates;
+  return launched(rl::launch_lbf_run(es.lbf, a, static_cast<int32_t*>(state), t0, n_steps, o, (hipStream_t)stream),
+                  "rollout_run_teams");
+}
+
 rl_status rollout_run_ac(const rl_env_config* cfg, const rl_policy* policy, void* state, uint64_t t0,
                          int32_t n_steps, const rl_traj* out, const rl_ac_traj* ac, void* stream) {
   EnvSpec es;

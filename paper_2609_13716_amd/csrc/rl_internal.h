@@ -123,6 +123,7 @@ struct TrajArgs {
   float* value = nullptr;       // [T, E, A] V(o_t) (value head only)
   float* logp = nullptr;        // [T, E, A] log pi(a_t | o_t) of the sampled action
   float* value_last = nullptr;  // [E, A] V(o_{t0+T})
+  const int32_t* teammates = nullptr;  // [E, A] heuristic kind per agent (LBF_NHEUR kinds), else the policy
 };
 
 // LDS layout of the fused rollout kernel for one env tile of TILE_E envs.

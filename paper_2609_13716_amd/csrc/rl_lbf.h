@@ -200,6 +200,69 @@ __device__ __forceinline__ void lbf_reset(const LbfParams& p, uint64_t env, uint
   lbf_reset_from_draws<AC, FC>(p, dw, s);
 }
 
+// Heuristic teammates (the paper's Greedy and Sequential LBF agents, read as
+// deterministic policies).  Kinds: 0-2 Greedy closest to self / to the
+// teammate (agent (i + 1) mod A) / to both (sum of distances); 3-4 Greedy
+// lowest / highest food level (then closest to self); 5-8 Sequential in
+// row-major, reverse row-major, column-major, reverse column-major order of
+// the food cells.  The target is the uneaten food of least key (the lowest
+// index on ties).  Next to it the agent loads; otherwise it steps along the
+// axis with more distance left (rows on ties), or along the other axis when
+// that cell holds an uneaten food or another agent and the other axis also
+// closes in.
+constexpr int LBF_NHEUR = 9;
+
+__device__ __forceinline__ int lbf_heuristic_action(const LbfParams& p, const LbfEnv& s, int agent, int kind) {
+  const int A = p.A, F = p.F, W = p.W;
+  const int me = s.acell[agent], mate = s.acell[agent + 1 < A ? agent + 1 : 0];
+  const int mr = lbf_row(p, me), mc = me - mr * W;
+  const int tr_ = lbf_row(p, mate), tc_ = mate - tr_ * W;
+  int best = -1, b1 = 0, b2 = 0, bcell = 0;
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j) {
+    if (j < F && !((s.eaten >> j) & 1u)) {
+      const int fcell = s.fcell[j];
+      const int fr = lbf_row(p, fcell), fc = fcell - fr * W;
+      const int dme = abs(fr - mr) + abs(fc - mc), dmate = abs(fr - tr_) + abs(fc - tc_);
+      int k1, k2 = 0;
+      switch (kind) {
+        case 0: k1 = dme; break;
+        case 1: k1 = dmate; break;
+        case 2: k1 = dme + dmate; break;
+        case 3: k1 = s.flevel[j]; k2 = dme; break;
+        case 4: k1 = -s.flevel[j]; k2 = dme; break;
+        case 5: k1 = fcell; break;
+        case 6: k1 = -fcell; break;
+        case 7: k1 = fc * 64 + fr; break;
+        default: k1 = -(fc * 64 + fr); break;
+      }
+      if (best < 0 || k1 < b1 || (k1 == b1 && k2 < b2)) {
+        best = j;
+        b1 = k1;
+        b2 = k2;
+        bcell = fcell;
+      }
+    }
+  }
+  if (best < 0) return 0;  // (no uneaten food: the episode has ended)
+  const int tr = lbf_row(p, bcell), tc = bcell - tr * W;
+  const int dr = tr - mr, dc = tc - mc;
+  if (abs(dr) + abs(dc) == 1) return 5;  // LOAD
+  const int vert = dr < 0 ? 1 : 2, horiz = dc < 0 ? 3 : 4;  // NORTH / SOUTH, WEST / EAST
+  const bool rows_first = abs(dr) >= abs(dc);
+  const int first = rows_first ? vert : horiz, other = rows_first ? horiz : vert;
+  const bool other_closes = rows_first ? dc != 0 : dr != 0;
+  const int next = me + (first == 1 ? -W : first == 2 ? W : first == 3 ? -1 : 1);
+  bool blocked = false;
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j)
+    if (j < F && !((s.eaten >> j) & 1u) && s.fcell[j] == next) blocked = true;
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i)
+    if (i < A && i != agent && s.acell[i] == next) blocked = true;
+  return (blocked && other_closes) ? other : first;
+}
+
 // One transition with actions act[0..A-1] (out-of-range -> noop).
 // Writes reward and done; `s` becomes the post-transition state (no reset).
 // Written without data-dependent branches: every candidate move and load is

@@ -318,9 +318,17 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
   const int e = e0 + tid;
   const uint64_t genv = (uint64_t)(p.env_base + e);
   LbfEnv s{};
+  int tkind[LBF_MAXA] = {-1, -1, -1, -1};  // heuristic teammates of this env's agents (-1: the policy)
   if (envlane) {
     lbf_load(state, p, e, s);
     lbf_paint(p, s, tid, L, true);
+    if (out.teammates) {
+#pragma unroll
+      for (int i = 0; i < LBF_MAXA; ++i) {
+        const int kd = i < A ? out.teammates[(size_t)e * A + i] : -1;
+        tkind[i] = (kd >= 0 && kd < LBF_NHEUR) ? kd : -1;
+      }
+    }
   }
   __syncthreads();
 
@@ -335,6 +343,18 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
     __syncthreads();
     mlp_logits<DT>(h2, RL.ld2, R, pol.H2, W3, b3, NOUT, lg, MAX_NA, wave, NTHREADS / 64, lane);
     __syncthreads();
+    if (out.teammates) {  // heuristic agents: logits 0 for their action, -inf for the others
+      if (envlane) {
+#pragma unroll
+        for (int i = 0; i < LBF_MAXA; ++i)
+          if (tkind[i] >= 0) {
+            const int act = lbf_heuristic_action(p, s, i, tkind[i]);
+            float* l = lg + (tid * A + i) * MAX_NA;
+            for (int a = 0; a < NA; ++a) l[a] = a == act ? 0.f : -INFINITY;
+          }
+      }
+      __syncthreads();
+    }
     // Gumbel scores per (row, action); every LBF action is legal
     for (int idx = tid; idx < R * NA; idx += NTHREADS) {
       const int r = fdiv(idx, m.na), a = idx - r * NA;
@@ -1015,7 +1035,7 @@ static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic&, const 
 
 static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const PolicyArgs& pol, int32_t* state,
                                    uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s, hipError_t* err) {
-  if (pol.NA != LBF_NACT + pol.VH) return false;
+  if (pol.NA != LBF_NACT + pol.VH || out.teammates) return false;
 #define RL_REG_CASE(DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV, VHV)                                    \
   if (pol.dt == DTV && p.H == GHV && p.W == GWV && pol.H1 == H1V && pol.H2 == H2V && p.A == AV &&            \
       p.F == FV && pol.VH == VHV) {                                                                          \

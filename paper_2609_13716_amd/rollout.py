@@ -98,6 +98,9 @@ def _load():
     lib.rollout_sample.argtypes = [cfgp, ctypes.c_uint64, P, P, P, P]
     lib.rollout_sample.restype = st
     lib.rl_gumbel_noise.argtypes, lib.rl_gumbel_noise.restype = [P, ctypes.c_int64, P, P], st
+    lib.rollout_run_teams.argtypes = [cfgp, ctypes.POINTER(_Policy), P, P, ctypes.c_uint64, ctypes.c_int32,
+                                      ctypes.POINTER(_Traj), P]
+    lib.rollout_run_teams.restype = st
     s5p = ctypes.POINTER(_S5Policy)
     lib.rl_s5_discretize.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P, P, P]
     lib.rl_s5_discretize.restype = st
@@ -113,7 +116,11 @@ lib = _load()
 # Every symbol the C header declares (checked by the test suite).
 EXPORTED = ("rl_state_bytes", "rl_obs_dim", "rl_num_actions", "rollout_last_error", "rollout_init",
             "rollout_step", "policy_forward", "rollout_run", "rollout_sample", "rl_gumbel_noise", "rollout_run_pop",
-            "rollout_run_ac", "rl_gae", "rl_s5_discretize", "rl_s5_workspace_bytes", "rollout_run_s5")
+            "rollout_run_ac", "rl_gae", "rl_s5_discretize", "rl_s5_workspace_bytes", "rollout_run_s5",
+            "rollout_run_teams")
+HEURISTICS = ("greedy_closest_self", "greedy_closest_teammate", "greedy_closest_avg", "greedy_lowest_level",
+              "greedy_highest_level", "seq_lexicographic", "seq_reverse_lexicographic", "seq_column_major",
+              "seq_reverse_column_major")  # kind k of rollout_run_teams
 
 
 def _check(status):
@@ -354,6 +361,28 @@ def rollout_run_ac(cfg, policy, state, t0, n_steps, value=None, logp=None, value
     pc = policy.c()
     _check(lib.rollout_run_ac(ctypes.byref(cfg.c()), ctypes.byref(pc), _ptr(state), t0, T, ctypes.byref(tr),
                               ctypes.byref(ac), _stream(stream)))
+
+
+def rollout_run_teams(cfg, policy, teammates, state, t0, n_steps, obs=None, actions=None, logits=None, reward=None,
+                      done=None, obs_last=None, stream=None):
+    """rollout_run where agent a of env e acts with heuristic teammates[e, a] (0..8, see HEURISTICS) or,
+    for any other value, with the policy."""
+    E, A = cfg.n_envs, cfg.n_agents
+    D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
+    T = n_steps
+    _need(teammates, "teammates", torch.int32, (E, A))
+    _need(state, "state", torch.int32)
+    _need(obs, "obs", policy.torch_dtype, (T, E, A, D))
+    _need(actions, "actions", torch.int32, (T, E, A))
+    _need(logits, "logits", torch.float32, (T, E, A, nA))
+    _need(reward, "reward", torch.float32, (T, E))
+    _need(done, "done", torch.uint8, (T, E))
+    _need(obs_last, "obs_last", policy.torch_dtype, (E, A, D))
+    tr = _Traj(obs=_ptr(obs), actions=_ptr(actions), logits=_ptr(logits), reward=_ptr(reward), done=_ptr(done),
+               obs_last=_ptr(obs_last))
+    pc = policy.c()
+    _check(lib.rollout_run_teams(ctypes.byref(cfg.c()), ctypes.byref(pc), _ptr(teammates), _ptr(state), t0, T,
+                                 ctypes.byref(tr), _stream(stream)))
 
 
 class S5Policy:

@@ -1,0 +1,76 @@
+"""GPU parity of rollouts with heuristic LBF teammates (rollout_run_teams) against the oracle, through the C ABI.
+
+Every heuristic kind drives some agent (kind = env index mod 9 on agent 1,
+plus out-of-range kinds that fall back to the policy); agent 0 runs the
+policy.  Env outputs and actions are bit-exact; a heuristic agent's logits
+(0 for its action, -inf elsewhere) are exact; policy logits are within the
+dtype tolerance; a strict run samples the oracle's actions from the GPU's
+logits.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import lbf, rollout
+from paper_2609_13716_amd import rollout as R
+from paper_2609_13716_amd import workloads
+
+from parity import RTOL, NearTieLockstep, assert_logits_close, oracle_cfg, require_gpu, states_from_device
+
+pytestmark = pytest.mark.gpu
+
+
+def _note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.mark.parametrize("cfgkw,hidden,dtype", [
+    (dict(grid_h=7, grid_w=7, max_agent_level=1, max_food_level=2, const_levels=True), (64, 64), "bf16"),
+    (dict(), (64, 64), "f32"),
+    (dict(n_agents=3, n_food=4, max_agent_level=2, max_food_level=4), (32, 48), "bf16"),
+])
+def test_heuristic_teammates_parity(cfgkw, hidden, dtype):
+    require_gpu()
+    cfg = R.EnvConfig(n_envs=41, seed=13, env_base=9, max_steps=25, **cfgkw)
+    E, A, D = cfg.n_envs, cfg.n_agents, R.rl_obs_dim(cfg)
+    _note(f"rollout_run_teams {cfgkw} {hidden} {dtype}")
+    tm = np.full((E, A), -1, dtype=np.int32)
+    tm[:, 1] = np.arange(E) % 9
+    tm[3, 1], tm[4, 1] = 9, -5  # out of range: the policy
+    if A > 2:
+        tm[:, 2] = (np.arange(E) * 5 + 2) % 9
+    ws, bs = workloads.policy_weights((D, *hidden, 6), seed=77, bias_scale=0.2)
+    pol = R.Policy(ws, bs, dtype)
+    T = 60
+    state = R.new_state(cfg)
+    R.rollout_init(cfg, state)
+    out = dict(obs=torch.empty(T, E, A, D, dtype=pol.torch_dtype, device="cuda"),
+               actions=torch.empty(T, E, A, dtype=torch.int32, device="cuda"),
+               logits=torch.empty(T, E, A, 6, device="cuda"),
+               reward=torch.empty(T, E, device="cuda"), done=torch.empty(T, E, dtype=torch.uint8, device="cuda"),
+               obs_last=torch.empty(E, A, D, dtype=pol.torch_dtype, device="cuda"))
+    R.rollout_run_teams(cfg, pol, torch.from_numpy(tm).cuda(), state, 0, T, **out)
+    torch.cuda.synchronize()
+    g = {k: v.cpu() for k, v in out.items()}
+    oc = oracle_cfg(cfg)
+    env_ids = list(range(9, 9 + E))
+    hook = NearTieLockstep(g["actions"].numpy(), cfg.seed, env_ids, RTOL[dtype])
+    ref = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, dtype, action_hook=hook, teammates=tm)
+    assert np.array_equal(g["obs"].float().numpy().astype(np.float64), ref["obs"])
+    assert np.array_equal(g["reward"].numpy().view(np.uint32), ref["reward"].view(np.uint32))
+    assert np.array_equal(g["done"].numpy(), ref["done"])
+    assert np.array_equal(g["actions"].numpy(), ref["actions"])
+    assert np.array_equal(g["obs_last"].float().numpy().astype(np.float64), ref["obs_last"])
+    assert states_from_device(cfg, state) == ref["states"]
+    heur = (tm >= 0) & (tm < 9)
+    gl, rl_ = g["logits"].numpy().astype(np.float64), ref["logits"]
+    assert np.array_equal(gl[:, heur], rl_[:, heur])
+    assert_logits_close(gl[:, ~heur], rl_[:, ~heur], RTOL[dtype])
+    assert ref["done"].any()
+    strict = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, dtype, teammates=tm,
+                             logits_source=lambda k, _: g["logits"][k].numpy())
+    assert np.array_equal(strict["actions"], g["actions"].numpy())
