@@ -471,7 +471,8 @@ def main():
     if not args.no_workloads:
         # the other workloads at full size, bf16, a few timed launches each
         line["workloads"] = {n: measure_workload(R, workloads, n, "bf16", min(args.steps, 5), 1)
-                             for n in ("lbf12_16k", "oc_4096", "hn_4096", "lbf7_const_4096", "lbf7_teams_4096")}
+                             for n in ("lbf12_16k", "oc_4096", "hn_4096", "hn_mini_4096", "lbf7_const_4096",
+                                       "lbf7_teams_4096")}
         line["workloads"]["lbf8_4096_ac"] = measure_actor_critic(R, workloads, "lbf8_4096_ac", "bf16",
                                                                  min(args.steps, 5), 1)
         line["workloads"]["lbf8_4096_pop"] = measure_population(R, workloads, "lbf8_4096_pop", "bf16",

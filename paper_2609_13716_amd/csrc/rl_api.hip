@@ -114,20 +114,25 @@ rl_status check_hanabi(const rl_env_config* cfg, EnvSpec* es) {
   if (cfg->hn_colors < 1 || cfg->hn_ranks < 1 || cfg->hn_hand_size < 1 || cfg->hn_info_tokens < 1 ||
       cfg->hn_life_tokens < 1)
     return fail(RL_EINVAL, "Hanabi colours, ranks, hand size, info and life tokens must be >= 1");
-  if (cfg->hn_colors != rl::HN_COLOURS || cfg->hn_ranks != rl::HN_RANKS || cfg->hn_hand_size != rl::HN_HAND ||
-      cfg->hn_info_tokens != rl::HN_INFO || cfg->hn_life_tokens != rl::HN_LIVES)
-    return fail(RL_EUNSUPPORTED, "Hanabi is built for 5 colours, 5 ranks, hands of 5, 8 info tokens, 3 lives");
+  const bool std_game = cfg->hn_colors == rl::HnStd::C && cfg->hn_ranks == rl::HnStd::R &&
+                        cfg->hn_hand_size == rl::HnStd::H;
+  const bool mini_game = cfg->hn_colors == rl::HnMini::C && cfg->hn_ranks == rl::HnMini::R &&
+                         cfg->hn_hand_size == rl::HnMini::H;
+  if (!(std_game || mini_game) || cfg->hn_info_tokens != rl::HN_INFO || cfg->hn_life_tokens != rl::HN_LIVES)
+    return fail(RL_EUNSUPPORTED,
+                "Hanabi is built for 5 colours x 5 ranks or 3 colours x 3 ranks, hands of 5, 8 info tokens, 3 lives");
   if (cfg->grid_h || cfg->grid_w || cfg->n_food || cfg->max_agent_level || cfg->max_food_level ||
       cfg->lbf_const_levels || cfg->oc_cook_time || cfg->oc_soup_reward)
     return fail(RL_EINVAL, "LBF/Overcooked fields must be 0 for Hanabi");
   rl::HnParams& p = es->hn;
   p.E = cfg->n_envs;
   p.max_steps = cfg->max_steps;
+  p.mini = mini_game ? 1 : 0;
   p.env_base = cfg->env_base;
   p.seed = cfg->seed;
   es->A = 2;
-  es->D = rl::HN_OBS;
-  es->NA = rl::HN_NACT;
+  es->D = mini_game ? rl::HnMini::OBS : rl::HnStd::OBS;
+  es->NA = mini_game ? rl::HnMini::NACT : rl::HnStd::NACT;
   es->state_bytes = (size_t)rl::HN_PLANES_STATE * (size_t)p.E * sizeof(int32_t);
   return RL_OK;
 }

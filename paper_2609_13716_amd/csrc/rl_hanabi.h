@@ -16,14 +16,43 @@
 
 namespace rl {
 
-constexpr int HN_COLOURS = 5, HN_RANKS = 5, HN_HAND = 5, HN_INFO = 8, HN_LIVES = 3;
-constexpr int HN_CARDS = 50, HN_KINDS = 25, HN_NACT = 20, HN_OBS = 658;
-constexpr int HN_DECK_WORDS = 13;
-constexpr int HN_PLANES_STATE = 35;  // int32 state planes per env
+constexpr int HN_INFO = 8, HN_LIVES = 3;
+constexpr int HN_DECK_WORDS = 13;     // deck words of the state (the standard game's 50 cards; smaller games use fewer)
+constexpr int HN_PLANES_STATE = 35;  // int32 state planes per env (the same layout for every game size)
+
+// Game sizes: C colours, R ranks (copies 3, 2, ..., 2, 1 per colour), hands
+// of H (H <= 5, C * R <= 25: card ids fit the 5-bit fields), 8 tokens, 3 lives.
+template <int C_, int R_, int H_>
+struct HnGame {
+  static constexpr int C = C_, R = R_, H = H_;
+  static_assert(C >= 1 && C <= 5 && R >= 2 && R <= 5 && H >= 1 && H <= 5, "packed fields hold 5 slots of 5 bits");
+  static constexpr int PER_COLOUR = 3 + 2 * (R - 2) + 1;
+  static constexpr int CARDS = C * PER_COLOUR, KINDS = C * R, NACT = 2 * H + C + R;
+  static constexpr int DW = (CARDS + 3) / 4;  // deck words in use
+  static constexpr int LASTW = 2 + 4 + 2 + C + R + H + H + KINDS + 1 + 1;
+  // observation sections, in order
+  static constexpr int O_FLAGS = H * KINDS, O_DECK = O_FLAGS + 2, O_FW = O_DECK + CARDS - 2 * H,
+                       O_INFO = O_FW + KINDS, O_LIVES = O_INFO + HN_INFO, O_DISC = O_LIVES + HN_LIVES,
+                       O_LAST = O_DISC + CARDS, O_KNOW = O_LAST + LASTW;
+  static constexpr int KNOW_SLOT = KINDS + C + R;
+  static constexpr int OBS = O_KNOW + 2 * H * KNOW_SLOT;
+  static constexpr int NFIELDS = 3 * H + C + 6;  // field computations per observation row (hn_field_bits)
+  static constexpr int OBS_WORDS = (OBS + 63) / 64;
+  static constexpr uint32_t FW_FULL = []() {
+    uint32_t m = 0;
+    for (int c = 0; c < C; ++c) m |= (uint32_t)R << (3 * c);
+    return m;
+  }();
+};
+using HnStd = HnGame<5, 5, 5>;   // the standard game: 50 cards, 20 actions, 658 features
+using HnMini = HnGame<3, 3, 5>;  // 3 colours x 3 ranks: 18 cards, 16 actions
+static_assert(HnStd::OBS == 658 && HnStd::NACT == 20 && HnStd::CARDS == 50 && HnStd::NFIELDS == 26, "standard game");
+constexpr int HN_OBS = HnStd::OBS, HN_NACT = HnStd::NACT;  // the largest game's sizes
 enum : int { HN_PLAY = 0, HN_DISCARD = 1, HN_HINT_COLOUR = 2, HN_HINT_RANK = 3 };
 
 struct HnParams {
   int E, max_steps;
+  int mini;  // 1: the 3 x 3 game (HnMini), 0: the standard game (HnStd)
   int64_t env_base;
   uint64_t seed;
 };
@@ -73,37 +102,42 @@ __device__ __forceinline__ void hn_add_disc(HnEnv& s, int card) {
 }
 
 // The deck of a fresh game at step t, shuffled by one whole wave (all lanes
-// call this with the same env and t): lane l < 50 holds the card at position
-// l, starting from the ordered deck (per colour: rank 1 x3, ranks 2-4 x2,
-// rank 5 x1); Fisher-Yates for i = 49 down to 1 swaps positions i and
-// j = u(i + 1), with draw k = 49 - i of the reset stream.  Lanes 0..6 first
-// evaluate the 7 Philox blocks of the 49 draws; every swap is then two
-// readlanes.  The 13 packed deck words (card k in byte k % 4 of word k / 4)
-// are written to `words` (LDS).
+// call this with the same env and t): lane l < CARDS holds the card at
+// position l, starting from the ordered deck (per colour: rank 1 x3, middle
+// ranks x2, the top rank x1); Fisher-Yates for i = CARDS-1 down to 1 swaps
+// positions i and j = u(i + 1), with draw k = CARDS-1 - i of the reset
+// stream.  The first lanes evaluate the Philox blocks of the draws; every
+// swap is then two readlanes.  The packed deck words (card k in byte k % 4 of
+// word k / 4; the words past the game's deck are 0) are written to `words`.
+template <class G>
 __device__ __forceinline__ void hn_wave_shuffle(uint64_t seed, uint64_t env, uint64_t t, int lane,
                                                 uint32_t* __restrict__ words) {
+  constexpr int NB = (G::CARDS - 1 + 7) / 8;
   Block4 b{0, 0, 0, 0};
-  if (lane < 7) b = draw_block(seed, env, t, (uint64_t)lane, TAG_RESET);
-  const int c = lane / 10, o = lane - c * 10;
-  int a = c * HN_RANKS + (o < 3 ? 0 : o < 5 ? 1 : o < 7 ? 2 : o < 9 ? 3 : 4);
+  if (lane < NB) b = draw_block(seed, env, t, (uint64_t)lane, TAG_RESET);
+  const int c = lane / G::PER_COLOUR, o = lane - c * G::PER_COLOUR;
+  const int rk = o < 3 ? 0 : min((o - 3) / 2 + 1, G::R - 1);
+  int a = c * G::R + rk;
 #pragma unroll
-  for (int k = 0; k < HN_CARDS - 1; ++k) {
-    const int i = HN_CARDS - 1 - k;
+  for (int k = 0; k < G::CARDS - 1; ++k) {
+    const int i = G::CARDS - 1 - k;
     const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)block_u32(b, k & 7), k >> 3);
     const int j = (int)range_map(d, (uint32_t)(i + 1));
     const int ai = __builtin_amdgcn_readlane(a, i), aj = __builtin_amdgcn_readlane(a, j);
     a = lane == i ? aj : lane == j ? ai : a;
   }
-  uint32_t v = lane < HN_CARDS ? (uint32_t)a << (8 * (lane & 3)) : 0u;
+  uint32_t v = lane < G::CARDS ? (uint32_t)a << (8 * (lane & 3)) : 0u;
   v |= (uint32_t)__shfl_xor((int)v, 1);
   v |= (uint32_t)__shfl_xor((int)v, 2);
   if ((lane & 3) == 0 && lane < 4 * HN_DECK_WORDS) words[lane >> 2] = v;
 }
 
-// A fresh game on the shuffled deck `words`: player 0 holds cards 0..4 in
-// slots 0..4, player 1 cards 5..9, card 10 is drawn next; player 0 moves
+// A fresh game on the shuffled deck `words`: player 0 holds cards 0..H-1 in
+// slots 0..H-1, player 1 cards H..2H-1, card 2H is drawn next; player 0 moves
 // first with all tokens and lives, blank knowledge, no fireworks or discards.
+template <class G>
 __device__ __forceinline__ void hn_deal(HnEnv& s, const uint32_t* __restrict__ words) {
+  constexpr int HN_HAND = G::H;
 #pragma unroll
   for (int w = 0; w < HN_DECK_WORDS; ++w) s.deck[w] = words[w];
 #pragma unroll
@@ -116,7 +150,9 @@ __device__ __forceinline__ void hn_deal(HnEnv& s, const uint32_t* __restrict__ w
     }
     s.hand[pl] = h;
     s.n[pl] = HN_HAND;
-    s.kc[pl] = s.kr[pl] = 0x1ffffffu;  // every colour and rank possible in all 5 slots
+    s.kc[pl] = s.kr[pl] = 0x1ffffffu & ((1u << (5 * HN_HAND)) - 1u);  // every colour and rank possible
+    s.kc[pl] &= 0x108421u * ((1u << G::C) - 1u);  // (only the game's colours and ranks)
+    s.kr[pl] &= 0x108421u * ((1u << G::R) - 1u);
     s.hc[pl] = s.hr[pl] = 0;
   }
   s.fw = 0;
@@ -133,7 +169,9 @@ __device__ __forceinline__ void hn_deal(HnEnv& s, const uint32_t* __restrict__ w
 // Legal actions of the player to move as a 20-bit mask.  (Player-indexed
 // fields are picked with selects, not indexed by the mover: a register array
 // indexed at run time would live in scratch memory.)
+template <class G>
 __device__ __forceinline__ uint32_t hn_legal(const HnEnv& s) {
+  constexpr int HN_HAND = G::H, HN_RANKS = G::R, HN_COLOURS = G::C;
   const bool one = s.cur == 1;
   const int np = one ? s.n[1] : s.n[0], nq = one ? s.n[0] : s.n[1];
   const uint32_t hq = one ? s.hand[0] : s.hand[1];
@@ -175,16 +213,19 @@ __device__ __forceinline__ void hn_orient(HnEnv& s, bool sw) {
 
 // One move of the player to move (an illegal or out-of-range action acts as
 // its lowest legal one); `s` becomes the post-transition state (no reset).
+template <class G>
 __device__ __forceinline__ void hn_transition(const HnParams& p, HnEnv& s, int a_in, float& reward, uint32_t& done) {
-  const uint32_t legal = hn_legal(s);
+  constexpr int HN_HAND = G::H, HN_RANKS = G::R, HN_COLOURS = G::C, HN_CARDS = G::CARDS, HN_NACT = G::NACT;
+  const uint32_t legal = hn_legal<G>(s);
   const int a = ((unsigned)a_in < (unsigned)HN_NACT && ((legal >> a_in) & 1u)) ? a_in : __builtin_ctz(legal);
   const int mover = s.cur;
   hn_orient(s, mover == 1);
   constexpr int pl = 0, q = 1;  // the mover and its partner after hn_orient
   int rew = 0;
   bool drew_last = false;
-  const int fw_total_before = (int)(hn_field(s.fw, 3, 0) + hn_field(s.fw, 3, 1) + hn_field(s.fw, 3, 2) +
-                                    hn_field(s.fw, 3, 3) + hn_field(s.fw, 3, 4));
+  int fw_total_before = 0;
+#pragma unroll
+  for (int c = 0; c < HN_COLOURS; ++c) fw_total_before += (int)hn_field(s.fw, 3, c);
   if (a < 2 * HN_HAND) {
     const int slot = a % HN_HAND;
     const bool play = a >= HN_HAND;
@@ -219,8 +260,8 @@ __device__ __forceinline__ void hn_transition(const HnParams& p, HnEnv& s, int a
     if (s.next < HN_CARDS) {
       const int sh = 5 * s.n[pl];
       s.hand[pl] |= (uint32_t)hn_deck_card(s, s.next) << sh;
-      s.kc[pl] |= 31u << sh;
-      s.kr[pl] |= 31u << sh;
+      s.kc[pl] |= ((1u << HN_COLOURS) - 1u) << sh;
+      s.kr[pl] |= ((1u << HN_RANKS) - 1u) << sh;
       s.n[pl] += 1;
       s.next += 1;
       drew_last = s.next == HN_CARDS;
@@ -262,7 +303,7 @@ __device__ __forceinline__ void hn_transition(const HnParams& p, HnEnv& s, int a
   if (s.lives == 0) {
     terminated = true;
     rew = -fw_total_before;
-  } else if (s.fw == 0x5b6du /* every height 5 */ || s.turns_left == 0) {
+  } else if (s.fw == G::FW_FULL /* every firework complete */ || s.turns_left == 0) {
     terminated = true;
   }
   s.cur = 1 - mover;
@@ -322,11 +363,11 @@ __device__ __forceinline__ void hn_store(int32_t* __restrict__ st, int E, int e,
   w(34, s.last);
 }
 
-// The observation as a 658-bit vector in eleven 64-bit words (bit f =
-// feature f), assembled from 26 fields per row that different threads
-// compute in parallel (hn_field_bits) and OR into the row's words.
-constexpr int HN_OBS_WORDS = (HN_OBS + 63) / 64;
-constexpr int HN_NFIELDS = 26;
+// The observation as a bit vector in 64-bit words (bit f = feature f),
+// assembled from G::NFIELDS fields per row that different threads compute
+// in parallel (hn_field_bits) and OR into the row's words.
+constexpr int HN_OBS_WORDS = (HN_OBS + 63) / 64;  // (the largest game)
+constexpr int HN_NFIELDS = HnStd::NFIELDS;
 
 // What the field computations read of one game (published to LDS after each move).
 struct HnPub {
@@ -361,83 +402,90 @@ __device__ __forceinline__ uint64_t hn_therm(int n, int width) {  // n ones (cla
   return k >= 64 ? ~0ull : ((1ull << k) - 1ull);
 }
 
-// Field f (0..25) of player me's observation: its bits, and in `off` the
-// feature index of its bit 0.  Fields: 0-4 partner slots (25-bit one-hot),
-// 5 short hands, 6 deck thermometer, 7 fireworks, 8 tokens, 9 lives, 10-14
-// the discard thermometers of one colour, 15 the last move, 16-25 the
-// knowledge of one slot (observer's hand, then the partner's).  `v` is
-// normally in LDS; player indices are plain memory indices there.
+// Field f (0..NFIELDS-1) of player me's observation: its bits, and in `off`
+// the feature index of its bit 0.  Fields: 0..H-1 partner slots (one-hot
+// card id), H short hands, H+1 deck thermometer, H+2 fireworks, H+3 tokens,
+// H+4 lives, then C fields of one colour's discard thermometers, the last
+// move, and 2H fields of the knowledge of one slot (observer's hand, then the
+// partner's).  `v` is normally in LDS; player indices are plain memory
+// indices there.
+template <class G>
 __device__ __forceinline__ uint64_t hn_field_bits(const HnPub& v, int me, int f, int& off) {
+  constexpr int H = G::H, C = G::C, R = G::R, K = G::KINDS;
   const int pt = 1 - me;
-  if (f < 5) {
-    off = 25 * f;
+  if (f < H) {
+    off = K * f;
     return f < v.n[pt] ? (1ull << hn_field(v.hand[pt], 5, f)) : 0ull;
   }
-  if (f == 5) {
-    off = 125;
-    return (v.n[me] < HN_HAND ? 1ull : 0ull) | (v.n[pt] < HN_HAND ? 2ull : 0ull);
+  if (f == H) {
+    off = G::O_FLAGS;
+    return (v.n[me] < H ? 1ull : 0ull) | (v.n[pt] < H ? 2ull : 0ull);
   }
-  if (f == 6) {
-    off = 127;
-    return hn_therm(HN_CARDS - v.next, 40);
+  if (f == H + 1) {
+    off = G::O_DECK;
+    return hn_therm(G::CARDS - v.next, G::CARDS - 2 * H);
   }
-  if (f == 7) {
-    off = 167;
+  if (f == H + 2) {
+    off = G::O_FW;
     uint64_t fw = 0;
 #pragma unroll
-    for (int c = 0; c < HN_COLOURS; ++c) {
+    for (int c = 0; c < C; ++c) {
       const uint32_t h = hn_field(v.fw, 3, c);
-      fw |= h ? (1ull << (5 * c + h - 1)) : 0ull;
+      fw |= h ? (1ull << (R * c + h - 1)) : 0ull;
     }
     return fw;
   }
-  if (f == 8) {
-    off = 192;
-    return hn_therm(v.info, 8);
+  if (f == H + 3) {
+    off = G::O_INFO;
+    return hn_therm(v.info, HN_INFO);
   }
-  if (f == 9) {
-    off = 200;
-    return hn_therm(v.lives, 3);
+  if (f == H + 4) {
+    off = G::O_LIVES;
+    return hn_therm(v.lives, HN_LIVES);
   }
-  if (f < 15) {  // one colour's discards: thermometers of 3, 2, 2, 2, 1 copies
-    const int c = f - 10;
-    off = 203 + 10 * c;
+  if (f < H + 5 + C) {  // one colour's discards: thermometers of 3, 2, ..., 2, 1 copies
+    const int c = f - (H + 5);
+    off = G::O_DISC + G::PER_COLOUR * c;
     uint64_t d = 0;
 #pragma unroll
-    for (int r = 0; r < HN_RANKS; ++r) {
-      const int card = c * HN_RANKS + r;
+    for (int r = 0; r < R; ++r) {
+      const int card = c * R + r;
       const uint32_t cnt = card < 16 ? (v.disc0 >> (2 * card)) & 3u : (v.disc1 >> (2 * (card - 16))) & 3u;
-      d |= hn_therm((int)cnt, r == 0 ? 3 : r == 4 ? 1 : 2) << (r == 0 ? 0 : 2 * r + 1);
+      d |= hn_therm((int)cnt, r == 0 ? 3 : r == R - 1 ? 1 : 2) << (r == 0 ? 0 : 2 * r + 1);
     }
     return d;
   }
-  if (f == 15) {  // last move: 2 + 4 + 2 + 5 + 5 + 5 + 5 bits, then the card (25), success, token
-    off = 253;
+  if (f == H + 5 + C) {  // last move: actor 2, kind 4, target 2, colour C, rank R, revealed H, slot H,
+                         // card C * R, success, token
+    off = G::O_LAST;
     const uint32_t L = v.last;
     if (!(L & 1u)) return 0ull;
     const int actor = (int)((L >> 1) & 1u), kind = (int)((L >> 2) & 3u), target = (int)((L >> 4) & 1u);
     const uint32_t hcol = (L >> 5) & 7u, hrank = (L >> 8) & 7u, slot = (L >> 16) & 7u, card = (L >> 19) & 31u;
+    constexpr int B_COL = 8, B_RANK = B_COL + C, B_REV = B_RANK + R, B_SLOT = B_REV + H, B_CARD = B_SLOT + H,
+                  B_OK = B_CARD + K;
     uint64_t a = (1ull << ((actor - me) & 1)) | (1ull << (2 + kind));
     if (kind >= HN_HINT_COLOUR) a |= 1ull << (6 + ((target - me) & 1));
-    if (hcol) a |= 1ull << (8 + hcol - 1);
-    if (hrank) a |= 1ull << (13 + hrank - 1);
-    a |= (uint64_t)((L >> 11) & 31u) << 18;
-    if (slot) a |= 1ull << (23 + slot - 1);
-    if (card) a |= 1ull << (28 + card - 1);
-    a |= (uint64_t)((L >> 24) & 3u) << 53;
+    if (hcol) a |= 1ull << (B_COL + hcol - 1);
+    if (hrank) a |= 1ull << (B_RANK + hrank - 1);
+    a |= (uint64_t)((L >> 11) & ((1u << H) - 1u)) << B_REV;
+    if (slot) a |= 1ull << (B_SLOT + slot - 1);
+    if (card) a |= 1ull << (B_CARD + card - 1);
+    a |= (uint64_t)((L >> 24) & 3u) << B_OK;
     return a;
   }
-  // knowledge of one card: 25 plausible cards, hinted colour, hinted rank
-  const int j = (f - 16) / 5, sl = (f - 16) - 5 * j, who = j ? pt : me;
-  off = 308 + 175 * j + 35 * sl;
+  // knowledge of one card: C * R plausible cards, hinted colour, hinted rank
+  const int f0 = f - (H + 6 + C);
+  const int j = f0 / H, sl = f0 - H * j, who = j ? pt : me;
+  off = G::O_KNOW + H * G::KNOW_SLOT * j + G::KNOW_SLOT * sl;
   if (sl >= v.n[who]) return 0ull;
   const uint32_t kc = hn_field(v.kc[who], 5, sl), kr = hn_field(v.kr[who], 5, sl);
   const uint32_t hc = hn_field(v.hc[who], 3, sl), hr = hn_field(v.hr[who], 3, sl);
-  uint64_t spread = 0;  // colour bits at the bottom of 5-bit groups; times the rank mask fills each group
+  uint64_t spread = 0;  // colour bits at the bottom of R-bit groups; times the rank mask fills each group
 #pragma unroll
-  for (int c = 0; c < HN_COLOURS; ++c) spread |= (uint64_t)((kc >> c) & 1u) << (5 * c);
+  for (int c = 0; c < C; ++c) spread |= (uint64_t)((kc >> c) & 1u) << (R * c);
   const uint64_t plaus = spread * (uint64_t)kr;
-  return plaus | ((hc ? 1ull << (hc - 1) : 0ull) << 25) | ((hr ? 1ull << (hr - 1) : 0ull) << 30);
+  return plaus | ((hc ? 1ull << (hc - 1) : 0ull) << K) | ((hr ? 1ull << (hr - 1) : 0ull) << (K + C));
 }
 
 }  // namespace rl

@@ -27,13 +27,13 @@ struct HnTile {
 // same field of different rows, so a wave runs few of the field branches) and
 // ORs it into the row's words (LDS atomics; the words are zero beforehand).
 // Needs the published games.
-template <int TE, int NT>
+template <class G, int TE, int NT>
 __device__ __forceinline__ void hn_build_bits(HnTile* envs, int te_valid, int tid) {
-  for (int t = tid; t < 2 * TE * HN_NFIELDS; t += NT) {
+  for (int t = tid; t < 2 * TE * G::NFIELDS; t += NT) {
     const int f = t / (2 * TE), row = t - f * (2 * TE), el = row >> 1, me = row & 1;
     if (el >= te_valid) continue;
     int off;
-    const uint64_t v = hn_field_bits(envs[el].pub, me, f, off);
+    const uint64_t v = hn_field_bits<G>(envs[el].pub, me, f, off);
     if (v) {
       unsigned long long* w = reinterpret_cast<unsigned long long*>(envs[el].bits[me]);
       const int i = off >> 6, sh = off & 63;
@@ -46,7 +46,7 @@ __device__ __forceinline__ void hn_build_bits(HnTile* envs, int te_valid, int ti
 // Paint rows 2*el + me (el < te_valid) of the observation tile from the
 // assembled bit vectors, one row per wave at a time (lane l writes features
 // l, l + 64, ...), and clear the vectors for the next step.
-template <typename T, int NW>
+template <class G, typename T, int NW>
 __device__ __forceinline__ void hn_paint(HnTile* envs, int te_valid, T* tile, int ld, int wave, int lane) {
   for (int r = wave; r < 2 * te_valid; r += NW) {
     uint64_t* wp = envs[r >> 1].bits[r & 1];
@@ -60,36 +60,37 @@ __device__ __forceinline__ void hn_paint(HnTile* envs, int te_valid, T* tile, in
 #pragma unroll
     for (int i = 0; i < HN_OBS_WORDS; ++i) {
       const int f = 64 * i + lane;
-      if (f < HN_OBS) row[f] = small_int_to<T>((uint32_t)(w[i] >> lane) & 1u);
+      if (f < G::OBS) row[f] = small_int_to<T>((uint32_t)(w[i] >> lane) & 1u);
     }
   }
 }
 
 // Legal masks of both players of envs 0..te_valid-1 ([env][agent][20] bytes).
-template <int NT>
+template <class G, int NT>
 __device__ __forceinline__ void hn_write_legal(const HnTile* __restrict__ envs, int te_valid, uint8_t* __restrict__ g,
                                                int tid) {
-  for (int i = tid; i < te_valid * 2 * HN_NACT; i += NT) {
-    const int el = i / (2 * HN_NACT), rem = i - el * 2 * HN_NACT, ag = rem / HN_NACT, a = rem - ag * HN_NACT;
+  for (int i = tid; i < te_valid * 2 * G::NACT; i += NT) {
+    const int el = i / (2 * G::NACT), rem = i - el * 2 * G::NACT, ag = rem / G::NACT, a = rem - ag * G::NACT;
     g[i] = (ag == envs[el].pub.cur) ? (uint8_t)((envs[el].legal >> a) & 1u) : (uint8_t)0;
   }
 }
 
 // What the workgroup reads of a game after each move: the packed game and
 // the mover's legal actions.
+template <class G>
 __device__ __forceinline__ void hn_publish(const HnEnv& s, HnTile& t) {
   hn_pub(s, t.pub);
-  t.legal = hn_legal(s);
+  t.legal = hn_legal<G>(s);
 }
 
 // Shuffles for the envs of the tile flagged in need[] (drawn at step t):
 // wave w takes envs w, w + NW, ...
-template <int NW>
+template <class G, int NW>
 __device__ __forceinline__ void hn_shuffle_flagged(const HnParams& p, int e0, int te_valid, uint64_t t,
                                                    const uint32_t* need, uint32_t (*words)[HN_DECK_WORDS], int wave,
                                                    int lane) {
   for (int el = wave; el < te_valid; el += NW)
-    if (need[el]) hn_wave_shuffle(p.seed, (uint64_t)(p.env_base + e0 + el), t, lane, words[el]);
+    if (need[el]) hn_wave_shuffle<G>(p.seed, (uint64_t)(p.env_base + e0 + el), t, lane, words[el]);
 }
 
 // need[TE] = whether any env lane (all in wave 0) has d != 0; read after a barrier.
@@ -102,39 +103,39 @@ __device__ __forceinline__ void hn_flag_any(uint32_t* need, int TE, uint32_t d, 
 
 // -------------------------------------------------------------- init ----
 
-template <typename OT, int TE>
+template <class G, typename OT, int TE>
 __global__ __launch_bounds__(NTHREADS) void hn_init_kernel(HnParams p, int32_t* __restrict__ state,
                                                            OT* __restrict__ obs, uint8_t* __restrict__ legal) {
   constexpr int NW = NTHREADS / 64;
   __shared__ HnTile envs[TE];
   __shared__ uint32_t words[TE][HN_DECK_WORDS];
-  __shared__ __align__(16) OT tile[2 * TE * HN_OBS];
+  __shared__ __align__(16) OT tile[2 * TE * G::OBS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0);
   zero_lds<NTHREADS>(envs, sizeof(envs), tid);  // the bit vectors start clear
   for (int el = wave; el < te_valid; el += NW)
-    hn_wave_shuffle(p.seed, (uint64_t)(p.env_base + e0 + el), 0, lane, words[el]);
+    hn_wave_shuffle<G>(p.seed, (uint64_t)(p.env_base + e0 + el), 0, lane, words[el]);
   __syncthreads();
   if (tid < te_valid) {
     HnEnv s;
-    hn_deal(s, words[tid]);
+    hn_deal<G>(s, words[tid]);
     hn_store(state, p.E, e0 + tid, s);
-    hn_publish(s, envs[tid]);
+    hn_publish<G>(s, envs[tid]);
   }
   __syncthreads();
   if (obs) {
-    hn_build_bits<TE, NTHREADS>(envs, te_valid, tid);
+    hn_build_bits<G, TE, NTHREADS>(envs, te_valid, tid);
     __syncthreads();
-    hn_paint<OT, NW>(envs, te_valid, tile, HN_OBS, wave, lane);
+    hn_paint<G, OT, NW>(envs, te_valid, tile, G::OBS, wave, lane);
     __syncthreads();
-    copy_tile(tile, obs + (size_t)e0 * 2 * HN_OBS, 2 * te_valid * HN_OBS, tid, NTHREADS);
+    copy_tile(tile, obs + (size_t)e0 * 2 * G::OBS, 2 * te_valid * G::OBS, tid, NTHREADS);
   }
-  if (legal) hn_write_legal<NTHREADS>(envs, te_valid, legal + (size_t)e0 * 2 * HN_NACT, tid);
+  if (legal) hn_write_legal<G, NTHREADS>(envs, te_valid, legal + (size_t)e0 * 2 * G::NACT, tid);
 }
 
 // ---------------------------------------------------------- env-only ----
 
-template <typename OT, int TE>
+template <class G, typename OT, int TE>
 __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* __restrict__ state, uint64_t t0,
                                                           int n_steps, const int32_t* __restrict__ actions,
                                                           OT* __restrict__ obs, float* __restrict__ reward,
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
   __shared__ HnTile envs[TE];
   __shared__ uint32_t need[TE + 1];  // per env, then "any" at [TE]
   __shared__ uint32_t words[TE][HN_DECK_WORDS];
-  __shared__ __align__(16) OT tile[2 * TE * HN_OBS];
+  __shared__ __align__(16) OT tile[2 * TE * G::OBS];
   __shared__ int32_t act_lds[ACT_CHUNK * TE * 2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
@@ -163,31 +164,31 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
       uint32_t d = 0;
       if (envlane) {
         float r;
-        hn_transition(p, s, act_lds[kk * TE * 2 + tid * 2 + s.cur], r, d);
+        hn_transition<G>(p, s, act_lds[kk * TE * 2 + tid * 2 + s.cur], r, d);
         need[tid] = d;
-        if (!d) hn_publish(s, envs[tid]);
+        if (!d) hn_publish<G>(s, envs[tid]);
         if (reward) reward[(size_t)k * E + e] = r;
         if (done) done[(size_t)k * E + e] = (uint8_t)d;
       }
       hn_flag_any(need, TE, d, wave, lane);
       __syncthreads();
       if (need[TE]) {  // some game of the tile ended: deal new ones drawn at t + 1
-        hn_shuffle_flagged<NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
+        hn_shuffle_flagged<G, NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
         __syncthreads();
         if (d) {
-          hn_deal(s, words[tid]);
-          hn_publish(s, envs[tid]);
+          hn_deal<G>(s, words[tid]);
+          hn_publish<G>(s, envs[tid]);
         }
         __syncthreads();
       }
       if (obs) {
-        hn_build_bits<TE, NTHREADS>(envs, te_valid, tid);
+        hn_build_bits<G, TE, NTHREADS>(envs, te_valid, tid);
         __syncthreads();
-        hn_paint<OT, NW>(envs, te_valid, tile, HN_OBS, wave, lane);
+        hn_paint<G, OT, NW>(envs, te_valid, tile, G::OBS, wave, lane);
         __syncthreads();
-        copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * HN_OBS, 2 * te_valid * HN_OBS, tid, NTHREADS);
+        copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * G::OBS, 2 * te_valid * G::OBS, tid, NTHREADS);
       }
-      if (legal) hn_write_legal<NTHREADS>(envs, te_valid, legal + ((size_t)k * E + e0) * 2 * HN_NACT, tid);
+      if (legal) hn_write_legal<G, NTHREADS>(envs, te_valid, legal + ((size_t)k * E + e0) * 2 * G::NACT, tid);
       __syncthreads();  // the tile and masks are read before the next move rewrites them
     }
   }
@@ -203,10 +204,10 @@ struct HnRunLayout {
   size_t off_x, off_h1, off_h2, off_lg, off_sc, off_env, off_words, off_need, off_rows, total;
 };
 
-__host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt) {
+__host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int obs) {
   HnRunLayout L;
   const size_t es = dt == DT_F32 ? 4 : 2;
-  L.ldx = dt == DT_F32 ? lds_ld<DT_F32>(HN_OBS) : lds_ld<DT_BF16>(HN_OBS);
+  L.ldx = dt == DT_F32 ? lds_ld<DT_F32>(obs) : lds_ld<DT_BF16>(obs);
   L.ld1 = dt == DT_F32 ? lds_ld<DT_F32>(H1) : lds_ld<DT_BF16>(H1);
   L.ld2 = dt == DT_F32 ? lds_ld<DT_F32>(H2) : lds_ld<DT_BF16>(H2);
   size_t o = 0;
@@ -224,16 +225,16 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt) {
   return L;
 }
 
-size_t hn_run_lds_bytes(const PolicyArgs& pol) { return hn_run_layout(pol.H1, pol.H2, pol.dt).total; }
+size_t hn_run_lds_bytes(const PolicyArgs& pol) { return hn_run_layout(pol.H1, pol.H2, pol.dt, pol.D).total; }
 
-template <int DT>
+template <class G, int DT>
 __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs pol, int32_t* __restrict__ state,
                                                           uint64_t t0, int n_steps, TrajArgs out) {
   using T = typename DType<DT>::T;
-  constexpr int TE = HN_RUN_TE, NA = HN_NACT, NW = NTHREADS / 64;
-  constexpr int LDX = lds_ld<DT>(HN_OBS);
+  constexpr int TE = HN_RUN_TE, NA = G::NACT, NW = NTHREADS / 64;
+  constexpr int LDX = lds_ld<DT>(G::OBS);
   extern __shared__ __align__(16) uint8_t smem[];
-  const HnRunLayout L = hn_run_layout(pol.H1, pol.H2, DT);
+  const HnRunLayout L = hn_run_layout(pol.H1, pol.H2, DT, G::OBS);
   T* xs = reinterpret_cast<T*>(smem + L.off_x);
   T* h1 = reinterpret_cast<T*>(smem + L.off_h1);
   T* h2 = reinterpret_cast<T*>(smem + L.off_h2);
@@ -259,17 +260,17 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
   HnEnv s;
   if (envlane) {
     hn_load(state, E, e, s);
-    hn_publish(s, envs[tid]);
+    hn_publish<G>(s, envs[tid]);
   }
   if (tid < TE) rows[tid] = 2 * tid + (envlane ? s.cur : 0);  // the mover's row (a zero row for padding)
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     __syncthreads();  // the previous move's games are published
-    hn_build_bits<TE, NTHREADS>(envs, te_valid, tid);
+    hn_build_bits<G, TE, NTHREADS>(envs, te_valid, tid);
     __syncthreads();
-    hn_paint<T, NW>(envs, te_valid, xs, LDX, wave, lane);
+    hn_paint<G, T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
-    mlp_input_layer_const<DT, HN_OBS>(xs, LDX, rows, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane);
+    mlp_input_layer_const<DT, G::OBS>(xs, LDX, rows, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane);
     __syncthreads();
     mlp_hidden<DT>(h1, L.ld1, TE, pol.H1, W2, b2, pol.H2, h2, L.ld2, wave, NW, lane);
     __syncthreads();
@@ -290,7 +291,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
     // The trajectory copy of o_t is issued after the step's weight loads: a
     // wave's loads wait for its earlier stores (one in-order counter).
     if (out.obs)
-      copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * HN_OBS, HN_OBS,
+      copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * G::OBS, G::OBS,
                          2 * te_valid, tid, NTHREADS);
     __syncthreads();
     uint32_t d = 0;
@@ -309,10 +310,10 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
         out.actions[((size_t)k * E + e) * 2 + 1 - s.cur] = 0;
       }
       float r;
-      hn_transition(p, s, best, r, d);
+      hn_transition<G>(p, s, best, r, d);
       need[tid] = d;
       if (!d) {
-        hn_publish(s, envs[tid]);
+        hn_publish<G>(s, envs[tid]);
         rows[tid] = 2 * tid + s.cur;
       }
       if (out.reward) out.reward[(size_t)k * E + e] = r;
@@ -321,22 +322,22 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
     hn_flag_any(need, TE, d, wave, lane);
     __syncthreads();
     if (need[TE]) {
-      hn_shuffle_flagged<NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
+      hn_shuffle_flagged<G, NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
       __syncthreads();
       if (d) {
-        hn_deal(s, words[tid]);
-        hn_publish(s, envs[tid]);
+        hn_deal<G>(s, words[tid]);
+        hn_publish<G>(s, envs[tid]);
         rows[tid] = 2 * tid + s.cur;
       }
     }
   }
   __syncthreads();
   if (out.obs_last) {
-    hn_build_bits<TE, NTHREADS>(envs, te_valid, tid);
+    hn_build_bits<G, TE, NTHREADS>(envs, te_valid, tid);
     __syncthreads();
-    hn_paint<T, NW>(envs, te_valid, xs, LDX, wave, lane);
+    hn_paint<G, T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
-    copy_rows_global16(xs, LDX, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * HN_OBS, HN_OBS, 2 * te_valid,
+    copy_rows_global16(xs, LDX, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * G::OBS, G::OBS, 2 * te_valid,
                        tid, NTHREADS);
   }
   if (envlane) hn_store(state, E, e, s);
@@ -348,38 +349,60 @@ constexpr int HN_ENV_TE = 8;  // envs per workgroup of the init and env-only ker
 
 static dim3 hn_tiles(int E, int te) { return dim3((unsigned)((E + te - 1) / te)); }
 
-hipError_t launch_hn_init(const HnParams& p, int32_t* state, void* obs, int obs_dt, uint8_t* legal, hipStream_t s) {
+template <class G>
+static hipError_t launch_hn_init_g(const HnParams& p, int32_t* state, void* obs, int obs_dt, uint8_t* legal,
+                                   hipStream_t s) {
   if (obs_dt == DT_F32)
-    hn_init_kernel<float, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(p, state, static_cast<float*>(obs),
-                                                                                  legal);
+    hn_init_kernel<G, float, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(
+        p, state, static_cast<float*>(obs), legal);
   else
-    hn_init_kernel<uint16_t, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(
+    hn_init_kernel<G, uint16_t, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(
         p, state, static_cast<uint16_t*>(obs), legal);
   return hipGetLastError();
 }
 
-hipError_t launch_hn_step(const HnParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,
-                          void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s) {
+template <class G>
+static hipError_t launch_hn_step_g(const HnParams& p, int32_t* state, uint64_t t0, int n_steps,
+                                   const int32_t* actions, void* obs, int obs_dt, float* reward, uint8_t* done,
+                                   uint8_t* legal, hipStream_t s) {
   if (obs_dt == DT_F32)
-    hn_env_kernel<float, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(
+    hn_env_kernel<G, float, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(
         p, state, t0, n_steps, actions, static_cast<float*>(obs), reward, done, legal);
   else
-    hn_env_kernel<uint16_t, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(
+    hn_env_kernel<G, uint16_t, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(
         p, state, t0, n_steps, actions, static_cast<uint16_t*>(obs), reward, done, legal);
   return hipGetLastError();
 }
 
-hipError_t launch_hn_run(const HnParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
-                         const TrajArgs& out, hipStream_t s) {
+template <class G>
+static hipError_t launch_hn_run_g(const HnParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0,
+                                  int n_steps, const TrajArgs& out, hipStream_t s) {
   const size_t lds = hn_run_lds_bytes(pol);
-  const void* fn = pol.dt == DT_F32 ? (const void*)hn_run_kernel<DT_F32> : (const void*)hn_run_kernel<DT_BF16>;
+  const void* fn = pol.dt == DT_F32 ? (const void*)hn_run_kernel<G, DT_F32> : (const void*)hn_run_kernel<G, DT_BF16>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   if (pol.dt == DT_F32)
-    hn_run_kernel<DT_F32><<<hn_tiles(p.E, HN_RUN_TE), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
+    hn_run_kernel<G, DT_F32><<<hn_tiles(p.E, HN_RUN_TE), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
   else
-    hn_run_kernel<DT_BF16><<<hn_tiles(p.E, HN_RUN_TE), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
+    hn_run_kernel<G, DT_BF16><<<hn_tiles(p.E, HN_RUN_TE), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
+}
+
+hipError_t launch_hn_init(const HnParams& p, int32_t* state, void* obs, int obs_dt, uint8_t* legal, hipStream_t s) {
+  return p.mini ? launch_hn_init_g<HnMini>(p, state, obs, obs_dt, legal, s)
+                : launch_hn_init_g<HnStd>(p, state, obs, obs_dt, legal, s);
+}
+
+hipError_t launch_hn_step(const HnParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,
+                          void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s) {
+  return p.mini ? launch_hn_step_g<HnMini>(p, state, t0, n_steps, actions, obs, obs_dt, reward, done, legal, s)
+                : launch_hn_step_g<HnStd>(p, state, t0, n_steps, actions, obs, obs_dt, reward, done, legal, s);
+}
+
+hipError_t launch_hn_run(const HnParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0, int n_steps,
+                         const TrajArgs& out, hipStream_t s) {
+  return p.mini ? launch_hn_run_g<HnMini>(p, pol, state, t0, n_steps, out, s)
+                : launch_hn_run_g<HnStd>(p, pol, state, t0, n_steps, out, s);
 }
 
 }  // namespace rl

@@ -168,10 +168,11 @@ def overcooked_config(n_envs, cook_time=20, soup_reward=20, max_steps=400, env_b
                      extra={"oc_cook_time": cook_time, "oc_soup_reward": soup_reward})
 
 
-def hanabi_config(n_envs, max_steps=1000, env_base=0, seed=0):
-    """An ``EnvConfig`` for two-player Hanabi (5 colours x 5 ranks, hands of 5, 8 info tokens, 3 lives)."""
+def hanabi_config(n_envs, max_steps=1000, env_base=0, seed=0, colours=5, ranks=5):
+    """An ``EnvConfig`` for two-player Hanabi: the standard 5 colours x 5 ranks game, or with colours=ranks=3
+    the mini game (hands of 5, 8 info tokens, 3 lives either way)."""
     return EnvConfig(n_envs, kind=RL_ENV_HANABI, n_agents=2, max_steps=max_steps, env_base=env_base, seed=seed,
-                     extra={"hn_colors": 5, "hn_ranks": 5, "hn_hand_size": 5, "hn_info_tokens": 8,
+                     extra={"hn_colors": colours, "hn_ranks": ranks, "hn_hand_size": 5, "hn_info_tokens": 8,
                             "hn_life_tokens": 3})
 
 

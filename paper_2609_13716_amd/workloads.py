@@ -68,6 +68,8 @@ WORKLOADS = {
                     n_envs=4096, n_steps=400, hidden=(256, 256), dtypes=("bf16",)),
     "hn_4096": dict(kind="hanabi", env=dict(max_steps=1000), n_envs=4096, n_steps=80, hidden=(512, 512),
                     dtypes=("bf16",)),
+    "hn_mini_4096": dict(kind="hanabi", env=dict(max_steps=1000, colours=3, ranks=3), n_envs=4096, n_steps=80,
+                         hidden=(256, 256), dtypes=("bf16",)),
     "lbf8_4096_ac": dict(env=dict(grid_h=8, grid_w=8, n_agents=2, n_food=3, max_agent_level=2, max_food_level=3,
                                   max_steps=50),
                          n_envs=4096, n_steps=128, hidden=(128, 128), dtypes=("bf16",), value_head=True,
@@ -100,6 +102,8 @@ def policy_dims(name):
     if kind(name) == "overcooked":
         return (OC_OBS_DIM, *w["hidden"], OC_ACTIONS)
     if kind(name) == "hanabi":
+        if w["env"].get("colours") == 3:  # the mini game: 278 features, 16 actions
+            return (278, *w["hidden"], 16)
         return (HN_OBS_DIM, *w["hidden"], HN_ACTIONS)
     return (lbf_obs_dim(w["env"]), *w["hidden"], LBF_ACTIONS)
 

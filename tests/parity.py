@@ -127,7 +127,9 @@ def oc_state_tuple(s):
 
 
 def hn_oracle_cfg(cfg):
-    return hanabi.Config(max_steps=cfg.max_steps)
+    x = cfg.extra
+    return hanabi.Config(colours=x["hn_colors"], ranks=x["hn_ranks"], hand_size=x["hn_hand_size"],
+                         max_steps=cfg.max_steps)
 
 
 def _hn_last_from_word(L):
@@ -160,9 +162,10 @@ def hn_states_from_device(cfg, state):
     """Oracle Hanabi State objects from a device (or host) state buffer."""
     from paper_2609_13716_amd import rollout as R
     v = {k: t.cpu().numpy().astype(np.int64) & 0xFFFFFFFF for k, t in R.hn_state_planes(cfg, state.cpu()).items()}
+    oc = hn_oracle_cfg(cfg)
     out = []
     for e in range(cfg.n_envs):
-        deck = [(int(v["deck"][k // 4, e]) >> (8 * (k % 4))) & 0xFF for k in range(50)]
+        deck = [(int(v["deck"][k // 4, e]) >> (8 * (k % 4))) & 0xFF for k in range(oc.n_cards)]
         hands, know = [], []
         for p in range(2):
             n = int(v["n"][p, e])
@@ -171,10 +174,10 @@ def hn_states_from_device(cfg, state):
                                           ((int(v["hc"][p, e]) >> (3 * i)) & 7) - 1,
                                           ((int(v["hr"][p, e]) >> (3 * i)) & 7) or -1) for i in range(n)])
         disc = [(int(v["disc0"][e]) >> (2 * c)) & 3 if c < 16 else (int(v["disc1"][e]) >> (2 * (c - 16))) & 3
-                for c in range(25)]
+                for c in range(oc.colours * oc.ranks)]
         tl = int(v["turns_left"][e])
         out.append(hanabi.State(deck, int(v["next"][e]), hands, know, [(int(v["fw"][e]) >> (3 * c)) & 7
-                                                                        for c in range(5)],
+                                                                        for c in range(oc.colours)],
                                 disc, int(v["info"][e]), int(v["lives"][e]), int(v["cur"][e]),
                                 tl - (1 << 32) if tl >= 1 << 31 else tl, _hn_last_from_word(int(v["last"][e])),
                                 int(v["steps"][e])))
@@ -188,7 +191,7 @@ def hn_states_to_device(cfg, states, device="cuda"):
     for k, (_, n) in R.HN_FIELDS.items():
         pl[k] = np.zeros((n, E), np.int64) if n > 1 else np.zeros(E, np.int64)
     for e, s in enumerate(states):
-        for k in range(50):
+        for k in range(len(s.deck)):
             pl["deck"][k // 4, e] |= s.deck[k] << (8 * (k % 4))
         for p in range(2):
             pl["n"][p, e] = len(s.hands[p])
@@ -199,8 +202,8 @@ def hn_states_to_device(cfg, states, device="cuda"):
                 pl["hc"][p, e] |= (kn.hint_colour + 1) << (3 * i)
                 pl["hr"][p, e] |= max(kn.hint_rank, 0) << (3 * i)
         pl["fw"][e] = sum(f << (3 * c) for c, f in enumerate(s.fireworks))
-        pl["disc0"][e] = sum(s.discards[c] << (2 * c) for c in range(16))
-        pl["disc1"][e] = sum(s.discards[c] << (2 * (c - 16)) for c in range(16, 25))
+        pl["disc0"][e] = sum(s.discards[c] << (2 * c) for c in range(min(16, len(s.discards))))
+        pl["disc1"][e] = sum(s.discards[c] << (2 * (c - 16)) for c in range(16, len(s.discards)))
         pl["info"][e], pl["lives"][e], pl["cur"][e] = s.info, s.lives, s.cur
         pl["turns_left"][e], pl["next"][e], pl["steps"][e] = s.turns_left, s.next_card, s.step_count
         pl["last"][e] = _hn_last_to_word(s.last)

@@ -89,6 +89,10 @@ def test_hanabi_config_checks():
     cfg = R.hanabi_config(100)
     assert R.rl_obs_dim(cfg) == 658 and R.rl_num_actions(cfg) == 20
     assert R.rl_state_bytes(cfg) == 35 * 100 * 4
+    mini = R.hanabi_config(16, colours=3, ranks=3)
+    assert R.rl_obs_dim(mini) == 278 and R.rl_num_actions(mini) == 16 and R.rl_state_bytes(mini) == 35 * 16 * 4
+    bad = R.hanabi_config(16, colours=3, ranks=5)
+    assert R.rl_obs_dim(bad) == R.RL_EUNSUPPORTED
     for name, v, code in (("hn_colors", 4, R.RL_EUNSUPPORTED), ("hn_hand_size", 4, R.RL_EUNSUPPORTED),
                           ("hn_life_tokens", 0, R.RL_EINVAL), ("n_agents", 3, R.RL_EINVAL),
                           ("grid_w", 3, R.RL_EINVAL), ("oc_cook_time", 20, R.RL_EINVAL),
