@@ -658,8 +658,69 @@ __device__ __forceinline__ void lbf_paint_tile(const LbfEnv& s, int el, T* xs, i
 template <typename T, int R, int D, int LDX, int NT, bool CLEAR = false, int G = 4>
 __device__ __forceinline__ void copy_obs_rows(T* xs, T* __restrict__ g, int rows_live, int tid) {
   constexpr int VE = 16 / sizeof(T);
-  static_assert(D % VE == 0, "observation rows must be whole 16-byte vectors");
-  constexpr int VPR = D / VE;
+  if constexpr (D % VE != 0) {
+    // Rows that are not whole vectors (e.g. the 7x7 grid's 147 features): the
+    // tile's rows are contiguous in global memory, so the tile goes out as
+    // R * D elements in 16-byte vectors, each gathered element by element
+    // from the (padded) LDS rows; the vector that ends the live rows is
+    // stored element by element.
+    static_assert((R * D) % VE == 0, "the tile must be whole 16-byte vectors");
+    constexpr int NV = R * D / VE;
+    constexpr int IT = (NV + NT - 1) / NT;
+    const int nlive = rows_live * D;
+#pragma unroll
+    for (int i0 = 0; i0 < IT; i0 += G) {
+      uint32_t w[G][4];
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const int v = tid + (i0 + j) * NT;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) w[j][q] = 0u;
+        if (i0 + j < IT && (NV % NT == 0 || v < NV)) {
+#pragma unroll
+          for (int q = 0; q < VE; ++q) {
+            const int el = v * VE + q, r = el / D, c = el - r * D;
+            const T x = xs[r * LDX + c];
+            if constexpr (sizeof(T) == 2)
+              w[j][q >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, x) << (16 * (q & 1));
+            else
+              w[j][q] = __builtin_bit_cast(uint32_t, x);
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const int v = tid + (i0 + j) * NT;
+        const int e0 = v * VE;
+        if (i0 + j < IT && (NV % NT == 0 || v < NV) && e0 < nlive) {
+          if (g) {
+            if (e0 + VE <= nlive) {
+              *reinterpret_cast<u32x4*>(g + e0) = u32x4{w[j][0], w[j][1], w[j][2], w[j][3]};
+            } else {
+#pragma unroll
+              for (int q = 0; q < VE; ++q)
+                if (e0 + q < nlive) {
+                  const uint32_t bits = sizeof(T) == 2 ? (w[j][q >> 1] >> (16 * (q & 1))) & 0xffffu : w[j][q];
+                  if constexpr (sizeof(T) == 2)
+                    g[e0 + q] = __builtin_bit_cast(T, (uint16_t)bits);
+                  else
+                    g[e0 + q] = __builtin_bit_cast(T, bits);
+                }
+            }
+          }
+          if constexpr (CLEAR) {
+#pragma unroll
+            for (int q = 0; q < VE; ++q) {
+              const int el = e0 + q, r = el / D, c = el - r * D;
+              if (el < nlive) xs[r * LDX + c] = (T)0;
+            }
+          }
+        }
+      }
+    }
+    return;
+  }
+  constexpr int VPR = D / VE > 0 ? D / VE : 1;
   constexpr int NV = R * VPR;
   constexpr int IT = (NV + NT - 1) / NT;
 #pragma unroll
@@ -1050,6 +1111,7 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
   RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1, 0)
   RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2, 0)
   RL_REG_CASE(DT_BF16, 12, 12, 256, 256, 3, 6, 16, 8, 1, 0)
+  RL_REG_CASE(DT_BF16, 7, 7, 128, 128, 2, 3, 8, 4, 2, 0)
   RL_REG_CASE(DT_F32, 8, 8, 64, 64, 2, 3, 8, 4, 2, 1)
   RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2, 1)
   RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1, 1)
@@ -1184,6 +1246,13 @@ static bool try_launch_env_ct(const LbfParams& p, int32_t* state, uint64_t t0, i
     *err = obs_dt == DT_F32 ? launch_env_ct<float, 8, 8, 2, 3, 8>(p, state, t0, n_steps, actions, obs, reward, done,
                                                                    legal, s)
                             : launch_env_ct<uint16_t, 8, 8, 2, 3, 8>(p, state, t0, n_steps, actions, obs, reward,
+                                                                      done, legal, s);
+    return true;
+  }
+  if (p.H == 7 && p.W == 7 && p.A == 2 && p.F == 3) {
+    *err = obs_dt == DT_F32 ? launch_env_ct<float, 7, 7, 2, 3, 8>(p, state, t0, n_steps, actions, obs, reward, done,
+                                                                   legal, s)
+                            : launch_env_ct<uint16_t, 7, 7, 2, 3, 8>(p, state, t0, n_steps, actions, obs, reward,
                                                                       done, legal, s);
     return true;
   }

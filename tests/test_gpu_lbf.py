@@ -99,6 +99,8 @@ def test_init_matches_oracle(dtype):
     (dict(n_envs=5, grid_h=3, grid_w=3, n_agents=2, n_food=1, max_steps=7), 40, torch.float32),
     (dict(n_envs=23, grid_h=7, grid_w=7, n_agents=2, n_food=3, max_agent_level=1, max_food_level=2,
           const_levels=True), 90, torch.bfloat16),
+    (dict(n_envs=19, grid_h=7, grid_w=7, n_agents=2, n_food=3, max_agent_level=2, max_food_level=3), 70,
+     torch.float32),
 ])
 def test_env_only_parity(cfgkw, T, dtype):
     require_gpu()
