@@ -792,7 +792,10 @@ __device__ __forceinline__ float row_log_pi(const float (&logit)[4], int g, int 
 // VH: layer 3 has one more output, the value head V(o) of an actor-critic
 // network, written with log pi of each sampled action and, after the last
 // step, V of the final observation.
-template <int DT, int GH, int GW, int H1, int H2, int NA, int A, int F, int TE, int NW, int MINB, bool VH = false>
+// TM: agents whose teammates entry is a heuristic kind act with that
+// heuristic (evaluated by the env lanes) instead of the network.
+template <int DT, int GH, int GW, int H1, int H2, int NA, int A, int F, int TE, int NW, int MINB, bool VH = false,
+          bool TM = false>
 __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p, PolicyArgs pol,
                                                                     int32_t* __restrict__ state, uint64_t t0,
                                                                     int n_steps, TrajArgs out) {
@@ -818,6 +821,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   constexpr int NOUT = NA + (VH ? 1 : 0);  // layer-3 outputs: the actions, then the value
   static_assert(NA <= 8 && NOUT <= 8, "one Philox block of action noise per row; outputs in two lane groups");
   static_assert(!(VH && LEAN), "the value head runs on shapes whose env state stays in registers");
+  static_assert(!(VH && TM), "heuristic teammates run without the value head");
   static_assert(TE <= 64, "env lanes live in wave 0");
   static_assert(TE * ((2 * A + 2 * F + 7) / 8) <= 64, "one lane per reset block");
 
@@ -831,6 +835,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];    // reset draws of envs being reset
   __shared__ __align__(16) float bias_s[LEAN ? H1 + H2 : 4];
   __shared__ LbfEnv env_s[LEAN ? TE : 1];
+  __shared__ int tk_s[TM ? RP : 1];  // TM: heuristic kind of each row (-1: the network)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE;
@@ -869,6 +874,12 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     b3r[r] = act < NOUT ? DType<DT>::to_f32(static_cast<const T*>(pol.b[2])[act]) : 0.f;
   }
 
+  if constexpr (TM) {
+    for (int row = tid; row < RP; row += NT) {
+      const int kd = row < te_valid * A ? out.teammates[(size_t)e0 * A + row] : -1;
+      tk_s[row] = (kd >= 0 && kd < LBF_NHEUR) ? kd : -1;
+    }
+  }
   // zero the operand tiles (their K padding and unused rows stay zero)
   for (int i = tid; i < RP * LDX; i += NT) xs[i] = (T)0;
   for (int i = tid; i < RP * LD1; i += NT) h1s[i] = (T)0;
@@ -980,9 +991,10 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
           best_a = take ? oa : best_a;
         }
         const bool live = row < te_valid * A;
+        const bool heur = TM && live && tk_s[TM ? row : 0] >= 0;  // written by the env lane below
         if (live && g == 0) {
           if constexpr (!DIRECT) act_s[row] = best_a;
-          if (out.actions) out.actions[((size_t)k * E + e0) * A + row] = best_a;
+          if (out.actions && !heur) out.actions[((size_t)k * E + e0) * A + row] = best_a;
         }
         if constexpr (VH) {
           const size_t gr = ((size_t)k * E + e0) * A + row;
@@ -998,7 +1010,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
           if constexpr (A > 2) act_d[2] = __builtin_amdgcn_update_dpp(0, best_a, 0x102, 0xf, 0xf, false);
           if constexpr (A > 3) act_d[3] = __builtin_amdgcn_update_dpp(0, best_a, 0x103, 0xf, 0xf, false);
         }
-        if (out.logits && live && g < 2) {
+        if (out.logits && live && g < 2 && !heur) {
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             if (4 * g + r < NA) out.logits[(((size_t)k * E + e0) * A + row) * NA + 4 * g + r] = logit[r];
@@ -1015,6 +1027,20 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
             act[i] = act_d[i];
           else
             act[i] = i < A ? act_s[lane * A + i] : 0;
+        }
+        if constexpr (TM) {  // heuristic agents: their action, and logits 0 for it / -inf for the others
+#pragma unroll
+          for (int i = 0; i < A; ++i) {
+            const int kd = tk_s[el * A + i];
+            if (kd >= 0) {
+              act[i] = lbf_heuristic_action(p, s, i, kd);
+              const size_t gr = ((size_t)k * E + e) * A + i;
+              if (out.actions) out.actions[gr] = act[i];
+              if (out.logits)
+#pragma unroll
+                for (int a = 0; a < NA; ++a) out.logits[gr * NA + a] = a == act[i] ? 0.f : -INFINITY;
+            }
+          }
         }
         lbf_transition<A, F, GH, GW>(p, s, act, r, d);
       }
@@ -1085,10 +1111,10 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
 // Compile-time shapes that run on lbf_rollout_kernel (everything else uses
 // lbf_run_kernel): LBF 8x8 with 2 agents and 3 foods (obs 192) under 64- and
 // 128-wide layers.
-template <int DT, int GH, int GW, int H1, int H2, int A, int F, int TE, int NW, int MINB, bool VH>
+template <int DT, int GH, int GW, int H1, int H2, int A, int F, int TE, int NW, int MINB, bool VH, bool TM>
 static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic&, const PolicyArgs& pol, int32_t* state,
                                      uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s) {
-  auto kern = lbf_rollout_kernel<DT, GH, GW, H1, H2, LBF_NACT, A, F, TE, NW, MINB, VH>;
+  auto kern = lbf_rollout_kernel<DT, GH, GW, H1, H2, LBF_NACT, A, F, TE, NW, MINB, VH, TM>;
   const dim3 grid((unsigned)((p.E + TE - 1) / TE));
   kern<<<grid, NW * 64, 0, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
@@ -1096,14 +1122,17 @@ static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic&, const 
 
 static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const PolicyArgs& pol, int32_t* state,
                                    uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s, hipError_t* err) {
-  if (pol.NA != LBF_NACT + pol.VH || out.teammates) return false;
-#define RL_REG_CASE(DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV, VHV)                                    \
+  if (pol.NA != LBF_NACT + pol.VH) return false;
+  const bool tm = out.teammates != nullptr;
+#define RL_REG_CASE_T(DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV, VHV, TMV)                              \
   if (pol.dt == DTV && p.H == GHV && p.W == GWV && pol.H1 == H1V && pol.H2 == H2V && p.A == AV &&            \
-      p.F == FV && pol.VH == VHV) {                                                                          \
-    *err = launch_rollout_reg<DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV, VHV>(p, m, pol, state, t0,    \
-                                                                                     n_steps, out, s);       \
+      p.F == FV && pol.VH == VHV && tm == TMV) {                                                             \
+    *err = launch_rollout_reg<DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV, VHV, TMV>(p, m, pol, state,   \
+                                                                                          t0, n_steps, out, s); \
     return true;                                                                                             \
   }
+#define RL_REG_CASE(DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV, VHV) \
+  RL_REG_CASE_T(DTV, GHV, GWV, H1V, H2V, AV, FV, TEV, NWV, MINBV, VHV, false)
   // (dtype, grid rows, grid cols, hidden, hidden, agents, foods, envs per workgroup, waves, workgroups per CU,
   //  value head)
   RL_REG_CASE(DT_F32, 8, 8, 64, 64, 2, 3, 8, 4, 2, 0)
@@ -1116,7 +1145,13 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
   RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2, 1)
   RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1, 1)
   RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2, 1)
+  // (heuristic teammates)
+  RL_REG_CASE_T(DT_BF16, 7, 7, 128, 128, 2, 3, 8, 4, 2, 0, true)
+  RL_REG_CASE_T(DT_BF16, 7, 7, 64, 64, 2, 3, 8, 4, 2, 0, true)
+  RL_REG_CASE_T(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2, 0, true)
+  RL_REG_CASE_T(DT_F32, 8, 8, 64, 64, 2, 3, 8, 4, 2, 0, true)
 #undef RL_REG_CASE
+#undef RL_REG_CASE_T
   return false;
 }
 
