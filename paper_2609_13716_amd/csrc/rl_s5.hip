@@ -76,8 +76,10 @@ __host__ __device__ inline S5Lds s5_lds(int D, int H, int P) {
   S5Lds L;
   L.ldx = lds_ld<DT_BF16>(D);
   L.ldu = lds_ld<DT_BF16>(H);
-  L.ldf = H + 1;       // odd strides: the float32 operand rows of a 16-row tile start on different banks
-  L.ldxf = 2 * P + 1;  // state tile: real parts, then imaginary parts
+  // float32 operand rows: a stride of 2 (mod 32) words puts the 16 rows x 2 k
+  // of each half-wave's MFMA operand reads on 32 distinct banks
+  L.ldf = round_up(H, 32) + 2;
+  L.ldxf = round_up(2 * P, 32) + 2;  // state tile: real parts, then imaginary parts
   const size_t r0 = (size_t)S5_RT * (L.ldx * 2 > L.ldf * 4 ? L.ldx * 2 : L.ldf * 4);
   L.off_u = (r0 + 15) / 16 * 16;
   L.off_xf = (L.off_u + (size_t)S5_RT * L.ldu * 2 + 15) / 16 * 16;
@@ -264,22 +266,25 @@ __global__ __launch_bounds__(S5_NT, 2) void s5_head_gemm_kernel(HeadGemmArgs g) 
   const uint16_t* __restrict__ W = g.w[z];
   const int wm = wave >> 1, wn = wave & 1;
 
-  u32x4 ra[4], rb[4];
-  auto gload = [&](int k0) {
+  // Two register stages: the global loads of stage s + 2 are issued before
+  // stage s's MFMAs and reach LDS after stage s + 1's, so each load has two
+  // stages of MFMA work to arrive in.
+  u32x4 ra0[4], rb0[4], ra1[4], rb1[4];
+  auto gload = [&](int k0, u32x4(&A4)[4], u32x4(&B4)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int q = tid + S5_NT * i, row = q >> 3, c = q & 7;
       const int ar = min(m0 + row, g.M - 1);
-      ra[i] = *reinterpret_cast<const u32x4*>(A + (size_t)ar * g.lda + k0 + c * 8);
-      rb[i] = *reinterpret_cast<const u32x4*>(W + (size_t)(n0 + row) * g.K + k0 + c * 8);
+      A4[i] = *reinterpret_cast<const u32x4*>(A + (size_t)ar * g.lda + k0 + c * 8);
+      B4[i] = *reinterpret_cast<const u32x4*>(W + (size_t)(n0 + row) * g.K + k0 + c * 8);
     }
   };
-  auto lstore = [&](int buf) {
+  auto lstore = [&](int buf, const u32x4(&A4)[4], const u32x4(&B4)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int q = tid + S5_NT * i, row = q >> 3, c = q & 7;
-      *reinterpret_cast<u32x4*>(&sa[buf][hg_off(row, c)]) = ra[i];
-      *reinterpret_cast<u32x4*>(&sb[buf][hg_off(row, c)]) = rb[i];
+      *reinterpret_cast<u32x4*>(&sa[buf][hg_off(row, c)]) = A4[i];
+      *reinterpret_cast<u32x4*>(&sb[buf][hg_off(row, c)]) = B4[i];
     }
   };
   f32x4 acc[4][4];
@@ -287,14 +292,7 @@ __global__ __launch_bounds__(S5_NT, 2) void s5_head_gemm_kernel(HeadGemmArgs g) 
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  const int nk = g.K / HG_BK;
-  for (int s = 0; s < nk; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nk) gload((s + 1) * HG_BK);
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       const int c = kk * 4 + (lane >> 4);
@@ -314,8 +312,25 @@ __global__ __launch_bounds__(S5_NT, 2) void s5_head_gemm_kernel(HeadGemmArgs g) 
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[j][i] = mfma_step(fw[j], fx[i], acc[j][i]);
     }
-    if (s + 1 < nk) lstore(buf ^ 1);
+  };
+
+  const int nk = g.K / HG_BK;  // >= 1
+  gload(0, ra0, rb0);
+  if (nk > 1) gload(HG_BK, ra1, rb1);
+  lstore(0, ra0, rb0);
+  __syncthreads();
+  for (int s = 0; s < nk; s += 2) {
+    // LDS buffer 0 holds stage s, registers 1 stage s + 1
+    if (s + 2 < nk) gload((s + 2) * HG_BK, ra0, rb0);
+    compute(0);
+    if (s + 1 < nk) lstore(1, ra1, rb1);
     __syncthreads();
+    if (s + 1 < nk) {
+      if (s + 3 < nk) gload((s + 3) * HG_BK, ra1, rb1);
+      compute(1);
+      if (s + 2 < nk) lstore(0, ra0, rb0);
+      __syncthreads();
+    }
   }
 
   const uint16_t* __restrict__ bias = g.b[z];
