@@ -262,8 +262,9 @@ rl_status rollout_run_teams(const rl_env_config* cfg, const rl_policy* policy, c
  * rounded to bfloat16; the S5 parameters and state are float32.  Every
  * pointer is device memory, 16-byte aligned.
  * Limits: dtype RL_BF16; H a multiple of 64 in 64..256; P a multiple of 16 in
- * 16..256; F a multiple of 128 in 128..4096; nA in 1..16; D (the env's
- * observation size) at most 1024. */
+ * 16..128; F a multiple of 128 in 128..4096; nA in 1..16; D (the env's
+ * observation size) at most 1024, and the encoder/S5 tile within 160 KiB of
+ * LDS (RL_EUNSUPPORTED otherwise; D 192, H 128, P 128 takes 128 KiB). */
 typedef struct {
   int32_t dtype;       /* RL_BF16 */
   int32_t obs_dim;     /* D, must equal rl_obs_dim(cfg) */

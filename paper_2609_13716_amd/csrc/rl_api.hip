@@ -357,7 +357,7 @@ static rl_status check_s5(const rl_env_config* cfg, const rl_s5_policy* pol, Env
   if (pol->dtype != RL_BF16) return fail(RL_EUNSUPPORTED, "the S5 policy runs in bfloat16 only");
   const int H = pol->d_model, P = pol->d_state, F = pol->head_width, NA = pol->n_actions;
   if (H < 64 || H > 256 || H % 64) return fail(RL_EUNSUPPORTED, "d_model %d must be a multiple of 64 in 64..256", H);
-  if (P < 16 || P > 256 || P % 16) return fail(RL_EUNSUPPORTED, "d_state %d must be a multiple of 16 in 16..256", P);
+  if (P < 16 || P > 128 || P % 16) return fail(RL_EUNSUPPORTED, "d_state %d must be a multiple of 16 in 16..128", P);
   if (F < 128 || F > 4096 || F % 128)
     return fail(RL_EUNSUPPORTED, "head_width %d must be a multiple of 128 in 128..4096", F);
   if (pol->obs_dim != es->D) return fail(RL_ESHAPE, "policy obs_dim %d != observation size %d", pol->obs_dim, es->D);

@@ -67,9 +67,13 @@ constexpr int S5F_NW = S5F_NT / 64;
 constexpr int S5_NT = 256;  // threads of the head and output kernels
 constexpr int S5_NW = S5_NT / 64;
 
+constexpr int S5_WK = 32;       // K slice of the float32 weights staged in LDS
+constexpr int S5_WLD = S5_WK + 2;  // its row stride in words: 16 rows x 2 k of a half-wave on 32 banks
+constexpr int S5_WROWS = 256;     // rows of a staged slice: at most 2P (B_bar) and H (C)
+
 struct S5Lds {
   int ldx, ldu, ldf, ldxf;
-  size_t off_u, off_xf, off_keep, total;  // region 0 (obs tile, then u as float) at 0
+  size_t off_u, off_xf, off_keep, off_w, total;  // region 0 (obs tile, then u as float) at 0
 };
 
 __host__ __device__ inline S5Lds s5_lds(int D, int H, int P) {
@@ -84,7 +88,8 @@ __host__ __device__ inline S5Lds s5_lds(int D, int H, int P) {
   L.off_u = (r0 + 15) / 16 * 16;
   L.off_xf = (L.off_u + (size_t)S5_RT * L.ldu * 2 + 15) / 16 * 16;
   L.off_keep = L.off_xf + (size_t)S5_RT * L.ldxf * 4;
-  L.total = L.off_keep + S5_RT * 4;
+  L.off_w = (L.off_keep + S5_RT * 4 + 15) / 16 * 16;
+  L.total = L.off_w + (size_t)2 * S5_WROWS * S5_WLD * 4;  // two slice buffers
   return L;
 }
 
@@ -113,6 +118,66 @@ __global__ void s5_cat_kernel(int H, int P, const float* __restrict__ c, float* 
   wcat[i] = k < P ? c[(size_t)h * P + k] : -c[(size_t)H * P + (size_t)h * P + (k - P)];
 }
 
+// float32 MFMA tiles acc[m][g] = A[16 m + r][0:K] . W[nb[g] + c][0:K] for
+// r, c < 16, where W ([N, K] row-major, N <= 256, K a multiple of 32) is read
+// from global memory with 16-byte loads in K slices of 32, all N rows of a
+// slice staged by the whole workgroup into LDS (double-buffered; the loads
+// of slice s + 1 are issued before slice s is multiplied).  Every wave must
+// call it (it holds barriers).  A rows are in LDS with stride lda.
+template <int MT, int G>
+__device__ __forceinline__ void s5_lds_mma(const float* A, int lda, const float* __restrict__ W, int N, int K,
+                                           const int (&nb)[G], float* wsl, int tid, int lane, f32x4 (&acc)[MT][G]) {
+  constexpr int CPT = S5_WROWS * (S5_WK / 4) / S5F_NT;  // 16-byte chunks per thread per slice (at most)
+  const int nchunk = N * (S5_WK / 4);
+  f32x4 reg[CPT];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int q = tid + S5F_NT * j;
+      if (q < nchunk) reg[j] = *reinterpret_cast<const f32x4*>(W + (size_t)(q >> 3) * K + k0 + (q & 7) * 4);
+    }
+  };
+  auto lstore = [&](int buf) {
+    float* w = wsl + buf * S5_WROWS * S5_WLD;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int q = tid + S5F_NT * j;
+      if (q < nchunk) {
+        float* d = w + (q >> 3) * S5_WLD + (q & 7) * 4;
+        *reinterpret_cast<float2*>(d) = float2{reg[j][0], reg[j][1]};
+        *reinterpret_cast<float2*>(d + 2) = float2{reg[j][2], reg[j][3]};
+      }
+    }
+  };
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[m][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int ns = K / S5_WK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int sl = 0; sl < ns; ++sl) {
+    if (sl + 1 < ns) gload((sl + 1) * S5_WK);
+    const float* w = wsl + (sl & 1) * S5_WROWS * S5_WLD;
+#pragma unroll
+    for (int kk = 0; kk < S5_WK; kk += 4) {
+      const int k = kk + (lane >> 4);
+      float av[MT];
+#pragma unroll
+      for (int m = 0; m < MT; ++m) av[m] = A[(16 * m + (lane & 15)) * lda + sl * S5_WK + k];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float bv = w[(nb[g] + (lane & 15)) * S5_WLD + k];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) acc[m][g] = mfma_step(av[m], bv, acc[m][g]);
+      }
+    }
+    if (sl + 1 < ns) lstore((sl + 1) & 1);
+    __syncthreads();
+  }
+}
+
 __global__ __launch_bounds__(S5F_NT) void s5_front_kernel(S5FrontArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   constexpr int MT = S5_RT / 16;
@@ -121,6 +186,7 @@ __global__ __launch_bounds__(S5F_NT) void s5_front_kernel(S5FrontArgs a) {
   float* uf = reinterpret_cast<float*>(smem);  // replaces xs once the encoder is done
   uint16_t* us = reinterpret_cast<uint16_t*>(smem + L.off_u);
   float* xf = reinterpret_cast<float*>(smem + L.off_xf);
+  float* wsl = reinterpret_cast<float*>(smem + L.off_w);
   int* keep_s = reinterpret_cast<int*>(smem + L.off_keep);  // 1: the row's episode continues (carry used)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r0 = blockIdx.x * S5_RT;
@@ -166,19 +232,14 @@ __global__ __launch_bounds__(S5F_NT) void s5_front_kernel(S5FrontArgs a) {
   }
   __syncthreads();
 
-  // x_new = Lambda_bar x (zeroed at an episode start) + B_bar u, per 16 states
-  const float* a_u[MT];
-#pragma unroll
-  for (int m = 0; m < MT; ++m) a_u[m] = uf + (16 * m + (lane & 15)) * L.ldf;
-  for (int item = wave; item < P / 16; item += S5F_NW) {
+  // x_new = Lambda_bar x (zeroed at an episode start) + B_bar u: wave w takes
+  // states 16 w.. (P <= 16 waves' worth): its real and imaginary rows of B_bar
+  // ([2P, H] rows 16 w.. and P + 16 w..) as two tiles
+  {
+    const int item = wave < P / 16 ? wave : 0;
     const int n0 = item * 16;
-    // the real and imaginary rows of these 16 states as two tiles of one chain
-    // ([2P, H] rows n0.. and P + n0..), 16 k-steps of weights in flight
-    f32x4 bu[MT][2];
-    mma_tiles<DT_F32, 2, MT, WALIGN_16, 16>(a_u, H, H, a.bbar, n0, 2 * P, lane, bu, P);
     const int p = n0 + (lane & 15);
-    const float lr = a.lbar[p], li = a.lbar[P + p];
-    // previous states of this lane's rows, loaded together (rows past the end read the last row)
+    // previous states of this lane's rows, loaded ahead of the product (rows past the end read the last row)
     float xo[MT][4][2];
 #pragma unroll
     for (int m = 0; m < MT; ++m)
@@ -188,6 +249,11 @@ __global__ __launch_bounds__(S5F_NT) void s5_front_kernel(S5FrontArgs a) {
         xo[m][q][0] = a.carry[row * 2 * P + p];
         xo[m][q][1] = a.carry[row * 2 * P + P + p];
       }
+    const float lr = a.lbar[p], li = a.lbar[P + p];
+    f32x4 bu[MT][2];
+    const int nb[2] = {n0, P + n0};
+    s5_lds_mma<MT, 2>(uf, L.ldf, a.bbar, 2 * P, H, nb, wsl, tid, lane, bu);
+    if (wave < P / 16)
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -207,24 +273,26 @@ __global__ __launch_bounds__(S5F_NT) void s5_front_kernel(S5FrontArgs a) {
   }
   __syncthreads();
 
-  // y = Re(C x) + D u = [C_re | -C_im] [x_re | x_im] + D u, rounded to bf16
-  const float* a_x[MT];
+  // y = Re(C x) + D u = [C_re | -C_im] [x_re | x_im] + D u, rounded to bf16:
+  // wave w takes outputs 16 w.. and 16 (w + 8).. (H <= 256)
+  {
+    f32x4 cy[MT][2];
+    const int nb[2] = {(16 * wave) % H, (16 * (wave + S5F_NW)) % H};
+    s5_lds_mma<MT, 2>(xf, L.ldxf, a.wcat, H, 2 * P, nb, wsl, tid, lane, cy);
 #pragma unroll
-  for (int m = 0; m < MT; ++m) a_x[m] = xf + (16 * m + (lane & 15)) * L.ldxf;
-  for (int item = wave; item < H / 16; item += S5F_NW) {
-    const int n0 = item * 16;
-    f32x4 cy[MT][1];
-    mma_tiles<DT_F32, 1, MT, WALIGN_16, 16>(a_x, 2 * P, 2 * P, a.wcat, n0, H, lane, cy);
-    const int h = n0 + (lane & 15);
-    const float dh = a.d[h];
+    for (int g = 0; g < 2; ++g) {
+      if (16 * (wave + S5F_NW * g) >= H) continue;
+      const int h = 16 * (wave + S5F_NW * g) + (lane & 15);
+      const float dh = a.d[h];
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
+      for (int m = 0; m < MT; ++m)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int rl = 16 * m + 4 * (lane >> 4) + q, row = r0 + rl;
-        const float yv = cy[m][0][q] + dh * uf[rl * L.ldf + h];
-        if (row < a.R) a.y[(size_t)row * H + h] = f32_to_bf16(yv);
-      }
+        for (int q = 0; q < 4; ++q) {
+          const int rl = 16 * m + 4 * (lane >> 4) + q, row = r0 + rl;
+          const float yv = cy[m][g][q] + dh * uf[rl * L.ldf + h];
+          if (row < a.R) a.y[(size_t)row * H + h] = f32_to_bf16(yv);
+        }
+    }
   }
 }
 

@@ -237,7 +237,7 @@ def test_s5_checks_before_launch():
     E, A = 16, 2
     assert need >= 4 * E * A * 1024 * 2 + E * A * 128 * 2
     for kw, code in ((dict(dtype=R.RL_F32), R.RL_EUNSUPPORTED), (dict(d_model=96), R.RL_EUNSUPPORTED),
-                     (dict(d_state=24), R.RL_EUNSUPPORTED), (dict(head_width=1000), R.RL_EUNSUPPORTED),
+                     (dict(d_state=24), R.RL_EUNSUPPORTED), (dict(d_state=144), R.RL_EUNSUPPORTED), (dict(head_width=1000), R.RL_EUNSUPPORTED),
                      (dict(obs_dim=191), R.RL_ESHAPE), (dict(n_actions=5), R.RL_ESHAPE),
                      (dict(w_enc=0), R.RL_EINVAL), (dict(c=0x1004), R.RL_EINVAL), (dict(heads=0x2008), R.RL_EINVAL)):
         p = _s5_struct(**kw)
