@@ -46,10 +46,16 @@ def parse():
     return ap.parse_args()
 
 
-def csrc_hash():
+# The translation unit of the fused LBF rollout kernels (the file and every header it includes):
+# HBM traffic counters taken on those kernels stay valid while these files are unchanged.
+LBF_KERNEL_SOURCES = ("rl_lbf.hip", "rl_lbf.h", "rl_internal.h", "rl_mlp.h", "rl_regmlp.h", "rl_sample.h",
+                      "rl_philox.h", "rl_hanabi.h", "rl_overcooked.h")
+
+
+def csrc_hash(files=LBF_KERNEL_SOURCES):
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2609_13716_amd", "csrc", "*"))):
-        h.update(open(p, "rb").read())
+    for f in files:
+        h.update(open(os.path.join(ROOT, "paper_2609_13716_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
 
