@@ -458,15 +458,38 @@ __global__ __launch_bounds__(S5_NT) void s5_out_kernel(S5OutArgs o) {
   const uint16_t* wc = o.wc + kb + 8 * (lane >> 4);
   const u32x4 zero = {0u, 0u, 0u, 0u};
   f32x4 acc_a = {0.f, 0.f, 0.f, 0.f}, acc_c = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-  for (int k = 0; k < kq; k += 32) {
-    const u32x4 fc = *reinterpret_cast<const u32x4*>(xc + k);
-    const u32x4 gc = *reinterpret_cast<const u32x4*>(wc + k);
-    acc_c = mfma_step(fc, n == 0 ? gc : zero, acc_c);
-    if (o.sample) {
-      const u32x4 fa = *reinterpret_cast<const u32x4*>(xa + k);
-      const u32x4 ga = *reinterpret_cast<const u32x4*>(wa + k);
-      acc_a = mfma_step(fa, n < o.NA ? ga : zero, acc_a);
+  // groups of 4 k-steps: every load of a group issued before its MFMAs
+  constexpr int KG = 4;
+  if (o.sample) {
+    for (int k0 = 0; k0 < kq; k0 += 32 * KG) {
+      u32x4 fc[KG], gc[KG], fa[KG], ga[KG];
+#pragma unroll
+      for (int j = 0; j < KG; ++j) {
+        const int k = min(k0 + 32 * j, kq - 32);  // (kq is a multiple of 32; a repeat past the end is not used)
+        fc[j] = *reinterpret_cast<const u32x4*>(xc + k);
+        gc[j] = *reinterpret_cast<const u32x4*>(wc + k);
+        fa[j] = *reinterpret_cast<const u32x4*>(xa + k);
+        ga[j] = *reinterpret_cast<const u32x4*>(wa + k);
+      }
+#pragma unroll
+      for (int j = 0; j < KG; ++j)
+        if (k0 + 32 * j < kq) {
+          acc_c = mfma_step(fc[j], n == 0 ? gc[j] : zero, acc_c);
+          acc_a = mfma_step(fa[j], n < o.NA ? ga[j] : zero, acc_a);
+        }
+    }
+  } else {
+    for (int k0 = 0; k0 < kq; k0 += 32 * KG) {
+      u32x4 fc[KG], gc[KG];
+#pragma unroll
+      for (int j = 0; j < KG; ++j) {
+        const int k = min(k0 + 32 * j, kq - 32);
+        fc[j] = *reinterpret_cast<const u32x4*>(xc + k);
+        gc[j] = *reinterpret_cast<const u32x4*>(wc + k);
+      }
+#pragma unroll
+      for (int j = 0; j < KG; ++j)
+        if (k0 + 32 * j < kq) acc_c = mfma_step(fc[j], n == 0 ? gc[j] : zero, acc_c);
     }
   }
 #pragma unroll
@@ -475,6 +498,24 @@ __global__ __launch_bounds__(S5_NT) void s5_out_kernel(S5OutArgs o) {
     if (n == 0) vp[wave][4 * (lane >> 4) + q] = acc_c[q];
   }
   __syncthreads();
+  // logits and Gumbel scores: thread t takes action t % 16 of row t / 16 (the
+  // noise draws, the costly part, run on all lanes instead of one per row)
+  __shared__ float lgs[16][17], scs[16][17];
+  if (o.sample) {
+    const int rl = tid >> 4, k = tid & 15, row = r0 + rl;
+    if (k < o.NA && row < o.R) {
+      float x = bf16_to_f32(o.ba[k]);
+#pragma unroll
+      for (int w = 0; w < S5_NW; ++w) x += lp[w][rl][k];
+      lgs[rl][k] = x;
+      const int e = row / o.A, ag = row - e * o.A;
+      // noise of action k: draw k % 8 of Philox block (env, t, agent * 256 + k / 8, action tag), top 24 bits
+      const Block4 b = draw_block(o.seed, (uint64_t)(o.env_base + e), o.t, (uint64_t)ag * 256u + (uint64_t)(k >> 3),
+                                  TAG_ACTION);
+      scs[rl][k] = action_score(x, gumbel24(block_u32(b, k & 7) >> 8), true);
+    }
+    __syncthreads();
+  }
   const int row = r0 + tid;
   if (tid < 16 && row < o.R) {
     float v = bf16_to_f32(o.bc[0]);
@@ -482,49 +523,17 @@ __global__ __launch_bounds__(S5_NT) void s5_out_kernel(S5OutArgs o) {
     for (int w = 0; w < S5_NW; ++w) v += vp[w][tid];
     if (o.value) o.value[row] = v;
     if (o.sample) {
-      float l[16];
-#pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        float x = k < o.NA ? bf16_to_f32(o.ba[k]) : 0.f;
-#pragma unroll
-        for (int w = 0; w < S5_NW; ++w) x += lp[w][tid][k];
-        l[k] = x;
-      }
-      const int e = row / o.A, ag = row - e * o.A;
-      // noise of action k: draw k % 8 of Philox block (env, t, agent * 256 + k / 8, action tag), top 24 bits
-      const Block4 b0 = draw_block(o.seed, (uint64_t)(o.env_base + e), o.t, (uint64_t)ag * 256u, TAG_ACTION);
-      Block4 b1 = b0;
-      if (o.NA > 8) b1 = draw_block(o.seed, (uint64_t)(o.env_base + e), o.t, (uint64_t)ag * 256u + 1u, TAG_ACTION);
       int best = 0;
-      float bs = -INFINITY, best_l = l[0];
-#pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        if (k < o.NA) {
-          const float nz = gumbel24(block_u32(k < 8 ? b0 : b1, k & 7) >> 8);
-          const float sc = action_score(l[k], nz, true);
-          if (sc > bs) {
-            bs = sc;
-            best = k;
-            best_l = l[k];
-          }
+      float bs = -INFINITY;
+      for (int k = 0; k < o.NA; ++k)
+        if (scs[tid][k] > bs) {
+          bs = scs[tid][k];
+          best = k;
         }
-      }
       o.actions[row] = best;
       if (o.logits)
-#pragma unroll
-        for (int k = 0; k < 16; ++k)
-          if (k < o.NA) o.logits[(size_t)row * o.NA + k] = l[k];
-      if (o.logp) {  // float32 log-softmax, as log_softmax_at
-        float m = l[0];
-#pragma unroll
-        for (int k = 1; k < 16; ++k)
-          if (k < o.NA) m = fmaxf(m, l[k]);
-        float sum = 0.f;
-#pragma unroll
-        for (int k = 0; k < 16; ++k)
-          if (k < o.NA) sum += expf(l[k] - m);
-        o.logp[row] = best_l - (m + logf(sum));
-      }
+        for (int k = 0; k < o.NA; ++k) o.logits[(size_t)row * o.NA + k] = lgs[tid][k];
+      if (o.logp) o.logp[row] = log_softmax_at(lgs[tid], o.NA, best);
     }
   }
 }
