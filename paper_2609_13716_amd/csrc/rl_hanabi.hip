@@ -197,7 +197,8 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
 
 // ----------------------------------------------------- fused rollout ----
 
-constexpr int HN_RUN_TE = 16;  // envs (and mover rows) per workgroup
+constexpr int HN_RUN_TE = 16;   // envs (and mover rows) per workgroup
+constexpr int HN_RUN_NT = 512;  // 8 waves: the MLP's weight-streaming chains of a workgroup spread over twice the waves
 
 struct HnRunLayout {
   int ldx, ld1, ld2;
@@ -228,10 +229,10 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int
 size_t hn_run_lds_bytes(const PolicyArgs& pol) { return hn_run_layout(pol.H1, pol.H2, pol.dt, pol.D).total; }
 
 template <class G, int DT>
-__global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs pol, int32_t* __restrict__ state,
+__global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArgs pol, int32_t* __restrict__ state,
                                                           uint64_t t0, int n_steps, TrajArgs out) {
   using T = typename DType<DT>::T;
-  constexpr int TE = HN_RUN_TE, NA = G::NACT, NW = NTHREADS / 64;
+  constexpr int TE = HN_RUN_TE, NA = G::NACT, NW = HN_RUN_NT / 64;
   constexpr int LDX = lds_ld<DT>(G::OBS);
   extern __shared__ __align__(16) uint8_t smem[];
   const HnRunLayout L = hn_run_layout(pol.H1, pol.H2, DT, G::OBS);
@@ -253,7 +254,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
   const T* b1 = static_cast<const T*>(pol.b[0]);
   const T* b2 = static_cast<const T*>(pol.b[1]);
   const T* b3 = static_cast<const T*>(pol.b[2]);
-  zero_lds(smem, L.total, tid);
+  zero_lds<HN_RUN_NT>(smem, L.total, tid);
   __syncthreads();
   const bool envlane = tid < te_valid;
   const int e = e0 + tid;
@@ -266,7 +267,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     __syncthreads();  // the previous move's games are published
-    hn_build_bits<G, TE, NTHREADS>(envs, te_valid, tid);
+    hn_build_bits<G, TE, HN_RUN_NT>(envs, te_valid, tid);
     __syncthreads();
     hn_paint<G, T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
@@ -276,7 +277,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
     __syncthreads();
     mlp_logits<DT>(h2, L.ld2, TE, pol.H2, W3, b3, NA, lg, MAX_NA, wave, NW, lane);
     __syncthreads();
-    for (int idx = tid; idx < te_valid * NA; idx += NTHREADS) {
+    for (int idx = tid; idx < te_valid * NA; idx += HN_RUN_NT) {
       const int el = idx / NA, a = idx - el * NA;
       const int cur = envs[el].pub.cur;
       const bool ok = (envs[el].legal >> a) & 1u;
@@ -292,7 +293,7 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
     // wave's loads wait for its earlier stores (one in-order counter).
     if (out.obs)
       copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * G::OBS, G::OBS,
-                         2 * te_valid, tid, NTHREADS);
+                         2 * te_valid, tid, HN_RUN_NT);
     __syncthreads();
     uint32_t d = 0;
     if (envlane) {
@@ -333,12 +334,12 @@ __global__ __launch_bounds__(NTHREADS) void hn_run_kernel(HnParams p, PolicyArgs
   }
   __syncthreads();
   if (out.obs_last) {
-    hn_build_bits<G, TE, NTHREADS>(envs, te_valid, tid);
+    hn_build_bits<G, TE, HN_RUN_NT>(envs, te_valid, tid);
     __syncthreads();
     hn_paint<G, T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
     copy_rows_global16(xs, LDX, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * G::OBS, G::OBS, 2 * te_valid,
-                       tid, NTHREADS);
+                       tid, HN_RUN_NT);
   }
   if (envlane) hn_store(state, E, e, s);
 }
@@ -382,9 +383,9 @@ static hipError_t launch_hn_run_g(const HnParams& p, const PolicyArgs& pol, int3
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   if (pol.dt == DT_F32)
-    hn_run_kernel<G, DT_F32><<<hn_tiles(p.E, HN_RUN_TE), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
+    hn_run_kernel<G, DT_F32><<<hn_tiles(p.E, HN_RUN_TE), HN_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
   else
-    hn_run_kernel<G, DT_BF16><<<hn_tiles(p.E, HN_RUN_TE), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
+    hn_run_kernel<G, DT_BF16><<<hn_tiles(p.E, HN_RUN_TE), HN_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
 }
 
