@@ -179,8 +179,10 @@ __global__ __launch_bounds__(64) void oc_env_kernel(OcParams p, int32_t* __restr
 
 // ----------------------------------------------------- fused rollout ----
 
+constexpr int OC_RUN_NT = 512;  // 8 waves: the streamed MLP's chains of a workgroup spread over twice the waves
+
 template <int DT, int TE>
-__global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs pol, int32_t* __restrict__ state,
+__global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArgs pol, int32_t* __restrict__ state,
                                                           uint64_t t0, int n_steps, TrajArgs out) {
   using T = typename DType<DT>::T;
   constexpr int R = TE * 2, NA = OC_NACT;
@@ -203,7 +205,7 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
   const T* b1 = static_cast<const T*>(pol.b[0]);
   const T* b2 = static_cast<const T*>(pol.b[1]);
   const T* b3 = static_cast<const T*>(pol.b[2]);
-  zero_lds(smem, total, tid);
+  zero_lds<OC_RUN_NT>(smem, total, tid);
   __syncthreads();
   const bool envlane = tid < te_valid;
   const int e = e0 + tid;
@@ -216,13 +218,13 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     __syncthreads();  // the env lanes' repaint of the previous step is visible
-    mlp_input_layer_const<DT, OC_D>(xs, LDX, nullptr, R, W1, b1, pol.H1, h1, ld1, wave, NTHREADS / 64, lane);
+    mlp_input_layer_const<DT, OC_D>(xs, LDX, nullptr, R, W1, b1, pol.H1, h1, ld1, wave, OC_RUN_NT / 64, lane);
     __syncthreads();
-    mlp_hidden<DT>(h1, ld1, R, pol.H1, W2, b2, pol.H2, h2, ld2, wave, NTHREADS / 64, lane);
+    mlp_hidden<DT>(h1, ld1, R, pol.H1, W2, b2, pol.H2, h2, ld2, wave, OC_RUN_NT / 64, lane);
     __syncthreads();
-    mlp_logits<DT>(h2, ld2, R, pol.H2, W3, b3, NA, lg, MAX_NA, wave, NTHREADS / 64, lane);
+    mlp_logits<DT>(h2, ld2, R, pol.H2, W3, b3, NA, lg, MAX_NA, wave, OC_RUN_NT / 64, lane);
     __syncthreads();
-    for (int idx = tid; idx < R * NA; idx += NTHREADS) {
+    for (int idx = tid; idx < R * NA; idx += OC_RUN_NT) {
       const int r = idx / NA, a = idx - r * NA, el = r >> 1, ag = r & 1;
       if (el < te_valid) {
         const float g = action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t, ag, a);
@@ -234,7 +236,7 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
     // wave's loads wait for its earlier stores (one in-order counter).
     if (out.obs)
       copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D, OC_D, te_valid * 2,
-                         tid, NTHREADS);
+                         tid, OC_RUN_NT);
     __syncthreads();
     if (tid < R && (tid >> 1) < te_valid) {
       int best = 0;
@@ -262,7 +264,7 @@ __global__ __launch_bounds__(NTHREADS) void oc_run_kernel(OcParams p, PolicyArgs
   __syncthreads();
   if (out.obs_last)
     copy_rows_global16(xs, LDX, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * OC_D, OC_D, te_valid * 2, tid,
-                       NTHREADS);
+                       OC_RUN_NT);
   if (envlane) oc_store(state, E, e, s);
 }
 
@@ -310,7 +312,7 @@ static hipError_t launch_oc_run_te(const OcParams& p, const PolicyArgs& pol, int
   hipError_t e = hipFuncSetAttribute((const void*)oc_run_kernel<DT, TE>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
-  oc_run_kernel<DT, TE><<<oc_tiles(p.E, TE), NTHREADS, lds, s>>>(p, pol, state, t0, n_steps, out);
+  oc_run_kernel<DT, TE><<<oc_tiles(p.E, TE), OC_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
 }
 
