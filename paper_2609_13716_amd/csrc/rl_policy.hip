@@ -204,6 +204,144 @@ __global__ __launch_bounds__(NW * 64, MINB) void policy_fwd_reg_kernel(PolicyArg
   store_logits();
 }
 
+// Software-pipelined variant for the narrow bf16 policies (one workgroup of
+// 4 waves per CU).  In a 128-wide layer the tanh epilogue (two
+// transcendental instructions per value) takes longer than the layer's
+// MFMAs, so each wave overlaps one tile's epilogue with the next tile's
+// matrix products: iteration j of a workgroup runs
+//   phase A: layer 3 of tile j-2 (logits out), layer-1 MFMAs of tile j+1
+//            interleaved with the layer-1 epilogue of tile j;
+//   phase B: the observation tile of j+2 staged from registers, the load of
+//            tile j+3 issued, layer-2 MFMAs of tile j interleaved with the
+//            layer-2 epilogue of tile j-1;
+// with one barrier after each phase.  The observation tile is double
+// buffered; h1 and h2 have one buffer each (every write of one is separated
+// from the reads of its previous contents by a barrier).  Tiles past this
+// workgroup's last are computed from zeros and never stored.  Every output
+// is the same MFMA chain and epilogue as policy_fwd_reg_kernel and the
+// rollout kernels, so the logits are bit-identical to theirs.
+template <int D, int H1, int H2, int NA, int MT, int MINB>
+__global__ __launch_bounds__(256, MINB) void policy_fwd_pipe_kernel(PolicyArgs pol, const void* __restrict__ obs_v,
+                                                                  const uint8_t* __restrict__ legal, int64_t rows,
+                                                                  float* __restrict__ logits) {
+  constexpr int DT = DT_BF16, NW = 4, NT = NW * 64, BM = MT * 16;
+  using T = typename DType<DT>::T;
+  using B = typename BOperand<DT>::type;
+  constexpr int LDX = lds_ld<DT>(D), LD1 = lds_ld<DT>(H1), LD2 = lds_ld<DT>(H2);
+  constexpr int K3 = round_up(H2, DType<DT>::KS) / DType<DT>::KS;
+  constexpr int VE = 16 / sizeof(T);
+  static_assert(D % VE == 0, "observation rows are whole 16-byte vectors");
+  static_assert(NA <= 16, "one transposed M tile of actions");
+  static_assert(MT <= NW, "one layer-3 M tile per wave");
+  __shared__ __align__(16) T xs[2][BM * LDX];
+  __shared__ __align__(16) T h1s[BM * LD1];
+  __shared__ __align__(16) T h2s[BM * LD2];
+  __shared__ __align__(16) B w3s[K3 * 64];
+  const T* obs = static_cast<const T*>(obs_v);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  RegLayer<DT, D, H1, NW> L1;
+  RegLayer<DT, H1, H2, NW> L2;
+  L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane);
+  L2.load(static_cast<const T*>(pol.W[1]), static_cast<const T*>(pol.b[1]), wave, lane);
+  if (tid < 64) {
+    const int n = lane & 15;
+    const T* row = static_cast<const T*>(pol.W[2]) + (size_t)(n < NA ? n : 0) * H2;
+#pragma unroll
+    for (int ks = 0; ks < K3; ++ks) w3s[ks * 64 + lane] = load_operand_global<DT, H2>(row, H2, ks, lane, n < NA);
+  }
+  float b3r[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int a = 4 * (lane >> 4) + r;
+    b3r[r] = a < NA ? DType<DT>::to_f32(static_cast<const T*>(pol.b[2])[a]) : 0.f;
+  }
+  for (int i = tid; i < 2 * BM * LDX; i += NT) (&xs[0][0])[i] = (T)0;
+  for (int i = tid; i < BM * LD1; i += NT) h1s[i] = (T)0;
+  for (int i = tid; i < BM * LD2; i += NT) h2s[i] = (T)0;
+
+  const int64_t ntiles = (rows + BM - 1) / BM;
+  const int nt = (int64_t)blockIdx.x < ntiles ? (int)((ntiles - 1 - blockIdx.x) / gridDim.x) + 1 : 0;
+  auto tile_of = [&](int j) { return (int64_t)blockIdx.x + (int64_t)j * gridDim.x; };
+  constexpr int VPR = D / VE, NV = BM * VPR, IT = (NV + NT - 1) / NT;
+  u32x4 v[IT];
+  auto prefetch = [&](int j) {  // tile j of this workgroup into registers (zeros past the last)
+    const int64_t row0 = tile_of(j) * BM;
+    const int nrow = j < nt ? (int)min((int64_t)BM, rows - row0) : 0;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int i = tid + it * NT;
+      const int r = i / VPR, c = (i - r * VPR) * VE;
+      v[it] = (i < NV && r < nrow) ? *reinterpret_cast<const u32x4*>(obs + (size_t)(row0 + r) * D + c)
+                                    : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto stage = [&](T* dst) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int i = tid + it * NT;
+      const int r = i / VPR, c = (i - r * VPR) * VE;
+      if (i < NV) *reinterpret_cast<u32x4*>(dst + r * LDX + c) = v[it];
+    }
+  };
+
+  __syncthreads();  // zero fill done before the staging writes
+  prefetch(0);
+  stage(xs[0]);
+  prefetch(1);
+  stage(xs[1]);
+  prefetch(2);
+  __syncthreads();
+  f32x4 acc1[MT][RegLayer<DT, D, H1, NW>::OWN];
+  f32x4 acc2[MT][RegLayer<DT, H1, H2, NW>::OWN];
+  L1.template run<MT>(xs[0], LDX, acc1, wave, lane);
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int o = 0; o < RegLayer<DT, H1, H2, NW>::OWN; ++o) acc2[m][o] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int j = 0;; ++j) {
+    // phase A
+    if (j >= 2 && wave < MT) {
+      const int row = wave * 16 + (lane & 15);
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < K3; ++ks)
+        acc = mfma16<DT>(w3s[ks * 64 + lane], load_operand_lds<DT>(h2s, LD2, row, ks, lane), acc);
+      const int64_t row0 = tile_of(j - 2) * BM;
+      if (row0 + row < rows) {
+        const size_t gr = (size_t)(row0 + row) * NA;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int a = 4 * (lane >> 4) + r;
+          if (a < NA) {
+            const bool ok = legal == nullptr || legal[gr + a] != 0;
+            logits[gr + a] = ok ? acc[r] + b3r[r] : -INFINITY;
+          }
+        }
+      }
+    }
+    if (j == nt + 1) break;
+    L1.template run_overlapped<MT>(xs[(j + 1) & 1], LDX, acc1, h1s, LD1, wave, lane);
+    __syncthreads();
+    // phase B
+    stage(xs[j & 1]);
+    prefetch(j + 3);
+    L2.template run_overlapped<MT>(h1s, LD1, acc2, h2s, LD2, wave, lane);
+    __syncthreads();
+  }
+}
+
+template <int D, int H1, int H2, int NA, int MT, int MINB>
+static hipError_t launch_policy_pipe(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
+                                     float* logits, hipStream_t s) {
+  constexpr int BM = MT * 16;
+  const int64_t ntiles = (rows + BM - 1) / BM;
+  const unsigned grid = (unsigned)(ntiles < (int64_t)256 * MINB ? ntiles : (int64_t)256 * MINB);
+  policy_fwd_pipe_kernel<D, H1, H2, NA, MT, MINB><<<dim3(grid), 256, 0, s>>>(pol, obs, legal, rows, logits);
+  return hipGetLastError();
+}
+
 template <int DT, int D, int H1, int H2, int NA, int NW, int MT, int MINB>
 static hipError_t launch_policy_reg(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
                                     float* logits, hipStream_t s) {
@@ -222,7 +360,10 @@ static bool try_launch_policy_reg(const PolicyArgs& pol, const void* obs, const 
     return true;                                                                                         \
   }
   // (dtype, D, H1, H2, nA, waves, 16-row M tiles per workgroup tile, workgroups per CU)
-  RL_PF_CASE(DT_BF16, 192, 128, 128, 6, 4, 4, 2)
+  if (pol.dt == DT_BF16 && pol.D == 192 && pol.H1 == 128 && pol.H2 == 128 && pol.NA == 6) {
+    *err = launch_policy_pipe<192, 128, 128, 6, 2, 2>(pol, obs, legal, rows, logits, s);
+    return true;
+  }
   RL_PF_CASE(DT_F32, 192, 128, 128, 6, 4, 4, 1)
   RL_PF_CASE(DT_BF16, 192, 64, 64, 6, 4, 4, 2)
   RL_PF_CASE(DT_F32, 192, 64, 64, 6, 4, 4, 2)

@@ -143,8 +143,35 @@ struct RegLayer {
     }
   }
 
-  // out = tanh(acc + bias) in the layer dtype: four consecutive units of one
-  // row per lane, stored with one 8-byte (bf16) or 16-byte (f32) LDS write.
+  // out = tanh(acc + bias) in the layer dtype for one accumulator (row tile
+  // m, owned tile o): four consecutive units of one row per lane, stored with
+  // one 8-byte (bf16) or 16-byte (f32) LDS write.
+  __device__ __forceinline__ void store_block(const f32x4& acc, T* out, int ld, int m, int o, int wave, int lane,
+                                              const float* bias_lds) const {
+    const int row = m * 16 + (lane & 15);
+    const int col = (wave + o * NW) * 16 + 4 * (lane >> 4);
+    float bo[4];
+    if constexpr (BL) {
+      const f32x4 b4 = *reinterpret_cast<const f32x4*>(bias_lds + col);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) bo[r] = b4[r];
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) bo[r] = bias[o][r];
+    }
+    float v[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] = fast_tanh(acc[r] + bo[r]);
+    if constexpr (DT == DT_F32) {
+      *reinterpret_cast<f32x4*>(out + row * ld + col) = f32x4{v[0], v[1], v[2], v[3]};
+    } else {
+      const uint32_t lo = pack_bf16x2(v[0], v[1]);
+      const uint32_t hi = pack_bf16x2(v[2], v[3]);
+      typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+      *reinterpret_cast<u32x2*>(out + row * ld + col) = u32x2{lo, hi};
+    }
+  }
+
   template <int MT>
   __device__ __forceinline__ void store_tanh(const f32x4 (&acc)[MT][OWN], T* out, int ld, int wave, int lane,
                                              const float* bias_lds = nullptr) const {
@@ -153,29 +180,42 @@ struct RegLayer {
 #pragma unroll
       for (int o = 0; o < OWN; ++o) {
         if (NT % NW != 0 && wave + o * NW >= NT) continue;
-        const int row = m * 16 + (lane & 15);
-        const int col = (wave + o * NW) * 16 + 4 * (lane >> 4);
-        float bo[4];
-        if constexpr (BL) {
-          const f32x4 b4 = *reinterpret_cast<const f32x4*>(bias_lds + col);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) bo[r] = b4[r];
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) bo[r] = bias[o][r];
-        }
-        float v[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = fast_tanh(acc[m][o][r] + bo[r]);
-        if constexpr (DT == DT_F32) {
-          *reinterpret_cast<f32x4*>(out + row * ld + col) = f32x4{v[0], v[1], v[2], v[3]};
-        } else {
-          const uint32_t lo = pack_bf16x2(v[0], v[1]);
-          const uint32_t hi = pack_bf16x2(v[2], v[3]);
-          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-          *reinterpret_cast<u32x2*>(out + row * ld + col) = u32x2{lo, hi};
-        }
+        store_block(acc[m][o], out, ld, m, o, wave, lane, bias_lds);
       }
+  }
+
+  // Software-pipelined layer step for a wave that owns whole tiles: acc gets
+  // W in^T of a new row tile (the same MFMA chains as run, so the same bits),
+  // while the epilogue of acc's previous contents (store_tanh into out) is
+  // spread between the matrix instructions.  The wave's transcendental and
+  // conversion work then issues while its own MFMAs execute, instead of
+  // after them.
+  template <int MT>
+  __device__ __forceinline__ void run_overlapped(const T* in, int ld, f32x4 (&acc)[MT][OWN], T* out, int ldo,
+                                                 int wave, int lane) const {
+    static_assert(NT % NW == 0, "every wave owns whole tiles");
+    constexpr int STEPS = KSTEPS * MT, EB = MT * OWN;
+    f32x4 prev[MT][OWN];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int o = 0; o < OWN; ++o) {
+        prev[m][o] = acc[m][o];
+        acc[m][o] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    B a = load_operand_lds<DT>(in, ld, lane & 15, 0, lane);
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      const int ks = s / MT, m = s % MT;
+      B an = a;
+      if (s + 1 < STEPS) an = load_operand_lds<DT>(in, ld, ((s + 1) % MT) * 16 + (lane & 15), (s + 1) / MT, lane);
+#pragma unroll
+      for (int o = 0; o < OWN; ++o) acc[m][o] = mfma16<DT>(w[o][ks], a, acc[m][o]);
+#pragma unroll
+      for (int e = 0; e < EB; ++e)
+        if (e * STEPS / EB == s) store_block(prev[e / OWN][e % OWN], out, ldo, e / OWN, e % OWN, wave, lane, nullptr);
+      a = an;
+    }
   }
 };
 

@@ -227,6 +227,27 @@ def test_policy_forward_parity(dims, dtype):
     assert np.array_equal(gm[legal == 1], got[legal == 1])
 
 
+@pytest.mark.parametrize("rows", [256 * 64 + 5, 3 * 256 * 64 + 37])
+@pytest.mark.parametrize("dims", [(192, 128, 128, 6), (192, 64, 64, 6)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_policy_forward_many_tiles(rows, dims, dtype):
+    """Batches that give every workgroup of the persistent policy kernels several 64-row tiles
+    (the first workgroups one more than the rest) and end in a ragged tile."""
+    require_gpu()
+    _note(f"policy_forward {dims} {dtype} rows={rows}")
+    rng = np.random.default_rng(rows + dims[1])
+    ws, bs = workloads.policy_weights(dims, seed=11, bias_scale=0.3)
+    obs = rng.integers(0, 3, size=(rows, dims[0])).astype(np.float32)
+    legal = (rng.random((rows, dims[3])) < 0.9).astype(np.uint8)
+    pol = R.Policy(ws, bs, dtype)
+    x = torch.from_numpy(obs).to("cuda", pol.torch_dtype)
+    got = R.policy_forward(pol, x).cpu().numpy()
+    assert_logits_close(got, mlp.forward(obs, ws, bs, dtype), RTOL[dtype])
+    gm = R.policy_forward(pol, x, torch.from_numpy(legal).cuda()).cpu().numpy()
+    assert np.all(np.isneginf(gm[legal == 0]))
+    assert np.array_equal(gm[legal == 1], got[legal == 1])
+
+
 # ------------------------------------------------------------- full rollout
 
 def _run_gpu(cfg, pol, T, t0=0, state=None):
