@@ -112,6 +112,13 @@ typedef struct {
   int32_t dims[4];  /* D, H1, H2, nA */
   const void* W[3];
   const void* b[3];
+  /* Optional (RL_BF16 only): a copy of W[0..2] in the fragment-major layout
+   * written by rl_policy_pack, or NULL.  When set, the streamed-weight
+   * rollout kernels (kitchen and Hanabi rollouts) read their operands from it,
+   * 1 KB contiguous per load instead of 16 rows x 64 bytes; results are
+   * bit-identical to reading W.  Must be 16-byte aligned and stay valid and
+   * unchanged while calls that use the policy run. */
+  const void* packed;
 } rl_policy;
 
 /* Trajectory outputs of rollout_run (host struct of device pointers).  Any
@@ -168,6 +175,20 @@ rl_status rollout_init(const rl_env_config* cfg, void* state, void* obs, int32_t
 rl_status rollout_step(const rl_env_config* cfg, void* state, uint64_t t0, int32_t n_steps,
                        const int32_t* actions, void* obs_out, int32_t obs_dtype, float* reward,
                        uint8_t* done, uint8_t* legal_out, void* stream);
+
+/* Bytes of the fragment-major weight copy of an RL_BF16 policy (host query;
+ * 0 when the policy is invalid or float32).  Layer l (W_l of N = dims[l+1]
+ * rows and K = dims[l] columns) takes ceil(N/16) * ceil(K/32) KB, starting at
+ * a 256-byte boundary after the previous layer; for each 16-row tile t and
+ * 32-wide K step s the 1 KB block at ((t * ceil(K/32) + s) * 1024) holds, for
+ * lane l = 0..63, the 8 bf16 W_l[16t + l%16][32s + 8(l/16) + j], j = 0..7
+ * (zero outside W_l), i.e. the MFMA B operands of that tile and step. */
+size_t rl_policy_packed_bytes(const rl_policy* policy);
+
+/* Writes that copy of policy->W into `packed` (device, 16-byte aligned, at
+ * least rl_policy_packed_bytes bytes, caller-owned), enqueued on `stream`.
+ * policy->packed is ignored.  RL_EUNSUPPORTED for a float32 policy. */
+rl_status rl_policy_pack(const rl_policy* policy, void* packed, void* stream);
 
 /* pi(. | o): policy logits for `rows` observations.
  *   obs    [rows, D] of policy->dtype, read.

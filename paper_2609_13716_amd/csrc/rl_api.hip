@@ -165,15 +165,21 @@ rl_status check_policy(const rl_policy* pol, rl::PolicyArgs* a) {
   if (NA < 1 || NA > rl::MAX_NA) return fail(RL_EUNSUPPORTED, "action count %d outside 1..%d", NA, rl::MAX_NA);
   for (int l = 0; l < 3; ++l)
     if (!pol->W[l] || !pol->b[l]) return fail(RL_EINVAL, "policy weight or bias %d is NULL", l);
+  if (pol->packed) {
+    if (pol->dtype != RL_BF16) return fail(RL_EUNSUPPORTED, "packed weights are for bf16 policies only");
+    if ((uintptr_t)pol->packed % 16) return fail(RL_EINVAL, "packed weights must be 16-byte aligned");
+  }
   if (a) {
     a->dt = pol->dtype == RL_F32 ? rl::DT_F32 : rl::DT_BF16;
     a->D = D;
     a->H1 = H1;
     a->H2 = H2;
     a->NA = NA;
+    const int dims[4] = {D, H1, H2, NA};
     for (int l = 0; l < 3; ++l) {
       a->W[l] = pol->W[l];
       a->b[l] = pol->b[l];
+      a->Wp[l] = pol->packed ? static_cast<const uint8_t*>(pol->packed) + rl::packed_layer_offset(dims, l) : nullptr;
     }
   }
   return RL_OK;
@@ -241,6 +247,23 @@ rl_status rollout_step(const rl_env_config* cfg, void* state, uint64_t t0, int32
   else
     e = rl::launch_hn_step(es.hn, st, t0, n_steps, actions, obs_out, dt, reward, done, legal_out, hs);
   return launched(e, "rollout_step");
+}
+
+size_t rl_policy_packed_bytes(const rl_policy* policy) {
+  rl::PolicyArgs a;
+  if (check_policy(policy, &a) != RL_OK || a.dt != rl::DT_BF16) return 0;
+  const int dims[4] = {a.D, a.H1, a.H2, a.NA};
+  return rl::packed_layer_offset(dims, 2) + rl::packed_layer_bytes(a.NA, a.H2);
+}
+
+rl_status rl_policy_pack(const rl_policy* policy, void* packed, void* stream) {
+  rl::PolicyArgs a;
+  const rl_status s = check_policy(policy, &a);
+  if (s != RL_OK) return s;
+  if (a.dt != rl::DT_BF16) return fail(RL_EUNSUPPORTED, "packed weights are for bf16 policies only");
+  if (!packed) return fail(RL_EINVAL, "packed is NULL");
+  if ((uintptr_t)packed % 16) return fail(RL_EINVAL, "packed must be 16-byte aligned");
+  return launched(rl::launch_policy_pack(a, packed, (hipStream_t)stream), "rl_policy_pack");
 }
 
 rl_status policy_forward(const rl_policy* policy, const void* obs, const uint8_t* legal, int64_t rows,

@@ -228,7 +228,7 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int
 
 size_t hn_run_lds_bytes(const PolicyArgs& pol) { return hn_run_layout(pol.H1, pol.H2, pol.dt, pol.D).total; }
 
-template <class G, int DT>
+template <class G, int DT, bool PK>
 __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArgs pol, int32_t* __restrict__ state,
                                                           uint64_t t0, int n_steps, TrajArgs out) {
   using T = typename DType<DT>::T;
@@ -254,6 +254,9 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
   const T* b1 = static_cast<const T*>(pol.b[0]);
   const T* b2 = static_cast<const T*>(pol.b[1]);
   const T* b3 = static_cast<const T*>(pol.b[2]);
+  const T* Wp1 = static_cast<const T*>(pol.Wp[0]);
+  const T* Wp2 = static_cast<const T*>(pol.Wp[1]);
+  const T* Wp3 = static_cast<const T*>(pol.Wp[2]);
   zero_lds<HN_RUN_NT>(smem, L.total, tid);
   __syncthreads();
   const bool envlane = tid < te_valid;
@@ -271,11 +274,11 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
     __syncthreads();
     hn_paint<G, T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
-    mlp_input_layer_const<DT, G::OBS>(xs, LDX, rows, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane);
+    mlp_input_layer_const<DT, G::OBS, PK>(xs, LDX, rows, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane, Wp1);
     __syncthreads();
-    mlp_hidden<DT>(h1, L.ld1, TE, pol.H1, W2, b2, pol.H2, h2, L.ld2, wave, NW, lane);
+    mlp_hidden<DT, PK>(h1, L.ld1, TE, pol.H1, W2, b2, pol.H2, h2, L.ld2, wave, NW, lane, Wp2);
     __syncthreads();
-    mlp_logits<DT>(h2, L.ld2, TE, pol.H2, W3, b3, NA, lg, MAX_NA, wave, NW, lane);
+    mlp_logits<DT, PK>(h2, L.ld2, TE, pol.H2, W3, b3, NA, lg, MAX_NA, wave, NW, lane, Wp3);
     __syncthreads();
     for (int idx = tid; idx < te_valid * NA; idx += HN_RUN_NT) {
       const int el = idx / NA, a = idx - el * NA;
@@ -379,13 +382,18 @@ template <class G>
 static hipError_t launch_hn_run_g(const HnParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0,
                                   int n_steps, const TrajArgs& out, hipStream_t s) {
   const size_t lds = hn_run_lds_bytes(pol);
-  const void* fn = pol.dt == DT_F32 ? (const void*)hn_run_kernel<G, DT_F32> : (const void*)hn_run_kernel<G, DT_BF16>;
+  const bool pk = pol.dt == DT_BF16 && pol.Wp[0] != nullptr;  // fragment-major weights
+  const void* fn = pol.dt == DT_F32 ? (const void*)hn_run_kernel<G, DT_F32, false>
+                   : pk             ? (const void*)hn_run_kernel<G, DT_BF16, true>
+                                    : (const void*)hn_run_kernel<G, DT_BF16, false>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   if (pol.dt == DT_F32)
-    hn_run_kernel<G, DT_F32><<<hn_tiles(p.E, HN_RUN_TE), HN_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
+    hn_run_kernel<G, DT_F32, false><<<hn_tiles(p.E, HN_RUN_TE), HN_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
+  else if (pk)
+    hn_run_kernel<G, DT_BF16, true><<<hn_tiles(p.E, HN_RUN_TE), HN_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
   else
-    hn_run_kernel<G, DT_BF16><<<hn_tiles(p.E, HN_RUN_TE), HN_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
+    hn_run_kernel<G, DT_BF16, false><<<hn_tiles(p.E, HN_RUN_TE), HN_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
 }
 

@@ -111,7 +111,24 @@ struct PolicyArgs {
   const void* W[3];
   const void* b[3];
   int VH = 0;  // 1: the last of the NA outputs is the critic's value V(o), the others are action logits
+  // bf16 only: the layers' fragment-major copies (nullptr: read W; see
+  // packed_layer_offset), used by the streamed-weight rollout kernels
+  const void* Wp[3] = {nullptr, nullptr, nullptr};
 };
+
+// Fragment-major copy of a bf16 layer W [N x K] (the nn.Linear layout): for
+// 16-row tile t and 32-wide K step s, the MFMA B operands of the 64 lanes
+// (lane l: row 16t + l % 16, k = 32s + 8(l / 16) .. +7, zero outside W) are
+// 1 KB at element ((t * S + s) * 64 + l) * 8, S = ceil(K / 32).  The three
+// layers of a policy follow one another, each at a 256-byte boundary.
+__host__ __device__ inline size_t packed_layer_bytes(int N, int K) {
+  return (size_t)((N + 15) / 16) * (size_t)((K + 31) / 32) * 1024;
+}
+__host__ __device__ inline size_t packed_layer_offset(const int (&dims)[4], int layer) {
+  size_t o = 0;
+  for (int l = 0; l < layer; ++l) o += (packed_layer_bytes(dims[l + 1], dims[l]) + 255) & ~(size_t)255;
+  return o;
+}
 
 struct TrajArgs {
   void* obs;
@@ -220,6 +237,7 @@ hipError_t launch_hn_run(const HnParams& p, const PolicyArgs& pol, int32_t* stat
                          const TrajArgs& out, hipStream_t s);
 
 size_t policy_lds_bytes(const PolicyArgs& pol);
+hipError_t launch_policy_pack(const PolicyArgs& pol, void* packed, hipStream_t s);
 hipError_t launch_policy_forward(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
                                  float* logits, hipStream_t s);
 hipError_t launch_sample(uint64_t seed, int64_t env_base, int E, int A, int NA, uint64_t t, const float* logits,

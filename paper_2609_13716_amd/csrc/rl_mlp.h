@@ -148,23 +148,36 @@ __device__ __forceinline__ f32x4 mfma_step(u32x4 a, u32x4 b, f32x4 acc) {
 // end is guarded.  Each tile's sum runs over k in the same order whatever G
 // and MT are, so results do not depend on them.  PFX > 0 sets the ring depth
 // (deeper rings hide more of the weight-load latency in short, long-K chains);
-// tile g covers output columns n0 + gstride * g (gstride 16: adjacent tiles).
-template <int DT, int G, int MT, int AL, int PFX = 0>
+// tile g covers output columns n0 + gstride * g (gstride 16: adjacent tiles;
+// n0 and gstride are multiples of 16).  PK (bf16): the B operands come from
+// Wp, the layer's fragment-major copy (packed_layer_offset), where each
+// operand load is one contiguous 1 KB block instead of 16 rows x 64 bytes;
+// the operands, and so the results, are the same as from W.
+template <int DT, int G, int MT, int AL, int PFX = 0, bool PK = false>
 __device__ __forceinline__ void mma_tiles(const typename DType<DT>::T* const (&a_row)[MT], int Kpad, int K,
                                           const typename DType<DT>::T* __restrict__ W, int n0, int N, int lane,
-                                          f32x4 (&acc)[MT][G], int gstride = 16) {
+                                          f32x4 (&acc)[MT][G], int gstride = 16,
+                                          const typename DType<DT>::T* __restrict__ Wp = nullptr) {
   using T = typename DType<DT>::T;
   using BT = typename std::conditional<DT == DT_F32, float, u32x4>::type;
   constexpr int KS = DType<DT>::KS;
   constexpr int KL = DT == DT_F32 ? 1 : 8;  // k values per lane per step
   constexpr int PF = PFX > 0 ? PFX : G >= 4 ? 2 : 4;  // k-steps of weights in flight
+  constexpr bool PACKED = PK && DT == DT_BF16;
   const T* wrow[G];
   bool nok[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     const int n = n0 + gstride * g + (lane & 15);
     nok[g] = n < N;
-    wrow[g] = W + (size_t)(nok[g] ? n : 0) * K + (lane >> 4) * KL;
+    if constexpr (PACKED) {
+      // operand block of this lane in k step 0 of tile (n0 + gstride g) / 16
+      // (tiles past the layer read tile 0; nok zeroes them)
+      const int tile = n0 + gstride * g < N ? (n0 + gstride * g) >> 4 : 0;
+      wrow[g] = Wp + ((size_t)tile * (Kpad / KS) * 64 + lane) * 8;
+    } else {
+      wrow[g] = W + (size_t)(nok[g] ? n : 0) * K + (lane >> 4) * KL;
+    }
   }
 #pragma unroll
   for (int m = 0; m < MT; ++m)
@@ -180,6 +193,8 @@ __device__ __forceinline__ void mma_tiles(const typename DType<DT>::T* const (&a
   auto b_at = [&](int g, int k0) -> BT {
     if constexpr (DT == DT_F32)
       return wrow[g][k0];
+    else if constexpr (PACKED)
+      return *reinterpret_cast<const u32x4*>(wrow[g] + (size_t)(k0 / KS) * 512);
     else
       return load_w8<AL>(wrow[g] + k0);
   };
@@ -226,7 +241,12 @@ __device__ __forceinline__ void mma_tiles(const typename DType<DT>::T* const (&a
     const int k0 = nsteps * KS, kk = k0 + koff;
     BT b[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) b[g] = load_b_tail<DT>(wrow[g], k0, kk, K);
+    for (int g = 0; g < G; ++g) {
+      if constexpr (PACKED)
+        b[g] = b_at(g, k0);  // the copy holds the zeros past K
+      else
+        b[g] = load_b_tail<DT>(wrow[g], k0, kk, K);
+    }
     mfma_all(k0, b);
   }
 }
@@ -236,12 +256,12 @@ __device__ __forceinline__ void mma_tiles(const typename DType<DT>::T* const (&a
 // in[rows ? rows[r] : r].  Hidden layers (LOGITS false) store
 // tanh(x W^T + b) in the layer dtype to `out`; the output layer stores
 // x W^T + b as float32 to `logits` (columns < N only).
-template <int DT, int G, int MT, int AL, bool LOGITS>
+template <int DT, int G, int MT, int AL, bool LOGITS, bool PK = false>
 __device__ __forceinline__ void mlp_layer_g(const typename DType<DT>::T* in, int lda, const int* rows, int K,
                                             const typename DType<DT>::T* __restrict__ W,
                                             const typename DType<DT>::T* __restrict__ b, int N,
                                             typename DType<DT>::T* out, float* logits, int ldo, int wave, int nwaves,
-                                            int lane) {
+                                            int lane, const typename DType<DT>::T* __restrict__ Wp = nullptr) {
   using T = typename DType<DT>::T;
   using DTy = DType<DT>;
   const int Kpad = round_up(K, DTy::KS);
@@ -261,7 +281,7 @@ __device__ __forceinline__ void mlp_layer_g(const typename DType<DT>::T* in, int
       bias[g] = DTy::to_f32(b[col < N ? col : 0]);
     }
     f32x4 acc[MT][G];
-    mma_tiles<DT, G, MT, AL>(a_row, Kpad, K, W, n0, N, lane, acc);
+    mma_tiles<DT, G, MT, AL, 0, PK>(a_row, Kpad, K, W, n0, N, lane, acc, 16, Wp);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const int col = n0 + 16 * g + (lane & 15);
@@ -281,41 +301,41 @@ __device__ __forceinline__ void mlp_layer_g(const typename DType<DT>::T* in, int
   }
 }
 
-template <int DT, int MT, int AL, bool LOGITS>
+template <int DT, int MT, int AL, bool LOGITS, bool PK = false>
 __device__ __forceinline__ void mlp_layer_mt(const typename DType<DT>::T* in, int lda, const int* rows, int K,
                                              const typename DType<DT>::T* __restrict__ W,
                                              const typename DType<DT>::T* __restrict__ b, int N,
                                              typename DType<DT>::T* out, float* logits, int ldo, int wave,
-                                             int nwaves, int lane) {
+                                             int nwaves, int lane, const typename DType<DT>::T* __restrict__ Wp = nullptr) {
   const int nt = (N + 15) >> 4;
   if (nt >= 4 * nwaves && nt % 4 == 0)
-    mlp_layer_g<DT, 4, MT, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+    mlp_layer_g<DT, 4, MT, AL, LOGITS, PK>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane, Wp);
   else if (nt >= 2 * nwaves && nt % 2 == 0)
-    mlp_layer_g<DT, 2, MT, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+    mlp_layer_g<DT, 2, MT, AL, LOGITS, PK>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane, Wp);
   else
-    mlp_layer_g<DT, 1, MT, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+    mlp_layer_g<DT, 1, MT, AL, LOGITS, PK>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane, Wp);
 }
 
 // Picks the row-tile count (R = 16, 32, 48 or 64) and the widest tile group
 // that still gives every wave work.
-template <int DT, int AL, bool LOGITS>
+template <int DT, int AL, bool LOGITS, bool PK = false>
 __device__ __forceinline__ void mlp_layer_al(const typename DType<DT>::T* in, int lda, const int* rows, int R, int K,
                                              const typename DType<DT>::T* __restrict__ W,
                                              const typename DType<DT>::T* __restrict__ b, int N,
                                              typename DType<DT>::T* out, float* logits, int ldo, int wave,
-                                             int nwaves, int lane) {
+                                             int nwaves, int lane, const typename DType<DT>::T* __restrict__ Wp = nullptr) {
   switch (R >> 4) {
     case 1:
-      mlp_layer_mt<DT, 1, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+      mlp_layer_mt<DT, 1, AL, LOGITS, PK>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane, Wp);
       break;
     case 2:
-      mlp_layer_mt<DT, 2, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+      mlp_layer_mt<DT, 2, AL, LOGITS, PK>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane, Wp);
       break;
     case 3:
-      mlp_layer_mt<DT, 3, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+      mlp_layer_mt<DT, 3, AL, LOGITS, PK>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane, Wp);
       break;
     default:
-      mlp_layer_mt<DT, 4, AL, LOGITS>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane);
+      mlp_layer_mt<DT, 4, AL, LOGITS, PK>(in, lda, rows, K, W, b, N, out, logits, ldo, wave, nwaves, lane, Wp);
   }
 }
 
@@ -336,34 +356,35 @@ __device__ __forceinline__ void mlp_input_layer(const typename DType<DT>::T* in,
 }
 
 // The first layer for an input width KC known at compile time.
-template <int DT, int KC>
+template <int DT, int KC, bool PK = false>
 __device__ __forceinline__ void mlp_input_layer_const(const typename DType<DT>::T* in, int lda, const int* rows,
                                                       int R, const typename DType<DT>::T* __restrict__ W,
                                                       const typename DType<DT>::T* __restrict__ b, int N,
                                                       typename DType<DT>::T* out, int ldo, int wave, int nwaves,
-                                                      int lane) {
+                                                      int lane, const typename DType<DT>::T* __restrict__ Wp = nullptr) {
   constexpr int AL = DT == DT_F32 ? WALIGN_16 : weight_align(KC);
-  mlp_layer_al<DT, AL, false>(in, lda, rows, R, KC, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
+  mlp_layer_al<DT, AL, false, PK>(in, lda, rows, R, KC, W, b, N, out, nullptr, ldo, wave, nwaves, lane, Wp);
 }
 
 // A hidden layer after the first: K (a hidden width) is a multiple of 16.
 // R rows: 16, 32, 48 or 64.
-template <int DT>
+template <int DT, bool PK = false>
 __device__ __forceinline__ void mlp_hidden(const typename DType<DT>::T* in, int lda, int R, int K,
                                            const typename DType<DT>::T* __restrict__ W,
                                            const typename DType<DT>::T* __restrict__ b, int N,
                                            typename DType<DT>::T* out, int ldo, int wave, int nwaves,
-                                           int lane) {
-  mlp_layer_al<DT, WALIGN_16, false>(in, lda, nullptr, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
+                                           int lane, const typename DType<DT>::T* __restrict__ Wp = nullptr) {
+  mlp_layer_al<DT, WALIGN_16, false, PK>(in, lda, nullptr, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane, Wp);
 }
 
 // The output layer: logits = in W^T + b as float32, N <= 32 actions, K a multiple of 16.
-template <int DT>
+template <int DT, bool PK = false>
 __device__ __forceinline__ void mlp_logits(const typename DType<DT>::T* in, int lda, int R, int K,
                                            const typename DType<DT>::T* __restrict__ W,
                                            const typename DType<DT>::T* __restrict__ b, int N, float* out,
-                                           int ldo, int wave, int nwaves, int lane) {
-  mlp_layer_al<DT, WALIGN_16, true>(in, lda, nullptr, R, K, W, b, N, nullptr, out, ldo, wave, nwaves, lane);
+                                           int ldo, int wave, int nwaves, int lane,
+                                           const typename DType<DT>::T* __restrict__ Wp = nullptr) {
+  mlp_layer_al<DT, WALIGN_16, true, PK>(in, lda, nullptr, R, K, W, b, N, nullptr, out, ldo, wave, nwaves, lane, Wp);
 }
 
 }  // namespace rl

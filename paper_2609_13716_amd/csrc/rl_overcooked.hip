@@ -181,7 +181,7 @@ __global__ __launch_bounds__(64) void oc_env_kernel(OcParams p, int32_t* __restr
 
 constexpr int OC_RUN_NT = 512;  // 8 waves: the streamed MLP's chains of a workgroup spread over twice the waves
 
-template <int DT, int TE>
+template <int DT, int TE, bool PK>
 __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArgs pol, int32_t* __restrict__ state,
                                                           uint64_t t0, int n_steps, TrajArgs out) {
   using T = typename DType<DT>::T;
@@ -218,11 +218,14 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     __syncthreads();  // the env lanes' repaint of the previous step is visible
-    mlp_input_layer_const<DT, OC_D>(xs, LDX, nullptr, R, W1, b1, pol.H1, h1, ld1, wave, OC_RUN_NT / 64, lane);
+    mlp_input_layer_const<DT, OC_D, PK>(xs, LDX, nullptr, R, W1, b1, pol.H1, h1, ld1, wave, OC_RUN_NT / 64, lane,
+                                        static_cast<const T*>(pol.Wp[0]));
     __syncthreads();
-    mlp_hidden<DT>(h1, ld1, R, pol.H1, W2, b2, pol.H2, h2, ld2, wave, OC_RUN_NT / 64, lane);
+    mlp_hidden<DT, PK>(h1, ld1, R, pol.H1, W2, b2, pol.H2, h2, ld2, wave, OC_RUN_NT / 64, lane,
+                       static_cast<const T*>(pol.Wp[1]));
     __syncthreads();
-    mlp_logits<DT>(h2, ld2, R, pol.H2, W3, b3, NA, lg, MAX_NA, wave, OC_RUN_NT / 64, lane);
+    mlp_logits<DT, PK>(h2, ld2, R, pol.H2, W3, b3, NA, lg, MAX_NA, wave, OC_RUN_NT / 64, lane,
+                       static_cast<const T*>(pol.Wp[2]));
     __syncthreads();
     for (int idx = tid; idx < R * NA; idx += OC_RUN_NT) {
       const int r = idx / NA, a = idx - r * NA, el = r >> 1, ag = r & 1;
@@ -306,13 +309,13 @@ hipError_t launch_oc_step(const OcParams& p, int32_t* state, uint64_t t0, int n_
   return hipGetLastError();
 }
 
-template <int DT, int TE>
+template <int DT, int TE, bool PK>
 static hipError_t launch_oc_run_te(const OcParams& p, const PolicyArgs& pol, int32_t* state, uint64_t t0,
                                    int n_steps, const TrajArgs& out, size_t lds, hipStream_t s) {
-  hipError_t e = hipFuncSetAttribute((const void*)oc_run_kernel<DT, TE>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)lds);
+  hipError_t e = hipFuncSetAttribute((const void*)oc_run_kernel<DT, TE, PK>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  oc_run_kernel<DT, TE><<<oc_tiles(p.E, TE), OC_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
+  oc_run_kernel<DT, TE, PK><<<oc_tiles(p.E, TE), OC_RUN_NT, lds, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
 }
 
@@ -321,10 +324,13 @@ hipError_t launch_oc_run(const OcParams& p, const PolicyArgs& pol, int32_t* stat
   const int te = oc_run_te(pol);
   const size_t lds = oc_run_lds_bytes_te(pol, te);
   if (pol.dt == DT_F32)
-    return te == 16 ? launch_oc_run_te<DT_F32, 16>(p, pol, state, t0, n_steps, out, lds, s)
-                    : launch_oc_run_te<DT_F32, 8>(p, pol, state, t0, n_steps, out, lds, s);
-  return te == 16 ? launch_oc_run_te<DT_BF16, 16>(p, pol, state, t0, n_steps, out, lds, s)
-                  : launch_oc_run_te<DT_BF16, 8>(p, pol, state, t0, n_steps, out, lds, s);
+    return te == 16 ? launch_oc_run_te<DT_F32, 16, false>(p, pol, state, t0, n_steps, out, lds, s)
+                    : launch_oc_run_te<DT_F32, 8, false>(p, pol, state, t0, n_steps, out, lds, s);
+  if (pol.Wp[0] != nullptr)  // fragment-major weights
+    return te == 16 ? launch_oc_run_te<DT_BF16, 16, true>(p, pol, state, t0, n_steps, out, lds, s)
+                    : launch_oc_run_te<DT_BF16, 8, true>(p, pol, state, t0, n_steps, out, lds, s);
+  return te == 16 ? launch_oc_run_te<DT_BF16, 16, false>(p, pol, state, t0, n_steps, out, lds, s)
+                  : launch_oc_run_te<DT_BF16, 8, false>(p, pol, state, t0, n_steps, out, lds, s);
 }
 
 }  // namespace rl

@@ -425,7 +425,7 @@ __device__ __forceinline__ u32x4 pt_mask8(u32x4 v, int left) {
   return v;
 }
 
-template <int HMAX, int BM, int NB, int MINB>
+template <int HMAX, int BM, int NB, int MINB, bool PK>
 __global__ __launch_bounds__(PT_NT, MINB) void policy_fwd_tiled_kernel(PolicyArgs pol, const uint16_t* __restrict__ obs,
                                                                  const uint8_t* __restrict__ legal, int64_t rows,
                                                                  float* __restrict__ logits) {
@@ -455,7 +455,8 @@ __global__ __launch_bounds__(PT_NT, MINB) void policy_fwd_tiled_kernel(PolicyArg
   // One dense tanh layer of HMAX units: out = tanh(in W^T + b) into hs.
   // Layer 1 (tag true) stages observation rows with the weights; layer 2
   // reads its input from hs.
-  auto layer = [&](auto l1_tag, const uint16_t* __restrict__ W, int K, const float* bias) {
+  auto layer = [&](auto l1_tag, const uint16_t* __restrict__ W, const uint16_t* __restrict__ Wp, int K,
+                   const float* bias) {
     constexpr bool L1 = decltype(l1_tag)::value;
     const int nsteps = (K + PT_KC - 1) / PT_KC;
     // Weight slices are fetched one step before they are stored to LDS (they
@@ -465,14 +466,25 @@ __global__ __launch_bounds__(PT_NT, MINB) void policy_fwd_tiled_kernel(PolicyArg
     u32x4 wv[WV], xv[PX][XV];
     // per-thread byte offsets of the staged vectors (global) and their LDS
     // slots, fixed for the layer; the slice offset goes in a scalar register
-    const __amdgpu_buffer_rsrc_t wres = pt_rsrc(W, (uint32_t)HMAX * K * 2);
+    // PK: weights from the fragment-major copy (1 KB per 16 rows x 32 k),
+    // one contiguous 1 KB block per wave-wide load instead of 16 rows x 64 B
+    const int S = (K + PT_KC - 1) / PT_KC;
+    const __amdgpu_buffer_rsrc_t wres =
+        PK ? pt_rsrc(Wp, (uint32_t)(HMAX / 16) * S * 1024) : pt_rsrc(W, (uint32_t)HMAX * K * 2);
     const __amdgpu_buffer_rsrc_t xres = pt_rsrc(obs + (size_t)row0 * D, (uint32_t)nrow * D * 2);
     int wgo[WV], wlo[WV], xgo[XV], xlo[XV];
 #pragma unroll
     for (int j = 0; j < WV; ++j) {
-      const int v = tid + j * PT_NT, n = v >> 2, q = v & 3;
-      wgo[j] = (n * K + 8 * q) * 2;
-      wlo[j] = pt_slot(n, q);
+      const int v = tid + j * PT_NT;
+      if constexpr (PK) {
+        const int t = v >> 6, l = v & 63;  // operand block of tile t, lane l: row 16t + l % 16, chunk l / 16
+        wgo[j] = (t * S * 64 + l) * 16;
+        wlo[j] = pt_slot(16 * t + (l & 15), l >> 4);
+      } else {
+        const int n = v >> 2, q = v & 3;
+        wgo[j] = (n * K + 8 * q) * 2;
+        wlo[j] = pt_slot(n, q);
+      }
     }
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
@@ -483,7 +495,8 @@ __global__ __launch_bounds__(PT_NT, MINB) void policy_fwd_tiled_kernel(PolicyArg
     constexpr bool XALL = BM * 4 % PT_NT == 0;  // every thread stages XV observation vectors
     auto fetch_w = [&](int st) {
 #pragma unroll
-      for (int j = 0; j < WV; ++j) wv[j] = __builtin_amdgcn_raw_buffer_load_b128(wres, wgo[j], st * PT_KC * 2, 0);
+      for (int j = 0; j < WV; ++j)
+        wv[j] = __builtin_amdgcn_raw_buffer_load_b128(wres, wgo[j], PK ? st * 1024 : st * PT_KC * 2, 0);
     };
     auto fetch_x = [&](int st, u32x4 (&x)[XV]) {
       if constexpr (L1) {
@@ -501,7 +514,8 @@ __global__ __launch_bounds__(PT_NT, MINB) void policy_fwd_tiled_kernel(PolicyArg
       const int left = K - k0 - 8 * (tid & 3);
       uint16_t* wb = wst + (st % NB) * (HMAX * PT_KC);
 #pragma unroll
-      for (int j = 0; j < WV; ++j) *reinterpret_cast<u32x4*>(wb + wlo[j]) = part ? pt_mask8(wv[j], left) : wv[j];
+      for (int j = 0; j < WV; ++j)  // (the packed copy already holds zeros past K)
+        *reinterpret_cast<u32x4*>(wb + wlo[j]) = (part && !PK) ? pt_mask8(wv[j], left) : wv[j];
       if constexpr (L1) {
         uint16_t* xb = xst + (st % NB) * (BM * PT_KC);
 #pragma unroll
@@ -615,8 +629,9 @@ __global__ __launch_bounds__(PT_NT, MINB) void policy_fwd_tiled_kernel(PolicyArg
     }
     __syncthreads();
   };
-  layer(std::true_type{}, static_cast<const uint16_t*>(pol.W[0]), D, bias_s);
-  layer(std::false_type{}, static_cast<const uint16_t*>(pol.W[1]), HMAX, bias_s + HMAX);
+  layer(std::true_type{}, static_cast<const uint16_t*>(pol.W[0]), static_cast<const uint16_t*>(pol.Wp[0]), D, bias_s);
+  layer(std::false_type{}, static_cast<const uint16_t*>(pol.W[1]), static_cast<const uint16_t*>(pol.Wp[1]), HMAX,
+        bias_s + HMAX);
 
   // layer 3, transposed: logits^T = W3 h2^T, items (action tile, row tile)
   constexpr int K3 = HMAX / PT_KC;
@@ -649,22 +664,29 @@ __global__ __launch_bounds__(PT_NT, MINB) void policy_fwd_tiled_kernel(PolicyArg
   }
 }
 
-template <int HMAX, int BM, int NB, int MINB>
-static hipError_t launch_policy_tiled(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
-                                      float* logits, hipStream_t s) {
+template <int HMAX, int BM, int NB, int MINB, bool PK>
+static hipError_t launch_policy_tiled_pk(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
+                                         float* logits, hipStream_t s) {
   using L = PtLayout<HMAX, BM, NB>;
   static_assert(L::TOTAL <= MAX_LDS_BYTES, "tile fits in LDS");
   static bool attr = false;
   if (!attr) {
-    const hipError_t e = hipFuncSetAttribute((const void*)policy_fwd_tiled_kernel<HMAX, BM, NB, MINB>,
+    const hipError_t e = hipFuncSetAttribute((const void*)policy_fwd_tiled_kernel<HMAX, BM, NB, MINB, PK>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::TOTAL);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const unsigned grid = (unsigned)((rows + BM - 1) / BM);
-  policy_fwd_tiled_kernel<HMAX, BM, NB, MINB><<<dim3(grid), PT_NT, L::TOTAL, s>>>(
+  policy_fwd_tiled_kernel<HMAX, BM, NB, MINB, PK><<<dim3(grid), PT_NT, L::TOTAL, s>>>(
       pol, static_cast<const uint16_t*>(obs), legal, rows, logits);
   return hipGetLastError();
+}
+
+template <int HMAX, int BM, int NB, int MINB>
+static hipError_t launch_policy_tiled(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,
+                                      float* logits, hipStream_t s) {
+  return pol.Wp[0] != nullptr ? launch_policy_tiled_pk<HMAX, BM, NB, MINB, true>(pol, obs, legal, rows, logits, s)
+                              : launch_policy_tiled_pk<HMAX, BM, NB, MINB, false>(pol, obs, legal, rows, logits, s);
 }
 
 // Shapes the tiled kernel serves: bf16, two hidden layers of 256 or of 512
@@ -679,6 +701,42 @@ static bool try_launch_policy_tiled(const PolicyArgs& pol, const void* obs, cons
   else
     return false;
   return true;
+}
+
+// ---------------------------------------------------- packed weights ----
+//
+// Writes the fragment-major copy of one bf16 layer W [N x K] (layout in
+// packed_layer_offset): one thread per 16-byte operand block, zero outside W.
+__global__ void policy_pack_kernel(const uint16_t* __restrict__ W, int N, int K, uint16_t* __restrict__ out,
+                                   int64_t nvec) {
+  const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= nvec) return;
+  const int S = (K + 31) / 32;
+  const int lane = (int)(v & 63);
+  const int64_t ts = v >> 6;
+  const int s = (int)(ts % S), t = (int)(ts / S);
+  const int n = 16 * t + (lane & 15), k0 = 32 * s + 8 * (lane >> 4);
+  uint32_t h[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t lo = (n < N && k0 + 2 * q < K) ? W[(size_t)n * K + k0 + 2 * q] : 0u;
+    const uint32_t hi = (n < N && k0 + 2 * q + 1 < K) ? W[(size_t)n * K + k0 + 2 * q + 1] : 0u;
+    h[q] = lo | (hi << 16);
+  }
+  *reinterpret_cast<u32x4*>(out + v * 8) = u32x4{h[0], h[1], h[2], h[3]};
+}
+
+hipError_t launch_policy_pack(const PolicyArgs& pol, void* packed, hipStream_t s) {
+  const int dims[4] = {pol.D, pol.H1, pol.H2, pol.NA};
+  for (int l = 0; l < 3; ++l) {
+    const int64_t nvec = (int64_t)(packed_layer_bytes(dims[l + 1], dims[l]) / 16);
+    uint16_t* out = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(packed) + packed_layer_offset(dims, l));
+    policy_pack_kernel<<<dim3((unsigned)((nvec + 255) / 256)), 256, 0, s>>>(static_cast<const uint16_t*>(pol.W[l]),
+                                                                          dims[l + 1], dims[l], out, nvec);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_policy_forward(const PolicyArgs& pol, const void* obs, const uint8_t* legal, int64_t rows,

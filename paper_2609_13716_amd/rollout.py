@@ -48,7 +48,7 @@ class _EnvConfig(ctypes.Structure):
 
 class _Policy(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("dims", ctypes.c_int32 * 4),
-                ("W", ctypes.c_void_p * 3), ("b", ctypes.c_void_p * 3)]
+                ("W", ctypes.c_void_p * 3), ("b", ctypes.c_void_p * 3), ("packed", ctypes.c_void_p)]
 
 
 class _Traj(ctypes.Structure):
@@ -108,6 +108,9 @@ def _load():
     lib.rollout_run_s5.argtypes = [cfgp, s5p, P, P, ctypes.c_uint64, ctypes.c_int32, ctypes.POINTER(_Traj),
                                    ctypes.POINTER(_AcTraj), P, ctypes.c_size_t, P]
     lib.rollout_run_s5.restype = st
+    lib.rl_policy_packed_bytes.argtypes = [ctypes.POINTER(_Policy)]
+    lib.rl_policy_packed_bytes.restype = ctypes.c_size_t
+    lib.rl_policy_pack.argtypes, lib.rl_policy_pack.restype = [ctypes.POINTER(_Policy), P, P], st
     return lib
 
 
@@ -117,7 +120,7 @@ lib = _load()
 EXPORTED = ("rl_state_bytes", "rl_obs_dim", "rl_num_actions", "rollout_last_error", "rollout_init",
             "rollout_step", "policy_forward", "rollout_run", "rollout_sample", "rl_gumbel_noise", "rollout_run_pop",
             "rollout_run_ac", "rl_gae", "rl_s5_discretize", "rl_s5_workspace_bytes", "rollout_run_s5",
-            "rollout_run_teams")
+            "rollout_run_teams", "rl_policy_packed_bytes", "rl_policy_pack")
 HEURISTICS = ("greedy_closest_self", "greedy_closest_teammate", "greedy_closest_avg", "greedy_lowest_level",
               "greedy_highest_level", "seq_lexicographic", "seq_reverse_lexicographic", "seq_column_major",
               "seq_reverse_column_major")  # kind k of rollout_run_teams
@@ -211,14 +214,26 @@ def rl_num_actions(cfg):
 
 
 class Policy:
-    """Device weights of the 3-layer MLP in the nn.Linear layout, and the C struct pointing at them."""
+    """Device weights of the 3-layer MLP in the nn.Linear layout, and the C struct pointing at them.
 
-    def __init__(self, weights, biases, dtype="f32", device="cuda"):
+    ``pack`` (bf16 only; default on): also keep the fragment-major copy that
+    ``rl_policy_pack`` writes, which the streamed-weight rollout kernels read.
+    """
+
+    def __init__(self, weights, biases, dtype="f32", device="cuda", pack=True):
         self.dtype = _DT_CODE[dtype]
         tdt = _TORCH_DT[self.dtype]
         self.W = [torch.as_tensor(w).to(device=device, dtype=tdt).contiguous() for w in weights]
         self.b = [torch.as_tensor(b).to(device=device, dtype=tdt).contiguous() for b in biases]
         self.dims = [self.W[0].shape[1]] + [w.shape[0] for w in self.W]
+        self.packed = None
+        if pack and self.dtype == _DT_CODE["bf16"]:
+            pc = self.c()
+            n = lib.rl_policy_packed_bytes(ctypes.byref(pc))
+            if n == 0:
+                raise RolloutError(RL_EINVAL, lib.rollout_last_error().decode())
+            self.packed = torch.empty(n, dtype=torch.uint8, device=device)
+            _check(lib.rl_policy_pack(ctypes.byref(pc), self.packed.data_ptr(), _stream(None)))
 
     @property
     def torch_dtype(self):
@@ -233,6 +248,7 @@ class Policy:
         for i in range(3):
             p.W[i] = self.W[i].data_ptr()
             p.b[i] = self.b[i].data_ptr()
+        p.packed = self.packed.data_ptr() if getattr(self, "packed", None) is not None else None
         return p
 
 

@@ -252,3 +252,28 @@ def test_s5_checks_before_launch():
     assert L.rl_s5_discretize(0, 4, None, None, None, None, None, None) == R.RL_EINVAL
     assert L.rl_s5_discretize(4, 4, ctypes.c_void_p(0x1000), None, ctypes.c_void_p(0x1000),
                               ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), None) == R.RL_EINVAL
+
+
+def test_packed_weight_queries():
+    """rl_policy_packed_bytes: ceil(N/16) * ceil(K/32) KB per layer, each layer at a 256-byte boundary;
+    0 for float32 policies and for a packed pointer that is not 16-byte aligned or not bf16."""
+    for dims in [(658, 512, 512, 20), (1170, 256, 256, 6), (27, 16, 32, 6), (300, 48, 32, 7)]:
+        p = _policy_struct(R.RL_BF16, dims)
+        want = 0
+        for l in range(3):
+            n = -(-dims[l + 1] // 16) * -(-dims[l] // 32) * 1024
+            want += n if l == 2 else -(-n // 256) * 256
+        assert R.lib.rl_policy_packed_bytes(p) == want
+    assert R.lib.rl_policy_packed_bytes(_policy_struct(R.RL_F32, (192, 64, 64, 6))) == 0
+    p = _policy_struct(R.RL_BF16)
+    p.packed = 4104  # not 16-byte aligned
+    assert R.lib.rl_policy_packed_bytes(p) == 0
+    assert "aligned" in R.lib.rollout_last_error().decode()
+    p = _policy_struct(R.RL_F32)
+    p.packed = 4096
+    assert R.lib.rl_policy_packed_bytes(p) == 0
+    assert "bf16" in R.lib.rollout_last_error().decode()
+    q = _policy_struct(R.RL_F32)
+    assert R.lib.rl_policy_pack(q, 4096, None) == R.RL_EUNSUPPORTED
+    assert R.lib.rl_policy_pack(_policy_struct(R.RL_BF16), None, None) == R.RL_EINVAL
+
