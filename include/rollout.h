@@ -114,9 +114,9 @@ typedef struct {
   const void* b[3];
   /* Optional (RL_BF16 only): a copy of W[0..2] in the fragment-major layout
    * written by rl_policy_pack, or NULL.  When set, the streamed-weight
-   * rollout kernels (kitchen and Hanabi rollouts) read their operands from it,
-   * 1 KB contiguous per load instead of 16 rows x 64 bytes; results are
-   * bit-identical to reading W.  Must be 16-byte aligned and stay valid and
+   * kernels (the kitchen and Hanabi rollouts, the wide-layer policy_forward)
+   * read their operands from it, 1 KB contiguous per load instead of 16 rows
+   * x 64 bytes; results are bit-identical to reading W.  Must be 16-byte aligned and stay valid and
    * unchanged while calls that use the policy run. */
   const void* packed;
 } rl_policy;
@@ -239,6 +239,9 @@ rl_status rl_gae(const float* reward, const uint8_t* done, const float* value, c
  *                 ([n_policies, dims[l+1], dims[l]] row-major) and b[l] at
  *                 [n_policies, dims[l+1]]; device memory, read.
  *   n_policies    1..4096.
+ *                 pop->packed (optional, bf16): n_policies packed copies
+ *                 (rl_policy_pack of each policy), policy q at
+ *                 q * rl_policy_packed_bytes(pop) bytes.
  *   policy_index  [E, A] int32 device, read: agent a of env e acts with policy
  *                 policy_index[e * A + a]; an index outside 0..n_policies-1
  *                 selects policy 0.

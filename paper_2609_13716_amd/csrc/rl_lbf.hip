@@ -434,7 +434,7 @@ size_t lbf_pop_lds_bytes(const LbfParams& p, const PolicyArgs& pol) {
   return off + (size_t)(3 * RL.R + 17) * 4 + (size_t)RL.R * MAX_NA * 4;
 }
 
-template <int DT>
+template <int DT, bool PK>
 __global__ __launch_bounds__(NTHREADS) void lbf_run_pop_kernel(LbfParams p, LbfMagic m, PolicyArgs pol, int n_pol,
                                                                const int32_t* __restrict__ pidx,
                                                                int32_t* __restrict__ state, uint64_t t0,
@@ -460,6 +460,7 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_pop_kernel(LbfParams p, LbfM
   const int e0 = blockIdx.x * TILE_E;
   const int te_valid = min(TILE_E, p.E - e0);
   const int A = p.A, D = p.D, NA = pol.NA, H1 = pol.H1, H2 = pol.H2;
+  const int dims4[4] = {D, H1, H2, NA};
   T* gobs = static_cast<T*>(out.obs);
 
   zero_lds(smem, RL.total, tid);  // zero grids and the K padding of every operand tile
@@ -514,11 +515,16 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_pop_kernel(LbfParams p, LbfM
       const T* b1 = static_cast<const T*>(pol.b[0]) + q * H1;
       const T* b2 = static_cast<const T*>(pol.b[1]) + q * H2;
       const T* b3 = static_cast<const T*>(pol.b[2]) + q * NA;
-      mlp_input_layer<DT>(xs, RL.ldx, order + g0, R16, D, W1, b1, H1, h1, RL.ld1, wave, NTHREADS / 64, lane);
+      // PK: policy q's fragment-major copy starts q whole packed policies in
+      const size_t pq = PK ? q * (packed_layer_offset(dims4, 2) + packed_layer_bytes(NA, H2)) : 0;
+      const T* Wp1 = PK ? reinterpret_cast<const T*>(static_cast<const uint8_t*>(pol.Wp[0]) + pq) : nullptr;
+      const T* Wp2 = PK ? reinterpret_cast<const T*>(static_cast<const uint8_t*>(pol.Wp[1]) + pq) : nullptr;
+      const T* Wp3 = PK ? reinterpret_cast<const T*>(static_cast<const uint8_t*>(pol.Wp[2]) + pq) : nullptr;
+      mlp_input_layer<DT, PK>(xs, RL.ldx, order + g0, R16, D, W1, b1, H1, h1, RL.ld1, wave, NTHREADS / 64, lane, Wp1);
       __syncthreads();
-      mlp_hidden<DT>(h1, RL.ld1, R16, H1, W2, b2, H2, h2, RL.ld2, wave, NTHREADS / 64, lane);
+      mlp_hidden<DT, PK>(h1, RL.ld1, R16, H1, W2, b2, H2, h2, RL.ld2, wave, NTHREADS / 64, lane, Wp2);
       __syncthreads();
-      mlp_logits<DT>(h2, RL.ld2, R16, H2, W3, b3, NA, lgc, MAX_NA, wave, NTHREADS / 64, lane);
+      mlp_logits<DT, PK>(h2, RL.ld2, R16, H2, W3, b3, NA, lgc, MAX_NA, wave, NTHREADS / 64, lane, Wp3);
       __syncthreads();
       for (int idx = tid; idx < cnt * NA; idx += NTHREADS) {
         const int r = idx / NA, a = idx - r * NA;
@@ -584,21 +590,30 @@ hipError_t launch_lbf_run_pop(const LbfParams& p, const PolicyArgs& pol, int n_p
   if (pol.dt == DT_F32) {
     static bool attr = false;
     if (!attr) {
-      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_F32>,
+      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_F32, false>,
                                                hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
       if (e != hipSuccess) return e;
       attr = true;
     }
-    lbf_run_pop_kernel<DT_F32><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
+    lbf_run_pop_kernel<DT_F32, false><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
+  } else if (pol.Wp[0] != nullptr) {  // fragment-major weights
+    static bool attr = false;
+    if (!attr) {
+      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_BF16, true>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+    lbf_run_pop_kernel<DT_BF16, true><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
   } else {
     static bool attr = false;
     if (!attr) {
-      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_BF16>,
+      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_BF16, false>,
                                                hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
       if (e != hipSuccess) return e;
       attr = true;
     }
-    lbf_run_pop_kernel<DT_BF16><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
+    lbf_run_pop_kernel<DT_BF16, false><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
   }
   return hipGetLastError();
 }

@@ -340,19 +340,19 @@ __device__ __forceinline__ void mlp_layer_al(const typename DType<DT>::T* in, in
 }
 
 // The first layer for any input width K (picks the weight-load width at run time).
-template <int DT>
+template <int DT, bool PK = false>
 __device__ __forceinline__ void mlp_input_layer(const typename DType<DT>::T* in, int lda, const int* rows, int R,
                                                 int K, const typename DType<DT>::T* __restrict__ W,
                                                 const typename DType<DT>::T* __restrict__ b, int N,
                                                 typename DType<DT>::T* out, int ldo, int wave, int nwaves,
-                                                int lane) {
+                                                int lane, const typename DType<DT>::T* __restrict__ Wp = nullptr) {
   const int al = DT == DT_F32 ? WALIGN_16 : weight_align(K);
   if (al == WALIGN_16)
-    mlp_layer_al<DT, WALIGN_16, false>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
+    mlp_layer_al<DT, WALIGN_16, false, PK>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane, Wp);
   else if (al == WALIGN_4)
-    mlp_layer_al<DT, WALIGN_4, false>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
+    mlp_layer_al<DT, WALIGN_4, false, PK>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane, Wp);
   else
-    mlp_layer_al<DT, WALIGN_2, false>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane);
+    mlp_layer_al<DT, WALIGN_2, false, PK>(in, lda, rows, R, K, W, b, N, out, nullptr, ldo, wave, nwaves, lane, Wp);
 }
 
 // The first layer for an input width KC known at compile time.

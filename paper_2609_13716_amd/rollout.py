@@ -256,9 +256,11 @@ class Population:
     """Device weights of n policies of one shape, stacked per layer ([n, fan_out, fan_in] and [n, fan_out]).
 
     ``weights[p]`` / ``biases[p]`` are policy p's layers in the nn.Linear layout.
+    ``pack`` (bf16 only; default on): also keep the policies' fragment-major copies, policy p
+    at p * rl_policy_packed_bytes, which the population rollout reads.
     """
 
-    def __init__(self, weights, biases, dtype="f32", device="cuda"):
+    def __init__(self, weights, biases, dtype="f32", device="cuda", pack=True):
         if len(weights) < 1 or len(weights) != len(biases):
             raise ValueError("a population needs one (weights, biases) pair per policy")
         self.dtype = _DT_CODE[dtype]
@@ -269,6 +271,18 @@ class Population:
         self.b = [torch.stack([torch.as_tensor(b[l]) for b in biases]).to(device=device, dtype=tdt).contiguous()
                   for l in range(3)]
         self.dims = [self.W[0].shape[2]] + [w.shape[1] for w in self.W]
+        self.packed = None
+        if pack and self.dtype == _DT_CODE["bf16"]:
+            pc = self.c()
+            per = lib.rl_policy_packed_bytes(ctypes.byref(pc))
+            if per == 0:
+                raise RolloutError(RL_EINVAL, lib.rollout_last_error().decode())
+            self.packed = torch.empty(self.n * per, dtype=torch.uint8, device=device)
+            for q in range(self.n):
+                for i in range(3):
+                    pc.W[i] = self.W[i][q].data_ptr()
+                    pc.b[i] = self.b[i][q].data_ptr()
+                _check(lib.rl_policy_pack(ctypes.byref(pc), self.packed.data_ptr() + q * per, _stream(None)))
 
     @property
     def torch_dtype(self):
@@ -283,6 +297,7 @@ class Population:
         for i in range(3):
             p.W[i] = self.W[i].data_ptr()
             p.b[i] = self.b[i].data_ptr()
+        p.packed = self.packed.data_ptr() if getattr(self, "packed", None) is not None else None
         return p
 
 

@@ -103,3 +103,29 @@ def test_packed_policy_forward_equals_unpacked(dims):
     a = R.policy_forward(R.Policy(ws, bs, "bf16"), x).cpu()
     b = R.policy_forward(R.Policy(ws, bs, "bf16", pack=False), x).cpu()
     assert torch.equal(a, b)
+
+
+def test_packed_population_rollout_equals_unpacked():
+    """Population rollouts read policy q's packed copy at q * rl_policy_packed_bytes: same trajectories."""
+    require_gpu()
+    _note("packed vs unpacked population rollout")
+    dims = (192, 64, 32, 6)
+    nets = [workloads.policy_weights(dims, seed=30 + q, bias_scale=0.3) for q in range(5)]
+    E, T = 37, 30
+    cfg = R.EnvConfig(n_envs=E, seed=4)
+    idx = torch.from_numpy(np.random.default_rng(2).integers(0, 5, size=(E, 2)).astype(np.int32)).cuda()
+    res = []
+    for pk in (True, False):
+        pop = R.Population([w for w, _ in nets], [b for _, b in nets], "bf16", pack=pk)
+        state = R.new_state(cfg)
+        R.rollout_init(cfg, state)
+        out = dict(obs=torch.empty(T, E, 2, 192, dtype=torch.bfloat16, device="cuda"),
+                   actions=torch.empty(T, E, 2, dtype=torch.int32, device="cuda"),
+                   logits=torch.empty(T, E, 2, 6, device="cuda"),
+                   reward=torch.empty(T, E, device="cuda"), done=torch.empty(T, E, dtype=torch.uint8, device="cuda"))
+        R.rollout_run_pop(cfg, pop, idx, state, 0, T, **out)
+        torch.cuda.synchronize()
+        out["state"] = state
+        res.append({k: v.cpu() for k, v in out.items()})
+    for k in res[0]:
+        assert torch.equal(res[0][k], res[1][k]), k
