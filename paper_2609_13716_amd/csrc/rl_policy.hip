@@ -230,7 +230,11 @@ __global__ __launch_bounds__(256, MINB) void policy_fwd_pipe_kernel(PolicyArgs p
   constexpr int LDX = lds_ld<DT>(D), LD1 = lds_ld<DT>(H1), LD2 = lds_ld<DT>(H2);
   constexpr int K3 = round_up(H2, DType<DT>::KS) / DType<DT>::KS;
   constexpr int VE = 16 / sizeof(T);
-  static_assert(D % VE == 0, "observation rows are whole 16-byte vectors");
+  // rows of D elements: whole 16-byte vectors, or (FLAT) a tile read as one
+  // flat block of BM * D elements (16-byte aligned when BM * D is a multiple
+  // of 8) and scattered into the LDS rows element by element
+  constexpr bool FLAT = D % VE != 0;
+  static_assert(!FLAT || (BM * D) % VE == 0, "flat observation tiles start on 16-byte boundaries");
   static_assert(NA <= 16, "one transposed M tile of actions");
   static_assert(MT <= NW, "one layer-3 M tile per wave");
   __shared__ __align__(16) T xs[2][BM * LDX];
@@ -263,7 +267,7 @@ __global__ __launch_bounds__(256, MINB) void policy_fwd_pipe_kernel(PolicyArgs p
   const int64_t ntiles = (rows + BM - 1) / BM;
   const int nt = (int64_t)blockIdx.x < ntiles ? (int)((ntiles - 1 - blockIdx.x) / gridDim.x) + 1 : 0;
   auto tile_of = [&](int j) { return (int64_t)blockIdx.x + (int64_t)j * gridDim.x; };
-  constexpr int VPR = D / VE, NV = BM * VPR, IT = (NV + NT - 1) / NT;
+  constexpr int VPR = D / VE, NV = FLAT ? BM * D / VE : BM * VPR, IT = (NV + NT - 1) / NT;
   u32x4 v[IT];
   auto prefetch = [&](int j) {  // tile j of this workgroup into registers (zeros past the last)
     const int64_t row0 = tile_of(j) * BM;
@@ -271,17 +275,45 @@ __global__ __launch_bounds__(256, MINB) void policy_fwd_pipe_kernel(PolicyArgs p
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int i = tid + it * NT;
-      const int r = i / VPR, c = (i - r * VPR) * VE;
-      v[it] = (i < NV && r < nrow) ? *reinterpret_cast<const u32x4*>(obs + (size_t)(row0 + r) * D + c)
-                                    : u32x4{0u, 0u, 0u, 0u};
+      if constexpr (FLAT) {
+        // flat element i * VE of the tile; the vector that holds the tile's
+        // last element is read element by element (nothing past the batch)
+        const int nel = nrow * D, e0 = i * VE;
+        const T* src = obs + (size_t)row0 * D + e0;
+        if (i < NV && e0 + VE <= nel) {
+          v[it] = *reinterpret_cast<const u32x4*>(src);
+        } else {
+          uint32_t h[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t lo = (i < NV && e0 + 2 * q < nel) ? (uint32_t)src[2 * q] : 0u;
+            const uint32_t hi = (i < NV && e0 + 2 * q + 1 < nel) ? (uint32_t)src[2 * q + 1] : 0u;
+            h[q] = lo | (hi << 16);
+          }
+          v[it] = u32x4{h[0], h[1], h[2], h[3]};
+        }
+      } else {
+        const int r = i / VPR, c = (i - r * VPR) * VE;
+        v[it] = (i < NV && r < nrow) ? *reinterpret_cast<const u32x4*>(obs + (size_t)(row0 + r) * D + c)
+                                      : u32x4{0u, 0u, 0u, 0u};
+      }
     }
   };
   auto stage = [&](T* dst) {
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int i = tid + it * NT;
-      const int r = i / VPR, c = (i - r * VPR) * VE;
-      if (i < NV) *reinterpret_cast<u32x4*>(dst + r * LDX + c) = v[it];
+      if (i >= NV) continue;
+      if constexpr (FLAT) {
+#pragma unroll
+        for (int q = 0; q < VE; ++q) {
+          const int el = i * VE + q, r = el / D, c = el - r * D;
+          dst[r * LDX + c] = (T)((v[it][q >> 1] >> (16 * (q & 1))) & 0xffffu);
+        }
+      } else {
+        const int r = i / VPR, c = (i - r * VPR) * VE;
+        *reinterpret_cast<u32x4*>(dst + r * LDX + c) = v[it];
+      }
     }
   };
 
@@ -362,6 +394,10 @@ static bool try_launch_policy_reg(const PolicyArgs& pol, const void* obs, const 
   // (dtype, D, H1, H2, nA, waves, 16-row M tiles per workgroup tile, workgroups per CU)
   if (pol.dt == DT_BF16 && pol.D == 192 && pol.H1 == 128 && pol.H2 == 128 && pol.NA == 6) {
     *err = launch_policy_pipe<192, 128, 128, 6, 2, 2>(pol, obs, legal, rows, logits, s);
+    return true;
+  }
+  if (pol.dt == DT_BF16 && pol.D == 147 && pol.H1 == 128 && pol.H2 == 128 && pol.NA == 6) {  // 7 x 7 LBF
+    *err = launch_policy_pipe<147, 128, 128, 6, 2, 2>(pol, obs, legal, rows, logits, s);
     return true;
   }
   RL_PF_CASE(DT_F32, 192, 128, 128, 6, 4, 4, 1)

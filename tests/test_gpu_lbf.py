@@ -205,7 +205,7 @@ def test_brute_force_3x3_gpu():
 
 # ------------------------------------------------------------------ policy
 
-@pytest.mark.parametrize("dims", [(192, 64, 64, 6), (192, 128, 128, 6), (432, 256, 256, 6), (27, 16, 32, 6),
+@pytest.mark.parametrize("dims", [(192, 64, 64, 6), (192, 128, 128, 6), (147, 128, 128, 6), (432, 256, 256, 6), (27, 16, 32, 6),
                                   (658, 512, 512, 20), (1170, 256, 256, 6), (1170, 64, 96, 6), (300, 512, 32, 20)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_policy_forward_parity(dims, dtype):
@@ -228,7 +228,7 @@ def test_policy_forward_parity(dims, dtype):
 
 
 @pytest.mark.parametrize("rows", [256 * 64 + 5, 3 * 256 * 64 + 37])
-@pytest.mark.parametrize("dims", [(192, 128, 128, 6), (192, 64, 64, 6)])
+@pytest.mark.parametrize("dims", [(192, 128, 128, 6), (192, 64, 64, 6), (147, 128, 128, 6)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_policy_forward_many_tiles(rows, dims, dtype):
     """Batches that give every workgroup of the persistent policy kernels several 64-row tiles
@@ -409,7 +409,7 @@ def test_rollout_run_12x12_small_full_parity():
 
 
 @pytest.mark.parametrize("name,dtype", [("lbf8_4096", "bf16"), ("lbf8_4096", "f32"), ("lbf8_small", "f32"),
-                                        ("lbf12_16k", "bf16")])
+                                        ("lbf12_16k", "bf16"), ("lbf7_const_4096", "bf16")])
 def test_rollout_logits_equal_policy_forward(name, dtype):
     """The logits a rollout samples from are exactly policy_forward of the recorded observations."""
     require_gpu()
