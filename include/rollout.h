@@ -70,11 +70,15 @@ enum { RL_F32 = 0, RL_BF16 = 1 };
  * 6 actions (0 noop, 1 north, 2 south, 3 west, 4 east, 5 interact).  Rules in
  * the Overcooked section below.
  *
- * Hanabi: n_agents == 2 and the standard game (hn_colors 5, hn_ranks 5,
- * hn_hand_size 5, hn_info_tokens 8, hn_life_tokens 3; other positive values
- * give RL_EUNSUPPORTED), max_steps >= 1 (truncation; a game cannot last 100
- * moves, so 1000 never truncates).  Observations have 658 features (0/1) per
- * agent and there are 20 actions; rules in the Hanabi section below.
+ * Hanabi: n_agents == 2, hn_hand_size 5, hn_info_tokens 8, hn_life_tokens 3,
+ * and either the standard game (hn_colors 5, hn_ranks 5: 658 features (0/1)
+ * per agent, 20 actions) or the mini game of the paper's environment table
+ * (hn_colors 3, hn_ranks 3: 18 cards with 3, 2, 1 copies of ranks 1..3 per
+ * colour, 278 features, 16 actions: 5 discards, 5 plays, 3 colour and 3 rank
+ * hints); any other positive sizes give RL_EUNSUPPORTED.  max_steps >= 1
+ * (truncation; a game cannot last 100 moves, so 1000 never truncates).  Rules
+ * in the Hanabi section below (written for 5 x 5; the mini game sizes every
+ * section by its colours and ranks).
  * Fields of another kind must be 0 (RL_EINVAL otherwise). */
 typedef struct {
   int32_t kind;            /* RL_ENV_* */
@@ -190,17 +194,21 @@ size_t rl_policy_packed_bytes(const rl_policy* policy);
  * policy->packed is ignored.  RL_EUNSUPPORTED for a float32 policy. */
 rl_status rl_policy_pack(const rl_policy* policy, void* packed, void* stream);
 
-/* pi(. | o): policy logits for `rows` observations.
+/* pi(. | o): the logits of the decentralised policy pi_i(a_i | o_i) of
+ * Section 3 (problem setting: each agent acts on its own observation) for
+ * `rows` observations, i.e. the policy network of the step on its own.
  *   obs    [rows, D] of policy->dtype, read.
  *   legal  [rows, nA] uint8 or NULL (all legal); an illegal action's logit is -inf.
  *   logits [rows, nA] float32, written. */
 rl_status policy_forward(const rl_policy* policy, const void* obs, const uint8_t* legal,
                          int64_t rows, float* logits, void* stream);
 
-/* The full rollout loop: for t = t0 .. t0+n_steps-1, every env observes,
- * every agent samples a_t from pi(. | o_t) by Gumbel-max, the env steps and
- * auto-resets; results go to `out` (any field NULL = skipped).  Runs as one
- * persistent kernel; `state` is left at step t0 + n_steps. */
+/* The full rollout loop of the Dec-POMDP step of Section 3 (problem
+ * setting): for t = t0 .. t0+n_steps-1, every env observes (o_i of s), every
+ * agent samples a_i from pi(. | o_i) by Gumbel-max, the joint action moves
+ * the env through P and yields the shared reward r(s, a), and an ended
+ * episode restarts from rho; results go to `out` (any field NULL = skipped).
+ * Runs as one persistent kernel; `state` is left at step t0 + n_steps. */
 rl_status rollout_run(const rl_env_config* cfg, const rl_policy* policy, void* state,
                       uint64_t t0, int32_t n_steps, const rl_traj* out, void* stream);
 

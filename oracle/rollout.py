@@ -76,7 +76,9 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     ``policy_logits``); ``weights`` and ``biases`` are then per policy.
     ``value_head``: the network has nA + 1 outputs, the last being the
     critic's value V(o); the result then also holds ``value`` [T, n, A],
-    ``value_last`` [n, A] (V of obs_last) and ``logp`` [T, n, A], the float64
+    ``value_last`` [n, A] (V of obs_last), ``logits_last`` [n, A, nA] (the
+    logits of obs_last, for scaling value_last's tolerance like the values of
+    the steps) and ``logp`` [T, n, A], the float64
     log-probability of each sampled action under the float32 logits it was
     sampled from (``logits`` keeps the nA action logits).
     ``recurrent``: an ``s5.Params`` actor-critic that replaces (weights,
@@ -149,7 +151,9 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     res = {k: np.stack(v) if v else None for k, v in out.items()}
     res["obs_last"], res["mask_last"] = observe_all(env, cfg, states)
     if value_head:
-        res["value_last"] = net(res["obs_last"], states, False)[..., nA]
+        last = net(res["obs_last"], states, False)
+        res["value_last"] = last[..., nA]
+        res["logits_last"] = last[..., :nA]
     res["states"] = states
     if recurrent is not None:
         res["carry"] = carry

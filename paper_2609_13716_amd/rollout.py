@@ -201,6 +201,19 @@ def _need(t, name, dtype=None, shape=None):
         raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
 
 
+def _need_state(cfg, state):
+    """The env state buffer: a contiguous int32 device tensor of exactly rl_state_bytes(cfg) bytes."""
+    if state is None:
+        raise ValueError("state is required")
+    n = rl_state_bytes(cfg)
+    if n == 0:
+        _check(lib.rl_obs_dim(ctypes.byref(cfg.c())))
+    if state.numel() * state.element_size() != n:
+        raise ValueError(f"state holds {state.numel() * state.element_size()} bytes; "
+                         f"this config needs rl_state_bytes = {n}")
+    _need(state, "state", torch.int32)
+
+
 def rl_state_bytes(cfg):
     return lib.rl_state_bytes(ctypes.byref(cfg.c()))
 
@@ -312,7 +325,7 @@ def new_state(cfg, device="cuda"):
 def rollout_init(cfg, state, obs=None, legal=None, stream=None):
     E, A = cfg.n_envs, cfg.n_agents
     D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
-    _need(state, "state", torch.int32)
+    _need_state(cfg, state)
     if obs is not None:
         _need(obs, "obs", shape=(E, A, D))
     _need(legal, "legal", torch.uint8, (E, A, nA))
@@ -323,7 +336,7 @@ def rollout_init(cfg, state, obs=None, legal=None, stream=None):
 def rollout_step(cfg, state, t0, actions, obs_out=None, reward=None, done=None, legal_out=None, stream=None):
     E, A = cfg.n_envs, cfg.n_agents
     D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
-    _need(state, "state", torch.int32)
+    _need_state(cfg, state)
     _need(actions, "actions", torch.int32)
     if actions.dim() != 3 or tuple(actions.shape[1:]) != (E, A):
         raise ValueError(f"actions must be [T, {E}, {A}], got {tuple(actions.shape)}")
@@ -356,7 +369,7 @@ def rollout_run(cfg, policy, state, t0, n_steps, obs=None, actions=None, logits=
     E, A = cfg.n_envs, cfg.n_agents
     D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
     T = n_steps
-    _need(state, "state", torch.int32)
+    _need_state(cfg, state)
     _need(obs, "obs", policy.torch_dtype, (T, E, A, D))
     _need(actions, "actions", torch.int32, (T, E, A))
     _need(logits, "logits", torch.float32, (T, E, A, nA))
@@ -377,7 +390,7 @@ def rollout_run_ac(cfg, policy, state, t0, n_steps, value=None, logp=None, value
     E, A = cfg.n_envs, cfg.n_agents
     D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
     T = n_steps
-    _need(state, "state", torch.int32)
+    _need_state(cfg, state)
     _need(obs, "obs", policy.torch_dtype, (T, E, A, D))
     _need(actions, "actions", torch.int32, (T, E, A))
     _need(logits, "logits", torch.float32, (T, E, A, nA))
@@ -403,7 +416,7 @@ def rollout_run_teams(cfg, policy, teammates, state, t0, n_steps, obs=None, acti
     D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
     T = n_steps
     _need(teammates, "teammates", torch.int32, (E, A))
-    _need(state, "state", torch.int32)
+    _need_state(cfg, state)
     _need(obs, "obs", policy.torch_dtype, (T, E, A, D))
     _need(actions, "actions", torch.int32, (T, E, A))
     _need(logits, "logits", torch.float32, (T, E, A, nA))
@@ -479,7 +492,7 @@ def rollout_run_s5(cfg, policy, state, carry, t0, n_steps, value=None, logp=None
     E, A = cfg.n_envs, cfg.n_agents
     D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
     T = n_steps
-    _need(state, "state", torch.int32)
+    _need_state(cfg, state)
     _need(carry, "carry", torch.float32, (E * A, 2, policy.P))
     _need(obs, "obs", torch.bfloat16, (T, E, A, D))
     _need(actions, "actions", torch.int32, (T, E, A))
@@ -526,7 +539,7 @@ def rollout_run_pop(cfg, pop, policy_index, state, t0, n_steps, obs=None, action
     D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
     T = n_steps
     _need(policy_index, "policy_index", torch.int32, (E, A))
-    _need(state, "state", torch.int32)
+    _need_state(cfg, state)
     _need(obs, "obs", pop.torch_dtype, (T, E, A, D))
     _need(actions, "actions", torch.int32, (T, E, A))
     _need(logits, "logits", torch.float32, (T, E, A, nA))

@@ -277,3 +277,28 @@ def test_packed_weight_queries():
     assert R.lib.rl_policy_pack(q, 4096, None) == R.RL_EUNSUPPORTED
     assert R.lib.rl_policy_pack(_policy_struct(R.RL_BF16), None, None) == R.RL_EINVAL
 
+
+
+@pytest.mark.parametrize("make", [
+    lambda: R.EnvConfig(n_envs=16),
+    lambda: R.EnvConfig(n_envs=7, grid_h=12, grid_w=12, n_agents=3, n_food=6),
+    lambda: R.overcooked_config(16),
+    lambda: R.hanabi_config(16),
+])
+def test_binding_checks_the_state_size(make):
+    """Every binding wrapper that takes a state buffer rejects one whose size is not rl_state_bytes(cfg)
+    before anything is launched (the C ABI cannot see a buffer's size)."""
+    import torch
+    cfg = make()
+    n = R.rl_state_bytes(cfg) // 4
+    for bad in (torch.zeros(n - 1, dtype=torch.int32), torch.zeros(n + 4, dtype=torch.int32),
+                torch.zeros(n, dtype=torch.int16)):
+        with pytest.raises(ValueError, match="rl_state_bytes"):
+            R.rollout_init(cfg, bad)
+        with pytest.raises(ValueError, match="rl_state_bytes"):
+            R.rollout_step(cfg, bad, 0, torch.zeros(1, cfg.n_envs, cfg.n_agents, dtype=torch.int32))
+        with pytest.raises(ValueError, match="rl_state_bytes"):
+            R._need_state(cfg, bad)
+    # the right size passes the size check and then fails the device check (these are host tensors)
+    with pytest.raises(ValueError, match="device tensor"):
+        R.rollout_init(cfg, torch.zeros(n, dtype=torch.int32))

@@ -84,8 +84,9 @@ def test_actor_critic_rollout_parity(dims, dtype):
     lg_ref = np.concatenate([ref["logits"], ref["value"][..., None]], axis=-1)
     lg_gpu = np.concatenate([g["logits"].numpy(), g["value"].numpy()[..., None]], axis=-1)
     assert_logits_close(lg_gpu, lg_ref, RTOL[dtype])
-    last_ref = np.concatenate([np.zeros(ref["value_last"].shape + (6,)), ref["value_last"][..., None]], axis=-1)
-    last_gpu = np.concatenate([np.zeros(ref["value_last"].shape + (6,)), g["value_last"].numpy()[..., None]], axis=-1)
+    # V(o_last) is checked as the last output of its row, scaled like the steps' values by the row's logits
+    last_ref = np.concatenate([ref["logits_last"], ref["value_last"][..., None]], axis=-1)
+    last_gpu = np.concatenate([ref["logits_last"], g["value_last"].numpy()[..., None]], axis=-1)
     assert_logits_close(last_gpu, last_ref, RTOL[dtype])
     # strict: the oracle samples from the GPU's logits; log pi of the same float32 logits
     strict = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, dtype, value_head=True,

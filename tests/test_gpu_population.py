@@ -92,6 +92,69 @@ def test_population_rollout_parity(cfgkw, dims, npol, T, dtype):
     assert np.array_equal(strict["actions"], g["actions"].numpy())
 
 
+@pytest.mark.parametrize("block", [16, 8, 5])
+def test_population_benchmark_shape_parity(block):
+    """The benchmarked population shape: 9 packed policies 192-128-128-6 bf16, the ego (policy 0) on agent 0
+    and teammate 1 + (e // block) mod 8 on agent 1.  Blocks of 16 envs put at most two policies in each
+    16-env tile; blocks of 8 and 5 put three or four there (and out-of-range indices add policy 0 rows)."""
+    require_gpu()
+    cfg = R.EnvConfig(n_envs=150, seed=23, env_base=11, max_steps=30)
+    dims = (192, 128, 128, 6)
+    npol = 9
+    _note(f"rollout_run_pop {dims} P={npol} block={block}")
+    E, A = cfg.n_envs, cfg.n_agents
+    ws, bs = _pop(dims, npol, seed=500)
+    idx = np.zeros((E, A), dtype=np.int64)
+    idx[:, 1] = 1 + (np.arange(E) // block) % (npol - 1)
+    idx[7, 1], idx[40, 0], idx[149, 1] = -3, npol, 1 << 20  # out of range: policy 0
+    pop = R.Population(ws, bs, "bf16")
+    assert pop.packed is not None
+    T = 50
+    state, g = _run(cfg, pop, idx, T)
+    oc = oracle_cfg(cfg)
+    env_ids = list(range(11, 11 + E))
+    hook = NearTieLockstep(g["actions"].numpy(), cfg.seed, env_ids, RTOL["bf16"])
+    ref = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, "bf16", action_hook=hook, policy_index=idx)
+    assert np.array_equal(_obs_np(g["obs"]), ref["obs"])
+    assert np.array_equal(g["reward"].numpy().view(np.uint32), ref["reward"].view(np.uint32))
+    assert np.array_equal(g["done"].numpy(), ref["done"])
+    assert np.array_equal(g["actions"].numpy(), ref["actions"])
+    assert np.array_equal(_obs_np(g["obs_last"]), ref["obs_last"])
+    assert_logits_close(g["logits"].numpy(), ref["logits"], RTOL["bf16"])
+    assert states_from_device(cfg, state) == ref["states"]
+    assert ref["done"].any()
+    strict = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, "bf16", policy_index=idx,
+                             logits_source=lambda k, _: g["logits"][k].numpy())
+    assert np.array_equal(strict["actions"], g["actions"].numpy())
+
+
+def test_population_4096_sampled_envs():
+    """The benchmarked population rollout at full size (4096 envs x 128 steps, 9 policies, the bench's
+    weights and block layout); the oracle replays 16 sampled envs, two from each teammate's block."""
+    require_gpu()
+    name = "lbf8_4096_pop"
+    w = workloads.WORKLOADS[name]
+    cfg = R.EnvConfig(n_envs=w["n_envs"], seed=0, **w["env"])
+    ws, bs = workloads.population_weights(name, seed=1000)
+    pop = R.Population(ws, bs, "bf16")
+    idx = workloads.population_index(name)
+    T = w["n_steps"]
+    _note(f"rollout_run_pop {name} full size")
+    state, g = _run(cfg, pop, idx, T)
+    sample = sorted({b * 512 + o for b in range(8) for o in (0, 511)} | {1, 2047, 2048, 4095})
+    oc = oracle_cfg(cfg)
+    hook = NearTieLockstep(g["actions"][:, sample].numpy(), cfg.seed, sample, RTOL["bf16"])
+    ref = rollout.rollout(lbf, oc, cfg.seed, sample, 0, T, ws, bs, "bf16", action_hook=hook,
+                          policy_index=idx[sample])
+    assert np.array_equal(_obs_np(g["obs"][:, sample]), ref["obs"])
+    assert np.array_equal(g["reward"][:, sample].numpy().view(np.uint32), ref["reward"].view(np.uint32))
+    assert np.array_equal(g["done"][:, sample].numpy(), ref["done"])
+    assert np.array_equal(g["actions"][:, sample].numpy(), ref["actions"])
+    assert_logits_close(g["logits"][:, sample].numpy(), ref["logits"], RTOL["bf16"])
+    final = states_from_device(cfg, state)
+    assert [final[e] for e in sample] == ref["states"]
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_one_policy_population_is_rollout_run(dtype):
     """Every agent on policy 1 of a population == rollout_run with that policy (generic-kernel shape)."""

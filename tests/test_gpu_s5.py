@@ -74,6 +74,8 @@ def _obs_np(t):
 @pytest.mark.parametrize("cfgkw,sizes,T", [
     (dict(n_envs=37, max_steps=15), (64, 32, 128), 40),
     (dict(n_envs=64, max_steps=8), (128, 128, 1024), 12),
+    # the benchmarked widths over 600 agent rows: five 128-row head tiles, the last one ragged (88 rows)
+    (dict(n_envs=300, max_steps=20), (128, 128, 1024), 60),
 ])
 def test_s5_rollout_parity(cfgkw, sizes, T):
     require_gpu()
@@ -99,8 +101,9 @@ def test_s5_rollout_parity(cfgkw, sizes, T):
     lg_ref = np.concatenate([ref["logits"], ref["value"][..., None]], axis=-1)
     lg_gpu = np.concatenate([g["logits"].numpy(), g["value"].numpy()[..., None]], axis=-1)
     assert_logits_close(lg_gpu, lg_ref, RTOL["bf16"])
-    last_ref = np.concatenate([ref["obs_last"][..., :6] * 0, ref["value_last"][..., None]], axis=-1)
-    last_gpu = np.concatenate([ref["obs_last"][..., :6] * 0, g["value_last"].numpy()[..., None]], axis=-1)
+    # V(o_last) is checked as the last output of its row, scaled like the steps' values by the row's logits
+    last_ref = np.concatenate([ref["logits_last"], ref["value_last"][..., None]], axis=-1)
+    last_gpu = np.concatenate([ref["logits_last"], g["value_last"].numpy()[..., None]], axis=-1)
     assert_logits_close(last_gpu, last_ref, RTOL["bf16"])
     c = carry.cpu().numpy().astype(np.float64)
     assert_logits_close(c[:, 0], ref["carry"].real, RTOL["bf16"])
@@ -126,3 +129,47 @@ def test_s5_split_rollout_is_identical():
     for k in ("obs_last", "value_last"):
         assert torch.equal(a[k], b2[k]), k
     assert torch.equal(s1, s2) and torch.equal(c1, c2)
+
+
+def test_s5_rollout_4096_sampled_envs():
+    """The benchmarked S5 rollout at full size (4096 envs x 128 steps, 8192 agent rows = 64 head tiles, the
+    bench's parameters); the oracle replays 12 sampled envs, whose rows lie in different head tiles and
+    workgroups."""
+    require_gpu()
+    name = "lbf8_4096_s5"
+    w = workloads.WORKLOADS[name]
+    cfg = R.EnvConfig(n_envs=w["n_envs"], seed=0, **w["env"])
+    D, nA = R.rl_obs_dim(cfg), R.rl_num_actions(cfg)
+    x = w["s5"]
+    cont = workloads.s5_params(D, x["d_model"], x["d_state"], x["head_width"], nA, seed=1000)
+    pol = R.S5Policy(cont)
+    T = w["n_steps"]
+    _note(f"rollout_run_s5 {name} full size")
+    state, carry, g = _run(cfg, pol, T)
+    sample = [0, 1, 63, 64, 65, 1000, 2047, 2048, 3333, 4031, 4094, 4095]
+    net = s5.from_continuous(cont)
+    oc = oracle_cfg(cfg)
+    hook = NearTieLockstep(g["actions"][:, sample].numpy(), cfg.seed, sample, RTOL["bf16"])
+    ref = rollout.rollout(lbf, oc, cfg.seed, sample, 0, T, None, None, "bf16", action_hook=hook, recurrent=net)
+    assert np.array_equal(_obs_np(g["obs"][:, sample]), ref["obs"])
+    assert np.array_equal(g["reward"][:, sample].numpy().view(np.uint32), ref["reward"].view(np.uint32))
+    assert np.array_equal(g["done"][:, sample].numpy(), ref["done"])
+    assert np.array_equal(g["actions"][:, sample].numpy(), ref["actions"])
+    assert np.array_equal(_obs_np(g["obs_last"][sample]), ref["obs_last"])
+    final = states_from_device(cfg, state)
+    assert [final[e] for e in sample] == ref["states"]
+    lg_ref = np.concatenate([ref["logits"], ref["value"][..., None]], axis=-1)
+    lg_gpu = np.concatenate([g["logits"][:, sample].numpy(), g["value"][:, sample].numpy()[..., None]], axis=-1)
+    assert_logits_close(lg_gpu, lg_ref, RTOL["bf16"])
+    last_ref = np.concatenate([ref["logits_last"], ref["value_last"][..., None]], axis=-1)
+    last_gpu = np.concatenate([ref["logits_last"], g["value_last"][sample].numpy()[..., None]], axis=-1)
+    assert_logits_close(last_gpu, last_ref, RTOL["bf16"])
+    rows = np.array([[e * cfg.n_agents + a for a in range(cfg.n_agents)] for e in sample]).reshape(-1)
+    c = carry.cpu().numpy().astype(np.float64)[rows]
+    assert_logits_close(c[:, 0], ref["carry"].real, RTOL["bf16"])
+    assert_logits_close(c[:, 1], ref["carry"].imag, RTOL["bf16"])
+    # properties over every env
+    done = g["done"].numpy()
+    assert set(np.unique(done)) <= {0, 1, 2, 3}
+    assert ((done != 0).sum(axis=0) >= 2).all()
+    assert torch.isfinite(g["logits"]).all() and torch.isfinite(g["value"]).all()

@@ -32,6 +32,9 @@ def _note(msg):
     (dict(grid_h=7, grid_w=7, max_agent_level=1, max_food_level=2, const_levels=True), (64, 64), "bf16"),
     (dict(), (64, 64), "f32"),
     (dict(n_agents=3, n_food=4, max_agent_level=2, max_food_level=4), (32, 48), "bf16"),
+    # the register-resident 128-wide kernels with teammates: the benchmarked 7x7 one and its 8x8 sibling
+    (dict(grid_h=7, grid_w=7, max_agent_level=1, max_food_level=2, const_levels=True), (128, 128), "bf16"),
+    (dict(), (128, 128), "bf16"),
 ])
 def test_heuristic_teammates_parity(cfgkw, hidden, dtype):
     require_gpu()
@@ -74,3 +77,46 @@ def test_heuristic_teammates_parity(cfgkw, hidden, dtype):
     strict = rollout.rollout(lbf, oc, cfg.seed, env_ids, 0, T, ws, bs, dtype, teammates=tm,
                              logits_source=lambda k, _: g["logits"][k].numpy())
     assert np.array_equal(strict["actions"], g["actions"].numpy())
+
+
+def test_teams_4096_sampled_envs():
+    """The benchmarked teammate rollout at full size (7x7 constant levels, 4096 envs x 128 steps, policy
+    147-128-128-6 bf16 on agent 0, heuristic kind e mod 9 on agent 1); the oracle replays 18 sampled envs,
+    two of every heuristic kind."""
+    require_gpu()
+    name = "lbf7_teams_4096"
+    w = workloads.WORKLOADS[name]
+    cfg = R.EnvConfig(n_envs=w["n_envs"], seed=0, **w["env"])
+    E, A, D = cfg.n_envs, cfg.n_agents, R.rl_obs_dim(cfg)
+    dims = workloads.policy_dims(name)
+    ws, bs = workloads.policy_weights(dims, seed=1000)
+    pol = R.Policy(ws, bs, "bf16")
+    T = w["n_steps"]
+    tm = np.full((E, A), -1, dtype=np.int32)
+    tm[:, 1] = np.arange(E) % 9
+    _note(f"rollout_run_teams {name} full size")
+    state = R.new_state(cfg)
+    R.rollout_init(cfg, state)
+    out = dict(obs=torch.empty(T, E, A, D, dtype=pol.torch_dtype, device="cuda"),
+               actions=torch.empty(T, E, A, dtype=torch.int32, device="cuda"),
+               logits=torch.empty(T, E, A, 6, device="cuda"),
+               reward=torch.empty(T, E, device="cuda"), done=torch.empty(T, E, dtype=torch.uint8, device="cuda"),
+               obs_last=torch.empty(E, A, D, dtype=pol.torch_dtype, device="cuda"))
+    R.rollout_run_teams(cfg, pol, torch.from_numpy(tm).cuda(), state, 0, T, **out)
+    torch.cuda.synchronize()
+    g = {k: v.cpu() for k, v in out.items()}
+    sample = list(range(9)) + [1000 + k for k in range(9)]
+    sample[-1] = E - 1  # the last env (kind 4095 mod 9 = 0)
+    oc = oracle_cfg(cfg)
+    hook = NearTieLockstep(g["actions"][:, sample].numpy(), cfg.seed, sample, RTOL["bf16"])
+    ref = rollout.rollout(lbf, oc, cfg.seed, sample, 0, T, ws, bs, "bf16", action_hook=hook, teammates=tm[sample])
+    assert np.array_equal(g["obs"][:, sample].float().numpy().astype(np.float64), ref["obs"])
+    assert np.array_equal(g["reward"][:, sample].numpy().view(np.uint32), ref["reward"].view(np.uint32))
+    assert np.array_equal(g["done"][:, sample].numpy(), ref["done"])
+    assert np.array_equal(g["actions"][:, sample].numpy(), ref["actions"])
+    assert np.array_equal(g["obs_last"][sample].float().numpy().astype(np.float64), ref["obs_last"])
+    final = states_from_device(cfg, state)
+    assert [final[e] for e in sample] == ref["states"]
+    gl, rl_ = g["logits"][:, sample].numpy().astype(np.float64), ref["logits"]
+    assert np.array_equal(gl[:, :, 1], rl_[:, :, 1])
+    assert_logits_close(gl[:, :, 0], rl_[:, :, 0], RTOL["bf16"])
