@@ -347,6 +347,23 @@ rl_status rollout_run_s5(const rl_env_config* cfg, const rl_s5_policy* policy, v
                          uint64_t t0, int32_t n_steps, const rl_traj* out, const rl_ac_traj* ac, void* workspace,
                          size_t workspace_bytes, void* stream);
 
+/* rollout_run_s5 without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc).  The workspace is a file-scope device
+ * array of the library, 80 MiB (83,886,080 bytes) on every GPU the library
+ * runs on, held until the process ends; its address on the current GPU is
+ * resolved on the first call there.  Calls whose rl_s5_workspace_bytes
+ * exceeds 80 MiB fail with RL_EINVAL before anything is launched (4096 LBF
+ * 8x8 envs of 2 agents at D 192, H 128, P 128, F 1024 need 75.7 MB).  No
+ * call allocates memory.  Nothing in the array needs to start at zero: every
+ * call writes each workspace region before reading it.  Every call on one GPU
+ * shares that GPU's array, so calls that overlap in time on one GPU (on
+ * different streams or host threads) race and must be serialised by the
+ * caller.  Arguments, results and errors otherwise as rollout_run_s5. */
+rl_status rollout_run_s5_noalloc(const rl_env_config* cfg, const rl_s5_policy* policy, void* state, float* carry,
+                                 uint64_t t0, int32_t n_steps, const rl_traj* out, const rl_ac_traj* ac,
+                                 void* stream);
+
 /* Gumbel-max sampling of the actions of step t from given logits (the
  * sampling stage of rollout_run on its own).
  *   logits  [E, A, nA] float32 read;  legal [E, A, nA] uint8 or NULL;

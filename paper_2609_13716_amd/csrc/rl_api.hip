@@ -449,6 +449,36 @@ rl_status rollout_run_s5(const rl_env_config* cfg, const rl_s5_policy* policy, v
                   "rollout_run_s5");
 }
 
+rl_status rollout_run_s5_noalloc(const rl_env_config* cfg, const rl_s5_policy* policy, void* state, float* carry,
+                                 uint64_t t0, int32_t n_steps, const rl_traj* out, const rl_ac_traj* ac,
+                                 void* stream) {
+  EnvSpec es;
+  rl::S5Net net;
+  rl_status s = check_s5(cfg, policy, &es, &net);
+  if (s != RL_OK) return s;
+  if (!state || !carry) return fail(RL_EINVAL, "state or carry is NULL");
+  if (!out || !ac) return fail(RL_EINVAL, "out or ac is NULL");
+  if (n_steps < 1) return fail(RL_EINVAL, "n_steps %d must be >= 1", n_steps);
+  if (t0 > UINT64_MAX - (uint64_t)n_steps) return fail(RL_EINVAL, "t0 + n_steps overflows");
+  if ((int64_t)es.E * es.A > ((int64_t)1 << 24)) return fail(RL_EINVAL, "n_envs * n_agents above 2^24");
+  const size_t need = rl::s5_workspace(es.lbf, net).bytes;
+  if (need > rl::S5_SCRATCH_BYTES)
+    return fail(RL_EINVAL, "this rollout needs %zu bytes of workspace; the built-in scratch holds %zu "
+                "(use rollout_run_s5 with a caller-owned workspace)", need, rl::S5_SCRATCH_BYTES);
+  if ((out->obs && !aligned16(out->obs)) || (out->obs_last && !aligned16(out->obs_last)))
+    return fail(RL_EINVAL, "obs and obs_last must be 16-byte aligned");
+  void* scratch = nullptr;
+  const hipError_t e = rl::s5_scratch_ptr(&scratch);
+  if (e != hipSuccess) return fail(RL_EDEVICE, "resolving the S5 scratch array failed: %s", hipGetErrorString(e));
+  rl::TrajArgs o{out->obs, out->actions, out->logits, out->reward, out->done, out->obs_last};
+  o.value = ac->value;
+  o.logp = ac->logp;
+  o.value_last = ac->value_last;
+  return launched(rl::launch_s5_rollout(es.lbf, net, static_cast<int32_t*>(state), carry, t0, n_steps, o, scratch,
+                                        (hipStream_t)stream),
+                  "rollout_run_s5_noalloc");
+}
+
 rl_status rl_gae(const float* reward, const uint8_t* done, const float* value, const float* value_last,
                  int32_t n_steps, int32_t n_envs, int32_t n_agents, float gamma, float lambda, float* adv,
                  float* ret, void* stream) {

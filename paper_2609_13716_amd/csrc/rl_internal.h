@@ -210,6 +210,11 @@ hipError_t launch_s5_discretize(int P, int H, const float* lam, const float* log
                                 float* bbar, hipStream_t s);
 hipError_t launch_s5_rollout(const LbfParams& p, const S5Net& net, int32_t* state, float* carry, uint64_t t0,
                              int n_steps, const TrajArgs& out, void* workspace, hipStream_t s);
+// The allocation-free S5 rollout's workspace: a file-scope device array of
+// S5_SCRATCH_BYTES per GPU; s5_scratch_ptr resolves the current GPU's copy
+// (hipGetSymbolAddress, once per device) and returns its device address.
+constexpr size_t S5_SCRATCH_BYTES = (size_t)80 << 20;
+hipError_t s5_scratch_ptr(void** out);
 
 // Generalised advantage estimation over [T, E, A] values (rl_ac.hip).
 hipError_t launch_gae(const float* reward, const uint8_t* done, const float* value, const float* value_last, int T,

@@ -21,6 +21,7 @@
 //   env    one LBF step with the sampled actions (the env-only kernels).
 // The heads dominate (2 x (H F + 2 F F) MACs per row): they are the GEMMs
 // that the MFMA roofline is taken on.
+#include <mutex>
 #include "rl_internal.h"
 #include "rl_mlp.h"
 #include "rl_sample.h"
@@ -541,6 +542,35 @@ __global__ __launch_bounds__(S5_NT) void s5_out_kernel(S5OutArgs o) {
 // ------------------------------------------------------------- the loop ----
 
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Workspace of the allocation-free S5 rollout: one copy of this array per GPU
+// the library runs on, held until the process ends.  Host code never uses the
+// array's name as an address: s5_scratch_ptr() resolves the device copy of the
+// current GPU once and the kernels receive that pointer.
+static __device__ __align__(256) uint8_t s5_scratch[S5_SCRATCH_BYTES];
+
+namespace {
+constexpr int S5_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[S5_MAX_DEVICES] = {};
+}  // namespace
+
+hipError_t s5_scratch_ptr(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= S5_MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(s5_scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return hipSuccess;
+}
 
 S5Workspace s5_workspace(const LbfParams& p, const S5Net& net) {
   S5Workspace w;

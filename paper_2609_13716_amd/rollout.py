@@ -108,6 +108,9 @@ def _load():
     lib.rollout_run_s5.argtypes = [cfgp, s5p, P, P, ctypes.c_uint64, ctypes.c_int32, ctypes.POINTER(_Traj),
                                    ctypes.POINTER(_AcTraj), P, ctypes.c_size_t, P]
     lib.rollout_run_s5.restype = st
+    lib.rollout_run_s5_noalloc.argtypes = [cfgp, s5p, P, P, ctypes.c_uint64, ctypes.c_int32, ctypes.POINTER(_Traj),
+                                           ctypes.POINTER(_AcTraj), P]
+    lib.rollout_run_s5_noalloc.restype = st
     lib.rl_policy_packed_bytes.argtypes = [ctypes.POINTER(_Policy)]
     lib.rl_policy_packed_bytes.restype = ctypes.c_size_t
     lib.rl_policy_pack.argtypes, lib.rl_policy_pack.restype = [ctypes.POINTER(_Policy), P, P], st
@@ -120,7 +123,7 @@ lib = _load()
 EXPORTED = ("rl_state_bytes", "rl_obs_dim", "rl_num_actions", "rollout_last_error", "rollout_init",
             "rollout_step", "policy_forward", "rollout_run", "rollout_sample", "rl_gumbel_noise", "rollout_run_pop",
             "rollout_run_ac", "rl_gae", "rl_s5_discretize", "rl_s5_workspace_bytes", "rollout_run_s5",
-            "rollout_run_teams", "rl_policy_packed_bytes", "rl_policy_pack")
+            "rollout_run_teams", "rl_policy_packed_bytes", "rl_policy_pack", "rollout_run_s5_noalloc")
 HEURISTICS = ("greedy_closest_self", "greedy_closest_teammate", "greedy_closest_avg", "greedy_lowest_level",
               "greedy_highest_level", "seq_lexicographic", "seq_reverse_lexicographic", "seq_column_major",
               "seq_reverse_column_major")  # kind k of rollout_run_teams
@@ -514,6 +517,30 @@ def rollout_run_s5(cfg, policy, state, carry, t0, n_steps, value=None, logp=None
                               ctypes.byref(tr), ctypes.byref(ac), _ptr(workspace), workspace.numel(),
                               _stream(stream)))
     return workspace
+
+
+def rollout_run_s5_noalloc(cfg, policy, state, carry, t0, n_steps, value=None, logp=None, value_last=None, obs=None,
+                           actions=None, logits=None, reward=None, done=None, obs_last=None, stream=None):
+    """rollout_run_s5 on the library's built-in device scratch (no workspace, nothing allocated)."""
+    E, A = cfg.n_envs, cfg.n_agents
+    D, nA = rl_obs_dim(cfg), rl_num_actions(cfg)
+    T = n_steps
+    _need_state(cfg, state)
+    _need(carry, "carry", torch.float32, (E * A, 2, policy.P))
+    _need(obs, "obs", torch.bfloat16, (T, E, A, D))
+    _need(actions, "actions", torch.int32, (T, E, A))
+    _need(logits, "logits", torch.float32, (T, E, A, nA))
+    _need(reward, "reward", torch.float32, (T, E))
+    _need(done, "done", torch.uint8, (T, E))
+    _need(obs_last, "obs_last", torch.bfloat16, (E, A, D))
+    _need(value, "value", torch.float32, (T, E, A))
+    _need(logp, "logp", torch.float32, (T, E, A))
+    _need(value_last, "value_last", torch.float32, (E, A))
+    tr = _Traj(obs=_ptr(obs), actions=_ptr(actions), logits=_ptr(logits), reward=_ptr(reward), done=_ptr(done),
+               obs_last=_ptr(obs_last))
+    ac = _AcTraj(value=_ptr(value), logp=_ptr(logp), value_last=_ptr(value_last))
+    _check(lib.rollout_run_s5_noalloc(ctypes.byref(cfg.c()), ctypes.byref(policy.c()), _ptr(state), _ptr(carry), t0,
+                                      T, ctypes.byref(tr), ctypes.byref(ac), _stream(stream)))
 
 
 def gae(reward, done, value, value_last, gamma, lam, adv=None, ret=None, stream=None):
