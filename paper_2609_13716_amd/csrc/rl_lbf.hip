@@ -434,11 +434,16 @@ size_t lbf_pop_lds_bytes(const LbfParams& p, const PolicyArgs& pol) {
   return off + (size_t)(3 * RL.R + 17) * 4 + (size_t)RL.R * MAX_NA * 4;
 }
 
+__device__ __forceinline__ bool pop_two_slots(const int32_t* __restrict__ pidx, int e0, int te_valid, int A,
+                                              int n_pol, int& q0, int& q1);
+
+// skip_two: tiles whose agents use at most two policies are left alone (the
+// two-policy kernel has run them).
 template <int DT, bool PK>
 __global__ __launch_bounds__(NTHREADS) void lbf_run_pop_kernel(LbfParams p, LbfMagic m, PolicyArgs pol, int n_pol,
                                                                const int32_t* __restrict__ pidx,
                                                                int32_t* __restrict__ state, uint64_t t0,
-                                                               int n_steps, TrajArgs out) {
+                                                               int n_steps, TrajArgs out, int skip_two) {
   using T = typename DType<DT>::T;
   extern __shared__ __align__(16) uint8_t smem[];
   const RunLayout RL = make_run_layout(p.A, p.D, pol.H1, pol.H2, DT);
@@ -462,6 +467,15 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_pop_kernel(LbfParams p, LbfM
   const int A = p.A, D = p.D, NA = pol.NA, H1 = pol.H1, H2 = pol.H2;
   const int dims4[4] = {D, H1, H2, NA};
   T* gobs = static_cast<T*>(out.obs);
+  if (skip_two) {
+    __shared__ int two;
+    if (tid == 0) {
+      int q0, q1;
+      two = pop_two_slots(pidx, e0, te_valid, A, n_pol, q0, q1) ? 1 : 0;
+    }
+    __syncthreads();
+    if (two) return;
+  }
 
   zero_lds(smem, RL.total, tid);  // zero grids and the K padding of every operand tile
   if (tid == 0) {
@@ -580,44 +594,6 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_pop_kernel(LbfParams p, LbfM
   if (envlane) lbf_store(state, p, e, s);
 }
 
-hipError_t launch_lbf_run_pop(const LbfParams& p, const PolicyArgs& pol, int n_pol, const int32_t* pidx,
-                              int32_t* state, uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s) {
-  const LbfMagic m = make_magic(p, pol.NA);
-  const size_t lds = lbf_pop_lds_bytes(p, pol);
-  const dim3 grid((unsigned)((p.E + TILE_E - 1) / TILE_E));
-  // the dynamic limit leaves room for the kernel's few bytes of static LDS
-  const int max_dyn = (int)(MAX_LDS_BYTES - LBF_POP_STATIC_LDS);
-  if (pol.dt == DT_F32) {
-    static bool attr = false;
-    if (!attr) {
-      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_F32, false>,
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
-      if (e != hipSuccess) return e;
-      attr = true;
-    }
-    lbf_run_pop_kernel<DT_F32, false><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
-  } else if (pol.Wp[0] != nullptr) {  // fragment-major weights
-    static bool attr = false;
-    if (!attr) {
-      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_BF16, true>,
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
-      if (e != hipSuccess) return e;
-      attr = true;
-    }
-    lbf_run_pop_kernel<DT_BF16, true><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
-  } else {
-    static bool attr = false;
-    if (!attr) {
-      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_BF16, false>,
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
-      if (e != hipSuccess) return e;
-      attr = true;
-    }
-    lbf_run_pop_kernel<DT_BF16, false><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out);
-  }
-  return hipGetLastError();
-}
-
 // ------------------------------------ fused rollout, weights in registers ----
 
 constexpr int LBF_RB = 4;  // steps of reset states built per batch
@@ -648,13 +624,15 @@ constexpr int NOISE_STEPS = 16;
 // agent's level at its cell, plane 1 every uneaten food's level, plane 2 a 1
 // at the row's own agent.  Cell ids are clamped into the grid so that a
 // malformed caller-supplied state cannot address outside the row.
-template <typename T, int A, int F>
+// AMT > 0: the tile's rows are agent-major, row i * AMT + el (AMT envs per
+// tile); otherwise env-major, row el * A + i.
+template <typename T, int A, int F, int AMT = 0>
 __device__ __forceinline__ void lbf_paint_tile(const LbfEnv& s, int el, T* xs, int ldx, int HW, bool on) {
   const uint32_t cmax = (uint32_t)HW - 1u;
   const T one = on ? small_int_to<T>(1u) : (T)0;
 #pragma unroll
   for (int i = 0; i < A; ++i) {
-    T* xr = xs + (el * A + i) * ldx;
+    T* xr = xs + (AMT ? i * AMT + el : el * A + i) * ldx;
 #pragma unroll
     for (int q = 0; q < A; ++q) xr[min((uint32_t)s.acell[q], cmax)] = on ? small_int_to<T>((uint32_t)s.alevel[q]) : (T)0;
 #pragma unroll
@@ -670,9 +648,12 @@ __device__ __forceinline__ void lbf_paint_tile(const LbfEnv& s, int el, T* xs, i
 // zeroed in LDS after it is read, which leaves the tile blank for the next
 // paint.  The vectors of a thread go in groups of G: all reads of a group
 // are issued before its first store, so a group waits for LDS once.
-template <typename T, int R, int D, int LDX, int NT, bool CLEAR = false, int G = 4>
+// AMT > 0: the LDS rows are agent-major (row a * AMT + el, AMT envs of A
+// agents) and go to global rows el * A + a.
+template <typename T, int R, int D, int LDX, int NT, bool CLEAR = false, int G = 4, int AMT = 0, int A = 1>
 __device__ __forceinline__ void copy_obs_rows(T* xs, T* __restrict__ g, int rows_live, int tid) {
   constexpr int VE = 16 / sizeof(T);
+  static_assert(AMT == 0 || D % VE == 0, "agent-major tiles need whole-vector rows");
   if constexpr (D % VE != 0) {
     // Rows that are not whole vectors (e.g. the 7x7 grid's 147 features): the
     // tile's rows are contiguous in global memory, so the tile goes out as
@@ -752,8 +733,10 @@ __device__ __forceinline__ void copy_obs_rows(T* xs, T* __restrict__ g, int rows
     for (int j = 0; j < G; ++j) {
       const int v = tid + (i0 + j) * NT;
       const int r = v / VPR, c = (v - r * VPR) * VE;
-      if (i0 + j < IT && (NV % NT == 0 || v < NV) && r < rows_live) {
-        if (g) *reinterpret_cast<u32x4*>(g + (size_t)r * D + c) = val[j];
+      const int gr = AMT ? (r % AMT) * A + r / AMT : r;  // global row of LDS row r
+      const bool live = AMT ? (r % AMT) * A < rows_live : r < rows_live;
+      if (i0 + j < IT && (NV % NT == 0 || v < NV) && live) {
+        if (g) *reinterpret_cast<u32x4*>(g + (size_t)gr * D + c) = val[j];
         if constexpr (CLEAR) *reinterpret_cast<u32x4*>(xs + r * LDX + c) = u32x4{0u, 0u, 0u, 0u};
       }
     }
@@ -1168,6 +1151,352 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
 #undef RL_REG_CASE
 #undef RL_REG_CASE_T
   return false;
+}
+
+// ------------------------- population rollout, two resident policies ----
+//
+// rollout_run_pop for the common case of at most two distinct policies among
+// a tile's agents (the ego and one teammate per block of envs): both
+// policies' layer-1/2 weights stay in registers for the whole rollout, as in
+// lbf_rollout_kernel.  The tile's rows are agent-major (row a * TE + el), so
+// with the ego on agent 0 and a teammate on agent 1 each 16-row MFMA tile
+// holds a single policy and runs its own weights only; a tile whose rows mix
+// the two policies runs both and each lane keeps its row's result.  Tiles
+// with three or more policies are left to lbf_run_pop_kernel (launched after
+// this kernel with skip_two set), which skips the tiles handled here.
+
+// Policies of a tile's agents (an index outside the population selects policy
+// 0): slot 0 is the policy of env e0's agent 0, slot 1 the first other policy
+// in row order (slot 0 again when there is none).  True iff every agent of the
+// tile uses one of the two.
+__device__ __forceinline__ bool pop_two_slots(const int32_t* __restrict__ pidx, int e0, int te_valid, int A,
+                                              int n_pol, int& q0, int& q1) {
+  const int nr = te_valid * A;
+  q0 = -1;
+  q1 = -1;
+  bool ok = true;
+  for (int r = 0; r < nr; ++r) {
+    const int raw = pidx[(size_t)e0 * A + r];
+    const int id = (unsigned)raw < (unsigned)n_pol ? raw : 0;
+    if (q0 < 0) {
+      q0 = id;
+    } else if (id != q0) {
+      if (q1 < 0) q1 = id;
+      else if (id != q1) ok = false;
+    }
+  }
+  if (q1 < 0) q1 = q0;
+  return ok;
+}
+
+template <int GH, int GW, int H1, int H2, int A, int F, int TE, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void lbf_pop2_kernel(LbfParams p, PolicyArgs pol, int n_pol,
+                                                             const int32_t* __restrict__ pidx,
+                                                             int32_t* __restrict__ state, uint64_t t0, int n_steps,
+                                                             TrajArgs out) {
+  constexpr int DT = DT_BF16;
+  using T = uint16_t;
+  using B = u32x4;
+  constexpr int HW = GH * GW, D = 3 * HW;
+  constexpr int NT = NW * 64;
+  constexpr int R = TE * A;
+  constexpr int MT = (R + 15) / 16;
+  constexpr int RP = MT * 16;
+  constexpr int NA = LBF_NACT;
+  constexpr int LDX = lds_ld<DT>(D), LD1 = lds_ld<DT>(H1), LD2 = lds_ld<DT>(H2);
+  constexpr int K3 = round_up(H2, 32) / 32;
+  using L1T = RegLayer<DT, D, H1, NW, true>;
+  using L2T = RegLayer<DT, H1, H2, NW, true>;
+  static_assert(TE == 16, "agent-major rows: M tile m holds agent m of the tile's 16 envs");
+  static_assert(L1T::NT % NW == 0 && L2T::NT % NW == 0, "every wave owns whole output tiles");
+
+  __shared__ __align__(16) T xs[RP * LDX];
+  __shared__ __align__(16) T h1s[RP * LD1];
+  __shared__ __align__(16) T h2s[RP * LD2];
+  __shared__ __align__(16) B w3s[2][K3 * 64];
+  __shared__ __align__(16) float bias_s[2][H1 + H2];
+  __shared__ float b3s[2][8];
+  __shared__ int act_s[RP];
+  __shared__ int slot_s[RP];  // 0 or 1: the resident policy of each row
+  __shared__ int ctl_s[2 + MT];  // the two policies' indices (-1: the tile is not handled here), slot masks per M tile
+  __shared__ uint32_t words[NOISE_STEPS * RP * 8];
+  __shared__ __align__(16) float nz[2][RP * 8];
+  __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int e0 = blockIdx.x * TE;
+  const int te_valid = min(TE, p.E - e0);
+  const int E = p.E;
+  constexpr int nd = 2 * A + 2 * F;
+  constexpr int nblk = (nd + 7) >> 3;
+  static_assert(TE * nblk <= 64, "one lane per reset block");
+
+  if (tid == 0) {
+    int q0, q1;
+    const bool ok = pop_two_slots(pidx, e0, te_valid, A, n_pol, q0, q1);
+    ctl_s[0] = ok ? q0 : -1;
+    ctl_s[1] = q1;
+  }
+  __syncthreads();
+  if (ctl_s[0] < 0) return;  // three or more policies: lbf_run_pop_kernel runs this tile
+  const int q0 = ctl_s[0], q1 = ctl_s[1];
+  for (int row = tid; row < RP; row += NT) {
+    const int el = row % TE, ag = row / TE;
+    int sl = 0;
+    if (el < te_valid && ag < A) {
+      const int raw = pidx[(size_t)(e0 + el) * A + ag];
+      sl = ((unsigned)raw < (unsigned)n_pol ? raw : 0) == q0 ? 0 : 1;
+    }
+    slot_s[row] = sl;
+  }
+  __syncthreads();
+  if (tid < MT) {  // which slots the live rows of M tile tid use
+    int msk = 0;
+    for (int r = 0; r < 16; ++r) {
+      const int row = tid * 16 + r;
+      if (row < R && row % TE < te_valid) msk |= 1 << slot_s[row];
+    }
+    ctl_s[2 + tid] = msk;
+  }
+
+  // weights: layers 1 and 2 of both policies in registers, layer 3 and the biases in LDS
+  const T* W1 = static_cast<const T*>(pol.W[0]);
+  const T* W2 = static_cast<const T*>(pol.W[1]);
+  const T* W3 = static_cast<const T*>(pol.W[2]);
+  const T* b1 = static_cast<const T*>(pol.b[0]);
+  const T* b2 = static_cast<const T*>(pol.b[1]);
+  const T* b3 = static_cast<const T*>(pol.b[2]);
+  L1T L1a, L1b;
+  L2T L2a, L2b;
+  L1a.load(W1 + (size_t)q0 * H1 * D, b1, wave, lane);
+  L2a.load(W2 + (size_t)q0 * H2 * H1, b2, wave, lane);
+  if (q1 != q0) {
+    L1b.load(W1 + (size_t)q1 * H1 * D, b1, wave, lane);
+    L2b.load(W2 + (size_t)q1 * H2 * H1, b2, wave, lane);
+  }
+  for (int i = tid; i < 2 * (H1 + H2); i += NT) {
+    const int sl = i / (H1 + H2), j = i - sl * (H1 + H2);
+    const size_t q = sl ? q1 : q0;
+    bias_s[sl][j] = bf16_to_f32(j < H1 ? b1[q * H1 + j] : b2[q * H2 + j - H1]);
+  }
+  if (tid < 128) {
+    const int sl = tid >> 6, n = lane & 15;
+    const size_t q = sl ? q1 : q0;
+    const T* row = W3 + (q * NA + (n < NA ? n : 0)) * H2;
+#pragma unroll
+    for (int ks = 0; ks < K3; ++ks) w3s[sl][ks * 64 + lane] = load_operand_global<DT, H2>(row, H2, ks, lane, n < NA);
+    if (lane < 8) b3s[sl][lane] = lane < NA ? bf16_to_f32(b3[q * NA + lane]) : 0.f;
+  }
+  for (int i = tid; i < RP * LDX; i += NT) xs[i] = (T)0;
+  for (int i = tid; i < RP * LD1; i += NT) h1s[i] = (T)0;
+  for (int i = tid; i < RP * LD2; i += NT) h2s[i] = (T)0;
+  __syncthreads();
+  int tmask[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) tmask[m] = __builtin_amdgcn_readfirstlane(ctl_s[2 + m]);
+  const bool envlane = wave == 0 && lane < te_valid;
+  const int el = lane, e = e0 + el;
+  LbfEnv s{};
+  if (envlane) {
+    lbf_load<A, F>(state, p, e, s);
+    lbf_paint_tile<T, A, F, TE>(s, el, xs, LDX, HW, true);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+
+  auto draw_noise = [&](int sn, float* noise, int i0, int stride) {
+    for (int i = i0; i < R * NA; i += stride) {
+      const int row = i / NA, a = i - row * NA;
+      noise[row * 8 + a] = gumbel24(words[(sn * RP + row) * 8 + a] >> 8);
+    }
+  };
+  // one layer over every M tile: each tile runs the weights of the slots its
+  // rows use, each lane keeps its own row's result, then bias + tanh in bf16
+  auto layer = [&](const auto& La, const auto& Lb, const T* in, int ldi, T* outp, int ldo, const float* bias0,
+                   const float* bias1) {
+    using LT = std::decay_t<decltype(La)>;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      f32x4 a0[1][LT::OWN], a1[1][LT::OWN];
+#pragma unroll
+      for (int o = 0; o < LT::OWN; ++o) a0[0][o] = a1[0][o] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (tmask[m] & 1) La.template run<1>(in + m * 16 * ldi, ldi, a0, wave, lane);
+      if (tmask[m] & 2) Lb.template run<1>(in + m * 16 * ldi, ldi, a1, wave, lane);
+      const int sl = slot_s[m * 16 + (lane & 15)];
+#pragma unroll
+      for (int o = 0; o < LT::OWN; ++o)
+        La.store_block(sl ? a1[0][o] : a0[0][o], outp + m * 16 * ldo, ldo, 0, o, wave, lane, sl ? bias1 : bias0);
+    }
+  };
+
+  for (int k = 0; k < n_steps; ++k) {
+    const uint64_t t = t0 + (uint64_t)k;
+    const int sn = k % NOISE_STEPS;
+    __syncthreads();
+    if (sn == 0) {
+      const int nb = min(NOISE_STEPS, n_steps - k);
+      for (int i = tid; i < nb * R; i += NT) {
+        const int st = i / R, row = i - st * R;
+        const int rel = row % TE, ag = row / TE;
+        if (rel < te_valid) {
+          const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + rel), t + st, (uint64_t)ag * 256u,
+                                      TAG_ACTION);
+          uint32_t* d = words + (st * RP + row) * 8;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) d[q] = block_u32(b, q);
+        }
+      }
+      __syncthreads();
+      draw_noise(0, nz[k & 1], tid, NT);
+      __syncthreads();
+    }
+    layer(L1a, L1b, xs, LDX, h1s, LD1, bias_s[0], bias_s[1]);
+    __syncthreads();
+    copy_obs_rows<T, R, D, LDX, NT, true, 4, TE, A>(
+        xs, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, te_valid * A, tid);
+    layer(L2a, L2b, h1s, LD1, h2s, LD2, bias_s[0] + H1, bias_s[1] + H1);
+    __syncthreads();
+    if (wave == 0) {
+      const int g = lane >> 4;
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const int row = m * 16 + (lane & 15);
+        const int rel = row % TE, ag = row / TE;
+        const int sl = slot_s[row];
+        const f32x4 nz4 = *reinterpret_cast<const f32x4*>(&nz[k & 1][row * 8 + 4 * (g & 1)]);
+        f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+        if (tmask[m] & 1) {
+#pragma unroll
+          for (int ks = 0; ks < K3; ++ks)
+            a0 = mfma16<DT>(w3s[0][ks * 64 + lane], load_operand_lds<DT>(h2s, LD2, row, ks, lane), a0);
+        }
+        if (tmask[m] & 2) {
+#pragma unroll
+          for (int ks = 0; ks < K3; ++ks)
+            a1 = mfma16<DT>(w3s[1][ks * 64 + lane], load_operand_lds<DT>(h2s, LD2, row, ks, lane), a1);
+        }
+        float best_s = -INFINITY;
+        int best_a = 0;
+        float logit[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int act = 4 * g + r;
+          logit[r] = (sl ? a1[r] : a0[r]) + b3s[sl][act & 7];
+          const float sc = action_score(logit[r], nz4[r], (act < NA) & (row < R));
+          const bool take = (r == 0) | (sc > best_s);
+          best_s = take ? sc : best_s;
+          best_a = take ? act : best_a;
+        }
+        {
+          const auto ps = __builtin_amdgcn_permlane16_swap(__float_as_uint(best_s), __float_as_uint(best_s), false,
+                                                           false);
+          const auto pa = __builtin_amdgcn_permlane16_swap((uint32_t)best_a, (uint32_t)best_a, false, false);
+          const float os = __uint_as_float((g & 1) ? ps[0] : ps[1]);
+          const int oa = (int)((g & 1) ? pa[0] : pa[1]);
+          const bool take = (os > best_s) | ((os == best_s) & (oa < best_a));
+          best_s = take ? os : best_s;
+          best_a = take ? oa : best_a;
+        }
+        const bool live = row < R && rel < te_valid;
+        const size_t gr = ((size_t)k * E + e0 + rel) * A + ag;
+        if (live && g == 0) {
+          act_s[row] = best_a;
+          if (out.actions) out.actions[gr] = best_a;
+        }
+        if (out.logits && live && g < 2) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (4 * g + r < NA) out.logits[gr * NA + 4 * g + r] = logit[r];
+        }
+      }
+      wave_lds_sync();
+      uint32_t d = 0;
+      float r = 0.f;
+      if (envlane) {
+        int act[LBF_MAXA];
+#pragma unroll
+        for (int i = 0; i < LBF_MAXA; ++i) act[i] = i < A ? act_s[i * TE + el] : 0;
+        lbf_transition<A, F, GH, GW>(p, s, act, r, d);
+      }
+      const uint64_t done_mask = __ballot(envlane && d != 0);
+      if (done_mask) {
+        const int j = lane / nblk, blk = lane - j * nblk;
+        if (j < TE && ((done_mask >> j) & 1ull)) {
+          const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + j), t + 1, (uint64_t)blk, TAG_RESET);
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            if (blk * 8 + q < LBF_MAX_DRAWS) rdraw[j * LBF_MAX_DRAWS + blk * 8 + q] = block_u32(b, q);
+        }
+        wave_lds_sync();
+        if (envlane && d) {
+          uint32_t dw[LBF_MAX_DRAWS];
+#pragma unroll
+          for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[el * LBF_MAX_DRAWS + q] : 0u;
+          lbf_reset_from_draws<A, F>(p, dw, s);
+        }
+      }
+      if (envlane) {
+        lbf_paint_tile<T, A, F, TE>(s, el, xs, LDX, HW, true);
+        if (out.reward) out.reward[(size_t)k * E + e] = r;
+        if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
+      }
+    } else if (k + 1 < n_steps && (k + 1) % NOISE_STEPS != 0) {
+      draw_noise((k + 1) % NOISE_STEPS, nz[(k + 1) & 1], (wave - 1) * 64 + lane, (NW - 1) * 64);
+    }
+  }
+  __syncthreads();
+  if (out.obs_last)
+    copy_obs_rows<T, R, D, LDX, NT, false, 4, TE, A>(xs, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D,
+                                                     te_valid * A, tid);
+  if (envlane) lbf_store<A, F>(state, p, e, s);
+}
+
+hipError_t launch_lbf_run_pop(const LbfParams& p, const PolicyArgs& pol, int n_pol, const int32_t* pidx,
+                              int32_t* state, uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s) {
+  const LbfMagic m = make_magic(p, pol.NA);
+  // the register-resident two-policy kernel for its compiled shape; the
+  // generic kernel then runs only the tiles with three or more policies
+  int skip_two = 0;
+  if (pol.dt == DT_BF16 && p.H == 8 && p.W == 8 && p.A == 2 && p.F == 3 && pol.H1 == 128 && pol.H2 == 128 &&
+      pol.NA == LBF_NACT && TILE_E == 16) {
+    lbf_pop2_kernel<8, 8, 128, 128, 2, 3, 16, 8><<<dim3((unsigned)((p.E + 15) / 16)), 512, 0, s>>>(
+        p, pol, n_pol, pidx, state, t0, n_steps, out);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    skip_two = 1;
+  }
+  const size_t lds = lbf_pop_lds_bytes(p, pol);
+  const dim3 grid((unsigned)((p.E + TILE_E - 1) / TILE_E));
+  // the dynamic limit leaves room for the kernel's few bytes of static LDS
+  const int max_dyn = (int)(MAX_LDS_BYTES - LBF_POP_STATIC_LDS);
+  if (pol.dt == DT_F32) {
+    static bool attr = false;
+    if (!attr) {
+      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_F32, false>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+    lbf_run_pop_kernel<DT_F32, false><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out, skip_two);
+  } else if (pol.Wp[0] != nullptr) {  // fragment-major weights
+    static bool attr = false;
+    if (!attr) {
+      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_BF16, true>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+    lbf_run_pop_kernel<DT_BF16, true><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out, skip_two);
+  } else {
+    static bool attr = false;
+    if (!attr) {
+      const hipError_t e = hipFuncSetAttribute((const void*)lbf_run_pop_kernel<DT_BF16, false>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+    lbf_run_pop_kernel<DT_BF16, false><<<grid, NTHREADS, lds, s>>>(p, m, pol, n_pol, pidx, state, t0, n_steps, out, skip_two);
+  }
+  return hipGetLastError();
 }
 
 // ------------------------------------- env-only steps, three waves ----

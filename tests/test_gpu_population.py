@@ -92,11 +92,13 @@ def test_population_rollout_parity(cfgkw, dims, npol, T, dtype):
     assert np.array_equal(strict["actions"], g["actions"].numpy())
 
 
-@pytest.mark.parametrize("block", [16, 8, 5])
+@pytest.mark.parametrize("block", [16, 8, 5, 0])
 def test_population_benchmark_shape_parity(block):
     """The benchmarked population shape: 9 packed policies 192-128-128-6 bf16, the ego (policy 0) on agent 0
     and teammate 1 + (e // block) mod 8 on agent 1.  Blocks of 16 envs put at most two policies in each
-    16-env tile; blocks of 8 and 5 put three or four there (and out-of-range indices add policy 0 rows)."""
+    16-env tile (the two-policy kernel); blocks of 8 and 5 put three or four there (the generic kernel), and
+    block 0 mixes both kinds of tile in one call (blocks of 16 for envs 0..79, random teammates and a
+    teammate on agent 0 of env 100 after that).  Out-of-range indices add policy 0 rows."""
     require_gpu()
     cfg = R.EnvConfig(n_envs=150, seed=23, env_base=11, max_steps=30)
     dims = (192, 128, 128, 6)
@@ -105,7 +107,12 @@ def test_population_benchmark_shape_parity(block):
     E, A = cfg.n_envs, cfg.n_agents
     ws, bs = _pop(dims, npol, seed=500)
     idx = np.zeros((E, A), dtype=np.int64)
-    idx[:, 1] = 1 + (np.arange(E) // block) % (npol - 1)
+    if block:
+        idx[:, 1] = 1 + (np.arange(E) // block) % (npol - 1)
+    else:
+        idx[:80, 1] = 1 + (np.arange(80) // 16) % (npol - 1)
+        idx[80:, 1] = np.random.default_rng(5).integers(1, npol, size=E - 80)
+        idx[100, 0] = 3
     idx[7, 1], idx[40, 0], idx[149, 1] = -3, npol, 1 << 20  # out of range: policy 0
     pop = R.Population(ws, bs, "bf16")
     assert pop.packed is not None
@@ -155,12 +162,13 @@ def test_population_4096_sampled_envs():
     assert [final[e] for e in sample] == ref["states"]
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_one_policy_population_is_rollout_run(dtype):
-    """Every agent on policy 1 of a population == rollout_run with that policy (generic-kernel shape)."""
+@pytest.mark.parametrize("dtype,dims", [("f32", (192, 48, 32, 6)), ("bf16", (192, 48, 32, 6)),
+                                        ("bf16", (192, 128, 128, 6))])
+def test_one_policy_population_is_rollout_run(dtype, dims):
+    """Every agent on policy 1 of a population == rollout_run with that policy: the generic kernels, and the
+    two-policy kernel against the register-resident rollout kernel (the same MFMA chains and epilogues)."""
     require_gpu()
     cfg = R.EnvConfig(n_envs=45, seed=3)
-    dims = (192, 48, 32, 6)
     ws, bs = _pop(dims, 3, seed=11)
     T = 40
     _, g = _run(cfg, R.Population(ws, bs, dtype), np.ones((45, 2), dtype=np.int64), T)
