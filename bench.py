@@ -36,7 +36,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-envs", type=int, default=2048, help="envs in the oracle's timed sample")
+    ap.add_argument("--cpu-leg", nargs=5, default=None, metavar=("WORKLOAD", "ENV0", "N_ENVS", "DTYPE", "CORE"),
+                    help="(internal) run one timed oracle leg in this process and print its result")
+    ap.add_argument("--cpu-only", action="store_true", help="only the CPU baseline (no GPU work)")
     ap.add_argument("--only", choices=["run_bf16", "run_f32", "env_bf16", "policy_bf16", "copy"], default=None,
                     help="time one kernel only (for profiler runs); 'copy' runs a plain 512 MiB device copy, "
                          "the reference for scaling HBM byte counters")
@@ -300,30 +302,109 @@ def measure_s5(R, workloads, name, dt, steps, warmup):
                     "rocprofv3 summary of this workload"}
 
 
-def cpu_baseline(n_envs, T):
-    """The oracle, single-threaded, on the first n_envs envs of the workload for T steps."""
-    import numpy as np
+# The oracle's timed samples (the CPU baseline): the correctness workload in full, a prefix of each
+# 4096+-env workload for its full step count (64 envs for the headline; fewer where the oracle is slower per
+# step, so that every leg takes 5-20 s), and the headline workload on every host core at once.
+CPU_LEGS = (("lbf8_small", 16, "f32"), ("lbf8_4096", 64, "bf16"), ("lbf12_16k", 32, "bf16"),
+            ("oc_4096", 8, "bf16"), ("hn_4096", 32, "bf16"))
+
+
+def cpu_leg(name, env0, n_envs, dtype, core):
+    """One oracle rollout on one pinned core, in a process of its own that never touches the GPU (run as
+    ``bench.py --cpu-leg``): envs env0 .. env0 + n_envs - 1 of workload ``name`` for its full step count,
+    the workload's policy (weights seed 1000) sampling every action.  Prints agent-steps and seconds."""
+    if core is not None:
+        os.sched_setaffinity(0, {core})
     from threadpoolctl import threadpool_limits
 
-    from oracle import lbf, rollout as orollout
+    from oracle import hanabi, lbf, overcooked, rollout as orollout
     from paper_2609_13716_amd import workloads
-    w = workloads.WORKLOADS[WORKLOAD]
-    e = w["env"]
-    oc = lbf.Config(e["grid_h"], e["grid_w"], e["n_agents"], e["n_food"], e["max_agent_level"],
-                    e["max_food_level"], e["max_steps"])
-    ws, bs = workloads.policy_weights(workloads.policy_dims(WORKLOAD), seed=1000)
+    w = workloads.WORKLOADS[name]
+    kind, e = workloads.kind(name), w["env"]
+    if kind == "overcooked":
+        env, oc, A = overcooked, overcooked.Config(e["cook_time"], e["soup_reward"], e["max_steps"], 2), 2
+    elif kind == "hanabi":
+        env, oc, A = hanabi, hanabi.Config(max_steps=e["max_steps"]), 2
+    else:
+        env, A = lbf, e["n_agents"]
+        oc = lbf.Config(e["grid_h"], e["grid_w"], A, e["n_food"], e["max_agent_level"], e["max_food_level"],
+                        e["max_steps"], e.get("const_levels", False))
+    ws, bs = workloads.policy_weights(workloads.policy_dims(name), seed=1000)
+    T = w["n_steps"]
     with threadpool_limits(1):
         t0 = time.perf_counter()
-        orollout.rollout(lbf, oc, 0, range(n_envs), 0, T, ws, bs, "bf16")
+        orollout.rollout(env, oc, 0, range(env0, env0 + n_envs), 0, T, ws, bs, dtype)
         dt = time.perf_counter() - t0
-    agent_steps = n_envs * T * e["n_agents"]
-    return {"value": round(agent_steps / dt, 1), "unit": "agent-env steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n_envs} envs x {T} steps of {WORKLOAD} (bf16 policy), one thread, {dt:.1f} s",
-            "host_cpus": len(os.sched_getaffinity(0))}
+    acting = 1 if kind == "hanabi" else A  # Hanabi: the mover's row only, as in the GPU figures
+    print(json.dumps({"agent_steps": n_envs * T * acting, "env_steps": n_envs * T, "seconds": dt}), flush=True)
+
+
+def _cpu_children(jobs):
+    """Run oracle legs as child processes (each its own interpreter, pinned to one core, one BLAS thread);
+    jobs = [(name, env0, n_envs, dtype, core)].  Returns their results and the wall time of the batch."""
+    import subprocess
+    env = dict(os.environ, OMP_NUM_THREADS="1", OPENBLAS_NUM_THREADS="1", MKL_NUM_THREADS="1")
+    t0 = time.perf_counter()
+    procs = [subprocess.Popen([sys.executable, os.path.abspath(__file__), "--cpu-leg", n, str(e0), str(ne), dt,
+                               str(c)], stdout=subprocess.PIPE, env=env, cwd=ROOT)
+             for n, e0, ne, dt, c in jobs]
+    outs = []
+    for pr in procs:
+        out, _ = pr.communicate()
+        if pr.returncode != 0:
+            raise RuntimeError(f"oracle leg failed with status {pr.returncode}")
+        outs.append(json.loads(out.decode().strip().splitlines()[-1]))
+    return outs, time.perf_counter() - t0
+
+
+def _host_info():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    rocm = "unknown"
+    for path in ("/opt/rocm/.info/version", "/opt/rocm/.info/version-dev"):
+        if os.path.exists(path):
+            rocm = open(path).read().strip()
+            break
+    return model, rocm
+
+
+def cpu_baseline():
+    """The oracle timed on this host's cores: every leg of CPU_LEGS single-threaded on a core of its own, then the headline
+    workload's 64-env shards on P cores at once (P = this process's CPU affinity count, one process per core,
+    disjoint env ids).  The all-cores figure is the reported baseline value."""
+    cores = sorted(os.sched_getaffinity(0))
+    P = len(cores)
+    legs = {}
+    # the single-threaded legs run side by side, each alone on its own core
+    outs, _ = _cpu_children([(name, 0, n, dt, cores[i % P]) for i, (name, n, dt) in enumerate(CPU_LEGS)])
+    for (name, n, dt), r in zip(CPU_LEGS, outs):
+        legs[name] = {"agent_steps_per_s": round(r["agent_steps"] / r["seconds"], 1),
+                      "env_steps_per_s": round(r["env_steps"] / r["seconds"], 1),
+                      "sample": f"envs 0..{n - 1} x the full step count, {dt} policy", "seconds": round(r["seconds"], 2)}
+    outs, wall = _cpu_children([(WORKLOAD, 64 * i, 64, "bf16", c) for i, c in enumerate(cores)])
+    agent_steps = sum(o["agent_steps"] for o in outs)
+    model, rocm = _host_info()
+    return {"value": round(agent_steps / wall, 1), "unit": "agent-env steps/s", "cores": P, "kind": "oracle",
+            "sample": f"{WORKLOAD}: {P} processes, one per core, each envs 64i..64i+63 x 128 steps (bf16 policy), "
+                      f"{wall:.1f} s wall",
+            "single_thread": legs, "cpu_model": model, "rocm_version": rocm, "host_cpus": P}
 
 
 def main():
     args = parse()
+    if args.cpu_leg:
+        n, e0, ne, dt, c = args.cpu_leg
+        cpu_leg(n, int(e0), int(ne), dt, None if c == "none" else int(c))
+        return
+    if args.cpu_only:
+        print(json.dumps({"cpu_baseline": cpu_baseline()}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the rollout shards over GPUs "
               "by env id with no exchange, and this build times the single-GPU shard.", file=sys.stderr)
@@ -485,7 +566,7 @@ def main():
                                                                 min(args.steps, 5), 1)
         line["workloads"]["lbf8_4096_s5"] = measure_s5(R, workloads, "lbf8_4096_s5", "bf16", min(args.steps, 3), 1)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(args.cpu_envs, T)
+        line["cpu_baseline"] = cpu_baseline()
     print(json.dumps(line), flush=True)
 
 
