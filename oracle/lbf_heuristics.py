@@ -14,9 +14,12 @@ not their mechanics; this module is the reading the rollout kernels implement:
   order of the food cells: lexicographic (row, then column), its reverse,
   column_major (column, then row), its reverse.  These orders depend only on
   the food cells, which do not move, so the plan made at the episode start is
-  the same order read at every step.  (The two agent-position orders of the
-  paper's Sequential agents need the agent's start cell, which the env state
-  does not hold; they are not implemented.)
+  the same order read at every step.  nearest_agent / farthest_agent order
+  the foods by Manhattan distance from the agent's cell at the start of the
+  episode, nearest (farthest) first: the plan the agent makes before the
+  episode from where it stands.  The env state does not hold that start
+  cell; a rollout passes it (``start_cell``): the agent's cell in the first
+  state of its episode, as observed.
 * action: LOAD when the agent is next to its target (4-neighbourhood);
   otherwise one step along the axis with the larger remaining distance (the
   row axis on ties): NORTH/SOUTH by the sign of the row difference,
@@ -35,7 +38,8 @@ from . import lbf
 
 KINDS = ("greedy_closest_self", "greedy_closest_teammate", "greedy_closest_avg", "greedy_lowest_level",
          "greedy_highest_level", "seq_lexicographic", "seq_reverse_lexicographic", "seq_column_major",
-         "seq_reverse_column_major")
+         "seq_reverse_column_major", "seq_nearest_agent", "seq_farthest_agent")
+NEEDS_START = ("seq_nearest_agent", "seq_farthest_agent")  # kinds that read the agent's episode start cell
 
 
 def _rc(cfg, cell):
@@ -47,9 +51,13 @@ def _dist(cfg, a, b):
     return abs(ra - rb) + abs(ca - cb)
 
 
-def target(cfg, state, agent, kind):
-    """Index of the food the heuristic ``kind`` (an index into KINDS) heads for."""
+def target(cfg, state, agent, kind, start_cell=None):
+    """Index of the food the heuristic ``kind`` (an index into KINDS) heads for.
+
+    ``start_cell``: the agent's cell at the start of the episode (needed by the kinds in NEEDS_START)."""
     name = KINDS[kind]
+    if name in NEEDS_START and start_cell is None:
+        raise ValueError(f"{name} plans from the agent's start cell; pass start_cell")
     me = state.agent_cell[agent]
     mate = state.agent_cell[(agent + 1) % cfg.n_agents]
     live = [j for j in range(cfg.n_food) if not state.food_eaten[j]]
@@ -64,13 +72,15 @@ def target(cfg, state, agent, kind):
         "seq_reverse_lexicographic": lambda j: tuple(-x for x in _rc(cfg, fc[j])),
         "seq_column_major": lambda j: _rc(cfg, fc[j])[::-1],
         "seq_reverse_column_major": lambda j: tuple(-x for x in _rc(cfg, fc[j])[::-1]),
+        "seq_nearest_agent": lambda j: (_dist(cfg, start_cell, fc[j]),),
+        "seq_farthest_agent": lambda j: (-_dist(cfg, start_cell, fc[j]),),
     }[name]
     return min(live, key=lambda j: (keys(j), j))
 
 
-def action(cfg, state, agent, kind):
+def action(cfg, state, agent, kind, start_cell=None):
     """The heuristic's action for ``agent`` in ``state``."""
-    j = target(cfg, state, agent, kind)
+    j = target(cfg, state, agent, kind, start_cell)
     (r, c), (tr, tc) = _rc(cfg, state.agent_cell[agent]), _rc(cfg, state.food_cell[j])
     dr, dc = tr - r, tc - c
     if abs(dr) + abs(dc) == 1:
@@ -87,8 +97,8 @@ def action(cfg, state, agent, kind):
     return first
 
 
-def logits(cfg, state, agent, kind):
+def logits(cfg, state, agent, kind, start_cell=None):
     """float64 logits [nA] of the heuristic: 0 for its action, -inf for the others."""
     out = np.full(lbf.N_ACTIONS, -np.inf)
-    out[action(cfg, state, agent, kind)] = 0.0
+    out[action(cfg, state, agent, kind, start_cell)] = 0.0
     return out

@@ -64,7 +64,7 @@ def policy_logits(obs, weights, biases, dtype, policy_index=None):
 
 def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
             states=None, logits_source=None, action_hook=None, policy_index=None, value_head=False,
-            recurrent=None, carry=None, teammates=None):
+            recurrent=None, carry=None, teammates=None, start_cells=None):
     """Roll ``env_ids`` forward ``n_steps`` steps from absolute step ``t0``.
 
     ``states`` are the env states at t0 (default: the initial states, t0 = 0).
@@ -87,8 +87,14 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
     at every step whose observation starts an episode (step counter 0); the
     result also holds ``carry``, the state after the last step (value_last is
     computed without advancing it).
-    ``teammates`` [n, A] (LBF): k in 0..8 = heuristic k of ``lbf_heuristics``
-    (its logits replace the network's); any other value = the network.
+    ``teammates`` [n, A] (LBF): k in 0..len(KINDS)-1 = heuristic k of
+    ``lbf_heuristics`` (its logits replace the network's); any other value =
+    the network.  The start cells of the episodes (which the Sequential
+    nearest/farthest-agent teammates plan from) are tracked along the rollout:
+    the agents' cells in the first state of each episode.  ``start_cells``
+    [n][A] gives them for the episodes running at t0; by default they are the
+    cells of the given states when t0 = 0 (initial states), else the cells of
+    the reset of step t0 - step_count (where those episodes began).
     """
     env_ids = list(env_ids)
     if states is None:
@@ -113,6 +119,13 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
             carry = x
         return np.concatenate([lg, v[:, None]], axis=1).reshape(n, A, -1)
 
+    if teammates is not None:
+        if start_cells is not None:
+            starts = [list(c) for c in start_cells]
+        elif t0 == 0:
+            starts = [list(s.agent_cell) for s in states]
+        else:
+            starts = [list(env.reset(cfg, seed, e, t0 - s.step_count).agent_cell) for e, s in zip(env_ids, states)]
     for k in range(n_steps):
         t = t0 + k
         obs, mask = observe_all(env, cfg, states)
@@ -121,7 +134,8 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
             for i in range(n):
                 for a in range(A):
                     if 0 <= teammates[i][a] < len(lbf_heuristics.KINDS):
-                        logits64[i, a, :nA] = lbf_heuristics.logits(cfg, states[i], a, int(teammates[i][a]))
+                        logits64[i, a, :nA] = lbf_heuristics.logits(cfg, states[i], a, int(teammates[i][a]),
+                                                                    starts[i][a])
         if value_head:
             out["value"].append(logits64[..., nA])
             logits64 = logits64[..., :nA]
@@ -142,6 +156,8 @@ def rollout(env, cfg, seed, env_ids, t0, n_steps, weights, biases, dtype,
         dones = np.zeros(n, dtype=np.uint8)
         for i, e in enumerate(env_ids):
             states[i], rewards[i], dones[i] = env.step(cfg, seed, e, t, states[i], list(actions[i]))
+            if teammates is not None and dones[i]:  # a new episode starts from the reset's cells
+                starts[i] = list(states[i].agent_cell)
         out["obs"].append(obs)
         out["mask"].append(mask)
         out["logits"].append(logits64)

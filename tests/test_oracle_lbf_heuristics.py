@@ -5,7 +5,14 @@
   uneaten foods' distance arrays (first minimum = lowest index);
   Sequential lexicographic is the uneaten food with the smallest row-major
   cell id, column_major the smallest column-major id, their reverses the
-  largest; lowest/highest level is the extreme level, ties to the closest.
+  largest; nearest/farthest agent are numpy argmin/argmax of the distance
+  from the start cell; lowest/highest level is the extreme level, ties to the
+  closest.
+* Start cells in a rollout: every nearest/farthest-agent action is the
+  heuristic's for the agent's cell at its episode's first step, read back
+  from the rollout's own observations and dones; a rollout split in two
+  (the second part recovering the start cells from the reset draws of step
+  t0 - step_count) equals the whole.
 * Actions: LOAD exactly when next to the target; otherwise a move along the
   longer axis that brings the agent one cell closer to it.
 * Behaviour: Greedy agents able to eat alone clear the board (episodes end
@@ -79,16 +86,31 @@ def test_sequential_orders_are_cell_orders():
             assert H.target(CFG, s, a, 8) == max(live, key=col_major.get)
 
 
+def test_sequential_agent_orders_rank_by_distance_from_the_start_cell():
+    rng = np.random.default_rng(7)
+    for s in _states(seed=4):
+        fr, fc = _rows_cols(CFG, s.food_cell)
+        live = ~np.array(s.food_eaten)
+        for a in range(2):
+            start = int(rng.integers(0, 49))
+            sr, sc = divmod(start, 7)
+            d = np.abs(fr - sr) + np.abs(fc - sc)
+            assert H.target(CFG, s, a, 9, start) == int(np.argmin(np.where(live, d, 10 ** 6)))
+            assert H.target(CFG, s, a, 10, start) == int(np.argmax(np.where(live, d, -1)))
+    with pytest.raises(ValueError):
+        H.target(CFG, _states(1)[0], 0, 9)
+
+
 def test_actions_load_next_to_the_target_else_close_in():
     delta = {lbf.NORTH: (-1, 0), lbf.SOUTH: (1, 0), lbf.WEST: (0, -1), lbf.EAST: (0, 1)}
     for s in _states(seed=3):
         for a in range(2):
             for kind in range(len(H.KINDS)):
-                j = H.target(CFG, s, a, kind)
+                j = H.target(CFG, s, a, kind, s.agent_cell[1 - a])
                 r, c = divmod(s.agent_cell[a], 7)
                 tr, tc = divmod(s.food_cell[j], 7)
                 d = abs(tr - r) + abs(tc - c)
-                act = H.action(CFG, s, a, kind)
+                act = H.action(CFG, s, a, kind, s.agent_cell[1 - a])
                 if d == 1:
                     assert act == lbf.LOAD
                     continue
@@ -101,7 +123,7 @@ def test_actions_load_next_to_the_target_else_close_in():
                     cell = lr * 7 + lc
                     foods = {x for x, e in zip(s.food_cell, s.food_eaten) if not e}
                     assert cell in foods or cell == s.agent_cell[1 - a]
-                lg = H.logits(CFG, s, a, kind)
+                lg = H.logits(CFG, s, a, kind, s.agent_cell[1 - a])
                 assert lg[act] == 0 and np.isneginf(np.delete(lg, act)).all()
 
 
@@ -148,3 +170,33 @@ def test_rollout_with_heuristic_teammates(dtype):
     same = rollout.rollout(lbf, CFG, 6, envs, 0, 30, ws, bs, dtype, teammates=np.full((9, 2), -1))
     for key in ("obs", "actions", "reward", "done", "logits"):
         assert np.array_equal(plain[key], same[key]), key
+
+
+def _own_cell(cfg, obs_row):
+    """The agent's cell from its observation (plane 2 is 1 at its own cell)."""
+    hw = cfg.grid_h * cfg.grid_w
+    return int(np.flatnonzero(obs_row[2 * hw:])[0])
+
+
+def test_agent_order_teammates_plan_from_the_episode_start():
+    cfg = lbf.Config(7, 7, 2, 4, 2, 3, max_steps=12)
+    ws, bs = _net(cfg)
+    envs = list(range(8))
+    tm = np.array([[9 + (i % 2), 10 - (i % 2)] for i in envs])  # both agents heuristic, both new orders
+    T = 40
+    out = rollout.rollout(lbf, cfg, 3, envs, 0, T, ws, bs, "f32", teammates=tm)
+    states = rollout.initial_states(lbf, cfg, 3, envs)
+    for i in range(len(envs)):
+        starts = [None, None]
+        for k in range(T):
+            if k == 0 or out["done"][k - 1, i]:
+                starts = [_own_cell(cfg, out["obs"][k, i, a]) for a in range(2)]
+            for a in range(2):
+                assert out["actions"][k, i, a] == H.action(cfg, states[i], a, int(tm[i, a]), starts[a])
+            states[i], _, _ = lbf.step(cfg, 3, envs[i], k, states[i], list(out["actions"][k, i]))
+    assert (out["done"] != 0).sum() >= 2 * len(envs)
+    # a split rollout recovers the start cells of the running episodes from the reset draws
+    a = rollout.rollout(lbf, cfg, 3, envs, 0, 17, ws, bs, "f32", teammates=tm)
+    b = rollout.rollout(lbf, cfg, 3, envs, 17, T - 17, ws, bs, "f32", states=a["states"], teammates=tm)
+    for key in ("obs", "actions", "reward", "done"):
+        assert np.array_equal(out[key], np.concatenate([a[key], b[key]])), key
