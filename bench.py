@@ -134,9 +134,9 @@ def measure_workload(R, workloads, name, dt, steps, warmup):
     t_next = [0]
 
     tm = None
-    if w.get("teammates"):  # agent 0 the policy, agent 1 heuristic kind e mod 9 (a cross-play block per kind)
+    if w.get("teammates"):  # agent 0 the policy, agent 1 heuristic kind e mod 11 (every Greedy and Sequential kind)
         tm = torch.full((E, A), -1, dtype=torch.int32)
-        tm[:, 1] = torch.arange(E, dtype=torch.int32) % 9
+        tm[:, 1] = torch.arange(E, dtype=torch.int32) % len(R.HEURISTICS)
         tm = tm.cuda()
 
     def run():

@@ -261,15 +261,18 @@ rl_status rollout_run_pop(const rl_env_config* cfg, const rl_policy* pop, int32_
                           const rl_traj* out, void* stream);
 
 /* rollout_run with heuristic teammates in the loop (LBF only): agent a of
- * env e acts with the heuristic teammates[e * A + a] when it is in 0..8, and
+ * env e acts with the heuristic teammates[e * A + a] when it is in 0..10, and
  * with `policy` otherwise.  The heuristics are the paper's Greedy and
  * Sequential LBF teammates (Appendix, the table of heuristic teammates), read
  * as deterministic policies of the env state: kinds 0-2 Greedy toward the
  * uneaten food closest to the agent / to agent (a + 1) mod A / to both (sum of
  * Manhattan distances); 3-4 Greedy toward the lowest / highest food level
  * (then the closest); 5-8 Sequential in row-major, reverse row-major,
- * column-major, reverse column-major order of the food cells.  Ties go to
- * the lowest food index.  Next to its target the agent loads; otherwise it
+ * column-major, reverse column-major order of the food cells; 9-10
+ * Sequential nearest / farthest first by Manhattan distance from the agent's
+ * cell at the start of its episode (for an episode already running at t0,
+ * the cell the reset of step t0 - steps placed it on, i.e. where that
+ * episode began).  Ties go to the lowest food index.  Next to its target the agent loads; otherwise it
  * steps along the axis with more distance left (rows on ties), or along the
  * other axis when that cell holds an uneaten food or another agent and the
  * other axis also closes in.  A heuristic agent's logits are 0 for its

@@ -200,23 +200,41 @@ __device__ __forceinline__ void lbf_reset(const LbfParams& p, uint64_t env, uint
   lbf_reset_from_draws<AC, FC>(p, dw, s);
 }
 
+template <int AC, int FC>
+__device__ __forceinline__ void lbf_start_cells(const LbfParams& p, uint64_t env, uint64_t t, const LbfEnv& s,
+                                                int (&start)[LBF_MAXA]) {
+  LbfEnv s0{};
+  lbf_reset<AC, FC>(p, env, t - (uint64_t)s.steps, s0);
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) start[i] = s0.acell[i];
+}
+
 // Heuristic teammates (the paper's Greedy and Sequential LBF agents, read as
 // deterministic policies).  Kinds: 0-2 Greedy closest to self / to the
 // teammate (agent (i + 1) mod A) / to both (sum of distances); 3-4 Greedy
 // lowest / highest food level (then closest to self); 5-8 Sequential in
 // row-major, reverse row-major, column-major, reverse column-major order of
-// the food cells.  The target is the uneaten food of least key (the lowest
-// index on ties).  Next to it the agent loads; otherwise it steps along the
-// axis with more distance left (rows on ties), or along the other axis when
-// that cell holds an uneaten food or another agent and the other axis also
-// closes in.
-constexpr int LBF_NHEUR = 9;
+// the food cells; 9-10 Sequential nearest / farthest first from the agent's
+// cell at the start of its episode (`start`).  The target is the uneaten food
+// of least key (the lowest index on ties).  Next to it the agent loads;
+// otherwise it steps along the axis with more distance left (rows on ties),
+// or along the other axis when that cell holds an uneaten food or another
+// agent and the other axis also closes in.
+constexpr int LBF_NHEUR = 11;
 
-__device__ __forceinline__ int lbf_heuristic_action(const LbfParams& p, const LbfEnv& s, int agent, int kind) {
+// Agent cells at the start of the episode a state is in: the episode began at
+// step t - steps, and its first state is the reset drawn for that step.
+template <int AC = 0, int FC = 0>
+__device__ __forceinline__ void lbf_start_cells(const LbfParams& p, uint64_t env, uint64_t t, const LbfEnv& s,
+                                                int (&start)[LBF_MAXA]);
+
+__device__ __forceinline__ int lbf_heuristic_action(const LbfParams& p, const LbfEnv& s, int agent, int kind,
+                                                    int start) {
   const int A = p.A, F = p.F, W = p.W;
   const int me = s.acell[agent], mate = s.acell[agent + 1 < A ? agent + 1 : 0];
   const int mr = lbf_row(p, me), mc = me - mr * W;
   const int tr_ = lbf_row(p, mate), tc_ = mate - tr_ * W;
+  const int sr = lbf_row(p, start), sc = start - sr * W;
   int best = -1, b1 = 0, b2 = 0, bcell = 0;
 #pragma unroll
   for (int j = 0; j < LBF_MAXF; ++j) {
@@ -234,7 +252,9 @@ __device__ __forceinline__ int lbf_heuristic_action(const LbfParams& p, const Lb
         case 5: k1 = fcell; break;
         case 6: k1 = -fcell; break;
         case 7: k1 = fc * 64 + fr; break;
-        default: k1 = -(fc * 64 + fr); break;
+        case 8: k1 = -(fc * 64 + fr); break;
+        case 9: k1 = abs(fr - sr) + abs(fc - sc); break;
+        default: k1 = -(abs(fr - sr) + abs(fc - sc)); break;
       }
       if (best < 0 || k1 < b1 || (k1 == b1 && k2 < b2)) {
         best = j;

@@ -319,6 +319,7 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
   const uint64_t genv = (uint64_t)(p.env_base + e);
   LbfEnv s{};
   int tkind[LBF_MAXA] = {-1, -1, -1, -1};  // heuristic teammates of this env's agents (-1: the policy)
+  int start[LBF_MAXA] = {0, 0, 0, 0};       // the agents' cells at the start of the current episode
   if (envlane) {
     lbf_load(state, p, e, s);
     lbf_paint(p, s, tid, L, true);
@@ -328,6 +329,7 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
         const int kd = i < A ? out.teammates[(size_t)e * A + i] : -1;
         tkind[i] = (kd >= 0 && kd < LBF_NHEUR) ? kd : -1;
       }
+      lbf_start_cells(p, genv, t0, s, start);
     }
   }
   __syncthreads();
@@ -348,7 +350,7 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
 #pragma unroll
         for (int i = 0; i < LBF_MAXA; ++i)
           if (tkind[i] >= 0) {
-            const int act = lbf_heuristic_action(p, s, i, tkind[i]);
+            const int act = lbf_heuristic_action(p, s, i, tkind[i], start[i]);
             float* l = lg + (tid * A + i) * MAX_NA;
             for (int a = 0; a < NA; ++a) l[a] = a == act ? 0.f : -INFINITY;
           }
@@ -394,7 +396,11 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_kernel(LbfParams p, LbfMagic
       float r;
       uint32_t d;
       lbf_transition(p, s, act, r, d);
-      if (d) lbf_reset(p, genv, t + 1, s);
+      if (d) {
+        lbf_reset(p, genv, t + 1, s);
+#pragma unroll
+        for (int i = 0; i < LBF_MAXA; ++i) start[i] = s.acell[i];
+      }
       lbf_paint(p, s, tid, L, true);
       if (out.reward) out.reward[(size_t)k * p.E + e] = r;
       if (out.done) out.done[(size_t)k * p.E + e] = (uint8_t)d;
@@ -889,10 +895,12 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   // The env state; when LEAN it is kept in LDS between steps and reloaded by
   // the whole env wave, so it is dead (not holding registers) during the MLP.
   LbfEnv s{};
+  int start[TM ? LBF_MAXA : 1] = {};  // TM: the agents' cells at the start of the current episode
   if (envlane) {
     lbf_load<A, F>(state, p, e, s);
     lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
     if constexpr (LEAN) lbf_copy<A, F>(env_s[el], s);
+    if constexpr (TM) lbf_start_cells<A, F>(p, (uint64_t)(p.env_base + e), t0, s, start);
   }
   // Let the prologue loads land here, once (see lbf_env_kernel).
   __builtin_amdgcn_s_waitcnt(0);
@@ -1031,7 +1039,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
           for (int i = 0; i < A; ++i) {
             const int kd = tk_s[el * A + i];
             if (kd >= 0) {
-              act[i] = lbf_heuristic_action(p, s, i, kd);
+              act[i] = lbf_heuristic_action(p, s, i, kd, start[TM ? i : 0]);
               const size_t gr = ((size_t)k * E + e) * A + i;
               if (out.actions) out.actions[gr] = act[i];
               if (out.logits)
@@ -1058,6 +1066,10 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
 #pragma unroll
           for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[el * LBF_MAX_DRAWS + q] : 0u;
           lbf_reset_from_draws<A, F>(p, dw, s);
+          if constexpr (TM) {
+#pragma unroll
+            for (int i = 0; i < A; ++i) start[i] = s.acell[i];
+          }
         }
       }
       if (envlane) {

@@ -126,7 +126,7 @@ EXPORTED = ("rl_state_bytes", "rl_obs_dim", "rl_num_actions", "rollout_last_erro
             "rollout_run_teams", "rl_policy_packed_bytes", "rl_policy_pack", "rollout_run_s5_noalloc")
 HEURISTICS = ("greedy_closest_self", "greedy_closest_teammate", "greedy_closest_avg", "greedy_lowest_level",
               "greedy_highest_level", "seq_lexicographic", "seq_reverse_lexicographic", "seq_column_major",
-              "seq_reverse_column_major")  # kind k of rollout_run_teams
+              "seq_reverse_column_major", "seq_nearest_agent", "seq_farthest_agent")  # kind k of rollout_run_teams
 
 
 def _check(status):

@@ -60,7 +60,7 @@ WORKLOADS = {
                                   max_steps=50),
                          n_envs=4096, n_steps=128, s5=dict(d_model=128, d_state=128, head_width=1024),
                          dtypes=("bf16",)),
-    # ego policy (agent 0) with heuristic teammates (agent 1: Greedy / Sequential kind e mod 9)
+    # ego policy (agent 0) with heuristic teammates (agent 1: Greedy / Sequential kind e mod 11)
     "lbf7_teams_4096": dict(env=dict(grid_h=7, grid_w=7, n_agents=2, n_food=3, max_agent_level=1, max_food_level=2,
                                      max_steps=50, const_levels=True),
                             n_envs=4096, n_steps=128, hidden=(128, 128), dtypes=("bf16",), teammates=True),
