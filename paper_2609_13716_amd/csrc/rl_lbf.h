@@ -283,13 +283,115 @@ __device__ __forceinline__ int lbf_heuristic_action(const LbfParams& p, const Lb
   return (blocked && other_closes) ? other : first;
 }
 
+// The end of a transition: apply the moves and the eaten foods, the reward
+// (one IEEE division, skipped when no env of the wave ate: the quotient is
+// then +0), the step count and the done bits.
+template <int FC = 0>
+__device__ __forceinline__ void lbf_finish(const LbfParams& p, LbfEnv& s, const int (&newcell)[LBF_MAXA],
+                                           uint32_t eaten, int eaten_sum, float& reward, uint32_t& done) {
+  const int F = FC ? FC : p.F;
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) s.acell[i] = newcell[i];
+  s.eaten = eaten;
+  reward = __builtin_amdgcn_ballot_w64(eaten_sum != 0) ? (float)eaten_sum / (float)s.den : 0.f;
+  s.steps += 1;
+  const uint32_t all = (F >= 32) ? 0xffffffffu : ((1u << F) - 1u);
+  done = ((eaten & all) == all ? 1u : 0u) | (s.steps >= p.max_steps ? 2u : 0u);
+}
+
+// The transition on grids of at most 64 cells, with the grid as a 64-bit
+// occupancy mask (bit c = cell c): a move is legal iff its target is on the
+// grid and its bit is clear in the mask of uneaten foods and agents before
+// the step; a loader's 4-neighbourhood is one more mask, and food j is
+// adjacent to it iff bit fcell[j] is set there.  The same rules as
+// lbf_transition_rc in fewer, mostly independent instructions.
+template <int AC = 0, int FC = 0, int HC = 0, int WC = 0>
+__device__ __forceinline__ void lbf_transition_bb(const LbfParams& p, LbfEnv& s, const int (&act_in)[LBF_MAXA],
+                                                  float& reward, uint32_t& done) {
+  const int A = AC ? AC : p.A, F = FC ? FC : p.F, W = WC ? WC : p.W, H = HC ? HC : p.H;
+  const int HW = H * W;
+  int act[LBF_MAXA], col[LBF_MAXA];
+  uint64_t occ = 0;  // uneaten foods and agents before the step
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j)
+    occ |= ((j < F) & !((s.eaten >> j) & 1u)) ? (1ull << (s.fcell[j] & 63)) : 0ull;
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) {
+    act[i] = ((unsigned)act_in[i] < (unsigned)LBF_NACT) ? act_in[i] : 0;
+    col[i] = s.acell[i] - lbf_row_ct<WC>(p, s.acell[i]) * W;
+    occ |= (i < A) ? (1ull << (s.acell[i] & 63)) : 0ull;
+  }
+  // 1. moves: the target of a legal move, else -1
+  int tgt[LBF_MAXA];
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) {
+    const int a = act[i], c = s.acell[i];
+    const bool inb = ((a == 1) & (c >= W)) | ((a == 2) & (c < HW - W)) | ((a == 3) & (col[i] > 0)) |
+                     ((a == 4) & (col[i] < W - 1));
+    const int t = c + (a == 1 ? -W : a == 2 ? W : a == 3 ? -1 : 1);
+    const bool ok = (i < A) & inb & !((occ >> (t & 63)) & 1ull);
+    tgt[i] = ok ? t : -1;
+  }
+  int newcell[LBF_MAXA];
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) {
+    bool contested = false;
+#pragma unroll
+    for (int k = 0; k < LBF_MAXA; ++k)
+      if (k != i) contested |= (k < A) & (tgt[k] == tgt[i]);
+    newcell[i] = ((tgt[i] >= 0) & !contested) ? tgt[i] : s.acell[i];
+  }
+  // 2. loads, with the pre-step positions: the loaders' 4-neighbourhoods
+  uint64_t nb[LBF_MAXA];
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) {
+    const uint64_t b = 1ull << (s.acell[i] & 63);
+    const uint64_t n = (b << W) | (b >> W) | (col[i] > 0 ? b >> 1 : 0ull) | (col[i] < W - 1 ? b << 1 : 0ull);
+    nb[i] = ((i < A) & (act[i] == 5)) ? n : 0ull;
+  }
+  int eaten_sum = 0;
+  uint32_t eaten = s.eaten;
+#pragma unroll
+  for (int j = 0; j < LBF_MAXF; ++j) {
+    int lsum = 0;
+#pragma unroll
+    for (int i = 0; i < LBF_MAXA; ++i) lsum += ((nb[i] >> (s.fcell[j] & 63)) & 1ull) ? s.alevel[i] : 0;
+    const bool eat = (j < F) & !((s.eaten >> j) & 1u) & (lsum > 0) & (lsum >= s.flevel[j]);
+    eaten |= eat ? (1u << j) : 0u;
+    eaten_sum += eat ? s.flevel[j] : 0;
+  }
+  lbf_finish<FC>(p, s, newcell, eaten, eaten_sum, reward, done);
+}
+
 // One transition with actions act[0..A-1] (out-of-range -> noop).
 // Writes reward and done; `s` becomes the post-transition state (no reset).
 // Written without data-dependent branches: every candidate move and load is
 // evaluated and the outcome selected, so the lanes of a wave never diverge.
+// Grids of at most 64 cells take the occupancy-mask form above.
+template <int AC = 0, int FC = 0, int HC = 0, int WC = 0>
+__device__ __forceinline__ void lbf_transition_rc(const LbfParams& p, LbfEnv& s, const int (&act_in)[LBF_MAXA],
+                                                  float& reward, uint32_t& done);
+
 template <int AC = 0, int FC = 0, int HC = 0, int WC = 0>
 __device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, const int (&act_in)[LBF_MAXA],
                                                float& reward, uint32_t& done) {
+  if constexpr (HC > 0 && WC > 0) {
+    if constexpr (HC * WC <= 64)
+      lbf_transition_bb<AC, FC, HC, WC>(p, s, act_in, reward, done);
+    else
+      lbf_transition_rc<AC, FC, HC, WC>(p, s, act_in, reward, done);
+  } else {
+    if (p.HW <= 64)
+      lbf_transition_bb<AC, FC, HC, WC>(p, s, act_in, reward, done);
+    else
+      lbf_transition_rc<AC, FC, HC, WC>(p, s, act_in, reward, done);
+  }
+}
+
+// The transition by rows and columns (any grid size).
+template <int AC, int FC, int HC, int WC>
+__device__ __forceinline__ void lbf_transition_rc(const LbfParams& p, LbfEnv& s, const int (&act_in)[LBF_MAXA],
+                                                  float& reward, uint32_t& done) {
   const int A = AC ? AC : p.A, F = FC ? FC : p.F, W = WC ? WC : p.W, H = HC ? HC : p.H;
   int act[LBF_MAXA], ar[LBF_MAXA], ac[LBF_MAXA], fr[LBF_MAXF], fc[LBF_MAXF];
 #pragma unroll
@@ -344,14 +446,7 @@ __device__ __forceinline__ void lbf_transition(const LbfParams& p, LbfEnv& s, co
     eaten |= eat ? (1u << j) : 0u;
     eaten_sum += eat ? s.flevel[j] : 0;
   }
-#pragma unroll
-  for (int i = 0; i < LBF_MAXA; ++i) s.acell[i] = newcell[i];
-  s.eaten = eaten;
-  // one IEEE division, skipped when no env of the wave ate (the quotient is then +0)
-  reward = __builtin_amdgcn_ballot_w64(eaten_sum != 0) ? (float)eaten_sum / (float)s.den : 0.f;
-  s.steps += 1;
-  const uint32_t all = (F >= 32) ? 0xffffffffu : ((1u << F) - 1u);
-  done = ((eaten & all) == all ? 1u : 0u) | (s.steps >= p.max_steps ? 2u : 0u);
+  lbf_finish<FC>(p, s, newcell, eaten, eaten_sum, reward, done);
 }
 
 }  // namespace rl

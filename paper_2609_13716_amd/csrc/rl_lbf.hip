@@ -829,7 +829,12 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   static_assert(TE <= 64, "env lanes live in wave 0");
   static_assert(TE * ((2 * A + 2 * F + 7) / 8) <= 64, "one lane per reset block");
 
-  __shared__ __align__(16) T xs[RP * LDX];
+  // DB (one M tile): two observation tiles; o_t is read by layer 1 from tile
+  // t % 2 while the env wave paints o_{t+1} onto the other one, and the other
+  // waves copy o_t to the trajectory (clearing it) while the env wave steps.
+  // Otherwise one tile, copied under the layer-2 MFMAs.
+  constexpr bool DB = MT == 1;
+  __shared__ __align__(16) T xs[DB ? 2 : 1][RP * LDX];
   __shared__ __align__(16) T h1s[RP * LD1];
   __shared__ __align__(16) T h2s[RP * LD2];
   __shared__ __align__(16) B w3s[K3 * 64];
@@ -885,7 +890,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     }
   }
   // zero the operand tiles (their K padding and unused rows stay zero)
-  for (int i = tid; i < RP * LDX; i += NT) xs[i] = (T)0;
+  for (int i = tid; i < (DB ? 2 : 1) * RP * LDX; i += NT) (&xs[0][0])[i] = (T)0;
   for (int i = tid; i < RP * LD1; i += NT) h1s[i] = (T)0;
   for (int i = tid; i < RP * LD2; i += NT) h2s[i] = (T)0;
   __syncthreads();
@@ -898,7 +903,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   int start[TM ? LBF_MAXA : 1] = {};  // TM: the agents' cells at the start of the current episode
   if (envlane) {
     lbf_load<A, F>(state, p, e, s);
-    lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
+    lbf_paint_tile<T, A, F>(s, el, xs[0], LDX, HW, true);
     if constexpr (LEAN) lbf_copy<A, F>(env_s[el], s);
     if constexpr (TM) lbf_start_cells<A, F>(p, (uint64_t)(p.env_base + e), t0, s, start);
   }
@@ -908,6 +913,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     const int sn = k % NOISE_STEPS;
+    T* xcur = xs[DB ? (k & 1) : 0];       // o_t
+    T* xnext = xs[DB ? ((k + 1) & 1) : 0];  // o_{t+1}, painted by the env wave
     __syncthreads();  // the env wave is done with the previous step (tile, noise, actions)
     if (sn == 0) {
       // Philox action draws of the next NOISE_STEPS steps, one block (8 draws)
@@ -930,17 +937,18 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     }
     {
       f32x4 acc[MT][RegLayer<DT, D, H1, NW, LEAN>::OWN];
-      L1.template run<MT>(xs, LDX, acc, wave, lane);
+      L1.template run<MT>(xcur, LDX, acc, wave, lane);
       L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane, bias_s);
     }
     __syncthreads();
     {
       f32x4 acc[MT][RegLayer<DT, H1, H2, NW, LEAN>::OWN];
       L2.template run<MT>(h1s, LD1, acc, wave, lane);
-      // o_t to the trajectory while the layer-2 MFMAs run, clearing the tile
-      // behind the copy (the env wave paints o_{t+1} onto it after layer 3)
-      copy_obs_rows<T, R, D, LDX, NT, true>(
-          xs, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, te_valid * A, tid);
+      // (one tile) o_t to the trajectory while the layer-2 MFMAs run, clearing
+      // the tile behind the copy (the env wave paints o_{t+1} onto it after layer 3)
+      if constexpr (!DB)
+        copy_obs_rows<T, R, D, LDX, NT, true>(
+            xcur, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, te_valid * A, tid);
       L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane, bias_s + H1);
     }
     __syncthreads();
@@ -1073,25 +1081,32 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         }
       }
       if (envlane) {
-        lbf_paint_tile<T, A, F>(s, el, xs, LDX, HW, true);
+        lbf_paint_tile<T, A, F>(s, el, xnext, LDX, HW, true);
         if (out.reward) out.reward[(size_t)k * E + e] = r;
         if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
         if constexpr (LEAN) lbf_copy<A, F>(env_s[el], s);
       }
-    } else if (k + 1 < n_steps && (k + 1) % NOISE_STEPS != 0) {
-      // the other waves: Gumbel noise of the next step, while the env wave steps
-      // (a new batch's first step is drawn with the batch)
-      draw_noise((k + 1) % NOISE_STEPS, nz[(k + 1) & 1], (wave - 1) * 64 + lane, (NW - 1) * 64);
+    } else {
+      // the other waves, while the env wave steps: (two tiles) o_t to the
+      // trajectory, clearing its tile; the Gumbel noise of the next step (a new
+      // batch's first step is drawn with the batch)
+      if constexpr (DB)
+        copy_obs_rows<T, R, D, LDX, NT - 64, true>(
+            xcur, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, te_valid * A,
+            tid - 64);
+      if (k + 1 < n_steps && (k + 1) % NOISE_STEPS != 0)
+        draw_noise((k + 1) % NOISE_STEPS, nz[(k + 1) & 1], (wave - 1) * 64 + lane, (NW - 1) * 64);
     }
   }
   __syncthreads();
+  T* xlast = xs[DB ? (n_steps & 1) : 0];  // o_{t0+T}
   if (out.obs_last)
-    copy_obs_rows<T, R, D, LDX, NT>(xs, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, te_valid * A, tid);
+    copy_obs_rows<T, R, D, LDX, NT>(xlast, static_cast<T*>(out.obs_last) + (size_t)e0 * A * D, te_valid * A, tid);
   if constexpr (VH) {
     if (out.value_last) {  // V(o_{t0+T}): one more pass of the network over the final tile
       {
         f32x4 acc[MT][RegLayer<DT, D, H1, NW, LEAN>::OWN];
-        L1.template run<MT>(xs, LDX, acc, wave, lane);
+        L1.template run<MT>(xlast, LDX, acc, wave, lane);
         L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane, bias_s);
       }
       __syncthreads();
