@@ -363,6 +363,82 @@ __device__ __forceinline__ void lbf_transition_bb(const LbfParams& p, LbfEnv& s,
   lbf_finish<FC>(p, s, newcell, eaten, eaten_sum, reward, done);
 }
 
+// The occupancy-mask transition resolved by a group of 8 consecutive lanes
+// per env (a wave holds 8 groups), every lane of the group holding the env
+// state and the actions: lane q of the group evaluates the move of agent
+// q mod 4 (when < A) and the cooperative load of food q (when < F); the
+// agents' targets reach every lane by quad broadcasts (DPP), the contested
+// targets are resolved in every lane, and the eaten foods are gathered with
+// one ballot.  Every lane of the group ends with the same post-step state,
+// reward and done.  All 64 lanes of the wave must be active.
+template <int A, int F, int GH, int GW>
+__device__ __forceinline__ void lbf_transition_group(const LbfParams& p, LbfEnv& s, const int (&act_in)[LBF_MAXA],
+                                                     float& reward, uint32_t& done) {
+  constexpr int W = GW, HW = GH * GW;
+  static_assert(HW <= 64 && A <= 4 && F <= 8, "one occupancy word; agents in a quad; foods in a group");
+  const int lane = (int)(threadIdx.x & 63u), q = lane & 7, me = q & 3;
+  int act[LBF_MAXA], col[LBF_MAXA];
+  uint64_t occ = 0;  // uneaten foods and agents before the step
+#pragma unroll
+  for (int j = 0; j < F; ++j) occ |= !((s.eaten >> j) & 1u) ? (1ull << (s.fcell[j] & 63)) : 0ull;
+#pragma unroll
+  for (int i = 0; i < A; ++i) {
+    act[i] = ((unsigned)act_in[i] < (unsigned)LBF_NACT) ? act_in[i] : 0;
+    col[i] = s.acell[i] % W;
+    occ |= 1ull << (s.acell[i] & 63);
+  }
+  // 1. this lane's agent: the target of a legal move, else -1
+  int a = act[0], c = s.acell[0], cl = col[0];
+#pragma unroll
+  for (int i = 1; i < A; ++i) {
+    a = me == i ? act[i] : a;
+    c = me == i ? s.acell[i] : c;
+    cl = me == i ? col[i] : cl;
+  }
+  const bool inb = ((a == 1) & (c >= W)) | ((a == 2) & (c < HW - W)) | ((a == 3) & (cl > 0)) | ((a == 4) & (cl < W - 1));
+  const int t = c + (a == 1 ? -W : a == 2 ? W : a == 3 ? -1 : 1);
+  const int mytgt = ((me < A) & inb & !((occ >> (t & 63)) & 1ull)) ? t : -1;
+  int tgt[LBF_MAXA];
+  tgt[0] = __builtin_amdgcn_mov_dpp(mytgt, 0x00, 0xf, 0xf, false);  // quad_perm [0,0,0,0]
+  if constexpr (A > 1) tgt[1] = __builtin_amdgcn_mov_dpp(mytgt, 0x55, 0xf, 0xf, false);
+  if constexpr (A > 2) tgt[2] = __builtin_amdgcn_mov_dpp(mytgt, 0xaa, 0xf, 0xf, false);
+  if constexpr (A > 3) tgt[3] = __builtin_amdgcn_mov_dpp(mytgt, 0xff, 0xf, 0xf, false);
+  int newcell[LBF_MAXA];
+#pragma unroll
+  for (int i = 0; i < LBF_MAXA; ++i) {
+    if (i >= A) {
+      newcell[i] = s.acell[i];
+      continue;
+    }
+    bool contested = false;
+#pragma unroll
+    for (int k = 0; k < A; ++k)
+      if (k != i) contested |= tgt[k] == tgt[i];
+    newcell[i] = ((tgt[i] >= 0) & !contested) ? tgt[i] : s.acell[i];
+  }
+  // 2. this lane's food: the levels of the loaders 4-adjacent to it, with the pre-step positions
+  int fc = s.fcell[0], fl = s.flevel[0];
+#pragma unroll
+  for (int j = 1; j < F; ++j) {
+    fc = q == j ? s.fcell[j] : fc;
+    fl = q == j ? s.flevel[j] : fl;
+  }
+  const uint64_t fb = 1ull << (fc & 63);
+  int lsum = 0;
+#pragma unroll
+  for (int i = 0; i < A; ++i) {
+    const uint64_t b = 1ull << (s.acell[i] & 63);
+    const uint64_t n = (b << W) | (b >> W) | (col[i] > 0 ? b >> 1 : 0ull) | (col[i] < W - 1 ? b << 1 : 0ull);
+    lsum += ((act[i] == 5) & ((n & fb) != 0ull)) ? s.alevel[i] : 0;
+  }
+  const bool eat = (q < F) & !((s.eaten >> q) & 1u) & (lsum > 0) & (lsum >= fl);
+  const uint32_t got = (uint32_t)(__builtin_amdgcn_ballot_w64(eat) >> (lane & ~7)) & 0xffu;
+  int eaten_sum = 0;
+#pragma unroll
+  for (int j = 0; j < F; ++j) eaten_sum += ((got >> j) & 1u) ? s.flevel[j] : 0;
+  lbf_finish<F>(p, s, newcell, s.eaten | got, eaten_sum, reward, done);
+}
+
 // One transition with actions act[0..A-1] (out-of-range -> noop).
 // Writes reward and done; `s` becomes the post-transition state (no reset).
 // Written without data-dependent branches: every candidate move and load is

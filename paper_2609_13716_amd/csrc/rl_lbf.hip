@@ -602,8 +602,6 @@ __global__ __launch_bounds__(NTHREADS) void lbf_run_pop_kernel(LbfParams p, LbfM
 
 // ------------------------------------ fused rollout, weights in registers ----
 
-constexpr int LBF_RB = 4;  // steps of reset states built per batch
-
 // Field-wise copy of the A agents and F foods of an env state (a whole-struct
 // copy to or from LDS would turn the register copy into private memory).
 template <int A, int F>
@@ -1526,112 +1524,137 @@ hipError_t launch_lbf_run_pop(const LbfParams& p, const PolicyArgs& pol, int n_p
   return hipGetLastError();
 }
 
-// ------------------------------------- env-only steps, three waves ----
+// ------------------------------------- env-only steps ----
 //
-// rollout_step for compile-time LBF shapes.  Per step k only the transition
-// sits on the env lanes' dependent chain; observing and episode resets are
-// taken off it:
-//   * wave 0 (env): lanes 0..TE-1 keep the env state in registers, read
-//     their actions from LDS one step ahead (the chunk's actions are staged
-//     there, so the loop has no global loads), run the transition, take the
-//     next episode's state from the reset ring when an episode ends, and
-//     publish the post-step state to an LDS snapshot;
-//   * wave 1 (observe): after the step's barrier, paints the snapshot into the
-//     observation tile (one lane per observation row), copies the tile to
-//     the trajectory with 16-byte stores, clearing it behind the copy, and
-//     writes the legal masks, while wave 0 runs step k+1;
-//   * wave 2 (reset): a reset state depends only on (seed, env, step), so it
-//     is built ahead of need: every RB steps, the states that would start an
-//     episode at each of the steps RB..2RB-1 ahead, one (env, step) per lane,
-//     into a ring of 2RB slots.
-template <typename T, int A, int F>
-__device__ __forceinline__ void lbf_paint_row(const LbfEnv& s, int i, T* xr, int HW) {
-  const uint32_t cmax = (uint32_t)HW - 1u;
-#pragma unroll
-  for (int q = 0; q < A; ++q) xr[min((uint32_t)s.acell[q], cmax)] = small_int_to<T>((uint32_t)s.alevel[q]);
-#pragma unroll
-  for (int j = 0; j < F; ++j)  // an eaten food writes 0 at its own (distinct) cell: no branch
-    xr[HW + min((uint32_t)s.fcell[j], cmax)] = !((s.eaten >> j) & 1u) ? small_int_to<T>((uint32_t)s.flevel[j]) : (T)0;
-  xr[2 * HW + min((uint32_t)s.acell[i], cmax)] = small_int_to<T>(1u);
-}
-
-template <typename OT, int GH, int GW, int A, int F, int TE>
-__global__ __launch_bounds__(192) void lbf_env_kernel(LbfParams p, int32_t* __restrict__ state, uint64_t t0,
-                                                      int n_steps, const int32_t* __restrict__ actions,
-                                                      OT* __restrict__ obs, float* __restrict__ reward,
-                                                      uint8_t* __restrict__ done, uint8_t* __restrict__ legal) {
+// rollout_step for compile-time LBF shapes.  The env wave runs S steps
+// between workgroup barriers: per step the transition, the resets of the
+// episodes that ended and the paint of o_{t+1}.  Everything that touches
+// global memory inside the step loop is left to the other ("copy") waves:
+//   * wave 0 (env): the env state lives in registers; on grids of at most 64
+//     cells the 8 lanes of a group hold one env and resolve its transition
+//     together (lbf_transition_group), otherwise lane e holds env e.  The
+//     actions come from LDS one step ahead.  The reset draws of the envs that
+//     ended are made in parallel, one Philox block per lane.  The env's first
+//     lane paints o_{t+1} onto the observation tile of its step (cleared
+//     behind the previous copy of that tile) and leaves the reward and done
+//     in LDS;
+//   * waves 1..NCW (copy): after a barrier, copy the S tiles of the steps just
+//     run to the trajectory with 16-byte stores, clearing them behind the
+//     copy, and write the rewards, dones and legal masks, while wave 0 runs
+//     the next S steps on the other S tiles; at the start of each chunk of
+//     ACT_CHUNK steps they stage the next chunk's actions into the other half
+//     of a double buffer (a global load waits for its wave's earlier stores,
+//     so wave 0 issues none inside the loop).
+template <typename OT, int GH, int GW, int A, int F, int TE, int NCW, int S>
+__global__ __launch_bounds__(64 * (NCW + 1)) void lbf_env_kernel(LbfParams p, int32_t* __restrict__ state,
+                                                                 uint64_t t0, int n_steps,
+                                                                 const int32_t* __restrict__ actions,
+                                                                 OT* __restrict__ obs, float* __restrict__ reward,
+                                                                 uint8_t* __restrict__ done,
+                                                                 uint8_t* __restrict__ legal) {
   constexpr int HW = GH * GW, D = 3 * HW, R = TE * A;
-  constexpr int RS = 2 * LBF_RB;  // reset ring slots: slot k % RS holds the state an episode ending at step k restarts from
-  static_assert(TE <= 64 && TE * RS <= 64, "one lane per env, and per (env, step) of the first reset batch");
-  static_assert(ACT_CHUNK % LBF_RB == 0, "batches do not straddle action chunks");
-  __shared__ __align__(16) OT xs[R * D];
-  __shared__ int32_t act_lds[ACT_CHUNK * TE * A];
-  __shared__ LbfEnv snap[2][TE];   // post-step state of step k, in slot k % 2
-  __shared__ LbfEnv ring[RS][TE];  // reset states
-  constexpr int GC = (R * D * sizeof(OT) / 16 + 63) / 64 < 8 ? (R * D * sizeof(OT) / 16 + 63) / 64 : 8;
+  constexpr int NT = 64 * (NCW + 1), NC = 64 * NCW;
+  constexpr bool GRP = HW <= 64 && A <= 4 && F <= 8 && TE == 8;  // lane groups of 8 per env
+  constexpr int G = GRP ? 8 : 1;
+  constexpr int nd = 2 * A + 2 * F;
+  constexpr int nblk = (nd + 7) >> 3;
+  static_assert(TE * G <= 64 && TE * nblk <= 64, "env lanes in wave 0, and one lane per reset block");
+  constexpr int CH = ACT_CHUNK;
+  static_assert(CH % S == 0, "barrier groups of S steps do not straddle action chunks");
+  __shared__ __align__(16) OT xs[2][S][R * D];      // o_{t+1} of step k in xs[(k / S) % 2][k % S]
+  __shared__ int32_t act_lds[2][CH * TE * A];      // actions of chunk c in act_lds[c % 2]
+  __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];   // reset draws of the envs that ended
+  __shared__ float rw_s[2][S][TE];                 // reward and done of step k, as its tile
+  __shared__ uint32_t dn_s[2][S][TE];
+  constexpr int GC = (R * D * sizeof(OT) / 16 + NC - 1) / NC < 4 ? (R * D * sizeof(OT) / 16 + NC - 1) / NC : 4;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE;
   const int te_valid = min(TE, p.E - e0);
   const int E = p.E;
-  const bool envlane = wave == 0 && lane < te_valid;
-  const int e = e0 + lane;
-  // wave 2: reset states of steps k0 .. k0+n-1 (key t0 + step + 1), one (env, step) per lane
-  auto build_resets = [&](int k0, int n) {
-    const int j = lane % TE, u = lane / TE;
-    if (u < n && j < te_valid) {
-      LbfEnv r{};
-      lbf_reset<A, F>(p, (uint64_t)(p.env_base + e0 + j), t0 + (uint64_t)(k0 + u) + 1, r);
-      lbf_copy<A, F>(ring[(k0 + u) % RS][j], r);
-    }
-  };
+  const int el = lane / G;                          // wave 0: env of this lane
+  const bool grplane = wave == 0 && el < te_valid;  // lanes holding env el's state
+  const bool envlane = grplane && lane % G == 0;    // the lane that writes env el's outputs
+  const int e = e0 + el;
+  const int ea = min(el, TE - 1) * A;  // this lane's env's first action in a step's staged actions
 
-  zero_lds<192>(xs, sizeof(xs), tid);
-  if (wave == 2) build_resets(0, RS);
+  zero_lds<NT>(xs, sizeof(xs), tid);
+  stage_actions<TE * A, NT>(actions, E, e0, te_valid * A, A, 0, min(CH, n_steps), act_lds[0], tid);
   LbfEnv s{};
-  if (envlane) lbf_load<A, F>(state, p, e, s);
-  for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
-    const int nk = min(ACT_CHUNK, n_steps - k0);
-    stage_actions<TE * A, 192>(actions, E, e0, te_valid * A, A, k0, nk, act_lds, tid);
-    __syncthreads();
+  if (grplane) lbf_load<A, F>(state, p, e, s);
+  for (int k0 = 0; k0 < n_steps; k0 += CH) {
+    const int nk = min(CH, n_steps - k0);
+    const int32_t* acts = act_lds[(k0 / CH) & 1];
+    __syncthreads();  // this chunk's actions are staged
     int act[LBF_MAXA] = {0, 0, 0, 0};
-    if (envlane) {
+    if (wave == 0) {
 #pragma unroll
-      for (int i = 0; i < A; ++i) act[i] = act_lds[lane * A + i];
+      for (int i = 0; i < A; ++i) act[i] = acts[ea + i];
     }
-    for (int kk = 0; kk < nk; ++kk) {
-      const int k = k0 + kk;
+    for (int kb = 0; kb < nk; kb += S) {
+      const int ns = min(S, nk - kb);
+      const int pr = ((k0 + kb) / S) & 1;  // the tiles of these steps
       if (wave == 0) {
-        if (envlane) {
+#pragma unroll 1
+        for (int u = 0; u < ns; ++u) {
+          const int kk = kb + u, k = k0 + kk;
+          const uint64_t t = t0 + (uint64_t)k;
           uint32_t d = 0;
           float r = 0.f;
-          lbf_transition<A, F, GH, GW>(p, s, act, r, d);
-          if (d) lbf_copy<A, F>(s, ring[k % RS][lane]);
-          lbf_copy<A, F>(snap[k & 1][lane], s);
-          if (reward) reward[(size_t)k * E + e] = r;
-          if (done) done[(size_t)k * E + e] = (uint8_t)d;
-          if (kk + 1 < nk) {
+          if constexpr (GRP) {
+            lbf_transition_group<A, F, GH, GW>(p, s, act, r, d);  // every lane of the wave
+          } else {
+            if (grplane) lbf_transition<A, F, GH, GW>(p, s, act, r, d);
+          }
+          if (kk + 1 < nk) {  // the next step's actions, ahead of need
 #pragma unroll
-            for (int i = 0; i < A; ++i) act[i] = act_lds[(kk + 1) * TE * A + lane * A + i];
+            for (int i = 0; i < A; ++i) act[i] = acts[(kk + 1) * TE * A + ea + i];
+          }
+          // resets of the envs that ended, drawn at t + 1: one Philox block per lane
+          const uint64_t done_mask = __ballot(envlane && d != 0);
+          if (done_mask) {
+            const int j = lane / nblk, blk = lane - j * nblk;
+            if (j < TE && ((done_mask >> (j * G)) & 1ull)) {
+              const Block4 b = draw_block(p.seed, (uint64_t)(p.env_base + e0 + j), t + 1, (uint64_t)blk, TAG_RESET);
+#pragma unroll
+              for (int q = 0; q < 8; ++q)
+                if (blk * 8 + q < LBF_MAX_DRAWS) rdraw[j * LBF_MAX_DRAWS + blk * 8 + q] = block_u32(b, q);
+            }
+            wave_lds_sync();
+            if (grplane && d) {
+              uint32_t dw[LBF_MAX_DRAWS];
+#pragma unroll
+              for (int q = 0; q < LBF_MAX_DRAWS; ++q) dw[q] = q < nd ? rdraw[el * LBF_MAX_DRAWS + q] : 0u;
+              lbf_reset_from_draws<A, F>(p, dw, s);
+            }
+          }
+          if (envlane) {
+            if (obs) lbf_paint_tile<OT, A, F>(s, el, xs[pr][u], D, HW, true);
+            rw_s[pr][u][el] = r;
+            dn_s[pr][u][el] = d;
           }
         }
-      } else if (wave == 2) {
-        // slots of steps k+RB .. k+2RB-1: last read at steps k-RB .. k-1
-        if (k % LBF_RB == 0) build_resets(k + LBF_RB, LBF_RB);
       }
-      __syncthreads();  // snapshot k published (and snapshot k-1 observed)
-      if (wave == 1) {
-        if (obs) {
-          if (lane < te_valid * A) {
-            const int el = lane / A, i = lane - el * A;
-            lbf_paint_row<OT, A, F>(snap[k & 1][el], i, xs + lane * D, HW);
+      __syncthreads();  // these steps painted and published (and the previous ones copied and cleared)
+      if (wave != 0) {
+        const int ct = tid - 64;  // 0 .. NC-1
+        for (int u = 0; u < ns; ++u) {
+          const int k = k0 + kb + u;
+          if (obs)
+            copy_obs_rows<OT, R, D, D, NC, true, GC>(xs[pr][u], obs + ((size_t)k * E + e0) * A * D, te_valid * A,
+                                                     ct);
+          if (ct < te_valid) {
+            if (reward) reward[(size_t)k * E + e0 + ct] = rw_s[pr][u][ct];
+            if (done) done[(size_t)k * E + e0 + ct] = (uint8_t)dn_s[pr][u][ct];
           }
-          copy_obs_rows<OT, R, D, D, 64, true, GC>(xs, obs + ((size_t)k * E + e0) * A * D, te_valid * A, lane);
+          if (legal && wave == 1)
+            lbf_write_legal<64>(p, te_valid, legal + ((size_t)k * E + e0) * A * LBF_NACT, lane);
         }
-        if (legal) lbf_write_legal<64>(p, te_valid, legal + ((size_t)k * E + e0) * A * LBF_NACT, lane);
+        if (kb == 0 && k0 + CH < n_steps)  // the next chunk's actions, into the other buffer
+          stage_actions<TE * A, NC>(actions, E, e0, te_valid * A, A, k0 + CH, min(CH, n_steps - k0 - CH),
+                                    act_lds[(k0 / CH + 1) & 1], ct);
       }
     }
-    __syncthreads();  // the chunk's actions are read (and its last tile copied) before the next chunk
   }
   if (envlane) lbf_store<A, F>(state, p, e, s);
 }
@@ -1640,7 +1663,13 @@ template <typename OT, int GH, int GW, int A, int F, int TE>
 static hipError_t launch_env_ct(const LbfParams& p, int32_t* state, uint64_t t0, int n_steps,
                                 const int32_t* actions, void* obs, float* reward, uint8_t* done, uint8_t* legal,
                                 hipStream_t s) {
-  lbf_env_kernel<OT, GH, GW, A, F, TE><<<dim3((unsigned)((p.E + TE - 1) / TE)), 192, 0, s>>>(
+  // copy waves: enough that copying a step's observation tile keeps up with
+  // the env wave; steps per barrier: as many as two pairs of tiles fit in a
+  // quarter of the LDS
+  constexpr int NCW = sizeof(OT) == 4 ? 3 : 2;
+  constexpr size_t TILE = (size_t)TE * A * 3 * GH * GW * sizeof(OT);
+  constexpr int S = 4 * TILE <= MAX_LDS_BYTES / 4 ? 2 : 1;
+  lbf_env_kernel<OT, GH, GW, A, F, TE, NCW, S><<<dim3((unsigned)((p.E + TE - 1) / TE)), 64 * (NCW + 1), 0, s>>>(
       p, state, t0, n_steps, actions, static_cast<OT*>(obs), reward, done, legal);
   return hipGetLastError();
 }
