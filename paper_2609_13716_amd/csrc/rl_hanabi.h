@@ -102,30 +102,34 @@ __device__ __forceinline__ void hn_add_disc(HnEnv& s, int card) {
 }
 
 // The deck of a fresh game at step t, shuffled by one whole wave (all lanes
-// call this with the same env and t): lane l < CARDS holds the card at
-// position l, starting from the ordered deck (per colour: rank 1 x3, middle
-// ranks x2, the top rank x1); Fisher-Yates for i = CARDS-1 down to 1 swaps
-// positions i and j = u(i + 1), with draw k = CARDS-1 - i of the reset
-// stream.  The first lanes evaluate the Philox blocks of the draws; every
-// swap is then two readlanes.  The packed deck words (card k in byte k % 4 of
-// word k / 4; the words past the game's deck are 0) are written to `words`.
+// call this with the same env and t): Fisher-Yates from the ordered deck (per
+// colour: rank 1 x3, middle ranks x2, the top rank x1) for i = CARDS-1 down to
+// 1 swaps positions i and j_i = u(i + 1), with draw k = CARDS-1 - i of the
+// reset stream.  Each lane l < CARDS finds the card that ends at position l
+// without moving any card: the swaps applied in that order leave at l the
+// card that started at S_{CARDS-1}( ... S_1(l)), S_i exchanging i and j_i, so
+// the lane follows its position through S_1, S_2, ... (two compares and two
+// selects per swap, j_i in scalar registers) and reads the ordered deck
+// there.  The first lanes evaluate the Philox blocks of the draws.  The packed
+// deck words (card k in byte k % 4 of word k / 4; the words past the game's
+// deck are 0) are written to `words`.
 template <class G>
 __device__ __forceinline__ void hn_wave_shuffle(uint64_t seed, uint64_t env, uint64_t t, int lane,
                                                 uint32_t* __restrict__ words) {
   constexpr int NB = (G::CARDS - 1 + 7) / 8;
   Block4 b{0, 0, 0, 0};
   if (lane < NB) b = draw_block(seed, env, t, (uint64_t)lane, TAG_RESET);
-  const int c = lane / G::PER_COLOUR, o = lane - c * G::PER_COLOUR;
-  const int rk = o < 3 ? 0 : min((o - 3) / 2 + 1, G::R - 1);
-  int a = c * G::R + rk;
+  int x = lane;
 #pragma unroll
-  for (int k = 0; k < G::CARDS - 1; ++k) {
-    const int i = G::CARDS - 1 - k;
+  for (int i = 1; i < G::CARDS; ++i) {
+    const int k = G::CARDS - 1 - i;  // the draw of the swap at position i
     const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)block_u32(b, k & 7), k >> 3);
     const int j = (int)range_map(d, (uint32_t)(i + 1));
-    const int ai = __builtin_amdgcn_readlane(a, i), aj = __builtin_amdgcn_readlane(a, j);
-    a = lane == i ? aj : lane == j ? ai : a;
+    x = x == i ? j : x == j ? i : x;
   }
+  const int c = x / G::PER_COLOUR, o = x - c * G::PER_COLOUR;
+  const int rk = o < 3 ? 0 : min((o - 3) / 2 + 1, G::R - 1);
+  const int a = c * G::R + rk;
   uint32_t v = lane < G::CARDS ? (uint32_t)a << (8 * (lane & 3)) : 0u;
   v |= (uint32_t)__shfl_xor((int)v, 1);
   v |= (uint32_t)__shfl_xor((int)v, 2);

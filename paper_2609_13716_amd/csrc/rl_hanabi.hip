@@ -27,15 +27,18 @@ struct HnTile {
 // same field of different rows, so a wave runs few of the field branches) and
 // ORs it into the row's words (LDS atomics; the words are zero beforehand).
 // Needs the published games.
+// `rows`: the bit vectors row by row (row 2 el + me, HN_OBS_WORDS words
+// each), or null for the vectors inside the HnTiles.
 template <class G, int TE, int NT>
-__device__ __forceinline__ void hn_build_bits(HnTile* envs, int te_valid, int tid) {
+__device__ __forceinline__ void hn_build_bits(HnTile* envs, int te_valid, int tid, uint64_t* rows = nullptr) {
   for (int t = tid; t < 2 * TE * G::NFIELDS; t += NT) {
     const int f = t / (2 * TE), row = t - f * (2 * TE), el = row >> 1, me = row & 1;
     if (el >= te_valid) continue;
     int off;
     const uint64_t v = hn_field_bits<G>(envs[el].pub, me, f, off);
     if (v) {
-      unsigned long long* w = reinterpret_cast<unsigned long long*>(envs[el].bits[me]);
+      unsigned long long* w =
+          reinterpret_cast<unsigned long long*>(rows ? rows + row * HN_OBS_WORDS : envs[el].bits[me]);
       const int i = off >> 6, sh = off & 63;
       atomicOr(w + i, (unsigned long long)(v << sh));
       if (sh && (v >> (64 - sh))) atomicOr(w + i + 1, (unsigned long long)(v >> (64 - sh)));
@@ -62,6 +65,50 @@ __device__ __forceinline__ void hn_paint(HnTile* envs, int te_valid, T* tile, in
       const int f = 64 * i + lane;
       if (f < G::OBS) row[f] = small_int_to<T>((uint32_t)(w[i] >> lane) & 1u);
     }
+  }
+}
+
+// Features j .. j+n-1 (n <= 32) of an observation row held as a bit vector
+// (features past the row's end read as 0).
+__device__ __forceinline__ uint32_t hn_row_bits(const uint64_t* w, int j, int n) {
+  const int wi = j >> 6, sh = j & 63;
+  uint64_t x = w[wi] >> sh;
+  if (sh && wi + 1 < HN_OBS_WORDS) x |= w[wi + 1] << (64 - sh);
+  return (uint32_t)x & (n >= 32 ? ~0u : ((1u << n) - 1u));
+}
+
+// Write `nrows` observation rows of G::OBS features, held as bit vectors
+// (row r at rows + r * HN_OBS_WORDS), to consecutive global rows as 0 / 1
+// values, straight from the bits: each thread expands VB bytes of output at a
+// time (16 when the destination allows, else 4) from the features they cover,
+// which may span two rows.
+template <class G, typename OT, int NT>
+__device__ __forceinline__ void hn_write_obs(const uint64_t* rows, int nrows, OT* __restrict__ dst, int tid) {
+  const int total = nrows * G::OBS;
+  auto bits_at = [&](int f0, int ve) -> uint32_t {  // features f0 .. f0+ve-1 of the flat tile
+    const int r = f0 / G::OBS, j = f0 - r * G::OBS;
+    const int n0 = min(ve, G::OBS - j);
+    uint32_t b = hn_row_bits(rows + r * HN_OBS_WORDS, j, n0);
+    if (n0 < ve) b |= hn_row_bits(rows + (r + 1) * HN_OBS_WORDS, 0, ve - n0) << n0;
+    return b;
+  };
+  const uint32_t one = sizeof(OT) == 2 ? 0x3f80u : 0x3f800000u;  // 1.0 in OT
+  auto word = [&](uint32_t b, int q) -> uint32_t {  // output word q of a vector with feature bits b
+    if constexpr (sizeof(OT) == 2)
+      return (((b >> (2 * q)) & 1u) ? one : 0u) | (((b >> (2 * q + 1)) & 1u) ? one << 16 : 0u);
+    else
+      return ((b >> q) & 1u) ? one : 0u;
+  };
+  constexpr int VE = 16 / sizeof(OT), WE = 4 / sizeof(OT);  // features per 16-byte vector, per word
+  if ((reinterpret_cast<uintptr_t>(dst) & 15) == 0 && total % VE == 0) {
+    u32x4* g4 = reinterpret_cast<u32x4*>(dst);
+    for (int v = tid; v < total / VE; v += NT) {
+      const uint32_t b = bits_at(v * VE, VE);
+      g4[v] = u32x4{word(b, 0), word(b, 1), word(b, 2), word(b, 3)};
+    }
+  } else {
+    uint32_t* g = reinterpret_cast<uint32_t*>(dst);
+    for (int v = tid; v < total / WE; v += NT) g[v] = word(bits_at(v * WE, WE), 0);
   }
 }
 
@@ -144,13 +191,16 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
   __shared__ HnTile envs[TE];
   __shared__ uint32_t need[TE + 1];  // per env, then "any" at [TE]
   __shared__ uint32_t words[TE][HN_DECK_WORDS];
-  __shared__ __align__(16) OT tile[2 * TE * G::OBS];
+  // the observation bit vectors of step k, row 2 el + me, in rows[k % 2]; the
+  // other buffer is cleared while these are written out
+  __shared__ __align__(16) uint64_t rows[2][2 * TE * HN_OBS_WORDS];
   __shared__ int32_t act_lds[ACT_CHUNK * TE * 2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
   const bool envlane = tid < te_valid;
   const int e = e0 + tid;
-  zero_lds<NTHREADS>(envs, sizeof(envs), tid);  // the bit vectors start clear
+  zero_lds<NTHREADS>(envs, sizeof(envs), tid);
+  zero_lds<NTHREADS>(rows, sizeof(rows), tid);  // the bit vectors start clear
   HnEnv s;
   if (envlane) hn_load(state, E, e, s);
   for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
@@ -182,14 +232,14 @@ __global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* _
         __syncthreads();
       }
       if (obs) {
-        hn_build_bits<G, TE, NTHREADS>(envs, te_valid, tid);
+        uint64_t* cur = rows[k & 1];
+        hn_build_bits<G, TE, NTHREADS>(envs, te_valid, tid, cur);
         __syncthreads();
-        hn_paint<G, OT, NW>(envs, te_valid, tile, G::OBS, wave, lane);
-        __syncthreads();
-        copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * G::OBS, 2 * te_valid * G::OBS, tid, NTHREADS);
+        hn_write_obs<G, OT, NTHREADS>(cur, 2 * te_valid, obs + ((size_t)k * E + e0) * 2 * G::OBS, tid);
+        for (int i = tid; i < 2 * TE * HN_OBS_WORDS; i += NTHREADS) rows[(k + 1) & 1][i] = 0;
       }
       if (legal) hn_write_legal<G, NTHREADS>(envs, te_valid, legal + ((size_t)k * E + e0) * 2 * G::NACT, tid);
-      __syncthreads();  // the tile and masks are read before the next move rewrites them
+      __syncthreads();  // the bit vectors and masks are read before the next move rewrites them
     }
   }
   if (envlane) hn_store(state, E, e, s);
