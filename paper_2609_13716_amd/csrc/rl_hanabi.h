@@ -110,12 +110,11 @@ __device__ __forceinline__ void hn_add_disc(HnEnv& s, int card) {
 // card that started at S_{CARDS-1}( ... S_1(l)), S_i exchanging i and j_i, so
 // the lane follows its position through S_1, S_2, ... (two compares and two
 // selects per swap, j_i in scalar registers) and reads the ordered deck
-// there.  The first lanes evaluate the Philox blocks of the draws.  The packed
-// deck words (card k in byte k % 4 of word k / 4; the words past the game's
-// deck are 0) are written to `words`.
+// there.  The first lanes evaluate the Philox blocks of the draws.  Returns
+// the packed deck words (card k in byte k % 4 of word k / 4; the words past
+// the game's deck are 0): lane 4 w holds word w.
 template <class G>
-__device__ __forceinline__ void hn_wave_shuffle(uint64_t seed, uint64_t env, uint64_t t, int lane,
-                                                uint32_t* __restrict__ words) {
+__device__ __forceinline__ uint32_t hn_wave_deck(uint64_t seed, uint64_t env, uint64_t t, int lane) {
   constexpr int NB = (G::CARDS - 1 + 7) / 8;
   Block4 b{0, 0, 0, 0};
   if (lane < NB) b = draw_block(seed, env, t, (uint64_t)lane, TAG_RESET);
@@ -133,17 +132,24 @@ __device__ __forceinline__ void hn_wave_shuffle(uint64_t seed, uint64_t env, uin
   uint32_t v = lane < G::CARDS ? (uint32_t)a << (8 * (lane & 3)) : 0u;
   v |= (uint32_t)__shfl_xor((int)v, 1);
   v |= (uint32_t)__shfl_xor((int)v, 2);
+  return v;
+}
+
+// hn_wave_deck with the words written to `words` (LDS).
+template <class G>
+__device__ __forceinline__ void hn_wave_shuffle(uint64_t seed, uint64_t env, uint64_t t, int lane,
+                                                uint32_t* __restrict__ words) {
+  const uint32_t v = hn_wave_deck<G>(seed, env, t, lane);
   if ((lane & 3) == 0 && lane < 4 * HN_DECK_WORDS) words[lane >> 2] = v;
 }
 
 // A fresh game on the shuffled deck `words`: player 0 holds cards 0..H-1 in
 // slots 0..H-1, player 1 cards H..2H-1, card 2H is drawn next; player 0 moves
 // first with all tokens and lives, blank knowledge, no fireworks or discards.
+// hn_deal_deck deals from the deck already in s.deck.
 template <class G>
-__device__ __forceinline__ void hn_deal(HnEnv& s, const uint32_t* __restrict__ words) {
+__device__ __forceinline__ void hn_deal_deck(HnEnv& s) {
   constexpr int HN_HAND = G::H;
-#pragma unroll
-  for (int w = 0; w < HN_DECK_WORDS; ++w) s.deck[w] = words[w];
 #pragma unroll
   for (int pl = 0; pl < 2; ++pl) {
     uint32_t h = 0;
@@ -170,11 +176,19 @@ __device__ __forceinline__ void hn_deal(HnEnv& s, const uint32_t* __restrict__ w
   s.last = 0;
 }
 
-// Legal actions of the player to move as a 20-bit mask.  (Player-indexed
-// fields are picked with selects, not indexed by the mover: a register array
-// indexed at run time would live in scratch memory.)
 template <class G>
-__device__ __forceinline__ uint32_t hn_legal(const HnEnv& s) {
+__device__ __forceinline__ void hn_deal(HnEnv& s, const uint32_t* __restrict__ words) {
+#pragma unroll
+  for (int w = 0; w < HN_DECK_WORDS; ++w) s.deck[w] = words[w];
+  hn_deal_deck<G>(s);
+}
+
+// Legal actions of the player to move as a 20-bit mask, from a game or its
+// published copy.  (Player-indexed fields are picked with selects, not
+// indexed by the mover: a register array indexed at run time would live in
+// scratch memory.)
+template <class G, class S>
+__device__ __forceinline__ uint32_t hn_legal(const S& s) {
   constexpr int HN_HAND = G::H, HN_RANKS = G::R, HN_COLOURS = G::C;
   const bool one = s.cur == 1;
   const int np = one ? s.n[1] : s.n[0], nq = one ? s.n[0] : s.n[1];

@@ -27,18 +27,15 @@ struct HnTile {
 // same field of different rows, so a wave runs few of the field branches) and
 // ORs it into the row's words (LDS atomics; the words are zero beforehand).
 // Needs the published games.
-// `rows`: the bit vectors row by row (row 2 el + me, HN_OBS_WORDS words
-// each), or null for the vectors inside the HnTiles.
 template <class G, int TE, int NT>
-__device__ __forceinline__ void hn_build_bits(HnTile* envs, int te_valid, int tid, uint64_t* rows = nullptr) {
+__device__ __forceinline__ void hn_build_bits(HnTile* envs, int te_valid, int tid) {
   for (int t = tid; t < 2 * TE * G::NFIELDS; t += NT) {
     const int f = t / (2 * TE), row = t - f * (2 * TE), el = row >> 1, me = row & 1;
     if (el >= te_valid) continue;
     int off;
     const uint64_t v = hn_field_bits<G>(envs[el].pub, me, f, off);
     if (v) {
-      unsigned long long* w =
-          reinterpret_cast<unsigned long long*>(rows ? rows + row * HN_OBS_WORDS : envs[el].bits[me]);
+      unsigned long long* w = reinterpret_cast<unsigned long long*>(envs[el].bits[me]);
       const int i = off >> 6, sh = off & 63;
       atomicOr(w + i, (unsigned long long)(v << sh));
       if (sh && (v >> (64 - sh))) atomicOr(w + i + 1, (unsigned long long)(v >> (64 - sh)));
@@ -68,30 +65,19 @@ __device__ __forceinline__ void hn_paint(HnTile* envs, int te_valid, T* tile, in
   }
 }
 
-// Features j .. j+n-1 (n <= 32) of an observation row held as a bit vector
-// (features past the row's end read as 0).
-__device__ __forceinline__ uint32_t hn_row_bits(const uint64_t* w, int j, int n) {
-  const int wi = j >> 6, sh = j & 63;
-  uint64_t x = w[wi] >> sh;
-  if (sh && wi + 1 < HN_OBS_WORDS) x |= w[wi + 1] << (64 - sh);
-  return (uint32_t)x & (n >= 32 ? ~0u : ((1u << n) - 1u));
-}
-
 // Write `nrows` observation rows of G::OBS features, held as bit vectors
-// (row r at rows + r * HN_OBS_WORDS), to consecutive global rows as 0 / 1
-// values, straight from the bits: each thread expands VB bytes of output at a
-// time (16 when the destination allows, else 4) from the features they cover,
-// which may span two rows.
-template <class G, typename OT, int NT>
-__device__ __forceinline__ void hn_write_obs(const uint64_t* rows, int nrows, OT* __restrict__ dst, int tid) {
-  const int total = nrows * G::OBS;
-  auto bits_at = [&](int f0, int ve) -> uint32_t {  // features f0 .. f0+ve-1 of the flat tile
-    const int r = f0 / G::OBS, j = f0 - r * G::OBS;
-    const int n0 = min(ve, G::OBS - j);
-    uint32_t b = hn_row_bits(rows + r * HN_OBS_WORDS, j, n0);
-    if (n0 < ve) b |= hn_row_bits(rows + (r + 1) * HN_OBS_WORDS, 0, ve - n0) << n0;
-    return b;
-  };
+// (row r at rows + r * HN_OBS_WORDS; the bits past G::OBS are 0), to
+// consecutive global rows as 0 / 1 values, straight from the bits, by one
+// wave.  Each lane expands VE features (16 bytes of output) at a time; a
+// vector may run from the end of one row into the next.  All the LDS words a
+// lane needs are read before any of its stores (three independent 32-bit
+// reads per vector, no branches; batches of up to six vectors), so the wave
+// waits on LDS once a batch.  Rows at a destination that is not 16-byte
+// aligned, or a total that is not a whole number of vectors, go one 4-byte
+// word at a time.
+template <class G, typename OT, int MAXROWS>
+__device__ __forceinline__ void hn_write_obs(const uint64_t* rows, int nrows, OT* __restrict__ dst, int lane) {
+  constexpr int VE = 16 / sizeof(OT), WE = 4 / sizeof(OT);  // features per 16-byte vector, per word
   const uint32_t one = sizeof(OT) == 2 ? 0x3f80u : 0x3f800000u;  // 1.0 in OT
   auto word = [&](uint32_t b, int q) -> uint32_t {  // output word q of a vector with feature bits b
     if constexpr (sizeof(OT) == 2)
@@ -99,16 +85,51 @@ __device__ __forceinline__ void hn_write_obs(const uint64_t* rows, int nrows, OT
     else
       return ((b >> q) & 1u) ? one : 0u;
   };
-  constexpr int VE = 16 / sizeof(OT), WE = 4 / sizeof(OT);  // features per 16-byte vector, per word
+  // features f0 .. f0+n-1 (n <= 8) of the flat rows from three 32-bit words:
+  // the row's word holding feature f0 (lo) and the word after it (hi), and
+  // the next row's first word (nx)
+  const uint32_t* rw32 = reinterpret_cast<const uint32_t*>(rows);
+  constexpr int W32 = 2 * HN_OBS_WORDS;  // 32-bit words per row
+  auto load = [&](int f0, uint32_t& lo, uint32_t& hi, uint32_t& nx) {
+    const int r = f0 / G::OBS, j = f0 - r * G::OBS, wi = j >> 5;
+    const uint32_t* w = rw32 + r * W32;
+    lo = w[wi];
+    hi = w[min(wi + 1, W32 - 1)];
+    nx = rw32[min(r + 1, nrows - 1) * W32];
+  };
+  auto bits = [&](int f0, int n, uint32_t lo, uint32_t hi, uint32_t nx) -> uint32_t {
+    const int j = f0 % G::OBS, sh = j & 31, n0 = G::OBS - j;  // n0 features left in the row
+    uint32_t x = lo >> sh;
+    if ((j >> 5) + 1 < W32 && sh) x |= hi << (32 - sh);
+    if (n0 < n) x |= nx << n0;
+    return x & ((1u << n) - 1u);
+  };
+  const int total = nrows * G::OBS;
   if ((reinterpret_cast<uintptr_t>(dst) & 15) == 0 && total % VE == 0) {
+    constexpr int IT = (MAXROWS * G::OBS / VE + 63) / 64, B = IT < 6 ? IT : 6;  // vectors per lane, per batch
+    const int nv = total / VE;
     u32x4* g4 = reinterpret_cast<u32x4*>(dst);
-    for (int v = tid; v < total / VE; v += NT) {
-      const uint32_t b = bits_at(v * VE, VE);
-      g4[v] = u32x4{word(b, 0), word(b, 1), word(b, 2), word(b, 3)};
+#pragma unroll
+    for (int i0 = 0; i0 < IT; i0 += B) {
+      uint32_t lo[B], hi[B], nx[B];
+#pragma unroll
+      for (int it = 0; it < B; ++it) load(min(lane + 64 * (i0 + it), nv - 1) * VE, lo[it], hi[it], nx[it]);
+#pragma unroll
+      for (int it = 0; it < B; ++it) {
+        const int v = lane + 64 * (i0 + it);
+        if (i0 + it < IT && v < nv) {
+          const uint32_t b = bits(v * VE, VE, lo[it], hi[it], nx[it]);
+          g4[v] = u32x4{word(b, 0), word(b, 1), word(b, 2), word(b, 3)};
+        }
+      }
     }
   } else {
     uint32_t* g = reinterpret_cast<uint32_t*>(dst);
-    for (int v = tid; v < total / WE; v += NT) g[v] = word(bits_at(v * WE, WE), 0);
+    for (int v = lane; v < total / WE; v += 64) {
+      uint32_t lo, hi, nx;
+      load(v * WE, lo, hi, nx);
+      g[v] = word(bits(v * WE, WE, lo, hi, nx), 0);
+    }
   }
 }
 
@@ -182,65 +203,127 @@ __global__ __launch_bounds__(NTHREADS) void hn_init_kernel(HnParams p, int32_t* 
 
 // ---------------------------------------------------------- env-only ----
 
-template <class G, typename OT, int TE>
-__global__ __launch_bounds__(NTHREADS) void hn_env_kernel(HnParams p, int32_t* __restrict__ state, uint64_t t0,
-                                                          int n_steps, const int32_t* __restrict__ actions,
-                                                          OT* __restrict__ obs, float* __restrict__ reward,
-                                                          uint8_t* __restrict__ done, uint8_t* __restrict__ legal) {
-  constexpr int NW = NTHREADS / 64;
-  __shared__ HnTile envs[TE];
-  __shared__ uint32_t need[TE + 1];  // per env, then "any" at [TE]
-  __shared__ uint32_t words[TE][HN_DECK_WORDS];
-  // the observation bit vectors of step k, row 2 el + me, in rows[k % 2]; the
-  // other buffer is cleared while these are written out
-  __shared__ __align__(16) uint64_t rows[2][2 * TE * HN_OBS_WORDS];
-  __shared__ int32_t act_lds[ACT_CHUNK * TE * 2];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// Legal masks ([env][agent][NACT] bytes, the mover's row only) of the n
+// published games at `envs`, computed from the snapshots: one 4-byte word
+// per lane (NACT is a multiple of 4, so a word never straddles an agent).
+template <class G>
+__device__ __forceinline__ void hn_write_legal_pub(const HnTile* __restrict__ envs, int n, uint8_t* __restrict__ g,
+                                                   int lane) {
+  static_assert(G::NACT % 4 == 0, "word-wise mask rows");
+  constexpr int WPE = 2 * G::NACT / 4;  // words per env
+  for (int w = lane; w < n * WPE; w += 64) {
+    const int el = w / WPE, b0 = 4 * (w - el * WPE), ag = b0 / G::NACT, a0 = b0 - ag * G::NACT;
+    const HnPub& v = envs[el].pub;
+    const uint32_t m = ag == v.cur ? hn_legal<G>(v) >> a0 : 0u;
+    reinterpret_cast<uint32_t*>(g)[w] = (m & 1u) | ((m & 2u) << 7) | ((m & 4u) << 14) | ((m & 8u) << 21);
+  }
+}
+
+// Env-only steps, the workgroup run as a three-stage pipeline, one barrier
+// per iteration.  In iteration i wave 0, which holds the TE games (one lane
+// each), plays move i and publishes a snapshot of the games; waves 1..OW
+// assemble the observation bit vectors of move i - 1 from the snapshot of the
+// iteration before and write out those of move i - 2 (snapshots and bit
+// vectors are double-buffered), so moves, field computation and stores
+// overlap.  The field computations of a move are spread over the
+// observation waves a pass of 64 (field, row) items at a time, field-major,
+// so one pass takes few distinct fields (a wave runs the branch of every
+// field its lanes hold); each observation wave writes out, then clears, its
+// own rows.  A game that ends is re-dealt by the env wave itself: the whole
+// wave shuffles the new decks one at a time (hn_wave_deck) and the owning
+// lane picks its words up with readlane.  The actions are read straight
+// from global memory one move ahead (the env wave stores only rewards and
+// done flags, so those loads wait on little).
+template <class G, typename OT, int TE, int OW>
+__global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(sizeof(OT) == 2 ? 4 : 3))) void hn_env_kernel(HnParams p, int32_t* __restrict__ state, uint64_t t0,
+                                                                int n_steps, const int32_t* __restrict__ actions,
+                                                                OT* __restrict__ obs, float* __restrict__ reward,
+                                                                uint8_t* __restrict__ done, uint8_t* __restrict__ legal) {
+  static_assert(TE <= 64 && (2 * TE) % OW == 0, "one env wave; whole rows per observation wave");
+  constexpr int RB = 2 * TE, RPW = RB / OW;                      // rows per workgroup, per observation wave
+  constexpr int NPASS = (RB * G::NFIELDS + 63) / 64;            // field passes per move
+  constexpr int LPW = (TE + OW - 1) / OW;                        // envs whose legal masks a wave writes
+  __shared__ HnTile snap[2][TE];
+  __shared__ __align__(16) uint64_t rows[2][RB * HN_OBS_WORDS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, ow = wave - 1;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
-  const bool envlane = tid < te_valid;
-  const int e = e0 + tid;
-  zero_lds<NTHREADS>(envs, sizeof(envs), tid);
-  zero_lds<NTHREADS>(rows, sizeof(rows), tid);  // the bit vectors start clear
+  const bool envlane = wave == 0 && lane < te_valid;
+  const int e = e0 + lane;
   HnEnv s;
-  if (envlane) hn_load(state, E, e, s);
-  for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
-    const int nk = min(ACT_CHUNK, n_steps - k0);
-    // no global loads inside the step loop: a load there would wait for every earlier trajectory store
-    stage_actions<TE * 2, NTHREADS>(actions, E, e0, te_valid * 2, 2, k0, nk, act_lds, tid);
-    __syncthreads();
-    for (int kk = 0; kk < nk; ++kk) {
-      const int k = k0 + kk;
-      const uint64_t t = t0 + (uint64_t)k;
-      uint32_t d = 0;
-      if (envlane) {
-        float r;
-        hn_transition<G>(p, s, act_lds[kk * TE * 2 + tid * 2 + s.cur], r, d);
-        need[tid] = d;
-        if (!d) hn_publish<G>(s, envs[tid]);
-        if (reward) reward[(size_t)k * E + e] = r;
-        if (done) done[(size_t)k * E + e] = (uint8_t)d;
-      }
-      hn_flag_any(need, TE, d, wave, lane);
-      __syncthreads();
-      if (need[TE]) {  // some game of the tile ended: deal new ones drawn at t + 1
-        hn_shuffle_flagged<G, NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
-        __syncthreads();
-        if (d) {
-          hn_deal<G>(s, words[tid]);
-          hn_publish<G>(s, envs[tid]);
-        }
-        __syncthreads();
-      }
-      if (obs) {
-        uint64_t* cur = rows[k & 1];
-        hn_build_bits<G, TE, NTHREADS>(envs, te_valid, tid, cur);
-        __syncthreads();
-        hn_write_obs<G, OT, NTHREADS>(cur, 2 * te_valid, obs + ((size_t)k * E + e0) * 2 * G::OBS, tid);
-        for (int i = tid; i < 2 * TE * HN_OBS_WORDS; i += NTHREADS) rows[(k + 1) & 1][i] = 0;
-      }
-      if (legal) hn_write_legal<G, NTHREADS>(envs, te_valid, legal + ((size_t)k * E + e0) * 2 * G::NACT, tid);
-      __syncthreads();  // the bit vectors and masks are read before the next move rewrites them
+  int act0 = 0, act1 = 0;  // both agents' actions of the move about to be played
+  if (envlane) {
+    hn_load(state, E, e, s);
+    if (n_steps > 0) {
+      act0 = actions[(size_t)e * 2];
+      act1 = actions[(size_t)e * 2 + 1];
     }
+  }
+  zero_lds<64 * (OW + 1)>(rows, sizeof(rows), tid);  // the bit vectors start clear
+  for (int i = 0; i < n_steps + 2; ++i) {
+    if (wave == 0) {
+      if (i < n_steps) {  // move i
+        const uint64_t t = t0 + (uint64_t)i;
+        uint32_t d = 0;
+        if (envlane) {
+          float r;
+          hn_transition<G>(p, s, s.cur ? act1 : act0, r, d);
+          if (reward) reward[(size_t)i * E + e] = r;
+          if (done) done[(size_t)i * E + e] = (uint8_t)d;
+          if (i + 1 < n_steps) {
+            act0 = actions[((size_t)(i + 1) * E + e) * 2];
+            act1 = actions[((size_t)(i + 1) * E + e) * 2 + 1];
+          }
+        }
+        // an ended game restarts with the deal drawn at t + 1
+        uint64_t ended = __builtin_amdgcn_ballot_w64(d != 0);
+        while (ended) {
+          const int el = __builtin_ctzll(ended);
+          ended &= ended - 1;
+          const uint32_t v = hn_wave_deck<G>(p.seed, (uint64_t)(p.env_base + e0 + el), t + 1, lane);
+#pragma unroll
+          for (int w = 0; w < HN_DECK_WORDS; ++w) {
+            const uint32_t x = (uint32_t)__builtin_amdgcn_readlane((int)v, 4 * w);
+            s.deck[w] = lane == el ? x : s.deck[w];
+          }
+        }
+        if (d) hn_deal_deck<G>(s);
+        if (envlane) hn_pub(s, snap[i & 1][lane].pub);
+      }
+    } else {
+      if (i >= 1 && i <= n_steps) {  // the fields of move i - 1
+        const int k = i - 1;
+        const HnTile* sn = snap[k & 1];
+        if (obs) {
+          uint64_t* rw = rows[k & 1];
+          for (int q = ow; q < NPASS; q += OW) {
+            const int j = q * 64 + lane, f = j / RB, r = j - f * RB;
+            if (f >= G::NFIELDS || (r >> 1) >= te_valid) continue;
+            int off;
+            const uint64_t v = hn_field_bits<G>(sn[r >> 1].pub, r & 1, f, off);
+            if (v) {
+              unsigned long long* w = reinterpret_cast<unsigned long long*>(rw + r * HN_OBS_WORDS);
+              const int wi = off >> 6, sh = off & 63;
+              atomicOr(w + wi, (unsigned long long)(v << sh));
+              if (sh && (v >> (64 - sh))) atomicOr(w + wi + 1, (unsigned long long)(v >> (64 - sh)));
+            }
+          }
+        }
+        if (legal) {
+          const int l0 = ow * LPW, nl = max(0, min(LPW, te_valid - l0));
+          if (nl > 0) hn_write_legal_pub<G>(sn + l0, nl, legal + ((size_t)k * E + e0 + l0) * 2 * G::NACT, lane);
+        }
+      }
+      if (obs && i >= 2) {  // write out and clear this wave's rows of move i - 2
+        const int k = i - 2, r0 = ow * RPW, nr = max(0, min(RPW, 2 * te_valid - r0));
+        uint64_t* rw = rows[k & 1] + r0 * HN_OBS_WORDS;
+        if (nr > 0) {
+          hn_write_obs<G, OT, RPW>(rw, nr, obs + (((size_t)k * E + e0) * 2 + r0) * G::OBS, lane);
+          wave_lds_sync();
+          for (int j = lane; j < nr * HN_OBS_WORDS; j += 64) rw[j] = 0;
+        }
+      }
+    }
+    __syncthreads();  // snapshot i and the fields of move i - 1 are in; the rows of move i - 2 are out
   }
   if (envlane) hn_store(state, E, e, s);
 }
@@ -415,15 +498,19 @@ static hipError_t launch_hn_init_g(const HnParams& p, int32_t* state, void* obs,
   return hipGetLastError();
 }
 
+constexpr int HN_STEP_TE = 4;  // envs per workgroup of the env-only kernel
+constexpr int HN_STEP_OW = 2;  // its observation waves
+
 template <class G>
 static hipError_t launch_hn_step_g(const HnParams& p, int32_t* state, uint64_t t0, int n_steps,
                                    const int32_t* actions, void* obs, int obs_dt, float* reward, uint8_t* done,
                                    uint8_t* legal, hipStream_t s) {
+  constexpr int TE = HN_STEP_TE, OW = HN_STEP_OW;
   if (obs_dt == DT_F32)
-    hn_env_kernel<G, float, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(
+    hn_env_kernel<G, float, TE, OW><<<hn_tiles(p.E, TE), 64 * (OW + 1), 0, s>>>(
         p, state, t0, n_steps, actions, static_cast<float*>(obs), reward, done, legal);
   else
-    hn_env_kernel<G, uint16_t, HN_ENV_TE><<<hn_tiles(p.E, HN_ENV_TE), NTHREADS, 0, s>>>(
+    hn_env_kernel<G, uint16_t, TE, OW><<<hn_tiles(p.E, TE), 64 * (OW + 1), 0, s>>>(
         p, state, t0, n_steps, actions, static_cast<uint16_t*>(obs), reward, done, legal);
   return hipGetLastError();
 }

@@ -135,6 +135,34 @@ def test_env_only_last_round_and_resume():
     assert (g["done"].numpy() == 1).sum() >= 40  # nearly every game reached its end
 
 
+def test_env_only_4096_sampled_envs():
+    """Env-only steps at the full 4096-env, 80-step size in one launch (bf16 observations); sampled envs,
+    across workgroup tiles, replayed in the oracle."""
+    require_gpu()
+    w = workloads.WORKLOADS["hn_4096"]
+    cfg = R.hanabi_config(w["n_envs"], seed=5, **w["env"])
+    E, T = cfg.n_envs, 80
+    _note(f"hanabi env-only E={E} T={T} bf16 (sampled)")
+    sample = [0, 1, 2, 3, 4, 5, 7, 8, 1023, 1024, 2050, 3071, 4092, 4095]
+    state = R.new_state(cfg)
+    R.rollout_init(cfg, state)
+    actions = _actions(T, E, seed=17)
+    out = dict(obs_out=torch.empty(T, E, 2, D, dtype=torch.bfloat16, device="cuda"),
+               reward=torch.empty(T, E, device="cuda"),
+               done=torch.empty(T, E, dtype=torch.uint8, device="cuda"),
+               legal_out=torch.empty(T, E, 2, NA, dtype=torch.uint8, device="cuda"))
+    R.rollout_step(cfg, state, 0, torch.as_tensor(actions).cuda(), **out)
+    torch.cuda.synchronize()
+    g = {k: v[:, sample].cpu() for k, v in out.items()}
+    ref = rollout.env_only(hn, hn_oracle_cfg(cfg), cfg.seed, sample, 0, actions[:, sample])
+    assert np.array_equal(g["reward"].numpy().view(np.uint32), ref["reward"].view(np.uint32))
+    assert np.array_equal(g["done"].numpy(), ref["done"])
+    assert np.array_equal(g["legal_out"].numpy().astype(bool), ref["mask"])
+    assert np.array_equal(_obs_np(g["obs_out"]), ref["obs"])
+    final = hn_states_from_device(cfg, state)
+    assert [final[e] for e in sample] == ref["states"]
+
+
 # ------------------------------------------------------------- full rollout
 
 def _run_gpu(cfg, pol, T, t0=0, state=None):
