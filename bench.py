@@ -39,25 +39,35 @@ def parse():
     ap.add_argument("--cpu-leg", nargs=5, default=None, metavar=("WORKLOAD", "ENV0", "N_ENVS", "DTYPE", "CORE"),
                     help="(internal) run one timed oracle leg in this process and print its result")
     ap.add_argument("--cpu-only", action="store_true", help="only the CPU baseline (no GPU work)")
-    ap.add_argument("--only", choices=["run_bf16", "run_f32", "env_bf16", "policy_bf16", "copy"], default=None,
+    ap.add_argument("--only", choices=["run_bf16", "run_f32", "env_bf16", "env_f32", "policy_bf16", "policy_f32",
+                                       "copy"], default=None,
                     help="time one kernel only (for profiler runs); 'copy' runs a plain 512 MiB device copy, "
                          "the reference for scaling HBM byte counters")
     ap.add_argument("--workload-only", default=None,
                     help="time one secondary workload only (lbf12_16k, oc_4096, hn_4096; for profiler runs)")
     ap.add_argument("--no-workloads", action="store_true", help="skip the secondary workloads")
+    ap.add_argument("--counter-plan", action="store_true",
+                    help="print the rocprofv3 counter passes (one command per line) and exit")
+    ap.add_argument("--phases", action="store_true",
+                    help="per-phase cycles of the fused and env-only kernels' step loops from the phase-stamped "
+                         "library (python -m paper_2609_13716_amd.build --stamps); writes "
+                         "profiles/phase_stamps.md")
+    ap.add_argument("--phases-child", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--summarize-counters", metavar="DIR", default=None,
+                    help="read the counter CSVs of the passes under DIR and write profiles/traffic.json and "
+                         "profiles/counters_all_workloads.md (no GPU needed)")
     return ap.parse_args()
 
 
-# The translation unit of the fused LBF rollout kernels (the file and every header it includes):
-# HBM traffic counters taken on those kernels stay valid while these files are unchanged.
-LBF_KERNEL_SOURCES = ("rl_lbf.hip", "rl_lbf.h", "rl_internal.h", "rl_mlp.h", "rl_regmlp.h", "rl_sample.h",
-                      "rl_philox.h", "rl_hanabi.h", "rl_overcooked.h")
-
-
-def csrc_hash(files=LBF_KERNEL_SOURCES):
+def csrc_hash():
+    """Hash of every kernel source and of the workload definitions: hardware counters taken on the
+    benchmark's kernels stay valid while these files are unchanged."""
     h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2609_13716_amd", "csrc", "*")))
+    files.append(os.path.join(ROOT, "paper_2609_13716_amd", "workloads.py"))
     for f in files:
-        h.update(open(os.path.join(ROOT, "paper_2609_13716_amd", "csrc", f), "rb").read())
+        h.update(os.path.basename(f).encode())
+        h.update(open(f, "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -85,8 +95,9 @@ def roofline(bound, achieved, peak, unit, traffic=None):
             "frac": round(achieved / peak, 4), "traffic": traffic}
 
 
-def load_traffic(kernel_key):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it matches this source."""
+def load_traffic(key):
+    """HBM bytes per launch of one benchmark leg's kernels ("leg:role") from the committed rocprofv3 counter
+    summary, if that summary was taken on these kernel sources."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -96,8 +107,20 @@ def load_traffic(kernel_key):
         return None
     if rec.get("csrc_hash") != csrc_hash():
         return None
-    k = rec.get("kernels", {}).get(kernel_key)
+    k = rec.get("legs", {}).get(key)
     return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+def run_bytes(E, T, A, D, es, state_bytes, per_agent_extra=0):
+    """Algorithmic HBM bytes of one rollout_run launch: the trajectory (observations, actions, reward,
+    done, plus per_agent_extra bytes per agent-step) and the state read and written once."""
+    return E * T * (A * D * es + A * 4 + 4 + 1 + A * per_agent_extra) + 2 * state_bytes
+
+
+def env_bytes(E, T, A, D, es, state_bytes):
+    """Algorithmic HBM bytes of one env-only rollout_step launch: actions read, observations, reward and
+    done written, the state read and written once."""
+    return E * T * (A * 4 + A * D * es + 4 + 1) + 2 * state_bytes
 
 
 def env_config(R, workloads, name, n_envs=None, seed=0):
@@ -147,14 +170,16 @@ def measure_workload(R, workloads, name, dt, steps, warmup):
         t_next[0] += T
 
     kern_ms, wall_ms = timed(run, steps, warmup)
-    nbytes = E * T * (A * D * es + A * 4 + 4 + 1) + 2 * state_bytes
+    nbytes = run_bytes(E, T, A, D, es, state_bytes)
     flops = E * T * acting * flop_per_row
+    traffic = load_traffic(f"{name}:run")
     out = {"workload": name, "dtype": dt, "n_envs": E, "steps_per_rollout": T, "policy": "-".join(map(str, dims)),
            "value": round(E * T * acting / (wall_ms * 1e-3), 1), "unit": "agent-env steps/s",
            "env_steps_per_s": round(E * T / (wall_ms * 1e-3), 1), "ms_per_step": round(wall_ms, 4),
            "kernel_ms": round(kern_ms, 4),
-           "roofline_hbm": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"),
-           "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s")}
+           "roofline_hbm": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s", traffic),
+           "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s",
+                                     traffic)}
     # env-only stepping with injected uniform actions (illegal ones fall back to the lowest legal action)
     g = torch.Generator(device="cuda")
     g.manual_seed(7)
@@ -167,9 +192,10 @@ def measure_workload(R, workloads, name, dt, steps, warmup):
         t_next[0] += T
 
     kern_ms, wall_ms = timed(env, steps, warmup)
-    nbytes = E * T * (A * 4 + A * D * es + 4 + 1) + 2 * state_bytes
+    nbytes = env_bytes(E, T, A, D, es, state_bytes)
     out["env_only"] = {"env_steps_per_s": round(E * T / (wall_ms * 1e-3), 1), "kernel_ms": round(kern_ms, 4),
-                       "roofline": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s")}
+                       "roofline": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s",
+                                            load_traffic(f"{name}:env"))}
     del obs
     # standalone policy forward over a batch of this workload's observations
     rows = min(E * A * T, 1 << 18)
@@ -179,7 +205,7 @@ def measure_workload(R, workloads, name, dt, steps, warmup):
     kern_ms, _ = timed(lambda: R.policy_forward(pol, x, logits=lg), steps, warmup)
     out["policy_forward"] = {"rows": rows, "kernel_ms": round(kern_ms, 4),
                              "roofline": roofline("mfma", rows * flop_per_row / (kern_ms * 1e-3) / 1e12,
-                                                  MFMA_PEAK_TFLOPS[dt], "TFLOP/s")}
+                                                  MFMA_PEAK_TFLOPS[dt], "TFLOP/s", load_traffic(f"{name}:policy"))}
     del x, lg
     torch.cuda.empty_cache()
     return out
@@ -211,16 +237,18 @@ def measure_population(R, workloads, name, dt, steps, warmup):
         t_next[0] += T
 
     kern_ms, wall_ms = timed(run, steps, warmup)
-    nbytes = E * T * (A * D * es + A * 4 + 4 + 1) + 2 * R.rl_state_bytes(cfg)
+    nbytes = run_bytes(E, T, A, D, es, R.rl_state_bytes(cfg))
     flops = E * T * A * flop_per_row
+    traffic = load_traffic(f"{name}:run")
     n_teammates = w["population"] - 1
     return {"workload": name, "dtype": dt, "n_envs": E, "steps_per_rollout": T, "policy": "-".join(map(str, dims)),
             "population": w["population"], "assignment": f"agent 0: ego; agent 1: one of {n_teammates} teammates "
                                                           f"per block of {E // n_teammates} envs",
             "value": round(E * T * A / (wall_ms * 1e-3), 1), "unit": "agent-env steps/s",
             "ms_per_step": round(wall_ms, 4), "kernel_ms": round(kern_ms, 4),
-            "roofline_hbm": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"),
-            "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s")}
+            "roofline_hbm": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s", traffic),
+            "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s",
+                                      traffic)}
 
 
 def measure_actor_critic(R, workloads, name, dt, steps, warmup):
@@ -251,17 +279,26 @@ def measure_actor_critic(R, workloads, name, dt, steps, warmup):
         t_next[0] += T
 
     kern_ms, wall_ms = timed(run, steps, warmup)
-    nbytes = E * T * (A * D * es + A * 4 + 4 + 1 + A * 8) + E * A * 4 + 2 * R.rl_state_bytes(cfg)
+    nbytes = run_bytes(E, T, A, D, es, R.rl_state_bytes(cfg), per_agent_extra=8) + E * A * 4
     flops = E * T * A * flop_per_row
+    traffic = load_traffic(f"{name}:run")
     gae_ms, _ = timed(lambda: R.gae(rew, done, value, vlast, w["gamma"], w["lam"], adv=adv, ret=ret), steps, warmup)
-    gae_bytes = T * E * (4 + 1) + T * E * A * (4 + 8) + E * A * 4
+    gae_bytes = gae_alg_bytes(E, T, A)
     return {"workload": name, "dtype": dt, "n_envs": E, "steps_per_rollout": T, "policy": "-".join(map(str, dims)),
             "value": round(E * T * A / (wall_ms * 1e-3), 1), "unit": "agent-env steps/s",
             "ms_per_step": round(wall_ms, 4), "kernel_ms": round(kern_ms, 4),
-            "roofline_hbm": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"),
-            "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s"),
+            "roofline_hbm": roofline("hbm", nbytes / (kern_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s", traffic),
+            "roofline_mfma": roofline("mfma", flops / (kern_ms * 1e-3) / 1e12, MFMA_PEAK_TFLOPS[dt], "TFLOP/s",
+                                      traffic),
             "gae": {"kernel_ms": round(gae_ms, 4),
-                    "roofline": roofline("hbm", gae_bytes / (gae_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s")}}
+                    "roofline": roofline("hbm", gae_bytes / (gae_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s",
+                                         load_traffic(f"{name}:gae"))}}
+
+
+def gae_alg_bytes(E, T, A):
+    """Algorithmic HBM bytes of one GAE launch: reward and done read, values read, advantages and returns
+    written, the bootstrap values read."""
+    return T * E * (4 + 1) + T * E * A * (4 + 8) + E * A * 4
 
 
 def measure_s5(R, workloads, name, dt, steps, warmup):
@@ -297,9 +334,294 @@ def measure_s5(R, workloads, name, dt, steps, warmup):
             "policy": f"S5 D{D}-H{H}-P{P}, heads 3x{F}", "value": round(E * T * A / (wall_ms * 1e-3), 1),
             "unit": "agent-env steps/s", "ms_per_step": round(wall_ms, 4), "kernel_ms": round(kern_ms, 4),
             "roofline_mfma": roofline("mfma", 2 * macs_per_row * rows / (kern_ms * 1e-3) / 1e12,
-                                      MFMA_PEAK_TFLOPS[dt], "TFLOP/s"),
+                                      MFMA_PEAK_TFLOPS[dt], "TFLOP/s", load_traffic(f"{name}:run")),
             "note": "MFMA rate over the whole rollout (every kernel of every step); per-kernel times in the "
                     "rocprofv3 summary of this workload"}
+
+
+# ---------------------------------------------------------------- hardware counters
+# Each counter pass is its own rocprofv3 process over one benchmark leg (bench.py with the leg's arguments,
+# two timed launches after one warm-up, so every kernel of the leg is dispatched COUNTER_CALLS times); one
+# pass asks for no more counters of a hardware block than one run can collect.
+COUNTER_PASSES = {
+    "fetch": ("FETCH_SIZE",),
+    "write": ("WRITE_SIZE",),
+    "mfma": ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16",
+             "SQ_INSTS_VALU_MFMA_MOPS_F32", "GRBM_GUI_ACTIVE"),
+    "l1": ("TCP_TCC_READ_REQ_sum", "TCP_TCC_WRITE_REQ_sum", "TCP_TOTAL_CACHE_ACCESSES_sum", "GRBM_GUI_ACTIVE"),
+}
+COUNTER_CALLS = 3
+_SECONDARY = ("lbf12_16k", "oc_4096", "hn_4096", "hn_mini_4096", "lbf7_const_4096", "lbf7_teams_4096",
+              "lbf8_4096_ac", "lbf8_4096_pop", "lbf8_4096_s5")
+COUNTER_LEGS = (
+    ("lbf8_4096_run_bf16", "--only run_bf16", ("fetch", "write", "mfma", "l1")),
+    ("lbf8_4096_env_bf16", "--only env_bf16", ("fetch", "write")),
+    ("lbf8_4096_policy_bf16", "--only policy_bf16", ("fetch", "write", "mfma")),
+    ("lbf8_4096_run_f32", "--only run_f32", ("fetch", "write", "mfma")),
+    ("lbf8_4096_env_f32", "--only env_f32", ("fetch", "write")),
+    ("lbf8_4096_policy_f32", "--only policy_f32", ("fetch", "write", "mfma")),
+) + tuple((n, f"--workload-only {n}", ("fetch", "write", "mfma") + (("l1",) if n in ("hn_4096", "oc_4096") else ()))
+          for n in _SECONDARY) + (("copy", "--only copy", ("fetch", "write")),)
+
+
+def counter_commands(out_dir="gpurun_out/pmc"):
+    """(pass, leg, command) of every counter pass, each to be run alone from the repository root."""
+    cmds = []
+    for leg, args, passes in COUNTER_LEGS:
+        for ps in passes:
+            steps = "" if leg == "copy" else " --steps 2 --warmup 1 --no-cpu-baseline"
+            cmds.append((ps, leg, f"rocprofv3 --pmc {' '.join(COUNTER_PASSES[ps])} -d {out_dir}/{ps}/{leg} -o run "
+                                  f"--output-format csv -- python3 bench.py {args}{steps}"))
+    return cmds
+
+
+def kernel_role(name):
+    """Which benchmarked call a kernel belongs to: 'run', 'env', 'policy', 'gae', 'copy' or None (init
+    kernels and the input generators)."""
+    if "policy_fwd" in name or "policy_forward" in name:
+        return "policy"
+    if "_env_kernel" in name:
+        return "env"
+    if "gae" in name:
+        return "gae"
+    if any(k in name for k in ("lbf_rollout_kernel", "_run_kernel", "_run_pop_kernel", "_pop2_kernel", "s5_")):
+        return "run"
+    if "copyBuffer" in name:
+        return "copy"
+    return None
+
+
+def _read_counter_csv(d):
+    """{dispatch id: (kernel name, {counter: value})} from the counter CSV under directory d."""
+    import csv
+    paths = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    out = {}
+    for path in paths:
+        for r in csv.DictReader(open(path)):
+            rec = out.setdefault((path, r["Dispatch_Id"]), (r["Kernel_Name"], {}))
+            rec[1][r["Counter_Name"]] = rec[1].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return out
+
+
+def _algorithmic(R, workloads, leg, role):
+    """(algorithmic bytes, algorithmic flop) of one launch of a leg's call, by the formulas of the timed legs
+    (None where the leg has no such figure)."""
+    name = "lbf8_4096" if leg.startswith("lbf8_4096_") and leg.split("_")[2] in ("run", "env", "policy") else leg
+    dt = leg.rsplit("_", 1)[1] if name != leg else "bf16"
+    if name not in workloads.WORKLOADS:
+        return None, None
+    w = workloads.WORKLOADS[name]
+    cfg = env_config(R, workloads, name)
+    E, T, A = cfg.n_envs, w["n_steps"], cfg.n_agents
+    D, nA = R.rl_obs_dim(cfg), R.rl_num_actions(cfg)
+    es = 2 if dt == "bf16" else 4
+    sb = R.rl_state_bytes(cfg)
+    if "s5" in w:
+        return None, None
+    dims = workloads.policy_dims(name)
+    fpr = 2 * sum(dims[i] * dims[i + 1] for i in range(3))
+    acting = 1 if workloads.kind(name) == "hanabi" else A
+    if role == "run":
+        b = run_bytes(E, T, A, D, es, sb, per_agent_extra=8 if w.get("value_head") else 0)
+        b += E * A * D * es if name != leg else (E * A * 4 if w.get("value_head") else 0)
+        return b, E * T * acting * fpr
+    if role == "env":
+        return env_bytes(E, T, A, D, es, sb), None
+    if role == "policy":
+        rows = E * A * T if name != leg else min(E * A * T, 1 << 18)
+        return rows * (D * es + nA * 4), rows * fpr
+    if role == "gae":
+        return gae_alg_bytes(E, T, A), None
+    return None, None
+
+
+def summarize_counters(src):
+    """Write profiles/traffic.json (HBM bytes per launch of every leg's calls, FETCH_SIZE and WRITE_SIZE
+    scaled by what each reads on a plain 512 MiB device copy) and profiles/counters_all_workloads.md."""
+    import statistics
+
+    from paper_2609_13716_amd import rollout as R
+    from paper_2609_13716_amd import workloads
+    n_copy = 512 << 20
+    scale = {}
+    for ps, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        d = _read_counter_csv(os.path.join(src, ps, "copy"))
+        vals = [c[ctr] for k, c in d.values() if kernel_role(k) == "copy" and c[ctr] > 1024]  # the 512 MiB copies
+        scale[ctr] = n_copy / (statistics.mean(vals) * 1024)
+    legs, rows = {}, []
+    for leg, _, passes in COUNTER_LEGS:
+        if leg == "copy":
+            continue
+        per_role = {}
+        for ps in passes:
+            for k, c in _read_counter_csv(os.path.join(src, ps, leg)).values():
+                role = kernel_role(k)
+                if role is None or role == "copy":  # (device copies outside the copy leg are set-up)
+                    continue
+                rr = per_role.setdefault(role, {"kernels": set(), "sum": {}})
+                rr["kernels"].add(k.split("(")[0].replace("void ", "").replace("rl::", ""))
+                for ctr, v in c.items():
+                    rr["sum"][ctr] = rr["sum"].get(ctr, 0.0) + v
+        for role, rr in sorted(per_role.items()):
+            sm = {k: v / COUNTER_CALLS for k, v in rr["sum"].items()}
+            rec = {"kernels": sorted(rr["kernels"])}
+            if "FETCH_SIZE" in sm and "WRITE_SIZE" in sm:
+                rb = sm["FETCH_SIZE"] * 1024 * scale["FETCH_SIZE"]
+                wb = sm["WRITE_SIZE"] * 1024 * scale["WRITE_SIZE"]
+                rec.update(read_bytes=round(rb), write_bytes=round(wb), hbm_bytes_per_launch=round(rb + wb))
+            alg_b, alg_f = _algorithmic(R, workloads, leg, role)
+            if alg_b:
+                rec["algorithmic_bytes_per_launch"] = alg_b
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in sm and sm.get("GRBM_GUI_ACTIVE"):
+                simd_cycles = 256 * 4 * sm["GRBM_GUI_ACTIVE"] / 8  # GRBM_GUI_ACTIVE is summed over the 8 XCDs
+                rec["mfma_busy_frac"] = round(sm["SQ_VALU_MFMA_BUSY_CYCLES"] / simd_cycles, 4)
+                mops = sm.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) + sm.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0)
+                rec["mfma_flop_per_launch"] = round(512 * mops)
+                if alg_f:
+                    rec["algorithmic_flop_per_launch"] = alg_f
+            if "TCP_TCC_READ_REQ_sum" in sm:
+                rec["l2_to_l1_read_req_per_launch"] = round(sm["TCP_TCC_READ_REQ_sum"])
+                rec["l1_to_l2_write_req_per_launch"] = round(sm.get("TCP_TCC_WRITE_REQ_sum", 0.0))
+                rec["l1_tag_accesses_per_launch"] = round(sm.get("TCP_TOTAL_CACHE_ACCESSES_sum", 0.0))
+            legs[f"{leg}:{role}"] = rec
+            rows.append((leg, role, rec))
+    cmds = counter_commands()
+    out = {"csrc_hash": csrc_hash(),
+           "note": "per launch of each benchmark leg's call: HBM bytes from rocprofv3 FETCH_SIZE / WRITE_SIZE "
+                   "(KiB per dispatch, summed over the call's kernels) scaled by the factor that maps the same "
+                   "counter on a plain 512 MiB device copy to 512 MiB; MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / "
+                   "(1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs); MFMA flop = 512 x SQ_INSTS_VALU_MFMA_MOPS",
+           "scale": {k: round(v, 5) for k, v in scale.items()},
+           "commands": [c for _, _, c in cmds], "legs": legs}
+    json.dump(out, open(os.path.join(ROOT, "profiles", "traffic.json"), "w"), indent=1)
+    md = ["# Hardware counters of every benchmarked kernel, one MI355X", "",
+          "Each pass is its own process, run from the repository root after `cd /tmp && export TMPDIR=/tmp`; "
+          "this summary is written by `python3 bench.py --summarize-counters gpurun_out/pmc` from their CSVs.", "",
+          "```"] + [c for _, _, c in cmds] + ["```", "",
+          f"Copy calibration (512 MiB device copy): FETCH_SIZE x {scale['FETCH_SIZE']:.4f}, "
+          f"WRITE_SIZE x {scale['WRITE_SIZE']:.4f} (KiB to bytes).", "",
+          "Per launch of the leg's call (its kernels summed; the policy leg of a workload is its standalone "
+          "policy_forward over the first 2^18 rows).  MFMA busy: fraction of SIMD-cycles with the matrix "
+          "unit busy; MFMA Gflop: 512 x SQ_INSTS_VALU_MFMA_MOPS (padding included) against the algorithmic "
+          "flop.", "",
+          "| leg | call | kernels | HBM MB (read + write) | algorithmic MB | ratio | MFMA busy | MFMA Gflop (alg.) "
+          "| L2->L1 read req (M) |", "|---|---|---|---|---|---|---|---|---|"]
+    for leg, role, r in rows:
+        hb = r.get("hbm_bytes_per_launch")
+        ab = r.get("algorithmic_bytes_per_launch")
+        hbm = f"{hb / 1e6:,.1f} ({r['read_bytes'] / 1e6:,.1f} + {r['write_bytes'] / 1e6:,.1f})" if hb else "-"
+        ratio = f"{hb / ab:.3f}" if hb and ab else "-"
+        mf = f"{100 * r['mfma_busy_frac']:.1f}%" if "mfma_busy_frac" in r else "-"
+        fl = (f"{r['mfma_flop_per_launch'] / 1e9:,.1f} ({r['algorithmic_flop_per_launch'] / 1e9:,.1f})"
+              if "algorithmic_flop_per_launch" in r else
+              f"{r['mfma_flop_per_launch'] / 1e9:,.1f}" if "mfma_flop_per_launch" in r else "-")
+        l1 = f"{r['l2_to_l1_read_req_per_launch'] / 1e6:,.2f}" if "l2_to_l1_read_req_per_launch" in r else "-"
+        ks = "<br>".join(f"`{k}`" for k in r["kernels"][:3]) + (" ..." if len(r["kernels"]) > 3 else "")
+        md.append(f"| {leg} | {role} | {ks} | {hbm} | {ab / 1e6 if ab else 0:,.1f} | {ratio} | {mf} | {fl} | {l1} |")
+    open(os.path.join(ROOT, "profiles", "counters_all_workloads.md"), "w").write("\n".join(md) + "\n")
+    return out
+
+
+# ---------------------------------------------------------------- phase stamps
+# (case, workload, call, stamp unit, iterations per launch beyond n_steps, role names, phase names)
+PHASE_CASES = (
+    ("headline fused rollout", "lbf8_4096", "run", "lbf", 0, ("env wave", "other waves"),
+     {0: "barrier at the step's top", 1: "action Philox draws (one step in 8)", 2: "layer 1 + barrier",
+      3: "layer 2 + barrier", 4: "layer 3 + Gumbel argmax", 5: "transition", 6: "resets",
+      7: "paint o_t+1, reward/done stores", 8: "copy o_t to the trajectory", 9: "Gumbel noise of step t+1"}),
+    ("12x12 fused rollout", "lbf12_16k", "run", "lbf", 0, ("env wave", "other waves"), None),
+    ("Hanabi env-only", "hn_4096", "env", "hn", 2, ("env wave", "observation waves"),
+     {0: "move (transition, reward/done)", 1: "re-deals (wave shuffles)", 2: "publish snapshot",
+      4: "field passes (bit vectors)", 5: "legal masks", 6: "write out + clear rows", 7: "barrier wait"}),
+    ("Hanabi fused rollout", "hn_4096", "run", "hn", 0, ("all waves",),
+     {0: "barrier at the step's top", 1: "observation bit vectors", 2: "paint layer-1 tile", 3: "layer 1",
+      4: "layer 2", 5: "layer 3", 6: "legal mask + Gumbel scores", 7: "copy o_t to the trajectory",
+      8: "argmax + transition", 9: "re-deals"}),
+)
+
+
+def phases_child():
+    """(run with RL_LIB_PATH = the stamped library) one launch per case; prints the stamp tables as JSON."""
+    import ctypes
+
+    import torch
+
+    from paper_2609_13716_amd import rollout as R
+    from paper_2609_13716_amd import workloads
+    out = []
+    for case, name, call, unit, extra, _, _ in PHASE_CASES:
+        w = workloads.WORKLOADS[name]
+        cfg = env_config(R, workloads, name)
+        E, T, A = cfg.n_envs, w["n_steps"], cfg.n_agents
+        D, nA = R.rl_obs_dim(cfg), R.rl_num_actions(cfg)
+        pol = R.Policy(*workloads.policy_weights(workloads.policy_dims(name), seed=1000), "bf16")
+        state = R.new_state(cfg)
+        R.rollout_init(cfg, state)
+        obs = torch.empty(T, E, A, D, dtype=torch.bfloat16, device="cuda")
+        rew, done = torch.empty(T, E, device="cuda"), torch.empty(T, E, dtype=torch.uint8, device="cuda")
+        g = torch.Generator(device="cuda")
+        g.manual_seed(7)
+        inj = torch.randint(0, nA, (T, E, A), dtype=torch.int32, device="cuda", generator=g)
+        reader = getattr(R.lib, f"rl_phase_stamps_{unit}")
+        table = (ctypes.c_ulonglong * (8 * 12))()
+
+        def launch(t0):
+            if call == "run":
+                R.rollout_run(cfg, pol, state, t0, T, obs=obs, reward=rew, done=done)
+            else:
+                R.rollout_step(cfg, state, t0, inj, obs, rew, done)
+        launch(0)
+        torch.cuda.synchronize()
+        reader(table, 1)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        launch(T)
+        b.record()
+        torch.cuda.synchronize()
+        reader(table, 1)
+        out.append({"case": case, "iterations": T + extra, "ms": a.elapsed_time(b), "table": list(table)})
+        del obs
+        torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
+
+
+def phases():
+    """Run phases_child on the stamped library and write profiles/phase_stamps.md."""
+    import subprocess
+    from paper_2609_13716_amd import build
+    if not os.path.exists(build.LIB_STAMPS):
+        raise SystemExit(f"{build.LIB_STAMPS} is not built; run `python -m paper_2609_13716_amd.build --stamps`")
+    r = subprocess.run([sys.executable, os.path.abspath(__file__), "--phases-child"], capture_output=True,
+                       text=True, env=dict(os.environ, RL_LIB_PATH=build.LIB_STAMPS), cwd=ROOT)
+    if r.returncode != 0:
+        raise SystemExit(f"stamped run failed ({r.returncode}):\n{r.stderr[-2000:]}")
+    res = json.loads(r.stdout.strip().splitlines()[-1])
+    md = ["# Phase stamps of the fused and env-only step loops, one MI355X", "",
+          "Commands (repository root): `python -m paper_2609_13716_amd.build --stamps` (on the build host), then "
+          "`python3 bench.py --phases` on the GPU.  The stamped library marks phase boundaries in the kernels' "
+          "step loops with s_memtime; each wave sums the cycles between its marks, and the table below gives "
+          "shader-clock cycles per step (per loop iteration) per wave of each role, averaged over the grid.  "
+          "The stamps add waits of their own (each mark waits for the wave's outstanding LDS operations), so "
+          "the launch takes longer than in the product build: read the split, not the total.", ""]
+    for (case, name, call, unit, extra, roles, names), rr in zip(PHASE_CASES, res):
+        names = names or PHASE_CASES[0][6]
+        tab = rr["table"]
+        md += [f"## {case} ({name}, {call}; stamped launch {rr['ms']:.3f} ms, {rr['iterations']} iterations)", "",
+               "| phase | " + " | ".join(roles) + " |", "|---|" + "---|" * len(roles)]
+        counts = [tab[ro * 12 + 11] for ro in range(len(roles))]
+        # roles beyond the named ones (the other waves of a workgroup) are pooled into the last name
+        pooled = []
+        for ro in range(len(roles)):
+            rows = range(ro, 8) if ro == len(roles) - 1 else [ro]
+            n = sum(tab[x * 12 + 11] for x in rows)
+            pooled.append([sum(tab[x * 12 + ph] for x in rows) / max(n, 1) / rr["iterations"] for ph in range(11)])
+        for ph in range(11):
+            if any(pr[ph] > 0.5 for pr in pooled):
+                md.append(f"| {names.get(ph, ph)} | " + " | ".join(f"{pr[ph]:,.0f}" for pr in pooled) + " |")
+        md.append("| total | " + " | ".join(f"{sum(pr):,.0f}" for pr in pooled) + " |")
+        md.append("")
+    open(os.path.join(ROOT, "profiles", "phase_stamps.md"), "w").write("\n".join(md))
+    print("\n".join(md))
 
 
 # The oracle's timed samples (the CPU baseline): the correctness workload in full, a prefix of each
@@ -405,6 +727,19 @@ def main():
     if args.cpu_only:
         print(json.dumps({"cpu_baseline": cpu_baseline()}), flush=True)
         return
+    if args.phases_child:
+        phases_child()
+        return
+    if args.phases:
+        phases()
+        return
+    if args.counter_plan:
+        for ps, leg, cmd in counter_commands():
+            print(f"{ps} {leg}\t{cmd}")
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the rollout shards over GPUs "
               "by env id with no exchange, and this build times the single-GPU shard.", file=sys.stderr)
@@ -445,7 +780,7 @@ def main():
 
         kern_ms, wall_ms = timed(step, args.steps, args.warmup)
         # algorithmic bytes: trajectory outputs + final obs + state read and written once
-        nbytes = E * T * (A * D * es + A * 4 + 4 + 1) + E * A * D * es + 2 * E * planes * 4
+        nbytes = run_bytes(E, T, A, D, es, E * planes * 4) + E * A * D * es
         flops = E * A * T * flop_per_row
         agent_steps = E * A * T
         return dict(kern_ms=kern_ms, wall_ms=wall_ms, bytes=nbytes, flops=flops,
@@ -470,7 +805,7 @@ def main():
             t_next[0] += T
 
         kern_ms, wall_ms = timed(step, args.steps, args.warmup)
-        nbytes = E * T * (A * 4 + A * D * es + 4 + 1) + 2 * E * planes * 4
+        nbytes = env_bytes(E, T, A, D, es, E * planes * 4)
         return dict(kern_ms=kern_ms, wall_ms=wall_ms, bytes=nbytes, gbs=nbytes / (kern_ms * 1e-3) / 1e9,
                     env_steps_s=E * T / (wall_ms * 1e-3))
 
@@ -538,20 +873,22 @@ def main():
         "config": {"workload": "LBF 8x8, 2 agents, 3 food, 4096 envs x 128 steps, MLP 192-128-128-6 bf16",
                    "n_envs": E, "n_agents": A, "steps_per_rollout": T, "parallelism": "single GPU"},
         "env_steps_per_s": round(rb["env_steps_s"], 1),
-        "roofline": roofline("hbm", rb["gbs"], HBM_PEAK_GBS, "GB/s", load_traffic("lbf_run_kernel_bf16")),
+        "roofline": roofline("hbm", rb["gbs"], HBM_PEAK_GBS, "GB/s", load_traffic("lbf8_4096_run_bf16:run")),
         "kernel_ms": round(rb["kern_ms"], 4),
         "f32": {"value": round(rf["value"], 1), "ms_per_step": round(rf["wall_ms"], 4),
                 "kernel_ms": round(rf["kern_ms"], 4),
                 "roofline": roofline("mfma", rf["tflops"], MFMA_PEAK_TFLOPS["f32"], "TFLOP/s",
-                                     load_traffic("lbf_run_kernel_f32"))},
+                                     load_traffic("lbf8_4096_run_f32:run"))},
         "env_only": {dt: {"env_steps_per_s": round(results[f"env_{dt}"]["env_steps_s"], 1),
                           "kernel_ms": round(results[f"env_{dt}"]["kern_ms"], 4),
-                          "roofline": roofline("hbm", results[f"env_{dt}"]["gbs"], HBM_PEAK_GBS, "GB/s")}
+                          "roofline": roofline("hbm", results[f"env_{dt}"]["gbs"], HBM_PEAK_GBS, "GB/s",
+                                               load_traffic(f"lbf8_4096_env_{dt}:env"))}
                      for dt in ("bf16", "f32")},
         "policy_forward": {dt: {"rows": results[f"policy_{dt}"]["rows"],
                                 "kernel_ms": round(results[f"policy_{dt}"]["kern_ms"], 4),
                                 "roofline": roofline("mfma", results[f"policy_{dt}"]["tflops"],
-                                                     MFMA_PEAK_TFLOPS[dt], "TFLOP/s")}
+                                                     MFMA_PEAK_TFLOPS[dt], "TFLOP/s",
+                                                     load_traffic(f"lbf8_4096_policy_{dt}:policy"))}
                            for dt in ("bf16", "f32")},
         "csrc_hash": csrc_hash(),
     }

@@ -16,6 +16,9 @@
 
 namespace rl {
 
+RL_STAMP_TABLE
+
+
 struct HnTile {
   uint64_t bits[2][HN_OBS_WORDS];  // both players' observations as bit vectors (zero between steps)
   HnPub pub;                       // the game as of the last move
@@ -259,6 +262,7 @@ __global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(s
     }
   }
   zero_lds<64 * (OW + 1)>(rows, sizeof(rows), tid);  // the bit vectors start clear
+  RL_STAMP_BEGIN
   for (int i = 0; i < n_steps + 2; ++i) {
     if (wave == 0) {
       if (i < n_steps) {  // move i
@@ -274,6 +278,7 @@ __global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(s
             act1 = actions[((size_t)(i + 1) * E + e) * 2 + 1];
           }
         }
+        RL_STAMP(0)
         // an ended game restarts with the deal drawn at t + 1
         uint64_t ended = __builtin_amdgcn_ballot_w64(d != 0);
         while (ended) {
@@ -286,8 +291,10 @@ __global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(s
             s.deck[w] = lane == el ? x : s.deck[w];
           }
         }
+        RL_STAMP(1)
         if (d) hn_deal_deck<G>(s);
         if (envlane) hn_pub(s, snap[i & 1][lane].pub);
+        RL_STAMP(2)
       }
     } else {
       if (i >= 1 && i <= n_steps) {  // the fields of move i - 1
@@ -308,11 +315,13 @@ __global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(s
             }
           }
         }
+        RL_STAMP(4)
         if (legal) {
           const int l0 = ow * LPW, nl = max(0, min(LPW, te_valid - l0));
           if (nl > 0) hn_write_legal_pub<G>(sn + l0, nl, legal + ((size_t)k * E + e0 + l0) * 2 * G::NACT, lane);
         }
       }
+      RL_STAMP(5)
       if (obs && i >= 2) {  // write out and clear this wave's rows of move i - 2
         const int k = i - 2, r0 = ow * RPW, nr = max(0, min(RPW, 2 * te_valid - r0));
         uint64_t* rw = rows[k & 1] + r0 * HN_OBS_WORDS;
@@ -323,8 +332,11 @@ __global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(s
         }
       }
     }
+    RL_STAMP(6)
     __syncthreads();  // snapshot i and the fields of move i - 1 are in; the rows of move i - 2 are out
+    RL_STAMP(7)
   }
+  RL_STAMP_END(wave == 0 ? 0 : 1)
   if (envlane) hn_store(state, E, e, s);
 }
 
@@ -400,19 +412,26 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
     hn_publish<G>(s, envs[tid]);
   }
   if (tid < TE) rows[tid] = 2 * tid + (envlane ? s.cur : 0);  // the mover's row (a zero row for padding)
+  RL_STAMP_BEGIN
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     __syncthreads();  // the previous move's games are published
+    RL_STAMP(0)
     hn_build_bits<G, TE, HN_RUN_NT>(envs, te_valid, tid);
     __syncthreads();
+    RL_STAMP(1)
     hn_paint<G, T, NW>(envs, te_valid, xs, LDX, wave, lane);
     __syncthreads();
+    RL_STAMP(2)
     mlp_input_layer_const<DT, G::OBS, PK>(xs, LDX, rows, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane, Wp1);
     __syncthreads();
+    RL_STAMP(3)
     mlp_hidden<DT, PK>(h1, L.ld1, TE, pol.H1, W2, b2, pol.H2, h2, L.ld2, wave, NW, lane, Wp2);
     __syncthreads();
+    RL_STAMP(4)
     mlp_logits<DT, PK>(h2, L.ld2, TE, pol.H2, W3, b3, NA, lg, MAX_NA, wave, NW, lane, Wp3);
     __syncthreads();
+    RL_STAMP(5)
     for (int idx = tid; idx < te_valid * NA; idx += HN_RUN_NT) {
       const int el = idx / NA, a = idx - el * NA;
       const int cur = envs[el].pub.cur;
@@ -425,12 +444,14 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
         lo[(1 - cur) * NA + a] = -INFINITY;
       }
     }
+    RL_STAMP(6)
     // The trajectory copy of o_t is issued after the step's weight loads: a
     // wave's loads wait for its earlier stores (one in-order counter).
     if (out.obs)
       copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * G::OBS, G::OBS,
                          2 * te_valid, tid, HN_RUN_NT);
     __syncthreads();
+    RL_STAMP(7)
     uint32_t d = 0;
     if (envlane) {
       int best = 0;
@@ -458,6 +479,7 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
     }
     hn_flag_any(need, TE, d, wave, lane);
     __syncthreads();
+    RL_STAMP(8)
     if (need[TE]) {
       hn_shuffle_flagged<G, NW>(p, e0, te_valid, t + 1, need, words, wave, lane);
       __syncthreads();
@@ -467,7 +489,9 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
         rows[tid] = 2 * tid + s.cur;
       }
     }
+    RL_STAMP(9)
   }
+  RL_STAMP_END(wave)
   __syncthreads();
   if (out.obs_last) {
     hn_build_bits<G, TE, HN_RUN_NT>(envs, te_valid, tid);
@@ -552,3 +576,5 @@ hipError_t launch_hn_run(const HnParams& p, const PolicyArgs& pol, int32_t* stat
 }
 
 }  // namespace rl
+
+RL_STAMP_EXPORT(hn)

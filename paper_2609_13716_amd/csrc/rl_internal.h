@@ -23,6 +23,51 @@ __device__ __forceinline__ int fdiv(int x, uint32_t magic) {
   return magic ? (int)__umulhi((uint32_t)x, magic) : x;
 }
 
+// Phase stamps, compiled in only by the instrumented build (RL_PHASE_STAMPS;
+// every macro is empty otherwise).  Each wave adds the shader-clock cycles
+// (s_memtime) between consecutive marks of a kernel's step loop to
+// per-phase counters and, when the kernel ends, into a device table
+// [role][phase] summed over the grid (the role is the wave's part in its
+// workgroup, chosen by the kernel; the last phase counter of a role counts
+// its waves).  A translation unit that stamps declares
+// its table with RL_STAMP_TABLE and exports a reader with
+// RL_STAMP_EXPORT(unit): rl_phase_stamps_<unit>(out, reset) copies the
+// table to `out` (RL_STAMP_ROLES x RL_STAMP_PHASES counters) and clears it
+// when `reset` is non-zero.
+constexpr int RL_STAMP_PHASES = 12, RL_STAMP_ROLES = 8;
+#ifdef RL_PHASE_STAMPS
+#define RL_STAMP_TABLE static __device__ unsigned long long rl_stamp_table[RL_STAMP_ROLES * RL_STAMP_PHASES];
+#define RL_STAMP_BEGIN                                   \
+  uint64_t rl_st_last = __builtin_amdgcn_s_memtime(); \
+  uint64_t rl_st[RL_STAMP_PHASES] = {};
+#define RL_STAMP(i)                                            \
+  {                                                            \
+    const uint64_t rl_now = __builtin_amdgcn_s_memtime();     \
+    rl_st[i] += rl_now - rl_st_last;                           \
+    rl_st_last = rl_now;                                       \
+  }
+#define RL_STAMP_END(role)                                                                   \
+  rl_st[RL_STAMP_PHASES - 1] = 1; /* the last counter counts the waves of the role */       \
+  if ((threadIdx.x & 63) == 0)                                                               \
+    for (int rl_i = 0; rl_i < RL_STAMP_PHASES; ++rl_i)                                       \
+      atomicAdd(&rl_stamp_table[((role) % RL_STAMP_ROLES) * RL_STAMP_PHASES + rl_i], rl_st[rl_i]);
+#define RL_STAMP_EXPORT(unit)                                                                          \
+  extern "C" int rl_phase_stamps_##unit(unsigned long long* out, int reset) {                          \
+    hipError_t e = hipMemcpyFromSymbol(out, HIP_SYMBOL(rl::rl_stamp_table), sizeof(rl::rl_stamp_table)); \
+    if (e == hipSuccess && reset) {                                                                    \
+      static unsigned long long zero[rl::RL_STAMP_ROLES * rl::RL_STAMP_PHASES] = {};                   \
+      e = hipMemcpyToSymbol(HIP_SYMBOL(rl::rl_stamp_table), zero, sizeof(zero));                       \
+    }                                                                                                  \
+    return (int)e;                                                                                     \
+  }
+#else
+#define RL_STAMP_TABLE
+#define RL_STAMP_BEGIN
+#define RL_STAMP(i)
+#define RL_STAMP_END(role)
+#define RL_STAMP_EXPORT(unit)
+#endif
+
 // Make this wave's earlier LDS writes visible to its later LDS reads.
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

@@ -20,6 +20,9 @@
 
 namespace rl {
 
+RL_STAMP_TABLE
+
+
 struct LbfMagic {
   uint32_t d, a, hw, na;
 };
@@ -908,12 +911,14 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   // Let the prologue loads land here, once (see lbf_env_kernel).
   __builtin_amdgcn_s_waitcnt(0);
 
+  RL_STAMP_BEGIN
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     const int sn = k % NOISE_STEPS;
     T* xcur = xs[DB ? (k & 1) : 0];       // o_t
     T* xnext = xs[DB ? ((k + 1) & 1) : 0];  // o_{t+1}, painted by the env wave
     __syncthreads();  // the env wave is done with the previous step (tile, noise, actions)
+    RL_STAMP(0)
     if (sn == 0) {
       // Philox action draws of the next NOISE_STEPS steps, one block (8 draws)
       // per (step, row), in one pass over all lanes
@@ -933,12 +938,14 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       draw_noise(0, nz[k & 1], tid, NT);  // noise of the batch's first step
       __syncthreads();
     }
+    RL_STAMP(1)
     {
       f32x4 acc[MT][RegLayer<DT, D, H1, NW, LEAN>::OWN];
       L1.template run<MT>(xcur, LDX, acc, wave, lane);
       L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane, bias_s);
     }
     __syncthreads();
+    RL_STAMP(2)
     {
       f32x4 acc[MT][RegLayer<DT, H1, H2, NW, LEAN>::OWN];
       L2.template run<MT>(h1s, LD1, acc, wave, lane);
@@ -950,6 +957,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane, bias_s + H1);
     }
     __syncthreads();
+    RL_STAMP(3)
     if (wave == ew) {
       if constexpr (LEAN) lbf_copy<A, F>(s, env_s[min(el, TE - 1)]);
       // Layer 3 transposed, logits^T = W3 h2^T: lane holds row (lane % 16) of
@@ -1030,6 +1038,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       }
       if constexpr (!DIRECT) wave_lds_sync();
       uint32_t d = 0;
+      RL_STAMP(4)
       float r = 0.f;
       if (envlane) {
         int act[LBF_MAXA];
@@ -1057,6 +1066,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         lbf_transition<A, F, GH, GW>(p, s, act, r, d);
       }
       // reset blocks of every env that ended, one Philox block per lane
+      RL_STAMP(5)
       const uint64_t done_mask = __ballot(envlane && d != 0);
       if (done_mask) {
         const int j = lane / nblk, blk = lane - j * nblk;
@@ -1078,12 +1088,14 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
           }
         }
       }
+      RL_STAMP(6)
       if (envlane) {
         lbf_paint_tile<T, A, F>(s, el, xnext, LDX, HW, true);
         if (out.reward) out.reward[(size_t)k * E + e] = r;
         if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
         if constexpr (LEAN) lbf_copy<A, F>(env_s[el], s);
       }
+      RL_STAMP(7)
     } else {
       // the other waves, while the env wave steps: (two tiles) o_t to the
       // trajectory, clearing its tile; the Gumbel noise of the next step (a new
@@ -1092,10 +1104,13 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
         copy_obs_rows<T, R, D, LDX, NT - 64, true>(
             xcur, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, te_valid * A,
             tid - 64);
+      RL_STAMP(8)
       if (k + 1 < n_steps && (k + 1) % NOISE_STEPS != 0)
         draw_noise((k + 1) % NOISE_STEPS, nz[(k + 1) & 1], (wave - 1) * 64 + lane, (NW - 1) * 64);
+      RL_STAMP(9)
     }
   }
+  RL_STAMP_END(wave)
   __syncthreads();
   T* xlast = xs[DB ? (n_steps & 1) : 0];  // o_{t0+T}
   if (out.obs_last)
@@ -1764,3 +1779,5 @@ hipError_t launch_lbf_run(const LbfParams& p, const PolicyArgs& pol, int32_t* st
 }
 
 }  // namespace rl
+
+RL_STAMP_EXPORT(lbf)

@@ -17,7 +17,9 @@ import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "librollout.so")
+# RL_LIB_PATH selects another build of the same library (the phase-stamped
+# one of build.py --stamps); by default the product library next to this file.
+LIB_PATH = os.environ.get("RL_LIB_PATH") or os.path.join(_HERE, "librollout.so")
 
 RL_OK, RL_EINVAL, RL_EUNSUPPORTED, RL_ESHAPE, RL_EDEVICE = 0, -1, -2, -3, -4
 RL_ENV_LBF, RL_ENV_OVERCOOKED, RL_ENV_HANABI = 0, 1, 2
