@@ -29,16 +29,19 @@ struct HnTile {
 // computes field t / (2 TE) of row t % (2 TE) (consecutive lanes take the
 // same field of different rows, so a wave runs few of the field branches) and
 // ORs it into the row's words (LDS atomics; the words are zero beforehand).
-// Needs the published games.
+// Needs the published games.  `rows`: the bit vectors row by row (row
+// 2 el + me at rows + (2 el + me) * HN_OBS_WORDS), or null for the vectors
+// inside the HnTiles.
 template <class G, int TE, int NT>
-__device__ __forceinline__ void hn_build_bits(HnTile* envs, int te_valid, int tid) {
+__device__ __forceinline__ void hn_build_bits(HnTile* envs, int te_valid, int tid, uint64_t* rows = nullptr) {
   for (int t = tid; t < 2 * TE * G::NFIELDS; t += NT) {
     const int f = t / (2 * TE), row = t - f * (2 * TE), el = row >> 1, me = row & 1;
     if (el >= te_valid) continue;
     int off;
     const uint64_t v = hn_field_bits<G>(envs[el].pub, me, f, off);
     if (v) {
-      unsigned long long* w = reinterpret_cast<unsigned long long*>(envs[el].bits[me]);
+      unsigned long long* w =
+          reinterpret_cast<unsigned long long*>(rows ? rows + row * HN_OBS_WORDS : envs[el].bits[me]);
       const int i = off >> 6, sh = off & 63;
       atomicOr(w + i, (unsigned long long)(v << sh));
       if (sh && (v >> (64 - sh))) atomicOr(w + i + 1, (unsigned long long)(v >> (64 - sh)));
@@ -133,6 +136,34 @@ __device__ __forceinline__ void hn_write_obs(const uint64_t* rows, int nrows, OT
       load(v * WE, lo, hi, nx);
       g[v] = word(bits(v * WE, WE, lo, hi, nx), 0);
     }
+  }
+}
+
+// Paint the mover's observation of envs 0..te_valid-1 (bit-vector row
+// 2 el + cur, rows as in hn_build_bits) into row el of the layer-1 operand
+// tile as 0 / 1 values, 16 bytes (VE features) per store, by all NT threads.
+// The tile's row stride holds whole vectors (the features past G::OBS come
+// out 0, the K padding they fall in).
+template <class G, typename T, int NT>
+__device__ __forceinline__ void hn_paint_movers(const HnTile* __restrict__ envs, int te_valid,
+                                                const uint64_t* __restrict__ rows, T* __restrict__ tile, int ld,
+                                                int tid) {
+  constexpr int VE = 16 / sizeof(T), NV = (G::OBS + VE - 1) / VE;  // vectors per row
+  const uint32_t one = sizeof(T) == 2 ? 0x3f80u : 0x3f800000u;
+  for (int i = tid; i < te_valid * NV; i += NT) {
+    const int el = i / NV, v = i - el * NV, j = v * VE;
+    const uint64_t* w = rows + (2 * el + envs[el].pub.cur) * HN_OBS_WORDS;
+    const int wi = j >> 6, sh = j & 63;  // VE divides 64: a vector never straddles two words
+    const uint32_t b = (uint32_t)(w[wi] >> sh) & ((1u << VE) - 1u);
+    uint32_t q[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      if constexpr (sizeof(T) == 2)
+        q[c] = (((b >> (2 * c)) & 1u) ? one : 0u) | (((b >> (2 * c + 1)) & 1u) ? one << 16 : 0u);
+      else
+        q[c] = ((b >> c) & 1u) ? one : 0u;
+    }
+    *reinterpret_cast<u32x4*>(tile + (size_t)el * ld + j) = u32x4{q[0], q[1], q[2], q[3]};
   }
 }
 
@@ -347,7 +378,7 @@ constexpr int HN_RUN_NT = 512;  // 8 waves: the MLP's weight-streaming chains of
 
 struct HnRunLayout {
   int ldx, ld1, ld2;
-  size_t off_x, off_h1, off_h2, off_lg, off_sc, off_env, off_words, off_need, off_rows, total;
+  size_t off_x, off_h1, off_h2, off_lg, off_sc, off_env, off_words, off_need, off_bits, total;
 };
 
 __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int obs) {
@@ -357,7 +388,7 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int
   L.ld1 = dt == DT_F32 ? lds_ld<DT_F32>(H1) : lds_ld<DT_BF16>(H1);
   L.ld2 = dt == DT_F32 ? lds_ld<DT_F32>(H2) : lds_ld<DT_BF16>(H2);
   size_t o = 0;
-  L.off_x = o;     o += (size_t)2 * HN_RUN_TE * L.ldx * es;
+  L.off_x = o;     o += (size_t)HN_RUN_TE * L.ldx * es;
   L.off_h1 = o;    o += (size_t)HN_RUN_TE * L.ld1 * es;
   L.off_h2 = o;    o += (size_t)HN_RUN_TE * L.ld2 * es;
   L.off_lg = o;    o += (size_t)HN_RUN_TE * MAX_NA * 4;
@@ -366,7 +397,8 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int
   L.off_env = o;   o += (size_t)HN_RUN_TE * sizeof(HnTile);
   L.off_words = o; o += (size_t)HN_RUN_TE * HN_DECK_WORDS * 4;
   L.off_need = o;  o += (size_t)(HN_RUN_TE + 1) * 4;
-  L.off_rows = o;  o += (size_t)HN_RUN_TE * 4;
+  o = (o + 15) & ~(size_t)15;
+  L.off_bits = o;  o += (size_t)2 * HN_RUN_TE * HN_OBS_WORDS * 8;
   L.total = o;
   return L;
 }
@@ -389,7 +421,7 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
   HnTile* envs = reinterpret_cast<HnTile*>(smem + L.off_env);
   uint32_t(*words)[HN_DECK_WORDS] = reinterpret_cast<uint32_t(*)[HN_DECK_WORDS]>(smem + L.off_words);
   uint32_t* need = reinterpret_cast<uint32_t*>(smem + L.off_need);
-  int* rows = reinterpret_cast<int*>(smem + L.off_rows);
+  uint64_t* bits = reinterpret_cast<uint64_t*>(smem + L.off_bits);  // the observation bit vectors, row by row
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
@@ -411,19 +443,18 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
     hn_load(state, E, e, s);
     hn_publish<G>(s, envs[tid]);
   }
-  if (tid < TE) rows[tid] = 2 * tid + (envlane ? s.cur : 0);  // the mover's row (a zero row for padding)
   RL_STAMP_BEGIN
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     __syncthreads();  // the previous move's games are published
     RL_STAMP(0)
-    hn_build_bits<G, TE, HN_RUN_NT>(envs, te_valid, tid);
+    hn_build_bits<G, TE, HN_RUN_NT>(envs, te_valid, tid, bits);
     __syncthreads();
     RL_STAMP(1)
-    hn_paint<G, T, NW>(envs, te_valid, xs, LDX, wave, lane);
+    hn_paint_movers<G, T, HN_RUN_NT>(envs, te_valid, bits, xs, LDX, tid);  // row el: the mover of env el
     __syncthreads();
     RL_STAMP(2)
-    mlp_input_layer_const<DT, G::OBS, PK>(xs, LDX, rows, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane, Wp1);
+    mlp_input_layer_const<DT, G::OBS, PK>(xs, LDX, nullptr, TE, W1, b1, pol.H1, h1, L.ld1, wave, NW, lane, Wp1);
     __syncthreads();
     RL_STAMP(3)
     mlp_hidden<DT, PK>(h1, L.ld1, TE, pol.H1, W2, b2, pol.H2, h2, L.ld2, wave, NW, lane, Wp2);
@@ -445,11 +476,21 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
       }
     }
     RL_STAMP(6)
-    // The trajectory copy of o_t is issued after the step's weight loads: a
-    // wave's loads wait for its earlier stores (one in-order counter).
-    if (out.obs)
-      copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * G::OBS, G::OBS,
-                         2 * te_valid, tid, HN_RUN_NT);
+    // o_t to the trajectory straight from the bit vectors, each wave its own
+    // rows, which it then clears for the next step; issued after the step's
+    // weight loads (a wave's loads wait for its earlier stores: one in-order
+    // counter).
+    {
+      constexpr int RPW = 2 * TE / NW;  // rows per wave
+      const int r0 = wave * RPW, nr = max(0, min(RPW, 2 * te_valid - r0));
+      uint64_t* rw = bits + r0 * HN_OBS_WORDS;
+      if (nr > 0) {
+        if (out.obs)
+          hn_write_obs<G, T, RPW>(rw, nr, static_cast<T*>(out.obs) + (((size_t)k * E + e0) * 2 + r0) * G::OBS, lane);
+        wave_lds_sync();
+        for (int j = lane; j < nr * HN_OBS_WORDS; j += 64) rw[j] = 0;
+      }
+    }
     __syncthreads();
     RL_STAMP(7)
     uint32_t d = 0;
@@ -470,10 +511,7 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
       float r;
       hn_transition<G>(p, s, best, r, d);
       need[tid] = d;
-      if (!d) {
-        hn_publish<G>(s, envs[tid]);
-        rows[tid] = 2 * tid + s.cur;
-      }
+      if (!d) hn_publish<G>(s, envs[tid]);
       if (out.reward) out.reward[(size_t)k * E + e] = r;
       if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
     }
@@ -486,7 +524,6 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
       if (d) {
         hn_deal<G>(s, words[tid]);
         hn_publish<G>(s, envs[tid]);
-        rows[tid] = 2 * tid + s.cur;
       }
     }
     RL_STAMP(9)
@@ -494,12 +531,13 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
   RL_STAMP_END(wave)
   __syncthreads();
   if (out.obs_last) {
-    hn_build_bits<G, TE, HN_RUN_NT>(envs, te_valid, tid);
+    hn_build_bits<G, TE, HN_RUN_NT>(envs, te_valid, tid, bits);
     __syncthreads();
-    hn_paint<G, T, NW>(envs, te_valid, xs, LDX, wave, lane);
-    __syncthreads();
-    copy_rows_global16(xs, LDX, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * G::OBS, G::OBS, 2 * te_valid,
-                       tid, HN_RUN_NT);
+    constexpr int RPW = 2 * TE / NW;
+    const int r0 = wave * RPW, nr = max(0, min(RPW, 2 * te_valid - r0));
+    if (nr > 0)
+      hn_write_obs<G, T, RPW>(bits + r0 * HN_OBS_WORDS, nr, static_cast<T*>(out.obs_last) + ((size_t)e0 * 2 + r0) * G::OBS,
+                              lane);
   }
   if (envlane) hn_store(state, E, e, s);
 }
