@@ -126,6 +126,32 @@ def test_env_only_parity(cfgkw, T, dtype):
     assert (ref["done"] != 0).any()
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_env_only_4096_sampled_envs(dtype):
+    """Env-only steps of the 4096-env, 128-step 8x8 workload in one launch (the benchmarked launch, for both
+    observation dtypes); sampled envs, across workgroup tiles, replayed in the oracle."""
+    require_gpu()
+    w = workloads.WORKLOADS["lbf8_4096"]
+    cfg = R.EnvConfig(n_envs=w["n_envs"], seed=9, **w["env"])
+    E, T, A, D = cfg.n_envs, w["n_steps"], cfg.n_agents, R.rl_obs_dim(cfg)
+    _note(f"env-only E={E} T={T} {dtype} (sampled)")
+    sample = [0, 1, 7, 8, 15, 16, 2047, 2048, 4088, 4095]
+    acts = workloads.injected_actions(T, E, A, 6, seed=41, p_invalid=0.02)
+    state = R.new_state(cfg)
+    R.rollout_init(cfg, state)
+    obs = torch.empty(T, E, A, D, dtype=dtype, device="cuda")
+    rew = torch.empty(T, E, dtype=torch.float32, device="cuda")
+    done = torch.empty(T, E, dtype=torch.uint8, device="cuda")
+    R.rollout_step(cfg, state, 0, torch.from_numpy(acts).cuda(), obs, rew, done)
+    torch.cuda.synchronize()
+    ref = rollout.env_only(lbf, oracle_cfg(cfg), cfg.seed, sample, 0, acts[:, sample])
+    assert np.array_equal(rew[:, sample].cpu().numpy().view(np.uint32), ref["reward"].view(np.uint32))
+    assert np.array_equal(done[:, sample].cpu().numpy(), ref["done"])
+    assert np.array_equal(_obs_np(obs[:, sample]), ref["obs"])
+    final = states_from_device(cfg, state)
+    assert [final[e] for e in sample] == ref["states"]
+
+
 def test_env_only_resume_is_bit_identical():
     require_gpu()
     cfg = R.EnvConfig(n_envs=300, seed=5)
