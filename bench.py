@@ -380,7 +380,7 @@ def kernel_role(name):
     kernels and the input generators)."""
     if "policy_fwd" in name or "policy_forward" in name:
         return "policy"
-    if "_env_kernel" in name:
+    if "_env_kernel" in name or "_env3_kernel" in name:
         return "env"
     if "gae" in name:
         return "gae"
@@ -452,12 +452,15 @@ def summarize_counters(src):
     for leg, _, passes in COUNTER_LEGS:
         if leg == "copy":
             continue
+        one_call = "s5" in workloads.WORKLOADS.get(leg, {})  # the S5 leg times one call (its env steps included)
         per_role = {}
         for ps in passes:
             for k, c in _read_counter_csv(os.path.join(src, ps, leg)).values():
                 role = kernel_role(k)
                 if role is None or role == "copy":  # (device copies outside the copy leg are set-up)
                     continue
+                if one_call:
+                    role = "run"
                 rr = per_role.setdefault(role, {"kernels": set(), "sum": {}})
                 rr["kernels"].add(k.split("(")[0].replace("void ", "").replace("rl::", ""))
                 for ctr, v in c.items():
@@ -511,13 +514,14 @@ def summarize_counters(src):
         ab = r.get("algorithmic_bytes_per_launch")
         hbm = f"{hb / 1e6:,.1f} ({r['read_bytes'] / 1e6:,.1f} + {r['write_bytes'] / 1e6:,.1f})" if hb else "-"
         ratio = f"{hb / ab:.3f}" if hb and ab else "-"
-        mf = f"{100 * r['mfma_busy_frac']:.1f}%" if "mfma_busy_frac" in r else "-"
+        mf = f"{100 * r['mfma_busy_frac']:.1f}%" if r.get("mfma_flop_per_launch") else "-"
         fl = (f"{r['mfma_flop_per_launch'] / 1e9:,.1f} ({r['algorithmic_flop_per_launch'] / 1e9:,.1f})"
               if "algorithmic_flop_per_launch" in r else
-              f"{r['mfma_flop_per_launch'] / 1e9:,.1f}" if "mfma_flop_per_launch" in r else "-")
+              f"{r['mfma_flop_per_launch'] / 1e9:,.1f}" if r.get("mfma_flop_per_launch") else "-")
         l1 = f"{r['l2_to_l1_read_req_per_launch'] / 1e6:,.2f}" if "l2_to_l1_read_req_per_launch" in r else "-"
         ks = "<br>".join(f"`{k}`" for k in r["kernels"][:3]) + (" ..." if len(r["kernels"]) > 3 else "")
-        md.append(f"| {leg} | {role} | {ks} | {hbm} | {ab / 1e6 if ab else 0:,.1f} | {ratio} | {mf} | {fl} | {l1} |")
+        abs_ = f"{ab / 1e6:,.1f}" if ab else "-"
+        md.append(f"| {leg} | {role} | {ks} | {hbm} | {abs_} | {ratio} | {mf} | {fl} | {l1} |")
     open(os.path.join(ROOT, "profiles", "counters_all_workloads.md"), "w").write("\n".join(md) + "\n")
     return out
 
