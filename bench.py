@@ -530,7 +530,7 @@ def summarize_counters(src):
 # (case, workload, call, stamp unit, iterations per launch beyond n_steps, role names, phase names)
 PHASE_CASES = (
     ("headline fused rollout", "lbf8_4096", "run", "lbf", 0, ("env wave", "other waves"),
-     {0: "barrier at the step's top", 1: "action Philox draws (one step in 8)", 2: "layer 1 + barrier",
+     {0: "barrier at the step's top", 1: "action Philox draws (one step in 16)", 2: "layer 1 + barrier",
       3: "layer 2 + barrier", 4: "layer 3 + Gumbel argmax", 5: "transition", 6: "resets",
       7: "paint o_t+1, reward/done stores", 8: "copy o_t to the trajectory", 9: "Gumbel noise of step t+1"}),
     ("12x12 fused rollout", "lbf12_16k", "run", "lbf", 0, ("env wave", "other waves"), None),
