@@ -731,7 +731,7 @@ static bool try_launch_policy_tiled(const PolicyArgs& pol, const void* obs, cons
                                     float* logits, hipStream_t s, hipError_t* err) {
   if (pol.dt != DT_BF16 || pol.D % 2 != 0 || pol.H1 != pol.H2 || pol.NA > MAX_NA) return false;
   if (pol.H1 == 256)
-    *err = launch_policy_tiled<256, 128, 3, 1>(pol, obs, legal, rows, logits, s);
+    *err = launch_policy_tiled<256, 64, 2, 2>(pol, obs, legal, rows, logits, s);  // two workgroups per CU
   else if (pol.H1 == 512)
     *err = launch_policy_tiled<512, 64, 2, 1>(pol, obs, legal, rows, logits, s);
   else
