@@ -1,6 +1,7 @@
 """Edge cases of the GPU path against the oracle, through the C ABI: a single env, episodes truncated at every
 step (max_steps 1), one-step rollouts, and a batch of 65,537 envs (16 times the benchmark's, plus a ragged
-workgroup) checked on sampled envs at both ends of the batch."""
+workgroup) checked on sampled envs at both ends of the batch; for Hanabi and the kitchen, single envs and
+ragged tiles with every game truncated after one or two moves (a re-deal at nearly every move)."""
 
 import sys
 
@@ -106,3 +107,67 @@ def test_s5_single_env():
     lg_ref = np.concatenate([ref["logits"], ref["value"][..., None]], axis=-1)
     lg_gpu = np.concatenate([g["logits"].numpy(), g["value"].numpy()[..., None]], axis=-1)
     assert_logits_close(lg_gpu, lg_ref, RTOL["bf16"])
+
+
+# ------------------------------------------------- Hanabi and the kitchen
+
+@pytest.mark.parametrize("E,max_steps,dtype", [(1, 1, "f32"), (5, 2, "bf16"), (9, 1, "bf16")])
+def test_hanabi_env_only_every_move_truncated(E, max_steps, dtype):
+    """Env-only Hanabi where every game is truncated after one or two moves, so the env wave re-deals
+    every tile's games at (nearly) every move; a single env and ragged workgroup tiles."""
+    require_gpu()
+    from oracle import hanabi as hn
+    from parity import hn_oracle_cfg, hn_states_from_device
+    from test_gpu_hanabi import _actions, _check_env_only, _env_only_gpu
+    cfg = R.hanabi_config(E, max_steps=max_steps, seed=E + 40, env_base=7)
+    _note(f"hanabi env-only E={E} max_steps={max_steps} {dtype}")
+    state = R.new_state(cfg)
+    R.rollout_init(cfg, state)
+    T = 24
+    actions = _actions(T, E, seed=E + 3)
+    g = _env_only_gpu(cfg, state, 0, actions, dtype)
+    ref = rollout.env_only(hn, hn_oracle_cfg(cfg), cfg.seed, range(7, 7 + E), 0, actions)
+    _check_env_only(cfg, g, ref, state)
+    assert (g["done"].numpy() & 2).sum() >= T * E // max_steps - E
+
+
+@pytest.mark.parametrize("E,max_steps,dtype", [(1, 1, "bf16"), (17, 2, "f32")])
+def test_hanabi_rollout_every_move_truncated(E, max_steps, dtype):
+    """The fused Hanabi rollout with every game truncated after one or two moves (a re-deal of most of the
+    workgroup's games at every move), a single env and a ragged second workgroup."""
+    require_gpu()
+    from oracle import hanabi as hn
+    from parity import hn_oracle_cfg, hn_states_from_device
+    from test_gpu_hanabi import D, NA, _check_traj, _run_gpu
+    cfg = R.hanabi_config(E, max_steps=max_steps, seed=E + 50, env_base=11)
+    _note(f"hanabi rollout_run E={E} max_steps={max_steps} {dtype}")
+    dims = (D, 64, 64, NA)
+    ws, bs = workloads.policy_weights(dims, seed=5, bias_scale=0.1)
+    pol = R.Policy(ws, bs, dtype)
+    T = 20
+    state, g = _run_gpu(cfg, pol, T)
+    ids = list(range(11, 11 + E))
+    hook = NearTieLockstep(g["actions"].numpy(), cfg.seed, ids, RTOL[dtype])
+    ref = rollout.rollout(hn, hn_oracle_cfg(cfg), cfg.seed, ids, 0, T, ws, bs, dtype, action_hook=hook)
+    _check_traj(g, ref, slice(None), RTOL[dtype])
+    assert hn_states_from_device(cfg, state) == ref["states"]
+
+
+def test_overcooked_single_env_every_step_truncated():
+    """The fused kitchen rollout with one env whose episode is truncated at every step."""
+    require_gpu()
+    from oracle import overcooked as oc
+    from parity import oc_oracle_cfg, oc_states_from_device
+    from test_gpu_overcooked import D, NA, _check_traj, _run_gpu, _tuples
+    cfg = R.overcooked_config(1, cook_time=3, max_steps=1, seed=4, env_base=2)
+    _note("overcooked rollout_run E=1 max_steps=1")
+    dims = (D, 64, 64, NA)
+    ws, bs = workloads.policy_weights(dims, seed=6, bias_scale=0.1)
+    pol = R.Policy(ws, bs, "bf16")
+    T = 16
+    state, g = _run_gpu(cfg, pol, T)
+    hook = NearTieLockstep(g["actions"].numpy(), cfg.seed, [2], RTOL["bf16"])
+    ref = rollout.rollout(oc, oc_oracle_cfg(cfg), cfg.seed, [2], 0, T, ws, bs, "bf16", action_hook=hook)
+    _check_traj(g, ref, slice(None), RTOL["bf16"])
+    assert (g["done"].numpy() & 2).all()
+    assert _tuples(oc_states_from_device(cfg, state)) == _tuples(ref["states"])
