@@ -800,7 +800,7 @@ __device__ __forceinline__ float row_log_pi(const float (&logit)[4], int g, int 
 // TM: agents whose teammates entry is a heuristic kind act with that
 // heuristic (evaluated by the env lanes) instead of the network.
 template <int DT, int GH, int GW, int H1, int H2, int NA, int A, int F, int TE, int NW, int MINB, bool VH = false,
-          bool TM = false>
+          bool TM = false, bool S1 = false>
 __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p, PolicyArgs pol,
                                                                     int32_t* __restrict__ state, uint64_t t0,
                                                                     int n_steps, TrajArgs out) {
@@ -821,8 +821,11 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   // LEAN: the resident weights leave too few registers for the env step, so
   // the biases and the env state wait in LDS between uses.
   constexpr int REG_BUDGET = 512 / ((NW * MINB + 3) / 4);
-  constexpr bool LEAN =
-      RegLayer<DT, D, H1, NW>::WREGS + RegLayer<DT, H1, H2, NW>::WREGS + 160 > REG_BUDGET;
+  // S1: layer 1 streams its weights from L2 (StreamLayer) instead of holding them
+  constexpr int L1REGS = S1 ? StreamLayer<DT_BF16, D, H1, NW>::WREGS : RegLayer<DT, D, H1, NW>::WREGS;
+  constexpr bool LEAN = S1 || L1REGS + RegLayer<DT, H1, H2, NW>::WREGS + 160 > REG_BUDGET;
+  using L1T = std::conditional_t<S1, StreamLayer<DT_BF16, D, H1, NW, LEAN>, RegLayer<DT, D, H1, NW, LEAN>>;
+  static_assert(!S1 || DT == DT_BF16, "streamed layer 1: bf16");
   constexpr int NOUT = NA + (VH ? 1 : 0);  // layer-3 outputs: the actions, then the value
   static_assert(NA <= 8 && NOUT <= 8, "one Philox block of action noise per row; outputs in two lane groups");
   static_assert(!(VH && LEAN), "the value head runs on shapes whose env state stays in registers");
@@ -863,13 +866,17 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     }
   };
 
-  RegLayer<DT, D, H1, NW, LEAN> L1;
+  L1T L1;
   RegLayer<DT, H1, H2, NW, LEAN> L2;
   if constexpr (LEAN) {
     for (int i = tid; i < H1 + H2; i += NT)
       bias_s[i] = DType<DT>::to_f32(i < H1 ? static_cast<const T*>(pol.b[0])[i] : static_cast<const T*>(pol.b[1])[i - H1]);
   }
-  L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane);
+  if constexpr (S1)
+    L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane,
+            static_cast<const T*>(pol.Wp[0]));
+  else
+    L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane);
   L2.load(static_cast<const T*>(pol.W[1]), static_cast<const T*>(pol.b[1]), wave, lane);
   if (tid < 64) {
     const int n = lane & 15;
@@ -940,7 +947,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     }
     RL_STAMP(1)
     {
-      f32x4 acc[MT][RegLayer<DT, D, H1, NW, LEAN>::OWN];
+      f32x4 acc[MT][L1T::OWN];
       L1.template run<MT>(xcur, LDX, acc, wave, lane);
       L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane, bias_s);
     }
@@ -951,9 +958,12 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       L2.template run<MT>(h1s, LD1, acc, wave, lane);
       // (one tile) o_t to the trajectory while the layer-2 MFMAs run, clearing
       // the tile behind the copy (the env wave paints o_{t+1} onto it after layer 3)
-      if constexpr (!DB)
+      if constexpr (!DB) {
+        int ct = tid;
+        if constexpr (S1) asm volatile("" : "+v"(ct));  // (its addresses formed here, not held across the loop)
         copy_obs_rows<T, R, D, LDX, NT, true>(
-            xcur, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, te_valid * A, tid);
+            xcur, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, te_valid * A, ct);
+      }
       L2.template store_tanh<MT>(acc, h2s, LD2, wave, lane, bias_s + H1);
     }
     __syncthreads();
@@ -1118,7 +1128,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   if constexpr (VH) {
     if (out.value_last) {  // V(o_{t0+T}): one more pass of the network over the final tile
       {
-        f32x4 acc[MT][RegLayer<DT, D, H1, NW, LEAN>::OWN];
+        f32x4 acc[MT][L1T::OWN];
         L1.template run<MT>(xlast, LDX, acc, wave, lane);
         L1.template store_tanh<MT>(acc, h1s, LD1, wave, lane, bias_s);
       }
@@ -1149,10 +1159,11 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
 // Compile-time shapes that run on lbf_rollout_kernel (everything else uses
 // lbf_run_kernel): LBF 8x8 with 2 agents and 3 foods (obs 192) under 64- and
 // 128-wide layers.
-template <int DT, int GH, int GW, int H1, int H2, int A, int F, int TE, int NW, int MINB, bool VH, bool TM>
+template <int DT, int GH, int GW, int H1, int H2, int A, int F, int TE, int NW, int MINB, bool VH, bool TM,
+          bool S1 = false>
 static hipError_t launch_rollout_reg(const LbfParams& p, const LbfMagic&, const PolicyArgs& pol, int32_t* state,
                                      uint64_t t0, int n_steps, const TrajArgs& out, hipStream_t s) {
-  auto kern = lbf_rollout_kernel<DT, GH, GW, H1, H2, LBF_NACT, A, F, TE, NW, MINB, VH, TM>;
+  auto kern = lbf_rollout_kernel<DT, GH, GW, H1, H2, LBF_NACT, A, F, TE, NW, MINB, VH, TM, S1>;
   const dim3 grid((unsigned)((p.E + TE - 1) / TE));
   kern<<<grid, NW * 64, 0, s>>>(p, pol, state, t0, n_steps, out);
   return hipGetLastError();
@@ -1177,7 +1188,12 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
   RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2, 0)
   RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1, 0)
   RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2, 0)
-  RL_REG_CASE(DT_BF16, 12, 12, 256, 256, 3, 6, 16, 8, 1, 0)
+  if (pol.dt == DT_BF16 && p.H == 12 && p.W == 12 && pol.H1 == 256 && pol.H2 == 256 && p.A == 3 && p.F == 6 &&
+      !pol.VH && !tm) {  // layer 1 (432 x 256) streamed: both layers resident would spill
+    *err = launch_rollout_reg<DT_BF16, 12, 12, 256, 256, 3, 6, 16, 8, 1, false, false, true>(p, m, pol, state, t0,
+                                                                                          n_steps, out, s);
+    return true;
+  }
   RL_REG_CASE(DT_BF16, 7, 7, 128, 128, 2, 3, 8, 4, 2, 0)
   RL_REG_CASE(DT_F32, 8, 8, 64, 64, 2, 3, 8, 4, 2, 1)
   RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2, 1)

@@ -219,6 +219,123 @@ struct RegLayer {
   }
 };
 
+// A bf16 layer with the same interface, MFMA chains and outputs as RegLayer
+// whose weights are streamed instead of held: each K step's B operands of the
+// wave's tiles are read from global memory (L2) PD steps ahead of their MFMAs,
+// from the fragment-major packed copy when there is one (one contiguous 1 KB
+// block per wave-wide load) or else from the nn.Linear rows.  It holds PD
+// operand sets instead of all KSTEPS, for shapes whose resident weights would
+// not fit the register file.
+template <int DT, int K, int N, int NW, bool BL = false, int PD = 4>
+struct StreamLayer {
+  static_assert(DT == DT_BF16, "streamed resident-interface layer: bf16");
+  using T = typename DType<DT>::T;
+  using B = typename BOperand<DT>::type;
+  static constexpr int KS = DType<DT>::KS;
+  static constexpr int KSTEPS = round_up(K, KS) / KS;
+  static constexpr int NT = N / 16;
+  static constexpr int OWN = (NT + NW - 1) / NW;
+  static constexpr int P = PD < KSTEPS ? PD : KSTEPS;  // operand sets in flight
+  static constexpr int WREGS = OWN * P * (int)(sizeof(B) / 4) + (BL ? 0 : 4 * OWN);
+  static_assert(N % 16 == 0, "layer width must be a multiple of 16");
+
+  const T* W;   // nn.Linear rows [N x K]
+  const T* Wp;  // fragment-major copy, or null
+  float bias[BL ? 1 : OWN][4];
+
+  __device__ __forceinline__ void load(const T* __restrict__ W_, const T* __restrict__ b, int wave, int lane,
+                                       const T* __restrict__ Wp_) {
+    W = W_;
+    Wp = Wp_;
+    if constexpr (!BL) {
+#pragma unroll
+      for (int o = 0; o < OWN; ++o) {
+        const int tile = wave + o * NW;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          bias[o][r] = tile < NT ? DType<DT>::to_f32(b[tile * 16 + 4 * (lane >> 4) + r]) : 0.f;
+      }
+    }
+  }
+
+  __device__ __forceinline__ void fetch(int ks, B (&dst)[OWN], int wave, int lane) const {
+#pragma unroll
+    for (int o = 0; o < OWN; ++o) {
+      const int tile = wave + o * NW;
+      const bool valid = tile < NT;
+      if (Wp != nullptr) {  // (uniform) tile t, K step s at block (t * KSTEPS + s), lane l's 16 bytes
+        dst[o] = valid ? *reinterpret_cast<const B*>(Wp + ((size_t)(tile * KSTEPS + ks) * 64 + lane) * 8)
+                       : B{0u, 0u, 0u, 0u};
+      } else {
+        const int n = tile * 16 + (lane & 15);
+        dst[o] = load_operand_global<DT, K>(W + (size_t)(valid ? n : 0) * K, K, ks, lane, valid);
+      }
+    }
+  }
+
+  // Same products and accumulation order as RegLayer::run.
+  template <int MT>
+  __device__ __forceinline__ void run(const T* in, int ld, f32x4 (&acc)[MT][OWN], int wave, int lane) const {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int o = 0; o < OWN; ++o) acc[m][o] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // (the lane index is made opaque here, so that the weight addresses are
+    // formed inside each call rather than hoisted out of the caller's step
+    // loop into registers that would stay live for the whole rollout)
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    B ring[P][OWN];
+#pragma unroll
+    for (int q = 0; q < P; ++q) fetch(q, ring[q], wave, ln);
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const B a = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks, lane);
+#pragma unroll
+        for (int o = 0; o < OWN; ++o)
+          if (NT % NW == 0 || wave + o * NW < NT) acc[m][o] = mfma16<DT>(ring[ks % P][o], a, acc[m][o]);
+      }
+      if (ks + P < KSTEPS) fetch(ks + P, ring[ks % P], wave, ln);
+    }
+  }
+
+  __device__ __forceinline__ void store_block(const f32x4& acc, T* out, int ld, int m, int o, int wave, int lane,
+                                              const float* bias_lds) const {
+    const int row = m * 16 + (lane & 15);
+    const int col = (wave + o * NW) * 16 + 4 * (lane >> 4);
+    float bo[4];
+    if constexpr (BL) {
+      const f32x4 b4 = *reinterpret_cast<const f32x4*>(bias_lds + col);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) bo[r] = b4[r];
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) bo[r] = bias[o][r];
+    }
+    float v[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] = fast_tanh(acc[r] + bo[r]);
+    const uint32_t lo = pack_bf16x2(v[0], v[1]);
+    const uint32_t hi = pack_bf16x2(v[2], v[3]);
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    *reinterpret_cast<u32x2*>(out + row * ld + col) = u32x2{lo, hi};
+  }
+
+  template <int MT>
+  __device__ __forceinline__ void store_tanh(const f32x4 (&acc)[MT][OWN], T* out, int ld, int wave, int lane,
+                                             const float* bias_lds = nullptr) const {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int o = 0; o < OWN; ++o) {
+        if (NT % NW != 0 && wave + o * NW >= NT) continue;
+        store_block(acc[m][o], out, ld, m, o, wave, lane, bias_lds);
+      }
+  }
+};
+
 // Cross-lane argmax within each 16-lane row of a wave: lexicographic max of
 // (score, -index), i.e. the first index of the largest score.  Uses DPP lane
 // permutations (no LDS traffic): swap neighbours, swap pairs, mirror each
