@@ -980,10 +980,15 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       // several the M tiles run one at a time (not unrolled) and read W3 from
       // LDS per K step, which keeps the env wave within the register budget
       // of the layers whose weights stay resident.
-      B w3r[DIRECT ? K3 : 1];
+      // (DIRECT: the W3 and h2 operands of all K steps are read before the
+      // first MFMA, each into its own registers, so the reads overlap)
+      B w3r[DIRECT ? K3 : 1], h2r[DIRECT ? K3 : 1];
       if constexpr (DIRECT) {
 #pragma unroll
-        for (int ks = 0; ks < K3; ++ks) w3r[ks] = w3s[ks * 64 + lane];
+        for (int ks = 0; ks < K3; ++ks) {
+          w3r[ks] = w3s[ks * 64 + lane];
+          h2r[ks] = load_operand_lds<DT>(h2s, LD2, lane & 15, ks, lane);
+        }
       }
 #pragma nounroll
       for (int mt = 0; mt < MT; ++mt) {
@@ -996,7 +1001,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
           // registers through the whole step)
           if constexpr (!DIRECT) asm volatile("" ::: "memory");
           acc = mfma16<DT>(DIRECT ? w3r[DIRECT ? ks : 0] : w3s[ks * 64 + lane],
-                           load_operand_lds<DT>(h2s, LD2, row, ks, lane), acc);
+                           DIRECT ? h2r[DIRECT ? ks : 0] : load_operand_lds<DT>(h2s, LD2, row, ks, lane), acc);
         }
         float best_s = -INFINITY;
         int best_a = 0;

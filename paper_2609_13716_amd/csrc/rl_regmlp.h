@@ -85,6 +85,9 @@ struct RegLayer {
   static constexpr int OWN = (NT + NW - 1) / NW;
   // VGPRs per lane that the resident operands take
   static constexpr int WREGS = OWN * KSTEPS * (int)(sizeof(B) / 4) + (BL ? 0 : 4 * OWN);
+  // operand reads in flight ahead of the MFMAs in run (fewer where the
+  // resident weights already crowd the register file)
+  static constexpr int PFMAX = BL ? 2 : 6;
   static_assert(N % 16 == 0, "layer width must be a multiple of 16");
 
   B w[OWN][KSTEPS];                 // operand of output units tile*16 + lane%16
@@ -118,16 +121,25 @@ struct RegLayer {
 #pragma unroll
       for (int o = 0; o < OWN; ++o) acc[m][o] = f32x4{0.f, 0.f, 0.f, 0.f};
     if constexpr (NT % NW == 0) {
-      // every wave owns OWN full tiles: a branch-free chain, so the compiler
-      // can issue the LDS operand loads ahead of the MFMAs
+      // every wave owns OWN full tiles: a branch-free chain.  The LDS operand
+      // of step s (K step s / MT, row tile s % MT) is read PF steps ahead of
+      // its MFMAs into a register of its own, so that the reads are in flight
+      // together; with one operand register reused, each read would wait for
+      // the MFMAs of the previous one and the chain would pay the LDS latency
+      // once per K step.
+      constexpr int STEPS = KSTEPS * MT;
+      constexpr int PF = STEPS < PFMAX ? STEPS : PFMAX;
+      B a[STEPS];
 #pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) {
+      for (int s = 0; s < PF; ++s) a[s] = load_operand_lds<DT>(in, ld, (s % MT) * 16 + (lane & 15), s / MT, lane);
+      __builtin_amdgcn_sched_barrier(0);  // (the scheduler would sink these reads below the first MFMAs)
 #pragma unroll
-        for (int m = 0; m < MT; ++m) {
-          const B a = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks, lane);
+      for (int s = 0; s < STEPS; ++s) {
+        if (s + PF < STEPS)
+          a[s + PF] = load_operand_lds<DT>(in, ld, ((s + PF) % MT) * 16 + (lane & 15), (s + PF) / MT, lane);
+        const int ks = s / MT, m = s % MT;
 #pragma unroll
-          for (int o = 0; o < OWN; ++o) acc[m][o] = mfma16<DT>(w[o][ks], a, acc[m][o]);
-        }
+        for (int o = 0; o < OWN; ++o) acc[m][o] = mfma16<DT>(w[o][ks], a[s], acc[m][o]);
       }
     } else {
 #pragma unroll
