@@ -873,8 +873,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       bias_s[i] = DType<DT>::to_f32(i < H1 ? static_cast<const T*>(pol.b[0])[i] : static_cast<const T*>(pol.b[1])[i - H1]);
   }
   if constexpr (S1)
-    L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane,
-            static_cast<const T*>(pol.Wp[0]));
+    L1.load(static_cast<const T*>(pol.b[0]), wave, lane, static_cast<const T*>(pol.Wp[0]));
   else
     L1.load(static_cast<const T*>(pol.W[0]), static_cast<const T*>(pol.b[0]), wave, lane);
   L2.load(static_cast<const T*>(pol.W[1]), static_cast<const T*>(pol.b[1]), wave, lane);
@@ -1194,9 +1193,15 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
   RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1, 0)
   RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2, 0)
   if (pol.dt == DT_BF16 && p.H == 12 && p.W == 12 && pol.H1 == 256 && pol.H2 == 256 && p.A == 3 && p.F == 6 &&
-      !pol.VH && !tm) {  // layer 1 (432 x 256) streamed: both layers resident would spill
-    *err = launch_rollout_reg<DT_BF16, 12, 12, 256, 256, 3, 6, 16, 8, 1, false, false, true>(p, m, pol, state, t0,
-                                                                                          n_steps, out, s);
+      !pol.VH && !tm) {
+    // layer 1 (432 x 256) streamed from the packed copy: both layers resident
+    // spill; without a packed copy they stay resident all the same
+    if (pol.Wp[0] != nullptr)
+      *err = launch_rollout_reg<DT_BF16, 12, 12, 256, 256, 3, 6, 16, 8, 1, false, false, true>(p, m, pol, state, t0,
+                                                                                            n_steps, out, s);
+    else
+      *err = launch_rollout_reg<DT_BF16, 12, 12, 256, 256, 3, 6, 16, 8, 1, false, false, false>(p, m, pol, state, t0,
+                                                                                             n_steps, out, s);
     return true;
   }
   RL_REG_CASE(DT_BF16, 7, 7, 128, 128, 2, 3, 8, 4, 2, 0)

@@ -234,10 +234,10 @@ struct RegLayer {
 // A bf16 layer with the same interface, MFMA chains and outputs as RegLayer
 // whose weights are streamed instead of held: each K step's B operands of the
 // wave's tiles are read from global memory (L2) PD steps ahead of their MFMAs,
-// from the fragment-major packed copy when there is one (one contiguous 1 KB
-// block per wave-wide load) or else from the nn.Linear rows.  It holds PD
-// operand sets instead of all KSTEPS, for shapes whose resident weights would
-// not fit the register file.
+// from the fragment-major packed copy (one contiguous 1 KB block per
+// wave-wide load; the caller must supply it).  It holds PD operand sets
+// instead of all KSTEPS, for shapes whose resident weights would not fit the
+// register file.
 template <int DT, int K, int N, int NW, bool BL = false, int PD = 4>
 struct StreamLayer {
   static_assert(DT == DT_BF16, "streamed resident-interface layer: bf16");
@@ -251,13 +251,10 @@ struct StreamLayer {
   static constexpr int WREGS = OWN * P * (int)(sizeof(B) / 4) + (BL ? 0 : 4 * OWN);
   static_assert(N % 16 == 0, "layer width must be a multiple of 16");
 
-  const T* W;   // nn.Linear rows [N x K]
-  const T* Wp;  // fragment-major copy, or null
+  const T* Wp;  // fragment-major copy (rl_policy_pack layout)
   float bias[BL ? 1 : OWN][4];
 
-  __device__ __forceinline__ void load(const T* __restrict__ W_, const T* __restrict__ b, int wave, int lane,
-                                       const T* __restrict__ Wp_) {
-    W = W_;
+  __device__ __forceinline__ void load(const T* __restrict__ b, int wave, int lane, const T* __restrict__ Wp_) {
     Wp = Wp_;
     if constexpr (!BL) {
 #pragma unroll
@@ -274,14 +271,9 @@ struct StreamLayer {
 #pragma unroll
     for (int o = 0; o < OWN; ++o) {
       const int tile = wave + o * NW;
-      const bool valid = tile < NT;
-      if (Wp != nullptr) {  // (uniform) tile t, K step s at block (t * KSTEPS + s), lane l's 16 bytes
-        dst[o] = valid ? *reinterpret_cast<const B*>(Wp + ((size_t)(tile * KSTEPS + ks) * 64 + lane) * 8)
-                       : B{0u, 0u, 0u, 0u};
-      } else {
-        const int n = tile * 16 + (lane & 15);
-        dst[o] = load_operand_global<DT, K>(W + (size_t)(valid ? n : 0) * K, K, ks, lane, valid);
-      }
+      // tile t, K step s at block (t * KSTEPS + s), lane l's 16 bytes
+      dst[o] = tile < NT ? *reinterpret_cast<const B*>(Wp + ((size_t)(tile * KSTEPS + ks) * 64 + lane) * 8)
+                         : B{0u, 0u, 0u, 0u};
     }
   }
 
@@ -300,14 +292,24 @@ struct StreamLayer {
     B ring[P][OWN];
 #pragma unroll
     for (int q = 0; q < P; ++q) fetch(q, ring[q], wave, ln);
+    // the LDS operands of K step ks + 1 are read while the MFMAs of step ks
+    // run (two register sets), so each step does not wait out an LDS latency
+    B a[2][MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) a[0][m] = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), 0, lane);
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
+      if (ks + 1 < KSTEPS) {
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+          a[(ks + 1) & 1][m] = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks + 1, lane);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // (keeps those reads ahead of this step's MFMAs)
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
-        const B a = load_operand_lds<DT>(in, ld, m * 16 + (lane & 15), ks, lane);
 #pragma unroll
         for (int o = 0; o < OWN; ++o)
-          if (NT % NW == 0 || wave + o * NW < NT) acc[m][o] = mfma16<DT>(ring[ks % P][o], a, acc[m][o]);
+          if (NT % NW == 0 || wave + o * NW < NT) acc[m][o] = mfma16<DT>(ring[ks % P][o], a[ks & 1][m], acc[m][o]);
       }
       if (ks + P < KSTEPS) fetch(ks + P, ring[ks % P], wave, ln);
     }

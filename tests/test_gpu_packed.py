@@ -3,9 +3,10 @@
 * The packed buffer equals a copy built on the host from the documented layout (tile t, K step s,
   lane l: W[16t + l % 16][32s + 8(l // 16) + j], zero outside W), byte for byte, for shapes with
   ragged rows and a partial last K step.
-* Rollouts that read the packed copy (kitchen and Hanabi rollouts) are bit-identical to the same
-  rollouts reading W in the nn.Linear layout: observations, actions, logits, rewards, dones and the
-  final state.  (Parity of the packed path against the oracle is covered by the kitchen and Hanabi
+* Rollouts that read the packed copy (kitchen and Hanabi rollouts, and the 12x12 LBF rollout, whose
+  layer 1 streams from the packed copy while without one both layers stay in registers) are
+  bit-identical to the same rollouts reading W in the nn.Linear layout: observations, actions,
+  logits, rewards, dones and the final state.  (Parity of the packed path against the oracle is covered by the kitchen and Hanabi
   rollout tests, whose bf16 policies are packed by default.)
 """
 
@@ -74,12 +75,15 @@ def _run(cfg, pol, T):
 
 @pytest.mark.parametrize("env,dims", [("hanabi", (658, 512, 512, 20)), ("hanabi", (658, 64, 96, 20)),
                                       ("hanabi_mini", (278, 128, 128, 16)), ("overcooked", (1170, 256, 256, 6)),
-                                      ("overcooked", (1170, 64, 48, 6))])
+                                      ("overcooked", (1170, 64, 48, 6)), ("lbf12", (432, 256, 256, 6))])
 def test_packed_rollout_equals_unpacked(env, dims):
     require_gpu()
     _note(f"packed vs unpacked rollout {env} {dims}")
     E, T = 37, 30
-    if env == "hanabi":
+    if env == "lbf12":  # (three workgroups of 16 envs, the last ragged; episodes of 50 steps cross resets)
+        E, T = 37, 60
+        cfg = R.EnvConfig(n_envs=E, seed=3, **workloads.WORKLOADS["lbf12_16k"]["env"])
+    elif env == "hanabi":
         cfg = R.hanabi_config(E, seed=3)
     elif env == "hanabi_mini":
         cfg = R.hanabi_config(E, colours=3, ranks=3, seed=3)
