@@ -139,6 +139,86 @@ __device__ __forceinline__ void hn_write_obs(const uint64_t* rows, int nrows, OT
   }
 }
 
+// The flat bit layout of a tile's observation rows: row r's feature f is bit
+// r * G::OBS + f of one bit array (64-bit words), so that the 8 features of
+// an output vector of 8 bf16 (or the 4 of a vector of 4 float32) are one
+// byte (one nibble) of it when a wave's first row starts on a byte.  The
+// expansion table maps such a byte (nibble) to the vector's 16 bytes of 0 / 1
+// values.
+template <typename OT>
+struct HnExpand {
+  static constexpr int N = sizeof(OT) == 2 ? 256 : 16;  // table entries
+  __device__ static u32x4 entry(uint32_t i) {
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if constexpr (sizeof(OT) == 2)
+        w[q] = (((i >> (2 * q)) & 1u) ? 0x3f80u : 0u) | (((i >> (2 * q + 1)) & 1u) ? 0x3f800000u : 0u);
+      else
+        w[q] = ((i >> q) & 1u) ? 0x3f800000u : 0u;
+    }
+    return u32x4{w[0], w[1], w[2], w[3]};
+  }
+};
+
+// Write a tile's `total` observation features, held in the flat layout
+// (from bit 0 of `bytes`), to consecutive global elements from `dst` as
+// 0 / 1 values, and clear the bytes written out.  Wave w of the NW taking
+// part writes its share, a contiguous run of whole 16-byte vectors (or of
+// 4-byte words when `dst` is not 16-byte aligned or `total` is not a whole
+// number of vectors) that starts and ends on a byte of the bit array, so no
+// two waves clear the same byte.  Per vector: one LDS byte (or nibble) read
+// and one table read, in batches of up to eight whose reads are all issued
+// before their stores.
+template <class G, typename OT, int MAXF, int NW>
+__device__ __forceinline__ void hn_write_flat(uint8_t* bytes, int total, OT* __restrict__ dst, int w, int lane,
+                                              const u32x4* lut) {
+  constexpr int VE = 16 / sizeof(OT), WE = 4 / sizeof(OT);  // features per 16-byte vector, per word
+  static_assert(G::OBS % 2 == 0, "rows of whole 4-byte words");
+  if ((reinterpret_cast<uintptr_t>(dst) & 15) == 0 && total % VE == 0) {
+    constexpr int VB = 8 / VE;                                   // vectors per byte of bits
+    constexpr int CMAX = ((MAXF / VE + NW - 1) / NW + VB - 1) / VB * VB;
+    constexpr int IT = (CMAX + 63) / 64, B = IT < 8 ? IT : 8;  // vectors per lane, per batch
+    const int nv = total / VE, c = ((nv + NW - 1) / NW + VB - 1) / VB * VB;
+    const int v0 = min(nv, w * c), v1 = min(nv, v0 + c);
+    u32x4* g4 = reinterpret_cast<u32x4*>(dst);
+#pragma unroll
+    for (int i0 = 0; i0 < IT; i0 += B) {
+      uint32_t b[B];
+#pragma unroll
+      for (int it = 0; it < B; ++it) {
+        const int v = max(0, min(v0 + lane + 64 * (i0 + it), v1 - 1));
+        if constexpr (VE == 8)
+          b[it] = bytes[v];
+        else
+          b[it] = ((uint32_t)bytes[v >> 1] >> (4 * (v & 1))) & 15u;
+      }
+      u32x4 val[B];
+#pragma unroll
+      for (int it = 0; it < B; ++it) val[it] = lut[b[it]];
+#pragma unroll
+      for (int it = 0; it < B; ++it) {
+        const int v = v0 + lane + 64 * (i0 + it);
+        if (i0 + it < IT && v < v1) g4[v] = val[it];
+      }
+    }
+    wave_lds_sync();
+    for (int j = v0 / VB + lane; j < (v1 + VB - 1) / VB; j += 64) bytes[j] = 0;
+  } else {
+    constexpr int WB = 8 / WE;  // words per byte of bits
+    const int nw = total / WE, c = ((nw + NW - 1) / NW + WB - 1) / WB * WB;
+    const int w0 = min(nw, w * c), w1 = min(nw, w0 + c);
+    uint32_t* g = reinterpret_cast<uint32_t*>(dst);
+    for (int x = w0 + lane; x < w1; x += 64) {
+      const int f = x * WE;  // first feature of the word (its bits never straddle a byte)
+      const uint32_t bb = ((uint32_t)bytes[f >> 3] >> (f & 7)) & ((1u << WE) - 1u);
+      g[x] = lut[bb][0];  // (entry bb's first word holds features 0 .. WE-1 of bb)
+    }
+    wave_lds_sync();
+    for (int j = w0 / WB + lane; j < (w1 + WB - 1) / WB; j += 64) bytes[j] = 0;
+  }
+}
+
 // Paint the mover's observation of envs 0..te_valid-1 (bit-vector row
 // 2 el + cur, rows as in hn_build_bits) into row el of the layer-1 operand
 // tile as 0 / 1 values, 16 bytes (VE features) per store, by all NT threads.
@@ -273,12 +353,14 @@ __global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(s
                                                                 int n_steps, const int32_t* __restrict__ actions,
                                                                 OT* __restrict__ obs, float* __restrict__ reward,
                                                                 uint8_t* __restrict__ done, uint8_t* __restrict__ legal) {
-  static_assert(TE <= 64 && (2 * TE) % OW == 0, "one env wave; whole rows per observation wave");
-  constexpr int RB = 2 * TE, RPW = RB / OW;                      // rows per workgroup, per observation wave
+  static_assert(TE <= 64, "one env wave");
+  constexpr int RB = 2 * TE;                                     // rows per workgroup
   constexpr int NPASS = (RB * G::NFIELDS + 63) / 64;            // field passes per move
   constexpr int LPW = (TE + OW - 1) / OW;                        // envs whose legal masks a wave writes
+  constexpr int FW = (RB * G::OBS + 63) / 64;                    // words of a move's flat bit array
   __shared__ HnTile snap[2][TE];
-  __shared__ __align__(16) uint64_t rows[2][RB * HN_OBS_WORDS];
+  __shared__ __align__(16) uint64_t rows[2][FW];                 // move k's rows, flat, in rows[k % 2]
+  __shared__ u32x4 lut[HnExpand<OT>::N];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, ow = wave - 1;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
   const bool envlane = wave == 0 && lane < te_valid;
@@ -293,6 +375,10 @@ __global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(s
     }
   }
   zero_lds<64 * (OW + 1)>(rows, sizeof(rows), tid);  // the bit vectors start clear
+  for (int j = tid; j < HnExpand<OT>::N; j += 64 * (OW + 1)) lut[j] = HnExpand<OT>::entry((uint32_t)j);
+  // the env wave's serial chain sets the pace: it goes first when the waves
+  // sharing its SIMD are ready to issue too
+  if (wave == 0) __builtin_amdgcn_s_setprio(3);
   RL_STAMP_BEGIN
   for (int i = 0; i < n_steps + 2; ++i) {
     if (wave == 0) {
@@ -339,8 +425,8 @@ __global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(s
             int off;
             const uint64_t v = hn_field_bits<G>(sn[r >> 1].pub, r & 1, f, off);
             if (v) {
-              unsigned long long* w = reinterpret_cast<unsigned long long*>(rw + r * HN_OBS_WORDS);
-              const int wi = off >> 6, sh = off & 63;
+              unsigned long long* w = reinterpret_cast<unsigned long long*>(rw);
+              const int b = r * G::OBS + off, wi = b >> 6, sh = b & 63;
               atomicOr(w + wi, (unsigned long long)(v << sh));
               if (sh && (v >> (64 - sh))) atomicOr(w + wi + 1, (unsigned long long)(v >> (64 - sh)));
             }
@@ -353,14 +439,10 @@ __global__ __launch_bounds__(64 * (OW + 1)) __attribute__((amdgpu_waves_per_eu(s
         }
       }
       RL_STAMP(5)
-      if (obs && i >= 2) {  // write out and clear this wave's rows of move i - 2
-        const int k = i - 2, r0 = ow * RPW, nr = max(0, min(RPW, 2 * te_valid - r0));
-        uint64_t* rw = rows[k & 1] + r0 * HN_OBS_WORDS;
-        if (nr > 0) {
-          hn_write_obs<G, OT, RPW>(rw, nr, obs + (((size_t)k * E + e0) * 2 + r0) * G::OBS, lane);
-          wave_lds_sync();
-          for (int j = lane; j < nr * HN_OBS_WORDS; j += 64) rw[j] = 0;
-        }
+      if (obs && i >= 2) {  // write out and clear this wave's share of the rows of move i - 2
+        const int k = i - 2;
+        hn_write_flat<G, OT, RB * G::OBS, OW>(reinterpret_cast<uint8_t*>(rows[k & 1]), 2 * te_valid * G::OBS,
+                                              obs + ((size_t)k * E + e0) * 2 * G::OBS, ow, lane, lut);
       }
     }
     RL_STAMP(6)
@@ -561,18 +643,20 @@ static hipError_t launch_hn_init_g(const HnParams& p, int32_t* state, void* obs,
 }
 
 constexpr int HN_STEP_TE = 4;  // envs per workgroup of the env-only kernel
-constexpr int HN_STEP_OW = 2;  // its observation waves
+// its observation waves: three for bf16 (four waves of at most 128 VGPRs, four
+// workgroups per CU), two for float32 (whose kernel needs more registers)
+constexpr int HN_STEP_OW_BF16 = 3, HN_STEP_OW_F32 = 2;
 
 template <class G>
 static hipError_t launch_hn_step_g(const HnParams& p, int32_t* state, uint64_t t0, int n_steps,
                                    const int32_t* actions, void* obs, int obs_dt, float* reward, uint8_t* done,
                                    uint8_t* legal, hipStream_t s) {
-  constexpr int TE = HN_STEP_TE, OW = HN_STEP_OW;
+  constexpr int TE = HN_STEP_TE, OWF = HN_STEP_OW_F32, OWB = HN_STEP_OW_BF16;
   if (obs_dt == DT_F32)
-    hn_env_kernel<G, float, TE, OW><<<hn_tiles(p.E, TE), 64 * (OW + 1), 0, s>>>(
+    hn_env_kernel<G, float, TE, OWF><<<hn_tiles(p.E, TE), 64 * (OWF + 1), 0, s>>>(
         p, state, t0, n_steps, actions, static_cast<float*>(obs), reward, done, legal);
   else
-    hn_env_kernel<G, uint16_t, TE, OW><<<hn_tiles(p.E, TE), 64 * (OW + 1), 0, s>>>(
+    hn_env_kernel<G, uint16_t, TE, OWB><<<hn_tiles(p.E, TE), 64 * (OWB + 1), 0, s>>>(
         p, state, t0, n_steps, actions, static_cast<uint16_t*>(obs), reward, done, legal);
   return hipGetLastError();
 }

@@ -916,6 +916,9 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   }
   // Let the prologue loads land here, once (see lbf_env_kernel).
   __builtin_amdgcn_s_waitcnt(0);
+  // the env wave's serial section sets the pace: it goes first when the waves
+  // sharing its SIMD are ready to issue too
+  if (wave == ew) __builtin_amdgcn_s_setprio(3);
 
   RL_STAMP_BEGIN
   for (int k = 0; k < n_steps; ++k) {
@@ -1623,6 +1626,7 @@ __global__ __launch_bounds__(64 * (NCW + 1)) void lbf_env_kernel(LbfParams p, in
   stage_actions<TE * A, NT>(actions, E, e0, te_valid * A, A, 0, min(CH, n_steps), act_lds[0], tid);
   LbfEnv s{};
   if (grplane) lbf_load<A, F>(state, p, e, s);
+  if (wave == 0) __builtin_amdgcn_s_setprio(3);  // (the env wave's chain sets the pace)
   for (int k0 = 0; k0 < n_steps; k0 += CH) {
     const int nk = min(CH, n_steps - k0);
     const int32_t* acts = act_lds[(k0 / CH) & 1];
@@ -1764,6 +1768,7 @@ __global__ __launch_bounds__(192) void lbf_env3_kernel(LbfParams p, int32_t* __r
   if (wave == 2) build_resets(0, RS);
   LbfEnv s{};
   if (envlane) lbf_load<A, F>(state, p, e, s);
+  if (wave == 0) __builtin_amdgcn_s_setprio(3);  // (the transition wave's chain sets the pace)
   for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
     const int nk = min(ACT_CHUNK, n_steps - k0);
     stage_actions<TE * A, 192>(actions, E, e0, te_valid * A, A, k0, nk, act_lds, tid);
