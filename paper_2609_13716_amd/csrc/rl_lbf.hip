@@ -1605,7 +1605,10 @@ __global__ __launch_bounds__(64 * (NCW + 1)) void lbf_env_kernel(LbfParams p, in
   static_assert(TE * G <= 64 && TE * nblk <= 64, "env lanes in wave 0, and one lane per reset block");
   constexpr int CH = ACT_CHUNK;
   static_assert(CH % S == 0, "barrier groups of S steps do not straddle action chunks");
-  __shared__ __align__(16) OT xs[2][S][R * D];      // o_{t+1} of step k in xs[(k / S) % 2][k % S]
+  static_assert(R % NCW == 0, "whole rows per copy wave");
+  constexpr int RW = R / NCW, NSLOT = A + F + 1;    // rows per copy wave; non-zero features per row
+  __shared__ __align__(16) OT xs[S][R * D];         // o_{t+1} of a step, painted and copied by the copy waves
+  __shared__ LbfEnv pub[2][S][TE];                  // post-step state of step k in pub[(k / S) % 2][k % S]
   __shared__ int32_t act_lds[2][CH * TE * A];      // actions of chunk c in act_lds[c % 2]
   __shared__ uint32_t rdraw[TE * LBF_MAX_DRAWS];   // reset draws of the envs that ended
   __shared__ float rw_s[2][S][TE];                 // reward and done of step k, as its tile
@@ -1674,20 +1677,43 @@ __global__ __launch_bounds__(64 * (NCW + 1)) void lbf_env_kernel(LbfParams p, in
             }
           }
           if (envlane) {
-            if (obs) lbf_paint_tile<OT, A, F>(s, el, xs[pr][u], D, HW, true);
+            if (obs) lbf_copy<A, F>(pub[pr][u][el], s);
             rw_s[pr][u][el] = r;
             dn_s[pr][u][el] = d;
           }
         }
       }
-      __syncthreads();  // these steps painted and published (and the previous ones copied and cleared)
+      __syncthreads();  // these steps published (and the previous ones copied out)
       if (wave != 0) {
         const int ct = tid - 64;  // 0 .. NC-1
+        const int r0 = (wave - 1) * RW, live = max(0, min(RW, te_valid * A - r0));  // this wave's rows
         for (int u = 0; u < ns; ++u) {
           const int k = k0 + kb + u;
-          if (obs)
-            copy_obs_rows<OT, R, D, D, NC, true, GC>(xs[pr][u], obs + ((size_t)k * E + e0) * A * D, te_valid * A,
-                                                     ct);
+          if (obs && live > 0) {
+            // paint the wave's rows of o_{t+1} from the published states, one
+            // non-zero feature per lane (the tile is blank: the copy clears it)
+            OT* tile = xs[u] + r0 * D;
+            for (int it = lane; it < live * NSLOT; it += 64) {
+              const int rl = it / NSLOT, c = it - rl * NSLOT, row = r0 + rl, en = row / A, i = row - en * A;
+              const LbfEnv& st = pub[pr][u][en];
+              int cell, plane;
+              uint32_t v;
+              if (c < A) {
+                cell = st.acell[c], plane = 0, v = (uint32_t)st.alevel[c];
+              } else if (c < A + F) {
+                const int j = c - A;
+                cell = st.fcell[j], plane = 1, v = ((st.eaten >> j) & 1u) ? 0u : (uint32_t)st.flevel[j];
+              } else {
+                cell = st.acell[i], plane = 2, v = 1u;
+              }
+              // (cells clamped into the grid: a malformed state cannot address outside the row)
+              if (v) tile[rl * D + plane * HW + min((uint32_t)cell, (uint32_t)HW - 1u)] = small_int_to<OT>(v);
+            }
+            wave_lds_sync();
+            copy_obs_rows<OT, RW, D, D, 64, true, GC>(tile, obs + ((size_t)k * E + e0) * A * D + (size_t)r0 * D,
+                                                      live, lane);
+            wave_lds_sync();
+          }
           if (ct < te_valid) {
             if (reward) reward[(size_t)k * E + e0 + ct] = rw_s[pr][u][ct];
             if (done) done[(size_t)k * E + e0 + ct] = (uint8_t)dn_s[pr][u][ct];
@@ -1828,7 +1854,7 @@ static hipError_t launch_env_ct(const LbfParams& p, int32_t* state, uint64_t t0,
   } else {
     constexpr int NCW = 2;
     constexpr size_t TILE = (size_t)TE * A * 3 * GH * GW * sizeof(OT);
-    constexpr int S = 4 * TILE <= MAX_LDS_BYTES / 4 ? 2 : 1;
+    constexpr int S = 4 * TILE <= MAX_LDS_BYTES / 4 ? 4 : 2 * TILE <= MAX_LDS_BYTES / 4 ? 2 : 1;
     lbf_env_kernel<OT, GH, GW, A, F, TE, NCW, S><<<dim3((unsigned)((p.E + TE - 1) / TE)), 64 * (NCW + 1), 0, s>>>(
         p, state, t0, n_steps, actions, static_cast<OT*>(obs), reward, done, legal);
   }
