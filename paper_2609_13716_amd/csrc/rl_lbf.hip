@@ -982,29 +982,39 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
       // several the M tiles run one at a time (not unrolled) and read W3 from
       // LDS per K step, which keeps the env wave within the register budget
       // of the layers whose weights stay resident.
-      // (DIRECT: the W3 and h2 operands of all K steps are read before the
-      // first MFMA, each into its own registers, so the reads overlap)
-      B w3r[DIRECT ? K3 : 1], h2r[DIRECT ? K3 : 1];
-      if constexpr (DIRECT) {
+      // Layer 3 of every M tile: the K steps run in order over all M tiles at
+      // once (one W3 operand serves every tile), their LDS operands read PF3
+      // K steps ahead of the MFMAs that use them, each into its own registers,
+      // so the chains do not wait out an LDS latency per K step.  (The lane
+      // index is made opaque here so that the W3 reads are not hoisted out of
+      // the step loop into registers held through the whole step.)
+      f32x4 acc3[MT];
+      {
+        constexpr int PF3 = K3 < 4 ? K3 : MT > 2 ? 2 : 4;  // (fewer where three M tiles crowd the registers)
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        B wq[PF3], hq[PF3][MT];
+        auto fetch3 = [&](int ks, int q) {
+          wq[q] = w3s[ks * 64 + ln];
+#pragma unroll
+          for (int m = 0; m < MT; ++m) hq[q][m] = load_operand_lds<DT>(h2s, LD2, m * 16 + (ln & 15), ks, ln);
+        };
+#pragma unroll
+        for (int m = 0; m < MT; ++m) acc3[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < PF3; ++q) fetch3(q, q);
 #pragma unroll
         for (int ks = 0; ks < K3; ++ks) {
-          w3r[ks] = w3s[ks * 64 + lane];
-          h2r[ks] = load_operand_lds<DT>(h2s, LD2, lane & 15, ks, lane);
+#pragma unroll
+          for (int m = 0; m < MT; ++m) acc3[m] = mfma16<DT>(wq[ks % PF3], hq[ks % PF3][m], acc3[m]);
+          if (ks + PF3 < K3) fetch3(ks + PF3, ks % PF3);
         }
       }
-#pragma nounroll
+#pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int row = mt * 16 + (lane & 15);
         const f32x4 nz4 = *reinterpret_cast<const f32x4*>(&nz[k & 1][row * 8 + 4 * (g & 1)]);
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < K3; ++ks) {
-          // (keeps the W3 loads in the loop: hoisted out of it they would hold
-          // registers through the whole step)
-          if constexpr (!DIRECT) asm volatile("" ::: "memory");
-          acc = mfma16<DT>(DIRECT ? w3r[DIRECT ? ks : 0] : w3s[ks * 64 + lane],
-                           DIRECT ? h2r[DIRECT ? ks : 0] : load_operand_lds<DT>(h2s, LD2, row, ks, lane), acc);
-        }
+        const f32x4 acc = acc3[mt];
         float best_s = -INFINITY;
         int best_a = 0;
         float logit[4];
