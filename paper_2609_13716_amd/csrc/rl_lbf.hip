@@ -661,7 +661,41 @@ template <typename T, int R, int D, int LDX, int NT, bool CLEAR = false, int G =
 __device__ __forceinline__ void copy_obs_rows(T* xs, T* __restrict__ g, int rows_live, int tid) {
   constexpr int VE = 16 / sizeof(T);
   static_assert(AMT == 0 || D % VE == 0, "agent-major tiles need whole-vector rows");
-  if constexpr (D % VE != 0) {
+  if constexpr (D % VE != 0 && LDX == D) {
+    // Rows that are not whole vectors, unpadded in LDS as in global memory:
+    // the tile is one contiguous block of R * D elements, copied as 16-byte
+    // vectors; the vector that ends the live rows goes element by element.
+    static_assert((R * D) % VE == 0, "the tile must be whole 16-byte vectors");
+    constexpr int NV = R * D / VE;
+    constexpr int IT = (NV + NT - 1) / NT;
+    const int nlive = rows_live * D;
+#pragma unroll
+    for (int i0 = 0; i0 < IT; i0 += G) {
+      u32x4 val[G];
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const int v = tid + (i0 + j) * NT;
+        if (i0 + j < IT && (NV % NT == 0 || v < NV)) val[j] = *reinterpret_cast<const u32x4*>(xs + v * VE);
+      }
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const int v = tid + (i0 + j) * NT, e0 = v * VE;
+        if (i0 + j < IT && (NV % NT == 0 || v < NV) && e0 < nlive) {
+          if (g) {
+            if (e0 + VE <= nlive) {
+              *reinterpret_cast<u32x4*>(g + e0) = val[j];
+            } else {
+#pragma unroll
+              for (int q = 0; q < VE; ++q)
+                if (e0 + q < nlive) g[e0 + q] = xs[e0 + q];
+            }
+          }
+          if constexpr (CLEAR) *reinterpret_cast<u32x4*>(xs + e0) = u32x4{0u, 0u, 0u, 0u};
+        }
+      }
+    }
+    return;
+  } else if constexpr (D % VE != 0) {
     // Rows that are not whole vectors (e.g. the 7x7 grid's 147 features): the
     // tile's rows are contiguous in global memory, so the tile goes out as
     // R * D elements in 16-byte vectors, each gathered element by element
