@@ -82,7 +82,8 @@ __device__ __forceinline__ void hn_paint(HnTile* envs, int te_valid, T* tile, in
 // aligned, or a total that is not a whole number of vectors, go one 4-byte
 // word at a time.
 template <class G, typename OT, int MAXROWS>
-__device__ __forceinline__ void hn_write_obs(const uint64_t* rows, int nrows, OT* __restrict__ dst, int lane) {
+__device__ __forceinline__ void hn_write_obs(const uint64_t* rows, int nrows, OT* __restrict__ dst, int lane,
+                                             const u32x4* lut) {
   constexpr int VE = 16 / sizeof(OT), WE = 4 / sizeof(OT);  // features per 16-byte vector, per word
   const uint32_t one = sizeof(OT) == 2 ? 0x3f80u : 0x3f800000u;  // 1.0 in OT
   auto word = [&](uint32_t b, int q) -> uint32_t {  // output word q of a vector with feature bits b
@@ -120,13 +121,13 @@ __device__ __forceinline__ void hn_write_obs(const uint64_t* rows, int nrows, OT
       uint32_t lo[B], hi[B], nx[B];
 #pragma unroll
       for (int it = 0; it < B; ++it) load(min(lane + 64 * (i0 + it), nv - 1) * VE, lo[it], hi[it], nx[it]);
+      u32x4 val[B];  // the vectors' 16 bytes from the expansion table
+#pragma unroll
+      for (int it = 0; it < B; ++it) val[it] = lut[bits(min(lane + 64 * (i0 + it), nv - 1) * VE, VE, lo[it], hi[it], nx[it])];
 #pragma unroll
       for (int it = 0; it < B; ++it) {
         const int v = lane + 64 * (i0 + it);
-        if (i0 + it < IT && v < nv) {
-          const uint32_t b = bits(v * VE, VE, lo[it], hi[it], nx[it]);
-          g4[v] = u32x4{word(b, 0), word(b, 1), word(b, 2), word(b, 3)};
-        }
+        if (i0 + it < IT && v < nv) g4[v] = val[it];
       }
     }
   } else {
@@ -460,7 +461,7 @@ constexpr int HN_RUN_NT = 512;  // 8 waves: the MLP's weight-streaming chains of
 
 struct HnRunLayout {
   int ldx, ld1, ld2;
-  size_t off_x, off_h1, off_h2, off_lg, off_sc, off_env, off_words, off_need, off_bits, total;
+  size_t off_x, off_h1, off_h2, off_lg, off_sc, off_env, off_words, off_need, off_bits, off_lut, total;
 };
 
 __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int obs) {
@@ -481,6 +482,7 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int
   L.off_need = o;  o += (size_t)(HN_RUN_TE + 1) * 4;
   o = (o + 15) & ~(size_t)15;
   L.off_bits = o;  o += (size_t)2 * HN_RUN_TE * HN_OBS_WORDS * 8;
+  L.off_lut = o;   o += (size_t)HnExpand<uint16_t>::N * 16;  // (the larger expansion table)
   L.total = o;
   return L;
 }
@@ -504,6 +506,7 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
   uint32_t(*words)[HN_DECK_WORDS] = reinterpret_cast<uint32_t(*)[HN_DECK_WORDS]>(smem + L.off_words);
   uint32_t* need = reinterpret_cast<uint32_t*>(smem + L.off_need);
   uint64_t* bits = reinterpret_cast<uint64_t*>(smem + L.off_bits);  // the observation bit vectors, row by row
+  u32x4* lut = reinterpret_cast<u32x4*>(smem + L.off_lut);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
@@ -516,7 +519,8 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
   const T* Wp1 = static_cast<const T*>(pol.Wp[0]);
   const T* Wp2 = static_cast<const T*>(pol.Wp[1]);
   const T* Wp3 = static_cast<const T*>(pol.Wp[2]);
-  zero_lds<HN_RUN_NT>(smem, L.total, tid);
+  zero_lds<HN_RUN_NT>(smem, L.off_lut, tid);  // (all but the expansion table, which is written here)
+  for (int j = tid; j < HnExpand<T>::N; j += HN_RUN_NT) lut[j] = HnExpand<T>::entry((uint32_t)j);
   __syncthreads();
   const bool envlane = tid < te_valid;
   const int e = e0 + tid;
@@ -568,7 +572,8 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
       uint64_t* rw = bits + r0 * HN_OBS_WORDS;
       if (nr > 0) {
         if (out.obs)
-          hn_write_obs<G, T, RPW>(rw, nr, static_cast<T*>(out.obs) + (((size_t)k * E + e0) * 2 + r0) * G::OBS, lane);
+          hn_write_obs<G, T, RPW>(rw, nr, static_cast<T*>(out.obs) + (((size_t)k * E + e0) * 2 + r0) * G::OBS, lane,
+                                  lut);
         wave_lds_sync();
         for (int j = lane; j < nr * HN_OBS_WORDS; j += 64) rw[j] = 0;
       }
@@ -619,7 +624,7 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
     const int r0 = wave * RPW, nr = max(0, min(RPW, 2 * te_valid - r0));
     if (nr > 0)
       hn_write_obs<G, T, RPW>(bits + r0 * HN_OBS_WORDS, nr, static_cast<T*>(out.obs_last) + ((size_t)e0 * 2 + r0) * G::OBS,
-                              lane);
+                              lane, lut);
   }
   if (envlane) hn_store(state, E, e, s);
 }
