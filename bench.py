@@ -16,6 +16,7 @@ Prints one JSON line.
 import argparse
 import glob
 import hashlib
+import re
 import json
 import os
 import sys
@@ -60,14 +61,17 @@ def parse():
 
 
 def csrc_hash():
-    """Hash of every kernel source and of the workload definitions: hardware counters taken on the
-    benchmark's kernels stay valid while these files are unchanged."""
+    """Hash of every kernel source (comments removed) and of the workload definitions: hardware counters
+    taken on the benchmark's kernels stay valid while their code is unchanged."""
     h = hashlib.sha256()
     files = sorted(glob.glob(os.path.join(ROOT, "paper_2609_13716_amd", "csrc", "*")))
     files.append(os.path.join(ROOT, "paper_2609_13716_amd", "workloads.py"))
     for f in files:
         h.update(os.path.basename(f).encode())
-        h.update(open(f, "rb").read())
+        text = open(f, encoding="utf-8").read()
+        if not f.endswith(".py"):  # C++/HIP: drop // and /* */ comments
+            text = re.sub(r"/\*.*?\*/|//[^\n]*", "", text, flags=re.S)
+        h.update(text.encode())
     return h.hexdigest()[:16]
 
 
@@ -750,7 +754,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the rollout shards over GPUs "
-              "by env id with no exchange, and this build times the single-GPU shard.", file=sys.stderr)
+              "by env id with no exchange, and this benchmark times the single-GPU shard.", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch

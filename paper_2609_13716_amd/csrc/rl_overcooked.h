@@ -3,7 +3,7 @@
 //
 // The kitchen is an environment of Section 4 (environment table), run as the
 // Dec-POMDP step of Section 3; its dynamics, the synthetic layout generator
-// and the observation are this build's readings, documented in
+// and the observation are readings of the paper's description, documented in
 // include/rollout.h.  A kitchen lives on a fixed 5 x 9 canvas (cell id =
 // row * 9 + col); every cell set is a 45-bit mask, so neighbourhoods,
 // connectivity and "the k-th free cell" are a few 64-bit operations.
