@@ -69,8 +69,9 @@ def csrc_hash():
     for f in files:
         h.update(os.path.basename(f).encode())
         text = open(f, encoding="utf-8").read()
-        if not f.endswith(".py"):  # C++/HIP: drop // and /* */ comments
+        if not f.endswith(".py"):  # C++/HIP: drop // and /* */ comments, then blank lines
             text = re.sub(r"/\*.*?\*/|//[^\n]*", "", text, flags=re.S)
+            text = "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
         h.update(text.encode())
     return h.hexdigest()[:16]
 

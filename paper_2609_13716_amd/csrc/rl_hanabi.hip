@@ -1,15 +1,18 @@
 // Two-player Hanabi kernels: init (deal), env-only steps with injected
 // actions, and the fused rollout.
 //
-// Env lane e of wave 0 holds its game in registers (rl_hanabi.h).  After
-// every move it builds both players' 658-feature observations as bit vectors
-// and publishes them with the mover's legal-action mask to LDS; then all
-// waves expand the bits into an LDS tile (consecutive lanes take consecutive
-// features of one row) that is copied to the trajectory.  In the fused rollout only the mover's
-// row goes through the policy (the other player has no legal action): its
-// rows are gathered from the tile by index, and the MLP is the streaming
-// MFMA MLP of rl_mlp.h.  When games end, the waves shuffle the new decks
-// (one wave per deck) before the env lanes deal them.
+// Env lane e of wave 0 holds its game in registers (rl_hanabi.h) and, after
+// every move, publishes what the observation needs to LDS.  The 26 fields of
+// each player's 658-feature observation are computed by many threads at once
+// (hn_field_bits) and ORed into bit vectors, which are expanded into 0 / 1
+// values only where they are written: the trajectory rows (16 bytes per
+// store, through a 256-entry expansion table) and, in the fused rollout, the
+// mover's row of the layer-1 operand tile (the other player has no legal
+// action), whose MLP is the streaming MFMA MLP of rl_mlp.h.  The env-only
+// kernel keeps a move's rows in one flat bit array (row r's feature f at bit
+// r * 658 + f), where an output vector of 8 bf16 is one byte.  When games
+// end, the waves shuffle the new decks (one wave per deck) before the env
+// lanes deal them.
 #include "rl_hanabi.h"
 #include "rl_internal.h"
 #include "rl_sample.h"
