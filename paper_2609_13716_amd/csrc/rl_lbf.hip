@@ -814,19 +814,22 @@ __device__ __forceinline__ float row_log_pi(const float (&logit)[4], int g, int 
 
 // Same step as lbf_run_kernel for compile-time policy sizes, restructured for
 // latency:
-//   * layer-1/2 weights live in registers and layer 3 in LDS for the whole
-//     rollout; layers are computed transposed so each lane ends with four
-//     consecutive outputs of one row;
+//   * layer-1/2 weights live in registers (S1: layer 1 streamed from the
+//     packed copy) and layer 3 in LDS for the whole rollout; layers are
+//     computed transposed so each lane ends with four consecutive outputs of
+//     one row, with all of a layer's LDS operands read ahead of its MFMAs;
 //   * observations are painted by the env lanes straight into the layer-1
-//     operand tile (only the non-zero features are written), and copied to
-//     the trajectory while the layer-2 MFMAs run by all waves, which clear
-//     the tile behind the copy;
+//     operand tile (only the non-zero features are written); with two tiles
+//     (one M tile) the other waves copy o_t to the trajectory while the env
+//     wave steps, otherwise all waves copy it while the layer-2 MFMAs run;
+//     either way the copy clears the tile behind it;
 //   * the Philox action draws of NOISE_STEPS steps are made in one batch by
 //     all lanes; the Gumbel noise of step k+1 is evaluated from them by the
 //     other waves while the env wave steps the envs at step k;
-//   * one "env wave" (wave 0) computes layer 3, the Gumbel argmax (in
-//     registers plus one v_permlane16_swap) and steps the TE envs, drawing the
-//     reset blocks of ended episodes on idle lanes in parallel.
+//   * one "env wave" (wave 0, at raised issue priority: its serial section is
+//     the longest stage) computes layer 3, the Gumbel argmax (in registers
+//     plus one v_permlane16_swap) and steps the TE envs, drawing the reset
+//     blocks of ended episodes on idle lanes in parallel.
 // TE envs per workgroup; the launch bounds let MINB workgroups share a CU.
 // VH: layer 3 has one more output, the value head V(o) of an actor-critic
 // network, written with log pi of each sampled action and, after the last
@@ -1615,24 +1618,26 @@ hipError_t launch_lbf_run_pop(const LbfParams& p, const PolicyArgs& pol, int n_p
 // ------------------------------------- env-only steps ----
 //
 // rollout_step for compile-time LBF shapes.  The env wave runs S steps
-// between workgroup barriers: per step the transition, the resets of the
-// episodes that ended and the paint of o_{t+1}.  Everything that touches
-// global memory inside the step loop is left to the other ("copy") waves:
-//   * wave 0 (env): the env state lives in registers; on grids of at most 64
-//     cells the 8 lanes of a group hold one env and resolve its transition
-//     together (lbf_transition_group), otherwise lane e holds env e.  The
-//     actions come from LDS one step ahead.  The reset draws of the envs that
-//     ended are made in parallel, one Philox block per lane.  The env's first
-//     lane paints o_{t+1} onto the observation tile of its step (cleared
-//     behind the previous copy of that tile) and leaves the reward and done
-//     in LDS;
-//   * waves 1..NCW (copy): after a barrier, copy the S tiles of the steps just
-//     run to the trajectory with 16-byte stores, clearing them behind the
-//     copy, and write the rewards, dones and legal masks, while wave 0 runs
-//     the next S steps on the other S tiles; at the start of each chunk of
-//     ACT_CHUNK steps they stage the next chunk's actions into the other half
-//     of a double buffer (a global load waits for its wave's earlier stores,
-//     so wave 0 issues none inside the loop).
+// between workgroup barriers: per step the transition and the resets of the
+// episodes that ended.  Everything else, and everything that touches global
+// memory inside the step loop, is left to the other ("copy") waves:
+//   * wave 0 (env), at raised issue priority (its chain sets the pace): the
+//     env state lives in registers; on grids of at most 64 cells the 8 lanes
+//     of a group hold one env and resolve its transition together
+//     (lbf_transition_group), otherwise lane e holds env e.  The actions come
+//     from LDS one step ahead.  The reset draws of the envs that ended are
+//     made in parallel, one Philox block per lane.  The env's first lane
+//     publishes the post-step state, reward and done of each step to LDS
+//     (double-buffered by barrier interval);
+//   * waves 1..NCW (copy): after a barrier, each for its own share of the
+//     rows and for each of the S steps just run, paint o_{t+1} from the
+//     published states onto the step's observation tile (one non-zero
+//     feature per lane), copy the rows to the trajectory with 16-byte stores,
+//     clearing them behind the copy, and write the rewards, dones and legal
+//     masks, while wave 0 runs the next S steps; at the start of each chunk
+//     of ACT_CHUNK steps they stage the next chunk's actions into the other
+//     half of a double buffer (a global load waits for its wave's earlier
+//     stores, so wave 0 issues none inside the loop).
 template <typename OT, int GH, int GW, int A, int F, int TE, int NCW, int S>
 __global__ __launch_bounds__(64 * (NCW + 1)) void lbf_env_kernel(LbfParams p, int32_t* __restrict__ state,
                                                                  uint64_t t0, int n_steps,
