@@ -195,7 +195,8 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
   float* lg = reinterpret_cast<float*>(h2 + R * ld2);
   float* sc = lg + R * MAX_NA;
   int* act_s = reinterpret_cast<int*>(sc + R * MAX_NA);
-  const size_t total = (size_t)((uint8_t*)(act_s + R) - smem);
+  float* nz = reinterpret_cast<float*>(act_s + R);  // Gumbel noise of the next step's (row, action)
+  const size_t total = (size_t)((uint8_t*)(nz + R * MAX_NA) - smem);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
@@ -209,11 +210,20 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
   __syncthreads();
   const bool envlane = tid < te_valid;
   const int e = e0 + tid;
+  // the noise of step kn's (row, action) items, threads i0, i0 + stride, ...
+  auto draw_noise = [&](int kn, int i0, int stride) {
+    for (int idx = i0; idx < R * NA; idx += stride) {
+      const int r = idx / NA, a = idx - r * NA, el = r >> 1, ag = r & 1;
+      nz[r * MAX_NA + a] =
+          el < te_valid ? action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t0 + (uint64_t)kn, ag, a) : 0.f;
+    }
+  };
   OcEnv s;
   if (envlane) {
     oc_load(state, E, e, s);
     oc_paint_all(s, xs, LDX, tid);
   }
+  if (n_steps > 0) draw_noise(0, tid, OC_RUN_NT);
   __builtin_amdgcn_s_waitcnt(0);
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
@@ -230,8 +240,7 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
     for (int idx = tid; idx < R * NA; idx += OC_RUN_NT) {
       const int r = idx / NA, a = idx - r * NA, el = r >> 1, ag = r & 1;
       if (el < te_valid) {
-        const float g = action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t, ag, a);
-        sc[r * MAX_NA + a] = action_score(lg[r * MAX_NA + a], g, true);
+        sc[r * MAX_NA + a] = action_score(lg[r * MAX_NA + a], nz[r * MAX_NA + a], true);
         if (out.logits) out.logits[((size_t)k * E + e0) * 2 * NA + idx] = lg[r * MAX_NA + a];
       }
     }
@@ -262,6 +271,10 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
       oc_step_lane(p, s, tid, (uint64_t)(p.env_base + e), t, act, xs, LDX, r, d);
       if (out.reward) out.reward[(size_t)k * E + e] = r;
       if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
+    } else if (tid >= 64 && k + 1 < n_steps) {
+      // the other waves draw the next step's noise (it depends on nothing the
+      // step computes) while the env lanes step the kitchens
+      draw_noise(k + 1, tid - 64, OC_RUN_NT - 64);
     }
   }
   __syncthreads();
@@ -282,7 +295,7 @@ static size_t oc_run_lds_bytes_te(const PolicyArgs& pol, int te) {
   const int ldx = pol.dt == DT_F32 ? lds_ld<DT_F32>(OC_D) : lds_ld<DT_BF16>(OC_D);
   const int ld1 = pol.dt == DT_F32 ? lds_ld<DT_F32>(pol.H1) : lds_ld<DT_BF16>(pol.H1);
   const int ld2 = pol.dt == DT_F32 ? lds_ld<DT_F32>(pol.H2) : lds_ld<DT_BF16>(pol.H2);
-  return (size_t)R * (ldx + ld1 + ld2) * es + (size_t)R * MAX_NA * 4 * 2 + (size_t)R * 4;
+  return (size_t)R * (ldx + ld1 + ld2) * es + (size_t)R * MAX_NA * 4 * 3 + (size_t)R * 4;
 }
 
 // 16 envs per workgroup (two row tiles share every weight fragment) when their tiles fit in LDS, else 8.
