@@ -464,7 +464,7 @@ constexpr int HN_RUN_NT = 512;  // 8 waves: the MLP's weight-streaming chains of
 
 struct HnRunLayout {
   int ldx, ld1, ld2;
-  size_t off_x, off_h1, off_h2, off_lg, off_sc, off_env, off_words, off_need, off_bits, off_lut, total;
+  size_t off_x, off_h1, off_h2, off_lg, off_sc, off_env, off_words, off_need, off_bits, off_lut, off_nz, total;
 };
 
 __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int obs) {
@@ -486,6 +486,7 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int
   o = (o + 15) & ~(size_t)15;
   L.off_bits = o;  o += (size_t)2 * HN_RUN_TE * HN_OBS_WORDS * 8;
   L.off_lut = o;   o += (size_t)HnExpand<uint16_t>::N * 16;  // (the larger expansion table)
+  L.off_nz = o;    o += (size_t)HN_RUN_TE * 2 * MAX_NA * 4;   // next step's noise, both agents
   L.total = o;
   return L;
 }
@@ -510,6 +511,7 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
   uint32_t* need = reinterpret_cast<uint32_t*>(smem + L.off_need);
   uint64_t* bits = reinterpret_cast<uint64_t*>(smem + L.off_bits);  // the observation bit vectors, row by row
   u32x4* lut = reinterpret_cast<u32x4*>(smem + L.off_lut);
+  float* nz = reinterpret_cast<float*>(smem + L.off_nz);  // [env][agent][action]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
@@ -532,6 +534,16 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
     hn_load(state, E, e, s);
     hn_publish<G>(s, envs[tid]);
   }
+  // the noise of step kn for both agents of every game (the mover is known
+  // only after the previous move), threads i0, i0 + stride, ...
+  auto draw_noise = [&](int kn, int i0, int stride) {
+    for (int idx = i0; idx < te_valid * 2 * NA; idx += stride) {
+      const int el = idx / (2 * NA), rem = idx - el * 2 * NA, ag = rem / NA, a = rem - ag * NA;
+      nz[(el * 2 + ag) * MAX_NA + a] =
+          action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t0 + (uint64_t)kn, ag, a);
+    }
+  };
+  if (n_steps > 0) draw_noise(0, tid, HN_RUN_NT);
   RL_STAMP_BEGIN
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
@@ -556,8 +568,7 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
       const int el = idx / NA, a = idx - el * NA;
       const int cur = envs[el].pub.cur;
       const bool ok = (envs[el].legal >> a) & 1u;
-      const float g = action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t, cur, a);
-      sc[el * MAX_NA + a] = action_score(lg[el * MAX_NA + a], g, ok);
+      sc[el * MAX_NA + a] = action_score(lg[el * MAX_NA + a], nz[(el * 2 + cur) * MAX_NA + a], ok);
       if (out.logits) {
         float* lo = out.logits + ((size_t)k * E + e0 + el) * 2 * NA;
         lo[cur * NA + a] = ok ? lg[el * MAX_NA + a] : -INFINITY;
@@ -604,6 +615,9 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
       if (!d) hn_publish<G>(s, envs[tid]);
       if (out.reward) out.reward[(size_t)k * E + e] = r;
       if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
+    } else if (wave > 0 && k + 1 < n_steps) {
+      // the other waves draw the next step's noise while the env lanes move
+      draw_noise(k + 1, tid - 64, HN_RUN_NT - 64);
     }
     hn_flag_any(need, TE, d, wave, lane);
     __syncthreads();
