@@ -486,7 +486,7 @@ __host__ __device__ inline HnRunLayout hn_run_layout(int H1, int H2, int dt, int
   o = (o + 15) & ~(size_t)15;
   L.off_bits = o;  o += (size_t)2 * HN_RUN_TE * HN_OBS_WORDS * 8;
   L.off_lut = o;   o += (size_t)HnExpand<uint16_t>::N * 16;  // (the larger expansion table)
-  L.off_nz = o;    o += (size_t)HN_RUN_TE * 2 * MAX_NA * 4;   // next step's noise, both agents
+  L.off_nz = o;    o += (size_t)HN_RUN_TE * (MAX_NA + 2) * 4;  // next step's noise, its agent, the mover
   L.total = o;
   return L;
 }
@@ -511,7 +511,9 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
   uint32_t* need = reinterpret_cast<uint32_t*>(smem + L.off_need);
   uint64_t* bits = reinterpret_cast<uint64_t*>(smem + L.off_bits);  // the observation bit vectors, row by row
   u32x4* lut = reinterpret_cast<u32x4*>(smem + L.off_lut);
-  float* nz = reinterpret_cast<float*>(smem + L.off_nz);  // [env][agent][action]
+  float* nz = reinterpret_cast<float*>(smem + L.off_nz);  // [env][action]: the next step's noise
+  int* nz_ag = reinterpret_cast<int*>(nz + TE * MAX_NA);  // [env]: the agent nz was drawn for
+  int* mover = nz_ag + TE;                                // [env]: this step's mover
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0), E = p.E;
@@ -534,16 +536,20 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
     hn_load(state, E, e, s);
     hn_publish<G>(s, envs[tid]);
   }
-  // the noise of step kn for both agents of every game (the mover is known
-  // only after the previous move), threads i0, i0 + stride, ...
-  auto draw_noise = [&](int kn, int i0, int stride) {
-    for (int idx = i0; idx < te_valid * 2 * NA; idx += stride) {
-      const int el = idx / (2 * NA), rem = idx - el * 2 * NA, ag = rem / NA, a = rem - ag * NA;
-      nz[(el * 2 + ag) * MAX_NA + a] =
-          action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t0 + (uint64_t)kn, ag, a);
+  // the noise of step kn for agent ag(el) of every game, threads i0, i0 +
+  // stride, ...  The next step's mover is known only after the move; the
+  // turn passes to the other player unless the game ends, so that player's
+  // noise is drawn ahead, and a step whose mover differs (a new game)
+  // draws its own in the score loop.
+  auto draw_noise = [&](int kn, int i0, int stride, auto ag_of) {
+    for (int idx = i0; idx < te_valid * NA; idx += stride) {
+      const int el = idx / NA, a = idx - el * NA, ag = ag_of(el);
+      nz[el * MAX_NA + a] = action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t0 + (uint64_t)kn, ag, a);
+      if (a == 0) nz_ag[el] = ag;
     }
   };
-  if (n_steps > 0) draw_noise(0, tid, HN_RUN_NT);
+  __syncthreads();  // the games are published
+  if (n_steps > 0) draw_noise(0, tid, HN_RUN_NT, [&](int el) { return envs[el].pub.cur; });
   RL_STAMP_BEGIN
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
@@ -568,7 +574,10 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
       const int el = idx / NA, a = idx - el * NA;
       const int cur = envs[el].pub.cur;
       const bool ok = (envs[el].legal >> a) & 1u;
-      sc[el * MAX_NA + a] = action_score(lg[el * MAX_NA + a], nz[(el * 2 + cur) * MAX_NA + a], ok);
+      const float g = nz_ag[el] == cur ? nz[el * MAX_NA + a]
+                                       : action_noise(p.seed, (uint64_t)(p.env_base + e0 + el), t, cur, a);
+      sc[el * MAX_NA + a] = action_score(lg[el * MAX_NA + a], g, ok);
+      if (a == 0) mover[el] = cur;
       if (out.logits) {
         float* lo = out.logits + ((size_t)k * E + e0 + el) * 2 * NA;
         lo[cur * NA + a] = ok ? lg[el * MAX_NA + a] : -INFINITY;
@@ -616,8 +625,9 @@ __global__ __launch_bounds__(HN_RUN_NT) void hn_run_kernel(HnParams p, PolicyArg
       if (out.reward) out.reward[(size_t)k * E + e] = r;
       if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
     } else if (wave > 0 && k + 1 < n_steps) {
-      // the other waves draw the next step's noise while the env lanes move
-      draw_noise(k + 1, tid - 64, HN_RUN_NT - 64);
+      // the other waves draw the next step's noise (for the player whose turn
+      // it will be if the game goes on) while the env lanes move
+      draw_noise(k + 1, tid - 64, HN_RUN_NT - 64, [&](int el) { return 1 - mover[el]; });
     }
     hn_flag_any(need, TE, d, wave, lane);
     __syncthreads();
