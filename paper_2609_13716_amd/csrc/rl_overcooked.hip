@@ -16,6 +16,9 @@
 
 namespace rl {
 
+RL_STAMP_TABLE
+
+
 constexpr int OC_TE = 8;  // envs per workgroup of the init and env-only kernels (one wave)
 
 template <typename T>
@@ -225,18 +228,23 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
   }
   if (n_steps > 0) draw_noise(0, tid, OC_RUN_NT);
   __builtin_amdgcn_s_waitcnt(0);
+  RL_STAMP_BEGIN
   for (int k = 0; k < n_steps; ++k) {
     const uint64_t t = t0 + (uint64_t)k;
     __syncthreads();  // the env lanes' repaint of the previous step is visible
+    RL_STAMP(0)
     mlp_input_layer_const<DT, OC_D, PK>(xs, LDX, nullptr, R, W1, b1, pol.H1, h1, ld1, wave, OC_RUN_NT / 64, lane,
                                         static_cast<const T*>(pol.Wp[0]));
     __syncthreads();
+    RL_STAMP(1)
     mlp_hidden<DT, PK>(h1, ld1, R, pol.H1, W2, b2, pol.H2, h2, ld2, wave, OC_RUN_NT / 64, lane,
                        static_cast<const T*>(pol.Wp[1]));
     __syncthreads();
+    RL_STAMP(2)
     mlp_logits<DT, PK>(h2, ld2, R, pol.H2, W3, b3, NA, lg, MAX_NA, wave, OC_RUN_NT / 64, lane,
                        static_cast<const T*>(pol.Wp[2]));
     __syncthreads();
+    RL_STAMP(3)
     for (int idx = tid; idx < R * NA; idx += OC_RUN_NT) {
       const int r = idx / NA, a = idx - r * NA, el = r >> 1, ag = r & 1;
       if (el < te_valid) {
@@ -244,12 +252,9 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
         if (out.logits) out.logits[((size_t)k * E + e0) * 2 * NA + idx] = lg[r * MAX_NA + a];
       }
     }
-    // The trajectory copy of o_t is issued after the step's weight loads: a
-    // wave's loads wait for its earlier stores (one in-order counter).
-    if (out.obs)
-      copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D, OC_D, te_valid * 2,
-                         tid, OC_RUN_NT);
+    RL_STAMP(4)
     __syncthreads();
+    RL_STAMP(6)
     if (tid < R && (tid >> 1) < te_valid) {
       int best = 0;
       float bs = -INFINITY;
@@ -264,19 +269,43 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
       if (out.actions) out.actions[((size_t)k * E + e0) * 2 + tid] = best;
     }
     __syncthreads();
+    RL_STAMP(7)
+    // The env lanes step the kitchens (oc_step_lane, with the tile's repaint
+    // deferred) while the other waves copy o_t to the trajectory (after the
+    // step's weight loads: a wave's loads wait for its earlier stores, one
+    // in-order counter) and draw the next step's noise (it depends on
+    // nothing the step computes); after a barrier the env lanes repaint.
+    OcEnv s_old;
+    uint64_t changed = 0, had = 0;
+    uint32_t d = 0;
     if (envlane) {
       const int act[2] = {act_s[tid * 2], act_s[tid * 2 + 1]};
       float r;
-      uint32_t d;
-      oc_step_lane(p, s, tid, (uint64_t)(p.env_base + e), t, act, xs, LDX, r, d);
+      s_old = s;
+      oc_transition(p, s, act, r, d, changed);
+      if (d) {
+        had = s.it_onion | s.it_plate | s.it_soup;
+        oc_reset(p, (uint64_t)(p.env_base + e), t + 1, s);
+      }
       if (out.reward) out.reward[(size_t)k * E + e] = r;
       if (out.done) out.done[(size_t)k * E + e] = (uint8_t)d;
-    } else if (tid >= 64 && k + 1 < n_steps) {
-      // the other waves draw the next step's noise (it depends on nothing the
-      // step computes) while the env lanes step the kitchens
-      draw_noise(k + 1, tid - 64, OC_RUN_NT - 64);
+    } else if (tid >= 64) {
+      if (out.obs)
+        copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D, OC_D,
+                           te_valid * 2, tid - 64, OC_RUN_NT - 64);
+      if (k + 1 < n_steps) draw_noise(k + 1, tid - 64, OC_RUN_NT - 64);
     }
+    RL_STAMP(8)
+    __syncthreads();  // o_t is copied out
+    RL_STAMP(9)
+    if (envlane) {  // the tile becomes o_{t+1}: oc_step_lane's paints, in its order
+      oc_paint_agents(s_old, xs, LDX, tid, false);
+      oc_paint_items(s, xs, LDX, tid, d ? (had | changed) : changed);
+      oc_paint_agents(s, xs, LDX, tid, true);
+    }
+    RL_STAMP(10)
   }
+  RL_STAMP_END(wave == 0 ? 0 : 1)
   __syncthreads();
   if (out.obs_last)
     copy_rows_global16(xs, LDX, static_cast<T*>(out.obs_last) + (size_t)e0 * 2 * OC_D, OC_D, te_valid * 2, tid,
@@ -347,3 +376,5 @@ hipError_t launch_oc_run(const OcParams& p, const PolicyArgs& pol, int32_t* stat
 }
 
 }  // namespace rl
+
+RL_STAMP_EXPORT(oc)
