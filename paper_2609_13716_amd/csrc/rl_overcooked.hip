@@ -19,7 +19,10 @@ namespace rl {
 RL_STAMP_TABLE
 
 
-constexpr int OC_TE = 8;  // envs per workgroup of the init and env-only kernels (one wave)
+constexpr int OC_TE = 8;  // envs per workgroup of the init kernel (one wave)
+// env-only kernel: envs per workgroup and threads (one env wave, the rest copy)
+constexpr int OC_ENV_TE_BF16 = 16, OC_ENV_NT_BF16 = 256;
+constexpr int OC_ENV_TE_F32 = 8, OC_ENV_NT_F32 = 256;
 
 template <typename T>
 __device__ __forceinline__ void oc_put(T* xr, int plane, int cell, uint32_t v) {
@@ -136,47 +139,78 @@ __global__ __launch_bounds__(64) void oc_init_kernel(OcParams p, int32_t* __rest
 
 // ---------------------------------------------------------- env-only ----
 
-template <typename OT>
-__global__ __launch_bounds__(64) void oc_env_kernel(OcParams p, int32_t* __restrict__ state, uint64_t t0, int n_steps,
+// One workgroup steps TE kitchens with two observation tiles: step k's tile
+// is tile[k & 1]. The env lanes (wave 0) run step k's transition and bring
+// tile[k & 1] from o_{k-2} up to o_k while the other waves copy tile
+// [(k-1) & 1] (o_{k-1}) to the trajectory; one barrier per step. Going from
+// o_{k-2} to o_k erases the agents of s_{k-2}, repaints the counters whose
+// item changed in either step and paints the agents of s_k (the agent,
+// facing, held and pot planes never overlap the item planes). Before the
+// first step both tiles hold the launch's observation, whose agents are
+// those of the launch state.
+template <typename OT, int TE, int NT>
+__global__ __launch_bounds__(NT) void oc_env_kernel(OcParams p, int32_t* __restrict__ state, uint64_t t0, int n_steps,
                                                     const int32_t* __restrict__ actions, OT* __restrict__ obs,
                                                     float* __restrict__ reward, uint8_t* __restrict__ done,
                                                     uint8_t* __restrict__ legal) {
-  __shared__ __align__(16) OT tile[OC_TE * 2 * OC_D];
-  __shared__ int32_t act_lds[ACT_CHUNK * OC_TE * 2];
-  const int lane = threadIdx.x, e0 = blockIdx.x * OC_TE, te_valid = min(OC_TE, p.E - e0);
+  static_assert(TE <= 64 && NT % 64 == 0 && NT >= 128, "env lanes in wave 0, copy waves after it");
+  constexpr int TS = TE * 2 * OC_D;
+  __shared__ __align__(16) OT tile[2 * TS];
+  __shared__ int32_t act_lds[ACT_CHUNK * TE * 2];
+  const int tid = threadIdx.x, e0 = blockIdx.x * TE, te_valid = min(TE, p.E - e0);
   const int E = p.E;
-  const bool envlane = lane < te_valid;
-  const int e = e0 + lane;
-  zero_lds<64>(tile, sizeof(tile), lane);
-  wave_lds_sync();
-  OcEnv s;
+  const bool envlane = tid < te_valid;
+  const int e = e0 + tid;
+  zero_lds<NT>(tile, sizeof(tile), tid);
+  __syncthreads();
+  OcEnv s, s_pp;  // s_pp: the state whose agents tile[k & 1] shows when step k starts
+  uint64_t mask_prev = 0;  // counters whose item changed in the previous step
   if (envlane) {
     oc_load(state, E, e, s);
-    oc_paint_all(s, tile, OC_D, lane);
+    oc_paint_all(s, tile, OC_D, tid);
+    oc_paint_all(s, tile + TS, OC_D, tid);
+    s_pp = s;
   }
+  if (tid < 64) __builtin_amdgcn_s_setprio(3);
+  auto emit = [&](int k, int i0, int stride) {
+    if (obs) copy_tile(tile + (k & 1) * TS, obs + ((size_t)k * E + e0) * 2 * OC_D, te_valid * 2 * OC_D, i0, stride);
+    if (legal)
+      for (int i = i0; i < te_valid * 2 * OC_NACT; i += stride) legal[((size_t)k * E + e0) * 2 * OC_NACT + i] = 1;
+  };
   for (int k0 = 0; k0 < n_steps; k0 += ACT_CHUNK) {
     const int nk = min(ACT_CHUNK, n_steps - k0);
     // no global loads inside the step loop: a load there would wait for every earlier trajectory store
-    stage_actions<OC_TE * 2, 64>(actions, E, e0, te_valid * 2, 2, k0, nk, act_lds, lane);
-    wave_lds_sync();
+    stage_actions<TE * 2, NT>(actions, E, e0, te_valid * 2, 2, k0, nk, act_lds, tid);
+    __syncthreads();
     for (int kk = 0; kk < nk; ++kk) {
       const int k = k0 + kk;
       const uint64_t t = t0 + (uint64_t)k;
       if (envlane) {
-        const int act[2] = {act_lds[kk * OC_TE * 2 + lane * 2], act_lds[kk * OC_TE * 2 + lane * 2 + 1]};
+        const int act[2] = {act_lds[kk * TE * 2 + tid * 2], act_lds[kk * TE * 2 + tid * 2 + 1]};
+        const OcEnv s_prev = s;
         float r;
         uint32_t d;
-        oc_step_lane(p, s, lane, (uint64_t)(p.env_base + e), t, act, tile, OC_D, r, d);
+        uint64_t changed;
+        oc_transition(p, s, act, r, d, changed);
+        if (d) {
+          changed |= s.it_onion | s.it_plate | s.it_soup;
+          oc_reset(p, (uint64_t)(p.env_base + e), t + 1, s);
+        }
         if (reward) reward[(size_t)k * E + e] = r;
         if (done) done[(size_t)k * E + e] = (uint8_t)d;
+        OT* tk = tile + (k & 1) * TS;
+        oc_paint_agents(s_pp, tk, OC_D, tid, false);
+        oc_paint_items(s, tk, OC_D, tid, mask_prev | changed);
+        oc_paint_agents(s, tk, OC_D, tid, true);
+        s_pp = s_prev;
+        mask_prev = changed;
+      } else if (tid >= 64 && k > 0) {
+        emit(k - 1, tid - 64, NT - 64);
       }
-      wave_lds_sync();
-      if (obs) copy_tile(tile, obs + ((size_t)k * E + e0) * 2 * OC_D, te_valid * 2 * OC_D, lane, 64);
-      if (legal)
-        for (int i = lane; i < te_valid * 2 * OC_NACT; i += 64) legal[((size_t)k * E + e0) * 2 * OC_NACT + i] = 1;
-      wave_lds_sync();
+      __syncthreads();
     }
   }
+  if (n_steps > 0) emit(n_steps - 1, tid, NT);
   if (envlane) oc_store(state, E, e, s);
 }
 
@@ -343,11 +377,11 @@ hipError_t launch_oc_init(const OcParams& p, int32_t* state, void* obs, int obs_
 hipError_t launch_oc_step(const OcParams& p, int32_t* state, uint64_t t0, int n_steps, const int32_t* actions,
                           void* obs, int obs_dt, float* reward, uint8_t* done, uint8_t* legal, hipStream_t s) {
   if (obs_dt == DT_F32)
-    oc_env_kernel<float><<<oc_tiles(p.E, OC_TE), 64, 0, s>>>(p, state, t0, n_steps, actions, static_cast<float*>(obs), reward,
-                                                      done, legal);
+    oc_env_kernel<float, OC_ENV_TE_F32, OC_ENV_NT_F32><<<oc_tiles(p.E, OC_ENV_TE_F32), OC_ENV_NT_F32, 0, s>>>(
+        p, state, t0, n_steps, actions, static_cast<float*>(obs), reward, done, legal);
   else
-    oc_env_kernel<uint16_t><<<oc_tiles(p.E, OC_TE), 64, 0, s>>>(p, state, t0, n_steps, actions, static_cast<uint16_t*>(obs),
-                                                         reward, done, legal);
+    oc_env_kernel<uint16_t, OC_ENV_TE_BF16, OC_ENV_NT_BF16><<<oc_tiles(p.E, OC_ENV_TE_BF16), OC_ENV_NT_BF16, 0, s>>>(
+        p, state, t0, n_steps, actions, static_cast<uint16_t*>(obs), reward, done, legal);
   return hipGetLastError();
 }
 
