@@ -853,6 +853,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
   // others come from the next lanes by DPP row shifts (no LDS round trip).
   constexpr bool DIRECT = MT == 1 && 16 % A == 0;
   constexpr int ESTRIDE = DIRECT ? A : 1;  // lane of env e = e * ESTRIDE
+  constexpr bool SPLIT3 = MT > 1 && MT <= NW;
   constexpr int LDX = lds_ld<DT>(D), LD1 = lds_ld<DT>(H1), LD2 = lds_ld<DT>(H2);
   constexpr int K3 = round_up(H2, DType<DT>::KS) / DType<DT>::KS;
   // LEAN: the resident weights leave too few registers for the env step, so
@@ -1007,100 +1008,116 @@ __global__ __launch_bounds__(NW * 64, MINB) void lbf_rollout_kernel(LbfParams p,
     }
     __syncthreads();
     RL_STAMP(3)
+    // Layer 3 transposed, logits^T = W3 h2^T: lane holds row (lane % 16) of
+    // an M tile and actions 4 * (lane / 16) + r in accumulator element r.
+    // Each lane takes the Gumbel argmax of its four actions; one lane swap
+    // with the partner group (actions 0-3 <-> 4-7) finishes the row.
+    const int g = lane >> 4;
+    // Layer 3 of NTL M tiles from m0: the K steps run in order over the tiles
+    // at once (one W3 operand serves every tile), their LDS operands read PF3
+    // K steps ahead of the MFMAs that use them, each into its own registers,
+    // so the chains do not wait out an LDS latency per K step.  (The lane
+    // index is made opaque here so that the W3 reads are not hoisted out of
+    // the step loop into registers held through the whole step.)
+    auto l3_tiles = [&](auto ntl_c, int m0, auto& acc3) {
+      constexpr int NTL = decltype(ntl_c)::value;
+      constexpr int PF3 = K3 < 4 ? K3 : NTL > 2 ? 2 : 4;  // (fewer where three M tiles crowd the registers)
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      B wq[PF3], hq[PF3][NTL];
+      auto fetch3 = [&](int ks, int q) {
+        wq[q] = w3s[ks * 64 + ln];
+#pragma unroll
+        for (int m = 0; m < NTL; ++m) hq[q][m] = load_operand_lds<DT>(h2s, LD2, (m0 + m) * 16 + (ln & 15), ks, ln);
+      };
+#pragma unroll
+      for (int m = 0; m < NTL; ++m) acc3[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int q = 0; q < PF3; ++q) fetch3(q, q);
+#pragma unroll
+      for (int ks = 0; ks < K3; ++ks) {
+#pragma unroll
+        for (int m = 0; m < NTL; ++m) acc3[m] = mfma16<DT>(wq[ks % PF3], hq[ks % PF3][m], acc3[m]);
+        if (ks + PF3 < K3) fetch3(ks + PF3, ks % PF3);
+      }
+    };
+    // The Gumbel argmax of M tile mt and its outputs; returns this lane's
+    // row's action (valid in lane groups 0 and 1).
+    auto l3_argmax = [&](int mt, const f32x4 acc) -> int {
+      const int row = mt * 16 + (lane & 15);
+      const f32x4 nz4 = *reinterpret_cast<const f32x4*>(&nz[k & 1][row * 8 + 4 * (g & 1)]);
+      float best_s = -INFINITY;
+      int best_a = 0;
+      float logit[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int act = 4 * g + r;
+        logit[r] = acc[r] + b3r[r];
+        const float sc = action_score(logit[r], nz4[r], (act < NA) & (row < R));
+        const bool take = (r == 0) | (sc > best_s);
+        best_s = take ? sc : best_s;
+        best_a = take ? act : best_a;
+      }
+      {
+        const auto ps = __builtin_amdgcn_permlane16_swap(__float_as_uint(best_s), __float_as_uint(best_s), false,
+                                                         false);
+        const auto pa = __builtin_amdgcn_permlane16_swap((uint32_t)best_a, (uint32_t)best_a, false, false);
+        const float os = __uint_as_float((g & 1) ? ps[0] : ps[1]);
+        const int oa = (int)((g & 1) ? pa[0] : pa[1]);
+        const bool take = (os > best_s) | ((os == best_s) & (oa < best_a));
+        best_s = take ? os : best_s;
+        best_a = take ? oa : best_a;
+      }
+      const bool live = row < te_valid * A;
+      const bool heur = TM && live && tk_s[TM ? row : 0] >= 0;  // (kinds set in the prologue)
+      if (live && g == 0) {
+        if constexpr (!DIRECT) act_s[row] = best_a;
+        if (out.actions && !heur) out.actions[((size_t)k * E + e0) * A + row] = best_a;
+      }
+      if constexpr (VH) {
+        const size_t gr = ((size_t)k * E + e0) * A + row;
+        if (live && g == NA / 4 && out.value) out.value[gr] = logit[NA % 4];
+        if (out.logp) {
+          const float lp = row_log_pi<NA>(logit, g, best_a);
+          if (live && g == 0) out.logp[gr] = lp;
+        }
+      }
+      if (out.logits && live && g < 2 && !heur) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (4 * g + r < NA) out.logits[(((size_t)k * E + e0) * A + row) * NA + 4 * g + r] = logit[r];
+      }
+      return best_a;
+    };
+    // SPLIT3: with several M tiles, wave m runs layer 3 and the argmax of
+    // tile m before a barrier, instead of the env wave running them all.
+    if constexpr (SPLIT3) {
+      if (wave < MT) {
+        f32x4 acc3[1];
+        l3_tiles(std::integral_constant<int, 1>{}, wave, acc3);
+        l3_argmax(wave, acc3[0]);
+      }
+      __syncthreads();
+      RL_STAMP(4)
+    }
     if (wave == ew) {
       if constexpr (LEAN) lbf_copy<A, F>(s, env_s[min(el, TE - 1)]);
-      // Layer 3 transposed, logits^T = W3 h2^T: lane holds row (lane % 16) of
-      // the M tile and actions 4 * (lane / 16) + r in accumulator element r.
-      // Each lane takes the Gumbel argmax of its four actions; one lane swap
-      // with the partner group (actions 0-3 <-> 4-7) finishes the row.
-      const int g = lane >> 4;
       int act_d[LBF_MAXA] = {0, 0, 0, 0};  // DIRECT: this lane's env's actions
-      // With one M tile the W3 operands are loaded once into registers; with
-      // several the M tiles run one at a time (not unrolled) and read W3 from
-      // LDS per K step, which keeps the env wave within the register budget
-      // of the layers whose weights stay resident.
-      // Layer 3 of every M tile: the K steps run in order over all M tiles at
-      // once (one W3 operand serves every tile), their LDS operands read PF3
-      // K steps ahead of the MFMAs that use them, each into its own registers,
-      // so the chains do not wait out an LDS latency per K step.  (The lane
-      // index is made opaque here so that the W3 reads are not hoisted out of
-      // the step loop into registers held through the whole step.)
-      f32x4 acc3[MT];
-      {
-        constexpr int PF3 = K3 < 4 ? K3 : MT > 2 ? 2 : 4;  // (fewer where three M tiles crowd the registers)
-        int ln = lane;
-        asm volatile("" : "+v"(ln));
-        B wq[PF3], hq[PF3][MT];
-        auto fetch3 = [&](int ks, int q) {
-          wq[q] = w3s[ks * 64 + ln];
+      if constexpr (!SPLIT3) {
+        f32x4 acc3[MT];
+        l3_tiles(std::integral_constant<int, MT>{}, 0, acc3);
 #pragma unroll
-          for (int m = 0; m < MT; ++m) hq[q][m] = load_operand_lds<DT>(h2s, LD2, m * 16 + (ln & 15), ks, ln);
-        };
-#pragma unroll
-        for (int m = 0; m < MT; ++m) acc3[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int q = 0; q < PF3; ++q) fetch3(q, q);
-#pragma unroll
-        for (int ks = 0; ks < K3; ++ks) {
-#pragma unroll
-          for (int m = 0; m < MT; ++m) acc3[m] = mfma16<DT>(wq[ks % PF3], hq[ks % PF3][m], acc3[m]);
-          if (ks + PF3 < K3) fetch3(ks + PF3, ks % PF3);
-        }
-      }
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int row = mt * 16 + (lane & 15);
-        const f32x4 nz4 = *reinterpret_cast<const f32x4*>(&nz[k & 1][row * 8 + 4 * (g & 1)]);
-        const f32x4 acc = acc3[mt];
-        float best_s = -INFINITY;
-        int best_a = 0;
-        float logit[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int act = 4 * g + r;
-          logit[r] = acc[r] + b3r[r];
-          const float sc = action_score(logit[r], nz4[r], (act < NA) & (row < R));
-          const bool take = (r == 0) | (sc > best_s);
-          best_s = take ? sc : best_s;
-          best_a = take ? act : best_a;
-        }
-        {
-          const auto ps = __builtin_amdgcn_permlane16_swap(__float_as_uint(best_s), __float_as_uint(best_s), false,
-                                                           false);
-          const auto pa = __builtin_amdgcn_permlane16_swap((uint32_t)best_a, (uint32_t)best_a, false, false);
-          const float os = __uint_as_float((g & 1) ? ps[0] : ps[1]);
-          const int oa = (int)((g & 1) ? pa[0] : pa[1]);
-          const bool take = (os > best_s) | ((os == best_s) & (oa < best_a));
-          best_s = take ? os : best_s;
-          best_a = take ? oa : best_a;
-        }
-        const bool live = row < te_valid * A;
-        const bool heur = TM && live && tk_s[TM ? row : 0] >= 0;  // written by the env lane below
-        if (live && g == 0) {
-          if constexpr (!DIRECT) act_s[row] = best_a;
-          if (out.actions && !heur) out.actions[((size_t)k * E + e0) * A + row] = best_a;
-        }
-        if constexpr (VH) {
-          const size_t gr = ((size_t)k * E + e0) * A + row;
-          if (live && g == NA / 4 && out.value) out.value[gr] = logit[NA % 4];
-          if (out.logp) {
-            const float lp = row_log_pi<NA>(logit, g, best_a);
-            if (live && g == 0) out.logp[gr] = lp;
+        for (int mt = 0; mt < MT; ++mt) {
+          const int best_a = l3_argmax(mt, acc3[mt]);
+          if constexpr (DIRECT) {
+            act_d[0] = best_a;
+            if constexpr (A > 1) act_d[1] = __builtin_amdgcn_update_dpp(0, best_a, 0x101, 0xf, 0xf, false);  // row_shl:1
+            if constexpr (A > 2) act_d[2] = __builtin_amdgcn_update_dpp(0, best_a, 0x102, 0xf, 0xf, false);
+            if constexpr (A > 3) act_d[3] = __builtin_amdgcn_update_dpp(0, best_a, 0x103, 0xf, 0xf, false);
           }
         }
-        if constexpr (DIRECT) {
-          act_d[0] = best_a;
-          if constexpr (A > 1) act_d[1] = __builtin_amdgcn_update_dpp(0, best_a, 0x101, 0xf, 0xf, false);  // row_shl:1
-          if constexpr (A > 2) act_d[2] = __builtin_amdgcn_update_dpp(0, best_a, 0x102, 0xf, 0xf, false);
-          if constexpr (A > 3) act_d[3] = __builtin_amdgcn_update_dpp(0, best_a, 0x103, 0xf, 0xf, false);
-        }
-        if (out.logits && live && g < 2 && !heur) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (4 * g + r < NA) out.logits[(((size_t)k * E + e0) * A + row) * NA + 4 * g + r] = logit[r];
-        }
       }
-      if constexpr (!DIRECT) wave_lds_sync();
+      if constexpr (!DIRECT && !SPLIT3) wave_lds_sync();
       uint32_t d = 0;
       RL_STAMP(4)
       float r = 0.f;
