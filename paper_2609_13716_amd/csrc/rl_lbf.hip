@@ -1488,24 +1488,38 @@ __global__ __launch_bounds__(NW * 64, 1) void lbf_pop2_kernel(LbfParams p, Polic
         xs, out.obs ? static_cast<T*>(out.obs) + ((size_t)k * E + e0) * A * D : nullptr, te_valid * A, tid);
     layer(L2a, L2b, h1s, LD1, h2s, LD2, bias_s[0] + H1, bias_s[1] + H1);
     __syncthreads();
-    if (wave == 0) {
+    // wave m: layer 3 and the Gumbel argmax of M tile m; then the env wave steps
+    static_assert(MT <= NW, "one wave per M tile of layer 3");
+    if (wave < MT) {
       const int g = lane >> 4;
+      {
+        const int m = wave;
+        int tm = 0;  // tmask[m] (without indexing the register array at run time)
 #pragma unroll
-      for (int m = 0; m < MT; ++m) {
+        for (int q = 0; q < MT; ++q) tm = q == m ? tmask[q] : tm;
         const int row = m * 16 + (lane & 15);
         const int rel = row % TE, ag = row / TE;
         const int sl = slot_s[row];
         const f32x4 nz4 = *reinterpret_cast<const f32x4*>(&nz[k & 1][row * 8 + 4 * (g & 1)]);
         f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
-        if (tmask[m] & 1) {
+        // the row operands (shared by both policies' chains), then each
+        // policy's W3 operands, all read before the MFMAs that use them
+        B hq[K3];
 #pragma unroll
-          for (int ks = 0; ks < K3; ++ks)
-            a0 = mfma16<DT>(w3s[0][ks * 64 + lane], load_operand_lds<DT>(h2s, LD2, row, ks, lane), a0);
+        for (int ks = 0; ks < K3; ++ks) hq[ks] = load_operand_lds<DT>(h2s, LD2, row, ks, lane);
+        if (tm & 1) {
+          B wq[K3];
+#pragma unroll
+          for (int ks = 0; ks < K3; ++ks) wq[ks] = w3s[0][ks * 64 + lane];
+#pragma unroll
+          for (int ks = 0; ks < K3; ++ks) a0 = mfma16<DT>(wq[ks], hq[ks], a0);
         }
-        if (tmask[m] & 2) {
+        if (tm & 2) {
+          B wq[K3];
 #pragma unroll
-          for (int ks = 0; ks < K3; ++ks)
-            a1 = mfma16<DT>(w3s[1][ks * 64 + lane], load_operand_lds<DT>(h2s, LD2, row, ks, lane), a1);
+          for (int ks = 0; ks < K3; ++ks) wq[ks] = w3s[1][ks * 64 + lane];
+#pragma unroll
+          for (int ks = 0; ks < K3; ++ks) a1 = mfma16<DT>(wq[ks], hq[ks], a1);
         }
         float best_s = -INFINITY;
         int best_a = 0;
@@ -1541,7 +1555,9 @@ __global__ __launch_bounds__(NW * 64, 1) void lbf_pop2_kernel(LbfParams p, Polic
             if (4 * g + r < NA) out.logits[gr * NA + 4 * g + r] = logit[r];
         }
       }
-      wave_lds_sync();
+    }
+    __syncthreads();
+    if (wave == 0) {
       uint32_t d = 0;
       float r = 0.f;
       if (envlane) {
