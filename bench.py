@@ -544,9 +544,10 @@ PHASE_CASES = (
       4: "field passes (bit vectors)", 5: "legal masks", 6: "write out + clear rows", 7: "barrier wait"}),
     ("kitchen fused rollout", "oc_4096", "run", "oc", 0, ("env wave", "other waves"),
      {0: "barrier at the step's top", 1: "layer 1", 2: "layer 2", 3: "layer 3", 4: "Gumbel scores",
-      6: "barrier", 7: "argmax + barrier",
-      8: "transition (env lanes) / copy o_t, next step's noise (other waves)", 9: "barrier",
-      10: "repaint o_t+1 (env lanes)"}),
+      5: "copy o_t to the trajectory (other waves)", 6: "barrier", 7: "argmax + barrier",
+      8: "transition (env lanes)", 9: "barrier",
+      10: "repaint o_t+1 (env lanes) / next step's noise (other waves; with no trajectory copy it is drawn during "
+          "the transition)"}),
     ("Hanabi fused rollout", "hn_4096", "run", "hn", 0, ("all waves",),
      {0: "barrier at the step's top", 1: "observation bit vectors", 2: "paint layer-1 tile", 3: "layer 1",
       4: "layer 2", 5: "layer 3", 6: "legal mask + Gumbel scores", 7: "copy o_t to the trajectory",

@@ -307,8 +307,10 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
     // The env lanes step the kitchens (oc_step_lane, with the tile's repaint
     // deferred) while the other waves copy o_t to the trajectory (after the
     // step's weight loads: a wave's loads wait for its earlier stores, one
-    // in-order counter) and draw the next step's noise (it depends on
-    // nothing the step computes); after a barrier the env lanes repaint.
+    // in-order counter); after a barrier the env lanes repaint.  The other
+    // waves draw the next step's noise (it depends on nothing the step
+    // computes) during the repaint, or, with no trajectory copy, during the
+    // transition.
     OcEnv s_old;
     uint64_t changed = 0, had = 0;
     uint32_t d = 0;
@@ -327,7 +329,8 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
       if (out.obs)
         copy_rows_global16(xs, LDX, static_cast<T*>(out.obs) + ((size_t)k * E + e0) * 2 * OC_D, OC_D,
                            te_valid * 2, tid - 64, OC_RUN_NT - 64);
-      if (k + 1 < n_steps) draw_noise(k + 1, tid - 64, OC_RUN_NT - 64);
+      RL_STAMP(5)
+      if (!out.obs && k + 1 < n_steps) draw_noise(k + 1, tid - 64, OC_RUN_NT - 64);
     }
     RL_STAMP(8)
     __syncthreads();  // o_t is copied out
@@ -336,6 +339,8 @@ __global__ __launch_bounds__(OC_RUN_NT) void oc_run_kernel(OcParams p, PolicyArg
       oc_paint_agents(s_old, xs, LDX, tid, false);
       oc_paint_items(s, xs, LDX, tid, d ? (had | changed) : changed);
       oc_paint_agents(s, xs, LDX, tid, true);
+    } else if (tid >= 64 && out.obs && k + 1 < n_steps) {
+      draw_noise(k + 1, tid - 64, OC_RUN_NT - 64);
     }
     RL_STAMP(10)
   }
