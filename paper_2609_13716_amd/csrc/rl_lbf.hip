@@ -829,7 +829,9 @@ __device__ __forceinline__ float row_log_pi(const float (&logit)[4], int g, int 
 //   * one "env wave" (wave 0, at raised issue priority: its serial section is
 //     the longest stage) computes layer 3, the Gumbel argmax (in registers
 //     plus one v_permlane16_swap) and steps the TE envs, drawing the reset
-//     blocks of ended episodes on idle lanes in parallel.
+//     blocks of ended episodes on idle lanes in parallel; with several M
+//     tiles, wave m computes layer 3 and the argmax of tile m and the env
+//     wave steps the envs after a barrier.
 // TE envs per workgroup; the launch bounds let MINB workgroups share a CU.
 // VH: layer 3 has one more output, the value head V(o) of an actor-critic
 // network, written with log pi of each sampled action and, after the last
