@@ -1259,7 +1259,7 @@ static bool try_launch_rollout_reg(const LbfParams& p, const LbfMagic& m, const 
   //  value head)
   RL_REG_CASE(DT_F32, 8, 8, 64, 64, 2, 3, 8, 4, 2, 0)
   RL_REG_CASE(DT_BF16, 8, 8, 64, 64, 2, 3, 8, 4, 2, 0)
-  RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 4, 1, 0)
+  RL_REG_CASE(DT_F32, 8, 8, 128, 128, 2, 3, 16, 8, 1, 0)
   RL_REG_CASE(DT_BF16, 8, 8, 128, 128, 2, 3, 8, 4, 2, 0)
   if (pol.dt == DT_BF16 && p.H == 12 && p.W == 12 && pol.H1 == 256 && pol.H2 == 256 && p.A == 3 && p.F == 6 &&
       !pol.VH && !tm) {
